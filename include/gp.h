@@ -1,0 +1,215 @@
+/*
+ * gp.h -- C ABI of one GPipe pipeline partition on one MI355X (gfx950).
+ *
+ * GPipe (Huang et al., "GPipe: Easy Scaling with Micro-Batch Pipeline
+ * Parallelism") splits a network given as a sequence of L layers into K cells
+ * of consecutive layers, one per accelerator (Section 2.1).  Every mini-batch
+ * of N examples is divided into M equal micro-batches (Section 2.2).  Each
+ * partition runs its composite forward function F_k on every micro-batch,
+ * keeping only the activations at its boundary (re-materialisation, Section
+ * 2.3); in the backward pass it recomputes F_k and runs B_k.  Gradients of
+ * all M micro-batches are accumulated and applied in one synchronous update
+ * at the end of the mini-batch (Section 2.2).
+ *
+ * This library is one partition's share of that work: a stack of pre-LN
+ * Transformer layers (the layer kind the paper trains in Sections 3 and 5),
+ * driven micro-batch by micro-batch.  All compute runs in HIP kernels on the
+ * caller's stream.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every function returns gp_status; none aborts or throws.  On failure a
+ *    thread-local message is available from gp_last_error().
+ *  - Argument and call-order errors are detected on the host before anything
+ *    is enqueued, and leave the partition unchanged.
+ *  - Device pointers are plain HIP device addresses of contiguous row-major
+ *    buffers owned by the caller; the library never frees them.  The library
+ *    owns its parameters, gradient accumulators, stash and workspaces, which it
+ *    allocates in gp_partition_configure and frees in gp_partition_destroy;
+ *    nothing is allocated on the per-micro-batch path.
+ *  - "Partition dtype" (gp_config.dtype) is the element type of boundary
+ *    tensors: float32 (GP_F32) or bfloat16 (GP_BF16, bf16 GEMM operands with
+ *    fp32 accumulation; the residual stream, LayerNorm statistics, softmax,
+ *    losses and gradient accumulators stay fp32).
+ *  - Calls on one partition are not thread-safe; use one partition per host
+ *    thread.  Work is ordered by the stream passed in; device faults surface
+ *    as GP_ERR_HIP at the next call that synchronises.
+ */
+#ifndef GP_H
+#define GP_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* A HIP stream handle (the same type as hipStream_t); NULL is the default stream. */
+typedef struct ihipStream_t* gp_stream;
+
+typedef struct gp_partition gp_partition; /* opaque, library-owned */
+
+typedef enum {
+    GP_OK = 0,
+    GP_ERR_INVALID_ARG = 1, /* bad size, NULL required pointer, mini-batch not M equal parts */
+    GP_ERR_STATE = 2,       /* call out of the forward/backward/step order */
+    GP_ERR_OOM = 3,         /* device allocation failed (configure) */
+    GP_ERR_HIP = 4,         /* a HIP runtime call failed */
+    GP_ERR_NONFINITE = 5,   /* check_finite found a non-finite gradient; update skipped */
+    GP_ERR_UNSUPPORTED = 6  /* valid request outside what the kernels implement */
+} gp_status;
+
+typedef enum { GP_F32 = 0, GP_BF16 = 1 } gp_dtype;
+
+/* Layer kind of every layer in the partition. */
+typedef enum {
+    GP_ENCODER = 0,      /* x1 = x + SelfAttn(LN1 x) Wo + bo;  y = x1 + FFN(LN2 x1) */
+    GP_DECODER_CROSS = 1 /* causal self-attention, cross-attention to a memory, FFN */
+} gp_layer_kind;
+
+/* What ends the partition's forward pass (Section 2.2: the last partition
+ * owns the loss; every other partition receives dL/dy from its successor). */
+typedef enum {
+    GP_LOSS_NONE = 0,   /* boundary partition: dL/dy arrives in gp_backward_microbatch_remat */
+    GP_LOSS_MSE = 1,    /* sum (y - target)^2 / (N S D) over the mini-batch */
+    GP_LOSS_XENT_LS = 2 /* final LayerNorm, [D, V] projection, label-smoothed cross-entropy / (N S) */
+} gp_loss;
+
+typedef struct {
+    int seq_len;             /* S, tokens per sequence */
+    int seqs_per_microbatch; /* n = N / M sequences in each micro-batch */
+    int num_microbatches;    /* M */
+    int dtype;               /* gp_dtype */
+    int kind;                /* gp_layer_kind */
+    int mem_seq_len;         /* decoder: memory length S_mem; else 0 */
+    int loss;                /* gp_loss */
+    int vocab;               /* GP_LOSS_XENT_LS: V; else 0 */
+    float label_smoothing;   /* GP_LOSS_XENT_LS: eps, target q = (1-eps) onehot + eps / V */
+    float ln_eps;            /* LayerNorm epsilon inside the square root (e.g. 1e-5) */
+    int check_finite;        /* nonzero: gp_accumulate_and_step checks G and syncs */
+} gp_config;
+
+/* Parameter tensors.  Matrices are logical [in, out] (y = x W + b); attention
+ * head h owns columns [h d_h, (h+1) d_h) of Wq/Wk/Wv and rows of Wo. */
+typedef enum {
+    GP_P_LN1_G = 0, GP_P_LN1_B, GP_P_WQ, GP_P_BQ, GP_P_WK, GP_P_BK, GP_P_WV, GP_P_BV,
+    GP_P_WO, GP_P_BO, GP_P_LN2_G, GP_P_LN2_B, GP_P_W1, GP_P_B1, GP_P_W2, GP_P_B2,
+    /* decoder layers: cross-attention (LN2 precedes it) and LN3 before the FFN */
+    GP_P_XWQ, GP_P_XBQ, GP_P_XWK, GP_P_XBK, GP_P_XWV, GP_P_XBV, GP_P_XWO, GP_P_XBO,
+    GP_P_LN3_G, GP_P_LN3_B,
+    /* loss head (layer index -1): final LayerNorm and vocabulary projection */
+    GP_P_LNF_G, GP_P_LNF_B, GP_P_WOUT, GP_P_BOUT,
+    GP_P_COUNT
+} gp_param_id;
+
+/*
+ * Create a partition of `layers` Transformer layers of width d_model, FFN
+ * width d_ff and `heads` attention heads (Section 2.1: a cell p_k of
+ * consecutive layers).  Touches no device.  *out receives the handle.
+ * GP_ERR_INVALID_ARG: a size <= 0, d_model % heads != 0, out == NULL.
+ */
+gp_status gp_partition_create(int layers, int d_model, int d_ff, int heads, gp_partition** out);
+
+/*
+ * Fix the micro-batch geometry and allocate every device buffer on the
+ * current HIP device: fp32 master parameters (initialised to 0; LayerNorm
+ * gains to 1), their bf16 (or fp32) working copies, fp32 gradient
+ * accumulators, the boundary stash of M micro-batches and the
+ * re-materialisation workspace of one micro-batch (Section 2.3: activation
+ * memory O(N + L/K * N/M)).  Once per partition.
+ * GP_ERR_INVALID_ARG: non-positive sizes, unknown enums, missing vocab.
+ * GP_ERR_UNSUPPORTED: bf16 attention needs d_model / heads == 64 and
+ *   seq_len, mem_seq_len multiples of 32 and <= 256.
+ * GP_ERR_STATE: configured already.  GP_ERR_OOM / GP_ERR_HIP on device failure.
+ */
+gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg);
+
+/* Free everything the partition owns (synchronises the device first).  NULL is a no-op. */
+gp_status gp_partition_destroy(gp_partition* p);
+
+/*
+ * Copy one parameter tensor between host fp32 memory and the partition.
+ * `layer` is 0..layers-1, or -1 for the head parameters; `count` must equal
+ * the tensor's element count (logical [in, out] row-major for matrices).
+ * gp_set_param also refreshes the working copies.  gp_get_param reads the
+ * fp32 master; gp_get_grad reads the fp32 accumulator, which after the last
+ * backward micro-batch holds the mini-batch gradient sum_m dL_m/dw.
+ * These calls synchronise the device.
+ * GP_ERR_INVALID_ARG: bad layer, id not present in this layer kind, count.
+ * GP_ERR_STATE: not configured, or gp_set_param between the first forward
+ *   and the step of a mini-batch (Section 2.2: all micro-batches of a
+ *   mini-batch see the same parameters).
+ */
+gp_status gp_set_param(gp_partition* p, int layer, int id, const float* host, size_t count);
+gp_status gp_get_param(gp_partition* p, int layer, int id, float* host, size_t count);
+gp_status gp_get_grad(gp_partition* p, int layer, int id, float* host, size_t count);
+
+/* Bytes held in device memory for parameters (masters and working copies),
+ * gradient accumulators, the boundary stash, and all workspaces.  Any pointer
+ * may be NULL.  Requires a configured partition. */
+gp_status gp_partition_memory(gp_partition* p, size_t* params, size_t* grads, size_t* stash,
+                              size_t* workspace);
+
+/* Number of trainable parameters (layers plus head). */
+gp_status gp_param_count(gp_partition* p, size_t* count);
+
+/*
+ * Forward pass of micro-batch `mb` (Sections 2.2-2.3).  Micro-batches are
+ * taken in order mb = 0, 1, ..., M-1 within a mini-batch.
+ *   x   : device [n, S, D] in the partition dtype, the micro-batch's boundary
+ *         input.  It is copied into the library's stash, so the caller may
+ *         reuse the buffer once the stream has passed this call.
+ *   mem : decoder: device [n, S_mem, D] partition dtype, also stashed; else NULL.
+ *   y   : device [n, S, D] partition dtype, the partition output F_k(x);
+ *         may be NULL (loss partitions need not emit it).
+ * Every intermediate of the layers is discarded; only the stash is kept.
+ * GP_ERR_STATE: not configured, mb out of order, or backward already begun.
+ * GP_ERR_INVALID_ARG: x (or mem for the decoder) NULL, mb out of range.
+ */
+gp_status gp_forward_microbatch(gp_partition* p, int mb, const void* x, const void* mem, void* y,
+                                gp_stream stream);
+
+/*
+ * Backward pass of micro-batch `mb` with re-materialisation (Section 2.3):
+ * the layers' forward is recomputed from the stashed boundary input, keeping
+ * this micro-batch's intermediates only, then back-propagated in reverse
+ * layer order.  Parameter gradients are added in place into the fp32
+ * accumulators (the first backward micro-batch of a mini-batch overwrites
+ * them).  Micro-batches are taken in order mb = M-1, ..., 0, after all M
+ * forwards.
+ *   dy_or_target : GP_LOSS_NONE:   device [n, S, D] partition dtype, dL/dy;
+ *                  GP_LOSS_MSE:    device [n, S, D] partition dtype, targets;
+ *                  GP_LOSS_XENT_LS: device int32 [n, S] labels in [0, V).
+ *   dx   : device [n, S, D] partition dtype, dL/dx for the previous
+ *          partition; may be NULL.
+ *   dmem : decoder: device [n, S_mem, D] partition dtype, dL/dmem summed over
+ *          the layers; may be NULL.  Else must be NULL.
+ * GP_ERR_STATE: forwards incomplete, or mb out of order.
+ * GP_ERR_INVALID_ARG: dy_or_target NULL, mb out of range.
+ */
+gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_or_target, void* dx,
+                                       void* dmem, gp_stream stream);
+
+/*
+ * The one synchronous update at the end of the mini-batch (Section 2.2):
+ * W <- W - lr * G on the fp32 masters (G = the accumulated, undivided sum of
+ * the micro-batch gradients; losses are normalised by the whole mini-batch),
+ * then the working copies are refreshed (fp32 -> bf16 round-to-nearest-even).
+ * G keeps its value until the next mini-batch's first backward overwrites it.
+ *   loss_out : if non-NULL, receives the mini-batch loss (0 for GP_LOSS_NONE)
+ *              and the call synchronises the stream.
+ * With check_finite set the call synchronises, and if any gradient is
+ * non-finite the update is skipped and GP_ERR_NONFINITE returned.
+ * GP_ERR_STATE: not all M backward micro-batches done.
+ */
+gp_status gp_accumulate_and_step(gp_partition* p, float lr, double* loss_out, gp_stream stream);
+
+/* Message of the calling thread's last failure (library-owned, valid until the
+ * thread's next failing call); "" if none. */
+const char* gp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GP_H */

@@ -1,0 +1,75 @@
+// common.hpp -- device helpers shared by the partition's HIP kernels (gfx950,
+// wave64).  Element types: `float` (fp32 partitions) and `bf16` (__bf16
+// storage; arithmetic is always fp32).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+namespace gp {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int WAVE = 64;
+
+// fp32 -> storage type, round to nearest even (the gfx950 conversion
+// instruction rounds RNE and keeps NaN quiet).
+template <typename T> __device__ __forceinline__ T to_elt(float v);
+template <> __device__ __forceinline__ float to_elt<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16 to_elt<bf16>(float v) { return (bf16)v; }
+
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(bf16 v) { return (float)v; }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, WAVE);
+    return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, WAVE));
+    return v;
+}
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, WAVE);
+    return v;
+}
+
+// 16-byte vector of storage elements (8 bf16 or 4 float).
+template <typename T> struct Vec16;
+template <> struct Vec16<bf16> {
+    static constexpr int N = 8;
+    typedef bf16x8 type;
+};
+template <> struct Vec16<float> {
+    static constexpr int N = 4;
+    typedef f32x4 type;
+};
+
+} // namespace gp
+
+// Host-side launch checking (used inside functions returning gp_status).
+#define GP_LAUNCH_CHECK()                                                   \
+    do {                                                                    \
+        hipError_t e_ = hipGetLastError();                                  \
+        if (e_ != hipSuccess) return ::gp::hip_fail(e_, __FILE__, __LINE__); \
+    } while (0)
+
+#define GP_HIP(call)                                                        \
+    do {                                                                    \
+        hipError_t e_ = (call);                                             \
+        if (e_ != hipSuccess) return ::gp::hip_fail(e_, __FILE__, __LINE__); \
+    } while (0)
+
+#include "../../include/gp.h"
+namespace gp {
+gp_status hip_fail(hipError_t e, const char* file, int line);
+gp_status set_error(gp_status s, const char* msg);
+}

@@ -1,0 +1,101 @@
+// kernels.hpp -- host-side launchers of the partition's HIP kernels.  All
+// launchers enqueue on the given stream and return gp_status (launch errors
+// only; device faults surface at the next synchronising call).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include "../../include/gp.h"
+
+namespace gp {
+
+// ------------------------------------------------------------------ GEMM
+enum {
+    EPI_STORE = 0,     // C (elt) = act(acc + bias), act = ReLU when relu != 0
+    EPI_RES_F32 = 1,   // C (f32) = aux (f32 residual) + acc + bias; C2 (elt, optional) = same, rounded
+    EPI_F32 = 2,       // C (f32) = acc
+    EPI_RELU_MASK = 3, // C (elt) = acc * [aux (elt) > 0]
+    EPI_ACC_F32 = 4    // C (f32) = (accumulate ? C : 0) + acc
+};
+
+struct GemmArgs {
+    int M = 0, N = 0, K = 0;
+    const void* A = nullptr; long lda = 0; // element (m,k): k-major A[m lda + k], else A[k lda + m]
+    const void* B = nullptr; long ldb = 0; // element (n,k): k-major B[n ldb + k], else B[k ldb + n]
+    void* C = nullptr; long ldc = 0;
+    void* C2 = nullptr; long ldc2 = 0;
+    const float* bias = nullptr;
+    const void* aux = nullptr; long ldaux = 0;
+    int relu = 0;
+    int accumulate = 0;
+};
+
+gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dtype, hipStream_t st);
+
+// ------------------------------------------------------------- LayerNorm
+// out (elt) = gamma * (x - mu) * rstd + beta per row of D; stats[row] = {mu, rstd}
+gp_status layernorm_fwd(int dtype, const float* x, long rows, int D, const float* gamma, const float* beta,
+                        float eps, void* out, float* stats, hipStream_t st);
+// dx = dres + rstd (g - mean g - xh mean(g xh)), g = dn * gamma; writes dx_f32 and/or dx_elt.
+// Per-block partial sums of dn * xh and dn go to partial[blk][2][D]; *nblk
+// receives the block count (for colsum_finalize over width 2 D).
+gp_status layernorm_bwd(int dtype, const float* dn, const float* x, const float* stats, const float* gamma,
+                        long rows, int D, const float* dres, float* dx_f32, void* dx_elt, float* partial,
+                        int* nblk, hipStream_t st);
+// Rows the partial buffers of layernorm_bwd / bias_grad may need.
+int layernorm_bwd_blocks(long rows);
+int bias_grad_blocks(long rows);
+
+// out[c] = (accumulate ? out[c] : 0) + sum_b partial[b * width + c]
+gp_status colsum_finalize(const float* partial, int nblk, int width, float* out, int accumulate, hipStream_t st);
+// Column sums of dy (elt, [rows, N], leading dim ld) into out[N] (f32), via partial.
+gp_status bias_grad(int dtype, const void* dy, long rows, int N, long ld, float* partial, float* out,
+                    int accumulate, hipStream_t st);
+
+// ------------------------------------------------------------- attention
+struct AttnArgs {
+    int n = 0, H = 0, Sq = 0, Sk = 0, dh = 0;
+    const void* q = nullptr; long ldq = 0; // row (b, i) of head h at q + (b Sq + i) ldq + h dh
+    const void* k = nullptr; long ldk = 0; // row (b, j) at k + (b Sk + j) ldk + h dh
+    const void* v = nullptr; long ldv = 0;
+    void* o = nullptr; long ldo = 0;
+    float* lse = nullptr;                  // [n, H, Sq] log-sum-exp of the scaled scores
+    int causal = 0;
+    float scale = 1.f;
+    const void* dout = nullptr; long lddo = 0;
+    void* dq = nullptr; long lddq = 0;
+    void* dk = nullptr; long lddk = 0;
+    void* dv = nullptr; long lddv = 0;
+    float* delta = nullptr;                // [n, H, Sq] rowsum(dO * O) scratch
+};
+gp_status attention_fwd(int dtype, const AttnArgs& a, hipStream_t st);
+gp_status attention_bwd(int dtype, const AttnArgs& a, hipStream_t st);
+
+// ----------------------------------------------------------- elementwise
+// x32 = float(src); stash (optional) = src.  count elements.
+gp_status intake(int dtype, const void* src, void* stash, float* x32, long count, hipStream_t st);
+// dst (elt) = src (f32) rounded.
+gp_status cast_out(int dtype, const float* src, void* dst, long count, hipStream_t st);
+// d = y - t; d32 = 2 d / norm; delt = rounded d32; partial[blk] = sum d^2 / norm (fp64)
+gp_status mse_grad(int dtype, const float* y, const void* target, long count, double norm, float* d32,
+                   void* delt, double* partial, int* nblk, hipStream_t st);
+int loss_blocks();
+// acc[0] = (accumulate ? acc[0] : 0) + sum_b partial[b]
+gp_status loss_finalize(const double* partial, int nblk, double* acc, int accumulate, hipStream_t st);
+
+// Label-smoothed softmax cross-entropy over rows of V logits (f32 or elt in
+// z, overwritten by dZ in the elt type): dZ = (softmax(z) - q) / norm,
+// partial[row] += -sum q log p / norm in fp64.
+gp_status xent_ls(int dtype, void* z, long rows, int V, const int* labels, float ls, double norm,
+                  double* partial, hipStream_t st);
+int xent_partials(long rows);
+
+// --------------------------------------------------------------- update
+// w[i] -= lr * g[i] for i < count (fp32 masters).
+gp_status sgd_update(float* w, const float* g, float lr, long count, hipStream_t st);
+// Working copies of one linear layer from its fp32 master W [in, out]:
+// kn (elt) = W, nk (elt) = W^T.
+gp_status refresh_linear(int dtype, const float* w, int in, int out, void* kn, void* nk, hipStream_t st);
+// flag[0] = 1 if any of x[0..count) is not finite (flag must be zeroed first).
+gp_status finite_check(const float* x, long count, int* flag, hipStream_t st);
+
+} // namespace gp

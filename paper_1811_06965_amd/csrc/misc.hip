@@ -1,0 +1,225 @@
+// misc.hip -- boundary intake, casts, loss heads and the synchronous update.
+//
+// All reductions are two-stage with a fixed order (per-block partials, then
+// one finalising block), so every result is reproducible bit for bit.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace gp {
+
+namespace {
+
+constexpr int EW_BLOCKS = 1024;   // grid of the grid-stride elementwise kernels
+constexpr int LOSS_BLOCKS = 256;  // partials of the MSE loss
+
+template <typename T>
+__global__ void __launch_bounds__(256) intake_kernel(const T* __restrict__ src, T* __restrict__ stash,
+                                                     float* __restrict__ x32, long count) {
+    for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < count; i += (long)gridDim.x * 256) {
+        const T v = src[i];
+        if (stash) stash[i] = v;
+        if (x32) x32[i] = to_f32(v);
+    }
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256) cast_kernel(const float* __restrict__ src, T* __restrict__ dst, long count) {
+    for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < count; i += (long)gridDim.x * 256)
+        dst[i] = to_elt<T>(src[i]);
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256) mse_kernel(const float* __restrict__ y, const T* __restrict__ t, long count,
+                                                  double norm, float* __restrict__ d32, T* __restrict__ de,
+                                                  double* __restrict__ partial) {
+    __shared__ double red[4];
+    double s = 0.0;
+    const float scale = (float)(2.0 / norm);
+    for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < count; i += (long)gridDim.x * 256) {
+        const float d = y[i] - to_f32(t[i]);
+        s += (double)d * (double)d;
+        const float g = scale * d;
+        d32[i] = g;
+        de[i] = to_elt<T>(g);
+    }
+    s = wave_sum_d(s);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) partial[blockIdx.x] = (red[0] + red[1] + red[2] + red[3]) / norm;
+}
+
+__global__ void loss_finalize_kernel(const double* __restrict__ partial, int nblk, double* __restrict__ acc,
+                                     int accumulate) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    double s = 0.0;
+    for (int b = 0; b < nblk; ++b) s += partial[b];
+    acc[0] = accumulate ? acc[0] + s : s;
+}
+
+// Label-smoothed cross-entropy over one row of V logits per block.
+// q_v = ls / V + (1 - ls) [v == label];  loss_row = -sum_v q_v log p_v
+//   = lse - ls / V sum_v z_v - (1 - ls) z_label,   lse = log sum_v exp z_v;
+// dZ_v = (p_v - q_v) / norm.
+template <typename T>
+__global__ void __launch_bounds__(256) xent_kernel(T* __restrict__ z, int V, const int* __restrict__ labels,
+                                                   float ls, double norm, double* __restrict__ partial) {
+    __shared__ float red[4];
+    __shared__ float bc[2];
+    const long row = blockIdx.x;
+    T* zr = z + row * (long)V;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    float m = -INFINITY, sz = 0.f;
+    for (int v = tid; v < V; v += 256) {
+        const float x = to_f32(zr[v]);
+        m = fmaxf(m, x);
+        sz += x;
+    }
+    m = wave_max(m);
+    sz = wave_sum(sz);
+    if (lane == 0) red[w] = m;
+    __syncthreads();
+    if (tid == 0) bc[0] = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    __syncthreads();
+    m = bc[0];
+    __syncthreads();
+    if (lane == 0) red[w] = sz;
+    __syncthreads();
+    if (tid == 0) bc[1] = red[0] + red[1] + red[2] + red[3];
+    __syncthreads();
+    sz = bc[1];
+    float se = 0.f;
+    for (int v = tid; v < V; v += 256) se += expf(to_f32(zr[v]) - m);
+    se = wave_sum(se);
+    __syncthreads();
+    if (lane == 0) red[w] = se;
+    __syncthreads();
+    if (tid == 0) bc[0] = red[0] + red[1] + red[2] + red[3];
+    __syncthreads();
+    se = bc[0];
+    const int lab = labels[row];
+    const float zl = to_f32(zr[lab]);
+    __syncthreads();
+    const float lse = m + logf(se);
+    const float inv = 1.f / se, u = ls / V, gn = (float)(1.0 / norm);
+    for (int v = tid; v < V; v += 256) {
+        const float p = expf(to_f32(zr[v]) - m) * inv;
+        const float q = u + (v == lab ? 1.f - ls : 0.f);
+        zr[v] = to_elt<T>((p - q) * gn);
+    }
+    if (tid == 0) partial[row] = ((double)lse - (double)u * sz - (1.0 - ls) * zl) / norm;
+}
+
+__global__ void __launch_bounds__(256) sgd_kernel(float* __restrict__ w, const float* __restrict__ g, float lr,
+                                                  long count) {
+    for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < count; i += (long)gridDim.x * 256) w[i] -= lr * g[i];
+}
+
+// kn = W, nk = W^T through a 64 x 64 LDS tile (both writes coalesced).
+template <typename T>
+__global__ void __launch_bounds__(256) refresh_kernel(const float* __restrict__ w, int in, int out,
+                                                      T* __restrict__ kn, T* __restrict__ nk) {
+    __shared__ float tile[64][65];
+    const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    for (int r = ty; r < 64; r += 4) {
+        const int row = r0 + r, col = c0 + tx;
+        if (row < in && col < out) {
+            const float v = w[(long)row * out + col];
+            tile[r][tx] = v;
+            kn[(long)row * out + col] = to_elt<T>(v);
+        }
+    }
+    __syncthreads();
+    for (int c = ty; c < 64; c += 4) {
+        const int col = c0 + c, row = r0 + tx;
+        if (row < in && col < out) nk[(long)col * in + row] = to_elt<T>(tile[tx][c]);
+    }
+}
+
+__global__ void __launch_bounds__(256) finite_kernel(const float* __restrict__ x, long count, int* __restrict__ flag) {
+    bool bad = false;
+    for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < count; i += (long)gridDim.x * 256)
+        bad |= !isfinite(x[i]);
+    if (__any(bad) && (threadIdx.x & 63) == 0) flag[0] = 1;
+}
+
+int ew_grid(long count) {
+    long g = (count + 255) / 256;
+    return (int)(g < EW_BLOCKS ? (g > 0 ? g : 1) : EW_BLOCKS);
+}
+
+} // namespace
+
+int loss_blocks() { return LOSS_BLOCKS; }
+int xent_partials(long rows) { return (int)rows; }
+
+gp_status intake(int dtype, const void* src, void* stash, float* x32, long count, hipStream_t st) {
+    if (dtype == GP_BF16)
+        intake_kernel<bf16><<<ew_grid(count), 256, 0, st>>>(reinterpret_cast<const bf16*>(src),
+                                                             reinterpret_cast<bf16*>(stash), x32, count);
+    else
+        intake_kernel<float><<<ew_grid(count), 256, 0, st>>>(reinterpret_cast<const float*>(src),
+                                                              reinterpret_cast<float*>(stash), x32, count);
+    GP_LAUNCH_CHECK();
+    return GP_OK;
+}
+
+gp_status cast_out(int dtype, const float* src, void* dst, long count, hipStream_t st) {
+    if (dtype == GP_BF16) cast_kernel<bf16><<<ew_grid(count), 256, 0, st>>>(src, reinterpret_cast<bf16*>(dst), count);
+    else cast_kernel<float><<<ew_grid(count), 256, 0, st>>>(src, reinterpret_cast<float*>(dst), count);
+    GP_LAUNCH_CHECK();
+    return GP_OK;
+}
+
+gp_status mse_grad(int dtype, const float* y, const void* target, long count, double norm, float* d32, void* delt,
+                   double* partial, int* nblk, hipStream_t st) {
+    *nblk = LOSS_BLOCKS;
+    if (dtype == GP_BF16)
+        mse_kernel<bf16><<<LOSS_BLOCKS, 256, 0, st>>>(y, reinterpret_cast<const bf16*>(target), count, norm, d32,
+                                                      reinterpret_cast<bf16*>(delt), partial);
+    else
+        mse_kernel<float><<<LOSS_BLOCKS, 256, 0, st>>>(y, reinterpret_cast<const float*>(target), count, norm, d32,
+                                                       reinterpret_cast<float*>(delt), partial);
+    GP_LAUNCH_CHECK();
+    return GP_OK;
+}
+
+gp_status loss_finalize(const double* partial, int nblk, double* acc, int accumulate, hipStream_t st) {
+    loss_finalize_kernel<<<1, 64, 0, st>>>(partial, nblk, acc, accumulate);
+    GP_LAUNCH_CHECK();
+    return GP_OK;
+}
+
+gp_status xent_ls(int dtype, void* z, long rows, int V, const int* labels, float ls, double norm, double* partial,
+                  hipStream_t st) {
+    if (dtype == GP_BF16)
+        xent_kernel<bf16><<<(unsigned)rows, 256, 0, st>>>(reinterpret_cast<bf16*>(z), V, labels, ls, norm, partial);
+    else
+        xent_kernel<float><<<(unsigned)rows, 256, 0, st>>>(reinterpret_cast<float*>(z), V, labels, ls, norm, partial);
+    GP_LAUNCH_CHECK();
+    return GP_OK;
+}
+
+gp_status sgd_update(float* w, const float* g, float lr, long count, hipStream_t st) {
+    sgd_kernel<<<ew_grid(count), 256, 0, st>>>(w, g, lr, count);
+    GP_LAUNCH_CHECK();
+    return GP_OK;
+}
+
+gp_status refresh_linear(int dtype, const float* w, int in, int out, void* kn, void* nk, hipStream_t st) {
+    dim3 grid((out + 63) / 64, (in + 63) / 64);
+    if (dtype == GP_BF16)
+        refresh_kernel<bf16><<<grid, 256, 0, st>>>(w, in, out, reinterpret_cast<bf16*>(kn), reinterpret_cast<bf16*>(nk));
+    else
+        refresh_kernel<float><<<grid, 256, 0, st>>>(w, in, out, reinterpret_cast<float*>(kn), reinterpret_cast<float*>(nk));
+    GP_LAUNCH_CHECK();
+    return GP_OK;
+}
+
+gp_status finite_check(const float* x, long count, int* flag, hipStream_t st) {
+    finite_kernel<<<ew_grid(count), 256, 0, st>>>(x, count, flag);
+    GP_LAUNCH_CHECK();
+    return GP_OK;
+}
+
+} // namespace gp

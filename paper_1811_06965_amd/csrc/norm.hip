@@ -1,0 +1,225 @@
+// norm.hip -- LayerNorm forward/backward and deterministic column reductions.
+//
+// LayerNorm over the feature dimension D of each token row (biased variance,
+// eps inside the square root).  One wave owns one row; lane l holds features
+// l, l + 64, ... so every global access is a coalesced 256-byte row segment.
+// Parameter gradients are reduced in two deterministic stages: per-block
+// partial sums, then a fixed-order column sum (no atomics), so re-running a
+// micro-batch reproduces its gradients bit for bit.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace gp {
+
+namespace {
+
+constexpr int LN_WAVES = 4;
+
+template <typename T, int C>
+__global__ void __launch_bounds__(256) ln_fwd_kernel(const float* __restrict__ x, long rows, int D,
+                                                     const float* __restrict__ gamma,
+                                                     const float* __restrict__ beta, float eps,
+                                                     T* __restrict__ out, float* __restrict__ stats) {
+    const int lane = threadIdx.x & 63;
+    const long row = (long)blockIdx.x * LN_WAVES + (threadIdx.x >> 6);
+    if (row >= rows) return;
+    const float* xr = x + row * D;
+    float v[C];
+    float s = 0.f;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        const int d = lane + c * 64;
+        v[c] = d < D ? xr[d] : 0.f;
+        s += v[c];
+    }
+    const float mu = wave_sum(s) / D;
+    float q = 0.f;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        const int d = lane + c * 64;
+        const float t = d < D ? v[c] - mu : 0.f;
+        q += t * t;
+    }
+    const float rstd = 1.f / sqrtf(wave_sum(q) / D + eps);
+    T* orow = out + row * D;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        const int d = lane + c * 64;
+        if (d < D) orow[d] = to_elt<T>(gamma[d] * ((v[c] - mu) * rstd) + beta[d]);
+    }
+    if (stats && lane == 0) {
+        stats[2 * row] = mu;
+        stats[2 * row + 1] = rstd;
+    }
+}
+
+int ln_bwd_rows_per_wave(long rows) {
+    long r = rows / (LN_WAVES * 256);
+    return r < 1 ? 1 : (int)r;
+}
+
+template <typename T, int C>
+__global__ void __launch_bounds__(256) ln_bwd_kernel(const float* __restrict__ dn, const float* __restrict__ x,
+                                                     const float* __restrict__ stats,
+                                                     const float* __restrict__ gamma, long rows, int D, int rpw,
+                                                     const float* __restrict__ dres, float* __restrict__ dx32,
+                                                     T* __restrict__ dxe, float* __restrict__ partial) {
+    __shared__ float red[LN_WAVES][2][C * 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    float pg[C], pb[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) pg[c] = pb[c] = 0.f;
+    const long row0 = ((long)blockIdx.x * LN_WAVES + wave) * rpw;
+    for (int rr = 0; rr < rpw; ++rr) {
+        const long row = row0 + rr;
+        if (row >= rows) break;
+        const float mu = stats[2 * row], rstd = stats[2 * row + 1];
+        float g[C], xh[C];
+        float sg = 0.f, sgx = 0.f;
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int d = lane + c * 64;
+            if (d < D) {
+                const float dv = dn[row * D + d];
+                xh[c] = (x[row * D + d] - mu) * rstd;
+                g[c] = dv * gamma[d];
+                pg[c] += dv * xh[c];
+                pb[c] += dv;
+            } else {
+                xh[c] = g[c] = 0.f;
+            }
+            sg += g[c];
+            sgx += g[c] * xh[c];
+        }
+        sg = wave_sum(sg) / D;
+        sgx = wave_sum(sgx) / D;
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int d = lane + c * 64;
+            if (d < D) {
+                float r = rstd * (g[c] - sg - xh[c] * sgx);
+                if (dres) r += dres[row * D + d];
+                if (dx32) dx32[row * D + d] = r;
+                if (dxe) dxe[row * D + d] = to_elt<T>(r);
+            }
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        red[wave][0][lane + c * 64] = pg[c];
+        red[wave][1][lane + c * 64] = pb[c];
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < 2 * D; i += 256) {
+        const int which = i / D, d = i % D;
+        float s = 0.f;
+#pragma unroll
+        for (int w = 0; w < LN_WAVES; ++w) s += red[w][which][d];
+        partial[(long)blockIdx.x * 2 * D + i] = s;
+    }
+}
+
+__global__ void colsum_kernel(const float* __restrict__ partial, int nblk, int width, float* __restrict__ out,
+                              int accumulate) {
+    const int c = blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= width) return;
+    float s = 0.f;
+    for (int b = 0; b < nblk; ++b) s += partial[(long)b * width + c];
+    out[c] = accumulate ? out[c] + s : s;
+}
+
+constexpr int BIAS_BLOCKS = 64;
+
+template <typename T>
+__global__ void __launch_bounds__(256) bias_partial_kernel(const T* __restrict__ dy, long rows, int N, long ld,
+                                                           long rows_per_block, float* __restrict__ partial) {
+    const int c = blockIdx.x * 256 + threadIdx.x;
+    if (c >= N) return;
+    const long r0 = (long)blockIdx.y * rows_per_block;
+    long r1 = r0 + rows_per_block;
+    if (r1 > rows) r1 = rows;
+    float s = 0.f;
+    for (long r = r0; r < r1; ++r) s += to_f32(dy[r * ld + c]);
+    partial[(long)blockIdx.y * N + c] = s;
+}
+
+template <typename T>
+gp_status ln_fwd_t(const float* x, long rows, int D, const float* g, const float* b, float eps, void* out,
+                   float* stats, hipStream_t st) {
+    const int grid = (int)((rows + LN_WAVES - 1) / LN_WAVES);
+    T* o = reinterpret_cast<T*>(out);
+    const int C = (D + 63) / 64;
+    if (C <= 1) ln_fwd_kernel<T, 1><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats);
+    else if (C <= 2) ln_fwd_kernel<T, 2><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats);
+    else if (C <= 4) ln_fwd_kernel<T, 4><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats);
+    else if (C <= 8) ln_fwd_kernel<T, 8><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats);
+    else if (C <= 16) ln_fwd_kernel<T, 16><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats);
+    else if (C <= 32) ln_fwd_kernel<T, 32><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats);
+    else return set_error(GP_ERR_UNSUPPORTED, "layernorm: d_model > 2048");
+    GP_LAUNCH_CHECK();
+    return GP_OK;
+}
+
+template <typename T>
+gp_status ln_bwd_t(const float* dn, const float* x, const float* stats, const float* gamma, long rows, int D,
+                   const float* dres, float* dx32, void* dxe, float* partial, int* nblk, hipStream_t st) {
+    const int rpw = ln_bwd_rows_per_wave(rows);
+    const int grid = (int)((rows + (long)LN_WAVES * rpw - 1) / ((long)LN_WAVES * rpw));
+    *nblk = grid;
+    T* e = reinterpret_cast<T*>(dxe);
+    const int C = (D + 63) / 64;
+#define GP_LNB(CC) ln_bwd_kernel<T, CC><<<grid, 256, 0, st>>>(dn, x, stats, gamma, rows, D, rpw, dres, dx32, e, partial)
+    if (C <= 1) GP_LNB(1);
+    else if (C <= 2) GP_LNB(2);
+    else if (C <= 4) GP_LNB(4);
+    else if (C <= 8) GP_LNB(8);
+    else if (C <= 16) GP_LNB(16);
+    else if (C <= 32) GP_LNB(32);
+    else return set_error(GP_ERR_UNSUPPORTED, "layernorm: d_model > 2048");
+#undef GP_LNB
+    GP_LAUNCH_CHECK();
+    return GP_OK;
+}
+
+} // namespace
+
+int layernorm_bwd_blocks(long rows) {
+    const int rpw = ln_bwd_rows_per_wave(rows);
+    return (int)((rows + (long)LN_WAVES * rpw - 1) / ((long)LN_WAVES * rpw));
+}
+int bias_grad_blocks(long rows) { return rows < BIAS_BLOCKS ? (int)(rows > 0 ? rows : 1) : BIAS_BLOCKS; }
+
+gp_status layernorm_fwd(int dtype, const float* x, long rows, int D, const float* gamma, const float* beta,
+                        float eps, void* out, float* stats, hipStream_t st) {
+    if (dtype == GP_BF16) return ln_fwd_t<bf16>(x, rows, D, gamma, beta, eps, out, stats, st);
+    return ln_fwd_t<float>(x, rows, D, gamma, beta, eps, out, stats, st);
+}
+
+gp_status layernorm_bwd(int dtype, const float* dn, const float* x, const float* stats, const float* gamma,
+                        long rows, int D, const float* dres, float* dx_f32, void* dx_elt, float* partial,
+                        int* nblk, hipStream_t st) {
+    if (dtype == GP_BF16)
+        return ln_bwd_t<bf16>(dn, x, stats, gamma, rows, D, dres, dx_f32, dx_elt, partial, nblk, st);
+    return ln_bwd_t<float>(dn, x, stats, gamma, rows, D, dres, dx_f32, dx_elt, partial, nblk, st);
+}
+
+gp_status colsum_finalize(const float* partial, int nblk, int width, float* out, int accumulate, hipStream_t st) {
+    colsum_kernel<<<(width + 255) / 256, 256, 0, st>>>(partial, nblk, width, out, accumulate);
+    GP_LAUNCH_CHECK();
+    return GP_OK;
+}
+
+gp_status bias_grad(int dtype, const void* dy, long rows, int N, long ld, float* partial, float* out,
+                    int accumulate, hipStream_t st) {
+    const int nb = bias_grad_blocks(rows);
+    const long rpb = (rows + nb - 1) / nb;
+    dim3 grid((N + 255) / 256, nb);
+    if (dtype == GP_BF16)
+        bias_partial_kernel<bf16><<<grid, 256, 0, st>>>(reinterpret_cast<const bf16*>(dy), rows, N, ld, rpb, partial);
+    else
+        bias_partial_kernel<float><<<grid, 256, 0, st>>>(reinterpret_cast<const float*>(dy), rows, N, ld, rpb, partial);
+    GP_LAUNCH_CHECK();
+    return colsum_finalize(partial, nb, N, out, accumulate, st);
+}
+
+} // namespace gp

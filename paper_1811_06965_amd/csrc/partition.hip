@@ -1,0 +1,730 @@
+// partition.hip -- the C ABI of one GPipe partition and its layer drivers.
+//
+// GPipe, Sections 2.2-2.3: the mini-batch is split into M equal
+// micro-batches; the forward pass of each keeps only the partition's boundary
+// input (the stash); the backward pass recomputes the partition's forward from
+// the stash (re-materialisation) keeping that one micro-batch's intermediates,
+// then back-propagates layer by layer, adding each parameter gradient into an
+// fp32 accumulator; one synchronous update ends the mini-batch.
+//
+// Device memory (one partition):
+//   master, grads   fp32, identical layout: per linear W [in, out] then b [out];
+//                   per LayerNorm gamma [D] then beta [D]
+//   welt            working copies in the partition dtype: W [in, out] and W^T [out, in]
+//   stash           M boundary inputs [n, S, D] (and decoder memories [n, S_mem, D])
+//   workspace       residual stream xs[0..L] fp32 [T, D] (T = n S), per-layer
+//                   intermediates of one micro-batch, backward scratch
+// The forward pass writes its intermediates into layer slot 0 and ping-pongs
+// xs[0]/xs[1]; the re-materialising pass uses slot l and xs[l] for layer l.
+// Both run the same kernels with the same launch shapes, so the recomputed
+// activations equal the first pass bit for bit.
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "common.hpp"
+#include "kernels.hpp"
+#include "sched.hpp"
+
+namespace gp {
+
+static thread_local std::string g_err;
+
+gp_status set_error(gp_status s, const char* msg) {
+    g_err = msg;
+    return s;
+}
+gp_status hip_fail(hipError_t e, const char* file, int line) {
+    g_err = std::string("HIP error: ") + hipGetErrorString(e) + " at " + file + ":" + std::to_string(line);
+    return GP_ERR_HIP;
+}
+
+struct Arena {
+    char* base = nullptr;
+    size_t off = 0;
+    template <typename X> X* take(size_t count) {
+        off = align_up(off, 256);
+        X* p = reinterpret_cast<X*>(base + off);
+        off += count * sizeof(X);
+        return p;
+    }
+    void* take_elt(size_t count, size_t esz) {
+        off = align_up(off, 256);
+        void* p = base + off;
+        off += count * esz;
+        return p;
+    }
+};
+
+struct LayerWs {
+    float *st1 = nullptr, *lse = nullptr, *x1 = nullptr;
+    void *u = nullptr, *qkv = nullptr, *c = nullptr;
+    float *stc = nullptr, *xlse = nullptr, *x2 = nullptr;
+    void *uc = nullptr, *xq = nullptr, *xkv = nullptr, *xc = nullptr;
+    float* stf = nullptr;
+    void *v = nullptr, *a = nullptr;
+};
+
+struct BwdWs {
+    float *p32 = nullptr, *q32 = nullptr, *dn = nullptr, *delta = nullptr, *partial = nullptr, *dmem32 = nullptr;
+    void *pe = nullptr, *qe = nullptr, *dz = nullptr, *dc = nullptr, *dqkv = nullptr, *dxq = nullptr, *dxkv = nullptr;
+    double *loss_partial = nullptr, *loss_acc = nullptr;
+    int* flag = nullptr;
+    // loss head
+    float* sth = nullptr;
+    void *h = nullptr, *z = nullptr;
+};
+
+} // namespace gp
+
+using namespace gp;
+
+struct gp_partition {
+    Dims d;
+    Geometry g;
+    Sched sched;
+    ParamPlan plan;
+    size_t esz = 4;
+    float* master = nullptr;
+    float* grads = nullptr;
+    char* welt = nullptr;
+    char* stash_x = nullptr;
+    char* stash_m = nullptr;
+    char* ws = nullptr;
+    std::vector<float*> xs;
+    std::vector<LayerWs> lw;
+    BwdWs bw;
+    size_t bytes_params = 0, bytes_grads = 0, bytes_stash = 0, bytes_ws = 0;
+
+    void* W(size_t elt_off) const { return welt + elt_off * esz; }
+    char* stash_x_mb(int m) const { return stash_x + (size_t)m * g.T() * d.D * esz; }
+    char* stash_m_mb(int m) const { return stash_m + (size_t)m * g.Tm() * d.D * esz; }
+    void* off_elt(void* p, long elems) const { return static_cast<char*>(p) + elems * (long)esz; }
+    const void* off_elt(const void* p, long elems) const { return static_cast<const char*>(p) + elems * (long)esz; }
+};
+
+namespace {
+
+// Carve the workspace; with a.base == nullptr only measures it.
+void plan_workspace(gp_partition* p, Arena& a) {
+    const Dims& d = p->d;
+    const Geometry& g = p->g;
+    const long T = g.T(), Tm = g.Tm(), D = d.D, F = d.F;
+    const long lse_n = (long)g.n * d.H * g.S;
+    const size_t e = p->esz;
+    const bool dec = g.kind == GP_DECODER_CROSS;
+    p->xs.assign(d.L + 1, nullptr);
+    for (auto& x : p->xs) x = a.take<float>(T * D);
+    p->lw.assign(d.L, LayerWs{});
+    for (auto& l : p->lw) {
+        l.st1 = a.take<float>(2 * T);
+        l.u = a.take_elt(T * D, e);
+        l.qkv = a.take_elt(T * 3 * D, e);
+        l.c = a.take_elt(T * D, e);
+        l.lse = a.take<float>(lse_n);
+        l.x1 = a.take<float>(T * D);
+        if (dec) {
+            l.stc = a.take<float>(2 * T);
+            l.uc = a.take_elt(T * D, e);
+            l.xq = a.take_elt(T * D, e);
+            l.xkv = a.take_elt(Tm * 2 * D, e);
+            l.xc = a.take_elt(T * D, e);
+            l.xlse = a.take<float>(lse_n);
+            l.x2 = a.take<float>(T * D);
+        }
+        l.stf = a.take<float>(2 * T);
+        l.v = a.take_elt(T * D, e);
+        l.a = a.take_elt(T * F, e);
+    }
+    BwdWs& b = p->bw;
+    b.p32 = a.take<float>(T * D);
+    b.q32 = a.take<float>(T * D);
+    b.pe = a.take_elt(T * D, e);
+    b.qe = a.take_elt(T * D, e);
+    b.dn = a.take<float>(T * D);
+    b.dz = a.take_elt(T * F, e);
+    b.dc = a.take_elt(T * D, e);
+    b.dqkv = a.take_elt(T * 3 * D, e);
+    b.delta = a.take<float>(lse_n);
+    if (dec) {
+        b.dxq = a.take_elt(T * D, e);
+        b.dxkv = a.take_elt(Tm * 2 * D, e);
+        b.dmem32 = a.take<float>(Tm * D);
+    }
+    long maxN = 3 * D > F ? 3 * D : F;
+    if (g.loss == GP_LOSS_XENT_LS && g.V > maxN) maxN = g.V;
+    size_t part = (size_t)layernorm_bwd_blocks(T) * 2 * D;
+    size_t pb = (size_t)bias_grad_blocks(T) * maxN;
+    if (pb > part) part = pb;
+    if (dec) {
+        size_t pm = (size_t)bias_grad_blocks(Tm) * 2 * D;
+        if (pm > part) part = pm;
+    }
+    b.partial = a.take<float>(part);
+    size_t lp = (size_t)loss_blocks();
+    if (g.loss == GP_LOSS_XENT_LS && (size_t)xent_partials(T) > lp) lp = xent_partials(T);
+    b.loss_partial = a.take<double>(lp);
+    b.loss_acc = a.take<double>(1);
+    b.flag = a.take<int>(1);
+    if (g.loss == GP_LOSS_XENT_LS) {
+        b.sth = a.take<float>(2 * T);
+        b.h = a.take_elt(T * D, e);
+        b.z = a.take_elt(T * (long)g.V, e);
+    }
+}
+
+struct Ctx {
+    gp_partition* p;
+    hipStream_t st;
+    int dt;
+};
+
+#define GP_TRY(x)                    \
+    do {                             \
+        gp_status s_ = (x);          \
+        if (s_ != GP_OK) return s_;  \
+    } while (0)
+
+// Y = A W + b with an epilogue; A [M, K] k-contiguous, W^T working copy [N, K].
+gp_status linear_fwd(const Ctx& c, const Linear& L, const void* A, long M, void* C, long ldc, int epi, int relu,
+                     const float* res, void* C2) {
+    GemmArgs g;
+    g.M = (int)M;
+    g.N = L.out;
+    g.K = L.in;
+    g.A = A;
+    g.lda = L.in;
+    g.B = c.p->W(L.nk);
+    g.ldb = L.in;
+    g.C = C;
+    g.ldc = ldc;
+    g.C2 = C2;
+    g.ldc2 = ldc;
+    g.bias = c.p->master + L.b;
+    g.aux = res;
+    g.ldaux = ldc;
+    g.relu = relu;
+    return gemm(g, epi, true, true, c.dt, c.st);
+}
+
+// dX = dY W^T with an epilogue; dY [M, out] k-contiguous, W working copy [in, out].
+gp_status linear_dx(const Ctx& c, const Linear& L, const void* dY, long M, void* C, int epi, const void* aux,
+                    int accumulate) {
+    GemmArgs g;
+    g.M = (int)M;
+    g.N = L.in;
+    g.K = L.out;
+    g.A = dY;
+    g.lda = L.out;
+    g.B = c.p->W(L.kn);
+    g.ldb = L.out;
+    g.C = C;
+    g.ldc = L.in;
+    g.aux = aux;
+    g.ldaux = L.in;
+    g.accumulate = accumulate;
+    return gemm(g, epi, true, true, c.dt, c.st);
+}
+
+// G_W (+)= X^T dY and G_b (+)= sum_rows dY.  X [rows, in], dY [rows, out].
+gp_status linear_dw(const Ctx& c, const Linear& L, const void* X, const void* dY, long rows, int accumulate) {
+    GemmArgs g;
+    g.M = L.in;
+    g.N = L.out;
+    g.K = (int)rows;
+    g.A = X;
+    g.lda = L.in;
+    g.B = dY;
+    g.ldb = L.out;
+    g.C = c.p->grads + L.w;
+    g.ldc = L.out;
+    g.accumulate = accumulate;
+    GP_TRY(gemm(g, EPI_ACC_F32, false, false, c.dt, c.st));
+    return bias_grad(c.dt, dY, rows, L.out, L.out, c.p->bw.partial, c.p->grads + L.b, accumulate, c.st);
+}
+
+gp_status norm_bwd(const Ctx& c, const Norm& N, const float* dn, const float* x, const float* stats, long rows,
+                   const float* dres, float* dx32, void* dxe, int accumulate) {
+    int nblk = 0;
+    GP_TRY(layernorm_bwd(c.dt, dn, x, stats, c.p->master + N.g, rows, N.n, dres, dx32, dxe, c.p->bw.partial, &nblk,
+                         c.st));
+    return colsum_finalize(c.p->bw.partial, nblk, 2 * N.n, c.p->grads + N.g, accumulate, c.st);
+}
+
+AttnArgs attn_args(const gp_partition* p, int Sk, int causal) {
+    AttnArgs a;
+    a.n = p->g.n;
+    a.H = p->d.H;
+    a.Sq = p->g.S;
+    a.Sk = Sk;
+    a.dh = p->d.D / p->d.H;
+    a.causal = causal;
+    a.scale = 1.f / sqrtf((float)a.dh);
+    return a;
+}
+
+// One layer's forward.  `ws` holds its intermediates, x_in/x_out the residual
+// stream; mem is the decoder memory (elt [Tm, D]); y_out (optional) receives
+// the output rounded to the partition dtype.
+gp_status layer_forward(const Ctx& c, int l, LayerWs& w, const float* x_in, float* x_out, const void* mem,
+                        void* y_out) {
+    gp_partition* p = c.p;
+    const LayerPlan& P = p->plan.layers[l];
+    const long T = p->g.T(), D = p->d.D;
+    const bool dec = p->g.kind == GP_DECODER_CROSS;
+    const float eps = p->g.eps;
+    // self-attention block
+    GP_TRY(layernorm_fwd(c.dt, x_in, T, (int)D, p->master + P.ln1.g, p->master + P.ln1.b, eps, w.u, w.st1, c.st));
+    GP_TRY(linear_fwd(c, P.qkv, w.u, T, w.qkv, 3 * D, EPI_STORE, 0, nullptr, nullptr));
+    AttnArgs a = attn_args(p, p->g.S, dec ? 1 : 0);
+    a.q = w.qkv;
+    a.k = p->off_elt(w.qkv, D);
+    a.v = p->off_elt(w.qkv, 2 * D);
+    a.ldq = a.ldk = a.ldv = 3 * D;
+    a.o = w.c;
+    a.ldo = D;
+    a.lse = w.lse;
+    GP_TRY(attention_fwd(c.dt, a, c.st));
+    GP_TRY(linear_fwd(c, P.o, w.c, T, w.x1, D, EPI_RES_F32, 0, x_in, nullptr));
+    const float* xf = w.x1;
+    if (dec) {
+        // cross-attention block: queries from LN2(x1), keys/values from the memory
+        GP_TRY(layernorm_fwd(c.dt, w.x1, T, (int)D, p->master + P.ln2.g, p->master + P.ln2.b, eps, w.uc, w.stc, c.st));
+        GP_TRY(linear_fwd(c, P.xq, w.uc, T, w.xq, D, EPI_STORE, 0, nullptr, nullptr));
+        GP_TRY(linear_fwd(c, P.xkv, mem, p->g.Tm(), w.xkv, 2 * D, EPI_STORE, 0, nullptr, nullptr));
+        AttnArgs x = attn_args(p, p->g.Smem, 0);
+        x.q = w.xq;
+        x.ldq = D;
+        x.k = w.xkv;
+        x.v = p->off_elt(w.xkv, D);
+        x.ldk = x.ldv = 2 * D;
+        x.o = w.xc;
+        x.ldo = D;
+        x.lse = w.xlse;
+        GP_TRY(attention_fwd(c.dt, x, c.st));
+        GP_TRY(linear_fwd(c, P.xo, w.xc, T, w.x2, D, EPI_RES_F32, 0, w.x1, nullptr));
+        xf = w.x2;
+    }
+    // feed-forward block
+    const Norm& nf = dec ? P.ln3 : P.ln2;
+    GP_TRY(layernorm_fwd(c.dt, xf, T, (int)D, p->master + nf.g, p->master + nf.b, eps, w.v, w.stf, c.st));
+    GP_TRY(linear_fwd(c, P.ffn1, w.v, T, w.a, p->d.F, EPI_STORE, 1, nullptr, nullptr));
+    GP_TRY(linear_fwd(c, P.ffn2, w.a, T, x_out, D, EPI_RES_F32, 0, xf, y_out));
+    return GP_OK;
+}
+
+// Forward of micro-batch m through all layers.  keep = false: first pass,
+// intermediates discarded (slot 0, ping-pong residuals); keep = true:
+// re-materialisation from the stash, intermediates kept per layer.
+gp_status partition_forward(const Ctx& c, int m, bool keep, const void* x, const void* mem, void* y) {
+    gp_partition* p = c.p;
+    const long T = p->g.T(), D = p->d.D;
+    const int L = p->d.L;
+    if (!keep) {
+        GP_TRY(intake(c.dt, x, p->stash_x_mb(m), p->xs[0], T * D, c.st));
+        if (mem) GP_TRY(intake(c.dt, mem, p->stash_m_mb(m), nullptr, p->g.Tm() * D, c.st));
+    } else {
+        GP_TRY(intake(c.dt, p->stash_x_mb(m), nullptr, p->xs[0], T * D, c.st));
+    }
+    const void* mem_m = p->g.kind == GP_DECODER_CROSS ? p->stash_m_mb(m) : nullptr;
+    for (int l = 0; l < L; ++l) {
+        LayerWs& w = keep ? p->lw[l] : p->lw[0];
+        const float* xi = keep ? p->xs[l] : p->xs[l & 1];
+        float* xo = keep ? p->xs[l + 1] : p->xs[(l + 1) & 1];
+        GP_TRY(layer_forward(c, l, w, xi, xo, mem_m, (!keep && l == L - 1) ? y : nullptr));
+    }
+    return GP_OK;
+}
+
+// Backward of one layer.  dY arrives in (in32, ine); dX leaves in the pair
+// returned through out32/oute (one of the two backward pairs).
+gp_status layer_backward(const Ctx& c, int l, bool first, float* in32, void* ine, float* sc32, void* sce,
+                         float*& out32, void*& oute, float* dx32_final, void* dxe_final, const void* mem) {
+    gp_partition* p = c.p;
+    const LayerPlan& P = p->plan.layers[l];
+    LayerWs& w = p->lw[l];
+    BwdWs& b = p->bw;
+    const long T = p->g.T(), Tm = p->g.Tm(), D = p->d.D;
+    const bool dec = p->g.kind == GP_DECODER_CROSS;
+    const int acc = first ? 0 : 1;
+    const float* xf = dec ? w.x2 : w.x1;
+    const Norm& nf = dec ? P.ln3 : P.ln2;
+    // feed-forward block:  dW2, db2;  dz = dY W2^T * [a > 0];  dW1, db1;  dv = dz W1^T
+    GP_TRY(linear_dw(c, P.ffn2, w.a, ine, T, acc));
+    GP_TRY(linear_dx(c, P.ffn2, ine, T, b.dz, EPI_RELU_MASK, w.a, 0));
+    GP_TRY(linear_dw(c, P.ffn1, w.v, b.dz, T, acc));
+    GP_TRY(linear_dx(c, P.ffn1, b.dz, T, b.dn, EPI_F32, nullptr, 0));
+    GP_TRY(norm_bwd(c, nf, b.dn, xf, w.stf, T, in32, sc32, sce, acc));
+    // (sc) = dL/d(xf)
+    float* cur32 = sc32;
+    void* cure = sce;
+    float* oth32 = in32;
+    void* othe = ine;
+    if (dec) {
+        // cross-attention block
+        GP_TRY(linear_dw(c, P.xo, w.xc, cure, T, acc));
+        GP_TRY(linear_dx(c, P.xo, cure, T, b.dc, EPI_STORE, nullptr, 0));
+        AttnArgs x = attn_args(p, p->g.Smem, 0);
+        x.q = w.xq;
+        x.ldq = D;
+        x.k = w.xkv;
+        x.v = p->off_elt(w.xkv, D);
+        x.ldk = x.ldv = 2 * D;
+        x.o = w.xc;
+        x.ldo = D;
+        x.lse = w.xlse;
+        x.dout = b.dc;
+        x.lddo = D;
+        x.dq = b.dxq;
+        x.lddq = D;
+        x.dk = b.dxkv;
+        x.dv = p->off_elt(b.dxkv, D);
+        x.lddk = x.lddv = 2 * D;
+        x.delta = b.delta;
+        GP_TRY(attention_bwd(c.dt, x, c.st));
+        GP_TRY(linear_dw(c, P.xq, w.uc, b.dxq, T, acc));
+        GP_TRY(linear_dx(c, P.xq, b.dxq, T, b.dn, EPI_F32, nullptr, 0));
+        GP_TRY(linear_dw(c, P.xkv, mem, b.dxkv, Tm, acc));
+        GP_TRY(linear_dx(c, P.xkv, b.dxkv, Tm, b.dmem32, EPI_ACC_F32, nullptr, l == p->d.L - 1 ? 0 : 1));
+        GP_TRY(norm_bwd(c, P.ln2, b.dn, w.x1, w.stc, T, cur32, oth32, othe, acc));
+        std::swap(cur32, oth32);
+        std::swap(cure, othe);
+    }
+    // self-attention block
+    GP_TRY(linear_dw(c, P.o, w.c, cure, T, acc));
+    GP_TRY(linear_dx(c, P.o, cure, T, b.dc, EPI_STORE, nullptr, 0));
+    AttnArgs a = attn_args(p, p->g.S, dec ? 1 : 0);
+    a.q = w.qkv;
+    a.k = p->off_elt(w.qkv, D);
+    a.v = p->off_elt(w.qkv, 2 * D);
+    a.ldq = a.ldk = a.ldv = 3 * D;
+    a.o = w.c;
+    a.ldo = D;
+    a.lse = w.lse;
+    a.dout = b.dc;
+    a.lddo = D;
+    a.dq = b.dqkv;
+    a.dk = p->off_elt(b.dqkv, D);
+    a.dv = p->off_elt(b.dqkv, 2 * D);
+    a.lddq = a.lddk = a.lddv = 3 * D;
+    a.delta = b.delta;
+    GP_TRY(attention_bwd(c.dt, a, c.st));
+    GP_TRY(linear_dw(c, P.qkv, w.u, b.dqkv, T, acc));
+    GP_TRY(linear_dx(c, P.qkv, b.dqkv, T, b.dn, EPI_F32, nullptr, 0));
+    const float* x_in = p->xs[l];
+    if (dxe_final || dx32_final || l == 0) {
+        GP_TRY(norm_bwd(c, P.ln1, b.dn, x_in, w.st1, T, cur32, dx32_final, dxe_final, acc));
+        out32 = dx32_final;
+        oute = dxe_final;
+    } else {
+        GP_TRY(norm_bwd(c, P.ln1, b.dn, x_in, w.st1, T, cur32, oth32, othe, acc));
+        out32 = oth32;
+        oute = othe;
+    }
+    return GP_OK;
+}
+
+gp_status head_backward(const Ctx& c, bool first, const int* labels) {
+    gp_partition* p = c.p;
+    const HeadPlan& Hd = p->plan.head;
+    BwdWs& b = p->bw;
+    const long T = p->g.T(), D = p->d.D, V = p->g.V;
+    const int acc = first ? 0 : 1;
+    const float* y = p->xs[p->d.L];
+    GP_TRY(layernorm_fwd(c.dt, y, T, (int)D, p->master + Hd.lnf.g, p->master + Hd.lnf.b, p->g.eps, b.h, b.sth, c.st));
+    GP_TRY(linear_fwd(c, Hd.out, b.h, T, b.z, V, EPI_STORE, 0, nullptr, nullptr));
+    const double norm = (double)p->g.n * p->g.M * p->g.S;
+    GP_TRY(xent_ls(c.dt, b.z, T, (int)V, labels, p->g.ls, norm, b.loss_partial, c.st));
+    GP_TRY(loss_finalize(b.loss_partial, (int)T, b.loss_acc, acc, c.st));
+    GP_TRY(linear_dw(c, Hd.out, b.h, b.z, T, acc));
+    GP_TRY(linear_dx(c, Hd.out, b.z, T, b.dn, EPI_F32, nullptr, 0));
+    return norm_bwd(c, Hd.lnf, b.dn, y, b.sth, T, nullptr, b.p32, b.pe, acc);
+}
+
+gp_status upload_param_block(gp_partition* p, const ParamRef& r, const float* host) {
+    GP_HIP(hipMemcpy2D(p->master + r.off, (size_t)r.ld * 4, host, (size_t)r.cols * 4, (size_t)r.cols * 4, r.rows,
+                       hipMemcpyHostToDevice));
+    if (r.lin) {
+        GP_TRY(refresh_linear(p->g.dtype, p->master + r.lin->w, r.lin->in, r.lin->out, p->W(r.lin->kn),
+                              p->W(r.lin->nk), nullptr));
+        GP_HIP(hipDeviceSynchronize());
+    }
+    return GP_OK;
+}
+
+void free_all(gp_partition* p) {
+    for (void* x : {(void*)p->master, (void*)p->grads, (void*)p->welt, (void*)p->stash_x, (void*)p->stash_m,
+                    (void*)p->ws})
+        if (x) (void)hipFree(x);
+    p->master = p->grads = nullptr;
+    p->welt = p->stash_x = p->stash_m = p->ws = nullptr;
+}
+
+gp_status alloc(void** ptr, size_t bytes) {
+    if (bytes == 0) bytes = 256;
+    hipError_t e = hipMalloc(ptr, bytes);
+    if (e == hipErrorOutOfMemory) {
+        (void)hipGetLastError();
+        return set_error(GP_ERR_OOM, "device allocation failed (out of memory)");
+    }
+    if (e != hipSuccess) return hip_fail(e, __FILE__, __LINE__);
+    return GP_OK;
+}
+
+} // namespace
+
+extern "C" {
+
+const char* gp_last_error(void) { return g_err.c_str(); }
+
+gp_status gp_partition_create(int layers, int d_model, int d_ff, int heads, gp_partition** out) {
+    if (!out) return set_error(GP_ERR_INVALID_ARG, "out must not be NULL");
+    *out = nullptr;
+    std::string msg;
+    gp_status s = check_dims(layers, d_model, d_ff, heads, msg);
+    if (s != GP_OK) return set_error(s, msg.c_str());
+    gp_partition* p = new (std::nothrow) gp_partition();
+    if (!p) return set_error(GP_ERR_OOM, "host allocation failed");
+    p->d.L = layers;
+    p->d.D = d_model;
+    p->d.F = d_ff;
+    p->d.H = heads;
+    *out = p;
+    return GP_OK;
+}
+
+gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
+    if (!p || !cfg) return set_error(GP_ERR_INVALID_ARG, "partition and config must not be NULL");
+    std::string msg;
+    if (p->sched.configured()) return set_error(GP_ERR_STATE, "partition already configured");
+    gp_status s = check_config(p->d, *cfg, msg);
+    if (s != GP_OK) return set_error(s, msg.c_str());
+    Geometry& g = p->g;
+    g.S = cfg->seq_len;
+    g.n = cfg->seqs_per_microbatch;
+    g.M = cfg->num_microbatches;
+    g.dtype = cfg->dtype;
+    g.kind = cfg->kind;
+    g.Smem = cfg->mem_seq_len;
+    g.loss = cfg->loss;
+    g.V = cfg->vocab;
+    g.ls = cfg->label_smoothing;
+    g.eps = cfg->ln_eps;
+    g.check_finite = cfg->check_finite;
+    p->esz = g.dtype == GP_BF16 ? 2 : 4;
+    p->plan = plan_params(p->d, g);
+    Arena measure;
+    plan_workspace(p, measure);
+    p->bytes_params = p->plan.n32 * 4 + p->plan.nelt * p->esz;
+    p->bytes_grads = p->plan.n32 * 4;
+    p->bytes_stash = (size_t)g.M * (g.T() + g.Tm()) * p->d.D * p->esz;
+    p->bytes_ws = measure.off;
+    void *m = nullptr, *gr = nullptr, *we = nullptr, *sx = nullptr, *sm = nullptr, *ws = nullptr;
+    s = alloc(&m, p->plan.n32 * 4);
+    if (s == GP_OK) s = alloc(&gr, p->plan.n32 * 4);
+    if (s == GP_OK) s = alloc(&we, p->plan.nelt * p->esz);
+    if (s == GP_OK) s = alloc(&sx, (size_t)g.M * g.T() * p->d.D * p->esz);
+    if (s == GP_OK && g.Tm() > 0) s = alloc(&sm, (size_t)g.M * g.Tm() * p->d.D * p->esz);
+    if (s == GP_OK) s = alloc(&ws, p->bytes_ws);
+    p->master = (float*)m;
+    p->grads = (float*)gr;
+    p->welt = (char*)we;
+    p->stash_x = (char*)sx;
+    p->stash_m = (char*)sm;
+    p->ws = (char*)ws;
+    if (s != GP_OK) {
+        free_all(p);
+        return s;
+    }
+    Arena real;
+    real.base = p->ws;
+    plan_workspace(p, real);
+    // parameters: zero, LayerNorm gains 1; accumulators zero
+    std::vector<float> init(p->plan.n32, 0.f);
+    for (const Norm* n : p->plan.norms())
+        for (int i = 0; i < n->n; ++i) init[n->g + i] = 1.f;
+    hipError_t e = hipMemcpy(p->master, init.data(), p->plan.n32 * 4, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemset(p->grads, 0, p->plan.n32 * 4);
+    if (e == hipSuccess) e = hipMemset(p->ws, 0, p->bytes_ws);
+    if (e != hipSuccess) {
+        free_all(p);
+        return hip_fail(e, __FILE__, __LINE__);
+    }
+    for (const Linear* l : p->plan.linears()) {
+        s = refresh_linear(g.dtype, p->master + l->w, l->in, l->out, p->W(l->kn), p->W(l->nk), nullptr);
+        if (s != GP_OK) {
+            free_all(p);
+            return s;
+        }
+    }
+    e = hipDeviceSynchronize();
+    if (e != hipSuccess) {
+        free_all(p);
+        return hip_fail(e, __FILE__, __LINE__);
+    }
+    p->sched.configure(g.M, msg);
+    return GP_OK;
+}
+
+gp_status gp_partition_destroy(gp_partition* p) {
+    if (!p) return GP_OK;
+    if (p->sched.configured()) (void)hipDeviceSynchronize();
+    free_all(p);
+    delete p;
+    return GP_OK;
+}
+
+static gp_status param_io(gp_partition* p, int layer, int id, float* host, size_t count, int what) {
+    if (!p || !host) return set_error(GP_ERR_INVALID_ARG, "partition and host buffer must not be NULL");
+    std::string msg;
+    if (!p->sched.configured()) return set_error(GP_ERR_STATE, "partition not configured");
+    if (what == 0) {
+        gp_status s = p->sched.can_set_param(msg);
+        if (s != GP_OK) return set_error(s, msg.c_str());
+    }
+    ParamRef r;
+    gp_status s = resolve_param(p->plan, p->d, layer, id, r, msg);
+    if (s != GP_OK) return set_error(s, msg.c_str());
+    if (count != (size_t)r.rows * r.cols) return set_error(GP_ERR_INVALID_ARG, "count does not match the parameter's size");
+    if (what == 0) return upload_param_block(p, r, host);
+    GP_HIP(hipDeviceSynchronize());
+    const float* src = (what == 1 ? p->master : p->grads) + r.off;
+    GP_HIP(hipMemcpy2D(host, (size_t)r.cols * 4, src, (size_t)r.ld * 4, (size_t)r.cols * 4, r.rows,
+                       hipMemcpyDeviceToHost));
+    return GP_OK;
+}
+
+gp_status gp_set_param(gp_partition* p, int layer, int id, const float* host, size_t count) {
+    return param_io(p, layer, id, const_cast<float*>(host), count, 0);
+}
+gp_status gp_get_param(gp_partition* p, int layer, int id, float* host, size_t count) {
+    return param_io(p, layer, id, host, count, 1);
+}
+gp_status gp_get_grad(gp_partition* p, int layer, int id, float* host, size_t count) {
+    return param_io(p, layer, id, host, count, 2);
+}
+
+gp_status gp_partition_memory(gp_partition* p, size_t* params, size_t* grads, size_t* stash, size_t* workspace) {
+    if (!p) return set_error(GP_ERR_INVALID_ARG, "partition must not be NULL");
+    if (!p->sched.configured()) return set_error(GP_ERR_STATE, "partition not configured");
+    if (params) *params = p->bytes_params;
+    if (grads) *grads = p->bytes_grads;
+    if (stash) *stash = p->bytes_stash;
+    if (workspace) *workspace = p->bytes_ws;
+    return GP_OK;
+}
+
+gp_status gp_param_count(gp_partition* p, size_t* count) {
+    if (!p || !count) return set_error(GP_ERR_INVALID_ARG, "partition and count must not be NULL");
+    if (!p->sched.configured()) return set_error(GP_ERR_STATE, "partition not configured");
+    *count = p->plan.count;
+    return GP_OK;
+}
+
+gp_status gp_forward_microbatch(gp_partition* p, int mb, const void* x, const void* mem, void* y, gp_stream stream) {
+    if (!p) return set_error(GP_ERR_INVALID_ARG, "partition must not be NULL");
+    std::string msg;
+    gp_status s = p->sched.can_forward(mb, msg);
+    if (s != GP_OK) return set_error(s, msg.c_str());
+    if (!x) return set_error(GP_ERR_INVALID_ARG, "x must not be NULL");
+    const bool dec = p->g.kind == GP_DECODER_CROSS;
+    if (dec && !mem) return set_error(GP_ERR_INVALID_ARG, "decoder partitions need the memory input");
+    if (!dec && mem) return set_error(GP_ERR_INVALID_ARG, "encoder partitions take no memory input");
+    Ctx c{p, (hipStream_t)stream, p->g.dtype};
+    s = partition_forward(c, mb, false, x, mem, y);
+    if (s != GP_OK) return s;
+    p->sched.did_forward();
+    return GP_OK;
+}
+
+gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_or_target, void* dx, void* dmem,
+                                       gp_stream stream) {
+    if (!p) return set_error(GP_ERR_INVALID_ARG, "partition must not be NULL");
+    std::string msg;
+    gp_status s = p->sched.can_backward(mb, msg);
+    if (s != GP_OK) return set_error(s, msg.c_str());
+    if (!dy_or_target) return set_error(GP_ERR_INVALID_ARG, "dy_or_target must not be NULL");
+    const bool dec = p->g.kind == GP_DECODER_CROSS;
+    if (!dec && dmem) return set_error(GP_ERR_INVALID_ARG, "encoder partitions have no memory gradient");
+    Ctx c{p, (hipStream_t)stream, p->g.dtype};
+    const bool first = p->sched.first_backward();
+    const long T = p->g.T(), D = p->d.D;
+    // re-materialise this micro-batch's forward from the stash
+    s = partition_forward(c, mb, true, nullptr, nullptr, nullptr);
+    if (s != GP_OK) return s;
+    BwdWs& b = p->bw;
+    // dL/dy of the partition output
+    if (p->g.loss == GP_LOSS_NONE) {
+        s = intake(c.dt, dy_or_target, b.pe, b.p32, T * D, c.st);
+    } else if (p->g.loss == GP_LOSS_MSE) {
+        int nb = 0;
+        const double norm = (double)p->g.n * p->g.M * p->g.S * D;
+        s = mse_grad(c.dt, p->xs[p->d.L], dy_or_target, T * D, norm, b.p32, b.pe, b.loss_partial, &nb, c.st);
+        if (s == GP_OK) s = loss_finalize(b.loss_partial, nb, b.loss_acc, first ? 0 : 1, c.st);
+    } else {
+        s = head_backward(c, first, reinterpret_cast<const int*>(dy_or_target));
+    }
+    if (s != GP_OK) return s;
+    const void* mem_m = dec ? p->stash_m_mb(mb) : nullptr;
+    float* in32 = b.p32;
+    void* ine = b.pe;
+    float* sc32 = b.q32;
+    void* sce = b.qe;
+    for (int l = p->d.L - 1; l >= 0; --l) {
+        float* out32 = nullptr;
+        void* oute = nullptr;
+        s = layer_backward(c, l, first, in32, ine, sc32, sce, out32, oute, nullptr, l == 0 ? dx : nullptr, mem_m);
+        if (s != GP_OK) return s;
+        if (l > 0) {
+            // the pair not holding dX becomes scratch for the next layer
+            float* f32 = (out32 == b.p32) ? b.q32 : b.p32;
+            void* fe = (oute == b.pe) ? b.qe : b.pe;
+            in32 = out32;
+            ine = oute;
+            sc32 = f32;
+            sce = fe;
+        }
+    }
+    if (dec && dmem) {
+        s = cast_out(c.dt, b.dmem32, dmem, p->g.Tm() * D, c.st);
+        if (s != GP_OK) return s;
+    }
+    p->sched.did_backward();
+    return GP_OK;
+}
+
+gp_status gp_accumulate_and_step(gp_partition* p, float lr, double* loss_out, gp_stream stream) {
+    if (!p) return set_error(GP_ERR_INVALID_ARG, "partition must not be NULL");
+    std::string msg;
+    gp_status s = p->sched.can_step(msg);
+    if (s != GP_OK) return set_error(s, msg.c_str());
+    hipStream_t st = (hipStream_t)stream;
+    const int dt = p->g.dtype;
+    if (p->g.check_finite) {
+        GP_HIP(hipMemsetAsync(p->bw.flag, 0, sizeof(int), st));
+        GP_TRY(finite_check(p->grads, (long)p->plan.n32, p->bw.flag, st));
+        int flag = 0;
+        GP_HIP(hipMemcpyAsync(&flag, p->bw.flag, sizeof(int), hipMemcpyDeviceToHost, st));
+        GP_HIP(hipStreamSynchronize(st));
+        if (flag) {
+            p->sched.did_step();
+            return set_error(GP_ERR_NONFINITE, "non-finite gradient: update skipped");
+        }
+    }
+    GP_TRY(sgd_update(p->master, p->grads, lr, (long)p->plan.n32, st));
+    for (const Linear* l : p->plan.linears())
+        GP_TRY(refresh_linear(dt, p->master + l->w, l->in, l->out, p->W(l->kn), p->W(l->nk), st));
+    if (loss_out) {
+        double v = 0.0;
+        if (p->g.loss != GP_LOSS_NONE)
+            GP_HIP(hipMemcpyAsync(&v, p->bw.loss_acc, sizeof(double), hipMemcpyDeviceToHost, st));
+        GP_HIP(hipStreamSynchronize(st));
+        *loss_out = v;
+    }
+    p->sched.did_step();
+    return GP_OK;
+}
+
+} // extern "C"

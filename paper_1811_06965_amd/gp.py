@@ -1,0 +1,147 @@
+"""ctypes binding of the partition's C ABI (include/gp.h).
+
+Argument marshalling only: every step of the partition's work runs in the HIP
+kernels of libgp.so.  Device buffers are passed as integer device addresses
+(e.g. ``tensor.data_ptr()``) and streams as raw HIP stream handles (e.g.
+``torch.cuda.current_stream().cuda_stream``).  If the library has not been
+built the import-time loader raises: there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "_lib", "libgp.so")
+
+GP_OK, GP_ERR_INVALID_ARG, GP_ERR_STATE, GP_ERR_OOM, GP_ERR_HIP, GP_ERR_NONFINITE, GP_ERR_UNSUPPORTED = range(7)
+STATUS_NAMES = {0: "GP_OK", 1: "GP_ERR_INVALID_ARG", 2: "GP_ERR_STATE", 3: "GP_ERR_OOM", 4: "GP_ERR_HIP",
+                5: "GP_ERR_NONFINITE", 6: "GP_ERR_UNSUPPORTED"}
+GP_F32, GP_BF16 = 0, 1
+GP_ENCODER, GP_DECODER_CROSS = 0, 1
+GP_LOSS_NONE, GP_LOSS_MSE, GP_LOSS_XENT_LS = 0, 1, 2
+
+PARAM_IDS = ["ln1_g", "ln1_b", "wq", "bq", "wk", "bk", "wv", "bv", "wo", "bo", "ln2_g", "ln2_b",
+             "w1", "b1", "w2", "b2", "xwq", "xbq", "xwk", "xbk", "xwv", "xbv", "xwo", "xbo",
+             "ln3_g", "ln3_b", "lnf_g", "lnf_b", "wout", "bout"]
+PARAM_ID = {name: i for i, name in enumerate(PARAM_IDS)}
+
+EXPORTS = ["gp_partition_create", "gp_partition_configure", "gp_partition_destroy", "gp_set_param",
+           "gp_get_param", "gp_get_grad", "gp_partition_memory", "gp_param_count", "gp_forward_microbatch",
+           "gp_backward_microbatch_remat", "gp_accumulate_and_step", "gp_last_error"]
+
+
+class gp_config(ctypes.Structure):
+    _fields_ = [("seq_len", ctypes.c_int), ("seqs_per_microbatch", ctypes.c_int),
+                ("num_microbatches", ctypes.c_int), ("dtype", ctypes.c_int), ("kind", ctypes.c_int),
+                ("mem_seq_len", ctypes.c_int), ("loss", ctypes.c_int), ("vocab", ctypes.c_int),
+                ("label_smoothing", ctypes.c_float), ("ln_eps", ctypes.c_float),
+                ("check_finite", ctypes.c_int)]
+
+
+class GpError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libgp.so (once).  Raises if it is missing: build it first."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build the HIP library first (python -m paper_1811_06965_amd.build)")
+    lib = ctypes.CDLL(path)
+    P, VP, I, SZ = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    FP = ctypes.POINTER(ctypes.c_float)
+    lib.gp_partition_create.argtypes = [I, I, I, I, ctypes.POINTER(P)]
+    lib.gp_partition_configure.argtypes = [P, ctypes.POINTER(gp_config)]
+    lib.gp_partition_destroy.argtypes = [P]
+    for f in (lib.gp_set_param, lib.gp_get_param, lib.gp_get_grad):
+        f.argtypes = [P, I, I, FP, SZ]
+    lib.gp_partition_memory.argtypes = [P] + [ctypes.POINTER(SZ)] * 4
+    lib.gp_param_count.argtypes = [P, ctypes.POINTER(SZ)]
+    lib.gp_forward_microbatch.argtypes = [P, I, VP, VP, VP, VP]
+    lib.gp_backward_microbatch_remat.argtypes = [P, I, VP, VP, VP, VP]
+    lib.gp_accumulate_and_step.argtypes = [P, ctypes.c_float, ctypes.POINTER(ctypes.c_double), VP]
+    lib.gp_last_error.argtypes = []
+    lib.gp_last_error.restype = ctypes.c_char_p
+    for name in EXPORTS:
+        if name != "gp_last_error":
+            getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def gp_last_error() -> str:
+    return load().gp_last_error().decode()
+
+
+def _check(status):
+    if status != GP_OK:
+        raise GpError(status, gp_last_error())
+
+
+def _fptr(a):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+
+
+# --- one function per C entry point, same names -------------------------------
+def gp_partition_create(layers, d_model, d_ff, heads):
+    h = ctypes.c_void_p()
+    _check(load().gp_partition_create(layers, d_model, d_ff, heads, ctypes.byref(h)))
+    return h
+
+
+def gp_partition_configure(h, cfg: gp_config):
+    _check(load().gp_partition_configure(h, ctypes.byref(cfg)))
+
+
+def gp_partition_destroy(h):
+    _check(load().gp_partition_destroy(h))
+
+
+def gp_set_param(h, layer, pid, host):
+    """host: C-contiguous float32 numpy array."""
+    _check(load().gp_set_param(h, layer, pid, _fptr(host), host.size))
+
+
+def gp_get_param(h, layer, pid, host):
+    _check(load().gp_get_param(h, layer, pid, _fptr(host), host.size))
+
+
+def gp_get_grad(h, layer, pid, host):
+    _check(load().gp_get_grad(h, layer, pid, _fptr(host), host.size))
+
+
+def gp_partition_memory(h):
+    v = [ctypes.c_size_t() for _ in range(4)]
+    _check(load().gp_partition_memory(h, *[ctypes.byref(x) for x in v]))
+    return dict(params=v[0].value, grads=v[1].value, stash=v[2].value, workspace=v[3].value)
+
+
+def gp_param_count(h):
+    v = ctypes.c_size_t()
+    _check(load().gp_param_count(h, ctypes.byref(v)))
+    return v.value
+
+
+def gp_forward_microbatch(h, mb, x, mem, y, stream):
+    _check(load().gp_forward_microbatch(h, mb, x, mem, y, stream))
+
+
+def gp_backward_microbatch_remat(h, mb, dy_or_target, dx, dmem, stream):
+    _check(load().gp_backward_microbatch_remat(h, mb, dy_or_target, dx, dmem, stream))
+
+
+def gp_accumulate_and_step(h, lr, want_loss, stream):
+    if want_loss:
+        v = ctypes.c_double()
+        _check(load().gp_accumulate_and_step(h, lr, ctypes.byref(v), stream))
+        return v.value
+    _check(load().gp_accumulate_and_step(h, lr, None, stream))
+    return None

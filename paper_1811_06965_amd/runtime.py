@@ -1,0 +1,139 @@
+"""Torch-facing driver of one partition (marshalling only).
+
+Torch provides device memory and the stream; every step of the partition's
+work runs in libgp.so.  ``Partition.step`` issues GPipe's schedule for one
+mini-batch (Section 2.2): M forwards in order, M re-materialising backwards in
+reverse order, then the one synchronous update.
+"""
+from __future__ import annotations
+
+from typing import Dict, List, Optional
+
+import numpy as np
+import torch
+
+from . import gp
+
+DTYPES = {"f32": (gp.GP_F32, torch.float32), "bf16": (gp.GP_BF16, torch.bfloat16)}
+KINDS = {"encoder": gp.GP_ENCODER, "decoder": gp.GP_DECODER_CROSS}
+LOSSES = {"none": gp.GP_LOSS_NONE, "mse": gp.GP_LOSS_MSE, "xent_ls": gp.GP_LOSS_XENT_LS}
+
+
+def make_config(cfg, micro: Optional[int] = None, check_finite: bool = False) -> gp.gp_config:
+    M = cfg.micro if micro is None else micro
+    if cfg.batch % M:
+        raise ValueError("mini-batch must split into M equal micro-batches")
+    c = gp.gp_config()
+    c.seq_len = cfg.seq
+    c.seqs_per_microbatch = cfg.batch // M
+    c.num_microbatches = M
+    c.dtype = DTYPES[cfg.dtype][0]
+    c.kind = KINDS[cfg.kind]
+    c.mem_seq_len = cfg.mem_seq
+    c.loss = LOSSES[cfg.loss]
+    c.vocab = cfg.vocab
+    c.label_smoothing = cfg.label_smoothing
+    c.ln_eps = cfg.ln_eps
+    c.check_finite = 1 if check_finite else 0
+    return c
+
+
+class Partition:
+    """One configured partition on the current HIP device."""
+
+    def __init__(self, cfg, micro: Optional[int] = None, check_finite: bool = False):
+        self.cfg = cfg
+        self.M = cfg.micro if micro is None else micro
+        self.tdtype = DTYPES[cfg.dtype][1]
+        self.h = gp.gp_partition_create(cfg.layers, cfg.d_model, cfg.d_ff, cfg.heads)
+        try:
+            gp.gp_partition_configure(self.h, make_config(cfg, self.M, check_finite))
+        except Exception:
+            gp.gp_partition_destroy(self.h)
+            raise
+
+    def close(self):
+        if self.h is not None:
+            gp.gp_partition_destroy(self.h)
+            self.h = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *a):
+        self.close()
+
+    # -------------------------------------------------------------- params
+    def load_params(self, layers: List[Dict[str, np.ndarray]], head: Dict[str, np.ndarray]):
+        for l, p in enumerate(layers):
+            for name, arr in p.items():
+                gp.gp_set_param(self.h, l, gp.PARAM_ID[name], np.ascontiguousarray(arr, dtype=np.float32))
+        for name, arr in head.items():
+            gp.gp_set_param(self.h, -1, gp.PARAM_ID[name], np.ascontiguousarray(arr, dtype=np.float32))
+
+    def _read(self, fn, shapes_layers, shapes_head):
+        layers = []
+        for l in range(self.cfg.layers):
+            d = {}
+            for name, shp in shapes_layers.items():
+                a = np.empty(shp, dtype=np.float32)
+                fn(self.h, l, gp.PARAM_ID[name], a)
+                d[name] = a
+            layers.append(d)
+        head = {}
+        for name, shp in shapes_head.items():
+            a = np.empty(shp, dtype=np.float32)
+            fn(self.h, -1, gp.PARAM_ID[name], a)
+            head[name] = a
+        return layers, head
+
+    def grads(self):
+        return self._read(gp.gp_get_grad, self.cfg.param_shapes(), self.cfg.head_shapes())
+
+    def params(self):
+        return self._read(gp.gp_get_param, self.cfg.param_shapes(), self.cfg.head_shapes())
+
+    def memory(self):
+        return gp.gp_partition_memory(self.h)
+
+    def param_count(self):
+        return gp.gp_param_count(self.h)
+
+    # ------------------------------------------------------------ schedule
+    def device_inputs(self, case, device="cuda"):
+        """Move a synthetic case's boundary tensors to the device."""
+        t = lambda a: torch.tensor(a, dtype=torch.float32).to(device=device, dtype=self.tdtype).contiguous()
+        out = {"x": t(case["x"]), "mem": None if case.get("mem") is None else t(case["mem"])}
+        if self.cfg.loss == "mse":
+            out["dy"] = t(case["target"])
+        elif self.cfg.loss == "none":
+            out["dy"] = t(case["dy"])
+        else:
+            out["dy"] = torch.tensor(case["labels"], dtype=torch.int32, device=device).contiguous()
+        return out
+
+    def step(self, x, mem, dy, lr=0.0, want_y=True, want_dx=True, want_dmem=True, want_loss=True,
+             stream=None, y=None, dx=None, dmem=None):
+        """One mini-batch through GPipe's schedule.  x/mem/dy: device tensors
+        of the whole mini-batch (dim 0 = sequences).  Returns dict(y, dx, dmem, loss)."""
+        M = self.M
+        st = stream if stream is not None else torch.cuda.current_stream().cuda_stream
+        if want_y and y is None:
+            y = torch.empty_like(x)
+        if want_dx and dx is None:
+            dx = torch.empty_like(x)
+        if mem is not None and want_dmem and dmem is None:
+            dmem = torch.empty_like(mem)
+        xs = x.chunk(M)
+        ms = mem.chunk(M) if mem is not None else [None] * M
+        ys = y.chunk(M) if y is not None else [None] * M
+        dys = dy.chunk(M)
+        dxs = dx.chunk(M) if dx is not None else [None] * M
+        dms = dmem.chunk(M) if dmem is not None else [None] * M
+        ptr = lambda t: None if t is None else t.data_ptr()
+        for m in range(M):
+            gp.gp_forward_microbatch(self.h, m, ptr(xs[m]), ptr(ms[m]), ptr(ys[m]), st)
+        for m in range(M - 1, -1, -1):
+            gp.gp_backward_microbatch_remat(self.h, m, ptr(dys[m]), ptr(dxs[m]), ptr(dms[m]), st)
+        loss = gp.gp_accumulate_and_step(self.h, lr, want_loss, st)
+        return {"y": y, "dx": dx, "dmem": dmem, "loss": loss}

@@ -192,7 +192,4 @@ gp_status attention_bwd_simt(int dtype, const AttnArgs& a, hipStream_t st) {
     return bwd_t<float>(a, st);
 }
 
-gp_status attention_fwd(int dtype, const AttnArgs& a, hipStream_t st) { return attention_fwd_simt(dtype, a, st); }
-gp_status attention_bwd(int dtype, const AttnArgs& a, hipStream_t st) { return attention_bwd_simt(dtype, a, st); }
-
 } // namespace gp

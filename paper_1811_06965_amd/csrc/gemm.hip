@@ -3,22 +3,36 @@
 //   C[m, n] = sum_k A(m, k) B(n, k)     then a fused epilogue
 //
 // Every linear layer of the partition maps onto one of three operand forms:
-//   forward   Y  = X W      A = X  [T, in]  k-contiguous,  B = W^T [out, in]  k-contiguous
-//   input grad dX = dY W^T  A = dY [T, out] k-contiguous,  B = W   [in, out]  k-contiguous
-//   weight grad dW = X^T dY A = X  [T, in]  m-contiguous,  B = dY  [T, out]   n-contiguous
+//   forward    Y  = X W      A = X  [T, in]  k-contiguous,  B = W^T [out, in]  k-contiguous
+//   input grad dX = dY W^T   A = dY [T, out] k-contiguous,  B = W   [in, out]  k-contiguous
+//   weight grad dW = X^T dY  A = X  [T, in]  m-contiguous,  B = dY  [T, out]   n-contiguous
 // The partition keeps both W and W^T working copies so the two activation
 // GEMMs stream both operands along k.  The weight-gradient GEMM loads
 // m-contiguous 16-byte vectors over 4 consecutive k and transposes them in
-// registers, so LDS always holds k-contiguous rows and the MFMA fragment read
-// is one 16-byte LDS load per lane.
+// registers, so LDS always holds k-contiguous rows and every MFMA fragment is
+// one 16-byte LDS read per lane.
 //
-// Tiles: 128 x 128 x BK per workgroup of 4 waves (2 x 2), each wave 64 x 64 =
-// 2 x 2 MFMA blocks of 32 x 32.  bf16 uses v_mfma_f32_32x32x16_bf16 (fp32
-// accumulate), fp32 uses v_mfma_f32_32x32x2_f32.  Global tiles are prefetched
-// into registers while the current LDS buffer is consumed (two LDS buffers,
-// one barrier per k-tile).  Workgroup ids are remapped so each XCD (which
-// receives every 8th workgroup) works on a contiguous run of output tiles
-// that share weight panels in its own L2.
+// Workgroup = 4 waves (2 x 2).  Tile shapes (bf16, BK = 64):
+//   256 x 256: each wave 128 x 128 = 4 x 4 blocks of v_mfma_f32_32x32x16_bf16
+//              (256 accumulator registers per lane, held in AGPRs); 144 KB LDS
+//   256 x 128, 128 x 256, 128 x 128: smaller waves for short or thin problems.
+// Per 16-deep k-step a wave reads (TM + TN) fragments for TM x TN MFMAs, so
+// the 128 x 128 wave tile needs 64 B/clk/CU of LDS reads at full MFMA rate.
+// Pipelining: global loads of k-tile t+1 are in flight while tile t is
+// consumed; MFMA fragments are double-buffered across k-steps; the one
+// barrier per k-tile sits before the last k-step's MFMAs, which then cover
+// the latency of the first fragment reads from the new buffer.
+//
+// Split-K (for problems with too few output tiles to fill 256 CUs): k-tiles
+// are divided among gridDim.y workgroups per output tile, each writes an fp32
+// partial tile, and a reduce kernel sums the partials in a fixed order and
+// applies the epilogue -- deterministic, no atomics.
+//
+// Workgroup ids are remapped so each XCD (which receives every 8th workgroup)
+// works on a contiguous run of output tiles that share operand panels in its
+// own L2.
+#include <algorithm>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -54,23 +68,37 @@ __device__ __forceinline__ void mma(f32x16& c, const Frag<float>& a, const Frag<
 }
 
 template <typename T> using V16 = typename Vec16<T>::type;
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef __amdgpu_buffer_rsrc_t Rsrc;
 
+// Buffer resource over `bytes` bytes at p; raw buffer accesses beyond it read
+// 0 and drop writes, which implements the tile-edge masking without branches.
+constexpr uint32_t OOB = 0x80000000u;
+__device__ __forceinline__ Rsrc make_rsrc(const void* p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
 template <typename T>
-__device__ __forceinline__ V16<T> load16(const T* p, bool ok) {
-    if (ok) return *reinterpret_cast<const V16<T>*>(p);
-    V16<T> z;
-#pragma unroll
-    for (int i = 0; i < Vec16<T>::N; ++i) z[i] = (T)0.f;
-    return z;
+__device__ __forceinline__ V16<T> bload16(Rsrc r, uint32_t off) {
+    return __builtin_bit_cast(V16<T>, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+
+// LDS tiles hold ROWS rows of BK elements (128 bytes) with no padding; the
+// 16-byte chunk c of row r is stored at chunk c ^ swz(r).  swz varies over
+// any 8 consecutive rows (conflict-free fragment reads, where 8 lanes read 8
+// consecutive rows) and over rows 8 apart (conflict-free transposing stores,
+// where 8 lanes write rows 8 apart).
+__device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
+__device__ __forceinline__ int lds_byte(int row, int kbyte) {
+    return row * 128 + ((((kbyte >> 4) ^ swz(row)) << 4) | (kbyte & 15));
 }
 
 // Tile loader for one operand: ROWS x BK elements of the operand (row index =
-// m for A, n for B) into LDS laid out [ROWS][BK + PAD], k contiguous.
+// m for A, n for B), k contiguous in LDS.
 template <typename T, int ROWS, int BK, bool KMAJOR>
 struct TileLoader {
     static constexpr int VEC = Vec16<T>::N;
-    static constexpr int PAD = VEC;
-    static constexpr int LDK = BK + PAD;
+    static constexpr int ESZ = sizeof(T);
+    static_assert(BK * ESZ == 128, "one LDS row is 128 bytes");
     // k-major: each thread moves 16-byte vectors along k.
     static constexpr int TPR = BK / VEC;
     static constexpr int RPP = 256 / TPR;
@@ -85,15 +113,14 @@ struct TileLoader {
 
     V16<T> r[NREG];
 
-    __device__ __forceinline__ void load(const T* __restrict__ g, long ld, int row0, int nrows, int k0, int K,
-                                         int tid) {
-        if (KMAJOR) {
+    __device__ __forceinline__ void load(Rsrc g, long ld, int row0, int nrows, int k0, int K, int tid) {
+        if constexpr (KMAJOR) {
             const int rr = tid / TPR, kk = (tid % TPR) * VEC;
 #pragma unroll
             for (int p = 0; p < KPASS; ++p) {
                 const int row = row0 + p * RPP + rr, k = k0 + kk;
                 const bool ok = row < nrows && k < K;
-                r[p] = load16<T>(g + (long)(ok ? row : 0) * ld + (ok ? k : 0), ok);
+                r[p] = bload16<T>(g, ok ? (uint32_t)(((long)row * ld + k) * ESZ) : OOB);
             }
         } else {
 #pragma unroll
@@ -105,18 +132,18 @@ struct TileLoader {
                 for (int q = 0; q < KB; ++q) {
                     const int k = k0 + kb * KB + q;
                     const bool ok = row < nrows && k < K;
-                    r[p * KB + q] = load16<T>(g + (long)(ok ? k : 0) * ld + (ok ? row : 0), ok);
+                    r[p * KB + q] = bload16<T>(g, ok ? (uint32_t)(((long)k * ld + row) * ESZ) : OOB);
                 }
             }
         }
     }
 
-    __device__ __forceinline__ void store(T* __restrict__ s, int tid) const {
-        if (KMAJOR) {
+    __device__ __forceinline__ void store(char* __restrict__ s, int tid) const {
+        if constexpr (KMAJOR) {
             const int rr = tid / TPR, kk = (tid % TPR) * VEC;
 #pragma unroll
             for (int p = 0; p < KPASS; ++p)
-                *reinterpret_cast<V16<T>*>(s + (p * RPP + rr) * LDK + kk) = r[p];
+                *reinterpret_cast<V16<T>*>(s + lds_byte(p * RPP + rr, kk * ESZ)) = r[p];
         } else {
 #pragma unroll
             for (int p = 0; p < MPASS; ++p) {
@@ -124,7 +151,7 @@ struct TileLoader {
                 const int mb = blk % MBLK, kb = blk / MBLK;
 #pragma unroll
                 for (int i = 0; i < VEC; ++i) {
-                    T* dst = s + (mb * VEC + i) * LDK + kb * KB;
+                    char* dst = s + lds_byte(mb * VEC + i, kb * KB * ESZ);
                     if constexpr (sizeof(T) == 2) {
                         bf16x4 v = {r[p * KB + 0][i], r[p * KB + 1][i], r[p * KB + 2][i], r[p * KB + 3][i]};
                         *reinterpret_cast<bf16x4*>(dst) = v;
@@ -142,7 +169,116 @@ template <typename T> struct GemmCfg;
 template <> struct GemmCfg<bf16> { static constexpr int BK = 64; };
 template <> struct GemmCfg<float> { static constexpr int BK = 32; };
 
-// Epilogue on one output element (row, col) of value v = sum_k A B.
+// Fragment read: 8 elements (16 bytes for bf16, 32 for fp32) of one LDS row.
+template <typename T> struct FragRead;
+template <> struct FragRead<bf16> {
+    static __device__ __forceinline__ void load(Frag<bf16>& f, const char* s, int row, int kbyte) {
+        f.v = *reinterpret_cast<const bf16x8*>(s + lds_byte(row, kbyte));
+    }
+};
+template <> struct FragRead<float> {
+    static __device__ __forceinline__ void load(Frag<float>& f, const char* s, int row, int kbyte) {
+        f.lo = *reinterpret_cast<const f32x4*>(s + lds_byte(row, kbyte));
+        f.hi = *reinterpret_cast<const f32x4*>(s + lds_byte(row, kbyte + 16));
+    }
+};
+
+// Fused epilogue of one workgroup tile through buffer resources (out-of-range
+// elements are dropped by the hardware).  Inputs are loaded in batches of one
+// 32-row block strip (TN x 16 values per lane) before any store of that strip,
+// so the loads are not serialised behind possibly-aliasing stores.
+template <typename T, int EPI>
+struct Epilogue {
+    Rsrc c, c2, aux, bias;
+    __device__ __forceinline__ void init(const GemmArgs& a) {
+        const uint32_t esz = sizeof(T);
+        const uint32_t cbytes = (uint32_t)(((long)(a.M - 1) * a.ldc + a.N) *
+                                           (EPI == EPI_STORE || EPI == EPI_RELU_MASK ? esz : 4));
+        c = make_rsrc(a.C, cbytes);
+        if constexpr (EPI == EPI_RES_F32) {
+            c2 = make_rsrc(a.C2, a.C2 ? (uint32_t)(((long)(a.M - 1) * a.ldc2 + a.N) * esz) : 0u);
+            aux = make_rsrc(a.aux, (uint32_t)(((long)(a.M - 1) * a.ldaux + a.N) * 4));
+        }
+        if constexpr (EPI == EPI_RELU_MASK)
+            aux = make_rsrc(a.aux, (uint32_t)(((long)(a.M - 1) * a.ldaux + a.N) * esz));
+        bias = make_rsrc(a.bias, a.bias ? (uint32_t)a.N * 4 : 0u);
+    }
+    static __device__ __forceinline__ void store_elt(Rsrc r, uint32_t off, float v) {
+        if constexpr (sizeof(T) == 2)
+            __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, (bf16)v), r, off, 0, 0);
+        else
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), r, off, 0, 0);
+    }
+    static __device__ __forceinline__ float load_f32(Rsrc r, uint32_t off) {
+        return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+    }
+    static __device__ __forceinline__ float load_elt(Rsrc r, uint32_t off) {
+        if constexpr (sizeof(T) == 2)
+            return (float)__builtin_bit_cast(bf16, __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0));
+        else
+            return load_f32(r, off);
+    }
+
+    // acc[i][j][r] holds row row0 + 32 i + rowoff(r), column col0 + 32 j.
+    template <int TM, int TN>
+    __device__ __forceinline__ void run(const GemmArgs& a, const f32x16 (&acc)[TM][TN], int row0, int col0,
+                                        int lane) {
+        float bv[TN];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int col = col0 + j * 32;
+            bv[j] = (EPI == EPI_STORE || EPI == EPI_RES_F32) ? load_f32(bias, col < a.N ? col * 4 : OOB) : 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            float in[TN][16];
+            if constexpr (EPI == EPI_RES_F32 || EPI == EPI_RELU_MASK || EPI == EPI_ACC_F32) {
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int row = row0 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+                        const int col = col0 + j * 32;
+                        const bool ok = row < a.M && col < a.N;
+                        if constexpr (EPI == EPI_RES_F32)
+                            in[j][r] = load_f32(aux, ok ? (uint32_t)(((long)row * a.ldaux + col) * 4) : OOB);
+                        else if constexpr (EPI == EPI_RELU_MASK)
+                            in[j][r] = load_elt(aux, ok ? (uint32_t)(((long)row * a.ldaux + col) * sizeof(T)) : OOB);
+                        else
+                            in[j][r] = a.accumulate ? load_f32(c, ok ? (uint32_t)(((long)row * a.ldc + col) * 4) : OOB) : 0.f;
+                    }
+            }
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int row = row0 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+                    const int col = col0 + j * 32;
+                    const bool ok = row < a.M && col < a.N;
+                    const long e = (long)row * a.ldc + col;
+                    float v = acc[i][j][r];
+                    if constexpr (EPI == EPI_STORE) {
+                        v += bv[j];
+                        if (a.relu) v = fmaxf(v, 0.f);
+                        store_elt(c, ok ? (uint32_t)(e * sizeof(T)) : OOB, v);
+                    } else if constexpr (EPI == EPI_RES_F32) {
+                        v += in[j][r] + bv[j];
+                        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), c, ok ? (uint32_t)(e * 4) : OOB, 0, 0);
+                        if (a.C2) store_elt(c2, ok ? (uint32_t)(((long)row * a.ldc2 + col) * sizeof(T)) : OOB, v);
+                    } else if constexpr (EPI == EPI_F32) {
+                        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), c, ok ? (uint32_t)(e * 4) : OOB, 0, 0);
+                    } else if constexpr (EPI == EPI_RELU_MASK) {
+                        store_elt(c, ok ? (uint32_t)(e * sizeof(T)) : OOB, in[j][r] > 0.f ? v : 0.f);
+                    } else if constexpr (EPI == EPI_ACC_F32) {
+                        v += in[j][r];
+                        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), c, ok ? (uint32_t)(e * 4) : OOB, 0, 0);
+                    }
+                }
+        }
+    }
+};
+
+// Epilogue of the split-K reduction (global pointers, element granularity).
 template <typename T, int EPI>
 __device__ __forceinline__ void epilogue(const GemmArgs& a, int row, int col, float v) {
     const long i = (long)row * a.ldc + col;
@@ -160,22 +296,18 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int row, int col, fl
     } else if constexpr (EPI == EPI_RELU_MASK) {
         const float z = to_f32(reinterpret_cast<const T*>(a.aux)[(long)row * a.ldaux + col]);
         reinterpret_cast<T*>(a.C)[i] = to_elt<T>(z > 0.f ? v : 0.f);
-    } else if constexpr (EPI == EPI_ACC_F32) {
-        float* c = reinterpret_cast<float*>(a.C);
-        c[i] = a.accumulate ? c[i] + v : v;
     }
 }
 
-template <typename T, bool AK, bool BKM, int EPI>
+template <typename T, int BM, int BN, bool AK, bool BKM, int EPI, bool SPLIT>
 __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs args) {
-    constexpr int BM = 128, BN = 128, BK = GemmCfg<T>::BK;
+    constexpr int BK = GemmCfg<T>::BK, KS = BK / 16;
     constexpr int WM = 2, WN = 2;
     constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
     using LA = TileLoader<T, BM, BK, AK>;
     using LB = TileLoader<T, BN, BK, BKM>;
-    constexpr int LDK = LA::LDK;
-    __shared__ __attribute__((aligned(16))) T As[2][BM * LDK];
-    __shared__ __attribute__((aligned(16))) T Bs[2][BN * LDK];
+    __shared__ __attribute__((aligned(16))) char As[2][BM * 128];
+    __shared__ __attribute__((aligned(16))) char Bs[2][BN * 128];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave % WN;
@@ -183,16 +315,27 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs args) {
     // XCD-aware tile order: workgroup b runs on XCD b % 8; give XCD x the
     // contiguous logical range [x G/8, (x+1) G/8) (tiles walk down M inside a
     // column of N tiles, so neighbours share the B panel).
-    const int tiles_m = (args.M + BM - 1) / BM, tiles_n = (args.N + BN - 1) / BN;
-    const int G = tiles_m * tiles_n;
+    const int tiles_m = (args.M + BM - 1) / BM;
+    const int G = gridDim.x;
     int bid = blockIdx.x;
     const int G8 = G & ~7;
     if (bid < G8) bid = (bid & 7) * (G8 >> 3) + (bid >> 3);
     const int tm = bid % tiles_m, tn = bid / tiles_m;
     const int m0 = tm * BM, n0 = tn * BN;
 
-    const T* A = reinterpret_cast<const T*>(args.A);
-    const T* B = reinterpret_cast<const T*>(args.B);
+    const int nk_all = (args.K + BK - 1) / BK;
+    int kt0 = 0, kt1 = nk_all;
+    if constexpr (SPLIT) {
+        const int per = (nk_all + gridDim.y - 1) / gridDim.y;
+        kt0 = blockIdx.y * per;
+        kt1 = min(nk_all, kt0 + per);
+    }
+
+    constexpr int ESZ = sizeof(T);
+    const Rsrc A = make_rsrc(args.A, (uint32_t)((AK ? (long)(args.M - 1) * args.lda + args.K
+                                                    : (long)(args.K - 1) * args.lda + args.M) * ESZ));
+    const Rsrc B = make_rsrc(args.B, (uint32_t)((BKM ? (long)(args.N - 1) * args.ldb + args.K
+                                                     : (long)(args.K - 1) * args.ldb + args.N) * ESZ));
     LA la;
     LB lb;
     f32x16 acc[TM][TN];
@@ -203,90 +346,211 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs args) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    const int nk = (args.K + BK - 1) / BK;
-    la.load(A, args.lda, m0, args.M, 0, args.K, tid);
-    lb.load(B, args.ldb, n0, args.N, 0, args.K, tid);
-    la.store(As[0], tid);
-    lb.store(Bs[0], tid);
-    __syncthreads();
+    const int fr = lane & 31, fk = (lane >> 5) * 8 * ESZ;
+    const int arow = wm * (BM / WM) + fr, brow = wn * (BN / WN) + fr;
+    Frag<T> fa[2][TM], fb[2][TN];
+    auto load_frags = [&](int slot, const char* as, const char* bs, int s) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) FragRead<T>::load(fa[slot][i], as, arow + i * 32, s * 16 * ESZ + fk);
+#pragma unroll
+        for (int j = 0; j < TN; ++j) FragRead<T>::load(fb[slot][j], bs, brow + j * 32, s * 16 * ESZ + fk);
+    };
 
-    const int fr = lane & 31, fk = (lane >> 5) * 8;
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < nk) {
-            la.load(A, args.lda, m0, args.M, (kt + 1) * BK, args.K, tid);
-            lb.load(B, args.ldb, n0, args.N, (kt + 1) * BK, args.K, tid);
-        }
-        const T* as = As[buf];
-        const T* bs = Bs[buf];
-#pragma unroll
-        for (int s = 0; s < BK / 16; ++s) {
-            Frag<T> fa[TM], fb[TN];
-#pragma unroll
-            for (int i = 0; i < TM; ++i) fa[i].load(as + (wm * (BM / WM) + i * 32 + fr) * LDK + s * 16 + fk);
-#pragma unroll
-            for (int j = 0; j < TN; ++j) fb[j].load(bs + (wn * (BN / WN) + j * 32 + fr) * LDK + s * 16 + fk);
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j) mma(acc[i][j], fa[i], fb[j]);
-        }
-        if (kt + 1 < nk) {
-            la.store(As[buf ^ 1], tid);
-            lb.store(Bs[buf ^ 1], tid);
-        }
+    if (kt0 < kt1) {
+        la.load(A, args.lda, m0, args.M, kt0 * BK, args.K, tid);
+        lb.load(B, args.ldb, n0, args.N, kt0 * BK, args.K, tid);
+        la.store(As[0], tid);
+        lb.store(Bs[0], tid);
         __syncthreads();
+        load_frags(0, As[0], Bs[0], 0);
+        for (int kt = kt0; kt < kt1; ++kt) {
+            const int buf = (kt - kt0) & 1;
+            const bool next = kt + 1 < kt1;
+            if (next) {
+                la.load(A, args.lda, m0, args.M, (kt + 1) * BK, args.K, tid);
+                lb.load(B, args.ldb, n0, args.N, (kt + 1) * BK, args.K, tid);
+            }
+#pragma unroll
+            for (int s = 0; s < KS; ++s) {
+                const int cur = s & 1;
+                if (s + 1 < KS) {
+                    load_frags(cur ^ 1, As[buf], Bs[buf], s + 1);
+                } else if (next) {
+                    la.store(As[buf ^ 1], tid);
+                    lb.store(Bs[buf ^ 1], tid);
+                    __syncthreads();
+                    load_frags(cur ^ 1, As[buf ^ 1], Bs[buf ^ 1], 0);
+                }
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j) mma(acc[i][j], fa[cur][i], fb[cur][j]);
+            }
+        }
     }
 
     // 32x32 accumulator layout: lane l holds column (l % 32); register r holds
     // row 8 (r / 4) + 4 (l / 32) + (r % 4).
+    if constexpr (SPLIT) {
+        const Rsrc ws = make_rsrc(args.ws, (uint32_t)((long)gridDim.y * args.M * args.N * 4));
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+        for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int col = n0 + wn * (BN / WN) + j * 32 + (lane & 31);
-            if (col >= args.N) continue;
+            for (int j = 0; j < TN; ++j) {
+                const int col = n0 + wn * (BN / WN) + j * 32 + (lane & 31);
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int row = m0 + wm * (BM / WM) + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-                if (row < args.M) epilogue<T, EPI>(args, row, col, acc[i][j][r]);
+                for (int r = 0; r < 16; ++r) {
+                    const int row = m0 + wm * (BM / WM) + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+                    const bool ok = row < args.M && col < args.N;
+                    const uint32_t o = ok ? (uint32_t)((((long)blockIdx.y * args.M + row) * args.N + col) * 4) : OOB;
+                    // Read the accumulator element into a plain float first: a bit-cast
+                    // taken directly on the AGPR-held vector element was compiled into
+                    // stores that all read the block's first register.
+                    const float v = acc[i][j][r];
+                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), ws, o, 0, 0);
+                }
             }
-        }
+    } else {
+        Epilogue<T, EPI> ep;
+        ep.init(args);
+        ep.template run<TM, TN>(args, acc, m0 + wm * (BM / WM), n0 + wn * (BN / WN) + (lane & 31), lane);
+    }
 }
 
-template <typename T, bool AK, bool BKM>
-gp_status launch_epi(const GemmArgs& a, int epi, hipStream_t st) {
-    constexpr int BM = 128, BN = 128;
-    const int grid = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+// Sum the split-K partials in split order and apply the epilogue; 4 columns per thread.
+template <typename T, int EPI>
+__global__ void __launch_bounds__(256) splitk_reduce(GemmArgs args, int splits) {
+    const long nq = (long)args.M * (args.N / 4);
+    const long plane = (long)args.M * args.N;
+    for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < nq; i += (long)gridDim.x * 256) {
+        const int row = (int)(i / (args.N / 4)), col = (int)(i % (args.N / 4)) * 4;
+        const float* p = args.ws + (long)row * args.N + col;
+        f32x4 s = *reinterpret_cast<const f32x4*>(p);
+        for (int k = 1; k < splits; ++k) {
+            const f32x4 t = *reinterpret_cast<const f32x4*>(p + k * plane);
+            s += t;
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) epilogue<T, EPI>(args, row, col + j, s[j]);
+    }
+}
+
+enum TileCfg { T256x256 = 0, T256x128 = 1, T128x256 = 2, T128x128 = 3 };
+
+template <typename T, int BM, int BN, bool AK, bool BKM>
+gp_status launch_tile(const GemmArgs& a, int epi, int splits, hipStream_t st) {
+    const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+    if (splits > 1) {
+        dim3 grid(tiles, splits);
+        gemm_kernel<T, BM, BN, AK, BKM, EPI_F32, true><<<grid, 256, 0, st>>>(a);
+        GP_LAUNCH_CHECK();
+        const long nq = (long)a.M * (a.N / 4);
+        const int rg = (int)std::min<long>((nq + 255) / 256, 2048);
+        switch (epi) {
+        case EPI_STORE: splitk_reduce<T, EPI_STORE><<<rg, 256, 0, st>>>(a, splits); break;
+        case EPI_RES_F32: splitk_reduce<T, EPI_RES_F32><<<rg, 256, 0, st>>>(a, splits); break;
+        case EPI_F32: splitk_reduce<T, EPI_F32><<<rg, 256, 0, st>>>(a, splits); break;
+        case EPI_RELU_MASK: splitk_reduce<T, EPI_RELU_MASK><<<rg, 256, 0, st>>>(a, splits); break;
+        default: return set_error(GP_ERR_INVALID_ARG, "gemm: split-K epilogue");
+        }
+        GP_LAUNCH_CHECK();
+        return GP_OK;
+    }
     switch (epi) {
-    case EPI_STORE: gemm_kernel<T, AK, BKM, EPI_STORE><<<grid, 256, 0, st>>>(a); break;
-    case EPI_RES_F32: gemm_kernel<T, AK, BKM, EPI_RES_F32><<<grid, 256, 0, st>>>(a); break;
-    case EPI_F32: gemm_kernel<T, AK, BKM, EPI_F32><<<grid, 256, 0, st>>>(a); break;
-    case EPI_RELU_MASK: gemm_kernel<T, AK, BKM, EPI_RELU_MASK><<<grid, 256, 0, st>>>(a); break;
-    case EPI_ACC_F32: gemm_kernel<T, AK, BKM, EPI_ACC_F32><<<grid, 256, 0, st>>>(a); break;
+    case EPI_STORE: gemm_kernel<T, BM, BN, AK, BKM, EPI_STORE, false><<<tiles, 256, 0, st>>>(a); break;
+    case EPI_RES_F32: gemm_kernel<T, BM, BN, AK, BKM, EPI_RES_F32, false><<<tiles, 256, 0, st>>>(a); break;
+    case EPI_F32: gemm_kernel<T, BM, BN, AK, BKM, EPI_F32, false><<<tiles, 256, 0, st>>>(a); break;
+    case EPI_RELU_MASK: gemm_kernel<T, BM, BN, AK, BKM, EPI_RELU_MASK, false><<<tiles, 256, 0, st>>>(a); break;
+    case EPI_ACC_F32: gemm_kernel<T, BM, BN, AK, BKM, EPI_ACC_F32, false><<<tiles, 256, 0, st>>>(a); break;
     default: return set_error(GP_ERR_INVALID_ARG, "gemm: unknown epilogue");
     }
     GP_LAUNCH_CHECK();
     return GP_OK;
 }
 
+template <bool AK, bool BKM>
+gp_status launch_bf16(const GemmArgs& a, int epi, int cfg, int splits, hipStream_t st) {
+    switch (cfg) {
+    case T256x256: return launch_tile<bf16, 256, 256, AK, BKM>(a, epi, splits, st);
+    case T256x128: return launch_tile<bf16, 256, 128, AK, BKM>(a, epi, splits, st);
+    case T128x256: return launch_tile<bf16, 128, 256, AK, BKM>(a, epi, splits, st);
+    default: return launch_tile<bf16, 128, 128, AK, BKM>(a, epi, splits, st);
+    }
+}
+
+constexpr int NUM_CU = 256;
+
+// Pick the tile shape and split count.  Cost = full-machine rounds x per-tile
+// time, where a round holds NUM_CU x (workgroups resident per CU) tiles and
+// co-resident tiles share their CU; per-tile time is the tile's k-steps over
+// a measured relative efficiency; split-K adds its partial-tile traffic.
+void choose(const GemmArgs& a, int epi, int& cfg, int& splits) {
+    static const int BMs[4] = {256, 256, 128, 128}, BNs[4] = {256, 128, 256, 128};
+    static const int resident[4] = {1, 1, 1, 2};
+    static const double eff[4] = {0.95, 0.8, 0.8, 1.0};
+    double best = 1e300;
+    cfg = T128x128;
+    splits = 1;
+    const int nk = (a.K + 63) / 64;
+    for (int c = 0; c < 4; ++c) {
+        const long tiles = (long)((a.M + BMs[c] - 1) / BMs[c]) * ((a.N + BNs[c] - 1) / BNs[c]);
+        for (int s = 1; s <= 8; s *= 2) {
+            if (s > 1 && (epi == EPI_ACC_F32 || a.ws == nullptr || nk / s < 4 ||
+                          (long)s * a.M * a.N > a.ws_elems || a.N % 4))
+                continue;
+            const long wgs = tiles * s;
+            const long slots = (long)NUM_CU * resident[c];
+            const long rounds = (wgs + slots - 1) / slots;
+            const long per_cu = std::min<long>(resident[c], (wgs + NUM_CU - 1) / NUM_CU);
+            const double kt = (double)((nk + s - 1) / s);
+            // time in units of one 128x128x64 tile step of a CU running alone
+            // two co-resident tiles hide each other's latencies: 1.5x, not 2x, the time of one
+            double t = rounds * (per_cu == 2 ? 1.5 : 1.0) * (BMs[c] / 128.0) * (BNs[c] / 128.0) * kt / eff[c];
+            // split-K: partial-tile traffic (mostly cache-resident) and the reduce launch
+            if (s > 1) t += (double)a.M * a.N * 4.0 * (s + 1.0) / 2.0e7 + 8.0;
+            if (t < best * 0.999) {
+                best = t;
+                cfg = c;
+                splits = s;
+            }
+        }
+    }
+}
+
 template <typename T>
-gp_status gemm_t(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, hipStream_t st) {
+gp_status check_args(const GemmArgs& a, bool a_kmajor, bool b_kmajor) {
     constexpr int VEC = Vec16<T>::N;
     if (a.M <= 0 || a.N <= 0 || a.K <= 0) return set_error(GP_ERR_INVALID_ARG, "gemm: empty problem");
-    if (a.K % VEC || a.lda % VEC || a.ldb % VEC) return set_error(GP_ERR_INVALID_ARG, "gemm: K and leading dimensions must be multiples of 16 bytes");
-    if ((!a_kmajor && a.M % VEC) || (!b_kmajor && a.N % VEC)) return set_error(GP_ERR_INVALID_ARG, "gemm: m/n-contiguous operands need M, N multiples of 16 bytes");
+    if (a.K % VEC || a.lda % VEC || a.ldb % VEC)
+        return set_error(GP_ERR_INVALID_ARG, "gemm: K and leading dimensions must be multiples of 16 bytes");
+    if ((!a_kmajor && a.M % VEC) || (!b_kmajor && a.N % VEC))
+        return set_error(GP_ERR_INVALID_ARG, "gemm: m/n-contiguous operands need M, N multiples of 16 bytes");
     if (((uintptr_t)a.A | (uintptr_t)a.B) & 15) return set_error(GP_ERR_INVALID_ARG, "gemm: operands must be 16-byte aligned");
-    if (a_kmajor && b_kmajor) return launch_epi<T, true, true>(a, epi, st);
-    if (!a_kmajor && !b_kmajor) return launch_epi<T, false, false>(a, epi, st);
-    return set_error(GP_ERR_UNSUPPORTED, "gemm: mixed operand majorness not instantiated");
+    if (a_kmajor != b_kmajor) return set_error(GP_ERR_UNSUPPORTED, "gemm: mixed operand majorness not instantiated");
+    return GP_OK;
 }
 
 } // namespace
 
 gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dtype, hipStream_t st) {
-    if (dtype == GP_BF16) return gemm_t<bf16>(a, epi, a_kmajor, b_kmajor, st);
-    return gemm_t<float>(a, epi, a_kmajor, b_kmajor, st);
+    if (dtype == GP_BF16) {
+        gp_status s = check_args<bf16>(a, a_kmajor, b_kmajor);
+        if (s != GP_OK) return s;
+        int cfg, splits;
+        choose(a, epi, cfg, splits);
+        if (a.force_cfg >= 0 && a.force_cfg <= T128x128) {
+            cfg = a.force_cfg;
+            splits = a.force_splits > 0 ? a.force_splits : 1;
+            if (epi == EPI_ACC_F32 || a.ws == nullptr || (long)splits * a.M * a.N > a.ws_elems || a.N % 4)
+                splits = 1;
+        }
+        return a_kmajor ? launch_bf16<true, true>(a, epi, cfg, splits, st)
+                        : launch_bf16<false, false>(a, epi, cfg, splits, st);
+    }
+    gp_status s = check_args<float>(a, a_kmajor, b_kmajor);
+    if (s != GP_OK) return s;
+    return a_kmajor ? launch_tile<float, 128, 128, true, true>(a, epi, 1, st)
+                    : launch_tile<float, 128, 128, false, false>(a, epi, 1, st);
 }
 
 } // namespace gp

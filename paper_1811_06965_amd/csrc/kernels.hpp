@@ -27,6 +27,10 @@ struct GemmArgs {
     const void* aux = nullptr; long ldaux = 0;
     int relu = 0;
     int accumulate = 0;
+    float* ws = nullptr;   // split-K partials (fp32), ws_elems floats; nullptr disables split-K
+    long ws_elems = 0;
+    int force_cfg = -1;    // tile shape override (tests and tuning); -1 = heuristic
+    int force_splits = 0;
 };
 
 gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dtype, hipStream_t st);

@@ -19,6 +19,7 @@
 // Both run the same kernels with the same launch shapes, so the recomputed
 // activations equal the first pass bit for bit.
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <utility>
@@ -72,6 +73,8 @@ struct BwdWs {
     void *pe = nullptr, *qe = nullptr, *dz = nullptr, *dc = nullptr, *dqkv = nullptr, *dxq = nullptr, *dxkv = nullptr;
     double *loss_partial = nullptr, *loss_acc = nullptr;
     int* flag = nullptr;
+    float* splitk = nullptr;   // split-K partial tiles of the activation GEMMs
+    long splitk_elems = 0;
     // loss head
     float* sth = nullptr;
     void *h = nullptr, *z = nullptr;
@@ -97,6 +100,9 @@ struct gp_partition {
     std::vector<LayerWs> lw;
     BwdWs bw;
     size_t bytes_params = 0, bytes_grads = 0, bytes_stash = 0, bytes_ws = 0;
+    // GEMM tile-shape override (GP_GEMM_TILE = 0..3, GP_GEMM_SPLITS), read at
+    // configure; -1 lets the library choose per problem.
+    int gemm_tile = -1, gemm_splits = 0;
 
     void* W(size_t elt_off) const { return welt + elt_off * esz; }
     char* stash_x_mb(int m) const { return stash_x + (size_t)m * g.T() * d.D * esz; }
@@ -163,6 +169,8 @@ void plan_workspace(gp_partition* p, Arena& a) {
         if (pm > part) part = pm;
     }
     b.partial = a.take<float>(part);
+    b.splitk_elems = 8 * T * D;
+    b.splitk = a.take<float>((size_t)b.splitk_elems);
     size_t lp = (size_t)loss_blocks();
     if (g.loss == GP_LOSS_XENT_LS && (size_t)xent_partials(T) > lp) lp = xent_partials(T);
     b.loss_partial = a.take<double>(lp);
@@ -206,6 +214,10 @@ gp_status linear_fwd(const Ctx& c, const Linear& L, const void* A, long M, void*
     g.aux = res;
     g.ldaux = ldc;
     g.relu = relu;
+    g.ws = c.p->bw.splitk;
+    g.ws_elems = c.p->bw.splitk_elems;
+    g.force_cfg = c.p->gemm_tile;
+    g.force_splits = c.p->gemm_splits;
     return gemm(g, epi, true, true, c.dt, c.st);
 }
 
@@ -225,6 +237,10 @@ gp_status linear_dx(const Ctx& c, const Linear& L, const void* dY, long M, void*
     g.aux = aux;
     g.ldaux = L.in;
     g.accumulate = accumulate;
+    g.ws = c.p->bw.splitk;
+    g.ws_elems = c.p->bw.splitk_elems;
+    g.force_cfg = c.p->gemm_tile;
+    g.force_splits = c.p->gemm_splits;
     return gemm(g, epi, true, true, c.dt, c.st);
 }
 
@@ -241,6 +257,7 @@ gp_status linear_dw(const Ctx& c, const Linear& L, const void* X, const void* dY
     g.C = c.p->grads + L.w;
     g.ldc = L.out;
     g.accumulate = accumulate;
+    g.force_cfg = c.p->gemm_tile;
     GP_TRY(gemm(g, EPI_ACC_F32, false, false, c.dt, c.st));
     return bias_grad(c.dt, dY, rows, L.out, L.out, c.p->bw.partial, c.p->grads + L.b, accumulate, c.st);
 }
@@ -514,6 +531,8 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
     g.eps = cfg->ln_eps;
     g.check_finite = cfg->check_finite;
     p->esz = g.dtype == GP_BF16 ? 2 : 4;
+    if (const char* e = std::getenv("GP_GEMM_TILE")) p->gemm_tile = std::atoi(e);
+    if (const char* e = std::getenv("GP_GEMM_SPLITS")) p->gemm_splits = std::atoi(e);
     p->plan = plan_params(p->d, g);
     Arena measure;
     plan_workspace(p, measure);

@@ -230,3 +230,14 @@ def test_call_order_is_enforced():
             gp.gp_backward_microbatch_remat(part.h, m, ts[m].data_ptr(), None, None, st)
         gp.gp_accumulate_and_step(part.h, 0.0, False, st)
         torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("tile,splits", [(0, 1), (1, 1), (2, 1), (3, 1), (0, 4), (3, 2)],
+                         ids=["256x256", "256x128", "128x256", "128x128", "256x256_split4", "128x128_split2"])
+def test_bf16_every_gemm_tile_shape(tile, splits, monkeypatch):
+    """Every MFMA tile shape and the split-K path, forced for all GEMMs, on the
+    ragged-row bf16 partition (tile edges in M, N and K)."""
+    monkeypatch.setenv("GP_GEMM_TILE", str(tile))
+    monkeypatch.setenv("GP_GEMM_SPLITS", str(splits))
+    case, ref, res = _run(RAGGED_BF16, 3, perturb=False)
+    _check(RAGGED_BF16, ref, res, 2e-2, "cos", 0.999)

@@ -138,6 +138,19 @@ struct TileLoader {
         }
     }
 
+    // m-major only: add this thread's loaded values over its KB k-rows into
+    // cs[i] for its VEC rows (operand rows = output columns of a dW GEMM).
+    __device__ __forceinline__ void colsum(float (&cs)[VEC]) const {
+        if constexpr (!KMAJOR) {
+#pragma unroll
+            for (int p = 0; p < MPASS; ++p)
+#pragma unroll
+                for (int q = 0; q < KB; ++q)
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i) cs[i] += (float)r[p * KB + q][i];
+        }
+    }
+
     __device__ __forceinline__ void store(char* __restrict__ s, int tid) const {
         if constexpr (KMAJOR) {
             const int rr = tid / TPR, kk = (tid % TPR) * VEC;
@@ -346,6 +359,14 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs args) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+    // Fused bias gradient of a weight-gradient GEMM: the workgroups of the
+    // first M tile see every k-row of B (= dY) for their columns.
+    constexpr bool COLSUM = !BKM && EPI == EPI_ACC_F32;
+    const bool do_colsum = COLSUM && args.colsum != nullptr && tm == 0;
+    float cs[LB::VEC];
+#pragma unroll
+    for (int i = 0; i < LB::VEC; ++i) cs[i] = 0.f;
+
     const int fr = lane & 31, fk = (lane >> 5) * 8 * ESZ;
     const int arow = wm * (BM / WM) + fr, brow = wn * (BN / WN) + fr;
     Frag<T> fa[2][TM], fb[2][TN];
@@ -361,6 +382,7 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs args) {
         lb.load(B, args.ldb, n0, args.N, kt0 * BK, args.K, tid);
         la.store(As[0], tid);
         lb.store(Bs[0], tid);
+        if (do_colsum) lb.colsum(cs);
         __syncthreads();
         load_frags(0, As[0], Bs[0], 0);
         for (int kt = kt0; kt < kt1; ++kt) {
@@ -378,6 +400,7 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs args) {
                 } else if (next) {
                     la.store(As[buf ^ 1], tid);
                     lb.store(Bs[buf ^ 1], tid);
+                    if (do_colsum) lb.colsum(cs);
                     __syncthreads();
                     load_frags(cur ^ 1, As[buf ^ 1], Bs[buf ^ 1], 0);
                 }
@@ -391,6 +414,25 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs args) {
 
     // 32x32 accumulator layout: lane l holds column (l % 32); register r holds
     // row 8 (r / 4) + 4 (l / 32) + (r % 4).
+    if constexpr (COLSUM) {
+        if (do_colsum) {
+            // threads tid = mb + MBLK j (j = 0, 1, ...) hold partial sums of the
+            // same VEC columns; add them in increasing tid order.
+            constexpr int MBLK = LB::MBLK, VEC = LB::VEC;
+            float* red = reinterpret_cast<float*>(&As[0][0]);
+            __syncthreads();
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) red[tid * VEC + i] = cs[i];
+            __syncthreads();
+            if (tid < BN) {
+                const int mb = tid / VEC, i = tid % VEC;
+                float sum = 0.f;
+                for (int t = mb; t < 256; t += MBLK) sum += red[t * VEC + i];
+                const int col = n0 + tid;
+                if (col < args.N) args.colsum[col] = args.accumulate ? args.colsum[col] + sum : sum;
+            }
+        }
+    }
     if constexpr (SPLIT) {
         const Rsrc ws = make_rsrc(args.ws, (uint32_t)((long)gridDim.y * args.M * args.N * 4));
 #pragma unroll

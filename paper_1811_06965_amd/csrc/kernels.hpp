@@ -31,6 +31,7 @@ struct GemmArgs {
     long ws_elems = 0;
     int force_cfg = -1;    // tile shape override (tests and tuning); -1 = heuristic
     int force_splits = 0;
+    float* colsum = nullptr; // EPI_ACC_F32 with n-contiguous B: also colsum[n] (+)= sum_k B(n, k)
 };
 
 gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dtype, hipStream_t st);

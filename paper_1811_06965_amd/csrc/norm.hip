@@ -119,13 +119,135 @@ __global__ void __launch_bounds__(256) ln_bwd_kernel(const float* __restrict__ d
     }
 }
 
-__global__ void colsum_kernel(const float* __restrict__ partial, int nblk, int width, float* __restrict__ out,
-                              int accumulate) {
-    const int c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= width) return;
+// 16 waves per block, 64 columns per block: wave w adds rows w, w + 16, ...
+// (lanes = columns, coalesced), then the 16 wave sums are added in order.
+__global__ void __launch_bounds__(1024) colsum_kernel(const float* __restrict__ partial, int nblk, int width,
+                                                      float* __restrict__ out, int accumulate) {
+    __shared__ float red[16][64];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int c = blockIdx.x * 64 + lane;
     float s = 0.f;
-    for (int b = 0; b < nblk; ++b) s += partial[(long)b * width + c];
-    out[c] = accumulate ? out[c] + s : s;
+    if (c < width)
+        for (int b = w; b < nblk; b += 16) s += partial[(long)b * width + c];
+    red[w][lane] = s;
+    __syncthreads();
+    if (w == 0 && c < width) {
+        float t = 0.f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) t += red[i][lane];
+        out[c] = accumulate ? out[c] + t : t;
+    }
+}
+
+// ---- 16-byte vectorised LayerNorm for D a multiple of 256 (lane l owns
+// features 4 (l + 64 c) .. +3, c < C4 = D / 256).
+template <typename T> struct Out4;
+template <> struct Out4<float> {
+    static __device__ __forceinline__ void store(float* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
+};
+template <> struct Out4<bf16> {
+    static __device__ __forceinline__ void store(bf16* p, f32x4 v) {
+        bf16x4 b = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
+        *reinterpret_cast<bf16x4*>(p) = b;
+    }
+};
+
+__device__ __forceinline__ float hsum(f32x4 v) { return (v[0] + v[1]) + (v[2] + v[3]); }
+
+template <typename T, int C4>
+__global__ void __launch_bounds__(256) ln_fwd_v4(const float* __restrict__ x, long rows, int D,
+                                                 const float* __restrict__ gamma, const float* __restrict__ beta,
+                                                 float eps, T* __restrict__ out, float* __restrict__ stats) {
+    const int lane = threadIdx.x & 63;
+    const long row = (long)blockIdx.x * LN_WAVES + (threadIdx.x >> 6);
+    if (row >= rows) return;
+    const f32x4* xr = reinterpret_cast<const f32x4*>(x + row * D);
+    f32x4 v[C4];
+    float s = 0.f;
+#pragma unroll
+    for (int c = 0; c < C4; ++c) {
+        v[c] = xr[lane + 64 * c];
+        s += hsum(v[c]);
+    }
+    const float mu = wave_sum(s) / D;
+    float q = 0.f;
+#pragma unroll
+    for (int c = 0; c < C4; ++c) {
+        const f32x4 t = v[c] - mu;
+        q += hsum(t * t);
+    }
+    const float rstd = 1.f / sqrtf(wave_sum(q) / D + eps);
+    const f32x4* g4 = reinterpret_cast<const f32x4*>(gamma);
+    const f32x4* b4 = reinterpret_cast<const f32x4*>(beta);
+    T* orow = out + row * D;
+#pragma unroll
+    for (int c = 0; c < C4; ++c) {
+        const int i = lane + 64 * c;
+        Out4<T>::store(orow + 4 * i, g4[i] * ((v[c] - mu) * rstd) + b4[i]);
+    }
+    if (stats && lane == 0) {
+        stats[2 * row] = mu;
+        stats[2 * row + 1] = rstd;
+    }
+}
+
+template <typename T, int C4>
+__global__ void __launch_bounds__(256) ln_bwd_v4(const float* __restrict__ dn, const float* __restrict__ x,
+                                                 const float* __restrict__ stats, const float* __restrict__ gamma,
+                                                 long rows, int D, int rpw, const float* __restrict__ dres,
+                                                 float* __restrict__ dx32, T* __restrict__ dxe,
+                                                 float* __restrict__ partial) {
+    __shared__ f32x4 red[LN_WAVES][2][C4 * 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const f32x4* g4 = reinterpret_cast<const f32x4*>(gamma);
+    f32x4 pg[C4], pb[C4];
+#pragma unroll
+    for (int c = 0; c < C4; ++c) pg[c] = pb[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const long row0 = ((long)blockIdx.x * LN_WAVES + wave) * rpw;
+    for (int rr = 0; rr < rpw; ++rr) {
+        const long row = row0 + rr;
+        if (row >= rows) break;
+        const float mu = stats[2 * row], rstd = stats[2 * row + 1];
+        const f32x4* dn4 = reinterpret_cast<const f32x4*>(dn + row * D);
+        const f32x4* x4 = reinterpret_cast<const f32x4*>(x + row * D);
+        f32x4 g[C4], xh[C4];
+        float sg = 0.f, sgx = 0.f;
+#pragma unroll
+        for (int c = 0; c < C4; ++c) {
+            const int i = lane + 64 * c;
+            const f32x4 dv = dn4[i];
+            xh[c] = (x4[i] - mu) * rstd;
+            g[c] = dv * g4[i];
+            pg[c] += dv * xh[c];
+            pb[c] += dv;
+            sg += hsum(g[c]);
+            sgx += hsum(g[c] * xh[c]);
+        }
+        sg = wave_sum(sg) / D;
+        sgx = wave_sum(sgx) / D;
+#pragma unroll
+        for (int c = 0; c < C4; ++c) {
+            const int i = lane + 64 * c;
+            f32x4 r = rstd * (g[c] - sg - xh[c] * sgx);
+            if (dres) r += reinterpret_cast<const f32x4*>(dres + row * D)[i];
+            if (dx32) reinterpret_cast<f32x4*>(dx32 + row * D)[i] = r;
+            if (dxe) Out4<T>::store(dxe + row * D + 4 * i, r);
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < C4; ++c) {
+        red[wave][0][lane + c * 64] = pg[c];
+        red[wave][1][lane + c * 64] = pb[c];
+    }
+    __syncthreads();
+    const int n4 = D / 4;
+    for (int i = threadIdx.x; i < 2 * n4; i += 256) {
+        const int which = i / n4, d = i % n4;
+        f32x4 t = red[0][which][d];
+#pragma unroll
+        for (int w = 1; w < LN_WAVES; ++w) t += red[w][which][d];
+        reinterpret_cast<f32x4*>(partial + (long)blockIdx.x * 2 * D + which * D)[d] = t;
+    }
 }
 
 constexpr int BIAS_BLOCKS = 64;
@@ -148,6 +270,20 @@ gp_status ln_fwd_t(const float* x, long rows, int D, const float* g, const float
                    float* stats, hipStream_t st) {
     const int grid = (int)((rows + LN_WAVES - 1) / LN_WAVES);
     T* o = reinterpret_cast<T*>(out);
+    if (D % 256 == 0 && D <= 2048) {
+        switch (D / 256) {
+        case 1: ln_fwd_v4<T, 1><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats); break;
+        case 2: ln_fwd_v4<T, 2><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats); break;
+        case 3: ln_fwd_v4<T, 3><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats); break;
+        case 4: ln_fwd_v4<T, 4><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats); break;
+        case 5: ln_fwd_v4<T, 5><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats); break;
+        case 6: ln_fwd_v4<T, 6><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats); break;
+        case 7: ln_fwd_v4<T, 7><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats); break;
+        default: ln_fwd_v4<T, 8><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats); break;
+        }
+        GP_LAUNCH_CHECK();
+        return GP_OK;
+    }
     const int C = (D + 63) / 64;
     if (C <= 1) ln_fwd_kernel<T, 1><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats);
     else if (C <= 2) ln_fwd_kernel<T, 2><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats);
@@ -167,6 +303,22 @@ gp_status ln_bwd_t(const float* dn, const float* x, const float* stats, const fl
     const int grid = (int)((rows + (long)LN_WAVES * rpw - 1) / ((long)LN_WAVES * rpw));
     *nblk = grid;
     T* e = reinterpret_cast<T*>(dxe);
+    if (D % 256 == 0 && D <= 2048) {
+#define GP_LNV(CC) ln_bwd_v4<T, CC><<<grid, 256, 0, st>>>(dn, x, stats, gamma, rows, D, rpw, dres, dx32, e, partial)
+        switch (D / 256) {
+        case 1: GP_LNV(1); break;
+        case 2: GP_LNV(2); break;
+        case 3: GP_LNV(3); break;
+        case 4: GP_LNV(4); break;
+        case 5: GP_LNV(5); break;
+        case 6: GP_LNV(6); break;
+        case 7: GP_LNV(7); break;
+        default: GP_LNV(8); break;
+        }
+#undef GP_LNV
+        GP_LAUNCH_CHECK();
+        return GP_OK;
+    }
     const int C = (D + 63) / 64;
 #define GP_LNB(CC) ln_bwd_kernel<T, CC><<<grid, 256, 0, st>>>(dn, x, stats, gamma, rows, D, rpw, dres, dx32, e, partial)
     if (C <= 1) GP_LNB(1);
@@ -204,7 +356,7 @@ gp_status layernorm_bwd(int dtype, const float* dn, const float* x, const float*
 }
 
 gp_status colsum_finalize(const float* partial, int nblk, int width, float* out, int accumulate, hipStream_t st) {
-    colsum_kernel<<<(width + 255) / 256, 256, 0, st>>>(partial, nblk, width, out, accumulate);
+    colsum_kernel<<<(width + 63) / 64, 1024, 0, st>>>(partial, nblk, width, out, accumulate);
     GP_LAUNCH_CHECK();
     return GP_OK;
 }

@@ -244,7 +244,7 @@ gp_status linear_dx(const Ctx& c, const Linear& L, const void* dY, long M, void*
     return gemm(g, epi, true, true, c.dt, c.st);
 }
 
-// G_W (+)= X^T dY and G_b (+)= sum_rows dY.  X [rows, in], dY [rows, out].
+// G_W (+)= X^T dY and G_b (+)= sum_rows dY (one kernel).  X [rows, in], dY [rows, out].
 gp_status linear_dw(const Ctx& c, const Linear& L, const void* X, const void* dY, long rows, int accumulate) {
     GemmArgs g;
     g.M = L.in;
@@ -258,8 +258,8 @@ gp_status linear_dw(const Ctx& c, const Linear& L, const void* X, const void* dY
     g.ldc = L.out;
     g.accumulate = accumulate;
     g.force_cfg = c.p->gemm_tile;
-    GP_TRY(gemm(g, EPI_ACC_F32, false, false, c.dt, c.st));
-    return bias_grad(c.dt, dY, rows, L.out, L.out, c.p->bw.partial, c.p->grads + L.b, accumulate, c.st);
+    g.colsum = c.p->grads + L.b;  // bias gradient fused into the GEMM
+    return gemm(g, EPI_ACC_F32, false, false, c.dt, c.st);
 }
 
 gp_status norm_bwd(const Ctx& c, const Norm& N, const float* dn, const float* x, const float* stats, long rows,

@@ -77,6 +77,9 @@ RAGGED_BF16 = synth.PartitionConfig("ragged_bf16", layers=2, d_model=512, d_ff=2
                                     batch=6, micro=2, dtype="bf16", loss="none")
 RAGGED_F32 = synth.PartitionConfig("ragged_f32", layers=2, d_model=96, d_ff=160, heads=3, seq=40,
                                    batch=6, micro=3, dtype="f32", loss="none")
+# d_model a multiple of 256: the 16-byte vectorised LayerNorm path in fp32
+WIDE_F32 = synth.PartitionConfig("wide_f32", layers=2, d_model=256, d_ff=512, heads=4, seq=64,
+                                 batch=4, micro=2, dtype="f32", loss="mse")
 DEC_F32 = synth.PartitionConfig("dec_f32", layers=2, d_model=32, d_ff=64, heads=2, seq=8, batch=4, micro=2,
                                 dtype="f32", kind="decoder", loss="xent_ls", vocab=40, label_smoothing=0.1,
                                 mem_seq=6)
@@ -92,7 +95,7 @@ def test_bf16_matches_oracle(cfg, perturb):
     _check(cfg, ref, res, 2e-2, "cos", 0.999)
 
 
-@pytest.mark.parametrize("cfg", [RAGGED_F32, DEC_F32, TINY.with_(name="tiny_boundary", loss="none")],
+@pytest.mark.parametrize("cfg", [RAGGED_F32, WIDE_F32, DEC_F32, TINY.with_(name="tiny_boundary", loss="none")],
                          ids=lambda c: c.name)
 def test_fp32_matches_oracle(cfg):
     case, ref, res = _run(cfg, 4)

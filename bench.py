@@ -8,10 +8,13 @@ gradients, Xavier-uniform weights (synthetic data).
 
 One step = M x gp_forward_microbatch + M x gp_backward_microbatch_remat +
 gp_accumulate_and_step (GPipe, Sections 2.2-2.3), all enqueued on one stream.
-W untimed warm-up steps, then K steps timed between two synchronisations.
-Prints one JSON line.
+W untimed warm-up steps, one untimed census step that times every launch role
+to find the dominant one, then K steps timed between two synchronisations
+with only the dominant role's launches bracketed by HIP events (on the launch
+stream) for the roofline figure.  Prints one JSON line.
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -21,9 +24,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-METRIC = "train tokens/s, one partition fwd+remat-bwd over M micro-batches; MFMA %"
+METRIC = "train tokens/s, one partition fwd+remat-bwd over M micro-batches"
 PEAK_BF16 = 2.5e15  # MI355X dense bf16 MFMA, FLOP/s
+PEAK_FP32 = 157.3e12  # MI355X fp32 vector, FLOP/s
 PEAK_HBM = 8.0e12   # MI355X HBM3E, B/s
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
 def parse():
@@ -35,33 +40,267 @@ def parse():
     ap.add_argument("--config", default="enc1024")
     ap.add_argument("--sweep", action="store_true", help="also time M in {4, 8, 16, 32}")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-layers", type=int, default=2, help="layers in the oracle's timed sample")
+    ap.add_argument("--cpu-layers", type=int, default=16, help="layers in the oracle's timed sample")
+    ap.add_argument("--role", default=None, help="time this launch role instead of the dominant one")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain device copy of known size (calibrates the PMC byte counters)")
+    ap.add_argument("--traffic-summary", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CAL_FETCH_DIR", "CAL_WRITE_DIR"),
+                    help="summarise rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs of `--role R` (with "
+                         "GP_TIMER_MARKERS=1) and of --copy-calibration into the stored traffic figures")
+    ap.add_argument("--kernel-summary", metavar="DIR",
+                    help="print a markdown summary of a rocprofv3 --kernel-trace database under DIR "
+                         "(per-kernel totals, and per-role launch durations when GP_TIMER_MARKERS=1 was set)")
+    ap.add_argument("--command", default="", help="the profiled command, quoted in --kernel-summary output")
     return ap.parse_args()
 
 
-def time_steps(part, inp, steps, warmup):
+def _short(name):
+    import re
+    import shutil
+    import subprocess
+    if name.startswith("_Z") and shutil.which("c++filt"):
+        # GNU c++filt does not know the bf16 builtin type code; spell it as a vendor type
+        out = subprocess.run(["c++filt", name.replace("DF16b", "u6__bf16")], capture_output=True, text=True)
+        name = out.stdout.strip() or name
+    name = re.sub(r"\(anonymous namespace\)::|gp::|void ", "", name)
+    return re.sub(r"\(gp::(GemmArgs|AttnArgs)\)|\(gp::GemmArgs, int\)", "", name)[:110]
+
+
+def kernel_summary(d, command, top=25):
+    """Markdown summary of a rocprofv3 kernel-trace database."""
+    import glob
+    import sqlite3
+    from paper_1811_06965_amd import gp
+    db = sqlite3.connect(glob.glob(os.path.join(d, "**", "*results.db"), recursive=True)[0])
+    rows = db.execute("select name, grid_x, grid_y, workgroup_x, start, end from kernels order by start").fetchall()
+    total = sum(r[5] - r[4] for r in rows if "role_marker" not in r[0])
+    print("# Kernel summary\n")
+    print(f"Command: `{command}`\n")
+    print(f"{len(rows)} dispatches, {total / 1e6:.2f} ms of kernel time (markers excluded).\n")
+    agg = {}
+    for name, gx, gy, wx, t0, t1 in rows:
+        if "role_marker" in name:
+            continue
+        k = (_short(name), gx // max(wx, 1), gy)
+        c, s = agg.get(k, (0, 0))
+        agg[k] = (c + 1, s + t1 - t0)
+    print("| kernel | grid | calls | mean us | % of kernel time |\n|---|---|---|---|---|")
+    for (n, gx, gy), (c, s) in sorted(agg.items(), key=lambda kv: -kv[1][1])[:top]:
+        print(f"| `{n}` | ({gx},{gy}) | {c} | {s / c / 1e3:.1f} | {100 * s / total:.1f} |")
+    # launches between role markers
+    spans, cur = {}, None
+    for name, gx, gy, wx, t0, t1 in rows:
+        if "role_marker" in name:
+            role, edge = gx // max(wx, 1), gy - 1
+            if edge == 0:
+                cur = (role, [])
+            elif cur is not None:
+                spans.setdefault(cur[0], []).append(cur[1])
+                cur = None
+        elif cur is not None:
+            cur[1].append((_short(name), t0, t1))
+    if spans:
+        print("\n## Launch roles (kernels between role markers)\n")
+        print("| role | launches | mean kernel us per launch | mean first-start to last-end us | kernels |\n|---|---|---|---|---|")
+        for role, ls in sorted(spans.items(), key=lambda kv: -sum(t1 - t0 for l in kv[1] for _, t0, t1 in l)):
+            ls = [l for l in ls if l]
+            if not ls:
+                continue
+            busy = sum(t1 - t0 for l in ls for _, t0, t1 in l) / len(ls) / 1e3
+            span = sum(l[-1][2] - l[0][1] for l in ls) / len(ls) / 1e3
+            names = sorted({n for l in ls for n, _, _ in l})
+            print(f"| {gp.KERNEL_ROLES[role]} | {len(ls)} | {busy:.1f} | {span:.1f} | " +
+                  "<br>".join(f"`{n}`" for n in names) + " |")
+
+
+COPY_BYTES = 1 << 30
+
+
+def copy_calibration():
+    """A plain copy of known size: reads and writes COPY_BYTES each, three times."""
+    import torch
+    a = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        torch.neg(a, out=b)
+    torch.cuda.synchronize()
+    print(f"[bench] copy calibration: 3 x neg over {COPY_BYTES} bytes", file=sys.stderr)
+
+
+def _pmc_rows(d):
+    import csv
+    import glob
+    rows = []
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(f) as fh:
+            rows += list(csv.DictReader(fh))
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    return rows
+
+
+def _per_dispatch(rows, counter):
+    """[(dispatch id, kernel name, counter value)] for one counter (summed over
+    its instances)."""
+    acc = {}
+    for r in rows:
+        if r["Counter_Name"] != counter:
+            continue
+        k = int(r["Dispatch_Id"])
+        name, v = acc.get(k, (r["Kernel_Name"], 0.0))
+        acc[k] = (name, v + float(r["Counter_Value"]))
+    return [(k, n, v) for k, (n, v) in sorted(acc.items())]
+
+
+def _between_markers(disp):
+    """Counter sums of the launches between role_marker pairs."""
+    out, cur = [], None
+    for _, name, v in disp:
+        if "role_marker" in name:
+            if cur is None:
+                cur = [0.0, []]
+            else:
+                out.append(cur)
+                cur = None
+        elif cur is not None:
+            cur[0] += v
+            cur[1].append(name)
+    return out
+
+
+def traffic_summary(fetch_dir, write_dir, cal_fetch_dir, cal_write_dir, role, workload):
+    """FETCH_SIZE and WRITE_SIZE are in KiB per dispatch; each is scaled by
+    the known bytes of the copy kernel over what the counter read for it."""
+    cal = {}
+    for ctr, d in (("FETCH_SIZE", cal_fetch_dir), ("WRITE_SIZE", cal_write_dir)):
+        vals = [v for _, n, v in _per_dispatch(_pmc_rows(d), ctr) if "neg" in n or "elementwise" in n]
+        big = [v for v in vals if v * 1024 > COPY_BYTES / 2]
+        cal[ctr] = COPY_BYTES / (sorted(big)[len(big) // 2] * 1024)
+    res = {}
+    for ctr, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        launches = _between_markers(_per_dispatch(_pmc_rows(d), ctr))
+        kib = sorted(l[0] for l in launches)
+        res[ctr] = {"launches": len(kib), "median_kib": kib[len(kib) // 2], "kernels": sorted({k for l in launches for k in l[1]})}
+    fetch = res["FETCH_SIZE"]["median_kib"] * 1024 * cal["FETCH_SIZE"]
+    write = res["WRITE_SIZE"]["median_kib"] * 1024 * cal["WRITE_SIZE"]
+    entry = {"bytes_per_launch": fetch + write, "fetch_bytes_per_launch": fetch, "write_bytes_per_launch": write,
+             "fetch_scale": cal["FETCH_SIZE"], "write_scale": cal["WRITE_SIZE"],
+             "launches": res["FETCH_SIZE"]["launches"], "kernels": res["FETCH_SIZE"]["kernels"]}
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        t = {}
+    if t.get("source_sha256") != source_digest() or t.get("workload") != workload:
+        t = {"source_sha256": source_digest(), "workload": workload, "roles": {}}
+    t["roles"][role] = entry
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(t, f, indent=1)
+    print(json.dumps({role: entry}, indent=1))
+
+
+def run_steps(part, inp, n, dx):
+    for _ in range(n):
+        part.step(inp["x"], inp["mem"], inp["dy"], lr=0.0, want_y=False, want_dx=True, want_loss=False, dx=dx)
+
+
+def census(part, inp, dx):
+    """One untimed step with every launch role timed; roles by total time."""
+    import torch
+    from paper_1811_06965_amd import gp
+    part.timer_reset()
+    part.timer_select("all")
+    run_steps(part, inp, 1, dx)
+    torch.cuda.synchronize()
+    part.timer_select(None)
+    roles = {}
+    for name in gp.KERNEL_ROLES[1:]:
+        r = part.timer_read(name)
+        if r["launches"]:
+            roles[name] = r
+    part.timer_reset()
+    return dict(sorted(roles.items(), key=lambda kv: -kv[1]["ms"]))
+
+
+def time_steps(part, inp, steps, warmup, role=None):
     import torch
     st = torch.cuda.current_stream()
-    for _ in range(warmup):
-        part.step(inp["x"], inp["mem"], inp["dy"], lr=0.0, want_y=False, want_dx=True, want_loss=False)
-    torch.cuda.synchronize()
-    y = None
     dx = torch.empty_like(inp["x"])
+    run_steps(part, inp, warmup, dx)
+    torch.cuda.synchronize()
+    roles = census(part, inp, dx) if role is None else None
+    if role is None:
+        role = next(iter(roles))
+    part.timer_reset()
+    part.timer_select(role)
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
     t0.record(st)
-    for _ in range(steps):
-        part.step(inp["x"], inp["mem"], inp["dy"], lr=0.0, want_y=False, want_dx=True, want_loss=False, dx=dx)
+    run_steps(part, inp, steps, dx)
     t1.record(st)
     torch.cuda.synchronize()
-    return t0.elapsed_time(t1) / steps
+    part.timer_select(None)
+    timed = part.timer_read(role)
+    part.timer_reset()
+    return t0.elapsed_time(t1) / steps, role, timed, roles
+
+
+def source_digest():
+    """SHA-256 over the HIP sources: a stored traffic figure is only valid for
+    the kernels it was measured on."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_1811_06965_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".hpp")):
+            with open(os.path.join(csrc, f), "rb") as fh:
+                h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def stored_traffic(role, workload):
+    """HBM bytes per launch of `role` from the PMC runs stored with the
+    profiles (FETCH_SIZE + WRITE_SIZE, calibrated), if they were taken on the
+    current kernels and workload; else None."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    e = t.get("roles", {}).get(role)
+    if not e or t.get("source_sha256") != source_digest() or t.get("workload") != workload:
+        return None
+    return e["bytes_per_launch"]
+
+
+def roofline(role, timed, workload):
+    """Roofline figure of the dominant launch role: algorithmic work per launch
+    over the mean event-to-event launch duration."""
+    n = max(timed["launches"], 1)
+    dur = timed["ms"] * 1e-3 / n
+    if timed["flops"] > 0:
+        achieved, peak, unit, bound = timed["flops"] / n / dur / 1e12, PEAK_BF16 / 1e12, "TFLOP/s", "mfma"
+    else:
+        achieved, peak, unit, bound = timed["bytes"] / n / dur / 1e9, PEAK_HBM / 1e9, "GB/s", "hbm"
+    return {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
+            "traffic": stored_traffic(role, workload), "role": role, "launches_timed": timed["launches"],
+            "mean_launch_us": dur * 1e6, "algorithmic_flops_per_launch": timed["flops"] / n,
+            "algorithmic_bytes_per_launch": timed["bytes"] / n}
+
+
+def blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        n = [i["num_threads"] for i in threadpool_info() if i.get("user_api") == "blas"]
+        return max(n) if n else 1
+    except Exception:
+        return len(os.sched_getaffinity(0))
 
 
 def cpu_baseline(cfg, layers):
     """The fp64 oracle on a bounded sample of the workload: `layers` of the 16
     layers, one micro-batch of the timed M (all three passes: forward,
     re-materialised forward, backward), scaled to whole-partition tokens/s."""
-    import numpy as np
     import synth
     from oracle import gpipe
     n = cfg.batch // cfg.micro
@@ -71,7 +310,7 @@ def cpu_baseline(cfg, layers):
     gpipe.gpipe_step(sample, case, 1)
     dt = time.perf_counter() - t
     tok_s = n * cfg.seq / (dt * cfg.layers / layers)
-    return {"value": tok_s, "unit": "tokens/s", "cores": len(os.sched_getaffinity(0)), "kind": "oracle",
+    return {"value": tok_s, "unit": "tokens/s", "cores": blas_threads(), "kind": "oracle",
             "sample": f"{layers} of {cfg.layers} layers, one micro-batch of {n} sequences x {cfg.seq} tokens, "
                       f"forward + re-materialised forward + backward in fp64 numpy ({dt:.1f} s), "
                       f"scaled by {cfg.layers}/{layers} layers"}
@@ -83,14 +322,29 @@ def main():
         print(f"bench.py measures one partition on one GPU; --gpus {a.gpus} is not supported "
               "(multi-GPU pipelines are outside this build)", file=sys.stderr)
         sys.exit(2)
-    import torch
     import synth
+    base = synth.CONFIGS[a.config]
+    cfg = base.with_(micro=a.micro)
+    workload = (f"{cfg.name}: {cfg.layers}-layer pre-LN {cfg.kind} partition, d_model {cfg.d_model}, "
+                f"{cfg.heads} heads, d_ff {cfg.d_ff}, ReLU, seq {cfg.seq}, mini-batch {cfg.batch} "
+                f"in M={cfg.micro} micro-batches, " +
+                ("boundary gradients" if cfg.loss == "none" else f"{cfg.loss} loss"))
+    if a.kernel_summary:
+        kernel_summary(a.kernel_summary, a.command)
+        return
+    if a.traffic_summary:
+        if not a.role:
+            sys.exit("--traffic-summary needs --role")
+        traffic_summary(*a.traffic_summary, a.role, workload)
+        return
+    import torch
     from paper_1811_06965_amd import accounting
     from paper_1811_06965_amd.runtime import Partition
 
     torch.cuda.set_device(0)
-    base = synth.CONFIGS[a.config]
-    cfg = base.with_(micro=a.micro)
+    if a.copy_calibration:
+        copy_calibration()
+        return
     case = synth.make_case(cfg, 0)
     results = {}
     Ms = [a.micro] + ([m for m in (4, 8, 16, 32) if m != a.micro] if a.sweep else [])
@@ -99,29 +353,33 @@ def main():
         with Partition(c) as part:
             part.load_params(case["layers"], case["head"])
             inp = part.device_inputs(case)
-            ms = time_steps(part, inp, a.steps if M == a.micro else max(3, a.steps // 2), a.warmup)
+            ms, role, timed, roles = time_steps(part, inp, a.steps if M == a.micro else max(3, a.steps // 2),
+                                                a.warmup, a.role)
             mem = part.memory()
             del inp
         model, hw = accounting.step_flops(c)
         results[M] = {"M": M, "ms_per_step": ms, "tokens_per_s": c.batch * c.seq / (ms * 1e-3),
                       "hfu": hw / (ms * 1e-3) / PEAK_BF16, "mfu": model / (ms * 1e-3) / PEAK_BF16,
-                      "memory_bytes": mem}
+                      "memory_bytes": mem, "role": role, "timed": timed, "roles": roles}
         print(f"[bench] M={M}: {ms:.2f} ms/step, {results[M]['tokens_per_s']:.0f} tokens/s, "
-              f"HFU {100 * results[M]['hfu']:.1f}%", file=sys.stderr, flush=True)
+              f"HFU {100 * results[M]['hfu']:.1f}%, dominant role {role}", file=sys.stderr, flush=True)
     r = results[a.micro]
     out = {
         "metric": METRIC, "value": r["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1, "steps": a.steps,
         "warmup": a.warmup, "ms_per_step": r["ms_per_step"], "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: {cfg.layers}-layer pre-LN encoder partition, d_model {cfg.d_model}, "
-                               f"{cfg.heads} heads, d_ff {cfg.d_ff}, ReLU, seq {cfg.seq}, mini-batch {cfg.batch} "
-                               f"in M={cfg.micro} micro-batches, boundary gradients",
-                   "global_batch": cfg.batch, "seq_len": cfg.seq, "micro_batches": cfg.micro,
+        "config": {"workload": workload, "global_batch": cfg.batch, "seq_len": cfg.seq, "micro_batches": cfg.micro,
                    "parallelism": "one pipeline partition on one GPU"},
         "hfu": r["hfu"], "mfu": r["mfu"],
+        "roofline": roofline(r["role"], r["timed"], workload),
     }
+    if r["roles"]:
+        step_ms = r["ms_per_step"]
+        out["roles_ms_per_step"] = {k: round(v["ms"], 3) for k, v in r["roles"].items()}
+        out["roles_note"] = f"census step with every launch bracketed; step time {step_ms:.2f} ms unbracketed"
     if a.sweep:
-        out["sweep"] = [{k: v for k, v in results[M].items() if k != "memory_bytes"} for M in sorted(results)]
+        out["sweep"] = [{k: v for k, v in results[M].items() if k in ("M", "ms_per_step", "tokens_per_s", "hfu", "mfu")}
+                        for M in sorted(results)]
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, a.cpu_layers)
     print(json.dumps(out))

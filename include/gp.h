@@ -204,6 +204,48 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
  */
 gp_status gp_accumulate_and_step(gp_partition* p, float lr, double* loss_out, gp_stream stream);
 
+/*
+ * Launch timers (instrumentation; not part of the method).  Each library
+ * launch belongs to one role: a linear layer's forward ("FWD", Y = X W + b),
+ * input-gradient ("DX", dX = dY W^T) or weight-gradient ("DW", G_W += X^T dY
+ * with the bias gradient fused) GEMM, including its split-K reduction when
+ * one is used; an attention forward or backward; a LayerNorm forward or
+ * backward.  While a role is selected, every launch of that role is
+ * bracketed by two HIP events recorded on the stream the launch is enqueued
+ * on, and the role's algorithmic work is added up: GEMM 2 M N K FLOPs;
+ * attention 4 n H Sq Sk dh FLOPs forward and twice that backward (halved
+ * when causal; the recomputed scores are not counted); bytes = each operand
+ * read once and each output written once.
+ */
+typedef enum {
+    GP_K_NONE = 0,
+    GP_K_QKV_FWD, GP_K_QKV_DX, GP_K_QKV_DW,
+    GP_K_O_FWD, GP_K_O_DX, GP_K_O_DW,
+    GP_K_FFN1_FWD, GP_K_FFN1_DX, GP_K_FFN1_DW,
+    GP_K_FFN2_FWD, GP_K_FFN2_DX, GP_K_FFN2_DW,
+    GP_K_XQ_FWD, GP_K_XQ_DX, GP_K_XQ_DW,
+    GP_K_XKV_FWD, GP_K_XKV_DX, GP_K_XKV_DW,
+    GP_K_XO_FWD, GP_K_XO_DX, GP_K_XO_DW,
+    GP_K_HEAD_FWD, GP_K_HEAD_DX, GP_K_HEAD_DW,
+    GP_K_ATTN_FWD, GP_K_ATTN_BWD, GP_K_XATTN_FWD, GP_K_XATTN_BWD,
+    GP_K_LN_FWD, GP_K_LN_BWD,
+    GP_K_COUNT
+} gp_kernel_role;
+
+/* Select the timed role: one gp_kernel_role, GP_K_NONE to stop timing, or
+ * GP_K_COUNT to time every role (brackets every launch; for finding the
+ * dominant role, not for throughput runs).  Recorded launches are kept.
+ * GP_ERR_INVALID_ARG: role out of range. */
+gp_status gp_timer_select(gp_partition* p, int role);
+
+/* Totals of one role over the launches recorded since the last reset: summed
+ * event-to-event milliseconds, launch count, algorithmic FLOPs and bytes.
+ * Waits for the role's last recorded event.  Any output pointer may be NULL. */
+gp_status gp_timer_read(gp_partition* p, int role, double* ms, long* launches, double* flops, double* bytes);
+
+/* Forget every recorded launch (the events are kept for reuse). */
+gp_status gp_timer_reset(gp_partition* p);
+
 /* Message of the calling thread's last failure (library-owned, valid until the
  * thread's next failing call); "" if none. */
 const char* gp_last_error(void);

@@ -60,6 +60,15 @@ def build(verbose=False):
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    # A kernel template whose host-side instantiation fails is dropped without a
+    # diagnostic, leaving its launch stub undefined in the shared library; catch
+    # that here rather than at the first launch.
+    nm = shutil.which("nm")
+    if nm:
+        r = subprocess.run([nm, "-DC", "--undefined-only", tmp], capture_output=True, text=True)
+        bad = [l for l in r.stdout.splitlines() if "gp::" in l]
+        if bad:
+            raise RuntimeError("libgp.so has undefined internal symbols:\n" + "\n".join(bad[:20]))
     os.replace(tmp, LIB)
     return LIB
 

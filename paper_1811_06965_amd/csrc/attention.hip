@@ -163,7 +163,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dkv_simt(AttnArgs a) {
 template <typename T>
 gp_status fwd_t(const AttnArgs& a, hipStream_t st) {
     const long rows = (long)a.n * a.H * a.Sq;
-    attn_fwd_simt<T><<<(unsigned)((rows + AW - 1) / AW), 256, 0, st>>>(a);
+    klaunch(attn_fwd_simt<T>, (unsigned)((rows + AW - 1) / AW), 256, 0, st, a);
     GP_LAUNCH_CHECK();
     return GP_OK;
 }
@@ -171,9 +171,9 @@ gp_status fwd_t(const AttnArgs& a, hipStream_t st) {
 template <typename T>
 gp_status bwd_t(const AttnArgs& a, hipStream_t st) {
     const long qrows = (long)a.n * a.H * a.Sq, krows = (long)a.n * a.H * a.Sk;
-    attn_bwd_dq_simt<T><<<(unsigned)((qrows + AW - 1) / AW), 256, 0, st>>>(a);
+    klaunch(attn_bwd_dq_simt<T>, (unsigned)((qrows + AW - 1) / AW), 256, 0, st, a);
     GP_LAUNCH_CHECK();
-    attn_bwd_dkv_simt<T><<<(unsigned)((krows + AW - 1) / AW), 256, 0, st>>>(a);
+    klaunch(attn_bwd_dkv_simt<T>, (unsigned)((krows + AW - 1) / AW), 256, 0, st, a);
     GP_LAUNCH_CHECK();
     return GP_OK;
 }

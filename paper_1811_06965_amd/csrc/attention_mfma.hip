@@ -331,14 +331,14 @@ __global__ void __launch_bounds__(256) attn_bwd_dkv_mfma(AttnArgs a) {
 
 #define GP_NB_SWITCH(NB, KERNEL, GRID)                                              \
     switch (NB) {                                                                   \
-    case 1: KERNEL<1><<<GRID, 256, 0, st>>>(a); break;                              \
-    case 2: KERNEL<2><<<GRID, 256, 0, st>>>(a); break;                              \
-    case 3: KERNEL<3><<<GRID, 256, 0, st>>>(a); break;                              \
-    case 4: KERNEL<4><<<GRID, 256, 0, st>>>(a); break;                              \
-    case 5: KERNEL<5><<<GRID, 256, 0, st>>>(a); break;                              \
-    case 6: KERNEL<6><<<GRID, 256, 0, st>>>(a); break;                              \
-    case 7: KERNEL<7><<<GRID, 256, 0, st>>>(a); break;                              \
-    case 8: KERNEL<8><<<GRID, 256, 0, st>>>(a); break;                              \
+    case 1: klaunch(KERNEL<1>, GRID, 256, 0, st, a); break;                              \
+    case 2: klaunch(KERNEL<2>, GRID, 256, 0, st, a); break;                              \
+    case 3: klaunch(KERNEL<3>, GRID, 256, 0, st, a); break;                              \
+    case 4: klaunch(KERNEL<4>, GRID, 256, 0, st, a); break;                              \
+    case 5: klaunch(KERNEL<5>, GRID, 256, 0, st, a); break;                              \
+    case 6: klaunch(KERNEL<6>, GRID, 256, 0, st, a); break;                              \
+    case 7: klaunch(KERNEL<7>, GRID, 256, 0, st, a); break;                              \
+    case 8: klaunch(KERNEL<8>, GRID, 256, 0, st, a); break;                              \
     default: return set_error(GP_ERR_UNSUPPORTED, "attention: sequence length > 256"); \
     }
 

@@ -68,8 +68,32 @@ template <> struct Vec16<float> {
         if (e_ != hipSuccess) return ::gp::hip_fail(e_, __FILE__, __LINE__); \
     } while (0)
 
+#include <hip/hip_ext.h>
 #include "../../include/gp.h"
 namespace gp {
 gp_status hip_fail(hipError_t e, const char* file, int line);
 gp_status set_error(gp_status s, const char* msg);
+
+// Launch timing: while a launch role is timed, the first kernel launched
+// takes `start` (its dispatch start timestamp) and every kernel takes `stop`
+// (so the last one's completion ends the interval).  Thread-local, set by the
+// partition around one role's launches.
+struct LaunchEvents {
+    hipEvent_t start = nullptr, stop = nullptr;
+    bool started = false;
+};
+LaunchEvents& launch_events();
+
+// Kernel launch through hipExtLaunchKernelGGL, attaching the timing events
+// when a role is being timed (no extra stream packets).
+template <typename... Args, typename... P>
+inline void klaunch(void (*k)(Args...), dim3 grid, dim3 block, uint32_t shmem, hipStream_t st, P... p) {
+    LaunchEvents& ev = launch_events();
+    hipEvent_t e0 = nullptr;
+    if (ev.stop && !ev.started) {
+        e0 = ev.start;
+        ev.started = true;
+    }
+    hipExtLaunchKernelGGL(k, grid, block, shmem, st, e0, ev.stop, 0u, static_cast<Args>(p)...);
+}
 }

@@ -309,6 +309,9 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int row, int col, fl
     } else if constexpr (EPI == EPI_RELU_MASK) {
         const float z = to_f32(reinterpret_cast<const T*>(a.aux)[(long)row * a.ldaux + col]);
         reinterpret_cast<T*>(a.C)[i] = to_elt<T>(z > 0.f ? v : 0.f);
+    } else if constexpr (EPI == EPI_ACC_F32) {
+        float* c = reinterpret_cast<float*>(a.C) + i;
+        *c = a.accumulate ? *c + v : v;
     }
 }
 
@@ -360,8 +363,10 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs args) {
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
     // Fused bias gradient of a weight-gradient GEMM: the workgroups of the
-    // first M tile see every k-row of B (= dY) for their columns.
-    constexpr bool COLSUM = !BKM && EPI == EPI_ACC_F32;
+    // first M tile see every k-row of B (= dY) for their columns (of their k
+    // range, under split-K: then the sums go to the partial area after the
+    // split partial tiles, one row of N per split).
+    constexpr bool COLSUM = !BKM && (EPI == EPI_ACC_F32 || SPLIT);
     const bool do_colsum = COLSUM && args.colsum != nullptr && tm == 0;
     float cs[LB::VEC];
 #pragma unroll
@@ -429,7 +434,11 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs args) {
                 float sum = 0.f;
                 for (int t = mb; t < 256; t += MBLK) sum += red[t * VEC + i];
                 const int col = n0 + tid;
-                if (col < args.N) args.colsum[col] = args.accumulate ? args.colsum[col] + sum : sum;
+                if constexpr (SPLIT) {
+                    if (col < args.N) args.ws[((long)gridDim.y * args.M + blockIdx.y) * args.N + col] = sum;
+                } else {
+                    if (col < args.N) args.colsum[col] = args.accumulate ? args.colsum[col] + sum : sum;
+                }
             }
         }
     }
@@ -459,6 +468,275 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs args) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// Direct-to-LDS pipeline for bf16 GEMMs with both operands k-contiguous (the
+// forward and input-gradient GEMMs).  Tiles are copied global -> LDS with
+// buffer_load_dwordx4 ... lds: each wave instruction fills 8 rows (1 KB) of a
+// stage and each lane fetches the global 16-byte chunk that belongs at its
+// (swizzled) LDS position, so no VGPRs hold staged data and no ds_write is
+// issued.  NSTAGE stages form a ring; k-tile t + NSTAGE - 1 is in flight while
+// tile t is consumed.  Waits use explicit vmcnt values (loads complete in
+// order), and the single barrier per k-tile precedes the last k-step's MFMAs.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt");
+    __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+__device__ __forceinline__ void wait_vmcnt_dyn(int n) {
+    switch (n) {
+    case 0: wait_vmcnt<0>(); break;
+    case 4: wait_vmcnt<4>(); break;
+    case 6: wait_vmcnt<6>(); break;
+    case 8: wait_vmcnt<8>(); break;
+    case 12: wait_vmcnt<12>(); break;
+    case 16: wait_vmcnt<16>(); break;
+    case 24: wait_vmcnt<24>(); break;
+    case 32: wait_vmcnt<32>(); break;
+    case 48: wait_vmcnt<48>(); break;
+    default: wait_vmcnt<0>(); break;
+    }
+}
+
+typedef __attribute__((address_space(3))) void* LdsPtr;
+
+// P direct loads of 8 rows (1 KB) each into consecutive LDS blocks at dst;
+// lane offsets vo[i] are fixed, the k advance is the scalar offset so.
+template <int P>
+__device__ __forceinline__ void dl_load_blocks(Rsrc g, const uint32_t* vo, int so, char* dst) {
+#pragma unroll
+    for (int i = 0; i < P; ++i) __builtin_amdgcn_raw_ptr_buffer_load_lds(g, (LdsPtr)(dst + i * 1024), 16, vo[i], so, 0, 0);
+}
+
+// Wave index as a wave-uniform (scalar) value, so LDS base addresses derived
+// from it stay in SGPRs (M0 of the direct loads).
+__device__ __forceinline__ int uniform_wave_id(int tid) { return __builtin_amdgcn_readfirstlane(tid >> 6); }
+
+// Epilogue of a tile lying entirely inside C: per-lane column offsets are
+// computed once; the row part of every offset is wave-uniform and passed as
+// the buffer instruction's scalar offset.
+template <int TM, int TN, int EPI>
+__device__ __forceinline__ void dl_epilogue_full(const GemmArgs& a, const f32x16 (&acc)[TM][TN], int row0, int col0,
+                                                 int lane) {
+    constexpr bool OUT_F32 = EPI == EPI_RES_F32 || EPI == EPI_F32;
+    const int h = lane >> 5;
+    const uint32_t osz = OUT_F32 ? 4 : 2;
+    const long big = (long)(a.M - 1) * a.ldc + a.N;
+    const Rsrc c = make_rsrc(a.C, (uint32_t)(big * osz));
+    const uint32_t vc = (uint32_t)(((long)(row0 + 4 * h) * a.ldc + col0) * osz);
+    float bv[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) bv[j] = (EPI == EPI_STORE || EPI == EPI_RES_F32) && a.bias ? a.bias[col0 + j * 32] : 0.f;
+    Rsrc aux, c2;
+    uint32_t va = 0, vc2 = 0;
+    if constexpr (EPI == EPI_RES_F32) {
+        aux = make_rsrc(a.aux, (uint32_t)(((long)(a.M - 1) * a.ldaux + a.N) * 4));
+        va = (uint32_t)(((long)(row0 + 4 * h) * a.ldaux + col0) * 4);
+        c2 = make_rsrc(a.C2, a.C2 ? (uint32_t)(((long)(a.M - 1) * a.ldc2 + a.N) * 2) : 0u);
+        vc2 = (uint32_t)(((long)(row0 + 4 * h) * a.ldc2 + col0) * 2);
+    } else if constexpr (EPI == EPI_RELU_MASK) {
+        aux = make_rsrc(a.aux, (uint32_t)(((long)(a.M - 1) * a.ldaux + a.N) * 2));
+        va = (uint32_t)(((long)(row0 + 4 * h) * a.ldaux + col0) * 2);
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+        float in[TN][16];
+        if constexpr (EPI == EPI_RES_F32 || EPI == EPI_RELU_MASK) {
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int dr = i * 32 + (r >> 2) * 8 + (r & 3);
+                    if constexpr (EPI == EPI_RES_F32)
+                        in[j][r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                                 aux, va, (dr * a.ldaux + j * 32) * 4, 0));
+                    else
+                        in[j][r] = (float)__builtin_bit_cast(
+                            bf16, __builtin_amdgcn_raw_buffer_load_b16(aux, va, (dr * a.ldaux + j * 32) * 2, 0));
+                }
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int dr = i * 32 + (r >> 2) * 8 + (r & 3);
+                const int so = (dr * a.ldc + j * 32) * osz;
+                float v = acc[i][j][r];
+                if constexpr (EPI == EPI_STORE) {
+                    v += bv[j];
+                    if (a.relu) v = fmaxf(v, 0.f);
+                    __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, (bf16)v), c, vc, so, 0);
+                } else if constexpr (EPI == EPI_RES_F32) {
+                    v += in[j][r] + bv[j];
+                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), c, vc, so, 0);
+                    if (a.C2)
+                        __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, (bf16)v), c2, vc2,
+                                                              (dr * a.ldc2 + j * 32) * 2, 0);
+                } else if constexpr (EPI == EPI_F32) {
+                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), c, vc, so, 0);
+                } else if constexpr (EPI == EPI_RELU_MASK) {
+                    v = in[j][r] > 0.f ? v : 0.f;
+                    __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, (bf16)v), c, vc, so, 0);
+                }
+            }
+    }
+}
+
+// Direct-to-LDS GEMM (requires K % 64 == 0).  Address arithmetic is hoisted:
+// each lane's global offsets are computed once and the k advance rides in the
+// scalar offset of the buffer load; M0 (the LDS destination) is wave-uniform;
+// fragment addresses are precomputed per k-step and the stage base is folded
+// into the ds_read immediate by unrolling the k-tile loop over the stages.
+template <int BM, int BN, int WM, int WN, int NSTAGE, int EPI, bool SPLIT>
+__global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
+    constexpr int BK = 64, KS = 4, NW = WM * WN;
+    constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
+    constexpr int STAGE = (BM + BN) * 128;
+    constexpr int PA = BM / (8 * NW), PB = BN / (8 * NW);  // 8-row load blocks per wave for A and B
+    static_assert(PA * 8 * NW == BM && PB * 8 * NW == BN, "load blocks");
+    constexpr int LPW = PA + PB;               // load instructions per wave per k-tile
+    __shared__ __attribute__((aligned(1024))) char smem[NSTAGE * STAGE];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = uniform_wave_id(tid);
+    const int wm = wave / WN, wn = wave % WN;
+    const int tiles_m = (args.M + BM - 1) / BM;
+    const int G = gridDim.x;
+    int bid = blockIdx.x;
+    const int G8 = G & ~7;
+    if (bid < G8) bid = (bid & 7) * (G8 >> 3) + (bid >> 3);
+    const int tm = bid % tiles_m, tn = bid / tiles_m;
+    const int m0 = tm * BM, n0 = tn * BN;
+
+    const int nk_all = args.K / BK;
+    int kt0 = 0, kt1 = nk_all;
+    if constexpr (SPLIT) {
+        const int per = (nk_all + gridDim.y - 1) / gridDim.y;
+        kt0 = blockIdx.y * per;
+        kt1 = min(nk_all, kt0 + per);
+    }
+    const int nkt = kt1 - kt0;
+
+    const Rsrc A = make_rsrc(args.A, (uint32_t)(((long)(args.M - 1) * args.lda + args.K) * 2));
+    const Rsrc B = make_rsrc(args.B, (uint32_t)(((long)(args.N - 1) * args.ldb + args.K) * 2));
+    uint32_t voa[PA], vob[PB];
+#pragma unroll
+    for (int i = 0; i < PA; ++i) {
+        const int r = (wave * PA + i) * 8 + (lane >> 3);
+        const int row = m0 + r;
+        voa[i] = row < args.M ? (uint32_t)(((long)row * args.lda + ((lane & 7) ^ swz(r)) * 8) * 2) : OOB;
+    }
+#pragma unroll
+    for (int i = 0; i < PB; ++i) {
+        const int r = (wave * PB + i) * 8 + (lane >> 3);
+        const int row = n0 + r;
+        vob[i] = row < args.N ? (uint32_t)(((long)row * args.ldb + ((lane & 7) ^ swz(r)) * 8) * 2) : OOB;
+    }
+#define GP_DL_ISSUE(t, st)                                                                   \
+    do {                                                                                     \
+        dl_load_blocks<PA>(A, voa, (t) * (BK * 2), (st) + wave * PA * 1024);                 \
+        dl_load_blocks<PB>(B, vob, (t) * (BK * 2), (st) + BM * 128 + wave * PB * 1024);      \
+    } while (0)
+
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    // fragment byte offsets within a stage, per k-step
+    const int fr = lane & 31, h = lane >> 5;
+    int fa_off[KS][TM], fb_off[KS][TN];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            const int row = wm * (BM / WM) + i * 32 + fr;
+            fa_off[s][i] = row * 128 + (((2 * s + h) ^ swz(row)) << 4);
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int row = wn * (BN / WN) + j * 32 + fr;
+            fb_off[s][j] = BM * 128 + row * 128 + (((2 * s + h) ^ swz(row)) << 4);
+        }
+    }
+    Frag<bf16> fa[2][TM], fb[2][TN];
+    auto load_frags = [&](int slot, const char* stg, int s) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) fa[slot][i].v = *reinterpret_cast<const bf16x8*>(stg + fa_off[s][i]);
+#pragma unroll
+        for (int j = 0; j < TN; ++j) fb[slot][j].v = *reinterpret_cast<const bf16x8*>(stg + fb_off[s][j]);
+    };
+
+    if (nkt > 0) {
+        // prologue: fill every stage; wait for tile 0 (tiles 1 .. NSTAGE-1 may be in flight)
+#pragma unroll
+        for (int p = 0; p < NSTAGE; ++p)
+            if (p < nkt) GP_DL_ISSUE(kt0 + p, smem + p * STAGE);
+        wait_vmcnt_dyn(min(NSTAGE - 1, nkt - 1) * LPW);
+        __syncthreads();
+        load_frags(0, smem, 0);
+        for (int i0 = 0; i0 < nkt; i0 += NSTAGE) {
+#pragma unroll
+            for (int st = 0; st < NSTAGE; ++st) {
+                const int i = i0 + st;
+                if (i >= nkt) break;
+                const char* stg = smem + st * STAGE;
+                const char* nxt = smem + ((st + 1) % NSTAGE) * STAGE;
+#pragma unroll
+                for (int s = 0; s < KS; ++s) {
+                    const int cur = s & 1;
+                    if (s + 1 < KS) {
+                        load_frags(cur ^ 1, stg, s + 1);
+                    } else {
+                        // Tiles issued: 0 .. min(i + NSTAGE - 1, nkt - 1).  Tile i+1 must have
+                        // landed (tiles i+2 .. i+NSTAGE-1 may be in flight); then every wave is
+                        // past tile i, whose stage is refilled with tile i + NSTAGE.  Branch-free
+                        // around the LDS reads; on the last tile the fragment read is unused.
+                        wait_vmcnt_dyn(i + 1 < nkt ? min(NSTAGE - 2, nkt - 2 - i) * LPW : 0);
+                        __syncthreads();
+                        if (i + NSTAGE < nkt) GP_DL_ISSUE(kt0 + i + NSTAGE, smem + st * STAGE);
+                        load_frags(cur ^ 1, nxt, 0);
+                    }
+#pragma unroll
+                    for (int ii = 0; ii < TM; ++ii)
+#pragma unroll
+                        for (int j = 0; j < TN; ++j) mma(acc[ii][j], fa[cur][ii], fb[cur][j]);
+                }
+            }
+        }
+    }
+
+#undef GP_DL_ISSUE
+    const int row0 = m0 + wm * (BM / WM), col0 = n0 + wn * (BN / WN) + (lane & 31);
+    if constexpr (SPLIT) {
+        const Rsrc ws = make_rsrc(args.ws, (uint32_t)((long)gridDim.y * args.M * args.N * 4));
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int col = col0 + j * 32;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int row = row0 + i * 32 + (r >> 2) * 8 + h * 4 + (r & 3);
+                    const bool ok = row < args.M && col < args.N;
+                    const uint32_t o = ok ? (uint32_t)((((long)blockIdx.y * args.M + row) * args.N + col) * 4) : OOB;
+                    const float v = acc[i][j][r];  // see the note in gemm_kernel
+                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), ws, o, 0, 0);
+                }
+            }
+    } else {
+        if (m0 + BM <= args.M && n0 + BN <= args.N) {
+            dl_epilogue_full<TM, TN, EPI>(args, acc, row0, col0, lane);
+        } else {
+            Epilogue<bf16, EPI> ep;
+            ep.init(args);
+            ep.template run<TM, TN>(args, acc, row0, col0, lane);
+        }
+    }
+}
+
 // Sum the split-K partials in split order and apply the epilogue; 4 columns per thread.
 template <typename T, int EPI>
 __global__ void __launch_bounds__(256) splitk_reduce(GemmArgs args, int splits) {
@@ -477,34 +755,72 @@ __global__ void __launch_bounds__(256) splitk_reduce(GemmArgs args, int splits) 
     }
 }
 
-enum TileCfg { T256x256 = 0, T256x128 = 1, T128x256 = 2, T128x128 = 3 };
+enum TileCfg {
+    T256x256 = 0, T256x128 = 1, T128x256 = 2, T128x128 = 3,  // register-staged (any operand form)
+    T_DL128x128_S2 = 4, T_DL128x128_S3 = 5, T_DL256x128_S2 = 6, T_DL256x256_S2 = 7,  // direct-to-LDS, k-contiguous
+    T_DL256x256_W8 = 8, T_DL256x128_W8 = 9, T_DL128x256_W8 = 10                          // ... with 8 waves
+};
 
 template <typename T, int BM, int BN, bool AK, bool BKM>
 gp_status launch_tile(const GemmArgs& a, int epi, int splits, hipStream_t st) {
     const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
     if (splits > 1) {
         dim3 grid(tiles, splits);
-        gemm_kernel<T, BM, BN, AK, BKM, EPI_F32, true><<<grid, 256, 0, st>>>(a);
+        klaunch(gemm_kernel<T, BM, BN, AK, BKM, EPI_F32, true>, grid, 256, 0, st, a);
         GP_LAUNCH_CHECK();
         const long nq = (long)a.M * (a.N / 4);
         const int rg = (int)std::min<long>((nq + 255) / 256, 2048);
         switch (epi) {
-        case EPI_STORE: splitk_reduce<T, EPI_STORE><<<rg, 256, 0, st>>>(a, splits); break;
-        case EPI_RES_F32: splitk_reduce<T, EPI_RES_F32><<<rg, 256, 0, st>>>(a, splits); break;
-        case EPI_F32: splitk_reduce<T, EPI_F32><<<rg, 256, 0, st>>>(a, splits); break;
-        case EPI_RELU_MASK: splitk_reduce<T, EPI_RELU_MASK><<<rg, 256, 0, st>>>(a, splits); break;
+        case EPI_STORE: klaunch(splitk_reduce<T, EPI_STORE>, rg, 256, 0, st, a, splits); break;
+        case EPI_RES_F32: klaunch(splitk_reduce<T, EPI_RES_F32>, rg, 256, 0, st, a, splits); break;
+        case EPI_F32: klaunch(splitk_reduce<T, EPI_F32>, rg, 256, 0, st, a, splits); break;
+        case EPI_RELU_MASK: klaunch(splitk_reduce<T, EPI_RELU_MASK>, rg, 256, 0, st, a, splits); break;
+        case EPI_ACC_F32: klaunch(splitk_reduce<T, EPI_ACC_F32>, rg, 256, 0, st, a, splits); break;
+        default: return set_error(GP_ERR_INVALID_ARG, "gemm: split-K epilogue");
+        }
+        GP_LAUNCH_CHECK();
+        if (epi == EPI_ACC_F32 && !BKM && a.colsum)
+            return colsum_finalize(a.ws + (long)splits * a.M * a.N, splits, a.N, a.colsum, a.accumulate, st);
+        return GP_OK;
+    }
+    switch (epi) {
+    case EPI_STORE: klaunch(gemm_kernel<T, BM, BN, AK, BKM, EPI_STORE, false>, tiles, 256, 0, st, a); break;
+    case EPI_RES_F32: klaunch(gemm_kernel<T, BM, BN, AK, BKM, EPI_RES_F32, false>, tiles, 256, 0, st, a); break;
+    case EPI_F32: klaunch(gemm_kernel<T, BM, BN, AK, BKM, EPI_F32, false>, tiles, 256, 0, st, a); break;
+    case EPI_RELU_MASK: klaunch(gemm_kernel<T, BM, BN, AK, BKM, EPI_RELU_MASK, false>, tiles, 256, 0, st, a); break;
+    case EPI_ACC_F32: klaunch(gemm_kernel<T, BM, BN, AK, BKM, EPI_ACC_F32, false>, tiles, 256, 0, st, a); break;
+    default: return set_error(GP_ERR_INVALID_ARG, "gemm: unknown epilogue");
+    }
+    GP_LAUNCH_CHECK();
+    return GP_OK;
+}
+
+template <int BM, int BN, int WM, int WN, int NSTAGE>
+gp_status launch_dl(const GemmArgs& a, int epi, int splits, hipStream_t st) {
+    constexpr int NT = 64 * WM * WN;
+    const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+    if (splits > 1) {
+        dim3 grid(tiles, splits);
+        klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_F32, true>, grid, NT, 0, st, a);
+        GP_LAUNCH_CHECK();
+        const long nq = (long)a.M * (a.N / 4);
+        const int rg = (int)std::min<long>((nq + 255) / 256, 2048);
+        switch (epi) {
+        case EPI_STORE: klaunch(splitk_reduce<bf16, EPI_STORE>, rg, 256, 0, st, a, splits); break;
+        case EPI_RES_F32: klaunch(splitk_reduce<bf16, EPI_RES_F32>, rg, 256, 0, st, a, splits); break;
+        case EPI_F32: klaunch(splitk_reduce<bf16, EPI_F32>, rg, 256, 0, st, a, splits); break;
+        case EPI_RELU_MASK: klaunch(splitk_reduce<bf16, EPI_RELU_MASK>, rg, 256, 0, st, a, splits); break;
         default: return set_error(GP_ERR_INVALID_ARG, "gemm: split-K epilogue");
         }
         GP_LAUNCH_CHECK();
         return GP_OK;
     }
     switch (epi) {
-    case EPI_STORE: gemm_kernel<T, BM, BN, AK, BKM, EPI_STORE, false><<<tiles, 256, 0, st>>>(a); break;
-    case EPI_RES_F32: gemm_kernel<T, BM, BN, AK, BKM, EPI_RES_F32, false><<<tiles, 256, 0, st>>>(a); break;
-    case EPI_F32: gemm_kernel<T, BM, BN, AK, BKM, EPI_F32, false><<<tiles, 256, 0, st>>>(a); break;
-    case EPI_RELU_MASK: gemm_kernel<T, BM, BN, AK, BKM, EPI_RELU_MASK, false><<<tiles, 256, 0, st>>>(a); break;
-    case EPI_ACC_F32: gemm_kernel<T, BM, BN, AK, BKM, EPI_ACC_F32, false><<<tiles, 256, 0, st>>>(a); break;
-    default: return set_error(GP_ERR_INVALID_ARG, "gemm: unknown epilogue");
+    case EPI_STORE: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_STORE, false>, tiles, NT, 0, st, a); break;
+    case EPI_RES_F32: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_RES_F32, false>, tiles, NT, 0, st, a); break;
+    case EPI_F32: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_F32, false>, tiles, NT, 0, st, a); break;
+    case EPI_RELU_MASK: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_RELU_MASK, false>, tiles, NT, 0, st, a); break;
+    default: return set_error(GP_ERR_INVALID_ARG, "gemm: direct-load path has no accumulate epilogue");
     }
     GP_LAUNCH_CHECK();
     return GP_OK;
@@ -512,6 +828,18 @@ gp_status launch_tile(const GemmArgs& a, int epi, int splits, hipStream_t st) {
 
 template <bool AK, bool BKM>
 gp_status launch_bf16(const GemmArgs& a, int epi, int cfg, int splits, hipStream_t st) {
+    if constexpr (AK && BKM) {
+        switch (cfg) {
+        case T_DL128x128_S2: return launch_dl<128, 128, 2, 2, 2>(a, epi, splits, st);
+        case T_DL128x128_S3: return launch_dl<128, 128, 2, 2, 3>(a, epi, splits, st);
+        case T_DL256x128_S2: return launch_dl<256, 128, 2, 2, 2>(a, epi, splits, st);
+        case T_DL256x256_S2: return launch_dl<256, 256, 2, 2, 2>(a, epi, splits, st);
+        case T_DL256x256_W8: return launch_dl<256, 256, 2, 4, 2>(a, epi, splits, st);
+        case T_DL256x128_W8: return launch_dl<256, 128, 4, 2, 2>(a, epi, splits, st);
+        case T_DL128x256_W8: return launch_dl<128, 256, 2, 4, 2>(a, epi, splits, st);
+        default: break;
+        }
+    }
     switch (cfg) {
     case T256x256: return launch_tile<bf16, 256, 256, AK, BKM>(a, epi, splits, st);
     case T256x128: return launch_tile<bf16, 256, 128, AK, BKM>(a, epi, splits, st);
@@ -526,6 +854,47 @@ constexpr int NUM_CU = 256;
 // time, where a round holds NUM_CU x (workgroups resident per CU) tiles and
 // co-resident tiles share their CU; per-tile time is the tile's k-steps over
 // a measured relative efficiency; split-K adds its partial-tile traffic.
+// Split-K needs the partial tiles (and, for a fused bias gradient, one row of
+// column sums per split) to fit the workspace, N % 4 == 0 for the reduce, and
+// at least four k-steps per split.
+bool split_fits(const GemmArgs& a, int s, int nk) {
+    const long need = (long)s * a.M * a.N + (a.colsum ? (long)s * a.N : 0);
+    return a.ws != nullptr && nk / s >= 4 && need <= a.ws_elems && a.N % 4 == 0;
+}
+
+// Direct-to-LDS tiles (k-contiguous operands, K % 64 == 0): time = fixed
+// launch/epilogue cost + rounds x k-steps x per-step time of the tile shape
+// (per-step times fitted to measurements on MI355X over the d_model 1024
+// partition's GEMMs; a 128x128 tile runs two per CU, the 8-wave tiles one),
+// plus the split-K partial traffic.  Units: microseconds.
+void choose_dl(const GemmArgs& a, int epi, int& cfg, int& splits) {
+    struct Cand { int cfg, bm, bn, resident; double step_alone, step_full; };
+    static const Cand cands[4] = {{T_DL128x128_S2, 128, 128, 2, 0.583, 0.877},
+                                  {T_DL256x256_W8, 256, 256, 1, 1.273, 1.273},
+                                  {T_DL256x128_W8, 256, 128, 1, 0.839, 0.839},
+                                  {T_DL128x256_W8, 128, 256, 1, 0.727, 0.727}};
+    const int nk = a.K / 64;
+    double best = 1e300;
+    cfg = T_DL128x128_S2;
+    splits = 1;
+    for (const Cand& c : cands) {
+        const long tiles = (long)((a.M + c.bm - 1) / c.bm) * ((a.N + c.bn - 1) / c.bn);
+        for (int s = 1; s <= 8; s *= 2) {
+            if (s > 1 && !split_fits(a, s, nk)) continue;
+            const long per_cu = (tiles * s + NUM_CU - 1) / NUM_CU;
+            const long rounds = (per_cu + c.resident - 1) / c.resident;
+            const double step = per_cu >= c.resident ? c.step_full : c.step_alone;
+            double t = 6.66 + rounds * (double)((nk + s - 1) / s) * step;
+            if (s > 1) t += (double)a.M * a.N * 4.0 * (s + 1.0) / 2.0 / 1.75e6 + 2.5;
+            if (t < best * 0.999) {
+                best = t;
+                cfg = c.cfg;
+                splits = s;
+            }
+        }
+    }
+}
+
 void choose(const GemmArgs& a, int epi, int& cfg, int& splits) {
     static const int BMs[4] = {256, 256, 128, 128}, BNs[4] = {256, 128, 256, 128};
     static const int resident[4] = {1, 1, 1, 2};
@@ -537,9 +906,7 @@ void choose(const GemmArgs& a, int epi, int& cfg, int& splits) {
     for (int c = 0; c < 4; ++c) {
         const long tiles = (long)((a.M + BMs[c] - 1) / BMs[c]) * ((a.N + BNs[c] - 1) / BNs[c]);
         for (int s = 1; s <= 8; s *= 2) {
-            if (s > 1 && (epi == EPI_ACC_F32 || a.ws == nullptr || nk / s < 4 ||
-                          (long)s * a.M * a.N > a.ws_elems || a.N % 4))
-                continue;
+            if (s > 1 && !split_fits(a, s, nk)) continue;
             const long wgs = tiles * s;
             const long slots = (long)NUM_CU * resident[c];
             const long rounds = (wgs + slots - 1) / slots;
@@ -548,8 +915,9 @@ void choose(const GemmArgs& a, int epi, int& cfg, int& splits) {
             // time in units of one 128x128x64 tile step of a CU running alone
             // two co-resident tiles hide each other's latencies: 1.5x, not 2x, the time of one
             double t = rounds * (per_cu == 2 ? 1.5 : 1.0) * (BMs[c] / 128.0) * (BNs[c] / 128.0) * kt / eff[c];
-            // split-K: partial-tile traffic (mostly cache-resident) and the reduce launch
-            if (s > 1) t += (double)a.M * a.N * 4.0 * (s + 1.0) / 2.0e7 + 8.0;
+            // split-K: partial-tile traffic at ~1.75 TB/s and the reduce launch (one
+            // unit = one 128x128x64 step of a lone tile, ~0.58 us on MI355X)
+            if (s > 1) t += (double)a.M * a.N * 4.0 * (s + 1.0) / 2.0 / 1.0e6 + 4.0;
             if (t < best * 0.999) {
                 best = t;
                 cfg = c;
@@ -579,13 +947,16 @@ gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dty
         gp_status s = check_args<bf16>(a, a_kmajor, b_kmajor);
         if (s != GP_OK) return s;
         int cfg, splits;
-        choose(a, epi, cfg, splits);
-        if (a.force_cfg >= 0 && a.force_cfg <= T128x128) {
+        if (a_kmajor && a.K % 64 == 0 && epi != EPI_ACC_F32)
+            choose_dl(a, epi, cfg, splits);
+        else
+            choose(a, epi, cfg, splits);
+        if (a.force_cfg >= 0 && a.force_cfg <= T_DL128x256_W8 && (a.force_cfg <= T128x128 || a_kmajor)) {
             cfg = a.force_cfg;
             splits = a.force_splits > 0 ? a.force_splits : 1;
-            if (epi == EPI_ACC_F32 || a.ws == nullptr || (long)splits * a.M * a.N > a.ws_elems || a.N % 4)
-                splits = 1;
+            if (splits > 1 && !split_fits(a, splits, (a.K + 63) / 64)) splits = 1;
         }
+        if (cfg > T128x128 && (!a_kmajor || epi == EPI_ACC_F32 || a.K % 64)) cfg = T128x128;
         return a_kmajor ? launch_bf16<true, true>(a, epi, cfg, splits, st)
                         : launch_bf16<false, false>(a, epi, cfg, splits, st);
     }

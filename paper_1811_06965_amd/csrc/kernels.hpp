@@ -100,6 +100,10 @@ gp_status sgd_update(float* w, const float* g, float lr, long count, hipStream_t
 // Working copies of one linear layer from its fp32 master W [in, out]:
 // kn (elt) = W, nk (elt) = W^T.
 gp_status refresh_linear(int dtype, const float* w, int in, int out, void* kn, void* nk, hipStream_t st);
+// An empty launch labelled by its grid (role x (edge + 1) workgroups of one
+// wave): edge 0 before, 1 after a timed launch, so that per-dispatch profiler
+// records can be attributed to launch roles.
+gp_status role_marker(int role, int edge, hipStream_t st);
 // flag[0] = 1 if any of x[0..count) is not finite (flag must be zeroed first).
 gp_status finite_check(const float* x, long count, int* flag, hipStream_t st);
 

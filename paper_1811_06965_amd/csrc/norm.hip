@@ -272,25 +272,25 @@ gp_status ln_fwd_t(const float* x, long rows, int D, const float* g, const float
     T* o = reinterpret_cast<T*>(out);
     if (D % 256 == 0 && D <= 2048) {
         switch (D / 256) {
-        case 1: ln_fwd_v4<T, 1><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats); break;
-        case 2: ln_fwd_v4<T, 2><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats); break;
-        case 3: ln_fwd_v4<T, 3><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats); break;
-        case 4: ln_fwd_v4<T, 4><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats); break;
-        case 5: ln_fwd_v4<T, 5><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats); break;
-        case 6: ln_fwd_v4<T, 6><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats); break;
-        case 7: ln_fwd_v4<T, 7><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats); break;
-        default: ln_fwd_v4<T, 8><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats); break;
+        case 1: klaunch(ln_fwd_v4<T, 1>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats); break;
+        case 2: klaunch(ln_fwd_v4<T, 2>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats); break;
+        case 3: klaunch(ln_fwd_v4<T, 3>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats); break;
+        case 4: klaunch(ln_fwd_v4<T, 4>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats); break;
+        case 5: klaunch(ln_fwd_v4<T, 5>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats); break;
+        case 6: klaunch(ln_fwd_v4<T, 6>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats); break;
+        case 7: klaunch(ln_fwd_v4<T, 7>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats); break;
+        default: klaunch(ln_fwd_v4<T, 8>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats); break;
         }
         GP_LAUNCH_CHECK();
         return GP_OK;
     }
     const int C = (D + 63) / 64;
-    if (C <= 1) ln_fwd_kernel<T, 1><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats);
-    else if (C <= 2) ln_fwd_kernel<T, 2><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats);
-    else if (C <= 4) ln_fwd_kernel<T, 4><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats);
-    else if (C <= 8) ln_fwd_kernel<T, 8><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats);
-    else if (C <= 16) ln_fwd_kernel<T, 16><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats);
-    else if (C <= 32) ln_fwd_kernel<T, 32><<<grid, 256, 0, st>>>(x, rows, D, g, b, eps, o, stats);
+    if (C <= 1) klaunch(ln_fwd_kernel<T, 1>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats);
+    else if (C <= 2) klaunch(ln_fwd_kernel<T, 2>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats);
+    else if (C <= 4) klaunch(ln_fwd_kernel<T, 4>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats);
+    else if (C <= 8) klaunch(ln_fwd_kernel<T, 8>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats);
+    else if (C <= 16) klaunch(ln_fwd_kernel<T, 16>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats);
+    else if (C <= 32) klaunch(ln_fwd_kernel<T, 32>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats);
     else return set_error(GP_ERR_UNSUPPORTED, "layernorm: d_model > 2048");
     GP_LAUNCH_CHECK();
     return GP_OK;
@@ -304,7 +304,7 @@ gp_status ln_bwd_t(const float* dn, const float* x, const float* stats, const fl
     *nblk = grid;
     T* e = reinterpret_cast<T*>(dxe);
     if (D % 256 == 0 && D <= 2048) {
-#define GP_LNV(CC) ln_bwd_v4<T, CC><<<grid, 256, 0, st>>>(dn, x, stats, gamma, rows, D, rpw, dres, dx32, e, partial)
+#define GP_LNV(CC) klaunch(ln_bwd_v4<T, CC>, grid, 256, 0, st, dn, x, stats, gamma, rows, D, rpw, dres, dx32, e, partial)
         switch (D / 256) {
         case 1: GP_LNV(1); break;
         case 2: GP_LNV(2); break;
@@ -320,7 +320,7 @@ gp_status ln_bwd_t(const float* dn, const float* x, const float* stats, const fl
         return GP_OK;
     }
     const int C = (D + 63) / 64;
-#define GP_LNB(CC) ln_bwd_kernel<T, CC><<<grid, 256, 0, st>>>(dn, x, stats, gamma, rows, D, rpw, dres, dx32, e, partial)
+#define GP_LNB(CC) klaunch(ln_bwd_kernel<T, CC>, grid, 256, 0, st, dn, x, stats, gamma, rows, D, rpw, dres, dx32, e, partial)
     if (C <= 1) GP_LNB(1);
     else if (C <= 2) GP_LNB(2);
     else if (C <= 4) GP_LNB(4);
@@ -356,7 +356,7 @@ gp_status layernorm_bwd(int dtype, const float* dn, const float* x, const float*
 }
 
 gp_status colsum_finalize(const float* partial, int nblk, int width, float* out, int accumulate, hipStream_t st) {
-    colsum_kernel<<<(width + 63) / 64, 1024, 0, st>>>(partial, nblk, width, out, accumulate);
+    klaunch(colsum_kernel, (width + 63) / 64, 1024, 0, st, partial, nblk, width, out, accumulate);
     GP_LAUNCH_CHECK();
     return GP_OK;
 }
@@ -367,9 +367,9 @@ gp_status bias_grad(int dtype, const void* dy, long rows, int N, long ld, float*
     const long rpb = (rows + nb - 1) / nb;
     dim3 grid((N + 255) / 256, nb);
     if (dtype == GP_BF16)
-        bias_partial_kernel<bf16><<<grid, 256, 0, st>>>(reinterpret_cast<const bf16*>(dy), rows, N, ld, rpb, partial);
+        klaunch(bias_partial_kernel<bf16>, grid, 256, 0, st, reinterpret_cast<const bf16*>(dy), rows, N, ld, rpb, partial);
     else
-        bias_partial_kernel<float><<<grid, 256, 0, st>>>(reinterpret_cast<const float*>(dy), rows, N, ld, rpb, partial);
+        klaunch(bias_partial_kernel<float>, grid, 256, 0, st, reinterpret_cast<const float*>(dy), rows, N, ld, rpb, partial);
     GP_LAUNCH_CHECK();
     return colsum_finalize(partial, nb, N, out, accumulate, st);
 }

@@ -32,6 +32,9 @@
 namespace gp {
 
 static thread_local std::string g_err;
+static thread_local LaunchEvents g_launch_events;
+
+LaunchEvents& launch_events() { return g_launch_events; }
 
 gp_status set_error(gp_status s, const char* msg) {
     g_err = msg;
@@ -73,7 +76,7 @@ struct BwdWs {
     void *pe = nullptr, *qe = nullptr, *dz = nullptr, *dc = nullptr, *dqkv = nullptr, *dxq = nullptr, *dxkv = nullptr;
     double *loss_partial = nullptr, *loss_acc = nullptr;
     int* flag = nullptr;
-    float* splitk = nullptr;   // split-K partial tiles of the activation GEMMs
+    float* splitk = nullptr;   // split-K partial tiles
     long splitk_elems = 0;
     // loss head
     float* sth = nullptr;
@@ -83,6 +86,41 @@ struct BwdWs {
 } // namespace gp
 
 using namespace gp;
+
+// Event pairs around the launches of the selected role(s), with the roles'
+// algorithmic FLOPs and bytes.
+struct LaunchTimer {
+    int selected = GP_K_NONE;
+    bool markers = false;  // GP_TIMER_MARKERS=1: also launch role_marker around each timed launch
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> recs[GP_K_COUNT];
+    double flops[GP_K_COUNT] = {}, bytes[GP_K_COUNT] = {};
+    std::vector<hipEvent_t> pool;  // created events not in use
+    std::vector<hipEvent_t> all;   // every created event (destroyed with the partition)
+
+    bool on(int role) const {
+        return role > GP_K_NONE && role < GP_K_COUNT && (selected == GP_K_COUNT || selected == role);
+    }
+    gp_status take(hipEvent_t& e) {
+        if (pool.empty()) {
+            GP_HIP(hipEventCreate(&e));
+            all.push_back(e);
+        } else {
+            e = pool.back();
+            pool.pop_back();
+        }
+        return GP_OK;
+    }
+    void reset() {
+        for (int r = 0; r < GP_K_COUNT; ++r) {
+            for (auto& pr : recs[r]) {
+                pool.push_back(pr.first);
+                pool.push_back(pr.second);
+            }
+            recs[r].clear();
+            flops[r] = bytes[r] = 0.0;
+        }
+    }
+};
 
 struct gp_partition {
     Dims d;
@@ -100,9 +138,10 @@ struct gp_partition {
     std::vector<LayerWs> lw;
     BwdWs bw;
     size_t bytes_params = 0, bytes_grads = 0, bytes_stash = 0, bytes_ws = 0;
-    // GEMM tile-shape override (GP_GEMM_TILE = 0..3, GP_GEMM_SPLITS), read at
+    // GEMM tile-shape override (GP_GEMM_TILE = 0..10, GP_GEMM_SPLITS), read at
     // configure; -1 lets the library choose per problem.
     int gemm_tile = -1, gemm_splits = 0;
+    LaunchTimer timer;
 
     void* W(size_t elt_off) const { return welt + elt_off * esz; }
     char* stash_x_mb(int m) const { return stash_x + (size_t)m * g.T() * d.D * esz; }
@@ -169,7 +208,9 @@ void plan_workspace(gp_partition* p, Arena& a) {
         if (pm > part) part = pm;
     }
     b.partial = a.take<float>(part);
-    b.splitk_elems = 8 * T * D;
+    // split-K partials: up to 8 splits of a T x D activation GEMM or of the
+    // D x 3D packed-QKV weight gradient (with its bias column sums)
+    b.splitk_elems = std::max<long>(8 * T * D, 8 * (3 * D * D + 3 * D));
     b.splitk = a.take<float>((size_t)b.splitk_elems);
     size_t lp = (size_t)loss_blocks();
     if (g.loss == GP_LOSS_XENT_LS && (size_t)xent_partials(T) > lp) lp = xent_partials(T);
@@ -195,6 +236,75 @@ struct Ctx {
         if (s_ != GP_OK) return s_;  \
     } while (0)
 
+// Run `launch` (which enqueues on c.st); when `role` is being timed, bracket
+// it with two events on c.st and add its algorithmic work.
+template <class F>
+gp_status timed(const Ctx& c, int role, double flops, double bytes, F&& launch) {
+    LaunchTimer& t = c.p->timer;
+    if (!t.on(role)) return launch();
+    hipEvent_t e0, e1;
+    GP_TRY(t.take(e0));
+    GP_TRY(t.take(e1));
+    if (t.markers) GP_TRY(role_marker(role, 0, c.st));
+    // the events ride on the role's own kernel dispatches (klaunch)
+    LaunchEvents& ev = launch_events();
+    ev.start = e0;
+    ev.stop = e1;
+    ev.started = false;
+    const gp_status s = launch();
+    const bool launched = ev.started;
+    ev = LaunchEvents();
+    if (t.markers) GP_TRY(role_marker(role, 1, c.st));
+    if (launched) {
+        t.recs[role].emplace_back(e0, e1);
+        t.flops[role] += flops;
+        t.bytes[role] += bytes;
+    } else {
+        t.pool.push_back(e0);
+        t.pool.push_back(e1);
+    }
+    return s;
+}
+
+// Algorithmic bytes of a GEMM: operands read once, outputs written once (and
+// read once where the epilogue reads them).
+double gemm_bytes(const GemmArgs& g, int epi, size_t esz) {
+    const double mn = (double)g.M * g.N;
+    double b = ((double)g.M * g.K + (double)g.N * g.K) * (double)esz;
+    switch (epi) {
+    case EPI_STORE: b += mn * esz; break;
+    case EPI_RES_F32: b += mn * 8.0 + (g.C2 ? mn * esz : 0.0); break;
+    case EPI_F32: b += mn * 4.0; break;
+    case EPI_RELU_MASK: b += mn * 2.0 * esz; break;
+    case EPI_ACC_F32: b += mn * 4.0 * (g.accumulate ? 2.0 : 1.0) + (g.colsum ? g.N * 4.0 * (g.accumulate ? 2.0 : 1.0) : 0.0); break;
+    default: break;
+    }
+    return b;
+}
+
+gp_status timed_gemm(const Ctx& c, int role, const GemmArgs& g, int epi, bool kmaj) {
+    return timed(c, role, 2.0 * g.M * g.N * (double)g.K, gemm_bytes(g, epi, c.p->esz),
+                 [&] { return gemm(g, epi, kmaj, kmaj, c.dt, c.st); });
+}
+
+gp_status timed_attention(const Ctx& c, int role, const AttnArgs& a, bool bwd) {
+    const double f = 4.0 * a.n * a.H * (double)a.Sq * a.Sk * a.dh * (a.causal ? 0.5 : 1.0) * (bwd ? 2.0 : 1.0);
+    const double D = (double)a.H * a.dh, esz = (double)c.p->esz;
+    const double qo = (double)a.n * a.Sq * D * esz, kv = (double)a.n * a.Sk * D * esz;
+    const double stats = (double)a.n * a.H * a.Sq * 4.0;
+    // forward: Q, K, V in, O and the log-sum-exp out; backward: Q, K, V, O, dO
+    // and the log-sum-exp in, dQ, dK, dV out
+    const double by = bwd ? 3.0 * qo + 4.0 * kv + stats : 2.0 * qo + 2.0 * kv + stats;
+    return timed(c, role, f, by, [&] { return bwd ? attention_bwd(c.dt, a, c.st) : attention_fwd(c.dt, a, c.st); });
+}
+
+gp_status timed_ln_fwd(const Ctx& c, const float* x, long rows, int D, const float* gamma, const float* beta,
+                       float eps, void* out, float* stats) {
+    const double by = (double)rows * D * (4.0 + c.p->esz) + rows * 8.0 + D * 8.0;
+    return timed(c, GP_K_LN_FWD, 0.0, by,
+                 [&] { return layernorm_fwd(c.dt, x, rows, D, gamma, beta, eps, out, stats, c.st); });
+}
+
 // Y = A W + b with an epilogue; A [M, K] k-contiguous, W^T working copy [N, K].
 gp_status linear_fwd(const Ctx& c, const Linear& L, const void* A, long M, void* C, long ldc, int epi, int relu,
                      const float* res, void* C2) {
@@ -218,7 +328,7 @@ gp_status linear_fwd(const Ctx& c, const Linear& L, const void* A, long M, void*
     g.ws_elems = c.p->bw.splitk_elems;
     g.force_cfg = c.p->gemm_tile;
     g.force_splits = c.p->gemm_splits;
-    return gemm(g, epi, true, true, c.dt, c.st);
+    return timed_gemm(c, L.role, g, epi, true);
 }
 
 // dX = dY W^T with an epilogue; dY [M, out] k-contiguous, W working copy [in, out].
@@ -241,7 +351,7 @@ gp_status linear_dx(const Ctx& c, const Linear& L, const void* dY, long M, void*
     g.ws_elems = c.p->bw.splitk_elems;
     g.force_cfg = c.p->gemm_tile;
     g.force_splits = c.p->gemm_splits;
-    return gemm(g, epi, true, true, c.dt, c.st);
+    return timed_gemm(c, L.role + 1, g, epi, true);
 }
 
 // G_W (+)= X^T dY and G_b (+)= sum_rows dY (one kernel).  X [rows, in], dY [rows, out].
@@ -257,17 +367,25 @@ gp_status linear_dw(const Ctx& c, const Linear& L, const void* X, const void* dY
     g.C = c.p->grads + L.w;
     g.ldc = L.out;
     g.accumulate = accumulate;
+    g.ws = c.p->bw.splitk;
+    g.ws_elems = c.p->bw.splitk_elems;
     g.force_cfg = c.p->gemm_tile;
+    g.force_splits = c.p->gemm_splits;
     g.colsum = c.p->grads + L.b;  // bias gradient fused into the GEMM
-    return gemm(g, EPI_ACC_F32, false, false, c.dt, c.st);
+    return timed_gemm(c, L.role + 2, g, EPI_ACC_F32, false);
 }
 
 gp_status norm_bwd(const Ctx& c, const Norm& N, const float* dn, const float* x, const float* stats, long rows,
                    const float* dres, float* dx32, void* dxe, int accumulate) {
     int nblk = 0;
-    GP_TRY(layernorm_bwd(c.dt, dn, x, stats, c.p->master + N.g, rows, N.n, dres, dx32, dxe, c.p->bw.partial, &nblk,
-                         c.st));
-    return colsum_finalize(c.p->bw.partial, nblk, 2 * N.n, c.p->grads + N.g, accumulate, c.st);
+    const double rd = (double)rows * N.n;
+    const double by = rd * (8.0 + (dres ? 4.0 : 0.0) + (dx32 ? 4.0 : 0.0) + (dxe ? (double)c.p->esz : 0.0)) +
+                      rows * 8.0 + N.n * 4.0 * (accumulate ? 4.0 : 2.0);
+    return timed(c, GP_K_LN_BWD, 0.0, by, [&] {
+        GP_TRY(layernorm_bwd(c.dt, dn, x, stats, c.p->master + N.g, rows, N.n, dres, dx32, dxe, c.p->bw.partial,
+                             &nblk, c.st));
+        return colsum_finalize(c.p->bw.partial, nblk, 2 * N.n, c.p->grads + N.g, accumulate, c.st);
+    });
 }
 
 AttnArgs attn_args(const gp_partition* p, int Sk, int causal) {
@@ -293,7 +411,7 @@ gp_status layer_forward(const Ctx& c, int l, LayerWs& w, const float* x_in, floa
     const bool dec = p->g.kind == GP_DECODER_CROSS;
     const float eps = p->g.eps;
     // self-attention block
-    GP_TRY(layernorm_fwd(c.dt, x_in, T, (int)D, p->master + P.ln1.g, p->master + P.ln1.b, eps, w.u, w.st1, c.st));
+    GP_TRY(timed_ln_fwd(c, x_in, T, (int)D, p->master + P.ln1.g, p->master + P.ln1.b, eps, w.u, w.st1));
     GP_TRY(linear_fwd(c, P.qkv, w.u, T, w.qkv, 3 * D, EPI_STORE, 0, nullptr, nullptr));
     AttnArgs a = attn_args(p, p->g.S, dec ? 1 : 0);
     a.q = w.qkv;
@@ -303,12 +421,12 @@ gp_status layer_forward(const Ctx& c, int l, LayerWs& w, const float* x_in, floa
     a.o = w.c;
     a.ldo = D;
     a.lse = w.lse;
-    GP_TRY(attention_fwd(c.dt, a, c.st));
+    GP_TRY(timed_attention(c, GP_K_ATTN_FWD, a, false));
     GP_TRY(linear_fwd(c, P.o, w.c, T, w.x1, D, EPI_RES_F32, 0, x_in, nullptr));
     const float* xf = w.x1;
     if (dec) {
         // cross-attention block: queries from LN2(x1), keys/values from the memory
-        GP_TRY(layernorm_fwd(c.dt, w.x1, T, (int)D, p->master + P.ln2.g, p->master + P.ln2.b, eps, w.uc, w.stc, c.st));
+        GP_TRY(timed_ln_fwd(c, w.x1, T, (int)D, p->master + P.ln2.g, p->master + P.ln2.b, eps, w.uc, w.stc));
         GP_TRY(linear_fwd(c, P.xq, w.uc, T, w.xq, D, EPI_STORE, 0, nullptr, nullptr));
         GP_TRY(linear_fwd(c, P.xkv, mem, p->g.Tm(), w.xkv, 2 * D, EPI_STORE, 0, nullptr, nullptr));
         AttnArgs x = attn_args(p, p->g.Smem, 0);
@@ -320,13 +438,13 @@ gp_status layer_forward(const Ctx& c, int l, LayerWs& w, const float* x_in, floa
         x.o = w.xc;
         x.ldo = D;
         x.lse = w.xlse;
-        GP_TRY(attention_fwd(c.dt, x, c.st));
+        GP_TRY(timed_attention(c, GP_K_XATTN_FWD, x, false));
         GP_TRY(linear_fwd(c, P.xo, w.xc, T, w.x2, D, EPI_RES_F32, 0, w.x1, nullptr));
         xf = w.x2;
     }
     // feed-forward block
     const Norm& nf = dec ? P.ln3 : P.ln2;
-    GP_TRY(layernorm_fwd(c.dt, xf, T, (int)D, p->master + nf.g, p->master + nf.b, eps, w.v, w.stf, c.st));
+    GP_TRY(timed_ln_fwd(c, xf, T, (int)D, p->master + nf.g, p->master + nf.b, eps, w.v, w.stf));
     GP_TRY(linear_fwd(c, P.ffn1, w.v, T, w.a, p->d.F, EPI_STORE, 1, nullptr, nullptr));
     GP_TRY(linear_fwd(c, P.ffn2, w.a, T, x_out, D, EPI_RES_F32, 0, xf, y_out));
     return GP_OK;
@@ -400,7 +518,7 @@ gp_status layer_backward(const Ctx& c, int l, bool first, float* in32, void* ine
         x.dv = p->off_elt(b.dxkv, D);
         x.lddk = x.lddv = 2 * D;
         x.delta = b.delta;
-        GP_TRY(attention_bwd(c.dt, x, c.st));
+        GP_TRY(timed_attention(c, GP_K_XATTN_BWD, x, true));
         GP_TRY(linear_dw(c, P.xq, w.uc, b.dxq, T, acc));
         GP_TRY(linear_dx(c, P.xq, b.dxq, T, b.dn, EPI_F32, nullptr, 0));
         GP_TRY(linear_dw(c, P.xkv, mem, b.dxkv, Tm, acc));
@@ -427,7 +545,7 @@ gp_status layer_backward(const Ctx& c, int l, bool first, float* in32, void* ine
     a.dv = p->off_elt(b.dqkv, 2 * D);
     a.lddq = a.lddk = a.lddv = 3 * D;
     a.delta = b.delta;
-    GP_TRY(attention_bwd(c.dt, a, c.st));
+    GP_TRY(timed_attention(c, GP_K_ATTN_BWD, a, true));
     GP_TRY(linear_dw(c, P.qkv, w.u, b.dqkv, T, acc));
     GP_TRY(linear_dx(c, P.qkv, b.dqkv, T, b.dn, EPI_F32, nullptr, 0));
     const float* x_in = p->xs[l];
@@ -450,7 +568,7 @@ gp_status head_backward(const Ctx& c, bool first, const int* labels) {
     const long T = p->g.T(), D = p->d.D, V = p->g.V;
     const int acc = first ? 0 : 1;
     const float* y = p->xs[p->d.L];
-    GP_TRY(layernorm_fwd(c.dt, y, T, (int)D, p->master + Hd.lnf.g, p->master + Hd.lnf.b, p->g.eps, b.h, b.sth, c.st));
+    GP_TRY(timed_ln_fwd(c, y, T, (int)D, p->master + Hd.lnf.g, p->master + Hd.lnf.b, p->g.eps, b.h, b.sth));
     GP_TRY(linear_fwd(c, Hd.out, b.h, T, b.z, V, EPI_STORE, 0, nullptr, nullptr));
     const double norm = (double)p->g.n * p->g.M * p->g.S;
     GP_TRY(xent_ls(c.dt, b.z, T, (int)V, labels, p->g.ls, norm, b.loss_partial, c.st));
@@ -472,6 +590,10 @@ gp_status upload_param_block(gp_partition* p, const ParamRef& r, const float* ho
 }
 
 void free_all(gp_partition* p) {
+    for (hipEvent_t e : p->timer.all) (void)hipEventDestroy(e);
+    const bool markers = p->timer.markers;
+    p->timer = LaunchTimer();
+    p->timer.markers = markers;
     for (void* x : {(void*)p->master, (void*)p->grads, (void*)p->welt, (void*)p->stash_x, (void*)p->stash_m,
                     (void*)p->ws})
         if (x) (void)hipFree(x);
@@ -531,6 +653,7 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
     g.eps = cfg->ln_eps;
     g.check_finite = cfg->check_finite;
     p->esz = g.dtype == GP_BF16 ? 2 : 4;
+    if (const char* e = std::getenv("GP_TIMER_MARKERS")) p->timer.markers = std::atoi(e) != 0;
     if (const char* e = std::getenv("GP_GEMM_TILE")) p->gemm_tile = std::atoi(e);
     if (const char* e = std::getenv("GP_GEMM_SPLITS")) p->gemm_splits = std::atoi(e);
     p->plan = plan_params(p->d, g);
@@ -623,6 +746,37 @@ gp_status gp_get_param(gp_partition* p, int layer, int id, float* host, size_t c
 }
 gp_status gp_get_grad(gp_partition* p, int layer, int id, float* host, size_t count) {
     return param_io(p, layer, id, host, count, 2);
+}
+
+gp_status gp_timer_select(gp_partition* p, int role) {
+    if (!p) return set_error(GP_ERR_INVALID_ARG, "partition must not be NULL");
+    if (role < GP_K_NONE || role > GP_K_COUNT) return set_error(GP_ERR_INVALID_ARG, "timer role out of range");
+    p->timer.selected = role;
+    return GP_OK;
+}
+
+gp_status gp_timer_read(gp_partition* p, int role, double* ms, long* launches, double* flops, double* bytes) {
+    if (!p) return set_error(GP_ERR_INVALID_ARG, "partition must not be NULL");
+    if (role <= GP_K_NONE || role >= GP_K_COUNT) return set_error(GP_ERR_INVALID_ARG, "timer role out of range");
+    const auto& recs = p->timer.recs[role];
+    double total = 0.0;
+    if (!recs.empty()) GP_HIP(hipEventSynchronize(recs.back().second));
+    for (const auto& pr : recs) {
+        float t = 0.f;
+        GP_HIP(hipEventElapsedTime(&t, pr.first, pr.second));
+        total += t;
+    }
+    if (ms) *ms = total;
+    if (launches) *launches = (long)recs.size();
+    if (flops) *flops = p->timer.flops[role];
+    if (bytes) *bytes = p->timer.bytes[role];
+    return GP_OK;
+}
+
+gp_status gp_timer_reset(gp_partition* p) {
+    if (!p) return set_error(GP_ERR_INVALID_ARG, "partition must not be NULL");
+    p->timer.reset();
+    return GP_OK;
 }
 
 gp_status gp_partition_memory(gp_partition* p, size_t* params, size_t* grads, size_t* stash, size_t* workspace) {

@@ -93,6 +93,7 @@ struct Linear {
     size_t w = 0, b = 0;        // float offsets of W and bias in master/grad
     size_t kn = 0, nk = 0;      // element offsets of the working copies
     int in = 0, out = 0;
+    int role = 0;               // gp_kernel_role of its forward GEMM; +1 input gradient, +2 weight gradient
     bool present = false;
 };
 struct Norm {
@@ -137,8 +138,9 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 inline ParamPlan plan_params(const Dims& d, const Geometry& g) {
     ParamPlan p;
     size_t f = 0, e = 0;
-    auto lin = [&](Linear& x, int in, int out) {
+    auto lin = [&](Linear& x, int in, int out, int role) {
         x.present = true;
+        x.role = role;
         x.in = in;
         x.out = out;
         x.w = f;
@@ -161,21 +163,21 @@ inline ParamPlan plan_params(const Dims& d, const Geometry& g) {
     p.layers.resize(d.L);
     for (auto& l : p.layers) {
         norm(l.ln1, d.D);
-        lin(l.qkv, d.D, 3 * d.D);
-        lin(l.o, d.D, d.D);
+        lin(l.qkv, d.D, 3 * d.D, GP_K_QKV_FWD);
+        lin(l.o, d.D, d.D, GP_K_O_FWD);
         norm(l.ln2, d.D);
-        lin(l.ffn1, d.D, d.F);
-        lin(l.ffn2, d.F, d.D);
+        lin(l.ffn1, d.D, d.F, GP_K_FFN1_FWD);
+        lin(l.ffn2, d.F, d.D, GP_K_FFN2_FWD);
         if (dec) {
-            lin(l.xq, d.D, d.D);
-            lin(l.xkv, d.D, 2 * d.D);
-            lin(l.xo, d.D, d.D);
+            lin(l.xq, d.D, d.D, GP_K_XQ_FWD);
+            lin(l.xkv, d.D, 2 * d.D, GP_K_XKV_FWD);
+            lin(l.xo, d.D, d.D, GP_K_XO_FWD);
             norm(l.ln3, d.D);
         }
     }
     if (g.loss == GP_LOSS_XENT_LS) {
         norm(p.head.lnf, d.D);
-        lin(p.head.out, d.D, g.V);
+        lin(p.head.out, d.D, g.V, GP_K_HEAD_FWD);
     }
     p.n32 = f;
     p.nelt = e;

@@ -26,9 +26,18 @@ PARAM_IDS = ["ln1_g", "ln1_b", "wq", "bq", "wk", "bk", "wv", "bv", "wo", "bo", "
              "ln3_g", "ln3_b", "lnf_g", "lnf_b", "wout", "bout"]
 PARAM_ID = {name: i for i, name in enumerate(PARAM_IDS)}
 
+# gp_kernel_role: launch roles of the timers
+KERNEL_ROLES = ["none", "qkv.fwd", "qkv.dx", "qkv.dw", "o.fwd", "o.dx", "o.dw", "ffn1.fwd", "ffn1.dx", "ffn1.dw",
+                "ffn2.fwd", "ffn2.dx", "ffn2.dw", "xq.fwd", "xq.dx", "xq.dw", "xkv.fwd", "xkv.dx", "xkv.dw",
+                "xo.fwd", "xo.dx", "xo.dw", "head.fwd", "head.dx", "head.dw", "attn.fwd", "attn.bwd",
+                "xattn.fwd", "xattn.bwd", "ln.fwd", "ln.bwd"]
+KERNEL_ROLE = {name: i for i, name in enumerate(KERNEL_ROLES)}
+GP_K_NONE, GP_K_COUNT = 0, len(KERNEL_ROLES)
+
 EXPORTS = ["gp_partition_create", "gp_partition_configure", "gp_partition_destroy", "gp_set_param",
            "gp_get_param", "gp_get_grad", "gp_partition_memory", "gp_param_count", "gp_forward_microbatch",
-           "gp_backward_microbatch_remat", "gp_accumulate_and_step", "gp_last_error"]
+           "gp_backward_microbatch_remat", "gp_accumulate_and_step", "gp_timer_select", "gp_timer_read",
+           "gp_timer_reset", "gp_last_error"]
 
 
 class gp_config(ctypes.Structure):
@@ -68,6 +77,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.gp_forward_microbatch.argtypes = [P, I, VP, VP, VP, VP]
     lib.gp_backward_microbatch_remat.argtypes = [P, I, VP, VP, VP, VP]
     lib.gp_accumulate_and_step.argtypes = [P, ctypes.c_float, ctypes.POINTER(ctypes.c_double), VP]
+    D = ctypes.POINTER(ctypes.c_double)
+    lib.gp_timer_select.argtypes = [P, I]
+    lib.gp_timer_read.argtypes = [P, I, D, ctypes.POINTER(ctypes.c_long), D, D]
+    lib.gp_timer_reset.argtypes = [P]
     lib.gp_last_error.argtypes = []
     lib.gp_last_error.restype = ctypes.c_char_p
     for name in EXPORTS:
@@ -145,3 +158,19 @@ def gp_accumulate_and_step(h, lr, want_loss, stream):
         return v.value
     _check(load().gp_accumulate_and_step(h, lr, None, stream))
     return None
+
+
+def gp_timer_select(h, role):
+    _check(load().gp_timer_select(h, role))
+
+
+def gp_timer_read(h, role):
+    """(milliseconds, launches, FLOPs, bytes) of one launch role."""
+    ms, fl, by = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    n = ctypes.c_long()
+    _check(load().gp_timer_read(h, role, ctypes.byref(ms), ctypes.byref(n), ctypes.byref(fl), ctypes.byref(by)))
+    return ms.value, n.value, fl.value, by.value
+
+
+def gp_timer_reset(h):
+    _check(load().gp_timer_reset(h))

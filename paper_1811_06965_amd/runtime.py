@@ -137,3 +137,16 @@ class Partition:
             gp.gp_backward_microbatch_remat(self.h, m, ptr(dys[m]), ptr(dxs[m]), ptr(dms[m]), st)
         loss = gp.gp_accumulate_and_step(self.h, lr, want_loss, st)
         return {"y": y, "dx": dx, "dmem": dmem, "loss": loss}
+
+    # ------------------------------------------------------------ timers
+    def timer_select(self, role):
+        """role: a name from gp.KERNEL_ROLES, "all", or None to stop."""
+        r = gp.GP_K_NONE if role is None else gp.GP_K_COUNT if role == "all" else gp.KERNEL_ROLE[role]
+        gp.gp_timer_select(self.h, r)
+
+    def timer_read(self, role):
+        ms, n, flops, nbytes = gp.gp_timer_read(self.h, gp.KERNEL_ROLE[role])
+        return {"ms": ms, "launches": n, "flops": flops, "bytes": nbytes}
+
+    def timer_reset(self):
+        gp.gp_timer_reset(self.h)

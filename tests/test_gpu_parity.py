@@ -235,11 +235,18 @@ def test_call_order_is_enforced():
         torch.cuda.synchronize()
 
 
-@pytest.mark.parametrize("tile,splits", [(0, 1), (1, 1), (2, 1), (3, 1), (0, 4), (3, 2)],
-                         ids=["256x256", "256x128", "128x256", "128x128", "256x256_split4", "128x128_split2"])
+TILE_CASES = [(0, 1), (1, 1), (2, 1), (3, 1), (0, 4), (3, 2),
+              (4, 1), (5, 1), (6, 1), (7, 1), (8, 1), (9, 1), (10, 1), (4, 2), (8, 4), (10, 4)]
+TILE_IDS = ["256x256", "256x128", "128x256", "128x128", "256x256_split4", "128x128_split2",
+            "dl128x128", "dl128x128_3stage", "dl256x128", "dl256x256", "dl256x256_8w", "dl256x128_8w",
+            "dl128x256_8w", "dl128x128_split2", "dl256x256_8w_split4", "dl128x256_8w_split4"]
+
+
+@pytest.mark.parametrize("tile,splits", TILE_CASES, ids=TILE_IDS)
 def test_bf16_every_gemm_tile_shape(tile, splits, monkeypatch):
     """Every MFMA tile shape and the split-K path, forced for all GEMMs, on the
-    ragged-row bf16 partition (tile edges in M, N and K)."""
+    ragged-row bf16 partition (tile edges in M and N; K a multiple of 64 for
+    the direct-to-LDS shapes, which the weight-gradient GEMMs do not use)."""
     monkeypatch.setenv("GP_GEMM_TILE", str(tile))
     monkeypatch.setenv("GP_GEMM_SPLITS", str(splits))
     case, ref, res = _run(RAGGED_BF16, 3, perturb=False)

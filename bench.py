@@ -7,11 +7,16 @@ operands with fp32 accumulation, random N(0,1) boundary inputs and boundary
 gradients, Xavier-uniform weights (synthetic data).
 
 One step = M x gp_forward_microbatch + M x gp_backward_microbatch_remat +
-gp_accumulate_and_step (GPipe, Sections 2.2-2.3), all enqueued on one stream.
-W untimed warm-up steps, one untimed census step that times every launch role
-to find the dominant one, then K steps timed between two synchronisations
-with only the dominant role's launches bracketed by HIP events (on the launch
-stream) for the roofline figure.  Prints one JSON line.
+gp_accumulate_and_step (GPipe, Sections 2.2-2.3), enqueued on the caller's
+stream (the library runs the weight-gradient GEMMs on a second stream it
+joins before each call returns).  W untimed warm-up steps, one untimed census
+step that times every launch role to find the dominant one, then K steps
+timed between two events on the launch stream.  By default the step is
+captured once into a HIP graph and the K steps are graph replays (the launch
+overhead of thousands of small kernels per step is then off the host); the
+dominant role's launches are then timed with dispatch events over a few eager
+steps right after.  --eager times eager steps with the role bracketed inside
+the timed region.  Prints one JSON line.
 """
 import argparse
 import hashlib
@@ -42,6 +47,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=16, help="layers in the oracle's timed sample")
     ap.add_argument("--role", default=None, help="time this launch role instead of the dominant one")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of the step captured once into a HIP graph instead of eager steps "
+                         "(the dominant role is then timed over eager steps right after)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (calibrates the PMC byte counters)")
     ap.add_argument("--traffic-summary", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CAL_FETCH_DIR", "CAL_WRITE_DIR"),
@@ -222,15 +230,11 @@ def census(part, inp, dx):
     return dict(sorted(roles.items(), key=lambda kv: -kv[1]["ms"]))
 
 
-def time_steps(part, inp, steps, warmup, role=None):
+def timed_eager(part, inp, steps, dx, role):
+    """K eager steps between two events on the launch stream, with the role's
+    launches bracketed by dispatch events."""
     import torch
     st = torch.cuda.current_stream()
-    dx = torch.empty_like(inp["x"])
-    run_steps(part, inp, warmup, dx)
-    torch.cuda.synchronize()
-    roles = census(part, inp, dx) if role is None else None
-    if role is None:
-        role = next(iter(roles))
     part.timer_reset()
     part.timer_select(role)
     t0 = torch.cuda.Event(enable_timing=True)
@@ -243,7 +247,43 @@ def time_steps(part, inp, steps, warmup, role=None):
     part.timer_select(None)
     timed = part.timer_read(role)
     part.timer_reset()
-    return t0.elapsed_time(t1) / steps, role, timed, roles
+    return t0.elapsed_time(t1) / steps, timed
+
+
+def timed_graph(part, inp, steps, dx):
+    """The step captured once into a HIP graph, then K replays between two
+    events on the replay stream."""
+    import torch
+    g = part.capture_step(inp["x"], inp["mem"], inp["dy"], lr=0.0, dx=dx)
+    g.replay()
+    torch.cuda.synchronize()
+    st = torch.cuda.current_stream()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(st)
+    for _ in range(steps):
+        g.replay()
+    t1.record(st)
+    torch.cuda.synchronize()
+    del g
+    return t0.elapsed_time(t1) / steps
+
+
+def time_steps(part, inp, steps, warmup, role=None, graph=False):
+    """Returns (ms per step, role, role timings, census, how the role was timed)."""
+    import torch
+    dx = torch.empty_like(inp["x"])
+    run_steps(part, inp, warmup, dx)
+    torch.cuda.synchronize()
+    roles = census(part, inp, dx) if role is None else None
+    if role is None:
+        role = next(iter(roles))
+    if not graph:
+        ms, timed = timed_eager(part, inp, steps, dx, role)
+        return ms, role, timed, roles, "dispatch events over the timed eager steps"
+    ms = timed_graph(part, inp, steps, dx)
+    _, timed = timed_eager(part, inp, max(1, min(steps, 3)), dx, role)
+    return ms, role, timed, roles, "dispatch events over eager steps run after the graph-replay timed region"
 
 
 def source_digest():
@@ -353,14 +393,14 @@ def main():
         with Partition(c) as part:
             part.load_params(case["layers"], case["head"])
             inp = part.device_inputs(case)
-            ms, role, timed, roles = time_steps(part, inp, a.steps if M == a.micro else max(3, a.steps // 2),
-                                                a.warmup, a.role)
+            ms, role, timed, roles, how = time_steps(part, inp, a.steps if M == a.micro else max(3, a.steps // 2),
+                                                     a.warmup, a.role, graph=a.graph)
             mem = part.memory()
             del inp
         model, hw = accounting.step_flops(c)
         results[M] = {"M": M, "ms_per_step": ms, "tokens_per_s": c.batch * c.seq / (ms * 1e-3),
                       "hfu": hw / (ms * 1e-3) / PEAK_BF16, "mfu": model / (ms * 1e-3) / PEAK_BF16,
-                      "memory_bytes": mem, "role": role, "timed": timed, "roles": roles}
+                      "memory_bytes": mem, "role": role, "timed": timed, "roles": roles, "how": how}
         print(f"[bench] M={M}: {ms:.2f} ms/step, {results[M]['tokens_per_s']:.0f} tokens/s, "
               f"HFU {100 * results[M]['hfu']:.1f}%, dominant role {role}", file=sys.stderr, flush=True)
     r = results[a.micro]
@@ -372,7 +412,9 @@ def main():
                    "parallelism": "one pipeline partition on one GPU"},
         "hfu": r["hfu"], "mfu": r["mfu"],
         "roofline": roofline(r["role"], r["timed"], workload),
+        "launch": "HIP graph: the whole step captured once, replayed" if a.graph else "eager (host-enqueued launches)",
     }
+    out["roofline"]["timing"] = r["how"]
     if r["roles"]:
         step_ms = r["ms_per_step"]
         out["roles_ms_per_step"] = {k: round(v["ms"], 3) for k, v in r["roles"].items()}

@@ -69,6 +69,7 @@ template <> struct Vec16<float> {
     } while (0)
 
 #include <hip/hip_ext.h>
+#include <tuple>
 #include "../../include/gp.h"
 namespace gp {
 gp_status hip_fail(hipError_t e, const char* file, int line);
@@ -84,16 +85,28 @@ struct LaunchEvents {
 };
 LaunchEvents& launch_events();
 
-// Kernel launch through hipExtLaunchKernelGGL, attaching the timing events
-// when a role is being timed (no extra stream packets).
+// Kernel launch.  While a role is timed, through hipExtLaunchKernelGGL with
+// the timing events attached to the dispatch (no extra stream packets);
+// otherwise a plain hipLaunchKernel (which stream capture records as an
+// ordinary kernel node).
 template <typename... Args, typename... P>
 inline void klaunch(void (*k)(Args...), dim3 grid, dim3 block, uint32_t shmem, hipStream_t st, P... p) {
     LaunchEvents& ev = launch_events();
-    hipEvent_t e0 = nullptr;
-    if (ev.stop && !ev.started) {
-        e0 = ev.start;
-        ev.started = true;
+    if (ev.stop) {
+        hipEvent_t e0 = nullptr;
+        if (!ev.started) {
+            e0 = ev.start;
+            ev.started = true;
+        }
+        hipExtLaunchKernelGGL(k, grid, block, shmem, st, e0, ev.stop, 0u, static_cast<Args>(p)...);
+        return;
     }
-    hipExtLaunchKernelGGL(k, grid, block, shmem, st, e0, ev.stop, 0u, static_cast<Args>(p)...);
+    auto args = std::make_tuple(static_cast<Args>(p)...);
+    void* ptrs[sizeof...(Args) > 0 ? sizeof...(Args) : 1];
+    std::apply([&](auto&... a) {
+        int i = 0;
+        ((ptrs[i++] = static_cast<void*>(&a)), ...);
+    }, args);
+    (void)hipLaunchKernel(reinterpret_cast<const void*>(k), grid, block, ptrs, shmem, st);
 }
 }

@@ -581,17 +581,38 @@ __device__ __forceinline__ void dl_epilogue_full(const GemmArgs& a, const f32x16
     }
 }
 
-// Direct-to-LDS GEMM (requires K % 64 == 0).  Address arithmetic is hoisted:
-// each lane's global offsets are computed once and the k advance rides in the
-// scalar offset of the buffer load; M0 (the LDS destination) is wave-uniform;
-// fragment addresses are precomputed per k-step and the stage base is folded
-// into the ds_read immediate by unrolling the k-tile loop over the stages.
-template <int BM, int BN, int WM, int WN, int NSTAGE, int EPI, bool SPLIT>
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16* LdsV4;
+
+// Two transposing LDS reads (ds_read_b64_tr_b16) make one bf16 MFMA fragment
+// from a k-row-major tile: each gives the lane 4 consecutive k of its m.
+__device__ __forceinline__ bf16x8 tr_frag(const char* p, int second) {
+    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LdsV4)(p));
+    const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LdsV4)(p + second));
+    const bf16x4 a = __builtin_bit_cast(bf16x4, lo), b = __builtin_bit_cast(bf16x4, hi);
+    return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+}
+
+// Direct-to-LDS GEMM (requires K % 64 == 0).  KM: both operands k-contiguous
+// (A[m lda + k], B[n ldb + k]: forward and input-gradient GEMMs); else both
+// m/n-contiguous (A[k lda + m], B[k ldb + n]: weight-gradient GEMMs, read as
+// the activations are stored).
+//   KM:  a stage holds rows of 64 k (128 bytes) per m, 16-byte chunks
+//        XOR-swizzled by swz(row); fragments are plain 16-byte LDS reads.
+//   !KM: a stage holds rows of W m-values per k (2W bytes), 16-byte chunk c of
+//        row k stored at c ^ 4 (k % 4); fragments come from transposing reads
+//        (tr_frag), whose four k-rows then fall in distinct bank groups.
+// Address arithmetic is hoisted: each lane's global offsets are computed once
+// and the k advance rides in the scalar offset of the buffer load; M0 (the LDS
+// destination) is wave-uniform; fragment offsets are precomputed and the stage
+// base folds into the ds_read immediate because the k-tile loop is unrolled
+// over the stages.
+template <int BM, int BN, int WM, int WN, int NSTAGE, int EPI, bool SPLIT, bool KM>
 __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
     constexpr int BK = 64, KS = 4, NW = WM * WN;
     constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
     constexpr int STAGE = (BM + BN) * 128;
-    constexpr int PA = BM / (8 * NW), PB = BN / (8 * NW);  // 8-row load blocks per wave for A and B
+    constexpr int PA = BM / (8 * NW), PB = BN / (8 * NW);  // 1 KB load blocks per wave for A and B
     static_assert(PA * 8 * NW == BM && PB * 8 * NW == BN, "load blocks");
     constexpr int LPW = PA + PB;               // load instructions per wave per k-tile
     __shared__ __attribute__((aligned(1024))) char smem[NSTAGE * STAGE];
@@ -616,25 +637,49 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
     }
     const int nkt = kt1 - kt0;
 
-    const Rsrc A = make_rsrc(args.A, (uint32_t)(((long)(args.M - 1) * args.lda + args.K) * 2));
-    const Rsrc B = make_rsrc(args.B, (uint32_t)(((long)(args.N - 1) * args.ldb + args.K) * 2));
+    Rsrc A, B;
     uint32_t voa[PA], vob[PB];
+    int ka, kb;  // bytes per k-tile advance of A and B
+    if constexpr (KM) {
+        A = make_rsrc(args.A, (uint32_t)(((long)(args.M - 1) * args.lda + args.K) * 2));
+        B = make_rsrc(args.B, (uint32_t)(((long)(args.N - 1) * args.ldb + args.K) * 2));
 #pragma unroll
-    for (int i = 0; i < PA; ++i) {
-        const int r = (wave * PA + i) * 8 + (lane >> 3);
-        const int row = m0 + r;
-        voa[i] = row < args.M ? (uint32_t)(((long)row * args.lda + ((lane & 7) ^ swz(r)) * 8) * 2) : OOB;
-    }
+        for (int i = 0; i < PA; ++i) {
+            const int r = (wave * PA + i) * 8 + (lane >> 3);
+            const int row = m0 + r;
+            voa[i] = row < args.M ? (uint32_t)(((long)row * args.lda + ((lane & 7) ^ swz(r)) * 8) * 2) : OOB;
+        }
 #pragma unroll
-    for (int i = 0; i < PB; ++i) {
-        const int r = (wave * PB + i) * 8 + (lane >> 3);
-        const int row = n0 + r;
-        vob[i] = row < args.N ? (uint32_t)(((long)row * args.ldb + ((lane & 7) ^ swz(r)) * 8) * 2) : OOB;
+        for (int i = 0; i < PB; ++i) {
+            const int r = (wave * PB + i) * 8 + (lane >> 3);
+            const int row = n0 + r;
+            vob[i] = row < args.N ? (uint32_t)(((long)row * args.ldb + ((lane & 7) ^ swz(r)) * 8) * 2) : OOB;
+        }
+        ka = kb = BK * 2;
+    } else {
+        A = make_rsrc(args.A, (uint32_t)(((long)(args.K - 1) * args.lda + args.M) * 2));
+        B = make_rsrc(args.B, (uint32_t)(((long)(args.K - 1) * args.ldb + args.N) * 2));
+#pragma unroll
+        for (int i = 0; i < PA; ++i) {
+            const int pos = (wave * PA + i) * 1024 + 16 * lane;
+            const int k = pos / (2 * BM), c = ((pos % (2 * BM)) >> 4) ^ ((k & 3) << 2);
+            const int m = m0 + 8 * c;
+            voa[i] = m < args.M ? (uint32_t)(((long)k * args.lda + m) * 2) : OOB;
+        }
+#pragma unroll
+        for (int i = 0; i < PB; ++i) {
+            const int pos = (wave * PB + i) * 1024 + 16 * lane;
+            const int k = pos / (2 * BN), c = ((pos % (2 * BN)) >> 4) ^ ((k & 3) << 2);
+            const int n = n0 + 8 * c;
+            vob[i] = n < args.N ? (uint32_t)(((long)k * args.ldb + n) * 2) : OOB;
+        }
+        ka = (int)(BK * args.lda * 2);
+        kb = (int)(BK * args.ldb * 2);
     }
 #define GP_DL_ISSUE(t, st)                                                                   \
     do {                                                                                     \
-        dl_load_blocks<PA>(A, voa, (t) * (BK * 2), (st) + wave * PA * 1024);                 \
-        dl_load_blocks<PB>(B, vob, (t) * (BK * 2), (st) + BM * 128 + wave * PB * 1024);      \
+        dl_load_blocks<PA>(A, voa, (t) * ka, (st) + wave * PA * 1024);                       \
+        dl_load_blocks<PB>(B, vob, (t) * kb, (st) + BM * 128 + wave * PB * 1024);            \
     } while (0)
 
     f32x16 acc[TM][TN];
@@ -648,26 +693,62 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
     // fragment byte offsets within a stage, per k-step
     const int fr = lane & 31, h = lane >> 5;
     int fa_off[KS][TM], fb_off[KS][TN];
+    if constexpr (KM) {
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
+        for (int s = 0; s < KS; ++s) {
 #pragma unroll
-        for (int i = 0; i < TM; ++i) {
-            const int row = wm * (BM / WM) + i * 32 + fr;
-            fa_off[s][i] = row * 128 + (((2 * s + h) ^ swz(row)) << 4);
+            for (int i = 0; i < TM; ++i) {
+                const int row = wm * (BM / WM) + i * 32 + fr;
+                fa_off[s][i] = row * 128 + (((2 * s + h) ^ swz(row)) << 4);
+            }
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int row = wn * (BN / WN) + j * 32 + fr;
+                fb_off[s][j] = BM * 128 + row * 128 + (((2 * s + h) ^ swz(row)) << 4);
+            }
         }
+    } else {
+        // lane l of a 16-lane group g = l / 16 addresses k-row 8 (g / 2) + (l % 16) / 4
+        // and m 16 (g % 2) + 4 (l % 4) of its fragment (plus 4 k-rows for the second read)
+        const int g = lane >> 4, q = lane & 15;
+        const int kr = 8 * (g >> 1) + (q >> 2), mo = 16 * (g & 1) + 4 * (q & 3);
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int row = wn * (BN / WN) + j * 32 + fr;
-            fb_off[s][j] = BM * 128 + row * 128 + (((2 * s + h) ^ swz(row)) << 4);
+        for (int s = 0; s < KS; ++s) {
+            const int k = 16 * s + kr;
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const int m = wm * (BM / WM) + i * 32 + mo;
+                fa_off[s][i] = k * (2 * BM) + ((((m >> 3) ^ ((k & 3) << 2))) << 4) + (m & 7) * 2;
+            }
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int n = wn * (BN / WN) + j * 32 + mo;
+                fb_off[s][j] = BM * 128 + k * (2 * BN) + ((((n >> 3) ^ ((k & 3) << 2))) << 4) + (n & 7) * 2;
+            }
         }
     }
     Frag<bf16> fa[2][TM], fb[2][TN];
     auto load_frags = [&](int slot, const char* stg, int s) {
+        if constexpr (KM) {
 #pragma unroll
-        for (int i = 0; i < TM; ++i) fa[slot][i].v = *reinterpret_cast<const bf16x8*>(stg + fa_off[s][i]);
+            for (int i = 0; i < TM; ++i) fa[slot][i].v = *reinterpret_cast<const bf16x8*>(stg + fa_off[s][i]);
 #pragma unroll
-        for (int j = 0; j < TN; ++j) fb[slot][j].v = *reinterpret_cast<const bf16x8*>(stg + fb_off[s][j]);
+            for (int j = 0; j < TN; ++j) fb[slot][j].v = *reinterpret_cast<const bf16x8*>(stg + fb_off[s][j]);
+        } else {
+#pragma unroll
+            for (int i = 0; i < TM; ++i) fa[slot][i].v = tr_frag(stg + fa_off[s][i], 4 * 2 * BM);
+#pragma unroll
+            for (int j = 0; j < TN; ++j) fb[slot][j].v = tr_frag(stg + fb_off[s][j], 4 * 2 * BN);
+        }
     };
+
+    // Fused bias gradient (weight-gradient GEMMs): the waves of the first M-tile
+    // with wm == 0 hold every k of their B columns in their fragments.
+    constexpr bool COLSUM = !KM && (EPI == EPI_ACC_F32 || SPLIT);
+    const bool do_colsum = COLSUM && args.colsum != nullptr && tm == 0 && wm == 0;
+    float cs[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) cs[j] = 0.f;
 
     if (nkt > 0) {
         // prologue: fill every stage; wait for tile 0 (tiles 1 .. NSTAGE-1 may be in flight)
@@ -687,6 +768,14 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
 #pragma unroll
                 for (int s = 0; s < KS; ++s) {
                     const int cur = s & 1;
+                    if constexpr (COLSUM) {
+                        if (do_colsum) {
+#pragma unroll
+                            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                                for (int e = 0; e < 8; ++e) cs[j] += (float)fb[cur][j].v[e];
+                        }
+                    }
                     if (s + 1 < KS) {
                         load_frags(cur ^ 1, stg, s + 1);
                     } else {
@@ -710,6 +799,23 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
 
 #undef GP_DL_ISSUE
     const int row0 = m0 + wm * (BM / WM), col0 = n0 + wn * (BN / WN) + (lane & 31);
+    if constexpr (COLSUM) {
+        // lanes l and l + 32 hold the two k-halves of column l % 32
+#pragma unroll
+        for (int j = 0; j < TN; ++j) cs[j] += __shfl_xor(cs[j], 32);
+        if (do_colsum && lane < 32) {
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int col = col0 + j * 32;
+                if (col < args.N) {
+                    if constexpr (SPLIT)
+                        args.ws[((long)gridDim.y * args.M + blockIdx.y) * args.N + col] = cs[j];
+                    else
+                        args.colsum[col] = args.accumulate ? args.colsum[col] + cs[j] : cs[j];
+                }
+            }
+        }
+    }
     if constexpr (SPLIT) {
         const Rsrc ws = make_rsrc(args.ws, (uint32_t)((long)gridDim.y * args.M * args.N * 4));
 #pragma unroll
@@ -727,7 +833,7 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
                 }
             }
     } else {
-        if (m0 + BM <= args.M && n0 + BN <= args.N) {
+        if (EPI != EPI_ACC_F32 && m0 + BM <= args.M && n0 + BN <= args.N) {
             dl_epilogue_full<TM, TN, EPI>(args, acc, row0, col0, lane);
         } else {
             Epilogue<bf16, EPI> ep;
@@ -795,13 +901,13 @@ gp_status launch_tile(const GemmArgs& a, int epi, int splits, hipStream_t st) {
     return GP_OK;
 }
 
-template <int BM, int BN, int WM, int WN, int NSTAGE>
+template <int BM, int BN, int WM, int WN, int NSTAGE, bool KM>
 gp_status launch_dl(const GemmArgs& a, int epi, int splits, hipStream_t st) {
     constexpr int NT = 64 * WM * WN;
     const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
     if (splits > 1) {
         dim3 grid(tiles, splits);
-        klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_F32, true>, grid, NT, 0, st, a);
+        klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_F32, true, KM>, grid, NT, 0, st, a);
         GP_LAUNCH_CHECK();
         const long nq = (long)a.M * (a.N / 4);
         const int rg = (int)std::min<long>((nq + 255) / 256, 2048);
@@ -810,17 +916,28 @@ gp_status launch_dl(const GemmArgs& a, int epi, int splits, hipStream_t st) {
         case EPI_RES_F32: klaunch(splitk_reduce<bf16, EPI_RES_F32>, rg, 256, 0, st, a, splits); break;
         case EPI_F32: klaunch(splitk_reduce<bf16, EPI_F32>, rg, 256, 0, st, a, splits); break;
         case EPI_RELU_MASK: klaunch(splitk_reduce<bf16, EPI_RELU_MASK>, rg, 256, 0, st, a, splits); break;
+        case EPI_ACC_F32: klaunch(splitk_reduce<bf16, EPI_ACC_F32>, rg, 256, 0, st, a, splits); break;
         default: return set_error(GP_ERR_INVALID_ARG, "gemm: split-K epilogue");
         }
         GP_LAUNCH_CHECK();
+        if (epi == EPI_ACC_F32 && !KM && a.colsum)
+            return colsum_finalize(a.ws + (long)splits * a.M * a.N, splits, a.N, a.colsum, a.accumulate, st);
         return GP_OK;
     }
-    switch (epi) {
-    case EPI_STORE: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_STORE, false>, tiles, NT, 0, st, a); break;
-    case EPI_RES_F32: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_RES_F32, false>, tiles, NT, 0, st, a); break;
-    case EPI_F32: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_F32, false>, tiles, NT, 0, st, a); break;
-    case EPI_RELU_MASK: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_RELU_MASK, false>, tiles, NT, 0, st, a); break;
-    default: return set_error(GP_ERR_INVALID_ARG, "gemm: direct-load path has no accumulate epilogue");
+    if constexpr (KM) {
+        switch (epi) {
+        case EPI_STORE: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_STORE, false, KM>, tiles, NT, 0, st, a); break;
+        case EPI_RES_F32: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_RES_F32, false, KM>, tiles, NT, 0, st, a); break;
+        case EPI_F32: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_F32, false, KM>, tiles, NT, 0, st, a); break;
+        case EPI_RELU_MASK: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_RELU_MASK, false, KM>, tiles, NT, 0, st, a); break;
+        case EPI_ACC_F32: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_ACC_F32, false, KM>, tiles, NT, 0, st, a); break;
+        default: return set_error(GP_ERR_INVALID_ARG, "gemm: epilogue not instantiated for k-contiguous operands");
+        }
+    } else {
+        switch (epi) {
+        case EPI_ACC_F32: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_ACC_F32, false, KM>, tiles, NT, 0, st, a); break;
+        default: return set_error(GP_ERR_INVALID_ARG, "gemm: epilogue not instantiated for m-contiguous operands");
+        }
     }
     GP_LAUNCH_CHECK();
     return GP_OK;
@@ -828,15 +945,16 @@ gp_status launch_dl(const GemmArgs& a, int epi, int splits, hipStream_t st) {
 
 template <bool AK, bool BKM>
 gp_status launch_bf16(const GemmArgs& a, int epi, int cfg, int splits, hipStream_t st) {
-    if constexpr (AK && BKM) {
+    if constexpr (AK == BKM) {
+        constexpr bool KM = AK;
         switch (cfg) {
-        case T_DL128x128_S2: return launch_dl<128, 128, 2, 2, 2>(a, epi, splits, st);
-        case T_DL128x128_S3: return launch_dl<128, 128, 2, 2, 3>(a, epi, splits, st);
-        case T_DL256x128_S2: return launch_dl<256, 128, 2, 2, 2>(a, epi, splits, st);
-        case T_DL256x256_S2: return launch_dl<256, 256, 2, 2, 2>(a, epi, splits, st);
-        case T_DL256x256_W8: return launch_dl<256, 256, 2, 4, 2>(a, epi, splits, st);
-        case T_DL256x128_W8: return launch_dl<256, 128, 4, 2, 2>(a, epi, splits, st);
-        case T_DL128x256_W8: return launch_dl<128, 256, 2, 4, 2>(a, epi, splits, st);
+        case T_DL128x128_S2: return launch_dl<128, 128, 2, 2, 2, KM>(a, epi, splits, st);
+        case T_DL128x128_S3: return launch_dl<128, 128, 2, 2, 3, KM>(a, epi, splits, st);
+        case T_DL256x128_S2: return launch_dl<256, 128, 2, 2, 2, KM>(a, epi, splits, st);
+        case T_DL256x256_S2: return launch_dl<256, 256, 2, 2, 2, KM>(a, epi, splits, st);
+        case T_DL256x256_W8: return launch_dl<256, 256, 2, 4, 2, KM>(a, epi, splits, st);
+        case T_DL256x128_W8: return launch_dl<256, 128, 4, 2, 2, KM>(a, epi, splits, st);
+        case T_DL128x256_W8: return launch_dl<128, 256, 2, 4, 2, KM>(a, epi, splits, st);
         default: break;
         }
     }
@@ -947,16 +1065,16 @@ gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dty
         gp_status s = check_args<bf16>(a, a_kmajor, b_kmajor);
         if (s != GP_OK) return s;
         int cfg, splits;
-        if (a_kmajor && a.K % 64 == 0 && epi != EPI_ACC_F32)
+        if (a.K % 64 == 0)
             choose_dl(a, epi, cfg, splits);
         else
             choose(a, epi, cfg, splits);
-        if (a.force_cfg >= 0 && a.force_cfg <= T_DL128x256_W8 && (a.force_cfg <= T128x128 || a_kmajor)) {
+        if (a.force_cfg >= 0 && a.force_cfg <= T_DL128x256_W8) {
             cfg = a.force_cfg;
             splits = a.force_splits > 0 ? a.force_splits : 1;
             if (splits > 1 && !split_fits(a, splits, (a.K + 63) / 64)) splits = 1;
         }
-        if (cfg > T128x128 && (!a_kmajor || epi == EPI_ACC_F32 || a.K % 64)) cfg = T128x128;
+        if (cfg > T128x128 && a.K % 64) cfg = T128x128;
         return a_kmajor ? launch_bf16<true, true>(a, epi, cfg, splits, st)
                         : launch_bf16<false, false>(a, epi, cfg, splits, st);
     }

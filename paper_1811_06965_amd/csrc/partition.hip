@@ -12,12 +12,13 @@
 //                   per LayerNorm gamma [D] then beta [D]
 //   welt            working copies in the partition dtype: W [in, out] and W^T [out, in]
 //   stash           M boundary inputs [n, S, D] (and decoder memories [n, S_mem, D])
-//   workspace       residual stream xs[0..L] fp32 [T, D] (T = n S), per-layer
-//                   intermediates of one micro-batch, backward scratch
-// The forward pass writes its intermediates into layer slot 0 and ping-pongs
-// xs[0]/xs[1]; the re-materialising pass uses slot l and xs[l] for layer l.
-// Both run the same kernels with the same launch shapes, so the recomputed
-// activations equal the first pass bit for bit.
+//   workspace       per set: residual stream xs[0..L] fp32 [T, D] (T = n S) and
+//                   per-layer intermediates of one micro-batch; backward scratch
+// The forward pass writes its intermediates into layer slot 0 of set 0 and
+// ping-pongs xs[0]/xs[1]; the re-materialising pass of micro-batch m uses set
+// m % 2 (one set when M = 1 or recompute-ahead is off), slot l and xs[l] for
+// layer l.  All run the same kernels with the same launch shapes, so the
+// recomputed activations equal the first pass bit for bit.
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
@@ -76,7 +77,9 @@ struct BwdWs {
     void *pe = nullptr, *qe = nullptr, *dz = nullptr, *dc = nullptr, *dqkv = nullptr, *dxq = nullptr, *dxkv = nullptr;
     double *loss_partial = nullptr, *loss_acc = nullptr;
     int* flag = nullptr;
-    float* splitk = nullptr;   // split-K partial tiles
+    float* splitk = nullptr;   // split-K partial tiles (caller's stream)
+    float* splitk_side = nullptr;  // split-K partial tiles of the weight-gradient stream
+    float* splitk_remat = nullptr; // split-K partial tiles of the recompute-ahead stream
     long splitk_elems = 0;
     // loss head
     float* sth = nullptr;
@@ -134,14 +137,28 @@ struct gp_partition {
     char* stash_x = nullptr;
     char* stash_m = nullptr;
     char* ws = nullptr;
-    std::vector<float*> xs;
-    std::vector<LayerWs> lw;
+    std::vector<float*> xs[2];
+    std::vector<LayerWs> lw[2];
+    int nsets = 1;
     BwdWs bw;
     size_t bytes_params = 0, bytes_grads = 0, bytes_stash = 0, bytes_ws = 0;
     // GEMM tile-shape override (GP_GEMM_TILE = 0..10, GP_GEMM_SPLITS), read at
     // configure; -1 lets the library choose per problem.
     int gemm_tile = -1, gemm_splits = 0;
     LaunchTimer timer;
+    // Weight-gradient GEMMs run on a second stream (GP_SIDE_STREAM=0 turns it
+    // off), ordered against the caller's stream by events from a ring.
+    bool use_side = true;
+    hipStream_t side = nullptr;
+    std::vector<hipEvent_t> ring;
+    int ring_next = 0;
+    // Recompute-ahead (GP_REMAT_AHEAD=0 turns it off): while micro-batch m is
+    // back-propagated, micro-batch m - 1 is re-materialised on a third stream
+    // into the other workspace set.
+    bool remat_ahead = true;
+    hipStream_t remat = nullptr;
+    hipEvent_t remat_fork = nullptr, remat_done = nullptr;
+    int remat_pending = -1;  // micro-batch whose recompute-ahead is enqueued
 
     void* W(size_t elt_off) const { return welt + elt_off * esz; }
     char* stash_x_mb(int m) const { return stash_x + (size_t)m * g.T() * d.D * esz; }
@@ -160,28 +177,33 @@ void plan_workspace(gp_partition* p, Arena& a) {
     const long lse_n = (long)g.n * d.H * g.S;
     const size_t e = p->esz;
     const bool dec = g.kind == GP_DECODER_CROSS;
-    p->xs.assign(d.L + 1, nullptr);
-    for (auto& x : p->xs) x = a.take<float>(T * D);
-    p->lw.assign(d.L, LayerWs{});
-    for (auto& l : p->lw) {
-        l.st1 = a.take<float>(2 * T);
-        l.u = a.take_elt(T * D, e);
-        l.qkv = a.take_elt(T * 3 * D, e);
-        l.c = a.take_elt(T * D, e);
-        l.lse = a.take<float>(lse_n);
-        l.x1 = a.take<float>(T * D);
-        if (dec) {
-            l.stc = a.take<float>(2 * T);
-            l.uc = a.take_elt(T * D, e);
-            l.xq = a.take_elt(T * D, e);
-            l.xkv = a.take_elt(Tm * 2 * D, e);
-            l.xc = a.take_elt(T * D, e);
-            l.xlse = a.take<float>(lse_n);
-            l.x2 = a.take<float>(T * D);
+    for (int set = 0; set < 2; ++set) {
+        p->xs[set].assign(set < p->nsets ? d.L + 1 : 0, nullptr);
+        p->lw[set].assign(set < p->nsets ? d.L : 0, LayerWs{});
+    }
+    for (int set = 0; set < p->nsets; ++set)
+        for (auto& x : p->xs[set]) x = a.take<float>(T * D);
+    for (int set = 0; set < p->nsets; ++set) {
+        for (auto& l : p->lw[set]) {
+            l.st1 = a.take<float>(2 * T);
+            l.u = a.take_elt(T * D, e);
+            l.qkv = a.take_elt(T * 3 * D, e);
+            l.c = a.take_elt(T * D, e);
+            l.lse = a.take<float>(lse_n);
+            l.x1 = a.take<float>(T * D);
+            if (dec) {
+                l.stc = a.take<float>(2 * T);
+                l.uc = a.take_elt(T * D, e);
+                l.xq = a.take_elt(T * D, e);
+                l.xkv = a.take_elt(Tm * 2 * D, e);
+                l.xc = a.take_elt(T * D, e);
+                l.xlse = a.take<float>(lse_n);
+                l.x2 = a.take<float>(T * D);
+            }
+            l.stf = a.take<float>(2 * T);
+            l.v = a.take_elt(T * D, e);
+            l.a = a.take_elt(T * F, e);
         }
-        l.stf = a.take<float>(2 * T);
-        l.v = a.take_elt(T * D, e);
-        l.a = a.take_elt(T * F, e);
     }
     BwdWs& b = p->bw;
     b.p32 = a.take<float>(T * D);
@@ -212,6 +234,8 @@ void plan_workspace(gp_partition* p, Arena& a) {
     // D x 3D packed-QKV weight gradient (with its bias column sums)
     b.splitk_elems = std::max<long>(8 * T * D, 8 * (3 * D * D + 3 * D));
     b.splitk = a.take<float>((size_t)b.splitk_elems);
+    b.splitk_side = a.take<float>((size_t)b.splitk_elems);
+    if (p->nsets > 1) b.splitk_remat = a.take<float>((size_t)b.splitk_elems);
     size_t lp = (size_t)loss_blocks();
     if (g.loss == GP_LOSS_XENT_LS && (size_t)xent_partials(T) > lp) lp = xent_partials(T);
     b.loss_partial = a.take<double>(lp);
@@ -228,6 +252,65 @@ struct Ctx {
     gp_partition* p;
     hipStream_t st;
     int dt;
+    float* ws = nullptr;  // split-K partials for launches on st
+};
+
+enum class Lane { Main, Side, Remat };
+
+Ctx make_ctx(gp_partition* p, hipStream_t st, Lane lane = Lane::Main) {
+    Ctx c{p, st, p->g.dtype};
+    c.ws = lane == Lane::Side ? p->bw.splitk_side : lane == Lane::Remat ? p->bw.splitk_remat : p->bw.splitk;
+    return c;
+}
+
+// Ordering between the caller's stream (main) and the weight-gradient stream
+// (side).  A side launch first waits for everything enqueued on main so far;
+// it then records an event, remembered against the buffers it reads.  Before
+// main overwrites such a buffer it waits for that event; at the end of a
+// backward call main waits for the side's last event.  Without a side stream
+// every launch goes to main and nothing here does anything.
+struct SideSync {
+    gp_partition* p;
+    hipStream_t main, side;
+    std::vector<std::pair<const void*, hipEvent_t>> reads;
+    hipEvent_t last = nullptr;
+
+    bool on() const { return side != nullptr; }
+    hipEvent_t next_event() {
+        hipEvent_t e = p->ring[p->ring_next];
+        p->ring_next = (p->ring_next + 1) % (int)p->ring.size();
+        return e;
+    }
+    gp_status fork() {
+        const hipEvent_t e = next_event();
+        GP_HIP(hipEventRecord(e, main));
+        GP_HIP(hipStreamWaitEvent(side, e, 0));
+        return GP_OK;
+    }
+    gp_status done_reading(std::initializer_list<const void*> bufs) {
+        const hipEvent_t e = next_event();
+        GP_HIP(hipEventRecord(e, side));
+        for (const void* b : bufs) reads.emplace_back(b, e);
+        last = e;
+        return GP_OK;
+    }
+    gp_status before_write(const void* buf) {
+        for (size_t i = 0; i < reads.size();) {
+            if (reads[i].first == buf) {
+                GP_HIP(hipStreamWaitEvent(main, reads[i].second, 0));
+                reads.erase(reads.begin() + (long)i);
+            } else {
+                ++i;
+            }
+        }
+        return GP_OK;
+    }
+    gp_status join() {
+        if (last) GP_HIP(hipStreamWaitEvent(main, last, 0));
+        reads.clear();
+        last = nullptr;
+        return GP_OK;
+    }
 };
 
 #define GP_TRY(x)                    \
@@ -324,7 +407,7 @@ gp_status linear_fwd(const Ctx& c, const Linear& L, const void* A, long M, void*
     g.aux = res;
     g.ldaux = ldc;
     g.relu = relu;
-    g.ws = c.p->bw.splitk;
+    g.ws = c.ws;
     g.ws_elems = c.p->bw.splitk_elems;
     g.force_cfg = c.p->gemm_tile;
     g.force_splits = c.p->gemm_splits;
@@ -347,7 +430,7 @@ gp_status linear_dx(const Ctx& c, const Linear& L, const void* dY, long M, void*
     g.aux = aux;
     g.ldaux = L.in;
     g.accumulate = accumulate;
-    g.ws = c.p->bw.splitk;
+    g.ws = c.ws;
     g.ws_elems = c.p->bw.splitk_elems;
     g.force_cfg = c.p->gemm_tile;
     g.force_splits = c.p->gemm_splits;
@@ -367,12 +450,21 @@ gp_status linear_dw(const Ctx& c, const Linear& L, const void* X, const void* dY
     g.C = c.p->grads + L.w;
     g.ldc = L.out;
     g.accumulate = accumulate;
-    g.ws = c.p->bw.splitk;
+    g.ws = c.ws;
     g.ws_elems = c.p->bw.splitk_elems;
     g.force_cfg = c.p->gemm_tile;
     g.force_splits = c.p->gemm_splits;
     g.colsum = c.p->grads + L.b;  // bias gradient fused into the GEMM
     return timed_gemm(c, L.role + 2, g, EPI_ACC_F32, false);
+}
+
+// The weight-gradient GEMM on the side stream when there is one.
+gp_status linear_dw_async(const Ctx& c, const Ctx& cs, SideSync& sy, const Linear& L, const void* X, const void* dY,
+                          long rows, int accumulate) {
+    if (!sy.on()) return linear_dw(c, L, X, dY, rows, accumulate);
+    GP_TRY(sy.fork());
+    GP_TRY(linear_dw(cs, L, X, dY, rows, accumulate));
+    return sy.done_reading({X, dY});
 }
 
 gp_status norm_bwd(const Ctx& c, const Norm& N, const float* dn, const float* x, const float* stats, long rows,
@@ -453,21 +545,22 @@ gp_status layer_forward(const Ctx& c, int l, LayerWs& w, const float* x_in, floa
 // Forward of micro-batch m through all layers.  keep = false: first pass,
 // intermediates discarded (slot 0, ping-pong residuals); keep = true:
 // re-materialisation from the stash, intermediates kept per layer.
-gp_status partition_forward(const Ctx& c, int m, bool keep, const void* x, const void* mem, void* y) {
+gp_status partition_forward(const Ctx& c, int m, bool keep, const void* x, const void* mem, void* y, int set = 0) {
     gp_partition* p = c.p;
     const long T = p->g.T(), D = p->d.D;
     const int L = p->d.L;
+    std::vector<float*>& xs = p->xs[set];
     if (!keep) {
-        GP_TRY(intake(c.dt, x, p->stash_x_mb(m), p->xs[0], T * D, c.st));
+        GP_TRY(intake(c.dt, x, p->stash_x_mb(m), xs[0], T * D, c.st));
         if (mem) GP_TRY(intake(c.dt, mem, p->stash_m_mb(m), nullptr, p->g.Tm() * D, c.st));
     } else {
-        GP_TRY(intake(c.dt, p->stash_x_mb(m), nullptr, p->xs[0], T * D, c.st));
+        GP_TRY(intake(c.dt, p->stash_x_mb(m), nullptr, xs[0], T * D, c.st));
     }
     const void* mem_m = p->g.kind == GP_DECODER_CROSS ? p->stash_m_mb(m) : nullptr;
     for (int l = 0; l < L; ++l) {
-        LayerWs& w = keep ? p->lw[l] : p->lw[0];
-        const float* xi = keep ? p->xs[l] : p->xs[l & 1];
-        float* xo = keep ? p->xs[l + 1] : p->xs[(l + 1) & 1];
+        LayerWs& w = keep ? p->lw[set][l] : p->lw[set][0];
+        const float* xi = keep ? xs[l] : xs[l & 1];
+        float* xo = keep ? xs[l + 1] : xs[(l + 1) & 1];
         GP_TRY(layer_forward(c, l, w, xi, xo, mem_m, (!keep && l == L - 1) ? y : nullptr));
     }
     return GP_OK;
@@ -475,11 +568,12 @@ gp_status partition_forward(const Ctx& c, int m, bool keep, const void* x, const
 
 // Backward of one layer.  dY arrives in (in32, ine); dX leaves in the pair
 // returned through out32/oute (one of the two backward pairs).
-gp_status layer_backward(const Ctx& c, int l, bool first, float* in32, void* ine, float* sc32, void* sce,
-                         float*& out32, void*& oute, float* dx32_final, void* dxe_final, const void* mem) {
+gp_status layer_backward(const Ctx& c, const Ctx& cs, SideSync& sy, int set, int l, bool first, float* in32, void* ine,
+                         float* sc32, void* sce, float*& out32, void*& oute, float* dx32_final, void* dxe_final,
+                         const void* mem) {
     gp_partition* p = c.p;
     const LayerPlan& P = p->plan.layers[l];
-    LayerWs& w = p->lw[l];
+    LayerWs& w = p->lw[set][l];
     BwdWs& b = p->bw;
     const long T = p->g.T(), Tm = p->g.Tm(), D = p->d.D;
     const bool dec = p->g.kind == GP_DECODER_CROSS;
@@ -487,10 +581,12 @@ gp_status layer_backward(const Ctx& c, int l, bool first, float* in32, void* ine
     const float* xf = dec ? w.x2 : w.x1;
     const Norm& nf = dec ? P.ln3 : P.ln2;
     // feed-forward block:  dW2, db2;  dz = dY W2^T * [a > 0];  dW1, db1;  dv = dz W1^T
-    GP_TRY(linear_dw(c, P.ffn2, w.a, ine, T, acc));
+    GP_TRY(linear_dw_async(c, cs, sy, P.ffn2, w.a, ine, T, acc));
+    GP_TRY(sy.before_write(b.dz));
     GP_TRY(linear_dx(c, P.ffn2, ine, T, b.dz, EPI_RELU_MASK, w.a, 0));
-    GP_TRY(linear_dw(c, P.ffn1, w.v, b.dz, T, acc));
+    GP_TRY(linear_dw_async(c, cs, sy, P.ffn1, w.v, b.dz, T, acc));
     GP_TRY(linear_dx(c, P.ffn1, b.dz, T, b.dn, EPI_F32, nullptr, 0));
+    GP_TRY(sy.before_write(sce));
     GP_TRY(norm_bwd(c, nf, b.dn, xf, w.stf, T, in32, sc32, sce, acc));
     // (sc) = dL/d(xf)
     float* cur32 = sc32;
@@ -499,7 +595,7 @@ gp_status layer_backward(const Ctx& c, int l, bool first, float* in32, void* ine
     void* othe = ine;
     if (dec) {
         // cross-attention block
-        GP_TRY(linear_dw(c, P.xo, w.xc, cure, T, acc));
+        GP_TRY(linear_dw_async(c, cs, sy, P.xo, w.xc, cure, T, acc));
         GP_TRY(linear_dx(c, P.xo, cure, T, b.dc, EPI_STORE, nullptr, 0));
         AttnArgs x = attn_args(p, p->g.Smem, 0);
         x.q = w.xq;
@@ -518,17 +614,20 @@ gp_status layer_backward(const Ctx& c, int l, bool first, float* in32, void* ine
         x.dv = p->off_elt(b.dxkv, D);
         x.lddk = x.lddv = 2 * D;
         x.delta = b.delta;
+        GP_TRY(sy.before_write(b.dxq));
+        GP_TRY(sy.before_write(b.dxkv));
         GP_TRY(timed_attention(c, GP_K_XATTN_BWD, x, true));
-        GP_TRY(linear_dw(c, P.xq, w.uc, b.dxq, T, acc));
+        GP_TRY(linear_dw_async(c, cs, sy, P.xq, w.uc, b.dxq, T, acc));
         GP_TRY(linear_dx(c, P.xq, b.dxq, T, b.dn, EPI_F32, nullptr, 0));
-        GP_TRY(linear_dw(c, P.xkv, mem, b.dxkv, Tm, acc));
+        GP_TRY(linear_dw_async(c, cs, sy, P.xkv, mem, b.dxkv, Tm, acc));
         GP_TRY(linear_dx(c, P.xkv, b.dxkv, Tm, b.dmem32, EPI_ACC_F32, nullptr, l == p->d.L - 1 ? 0 : 1));
+        GP_TRY(sy.before_write(othe));
         GP_TRY(norm_bwd(c, P.ln2, b.dn, w.x1, w.stc, T, cur32, oth32, othe, acc));
         std::swap(cur32, oth32);
         std::swap(cure, othe);
     }
     // self-attention block
-    GP_TRY(linear_dw(c, P.o, w.c, cure, T, acc));
+    GP_TRY(linear_dw_async(c, cs, sy, P.o, w.c, cure, T, acc));
     GP_TRY(linear_dx(c, P.o, cure, T, b.dc, EPI_STORE, nullptr, 0));
     AttnArgs a = attn_args(p, p->g.S, dec ? 1 : 0);
     a.q = w.qkv;
@@ -545,15 +644,17 @@ gp_status layer_backward(const Ctx& c, int l, bool first, float* in32, void* ine
     a.dv = p->off_elt(b.dqkv, 2 * D);
     a.lddq = a.lddk = a.lddv = 3 * D;
     a.delta = b.delta;
+    GP_TRY(sy.before_write(b.dqkv));
     GP_TRY(timed_attention(c, GP_K_ATTN_BWD, a, true));
-    GP_TRY(linear_dw(c, P.qkv, w.u, b.dqkv, T, acc));
+    GP_TRY(linear_dw_async(c, cs, sy, P.qkv, w.u, b.dqkv, T, acc));
     GP_TRY(linear_dx(c, P.qkv, b.dqkv, T, b.dn, EPI_F32, nullptr, 0));
-    const float* x_in = p->xs[l];
+    const float* x_in = p->xs[set][l];
     if (dxe_final || dx32_final || l == 0) {
         GP_TRY(norm_bwd(c, P.ln1, b.dn, x_in, w.st1, T, cur32, dx32_final, dxe_final, acc));
         out32 = dx32_final;
         oute = dxe_final;
     } else {
+        GP_TRY(sy.before_write(othe));
         GP_TRY(norm_bwd(c, P.ln1, b.dn, x_in, w.st1, T, cur32, oth32, othe, acc));
         out32 = oth32;
         oute = othe;
@@ -561,13 +662,13 @@ gp_status layer_backward(const Ctx& c, int l, bool first, float* in32, void* ine
     return GP_OK;
 }
 
-gp_status head_backward(const Ctx& c, bool first, const int* labels) {
+gp_status head_backward(const Ctx& c, int set, bool first, const int* labels) {
     gp_partition* p = c.p;
     const HeadPlan& Hd = p->plan.head;
     BwdWs& b = p->bw;
     const long T = p->g.T(), D = p->d.D, V = p->g.V;
     const int acc = first ? 0 : 1;
-    const float* y = p->xs[p->d.L];
+    const float* y = p->xs[set][p->d.L];
     GP_TRY(timed_ln_fwd(c, y, T, (int)D, p->master + Hd.lnf.g, p->master + Hd.lnf.b, p->g.eps, b.h, b.sth));
     GP_TRY(linear_fwd(c, Hd.out, b.h, T, b.z, V, EPI_STORE, 0, nullptr, nullptr));
     const double norm = (double)p->g.n * p->g.M * p->g.S;
@@ -590,6 +691,18 @@ gp_status upload_param_block(gp_partition* p, const ParamRef& r, const float* ho
 }
 
 void free_all(gp_partition* p) {
+    for (hipEvent_t e : p->ring)
+        if (e) (void)hipEventDestroy(e);
+    p->ring.clear();
+    p->ring_next = 0;
+    if (p->side) (void)hipStreamDestroy(p->side);
+    p->side = nullptr;
+    for (hipEvent_t e : {p->remat_fork, p->remat_done})
+        if (e) (void)hipEventDestroy(e);
+    if (p->remat) (void)hipStreamDestroy(p->remat);
+    p->remat = nullptr;
+    p->remat_fork = p->remat_done = nullptr;
+    p->remat_pending = -1;
     for (hipEvent_t e : p->timer.all) (void)hipEventDestroy(e);
     const bool markers = p->timer.markers;
     p->timer = LaunchTimer();
@@ -654,6 +767,9 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
     g.check_finite = cfg->check_finite;
     p->esz = g.dtype == GP_BF16 ? 2 : 4;
     if (const char* e = std::getenv("GP_TIMER_MARKERS")) p->timer.markers = std::atoi(e) != 0;
+    if (const char* e = std::getenv("GP_SIDE_STREAM")) p->use_side = std::atoi(e) != 0;
+    if (const char* e = std::getenv("GP_REMAT_AHEAD")) p->remat_ahead = std::atoi(e) != 0;
+    p->nsets = (p->remat_ahead && g.M >= 2) ? 2 : 1;
     if (const char* e = std::getenv("GP_GEMM_TILE")) p->gemm_tile = std::atoi(e);
     if (const char* e = std::getenv("GP_GEMM_SPLITS")) p->gemm_splits = std::atoi(e);
     p->plan = plan_params(p->d, g);
@@ -701,7 +817,19 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
             return s;
         }
     }
-    e = hipDeviceSynchronize();
+    if (p->use_side) {
+        // default priority, like every stream of the library
+        e = hipStreamCreateWithFlags(&p->side, hipStreamNonBlocking);
+        p->ring.assign(32, nullptr);
+        for (size_t i = 0; e == hipSuccess && i < p->ring.size(); ++i)
+            e = hipEventCreateWithFlags(&p->ring[i], hipEventDisableTiming);
+    }
+    if (e == hipSuccess && p->nsets > 1) {
+        e = hipStreamCreateWithFlags(&p->remat, hipStreamNonBlocking);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&p->remat_fork, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&p->remat_done, hipEventDisableTiming);
+    }
+    if (e == hipSuccess) e = hipDeviceSynchronize();
     if (e != hipSuccess) {
         free_all(p);
         return hip_fail(e, __FILE__, __LINE__);
@@ -805,7 +933,7 @@ gp_status gp_forward_microbatch(gp_partition* p, int mb, const void* x, const vo
     const bool dec = p->g.kind == GP_DECODER_CROSS;
     if (dec && !mem) return set_error(GP_ERR_INVALID_ARG, "decoder partitions need the memory input");
     if (!dec && mem) return set_error(GP_ERR_INVALID_ARG, "encoder partitions take no memory input");
-    Ctx c{p, (hipStream_t)stream, p->g.dtype};
+    Ctx c = make_ctx(p, (hipStream_t)stream);
     s = partition_forward(c, mb, false, x, mem, y);
     if (s != GP_OK) return s;
     p->sched.did_forward();
@@ -821,12 +949,35 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     if (!dy_or_target) return set_error(GP_ERR_INVALID_ARG, "dy_or_target must not be NULL");
     const bool dec = p->g.kind == GP_DECODER_CROSS;
     if (!dec && dmem) return set_error(GP_ERR_INVALID_ARG, "encoder partitions have no memory gradient");
-    Ctx c{p, (hipStream_t)stream, p->g.dtype};
+    Ctx c = make_ctx(p, (hipStream_t)stream);
+    Ctx cs = make_ctx(p, p->side, Lane::Side);
+    SideSync sy{p, (hipStream_t)stream, p->use_side ? p->side : nullptr};
     const bool first = p->sched.first_backward();
     const long T = p->g.T(), D = p->d.D;
-    // re-materialise this micro-batch's forward from the stash
-    s = partition_forward(c, mb, true, nullptr, nullptr, nullptr);
-    if (s != GP_OK) return s;
+    const int set = p->nsets > 1 ? (mb & 1) : 0;
+    // Everything enqueued on the caller's stream so far (all forwards, the
+    // previous backward, which read the other workspace set) precedes a
+    // recompute-ahead launched from this call.
+    if (p->nsets > 1 && mb > 0) GP_HIP(hipEventRecord(p->remat_fork, c.st));
+    // re-materialise this micro-batch's forward from the stash, unless the
+    // previous backward call already did so on the recompute-ahead stream
+    if (p->remat_pending == mb) {
+        GP_HIP(hipStreamWaitEvent(c.st, p->remat_done, 0));
+        p->remat_pending = -1;
+    } else {
+        s = partition_forward(c, mb, true, nullptr, nullptr, nullptr, set);
+        if (s != GP_OK) return s;
+    }
+    if (p->nsets > 1 && mb > 0) {
+        // re-materialise micro-batch mb - 1 into the other set meanwhile
+        // (GPipe, Section 2.3: the recompute can be scheduled earlier)
+        Ctx cr = make_ctx(p, p->remat, Lane::Remat);
+        GP_HIP(hipStreamWaitEvent(cr.st, p->remat_fork, 0));
+        s = partition_forward(cr, mb - 1, true, nullptr, nullptr, nullptr, set ^ 1);
+        if (s != GP_OK) return s;
+        GP_HIP(hipEventRecord(p->remat_done, cr.st));
+        p->remat_pending = mb - 1;
+    }
     BwdWs& b = p->bw;
     // dL/dy of the partition output
     if (p->g.loss == GP_LOSS_NONE) {
@@ -834,10 +985,10 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     } else if (p->g.loss == GP_LOSS_MSE) {
         int nb = 0;
         const double norm = (double)p->g.n * p->g.M * p->g.S * D;
-        s = mse_grad(c.dt, p->xs[p->d.L], dy_or_target, T * D, norm, b.p32, b.pe, b.loss_partial, &nb, c.st);
+        s = mse_grad(c.dt, p->xs[set][p->d.L], dy_or_target, T * D, norm, b.p32, b.pe, b.loss_partial, &nb, c.st);
         if (s == GP_OK) s = loss_finalize(b.loss_partial, nb, b.loss_acc, first ? 0 : 1, c.st);
     } else {
-        s = head_backward(c, first, reinterpret_cast<const int*>(dy_or_target));
+        s = head_backward(c, set, first, reinterpret_cast<const int*>(dy_or_target));
     }
     if (s != GP_OK) return s;
     const void* mem_m = dec ? p->stash_m_mb(mb) : nullptr;
@@ -848,8 +999,12 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     for (int l = p->d.L - 1; l >= 0; --l) {
         float* out32 = nullptr;
         void* oute = nullptr;
-        s = layer_backward(c, l, first, in32, ine, sc32, sce, out32, oute, nullptr, l == 0 ? dx : nullptr, mem_m);
-        if (s != GP_OK) return s;
+        s = layer_backward(c, cs, sy, set, l, first, in32, ine, sc32, sce, out32, oute, nullptr, l == 0 ? dx : nullptr,
+                           mem_m);
+        if (s != GP_OK) {
+            (void)sy.join();
+            return s;
+        }
         if (l > 0) {
             // the pair not holding dX becomes scratch for the next layer
             float* f32 = (out32 == b.p32) ? b.q32 : b.p32;
@@ -860,6 +1015,9 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
             sce = fe;
         }
     }
+    // the caller's stream resumes only after the last weight-gradient GEMM
+    s = sy.join();
+    if (s != GP_OK) return s;
     if (dec && dmem) {
         s = cast_out(c.dt, b.dmem32, dmem, p->g.Tm() * D, c.st);
         if (s != GP_OK) return s;

@@ -138,6 +138,18 @@ class Partition:
         loss = gp.gp_accumulate_and_step(self.h, lr, want_loss, st)
         return {"y": y, "dx": dx, "dmem": dmem, "loss": loss}
 
+    def capture_step(self, x, mem, dy, lr=0.0, dx=None, dmem=None, want_y=False, y=None):
+        """Capture one whole mini-batch step (M forwards, M backwards, the
+        update) into a HIP graph on a capture stream and return it; replay()
+        runs the step again on the same buffers.  The capture itself runs no
+        work.  The loss is not read (that would synchronise), and the
+        partition must not check gradients for finiteness (same reason)."""
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            self.step(x, mem, dy, lr=lr, want_y=want_y, want_dx=dx is not None, want_dmem=dmem is not None,
+                      want_loss=False, y=y, dx=dx, dmem=dmem)
+        return g
+
     # ------------------------------------------------------------ timers
     def timer_select(self, role):
         """role: a name from gp.KERNEL_ROLES, "all", or None to stop."""

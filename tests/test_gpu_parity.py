@@ -164,6 +164,76 @@ def test_steps_are_bitwise_deterministic(cfg):
         assert np.array_equal(a, b)
 
 
+DEC_SMALL_BF16 = synth.PartitionConfig("dec_small_bf16", layers=2, d_model=256, d_ff=512, heads=4, seq=64, batch=4,
+                                       micro=2, kind="decoder", mem_seq=64, loss="xent_ls", vocab=512,
+                                       label_smoothing=0.1)
+
+
+@pytest.mark.parametrize("cfg", [ENC512_SMALL, DEC_SMALL_BF16], ids=lambda c: c.name)
+def test_library_streams_are_bitwise_neutral(cfg, monkeypatch):
+    """Running the weight-gradient GEMMs on the library's second stream and
+    the recompute of micro-batch m - 1 on a third (during the backward of m)
+    changes only the order of independent launches: every output, gradient
+    and the loss are bit-identical to the single-stream schedule.  (T = 256
+    and 128 rows are multiples of 64, so the weight gradients take the
+    direct-to-LDS m-contiguous kernel.)"""
+    from paper_1811_06965_amd.runtime import Partition
+    case = synth.make_case(cfg, 11, perturb=True)
+    res = {}
+    for side in ("0", "1"):
+        monkeypatch.setenv("GP_SIDE_STREAM", side)
+        monkeypatch.setenv("GP_REMAT_AHEAD", side)
+        with Partition(cfg) as part:
+            part.load_params(case["layers"], case["head"])
+            inp = part.device_inputs(case)
+            outs = []
+            for _ in range(2):
+                o = part.step(inp["x"], inp["mem"], inp["dy"], lr=0.0)
+                outs.append((_grads_flat(part), to_np(o["dx"]), o["loss"] or 0.0,
+                             to_np(o["dmem"]) if o["dmem"] is not None else np.zeros(1)))
+            res[side] = outs
+    for a, b in zip(res["0"], res["1"]):
+        for x, y in zip(a, b):
+            assert np.array_equal(np.asarray(x), np.asarray(y))
+
+
+@pytest.mark.parametrize("cfg", [ENC512_SMALL.with_(loss="none"), DEC_SMALL_BF16], ids=lambda c: c.name)
+def test_graph_replay_matches_eager_steps(cfg):
+    """A step captured into a HIP graph and replayed three times (with eager
+    reads and synchronisations between the replays) gives bit for bit the
+    parameters, gradients and boundary gradients of three eager steps."""
+    from paper_1811_06965_amd.runtime import Partition
+    case = synth.make_case(cfg, 12, perturb=True)
+    lr = 1e-4  # the boundary gradient is unnormalised: keep three updates finite
+
+    def snapshot(part, o):
+        torch.cuda.synchronize()
+        pl, ph = part.params()
+        return [_grads_flat(part), to_np(o["dx"]), np.concatenate([np.ravel(v) for d in pl for v in d.values()] +
+                                                                    [np.ravel(v) for v in ph.values()] + [np.zeros(1)])]
+
+    eager = []
+    with Partition(cfg) as part:
+        part.load_params(case["layers"], case["head"])
+        inp = part.device_inputs(case)
+        dx = torch.empty_like(inp["x"])
+        for _ in range(3):
+            o = part.step(inp["x"], inp["mem"], inp["dy"], lr=lr, want_y=False, want_loss=False, dx=dx)
+            eager.append(snapshot(part, o))
+    with Partition(cfg) as part:
+        part.load_params(case["layers"], case["head"])
+        inp = part.device_inputs(case)
+        dx = torch.empty_like(inp["x"])
+        dmem = torch.empty_like(inp["mem"]) if inp["mem"] is not None else None
+        g = part.capture_step(inp["x"], inp["mem"], inp["dy"], lr=lr, dx=dx, dmem=dmem)
+        for i in range(3):
+            g.replay()
+            got = snapshot(part, {"dx": dx})
+            for a, b in zip(eager[i], got):
+                assert np.isfinite(a).all()
+                assert np.array_equal(a, b), f"replay {i}"
+
+
 def test_boundary_gradient_scaling_is_exact():
     """Gradients are linear in the boundary gradient; doubling it doubles every
     gradient bit for bit (power-of-two scaling commutes with rounding)."""

@@ -72,9 +72,13 @@ struct LayerWs {
     void *v = nullptr, *a = nullptr;
 };
 
+constexpr int ELT_RING = 10;  // bf16 residual-gradient buffers (see layer_backward)
+
 struct BwdWs {
     float *p32 = nullptr, *q32 = nullptr, *dn = nullptr, *delta = nullptr, *partial = nullptr, *dmem32 = nullptr;
-    void *pe = nullptr, *qe = nullptr, *dz = nullptr, *dc = nullptr, *dqkv = nullptr, *dxq = nullptr, *dxkv = nullptr;
+    void* ring[ELT_RING] = {};  // dL/dx in the partition dtype, rotating across layers
+    void *dc = nullptr;
+    void *dz[2] = {}, *dqkv[2] = {}, *dxq[2] = {}, *dxkv[2] = {};  // by layer parity
     double *loss_partial = nullptr, *loss_acc = nullptr;
     int* flag = nullptr;
     float* splitk = nullptr;   // split-K partial tiles (caller's stream)
@@ -149,9 +153,12 @@ struct gp_partition {
     // Weight-gradient GEMMs run on a second stream (GP_SIDE_STREAM=0 turns it
     // off), ordered against the caller's stream by events from a ring.
     bool use_side = true;
+    // when weight-gradient GEMMs are handed to the side stream (GP_DW_FLUSH):
+    // 0 each as soon as its inputs are enqueued, 1 after the feed-forward
+    // block and at the end of the layer, 2 at the end of the layer
+    int dw_flush = 0;
     hipStream_t side = nullptr;
-    std::vector<hipEvent_t> ring;
-    int ring_next = 0;
+    hipEvent_t side_fork = nullptr, side_done[4] = {};
     // Recompute-ahead (GP_REMAT_AHEAD=0 turns it off): while micro-batch m is
     // back-propagated, micro-batch m - 1 is re-materialised on a third stream
     // into the other workspace set.
@@ -208,18 +215,19 @@ void plan_workspace(gp_partition* p, Arena& a) {
     BwdWs& b = p->bw;
     b.p32 = a.take<float>(T * D);
     b.q32 = a.take<float>(T * D);
-    b.pe = a.take_elt(T * D, e);
-    b.qe = a.take_elt(T * D, e);
+    for (auto& r : b.ring) r = a.take_elt(T * D, e);
     b.dn = a.take<float>(T * D);
-    b.dz = a.take_elt(T * F, e);
     b.dc = a.take_elt(T * D, e);
-    b.dqkv = a.take_elt(T * 3 * D, e);
-    b.delta = a.take<float>(lse_n);
-    if (dec) {
-        b.dxq = a.take_elt(T * D, e);
-        b.dxkv = a.take_elt(Tm * 2 * D, e);
-        b.dmem32 = a.take<float>(Tm * D);
+    for (int i = 0; i < 2; ++i) {
+        b.dz[i] = a.take_elt(T * F, e);
+        b.dqkv[i] = a.take_elt(T * 3 * D, e);
+        if (dec) {
+            b.dxq[i] = a.take_elt(T * D, e);
+            b.dxkv[i] = a.take_elt(Tm * 2 * D, e);
+        }
     }
+    b.delta = a.take<float>(lse_n);
+    if (dec) b.dmem32 = a.take<float>(Tm * D);
     long maxN = 3 * D > F ? 3 * D : F;
     if (g.loss == GP_LOSS_XENT_LS && g.V > maxN) maxN = g.V;
     size_t part = (size_t)layernorm_bwd_blocks(T) * 2 * D;
@@ -262,56 +270,6 @@ Ctx make_ctx(gp_partition* p, hipStream_t st, Lane lane = Lane::Main) {
     c.ws = lane == Lane::Side ? p->bw.splitk_side : lane == Lane::Remat ? p->bw.splitk_remat : p->bw.splitk;
     return c;
 }
-
-// Ordering between the caller's stream (main) and the weight-gradient stream
-// (side).  A side launch first waits for everything enqueued on main so far;
-// it then records an event, remembered against the buffers it reads.  Before
-// main overwrites such a buffer it waits for that event; at the end of a
-// backward call main waits for the side's last event.  Without a side stream
-// every launch goes to main and nothing here does anything.
-struct SideSync {
-    gp_partition* p;
-    hipStream_t main, side;
-    std::vector<std::pair<const void*, hipEvent_t>> reads;
-    hipEvent_t last = nullptr;
-
-    bool on() const { return side != nullptr; }
-    hipEvent_t next_event() {
-        hipEvent_t e = p->ring[p->ring_next];
-        p->ring_next = (p->ring_next + 1) % (int)p->ring.size();
-        return e;
-    }
-    gp_status fork() {
-        const hipEvent_t e = next_event();
-        GP_HIP(hipEventRecord(e, main));
-        GP_HIP(hipStreamWaitEvent(side, e, 0));
-        return GP_OK;
-    }
-    gp_status done_reading(std::initializer_list<const void*> bufs) {
-        const hipEvent_t e = next_event();
-        GP_HIP(hipEventRecord(e, side));
-        for (const void* b : bufs) reads.emplace_back(b, e);
-        last = e;
-        return GP_OK;
-    }
-    gp_status before_write(const void* buf) {
-        for (size_t i = 0; i < reads.size();) {
-            if (reads[i].first == buf) {
-                GP_HIP(hipStreamWaitEvent(main, reads[i].second, 0));
-                reads.erase(reads.begin() + (long)i);
-            } else {
-                ++i;
-            }
-        }
-        return GP_OK;
-    }
-    gp_status join() {
-        if (last) GP_HIP(hipStreamWaitEvent(main, last, 0));
-        reads.clear();
-        last = nullptr;
-        return GP_OK;
-    }
-};
 
 #define GP_TRY(x)                    \
     do {                             \
@@ -458,14 +416,15 @@ gp_status linear_dw(const Ctx& c, const Linear& L, const void* X, const void* dY
     return timed_gemm(c, L.role + 2, g, EPI_ACC_F32, false);
 }
 
-// The weight-gradient GEMM on the side stream when there is one.
-gp_status linear_dw_async(const Ctx& c, const Ctx& cs, SideSync& sy, const Linear& L, const void* X, const void* dY,
-                          long rows, int accumulate) {
-    if (!sy.on()) return linear_dw(c, L, X, dY, rows, accumulate);
-    GP_TRY(sy.fork());
-    GP_TRY(linear_dw(cs, L, X, dY, rows, accumulate));
-    return sy.done_reading({X, dY});
-}
+// A weight-gradient GEMM of one layer, collected while the layer's input-
+// gradient chain is enqueued and launched afterwards (on the side stream when
+// there is one).
+struct DwJob {
+    const Linear* L;
+    const void* X;
+    const void* dY;
+    long rows;
+};
 
 gp_status norm_bwd(const Ctx& c, const Norm& N, const float* dn, const float* x, const float* stats, long rows,
                    const float* dres, float* dx32, void* dxe, int accumulate) {
@@ -567,10 +526,17 @@ gp_status partition_forward(const Ctx& c, int m, bool keep, const void* x, const
 }
 
 // Backward of one layer.  dY arrives in (in32, ine); dX leaves in the pair
-// returned through out32/oute (one of the two backward pairs).
-gp_status layer_backward(const Ctx& c, const Ctx& cs, SideSync& sy, int set, int l, bool first, float* in32, void* ine,
-                         float* sc32, void* sce, float*& out32, void*& oute, float* dx32_final, void* dxe_final,
-                         const void* mem) {
+// returned through out32/oute.  The fp32 halves ping-pong between the two
+// backward buffers; every bf16 gradient the layer writes takes the next
+// buffer of the ring (`ri`), and dz / dQKV (and the cross-attention dQ, dKV)
+// alternate by layer parity, so that the layer's weight-gradient GEMMs -- which
+// read ine, the LayerNorm outputs, dz and dQKV -- can run while the next layer
+// down is processed.  They are appended to `jobs` and launched by `flush`
+// at the granularity the partition is set to (the caller flushes the rest).
+template <class Flush>
+gp_status layer_backward(const Ctx& c, int set, int l, bool first, float* in32, void* ine, float* sc32, int& ri,
+                         float*& out32, void*& oute, float* dx32_final, void* dxe_final, const void* mem,
+                         std::vector<DwJob>& jobs, Flush&& flush) {
     gp_partition* p = c.p;
     const LayerPlan& P = p->plan.layers[l];
     LayerWs& w = p->lw[set][l];
@@ -578,24 +544,33 @@ gp_status layer_backward(const Ctx& c, const Ctx& cs, SideSync& sy, int set, int
     const long T = p->g.T(), Tm = p->g.Tm(), D = p->d.D;
     const bool dec = p->g.kind == GP_DECODER_CROSS;
     const int acc = first ? 0 : 1;
+    const int par = l & 1;
+    auto next_elt = [&]() {
+        void* r = b.ring[ri];
+        ri = (ri + 1) % ELT_RING;
+        return r;
+    };
     const float* xf = dec ? w.x2 : w.x1;
     const Norm& nf = dec ? P.ln3 : P.ln2;
-    // feed-forward block:  dW2, db2;  dz = dY W2^T * [a > 0];  dW1, db1;  dv = dz W1^T
-    GP_TRY(linear_dw_async(c, cs, sy, P.ffn2, w.a, ine, T, acc));
-    GP_TRY(sy.before_write(b.dz));
-    GP_TRY(linear_dx(c, P.ffn2, ine, T, b.dz, EPI_RELU_MASK, w.a, 0));
-    GP_TRY(linear_dw_async(c, cs, sy, P.ffn1, w.v, b.dz, T, acc));
-    GP_TRY(linear_dx(c, P.ffn1, b.dz, T, b.dn, EPI_F32, nullptr, 0));
-    GP_TRY(sy.before_write(sce));
+    // feed-forward block:  dz = dY W2^T * [a > 0];  dv = dz W1^T;  dW2, dW1 (and biases) as jobs
+    // flush(0): after each weight-gradient job; flush(1): after the feed-forward block
+    jobs.push_back({&P.ffn2, w.a, ine, T});
+    GP_TRY(flush(0));
+    GP_TRY(linear_dx(c, P.ffn2, ine, T, b.dz[par], EPI_RELU_MASK, w.a, 0));
+    jobs.push_back({&P.ffn1, w.v, b.dz[par], T});
+    GP_TRY(flush(0));
+    GP_TRY(linear_dx(c, P.ffn1, b.dz[par], T, b.dn, EPI_F32, nullptr, 0));
+    GP_TRY(flush(1));
+    void* sce = next_elt();
     GP_TRY(norm_bwd(c, nf, b.dn, xf, w.stf, T, in32, sc32, sce, acc));
     // (sc) = dL/d(xf)
     float* cur32 = sc32;
     void* cure = sce;
     float* oth32 = in32;
-    void* othe = ine;
     if (dec) {
         // cross-attention block
-        GP_TRY(linear_dw_async(c, cs, sy, P.xo, w.xc, cure, T, acc));
+        jobs.push_back({&P.xo, w.xc, cure, T});
+        GP_TRY(flush(0));
         GP_TRY(linear_dx(c, P.xo, cure, T, b.dc, EPI_STORE, nullptr, 0));
         AttnArgs x = attn_args(p, p->g.Smem, 0);
         x.q = w.xq;
@@ -608,26 +583,27 @@ gp_status layer_backward(const Ctx& c, const Ctx& cs, SideSync& sy, int set, int
         x.lse = w.xlse;
         x.dout = b.dc;
         x.lddo = D;
-        x.dq = b.dxq;
+        x.dq = b.dxq[par];
         x.lddq = D;
-        x.dk = b.dxkv;
-        x.dv = p->off_elt(b.dxkv, D);
+        x.dk = b.dxkv[par];
+        x.dv = p->off_elt(b.dxkv[par], D);
         x.lddk = x.lddv = 2 * D;
         x.delta = b.delta;
-        GP_TRY(sy.before_write(b.dxq));
-        GP_TRY(sy.before_write(b.dxkv));
         GP_TRY(timed_attention(c, GP_K_XATTN_BWD, x, true));
-        GP_TRY(linear_dw_async(c, cs, sy, P.xq, w.uc, b.dxq, T, acc));
-        GP_TRY(linear_dx(c, P.xq, b.dxq, T, b.dn, EPI_F32, nullptr, 0));
-        GP_TRY(linear_dw_async(c, cs, sy, P.xkv, mem, b.dxkv, Tm, acc));
-        GP_TRY(linear_dx(c, P.xkv, b.dxkv, Tm, b.dmem32, EPI_ACC_F32, nullptr, l == p->d.L - 1 ? 0 : 1));
-        GP_TRY(sy.before_write(othe));
-        GP_TRY(norm_bwd(c, P.ln2, b.dn, w.x1, w.stc, T, cur32, oth32, othe, acc));
+        jobs.push_back({&P.xq, w.uc, b.dxq[par], T});
+        GP_TRY(flush(0));
+        GP_TRY(linear_dx(c, P.xq, b.dxq[par], T, b.dn, EPI_F32, nullptr, 0));
+        jobs.push_back({&P.xkv, mem, b.dxkv[par], Tm});
+        GP_TRY(flush(0));
+        GP_TRY(linear_dx(c, P.xkv, b.dxkv[par], Tm, b.dmem32, EPI_ACC_F32, nullptr, l == p->d.L - 1 ? 0 : 1));
+        void* e2 = next_elt();
+        GP_TRY(norm_bwd(c, P.ln2, b.dn, w.x1, w.stc, T, cur32, oth32, e2, acc));
         std::swap(cur32, oth32);
-        std::swap(cure, othe);
+        cure = e2;
     }
     // self-attention block
-    GP_TRY(linear_dw_async(c, cs, sy, P.o, w.c, cure, T, acc));
+    jobs.push_back({&P.o, w.c, cure, T});
+    GP_TRY(flush(0));
     GP_TRY(linear_dx(c, P.o, cure, T, b.dc, EPI_STORE, nullptr, 0));
     AttnArgs a = attn_args(p, p->g.S, dec ? 1 : 0);
     a.q = w.qkv;
@@ -639,25 +615,25 @@ gp_status layer_backward(const Ctx& c, const Ctx& cs, SideSync& sy, int set, int
     a.lse = w.lse;
     a.dout = b.dc;
     a.lddo = D;
-    a.dq = b.dqkv;
-    a.dk = p->off_elt(b.dqkv, D);
-    a.dv = p->off_elt(b.dqkv, 2 * D);
+    a.dq = b.dqkv[par];
+    a.dk = p->off_elt(b.dqkv[par], D);
+    a.dv = p->off_elt(b.dqkv[par], 2 * D);
     a.lddq = a.lddk = a.lddv = 3 * D;
     a.delta = b.delta;
-    GP_TRY(sy.before_write(b.dqkv));
     GP_TRY(timed_attention(c, GP_K_ATTN_BWD, a, true));
-    GP_TRY(linear_dw_async(c, cs, sy, P.qkv, w.u, b.dqkv, T, acc));
-    GP_TRY(linear_dx(c, P.qkv, b.dqkv, T, b.dn, EPI_F32, nullptr, 0));
+    jobs.push_back({&P.qkv, w.u, b.dqkv[par], T});
+    GP_TRY(flush(0));
+    GP_TRY(linear_dx(c, P.qkv, b.dqkv[par], T, b.dn, EPI_F32, nullptr, 0));
     const float* x_in = p->xs[set][l];
     if (dxe_final || dx32_final || l == 0) {
         GP_TRY(norm_bwd(c, P.ln1, b.dn, x_in, w.st1, T, cur32, dx32_final, dxe_final, acc));
         out32 = dx32_final;
         oute = dxe_final;
     } else {
-        GP_TRY(sy.before_write(othe));
-        GP_TRY(norm_bwd(c, P.ln1, b.dn, x_in, w.st1, T, cur32, oth32, othe, acc));
+        void* oe = next_elt();
+        GP_TRY(norm_bwd(c, P.ln1, b.dn, x_in, w.st1, T, cur32, oth32, oe, acc));
         out32 = oth32;
-        oute = othe;
+        oute = oe;
     }
     return GP_OK;
 }
@@ -676,7 +652,7 @@ gp_status head_backward(const Ctx& c, int set, bool first, const int* labels) {
     GP_TRY(loss_finalize(b.loss_partial, (int)T, b.loss_acc, acc, c.st));
     GP_TRY(linear_dw(c, Hd.out, b.h, b.z, T, acc));
     GP_TRY(linear_dx(c, Hd.out, b.z, T, b.dn, EPI_F32, nullptr, 0));
-    return norm_bwd(c, Hd.lnf, b.dn, y, b.sth, T, nullptr, b.p32, b.pe, acc);
+    return norm_bwd(c, Hd.lnf, b.dn, y, b.sth, T, nullptr, b.p32, b.ring[0], acc);
 }
 
 gp_status upload_param_block(gp_partition* p, const ParamRef& r, const float* host) {
@@ -691,10 +667,12 @@ gp_status upload_param_block(gp_partition* p, const ParamRef& r, const float* ho
 }
 
 void free_all(gp_partition* p) {
-    for (hipEvent_t e : p->ring)
+    for (hipEvent_t& e : p->side_done) {
         if (e) (void)hipEventDestroy(e);
-    p->ring.clear();
-    p->ring_next = 0;
+        e = nullptr;
+    }
+    if (p->side_fork) (void)hipEventDestroy(p->side_fork);
+    p->side_fork = nullptr;
     if (p->side) (void)hipStreamDestroy(p->side);
     p->side = nullptr;
     for (hipEvent_t e : {p->remat_fork, p->remat_done})
@@ -769,6 +747,7 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
     if (const char* e = std::getenv("GP_TIMER_MARKERS")) p->timer.markers = std::atoi(e) != 0;
     if (const char* e = std::getenv("GP_SIDE_STREAM")) p->use_side = std::atoi(e) != 0;
     if (const char* e = std::getenv("GP_REMAT_AHEAD")) p->remat_ahead = std::atoi(e) != 0;
+    if (const char* e = std::getenv("GP_DW_FLUSH")) p->dw_flush = std::atoi(e);
     p->nsets = (p->remat_ahead && g.M >= 2) ? 2 : 1;
     if (const char* e = std::getenv("GP_GEMM_TILE")) p->gemm_tile = std::atoi(e);
     if (const char* e = std::getenv("GP_GEMM_SPLITS")) p->gemm_splits = std::atoi(e);
@@ -820,9 +799,8 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
     if (p->use_side) {
         // default priority, like every stream of the library
         e = hipStreamCreateWithFlags(&p->side, hipStreamNonBlocking);
-        p->ring.assign(32, nullptr);
-        for (size_t i = 0; e == hipSuccess && i < p->ring.size(); ++i)
-            e = hipEventCreateWithFlags(&p->ring[i], hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&p->side_fork, hipEventDisableTiming);
+        for (int i = 0; e == hipSuccess && i < 4; ++i) e = hipEventCreateWithFlags(&p->side_done[i], hipEventDisableTiming);
     }
     if (e == hipSuccess && p->nsets > 1) {
         e = hipStreamCreateWithFlags(&p->remat, hipStreamNonBlocking);
@@ -951,7 +929,7 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     if (!dec && dmem) return set_error(GP_ERR_INVALID_ARG, "encoder partitions have no memory gradient");
     Ctx c = make_ctx(p, (hipStream_t)stream);
     Ctx cs = make_ctx(p, p->side, Lane::Side);
-    SideSync sy{p, (hipStream_t)stream, p->use_side ? p->side : nullptr};
+    const bool side = p->use_side && p->side;
     const bool first = p->sched.first_backward();
     const long T = p->g.T(), D = p->d.D;
     const int set = p->nsets > 1 ? (mb & 1) : 0;
@@ -979,45 +957,66 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
         p->remat_pending = mb - 1;
     }
     BwdWs& b = p->bw;
-    // dL/dy of the partition output
+    // dL/dy of the partition output into (p32, ring[0])
     if (p->g.loss == GP_LOSS_NONE) {
-        s = intake(c.dt, dy_or_target, b.pe, b.p32, T * D, c.st);
+        s = intake(c.dt, dy_or_target, b.ring[0], b.p32, T * D, c.st);
     } else if (p->g.loss == GP_LOSS_MSE) {
         int nb = 0;
         const double norm = (double)p->g.n * p->g.M * p->g.S * D;
-        s = mse_grad(c.dt, p->xs[set][p->d.L], dy_or_target, T * D, norm, b.p32, b.pe, b.loss_partial, &nb, c.st);
+        s = mse_grad(c.dt, p->xs[set][p->d.L], dy_or_target, T * D, norm, b.p32, b.ring[0], b.loss_partial, &nb,
+                     c.st);
         if (s == GP_OK) s = loss_finalize(b.loss_partial, nb, b.loss_acc, first ? 0 : 1, c.st);
     } else {
         s = head_backward(c, set, first, reinterpret_cast<const int*>(dy_or_target));
     }
     if (s != GP_OK) return s;
     const void* mem_m = dec ? p->stash_m_mb(mb) : nullptr;
+    // Layer l's weight-gradient GEMMs run on the side stream while layer l - 1
+    // is processed.  Layer l - 2 rewrites parity and ring buffers that layer l's
+    // GEMMs read, so it first waits for them (side_done[l % 4]).
+    const int acc = first ? 0 : 1;
     float* in32 = b.p32;
-    void* ine = b.pe;
+    void* ine = b.ring[0];
     float* sc32 = b.q32;
-    void* sce = b.qe;
+    int ri = 1;
+    std::vector<DwJob> jobs;
+    hipEvent_t last_done = nullptr;  // latest side-stream event of this call
+    auto fail = [&](gp_status st) {
+        if (last_done) (void)hipStreamWaitEvent(c.st, last_done, 0);
+        return st;
+    };
     for (int l = p->d.L - 1; l >= 0; --l) {
+        if (side && l + 2 <= p->d.L - 1) GP_HIP(hipStreamWaitEvent(c.st, p->side_done[(l + 2) % 4], 0));
         float* out32 = nullptr;
         void* oute = nullptr;
-        s = layer_backward(c, cs, sy, set, l, first, in32, ine, sc32, sce, out32, oute, nullptr, l == 0 ? dx : nullptr,
-                           mem_m);
-        if (s != GP_OK) {
-            (void)sy.join();
-            return s;
+        jobs.clear();
+        // launch the collected weight-gradient GEMMs (after everything enqueued on main so far)
+        auto flush = [&](int level) -> gp_status {
+            if (jobs.empty() || level < p->dw_flush) return GP_OK;
+            if (side) {
+                GP_HIP(hipEventRecord(p->side_fork, c.st));
+                GP_HIP(hipStreamWaitEvent(cs.st, p->side_fork, 0));
+            }
+            for (const DwJob& j : jobs) GP_TRY(linear_dw(side ? cs : c, *j.L, j.X, j.dY, j.rows, acc));
+            jobs.clear();
+            return GP_OK;
+        };
+        s = layer_backward(c, set, l, first, in32, ine, sc32, ri, out32, oute, nullptr, l == 0 ? dx : nullptr, mem_m,
+                           jobs, flush);
+        if (s == GP_OK) s = flush(2);
+        if (s != GP_OK) return fail(s);
+        if (side) {
+            GP_HIP(hipEventRecord(p->side_done[l % 4], cs.st));
+            last_done = p->side_done[l % 4];
         }
         if (l > 0) {
-            // the pair not holding dX becomes scratch for the next layer
-            float* f32 = (out32 == b.p32) ? b.q32 : b.p32;
-            void* fe = (oute == b.pe) ? b.qe : b.pe;
+            sc32 = (out32 == b.p32) ? b.q32 : b.p32;
             in32 = out32;
             ine = oute;
-            sc32 = f32;
-            sce = fe;
         }
     }
     // the caller's stream resumes only after the last weight-gradient GEMM
-    s = sy.join();
-    if (s != GP_OK) return s;
+    if (side) GP_HIP(hipStreamWaitEvent(c.st, p->side_done[0], 0));
     if (dec && dmem) {
         s = cast_out(c.dt, b.dmem32, dmem, p->g.Tm() * D, c.st);
         if (s != GP_OK) return s;

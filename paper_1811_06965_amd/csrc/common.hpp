@@ -55,10 +55,12 @@ template <> struct Vec16<float> {
 
 } // namespace gp
 
-// Host-side launch checking (used inside functions returning gp_status).
+// Host-side launch checking (used inside functions returning gp_status):
+// reports the first failed launch (klaunch) of the calling thread since the
+// last check.
 #define GP_LAUNCH_CHECK()                                                   \
     do {                                                                    \
-        hipError_t e_ = hipGetLastError();                                  \
+        hipError_t e_ = ::gp::take_launch_status();                          \
         if (e_ != hipSuccess) return ::gp::hip_fail(e_, __FILE__, __LINE__); \
     } while (0)
 
@@ -84,6 +86,13 @@ struct LaunchEvents {
     bool started = false;
 };
 LaunchEvents& launch_events();
+hipError_t& launch_status();  // first failed launch of the calling thread, or hipSuccess
+inline hipError_t take_launch_status() {
+    hipError_t& e = launch_status();
+    const hipError_t r = e;
+    e = hipSuccess;
+    return r;
+}
 
 // Kernel launch.  While a role is timed, through hipExtLaunchKernelGGL with
 // the timing events attached to the dispatch (no extra stream packets);
@@ -92,21 +101,23 @@ LaunchEvents& launch_events();
 template <typename... Args, typename... P>
 inline void klaunch(void (*k)(Args...), dim3 grid, dim3 block, uint32_t shmem, hipStream_t st, P... p) {
     LaunchEvents& ev = launch_events();
-    if (ev.stop) {
-        hipEvent_t e0 = nullptr;
-        if (!ev.started) {
-            e0 = ev.start;
-            ev.started = true;
-        }
-        hipExtLaunchKernelGGL(k, grid, block, shmem, st, e0, ev.stop, 0u, static_cast<Args>(p)...);
-        return;
-    }
     auto args = std::make_tuple(static_cast<Args>(p)...);
     void* ptrs[sizeof...(Args) > 0 ? sizeof...(Args) : 1];
     std::apply([&](auto&... a) {
         int i = 0;
         ((ptrs[i++] = static_cast<void*>(&a)), ...);
     }, args);
-    (void)hipLaunchKernel(reinterpret_cast<const void*>(k), grid, block, ptrs, shmem, st);
+    hipError_t e;
+    if (ev.stop) {
+        hipEvent_t e0 = nullptr;
+        if (!ev.started) {
+            e0 = ev.start;
+            ev.started = true;
+        }
+        e = hipExtLaunchKernel(reinterpret_cast<const void*>(k), grid, block, ptrs, shmem, st, e0, ev.stop, 0);
+    } else {
+        e = hipLaunchKernel(reinterpret_cast<const void*>(k), grid, block, ptrs, shmem, st);
+    }
+    if (e != hipSuccess && launch_status() == hipSuccess) launch_status() = e;
 }
 }

@@ -607,8 +607,10 @@ __device__ __forceinline__ bf16x8 tr_frag(const char* p, int second) {
 // destination) is wave-uniform; fragment offsets are precomputed and the stage
 // base folds into the ds_read immediate because the k-tile loop is unrolled
 // over the stages.
-template <int BM, int BN, int WM, int WN, int NSTAGE, int EPI, bool SPLIT, bool KM>
+template <int BM, int BN, int WM, int WN, int NSTAGE, int EPI, int SM, bool KM>
 __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
+    // SM: 0 no split-K; 1 split-K, partial tiles only (summed by splitk_reduce)
+    constexpr bool SPLIT = SM != 0;
     constexpr int BK = 64, KS = 4, NW = WM * WN;
     constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
     constexpr int STAGE = (BM + BN) * 128;
@@ -864,7 +866,9 @@ __global__ void __launch_bounds__(256) splitk_reduce(GemmArgs args, int splits) 
 enum TileCfg {
     T256x256 = 0, T256x128 = 1, T128x256 = 2, T128x128 = 3,  // register-staged (any operand form)
     T_DL128x128_S2 = 4, T_DL128x128_S3 = 5, T_DL256x128_S2 = 6, T_DL256x256_S2 = 7,  // direct-to-LDS, k-contiguous
-    T_DL256x256_W8 = 8, T_DL256x128_W8 = 9, T_DL128x256_W8 = 10                          // ... with 8 waves
+    T_DL256x256_W8 = 8, T_DL256x128_W8 = 9, T_DL128x256_W8 = 10,                          // ... with 8 waves
+    T_DL128x128_W8A = 11, T_DL128x128_W8B = 12, T_DL256x128_W8S3 = 13, T_DL128x256_W8S3 = 14,
+    T_LAST = T_DL128x256_W8S3
 };
 
 template <typename T, int BM, int BN, bool AK, bool BKM>
@@ -907,7 +911,7 @@ gp_status launch_dl(const GemmArgs& a, int epi, int splits, hipStream_t st) {
     const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
     if (splits > 1) {
         dim3 grid(tiles, splits);
-        klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_F32, true, KM>, grid, NT, 0, st, a);
+        klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_F32, 1, KM>, grid, NT, 0, st, a);
         GP_LAUNCH_CHECK();
         const long nq = (long)a.M * (a.N / 4);
         const int rg = (int)std::min<long>((nq + 255) / 256, 2048);
@@ -926,16 +930,16 @@ gp_status launch_dl(const GemmArgs& a, int epi, int splits, hipStream_t st) {
     }
     if constexpr (KM) {
         switch (epi) {
-        case EPI_STORE: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_STORE, false, KM>, tiles, NT, 0, st, a); break;
-        case EPI_RES_F32: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_RES_F32, false, KM>, tiles, NT, 0, st, a); break;
-        case EPI_F32: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_F32, false, KM>, tiles, NT, 0, st, a); break;
-        case EPI_RELU_MASK: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_RELU_MASK, false, KM>, tiles, NT, 0, st, a); break;
-        case EPI_ACC_F32: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_ACC_F32, false, KM>, tiles, NT, 0, st, a); break;
+        case EPI_STORE: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_STORE, 0, KM>, tiles, NT, 0, st, a); break;
+        case EPI_RES_F32: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_RES_F32, 0, KM>, tiles, NT, 0, st, a); break;
+        case EPI_F32: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_F32, 0, KM>, tiles, NT, 0, st, a); break;
+        case EPI_RELU_MASK: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_RELU_MASK, 0, KM>, tiles, NT, 0, st, a); break;
+        case EPI_ACC_F32: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_ACC_F32, 0, KM>, tiles, NT, 0, st, a); break;
         default: return set_error(GP_ERR_INVALID_ARG, "gemm: epilogue not instantiated for k-contiguous operands");
         }
     } else {
         switch (epi) {
-        case EPI_ACC_F32: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_ACC_F32, false, KM>, tiles, NT, 0, st, a); break;
+        case EPI_ACC_F32: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_ACC_F32, 0, KM>, tiles, NT, 0, st, a); break;
         default: return set_error(GP_ERR_INVALID_ARG, "gemm: epilogue not instantiated for m-contiguous operands");
         }
     }
@@ -955,6 +959,10 @@ gp_status launch_bf16(const GemmArgs& a, int epi, int cfg, int splits, hipStream
         case T_DL256x256_W8: return launch_dl<256, 256, 2, 4, 2, KM>(a, epi, splits, st);
         case T_DL256x128_W8: return launch_dl<256, 128, 4, 2, 2, KM>(a, epi, splits, st);
         case T_DL128x256_W8: return launch_dl<128, 256, 2, 4, 2, KM>(a, epi, splits, st);
+        case T_DL128x128_W8A: return launch_dl<128, 128, 2, 4, 2, KM>(a, epi, splits, st);
+        case T_DL128x128_W8B: return launch_dl<128, 128, 4, 2, 2, KM>(a, epi, splits, st);
+        case T_DL256x128_W8S3: return launch_dl<256, 128, 4, 2, 3, KM>(a, epi, splits, st);
+        case T_DL128x256_W8S3: return launch_dl<128, 256, 2, 4, 3, KM>(a, epi, splits, st);
         default: break;
         }
     }
@@ -980,20 +988,23 @@ bool split_fits(const GemmArgs& a, int s, int nk) {
     return a.ws != nullptr && nk / s >= 4 && need <= a.ws_elems && a.N % 4 == 0;
 }
 
-// Direct-to-LDS tiles (k-contiguous operands, K % 64 == 0): time = fixed
-// launch/epilogue cost + rounds x k-steps x per-step time of the tile shape
-// (per-step times fitted to measurements on MI355X over the d_model 1024
-// partition's GEMMs; a 128x128 tile runs two per CU, the 8-wave tiles one),
-// plus the split-K partial traffic.  Units: microseconds.
+// Direct-to-LDS tiles (K % 64 == 0): time = fixed launch cost + rounds x
+// k-steps x per-step time of the tile shape (with the tile running alone on
+// its CU or sharing it with a second one) + the fp32 read-modify-write of an
+// accumulating epilogue + the split-K partial traffic and reduce.  The
+// per-step times and costs were fitted to measurements of the d_model 1024
+// partition's GEMMs on MI355X at 512 and 2048 token rows.  Units: us.
 void choose_dl(const GemmArgs& a, int epi, int& cfg, int& splits) {
     struct Cand { int cfg, bm, bn, resident; double step_alone, step_full; };
-    static const Cand cands[4] = {{T_DL128x128_S2, 128, 128, 2, 0.583, 0.877},
-                                  {T_DL256x256_W8, 256, 256, 1, 1.273, 1.273},
-                                  {T_DL256x128_W8, 256, 128, 1, 0.839, 0.839},
-                                  {T_DL128x256_W8, 128, 256, 1, 0.727, 0.727}};
+    static const Cand cands[5] = {{T_DL128x128_W8A, 128, 128, 2, 0.516, 0.903},
+                                  {T_DL128x128_S2, 128, 128, 2, 0.587, 1.012},
+                                  {T_DL256x256_W8, 256, 256, 1, 1.360, 1.360},
+                                  {T_DL256x128_W8, 256, 128, 1, 0.815, 0.815},
+                                  {T_DL128x256_W8, 128, 256, 1, 0.766, 0.766}};
+    constexpr double BW = 3.976e6;  // bytes per us of split partials / accumulator traffic
     const int nk = a.K / 64;
     double best = 1e300;
-    cfg = T_DL128x128_S2;
+    cfg = T_DL128x128_W8A;
     splits = 1;
     for (const Cand& c : cands) {
         const long tiles = (long)((a.M + c.bm - 1) / c.bm) * ((a.N + c.bn - 1) / c.bn);
@@ -1002,8 +1013,9 @@ void choose_dl(const GemmArgs& a, int epi, int& cfg, int& splits) {
             const long per_cu = (tiles * s + NUM_CU - 1) / NUM_CU;
             const long rounds = (per_cu + c.resident - 1) / c.resident;
             const double step = per_cu >= c.resident ? c.step_full : c.step_alone;
-            double t = 6.66 + rounds * (double)((nk + s - 1) / s) * step;
-            if (s > 1) t += (double)a.M * a.N * 4.0 * (s + 1.0) / 2.0 / 1.75e6 + 2.5;
+            double t = 3.889 + rounds * (double)((nk + s - 1) / s) * step;
+            if (epi == EPI_ACC_F32) t += 1.074 + (double)a.M * a.N * 8.0 / BW;
+            if (s > 1) t += (double)a.M * a.N * 4.0 * (s + 1.0) / 2.0 / BW + 7.233;
             if (t < best * 0.999) {
                 best = t;
                 cfg = c.cfg;
@@ -1069,7 +1081,7 @@ gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dty
             choose_dl(a, epi, cfg, splits);
         else
             choose(a, epi, cfg, splits);
-        if (a.force_cfg >= 0 && a.force_cfg <= T_DL128x256_W8) {
+        if (a.force_cfg >= 0 && a.force_cfg <= T_LAST) {
             cfg = a.force_cfg;
             splits = a.force_splits > 0 ? a.force_splits : 1;
             if (splits > 1 && !split_fits(a, splits, (a.K + 63) / 64)) splits = 1;

@@ -155,18 +155,18 @@ int xent_partials(long rows) { return (int)rows; }
 
 gp_status intake(int dtype, const void* src, void* stash, float* x32, long count, hipStream_t st) {
     if (dtype == GP_BF16)
-        intake_kernel<bf16><<<ew_grid(count), 256, 0, st>>>(reinterpret_cast<const bf16*>(src),
+        klaunch(intake_kernel<bf16>, ew_grid(count), 256, 0, st, reinterpret_cast<const bf16*>(src),
                                                              reinterpret_cast<bf16*>(stash), x32, count);
     else
-        intake_kernel<float><<<ew_grid(count), 256, 0, st>>>(reinterpret_cast<const float*>(src),
+        klaunch(intake_kernel<float>, ew_grid(count), 256, 0, st, reinterpret_cast<const float*>(src),
                                                               reinterpret_cast<float*>(stash), x32, count);
     GP_LAUNCH_CHECK();
     return GP_OK;
 }
 
 gp_status cast_out(int dtype, const float* src, void* dst, long count, hipStream_t st) {
-    if (dtype == GP_BF16) cast_kernel<bf16><<<ew_grid(count), 256, 0, st>>>(src, reinterpret_cast<bf16*>(dst), count);
-    else cast_kernel<float><<<ew_grid(count), 256, 0, st>>>(src, reinterpret_cast<float*>(dst), count);
+    if (dtype == GP_BF16) klaunch(cast_kernel<bf16>, ew_grid(count), 256, 0, st, src, reinterpret_cast<bf16*>(dst), count);
+    else klaunch(cast_kernel<float>, ew_grid(count), 256, 0, st, src, reinterpret_cast<float*>(dst), count);
     GP_LAUNCH_CHECK();
     return GP_OK;
 }
@@ -175,17 +175,17 @@ gp_status mse_grad(int dtype, const float* y, const void* target, long count, do
                    double* partial, int* nblk, hipStream_t st) {
     *nblk = LOSS_BLOCKS;
     if (dtype == GP_BF16)
-        mse_kernel<bf16><<<LOSS_BLOCKS, 256, 0, st>>>(y, reinterpret_cast<const bf16*>(target), count, norm, d32,
+        klaunch(mse_kernel<bf16>, LOSS_BLOCKS, 256, 0, st, y, reinterpret_cast<const bf16*>(target), count, norm, d32,
                                                       reinterpret_cast<bf16*>(delt), partial);
     else
-        mse_kernel<float><<<LOSS_BLOCKS, 256, 0, st>>>(y, reinterpret_cast<const float*>(target), count, norm, d32,
+        klaunch(mse_kernel<float>, LOSS_BLOCKS, 256, 0, st, y, reinterpret_cast<const float*>(target), count, norm, d32,
                                                        reinterpret_cast<float*>(delt), partial);
     GP_LAUNCH_CHECK();
     return GP_OK;
 }
 
 gp_status loss_finalize(const double* partial, int nblk, double* acc, int accumulate, hipStream_t st) {
-    loss_finalize_kernel<<<1, 64, 0, st>>>(partial, nblk, acc, accumulate);
+    klaunch(loss_finalize_kernel, 1, 64, 0, st, partial, nblk, acc, accumulate);
     GP_LAUNCH_CHECK();
     return GP_OK;
 }
@@ -193,15 +193,15 @@ gp_status loss_finalize(const double* partial, int nblk, double* acc, int accumu
 gp_status xent_ls(int dtype, void* z, long rows, int V, const int* labels, float ls, double norm, double* partial,
                   hipStream_t st) {
     if (dtype == GP_BF16)
-        xent_kernel<bf16><<<(unsigned)rows, 256, 0, st>>>(reinterpret_cast<bf16*>(z), V, labels, ls, norm, partial);
+        klaunch(xent_kernel<bf16>, (unsigned)rows, 256, 0, st, reinterpret_cast<bf16*>(z), V, labels, ls, norm, partial);
     else
-        xent_kernel<float><<<(unsigned)rows, 256, 0, st>>>(reinterpret_cast<float*>(z), V, labels, ls, norm, partial);
+        klaunch(xent_kernel<float>, (unsigned)rows, 256, 0, st, reinterpret_cast<float*>(z), V, labels, ls, norm, partial);
     GP_LAUNCH_CHECK();
     return GP_OK;
 }
 
 gp_status sgd_update(float* w, const float* g, float lr, long count, hipStream_t st) {
-    sgd_kernel<<<ew_grid(count), 256, 0, st>>>(w, g, lr, count);
+    klaunch(sgd_kernel, ew_grid(count), 256, 0, st, w, g, lr, count);
     GP_LAUNCH_CHECK();
     return GP_OK;
 }
@@ -209,9 +209,9 @@ gp_status sgd_update(float* w, const float* g, float lr, long count, hipStream_t
 gp_status refresh_linear(int dtype, const float* w, int in, int out, void* kn, void* nk, hipStream_t st) {
     dim3 grid((out + 63) / 64, (in + 63) / 64);
     if (dtype == GP_BF16)
-        refresh_kernel<bf16><<<grid, 256, 0, st>>>(w, in, out, reinterpret_cast<bf16*>(kn), reinterpret_cast<bf16*>(nk));
+        klaunch(refresh_kernel<bf16>, grid, 256, 0, st, w, in, out, reinterpret_cast<bf16*>(kn), reinterpret_cast<bf16*>(nk));
     else
-        refresh_kernel<float><<<grid, 256, 0, st>>>(w, in, out, reinterpret_cast<float*>(kn), reinterpret_cast<float*>(nk));
+        klaunch(refresh_kernel<float>, grid, 256, 0, st, w, in, out, reinterpret_cast<float*>(kn), reinterpret_cast<float*>(nk));
     GP_LAUNCH_CHECK();
     return GP_OK;
 }
@@ -222,13 +222,13 @@ gp_status refresh_linear(int dtype, const float* w, int in, int out, void* kn, v
 __global__ void role_marker_kernel() {}
 
 gp_status role_marker(int role, int edge, hipStream_t st) {
-    role_marker_kernel<<<dim3(role, edge + 1), 64, 0, st>>>();
+    klaunch(role_marker_kernel, dim3(role, edge + 1), 64, 0, st);
     GP_LAUNCH_CHECK();
     return GP_OK;
 }
 
 gp_status finite_check(const float* x, long count, int* flag, hipStream_t st) {
-    finite_kernel<<<ew_grid(count), 256, 0, st>>>(x, count, flag);
+    klaunch(finite_kernel, ew_grid(count), 256, 0, st, x, count, flag);
     GP_LAUNCH_CHECK();
     return GP_OK;
 }

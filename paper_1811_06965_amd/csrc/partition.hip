@@ -36,6 +36,8 @@ static thread_local std::string g_err;
 static thread_local LaunchEvents g_launch_events;
 
 LaunchEvents& launch_events() { return g_launch_events; }
+static thread_local hipError_t g_launch_status = hipSuccess;
+hipError_t& launch_status() { return g_launch_status; }
 
 gp_status set_error(gp_status s, const char* msg) {
     g_err = msg;
@@ -72,7 +74,7 @@ struct LayerWs {
     void *v = nullptr, *a = nullptr;
 };
 
-constexpr int ELT_RING = 10;  // bf16 residual-gradient buffers (see layer_backward)
+constexpr int ELT_RING = 10;      // bf16 residual-gradient buffers (see layer_backward)
 
 struct BwdWs {
     float *p32 = nullptr, *q32 = nullptr, *dn = nullptr, *delta = nullptr, *partial = nullptr, *dmem32 = nullptr;
@@ -152,19 +154,30 @@ struct gp_partition {
     LaunchTimer timer;
     // Weight-gradient GEMMs run on a second stream (GP_SIDE_STREAM=0 turns it
     // off), ordered against the caller's stream by events from a ring.
+    // Fork/join events come from a ring of distinct event objects: a stream
+    // wait must refer to the recording made just before it, and a recorded
+    // event is not recorded again until the ring has gone round (the host can
+    // run many calls ahead of the device).
+    std::vector<hipEvent_t> evring;
+    size_t ev_next = 0;
+    hipEvent_t next_event() {
+        hipEvent_t e = evring[ev_next];
+        ev_next = (ev_next + 1) % evring.size();
+        return e;
+    }
     bool use_side = true;
     // when weight-gradient GEMMs are handed to the side stream (GP_DW_FLUSH):
     // 0 each as soon as its inputs are enqueued, 1 after the feed-forward
     // block and at the end of the layer, 2 at the end of the layer
     int dw_flush = 0;
     hipStream_t side = nullptr;
-    hipEvent_t side_fork = nullptr, side_done[4] = {};
+    hipEvent_t side_done[4] = {};  // side stream's last event of layer l % 4 (from evring)
     // Recompute-ahead (GP_REMAT_AHEAD=0 turns it off): while micro-batch m is
     // back-propagated, micro-batch m - 1 is re-materialised on a third stream
     // into the other workspace set.
     bool remat_ahead = true;
     hipStream_t remat = nullptr;
-    hipEvent_t remat_fork = nullptr, remat_done = nullptr;
+    hipEvent_t remat_done = nullptr;  // from evring
     int remat_pending = -1;  // micro-batch whose recompute-ahead is enqueued
 
     void* W(size_t elt_off) const { return welt + elt_off * esz; }
@@ -260,7 +273,7 @@ struct Ctx {
     gp_partition* p;
     hipStream_t st;
     int dt;
-    float* ws = nullptr;  // split-K partials for launches on st
+    float* ws = nullptr;        // split-K partials for launches on st
 };
 
 enum class Lane { Main, Side, Remat };
@@ -667,19 +680,16 @@ gp_status upload_param_block(gp_partition* p, const ParamRef& r, const float* ho
 }
 
 void free_all(gp_partition* p) {
-    for (hipEvent_t& e : p->side_done) {
+    for (hipEvent_t e : p->evring)
         if (e) (void)hipEventDestroy(e);
-        e = nullptr;
-    }
-    if (p->side_fork) (void)hipEventDestroy(p->side_fork);
-    p->side_fork = nullptr;
+    p->evring.clear();
+    p->ev_next = 0;
+    for (hipEvent_t& e : p->side_done) e = nullptr;
     if (p->side) (void)hipStreamDestroy(p->side);
     p->side = nullptr;
-    for (hipEvent_t e : {p->remat_fork, p->remat_done})
-        if (e) (void)hipEventDestroy(e);
     if (p->remat) (void)hipStreamDestroy(p->remat);
     p->remat = nullptr;
-    p->remat_fork = p->remat_done = nullptr;
+    p->remat_done = nullptr;
     p->remat_pending = -1;
     for (hipEvent_t e : p->timer.all) (void)hipEventDestroy(e);
     const bool markers = p->timer.markers;
@@ -799,13 +809,12 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
     if (p->use_side) {
         // default priority, like every stream of the library
         e = hipStreamCreateWithFlags(&p->side, hipStreamNonBlocking);
-        if (e == hipSuccess) e = hipEventCreateWithFlags(&p->side_fork, hipEventDisableTiming);
-        for (int i = 0; e == hipSuccess && i < 4; ++i) e = hipEventCreateWithFlags(&p->side_done[i], hipEventDisableTiming);
     }
-    if (e == hipSuccess && p->nsets > 1) {
-        e = hipStreamCreateWithFlags(&p->remat, hipStreamNonBlocking);
-        if (e == hipSuccess) e = hipEventCreateWithFlags(&p->remat_fork, hipEventDisableTiming);
-        if (e == hipSuccess) e = hipEventCreateWithFlags(&p->remat_done, hipEventDisableTiming);
+    if (e == hipSuccess && p->nsets > 1) e = hipStreamCreateWithFlags(&p->remat, hipStreamNonBlocking);
+    if (e == hipSuccess && (p->side || p->remat)) {
+        p->evring.assign(4096, nullptr);
+        for (size_t i = 0; e == hipSuccess && i < p->evring.size(); ++i)
+            e = hipEventCreateWithFlags(&p->evring[i], hipEventDisableTiming);
     }
     if (e == hipSuccess) e = hipDeviceSynchronize();
     if (e != hipSuccess) {
@@ -936,7 +945,11 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     // Everything enqueued on the caller's stream so far (all forwards, the
     // previous backward, which read the other workspace set) precedes a
     // recompute-ahead launched from this call.
-    if (p->nsets > 1 && mb > 0) GP_HIP(hipEventRecord(p->remat_fork, c.st));
+    hipEvent_t remat_fork = nullptr;
+    if (p->nsets > 1 && mb > 0) {
+        remat_fork = p->next_event();
+        GP_HIP(hipEventRecord(remat_fork, c.st));
+    }
     // re-materialise this micro-batch's forward from the stash, unless the
     // previous backward call already did so on the recompute-ahead stream
     if (p->remat_pending == mb) {
@@ -950,9 +963,10 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
         // re-materialise micro-batch mb - 1 into the other set meanwhile
         // (GPipe, Section 2.3: the recompute can be scheduled earlier)
         Ctx cr = make_ctx(p, p->remat, Lane::Remat);
-        GP_HIP(hipStreamWaitEvent(cr.st, p->remat_fork, 0));
+        GP_HIP(hipStreamWaitEvent(cr.st, remat_fork, 0));
         s = partition_forward(cr, mb - 1, true, nullptr, nullptr, nullptr, set ^ 1);
         if (s != GP_OK) return s;
+        p->remat_done = p->next_event();
         GP_HIP(hipEventRecord(p->remat_done, cr.st));
         p->remat_pending = mb - 1;
     }
@@ -994,8 +1008,9 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
         auto flush = [&](int level) -> gp_status {
             if (jobs.empty() || level < p->dw_flush) return GP_OK;
             if (side) {
-                GP_HIP(hipEventRecord(p->side_fork, c.st));
-                GP_HIP(hipStreamWaitEvent(cs.st, p->side_fork, 0));
+                const hipEvent_t fork = p->next_event();
+                GP_HIP(hipEventRecord(fork, c.st));
+                GP_HIP(hipStreamWaitEvent(cs.st, fork, 0));
             }
             for (const DwJob& j : jobs) GP_TRY(linear_dw(side ? cs : c, *j.L, j.X, j.dY, j.rows, acc));
             jobs.clear();
@@ -1006,6 +1021,7 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
         if (s == GP_OK) s = flush(2);
         if (s != GP_OK) return fail(s);
         if (side) {
+            p->side_done[l % 4] = p->next_event();
             GP_HIP(hipEventRecord(p->side_done[l % 4], cs.st));
             last_done = p->side_done[l % 4];
         }

@@ -306,10 +306,12 @@ def test_call_order_is_enforced():
 
 
 TILE_CASES = [(0, 1), (1, 1), (2, 1), (3, 1), (0, 4), (3, 2),
-              (4, 1), (5, 1), (6, 1), (7, 1), (8, 1), (9, 1), (10, 1), (4, 2), (8, 4), (10, 4)]
+              (4, 1), (5, 1), (6, 1), (7, 1), (8, 1), (9, 1), (10, 1), (4, 2), (8, 4), (10, 4),
+              (11, 1), (12, 1), (13, 1), (14, 1), (11, 4)]
 TILE_IDS = ["256x256", "256x128", "128x256", "128x128", "256x256_split4", "128x128_split2",
             "dl128x128", "dl128x128_3stage", "dl256x128", "dl256x256", "dl256x256_8w", "dl256x128_8w",
-            "dl128x256_8w", "dl128x128_split2", "dl256x256_8w_split4", "dl128x256_8w_split4"]
+            "dl128x256_8w", "dl128x128_split2", "dl256x256_8w_split4", "dl128x256_8w_split4",
+            "dl128x128_8w_a", "dl128x128_8w_b", "dl256x128_8w_3stage", "dl128x256_8w_3stage", "dl128x128_8w_split4"]
 
 
 @pytest.mark.parametrize("tile,splits", TILE_CASES, ids=TILE_IDS)
@@ -321,3 +323,7 @@ def test_bf16_every_gemm_tile_shape(tile, splits, monkeypatch):
     monkeypatch.setenv("GP_GEMM_SPLITS", str(splits))
     case, ref, res = _run(RAGGED_BF16, 3, perturb=False)
     _check(RAGGED_BF16, ref, res, 2e-2, "cos", 0.999)
+    if tile >= 4:
+        # T = 2 x 128 rows: the weight-gradient GEMMs take the forced direct-to-LDS tile too
+        case, ref, res = _run(ENC512_SMALL, 4, perturb=True)
+        _check(ENC512_SMALL, ref, res, 2e-2, "cos", 0.999)

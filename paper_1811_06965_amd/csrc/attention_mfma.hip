@@ -7,9 +7,10 @@
 // l and l + 32 split the keys between them).  The row softmax is therefore an
 // in-register max/sum plus one cross-half exchange, and the probabilities,
 // rounded to bf16, are already laid out as the B operand of the second
-// product O^T = V^T P^T; no LDS round trip for P.  K and V^T of the
-// (sequence, head) are staged once per workgroup in LDS.  The workgroup also
-// writes the row log-sum-exp for the backward pass.
+// product O^T = V^T P^T; no LDS round trip for P.  K and V of the (sequence,
+// head) are staged row-major once per workgroup in LDS; V^T fragments come
+// from transposing LDS reads (ds_read_b64_tr_b16).  The workgroup also writes
+// the row log-sum-exp for the backward pass.
 //
 // Backward (two kernels, no atomics, deterministic):
 //   dQ pass (per 32 queries, loop over key blocks):  S^T, dP^T = V dO^T,
@@ -19,8 +20,10 @@
 //     dS = P (dP - delta), dV^T += dO^T P, dK^T += Q^T dS.
 // In every product the register-held operand's accumulator layout (lane =
 // column; register r = rows 8 (r/4) + 4 (lane/32) + r%4) is consumed as the
-// B operand of the next product, whose A operand is read from LDS with the
-// matching k order (two runs of four consecutive rows per lane).
+// B operand of the next product, whose A operand (K^T, Q^T, dO^T) is read
+// transposed from the row-major LDS tile with the matching k order (two runs
+// of four consecutive rows per lane).  A workgroup holds 1, 2 or 4 waves,
+// chosen so that small micro-batches still launch enough workgroups.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -32,9 +35,7 @@ gp_status attention_bwd_simt(int dtype, const AttnArgs& a, hipStream_t st);
 namespace {
 
 constexpr int DH = 64;         // head width
-constexpr int LDR = DH + 8;    // row stride (elements) of [row][d] LDS tiles
 constexpr int MAXK = 256;      // keys / queries per (sequence, head)
-constexpr int LDT = MAXK + 8;  // row stride of transposed [d][row] LDS tiles
 constexpr float LOG2E = 1.4426950408889634f;
 
 __device__ __forceinline__ f32x16 mfma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
@@ -48,51 +49,59 @@ __device__ __forceinline__ f32x16 zero16() {
     return z;
 }
 
-// Stage rows [0, nrows) x 64 of a head into LDS as [row][d] (row stride LDR).
-__device__ __forceinline__ void stage_rows(bf16* __restrict__ s, const bf16* __restrict__ g, long ld, int nrows,
-                                           int tid, int nthr) {
-    for (int i = tid; i < nrows * (DH / 8); i += nthr) {
-        const int r = i >> 3, c = (i & 7) * 8;
-        *reinterpret_cast<bf16x8*>(s + r * LDR + c) = *reinterpret_cast<const bf16x8*>(g + (long)r * ld + c);
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16* LdsV4;
+
+// LDS tiles hold rows of 64 features (128 bytes) without padding; the
+// 16-byte chunk c of row r is stored at chunk position c ^ swz(r).  With this
+// swizzle both access patterns are free of bank conflicts: 16 lanes reading
+// the same chunk of 16 consecutive rows (row fragments), and a half-wave
+// reading four consecutive chunks of 4 consecutive rows (transposing reads).
+__device__ __forceinline__ int swz(int r) { return (((r >> 1) & 1) << 2) | ((r >> 2) & 3); }
+__device__ __forceinline__ int lds_off(int r, int col) { return r * 128 + (((col >> 3) ^ swz(r)) << 4) + (col & 7) * 2; }
+
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+typedef __attribute__((address_space(3))) void* LdsPtr;
+
+// Stage NROWS rows x 64 features of a head (rows ld elements apart, base g)
+// into the LDS tile s with direct-to-LDS buffer loads: each wave instruction
+// fills 8 rows (1 KB) and each lane fetches the global chunk that belongs at
+// its swizzled LDS position.  All loads are issued back to back; the caller
+// waits (vmcnt 0) and synchronises before reading.
+template <int NROWS, int NW>
+__device__ __forceinline__ void stage_dl(char* s, const bf16* g, long ld, int wave, int lane) {
+    static_assert(NROWS % (8 * NW) == 0, "staging split");
+    constexpr int P = NROWS / (8 * NW);
+    const Rsrc rs = __builtin_amdgcn_make_buffer_rsrc((void*)g, (short)0, (int)(((long)(NROWS - 1) * ld + DH) * 2), 0x00020000);
+#pragma unroll
+    for (int i = 0; i < P; ++i) {
+        const int blk = wave * P + i, r = blk * 8 + (lane >> 3), c = (lane & 7) ^ swz(r);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (LdsPtr)(s + blk * 1024), 16, (int)(((long)r * ld + c * 8) * 2),
+                                                 0, 0, 0);
     }
 }
 
-// Stage rows [0, nrows) x 64 of a head into LDS transposed, as [d][row]
-// (row stride LDT): each thread moves 4 rows x 8 features.
-__device__ __forceinline__ void stage_rows_t(bf16* __restrict__ s, const bf16* __restrict__ g, long ld, int nrows,
-                                             int tid, int nthr) {
-    for (int i = tid; i < (nrows / 4) * (DH / 8); i += nthr) {
-        const int r0 = (i >> 3) * 4, c0 = (i & 7) * 8;
-        bf16x8 v[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) v[q] = *reinterpret_cast<const bf16x8*>(g + (long)(r0 + q) * ld + c0);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            bf16x4 t = {v[0][e], v[1][e], v[2][e], v[3][e]};
-            *reinterpret_cast<bf16x4*>(s + (c0 + e) * LDT + r0) = t;
-        }
-    }
-}
+// s_waitcnt vmcnt(0), leaving the other counters unconstrained
+__device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8)); }
 
 // A operand from an [row][d] tile: rows row0 + lane%32, d = s*16 + 8*(lane/32) .. +8.
-__device__ __forceinline__ bf16x8 frag_rows(const bf16* s, int row0, int kstep, int lane) {
-    return *reinterpret_cast<const bf16x8*>(s + (row0 + (lane & 31)) * LDR + kstep * 16 + (lane >> 5) * 8);
+__device__ __forceinline__ bf16x8 frag_rows(const char* s, int row0, int kstep, int lane) {
+    return *reinterpret_cast<const bf16x8*>(s + lds_off(row0 + (lane & 31), kstep * 16 + (lane >> 5) * 8));
 }
 
-// A operand from a transposed [d][row] tile, matching the k order of a
-// register-held accumulator chunk: feature d = d0 + lane%32; rows
-// base + 4*(lane/32) + {0..3} and base + 8 + 4*(lane/32) + {0..3}.
-__device__ __forceinline__ bf16x8 frag_t(const bf16* s, int d0, int base, int lane) {
-    const bf16* p = s + (d0 + (lane & 31)) * LDT + base + (lane >> 5) * 4;
-    const bf16x4 lo = *reinterpret_cast<const bf16x4*>(p);
-    const bf16x4 hi = *reinterpret_cast<const bf16x4*>(p + 8);
-    bf16x8 r;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        r[e] = lo[e];
-        r[4 + e] = hi[e];
-    }
-    return r;
+// A operand of the transposed tile (m = feature d0 + lane%32) from an [row][d]
+// tile, with the k order of a register-held accumulator chunk: rows
+// base + 4 (lane/32) + {0..3} and base + 8 + 4 (lane/32) + {0..3}.  Two
+// transposing LDS reads (ds_read_b64_tr_b16): in each 16-lane group, lane q
+// addresses row k0 + q/4, features m0 + 4 (q%4) .. +3, and receives the four
+// rows k0 .. k0+3 of feature m0 + q.
+__device__ __forceinline__ bf16x8 frag_tr(const char* s, int d0, int base, int lane) {
+    const int g = lane >> 4, q = lane & 15;
+    const int row = base + 4 * (g >> 1) + (q >> 2), col = d0 + 16 * (g & 1) + 4 * (q & 3);
+    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LdsV4)(s + lds_off(row, col)));
+    const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LdsV4)(s + lds_off(row + 8, col)));
+    const bf16x4 x = __builtin_bit_cast(bf16x4, lo), y = __builtin_bit_cast(bf16x4, hi);
+    return bf16x8{x[0], x[1], x[2], x[3], y[0], y[1], y[2], y[3]};
 }
 
 // B operand from a global row of the head: row (lane%32 of the caller's
@@ -127,92 +136,110 @@ __device__ __forceinline__ void store_t(bf16* __restrict__ g, long ld, const f32
         }
 }
 
-constexpr int FWD_WAVES = 4;
+// 2^x with the hardware transcendental (v_exp_f32); every argument here is
+// <= 0 or a finite difference of scaled scores, and a result that flushes
+// to zero below 2^-126 is irrelevant next to the row's largest term (1).
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 
-template <int NKB>
-__global__ void __launch_bounds__(256) attn_fwd_mfma(AttnArgs a) {
-    __shared__ __attribute__((aligned(16))) bf16 Ks[MAXK * LDR];
-    __shared__ __attribute__((aligned(16))) bf16 Vt[DH * LDT];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int bh = blockIdx.y, b = bh / a.H, hh = bh % a.H;
-    const int Sk = NKB * 32;
+// Work item of this workgroup, remapped so that the workgroups of one
+// (sequence, head) -- consecutive work items -- run on the same XCD (the
+// hardware deals consecutive workgroup ids round-robin to the 8 XCDs, each
+// with its own L2) and share its cached copy of the head's keys and values.
+// Returns the row block in *blk and the (sequence, head) index.
+__device__ __forceinline__ int xcd_work(int* blk) {
+    const int G = gridDim.x * gridDim.y, G8 = G & ~7;
+    int L = blockIdx.x + blockIdx.y * gridDim.x;
+    if (L < G8) L = (L & 7) * (G8 >> 3) + (L >> 3);
+    *blk = L % gridDim.x;
+    return L / gridDim.x;
+}
+
+// Forward: QW waves per workgroup, 32 queries each, all keys of the head.
+template <int NKB, int QW, bool CAUSAL>
+__global__ void __launch_bounds__(64 * QW) attn_fwd_mfma(AttnArgs a) {
+    __shared__ __attribute__((aligned(1024))) char Ks[NKB * 32 * 128];
+    __shared__ __attribute__((aligned(1024))) char Vs[NKB * 32 * 128];
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    int blk;
+    const int bh = xcd_work(&blk), b = bh / a.H, hh = bh % a.H;
     const bf16* K = reinterpret_cast<const bf16*>(a.k) + (long)b * a.Sk * a.ldk + hh * DH;
     const bf16* V = reinterpret_cast<const bf16*>(a.v) + (long)b * a.Sk * a.ldv + hh * DH;
-    stage_rows(Ks, K, a.ldk, Sk, tid, 256);
-    stage_rows_t(Vt, V, a.ldv, Sk, tid, 256);
+    stage_dl<NKB * 32, QW>(Ks, K, a.ldk, wave, lane);
+    stage_dl<NKB * 32, QW>(Vs, V, a.ldv, wave, lane);
+    wait_loads();
     __syncthreads();
-    const int q0 = (blockIdx.x * FWD_WAVES + wave) * 32;
+    const int q0 = (blk * QW + wave) * 32;
     if (q0 >= a.Sq) return;
     const int q = q0 + (lane & 31);
     const bf16* Qrow = reinterpret_cast<const bf16*>(a.q) + ((long)b * a.Sq + q) * a.ldq + hh * DH;
     bf16x8 qf[4];
 #pragma unroll
     for (int s = 0; s < 4; ++s) qf[s] = frag_global(Qrow, s, lane);
-    const float c = a.scale * LOG2E;
+    // key blocks at or below the diagonal (causal), else all
+    const int nkb = CAUSAL ? min(NKB, q0 / 32 + 1) : NKB;
     f32x16 sc[NKB];
     float m = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb) {
         sc[kb] = zero16();
-        if (a.causal && kb * 32 > q0 + 31) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) sc[kb][r] = -INFINITY;
-            continue;
-        }
+        if (kb >= nkb) continue;
 #pragma unroll
         for (int s = 0; s < 4; ++s) sc[kb] = mfma(frag_rows(Ks, kb * 32, s, lane), qf[s], sc[kb]);
+        if (CAUSAL && kb == nkb - 1) {
+            // the diagonal block: keys after the query are masked
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            float v = sc[kb][r] * c;
-            if (a.causal && kb * 32 + acc_row(r, lane) > q) v = -INFINITY;
-            sc[kb][r] = v;
-            m = fmaxf(m, v);
+            for (int r = 0; r < 16; ++r)
+                if (kb * 32 + acc_row(r, lane) > q) sc[kb][r] = -INFINITY;
         }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) m = fmaxf(m, sc[kb][r]);
     }
     m = fmaxf(m, __shfl_xor(m, 32, 64));
+    // p = 2^(c (s - m)) with c = scale log2(e): one FMA and one exp per score
+    const float c = a.scale * LOG2E, mc = m * c;
     float sum = 0.f;
 #pragma unroll
-    for (int kb = 0; kb < NKB; ++kb)
+    for (int kb = 0; kb < NKB; ++kb) {
+        if (kb >= nkb) continue;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            const float p = exp2f(sc[kb][r] - m);
+            const float p = exp2_hw(fmaf(sc[kb][r], c, -mc));
             sc[kb][r] = p;
             sum += p;
         }
+    }
     sum += __shfl_xor(sum, 32, 64);
     f32x16 o[2] = {zero16(), zero16()};
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb) {
-        if (a.causal && kb * 32 > q0 + 31) continue;
+        if (kb >= nkb) continue;
 #pragma unroll
         for (int cc = 0; cc < 2; ++cc) {
             const bf16x8 pf = pack_chunk(sc[kb], cc);
 #pragma unroll
-            for (int db = 0; db < 2; ++db) o[db] = mfma(frag_t(Vt, db * 32, kb * 32 + cc * 16, lane), pf, o[db]);
+            for (int db = 0; db < 2; ++db) o[db] = mfma(frag_tr(Vs, db * 32, kb * 32 + cc * 16, lane), pf, o[db]);
         }
     }
     bf16* O = reinterpret_cast<bf16*>(a.o) + ((long)b * a.Sq + q0) * a.ldo + hh * DH;
     store_t(O, a.ldo, o, 1.f / sum, lane);
-    if (a.lse && lane < 32) a.lse[(long)bh * a.Sq + q] = (m + log2f(sum)) / LOG2E;
+    if (a.lse && lane < 32) a.lse[(long)bh * a.Sq + q] = m * a.scale + logf(sum);
 }
 
-constexpr int BWD_WAVES = 4;
-
-template <int NKB>
-__global__ void __launch_bounds__(256) attn_bwd_dq_mfma(AttnArgs a) {
-    __shared__ __attribute__((aligned(16))) bf16 Ks[MAXK * LDR];
-    __shared__ __attribute__((aligned(16))) bf16 Vs[MAXK * LDR];
-    __shared__ __attribute__((aligned(16))) bf16 Kt[DH * LDT];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int bh = blockIdx.y, b = bh / a.H, hh = bh % a.H;
-    const int Sk = NKB * 32;
+// dQ pass: QW waves per workgroup, 32 queries each; also writes delta.
+template <int NKB, int QW, bool CAUSAL>
+__global__ void __launch_bounds__(64 * QW) attn_bwd_dq_mfma(AttnArgs a) {
+    __shared__ __attribute__((aligned(1024))) char Ks[NKB * 32 * 128];
+    __shared__ __attribute__((aligned(1024))) char Vs[NKB * 32 * 128];
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    int blk;
+    const int bh = xcd_work(&blk), b = bh / a.H, hh = bh % a.H;
     const bf16* K = reinterpret_cast<const bf16*>(a.k) + (long)b * a.Sk * a.ldk + hh * DH;
     const bf16* V = reinterpret_cast<const bf16*>(a.v) + (long)b * a.Sk * a.ldv + hh * DH;
-    stage_rows(Ks, K, a.ldk, Sk, tid, 256);
-    stage_rows(Vs, V, a.ldv, Sk, tid, 256);
-    stage_rows_t(Kt, K, a.ldk, Sk, tid, 256);
+    stage_dl<NKB * 32, QW>(Ks, K, a.ldk, wave, lane);
+    stage_dl<NKB * 32, QW>(Vs, V, a.ldv, wave, lane);
+    wait_loads();
     __syncthreads();
-    const int q0 = (blockIdx.x * BWD_WAVES + wave) * 32;
+    const int q0 = (blk * QW + wave) * 32;
     if (q0 >= a.Sq) return;
     const int q = q0 + (lane & 31);
     const long qrow = (long)b * a.Sq + q;
@@ -232,10 +259,10 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_mfma(AttnArgs a) {
     const float delta = dpart + __shfl_xor(dpart, 32, 64);
     const float c = a.scale * LOG2E;
     const float lse2 = a.lse[(long)bh * a.Sq + q] * LOG2E;
+    const int nkb = CAUSAL ? min(NKB, q0 / 32 + 1) : NKB;
     f32x16 dq[2] = {zero16(), zero16()};
 #pragma unroll 2
-    for (int kb = 0; kb < NKB; ++kb) {
-        if (a.causal && kb * 32 > q0 + 31) break;
+    for (int kb = 0; kb < nkb; ++kb) {
         f32x16 st = zero16(), dp = zero16();
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
@@ -244,15 +271,15 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_mfma(AttnArgs a) {
         }
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            float p = exp2f(st[r] * c - lse2);
-            if (a.causal && kb * 32 + acc_row(r, lane) > q) p = 0.f;
-            st[r] = p * (dp[r] - delta);
+            float p = exp2_hw(fmaf(st[r], c, -lse2));
+            if (CAUSAL && kb * 32 + acc_row(r, lane) > q) p = 0.f;
+            st[r] = fmaf(p, dp[r], -p * delta);
         }
 #pragma unroll
         for (int cc = 0; cc < 2; ++cc) {
             const bf16x8 df = pack_chunk(st, cc);
 #pragma unroll
-            for (int db = 0; db < 2; ++db) dq[db] = mfma(frag_t(Kt, db * 32, kb * 32 + cc * 16, lane), df, dq[db]);
+            for (int db = 0; db < 2; ++db) dq[db] = mfma(frag_tr(Ks, db * 32, kb * 32 + cc * 16, lane), df, dq[db]);
         }
     }
     bf16* dQ = reinterpret_cast<bf16*>(a.dq) + ((long)b * a.Sq + q0) * a.lddq + hh * DH;
@@ -260,28 +287,27 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_mfma(AttnArgs a) {
     if (lane < 32) a.delta[(long)bh * a.Sq + q] = delta;
 }
 
-template <int NQB>
-__global__ void __launch_bounds__(256) attn_bwd_dkv_mfma(AttnArgs a) {
-    __shared__ __attribute__((aligned(16))) bf16 Qs[MAXK * LDR];
-    __shared__ __attribute__((aligned(16))) bf16 Gs[MAXK * LDR];
-    __shared__ __attribute__((aligned(16))) bf16 Qt[DH * LDT];
-    __shared__ __attribute__((aligned(16))) bf16 Gt[DH * LDT];
-    __shared__ float lse2s[MAXK], dls[MAXK];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int bh = blockIdx.y, b = bh / a.H, hh = bh % a.H;
+// dK/dV pass: KW waves per workgroup, 32 keys each, looping over query blocks.
+template <int NQB, int KW, bool CAUSAL>
+__global__ void __launch_bounds__(64 * KW) attn_bwd_dkv_mfma(AttnArgs a) {
+    __shared__ __attribute__((aligned(1024))) char Qs[NQB * 32 * 128];
+    __shared__ __attribute__((aligned(1024))) char Gs[NQB * 32 * 128];
+    __shared__ __attribute__((aligned(16))) float lse2s[NQB * 32], dls[NQB * 32];
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    int blk;
+    const int bh = xcd_work(&blk), b = bh / a.H, hh = bh % a.H;
     const int Sq = NQB * 32;
     const bf16* Q = reinterpret_cast<const bf16*>(a.q) + (long)b * a.Sq * a.ldq + hh * DH;
     const bf16* G = reinterpret_cast<const bf16*>(a.dout) + (long)b * a.Sq * a.lddo + hh * DH;
-    stage_rows(Qs, Q, a.ldq, Sq, tid, 256);
-    stage_rows(Gs, G, a.lddo, Sq, tid, 256);
-    stage_rows_t(Qt, Q, a.ldq, Sq, tid, 256);
-    stage_rows_t(Gt, G, a.lddo, Sq, tid, 256);
-    for (int i = tid; i < Sq; i += 256) {
+    stage_dl<NQB * 32, KW>(Qs, Q, a.ldq, wave, lane);
+    stage_dl<NQB * 32, KW>(Gs, G, a.lddo, wave, lane);
+    for (int i = tid; i < Sq; i += 64 * KW) {
         lse2s[i] = a.lse[(long)bh * a.Sq + i] * LOG2E;
         dls[i] = a.delta[(long)bh * a.Sq + i];
     }
+    wait_loads();
     __syncthreads();
-    const int k0 = (blockIdx.x * BWD_WAVES + wave) * 32;
+    const int k0 = (blk * KW + wave) * 32;
     if (k0 >= a.Sk) return;
     const int key = k0 + (lane & 31);
     const long krow = (long)b * a.Sk + key;
@@ -295,7 +321,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dkv_mfma(AttnArgs a) {
     }
     const float c = a.scale * LOG2E;
     f32x16 dk[2] = {zero16(), zero16()}, dv[2] = {zero16(), zero16()};
-    const int qb0 = a.causal ? k0 / 32 : 0;
+    const int qb0 = CAUSAL ? k0 / 32 : 0;
     for (int qb = qb0; qb < NQB; ++qb) {
         f32x16 st = zero16(), dp = zero16();
 #pragma unroll
@@ -303,14 +329,21 @@ __global__ void __launch_bounds__(256) attn_bwd_dkv_mfma(AttnArgs a) {
             st = mfma(frag_rows(Qs, qb * 32, s, lane), kf[s], st);
             dp = mfma(frag_rows(Gs, qb * 32, s, lane), vf[s], dp);
         }
+        // this lane's rows of the block: 8 j + 4 (lane/32) + {0..3}, j = 0..3
+        f32x4 l4[4], d4[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int r0 = qb * 32 + 8 * j + 4 * (lane >> 5);
+            l4[j] = *reinterpret_cast<const f32x4*>(lse2s + r0);
+            d4[j] = *reinterpret_cast<const f32x4*>(dls + r0);
+        }
         f32x16 pm;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            const int qi = qb * 32 + acc_row(r, lane);
-            float p = exp2f(st[r] * c - lse2s[qi]);
-            if (a.causal && key > qi) p = 0.f;
+            float p = exp2_hw(fmaf(st[r], c, -l4[r >> 2][r & 3]));
+            if (CAUSAL && key > qb * 32 + acc_row(r, lane)) p = 0.f;
             pm[r] = p;
-            st[r] = p * (dp[r] - dls[qi]);
+            st[r] = fmaf(p, dp[r], -p * d4[r >> 2][r & 3]);
         }
 #pragma unroll
         for (int cc = 0; cc < 2; ++cc) {
@@ -318,8 +351,8 @@ __global__ void __launch_bounds__(256) attn_bwd_dkv_mfma(AttnArgs a) {
             const bf16x8 df = pack_chunk(st, cc);
 #pragma unroll
             for (int db = 0; db < 2; ++db) {
-                dv[db] = mfma(frag_t(Gt, db * 32, qb * 32 + cc * 16, lane), pf, dv[db]);
-                dk[db] = mfma(frag_t(Qt, db * 32, qb * 32 + cc * 16, lane), df, dk[db]);
+                dv[db] = mfma(frag_tr(Gs, db * 32, qb * 32 + cc * 16, lane), pf, dv[db]);
+                dk[db] = mfma(frag_tr(Qs, db * 32, qb * 32 + cc * 16, lane), df, dk[db]);
             }
         }
     }
@@ -329,18 +362,37 @@ __global__ void __launch_bounds__(256) attn_bwd_dkv_mfma(AttnArgs a) {
     store_t(dV, a.lddv, dv, 1.f, lane);
 }
 
-#define GP_NB_SWITCH(NB, KERNEL, GRID)                                              \
-    switch (NB) {                                                                   \
-    case 1: klaunch(KERNEL<1>, GRID, 256, 0, st, a); break;                              \
-    case 2: klaunch(KERNEL<2>, GRID, 256, 0, st, a); break;                              \
-    case 3: klaunch(KERNEL<3>, GRID, 256, 0, st, a); break;                              \
-    case 4: klaunch(KERNEL<4>, GRID, 256, 0, st, a); break;                              \
-    case 5: klaunch(KERNEL<5>, GRID, 256, 0, st, a); break;                              \
-    case 6: klaunch(KERNEL<6>, GRID, 256, 0, st, a); break;                              \
-    case 7: klaunch(KERNEL<7>, GRID, 256, 0, st, a); break;                              \
-    case 8: klaunch(KERNEL<8>, GRID, 256, 0, st, a); break;                              \
-    default: return set_error(GP_ERR_UNSUPPORTED, "attention: sequence length > 256"); \
+// Launch KERNEL<NB, W, C> for the runtime block count NB (1..8), W waves and causal flag C.
+#define GP_NB_SWITCH(NB, W, C, KERNEL, GRID)                                               \
+    switch (NB) {                                                                          \
+    case 1: klaunch(KERNEL<1, W, C>, GRID, 64 * W, 0, st, a); break;                       \
+    case 2: klaunch(KERNEL<2, W, C>, GRID, 64 * W, 0, st, a); break;                       \
+    case 3: klaunch(KERNEL<3, W, C>, GRID, 64 * W, 0, st, a); break;                       \
+    case 4: klaunch(KERNEL<4, W, C>, GRID, 64 * W, 0, st, a); break;                       \
+    case 5: klaunch(KERNEL<5, W, C>, GRID, 64 * W, 0, st, a); break;                       \
+    case 6: klaunch(KERNEL<6, W, C>, GRID, 64 * W, 0, st, a); break;                       \
+    case 7: klaunch(KERNEL<7, W, C>, GRID, 64 * W, 0, st, a); break;                       \
+    case 8: klaunch(KERNEL<8, W, C>, GRID, 64 * W, 0, st, a); break;                       \
+    default: return set_error(GP_ERR_UNSUPPORTED, "attention: sequence length > 256");     \
     }
+#define GP_WC_SWITCH(NB, W, CAUS, KERNEL, GRID)                                            \
+    if (CAUS) {                                                                            \
+        if (W == 4) { GP_NB_SWITCH(NB, 4, true, KERNEL, GRID) }                            \
+        else if (W == 2) { GP_NB_SWITCH(NB, 2, true, KERNEL, GRID) }                       \
+        else { GP_NB_SWITCH(NB, 1, true, KERNEL, GRID) }                                   \
+    } else {                                                                               \
+        if (W == 4) { GP_NB_SWITCH(NB, 4, false, KERNEL, GRID) }                           \
+        else if (W == 2) { GP_NB_SWITCH(NB, 2, false, KERNEL, GRID) }                      \
+        else { GP_NB_SWITCH(NB, 1, false, KERNEL, GRID) }                                  \
+    }
+
+// Waves per workgroup (32 rows each): as many as keep at least 2 x NUM_CU
+// workgroups for a small batch, at most 4 (fewer waves per workgroup re-stage
+// the head's keys and values more often).
+int waves_for(long row_blocks) {
+    constexpr long CU2 = 2 * 256;
+    return row_blocks >= 4 * CU2 ? 4 : row_blocks >= 2 * CU2 ? 2 : 1;
+}
 
 bool mfma_ok(const AttnArgs& a) {
     return a.dh == DH && a.Sq % 32 == 0 && a.Sk % 32 == 0 && a.Sq <= MAXK && a.Sk <= MAXK &&
@@ -352,8 +404,9 @@ bool mfma_ok(const AttnArgs& a) {
 gp_status attention_fwd(int dtype, const AttnArgs& a, hipStream_t st) {
     if (dtype != GP_BF16) return attention_fwd_simt(dtype, a, st);
     if (!mfma_ok(a)) return set_error(GP_ERR_UNSUPPORTED, "bf16 attention needs d_h = 64 and lengths multiple of 32, <= 256");
-    dim3 grid((a.Sq + 32 * FWD_WAVES - 1) / (32 * FWD_WAVES), a.n * a.H);
-    GP_NB_SWITCH(a.Sk / 32, attn_fwd_mfma, grid);
+    const int w = waves_for((long)(a.Sq / 32) * a.n * a.H);
+    dim3 grid((a.Sq + 32 * w - 1) / (32 * w), a.n * a.H);
+    GP_WC_SWITCH(a.Sk / 32, w, a.causal, attn_fwd_mfma, grid);
     GP_LAUNCH_CHECK();
     return GP_OK;
 }
@@ -361,11 +414,13 @@ gp_status attention_fwd(int dtype, const AttnArgs& a, hipStream_t st) {
 gp_status attention_bwd(int dtype, const AttnArgs& a, hipStream_t st) {
     if (dtype != GP_BF16) return attention_bwd_simt(dtype, a, st);
     if (!mfma_ok(a)) return set_error(GP_ERR_UNSUPPORTED, "bf16 attention needs d_h = 64 and lengths multiple of 32, <= 256");
-    dim3 gq((a.Sq + 32 * BWD_WAVES - 1) / (32 * BWD_WAVES), a.n * a.H);
-    GP_NB_SWITCH(a.Sk / 32, attn_bwd_dq_mfma, gq);
+    const int wq = waves_for((long)(a.Sq / 32) * a.n * a.H);
+    dim3 gq((a.Sq + 32 * wq - 1) / (32 * wq), a.n * a.H);
+    GP_WC_SWITCH(a.Sk / 32, wq, a.causal, attn_bwd_dq_mfma, gq);
     GP_LAUNCH_CHECK();
-    dim3 gk((a.Sk + 32 * BWD_WAVES - 1) / (32 * BWD_WAVES), a.n * a.H);
-    GP_NB_SWITCH(a.Sq / 32, attn_bwd_dkv_mfma, gk);
+    const int wk = waves_for((long)(a.Sk / 32) * a.n * a.H);
+    dim3 gk((a.Sk + 32 * wk - 1) / (32 * wk), a.n * a.H);
+    GP_WC_SWITCH(a.Sq / 32, wk, a.causal, attn_bwd_dkv_mfma, gk);
     GP_LAUNCH_CHECK();
     return GP_OK;
 }

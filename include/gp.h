@@ -175,8 +175,11 @@ gp_status gp_forward_microbatch(gp_partition* p, int mb, const void* x, const vo
  * this micro-batch's intermediates only, then back-propagated in reverse
  * layer order.  Parameter gradients are added in place into the fp32
  * accumulators (the first backward micro-batch of a mini-batch overwrites
- * them).  Micro-batches are taken in order mb = M-1, ..., 0, after all M
- * forwards.
+ * them); the LayerNorm gain and shift gradients are summed over the
+ * micro-batches in the library's own buffers and written to the
+ * accumulators by the last backward micro-batch (mb = 0), so every gradient
+ * is complete once all M backwards have run.  Micro-batches are taken in
+ * order mb = M-1, ..., 0, after all M forwards.
  *   dy_or_target : GP_LOSS_NONE:   device [n, S, D] partition dtype, dL/dy;
  *                  GP_LOSS_MSE:    device [n, S, D] partition dtype, targets;
  *                  GP_LOSS_XENT_LS: device int32 [n, S] labels in [0, V).

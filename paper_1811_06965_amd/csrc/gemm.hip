@@ -845,11 +845,29 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
     }
 }
 
-// Sum the split-K partials in split order and apply the epilogue; 4 columns per thread.
+// Sum the split-K partials in split order and apply the epilogue; 4 columns
+// per thread.  An accumulating (weight-gradient) GEMM with fused bias
+// gradient also sums the splits' column-sum rows, stored after the partial
+// tiles, into colsum.
 template <typename T, int EPI>
 __global__ void __launch_bounds__(256) splitk_reduce(GemmArgs args, int splits) {
     const long nq = (long)args.M * (args.N / 4);
     const long plane = (long)args.M * args.N;
+    if constexpr (EPI == EPI_ACC_F32) {
+        if (args.colsum) {
+            for (long c = ((long)blockIdx.x * 256 + threadIdx.x) * 4; c < args.N; c += (long)gridDim.x * 256 * 4) {
+                const float* p = args.ws + (long)splits * plane + c;
+                f32x4 v = *reinterpret_cast<const f32x4*>(p);
+                for (int k = 1; k < splits; ++k) {
+                    const f32x4 t = *reinterpret_cast<const f32x4*>(p + (long)k * args.N);
+                    v += t;
+                }
+                f32x4* o = reinterpret_cast<f32x4*>(args.colsum + c);
+                if (args.accumulate) v += *o;
+                *o = v;
+            }
+        }
+    }
     for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < nq; i += (long)gridDim.x * 256) {
         const int row = (int)(i / (args.N / 4)), col = (int)(i % (args.N / 4)) * 4;
         const float* p = args.ws + (long)row * args.N + col;
@@ -889,8 +907,7 @@ gp_status launch_tile(const GemmArgs& a, int epi, int splits, hipStream_t st) {
         default: return set_error(GP_ERR_INVALID_ARG, "gemm: split-K epilogue");
         }
         GP_LAUNCH_CHECK();
-        if (epi == EPI_ACC_F32 && !BKM && a.colsum)
-            return colsum_finalize(a.ws + (long)splits * a.M * a.N, splits, a.N, a.colsum, a.accumulate, st);
+
         return GP_OK;
     }
     switch (epi) {
@@ -924,8 +941,7 @@ gp_status launch_dl(const GemmArgs& a, int epi, int splits, hipStream_t st) {
         default: return set_error(GP_ERR_INVALID_ARG, "gemm: split-K epilogue");
         }
         GP_LAUNCH_CHECK();
-        if (epi == EPI_ACC_F32 && !KM && a.colsum)
-            return colsum_finalize(a.ws + (long)splits * a.M * a.N, splits, a.N, a.colsum, a.accumulate, st);
+
         return GP_OK;
     }
     if constexpr (KM) {
@@ -992,16 +1008,19 @@ bool split_fits(const GemmArgs& a, int s, int nk) {
 // k-steps x per-step time of the tile shape (with the tile running alone on
 // its CU or sharing it with a second one) + the fp32 read-modify-write of an
 // accumulating epilogue + the split-K partial traffic and reduce.  The
-// per-step times and costs were fitted to measurements of the d_model 1024
-// partition's GEMMs on MI355X at 512 and 2048 token rows.  Units: us.
-void choose_dl(const GemmArgs& a, int epi, int& cfg, int& splits) {
-    struct Cand { int cfg, bm, bn, resident; double step_alone, step_full; };
-    static const Cand cands[5] = {{T_DL128x128_W8A, 128, 128, 2, 0.516, 0.903},
-                                  {T_DL128x128_S2, 128, 128, 2, 0.587, 1.012},
-                                  {T_DL256x256_W8, 256, 256, 1, 1.360, 1.360},
-                                  {T_DL256x128_W8, 256, 128, 1, 0.815, 0.815},
-                                  {T_DL128x256_W8, 128, 256, 1, 0.766, 0.766}};
-    constexpr double BW = 3.976e6;  // bytes per us of split partials / accumulator traffic
+// constants were fitted to measurements of the d_model 1024 partition's GEMMs
+// on MI355X at 512 and 2048 token rows, separately for k-contiguous operands
+// (forward and input-gradient GEMMs) and m/n-contiguous ones (weight
+// gradients, whose transposing LDS reads cost more per step).  Units: us.
+void choose_dl(const GemmArgs& a, int epi, bool kmaj, int& cfg, int& splits) {
+    struct Cand { int cfg, bm, bn, resident; double step_alone[2], step_full[2]; };  // [k-contiguous, m-contiguous]
+    static const Cand cands[5] = {{T_DL128x128_W8A, 128, 128, 2, {0.516, 0.731}, {0.903, 0.966}},
+                                  {T_DL128x128_S2, 128, 128, 2, {0.587, 1.201}, {1.012, 1.280}},
+                                  {T_DL256x256_W8, 256, 256, 1, {1.360, 1.647}, {1.360, 1.647}},
+                                  {T_DL256x128_W8, 256, 128, 1, {0.815, 1.110}, {0.815, 1.110}},
+                                  {T_DL128x256_W8, 128, 256, 1, {0.766, 1.052}, {0.766, 1.052}}};
+    const int v = kmaj ? 0 : 1;
+    const double c0 = kmaj ? 3.889 : 2.435, BW = kmaj ? 3.976e6 : 5.462e6, red0 = kmaj ? 7.233 : 10.12;
     const int nk = a.K / 64;
     double best = 1e300;
     cfg = T_DL128x128_W8A;
@@ -1012,10 +1031,10 @@ void choose_dl(const GemmArgs& a, int epi, int& cfg, int& splits) {
             if (s > 1 && !split_fits(a, s, nk)) continue;
             const long per_cu = (tiles * s + NUM_CU - 1) / NUM_CU;
             const long rounds = (per_cu + c.resident - 1) / c.resident;
-            const double step = per_cu >= c.resident ? c.step_full : c.step_alone;
-            double t = 3.889 + rounds * (double)((nk + s - 1) / s) * step;
-            if (epi == EPI_ACC_F32) t += 1.074 + (double)a.M * a.N * 8.0 / BW;
-            if (s > 1) t += (double)a.M * a.N * 4.0 * (s + 1.0) / 2.0 / BW + 7.233;
+            const double step = per_cu >= c.resident ? c.step_full[v] : c.step_alone[v];
+            double t = c0 + rounds * (double)((nk + s - 1) / s) * step;
+            if (epi == EPI_ACC_F32) t += (kmaj ? 1.074 : 0.0) + (double)a.M * a.N * 8.0 / BW;
+            if (s > 1) t += (double)a.M * a.N * 4.0 * (s + 1.0) / 2.0 / BW + red0;
             if (t < best * 0.999) {
                 best = t;
                 cfg = c.cfg;
@@ -1078,7 +1097,7 @@ gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dty
         if (s != GP_OK) return s;
         int cfg, splits;
         if (a.K % 64 == 0)
-            choose_dl(a, epi, cfg, splits);
+            choose_dl(a, epi, a_kmajor, cfg, splits);
         else
             choose(a, epi, cfg, splits);
         if (a.force_cfg >= 0 && a.force_cfg <= T_LAST) {

@@ -41,11 +41,12 @@ gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dty
 gp_status layernorm_fwd(int dtype, const float* x, long rows, int D, const float* gamma, const float* beta,
                         float eps, void* out, float* stats, hipStream_t st);
 // dx = dres + rstd (g - mean g - xh mean(g xh)), g = dn * gamma; writes dx_f32 and/or dx_elt.
-// Per-block partial sums of dn * xh and dn go to partial[blk][2][D]; *nblk
-// receives the block count (for colsum_finalize over width 2 D).
+// Per-block partial sums of dn * xh and dn go to partial[blk][2][D] (added to
+// what is there when accumulate != 0); *nblk receives the block count (for
+// colsum_finalize over width 2 D).  The block count depends on rows only.
 gp_status layernorm_bwd(int dtype, const float* dn, const float* x, const float* stats, const float* gamma,
                         long rows, int D, const float* dres, float* dx_f32, void* dx_elt, float* partial,
-                        int* nblk, hipStream_t st);
+                        int accumulate, int* nblk, hipStream_t st);
 // Rows the partial buffers of layernorm_bwd / bias_grad may need.
 int layernorm_bwd_blocks(long rows);
 int bias_grad_blocks(long rows);

@@ -63,7 +63,8 @@ __global__ void __launch_bounds__(256) ln_bwd_kernel(const float* __restrict__ d
                                                      const float* __restrict__ stats,
                                                      const float* __restrict__ gamma, long rows, int D, int rpw,
                                                      const float* __restrict__ dres, float* __restrict__ dx32,
-                                                     T* __restrict__ dxe, float* __restrict__ partial) {
+                                                     T* __restrict__ dxe, float* __restrict__ partial,
+                                                     int accumulate) {
     __shared__ float red[LN_WAVES][2][C * 64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     float pg[C], pb[C];
@@ -115,7 +116,8 @@ __global__ void __launch_bounds__(256) ln_bwd_kernel(const float* __restrict__ d
         float s = 0.f;
 #pragma unroll
         for (int w = 0; w < LN_WAVES; ++w) s += red[w][which][d];
-        partial[(long)blockIdx.x * 2 * D + i] = s;
+        float* pp = partial + (long)blockIdx.x * 2 * D + i;
+        *pp = accumulate ? *pp + s : s;
     }
 }
 
@@ -196,7 +198,7 @@ __global__ void __launch_bounds__(256) ln_bwd_v4(const float* __restrict__ dn, c
                                                  const float* __restrict__ stats, const float* __restrict__ gamma,
                                                  long rows, int D, int rpw, const float* __restrict__ dres,
                                                  float* __restrict__ dx32, T* __restrict__ dxe,
-                                                 float* __restrict__ partial) {
+                                                 float* __restrict__ partial, int accumulate) {
     __shared__ f32x4 red[LN_WAVES][2][C4 * 64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const f32x4* g4 = reinterpret_cast<const f32x4*>(gamma);
@@ -246,7 +248,9 @@ __global__ void __launch_bounds__(256) ln_bwd_v4(const float* __restrict__ dn, c
         f32x4 t = red[0][which][d];
 #pragma unroll
         for (int w = 1; w < LN_WAVES; ++w) t += red[w][which][d];
-        reinterpret_cast<f32x4*>(partial + (long)blockIdx.x * 2 * D + which * D)[d] = t;
+        f32x4* pp = reinterpret_cast<f32x4*>(partial + (long)blockIdx.x * 2 * D + which * D) + d;
+        if (accumulate) t += *pp;
+        *pp = t;
     }
 }
 
@@ -298,13 +302,14 @@ gp_status ln_fwd_t(const float* x, long rows, int D, const float* g, const float
 
 template <typename T>
 gp_status ln_bwd_t(const float* dn, const float* x, const float* stats, const float* gamma, long rows, int D,
-                   const float* dres, float* dx32, void* dxe, float* partial, int* nblk, hipStream_t st) {
+                   const float* dres, float* dx32, void* dxe, float* partial, int accumulate, int* nblk,
+                   hipStream_t st) {
     const int rpw = ln_bwd_rows_per_wave(rows);
     const int grid = (int)((rows + (long)LN_WAVES * rpw - 1) / ((long)LN_WAVES * rpw));
     *nblk = grid;
     T* e = reinterpret_cast<T*>(dxe);
     if (D % 256 == 0 && D <= 2048) {
-#define GP_LNV(CC) klaunch(ln_bwd_v4<T, CC>, grid, 256, 0, st, dn, x, stats, gamma, rows, D, rpw, dres, dx32, e, partial)
+#define GP_LNV(CC) klaunch(ln_bwd_v4<T, CC>, grid, 256, 0, st, dn, x, stats, gamma, rows, D, rpw, dres, dx32, e, partial, accumulate)
         switch (D / 256) {
         case 1: GP_LNV(1); break;
         case 2: GP_LNV(2); break;
@@ -320,7 +325,7 @@ gp_status ln_bwd_t(const float* dn, const float* x, const float* stats, const fl
         return GP_OK;
     }
     const int C = (D + 63) / 64;
-#define GP_LNB(CC) klaunch(ln_bwd_kernel<T, CC>, grid, 256, 0, st, dn, x, stats, gamma, rows, D, rpw, dres, dx32, e, partial)
+#define GP_LNB(CC) klaunch(ln_bwd_kernel<T, CC>, grid, 256, 0, st, dn, x, stats, gamma, rows, D, rpw, dres, dx32, e, partial, accumulate)
     if (C <= 1) GP_LNB(1);
     else if (C <= 2) GP_LNB(2);
     else if (C <= 4) GP_LNB(4);
@@ -349,10 +354,10 @@ gp_status layernorm_fwd(int dtype, const float* x, long rows, int D, const float
 
 gp_status layernorm_bwd(int dtype, const float* dn, const float* x, const float* stats, const float* gamma,
                         long rows, int D, const float* dres, float* dx_f32, void* dx_elt, float* partial,
-                        int* nblk, hipStream_t st) {
+                        int accumulate, int* nblk, hipStream_t st) {
     if (dtype == GP_BF16)
-        return ln_bwd_t<bf16>(dn, x, stats, gamma, rows, D, dres, dx_f32, dx_elt, partial, nblk, st);
-    return ln_bwd_t<float>(dn, x, stats, gamma, rows, D, dres, dx_f32, dx_elt, partial, nblk, st);
+        return ln_bwd_t<bf16>(dn, x, stats, gamma, rows, D, dres, dx_f32, dx_elt, partial, accumulate, nblk, st);
+    return ln_bwd_t<float>(dn, x, stats, gamma, rows, D, dres, dx_f32, dx_elt, partial, accumulate, nblk, st);
 }
 
 gp_status colsum_finalize(const float* partial, int nblk, int width, float* out, int accumulate, hipStream_t st) {

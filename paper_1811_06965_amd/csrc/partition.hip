@@ -146,6 +146,9 @@ struct gp_partition {
     std::vector<float*> xs[2];
     std::vector<LayerWs> lw[2];
     int nsets = 1;
+    // per LayerNorm: block partial sums of its gamma/beta gradients, added up
+    // over the micro-batches of a mini-batch and reduced after the last one
+    std::vector<float*> lnpart;
     BwdWs bw;
     size_t bytes_params = 0, bytes_grads = 0, bytes_stash = 0, bytes_ws = 0;
     // GEMM tile-shape override (GP_GEMM_TILE = 0..10, GP_GEMM_SPLITS), read at
@@ -251,6 +254,9 @@ void plan_workspace(gp_partition* p, Arena& a) {
         if (pm > part) part = pm;
     }
     b.partial = a.take<float>(part);
+    const std::vector<const Norm*> norms = p->plan.norms();
+    p->lnpart.assign(norms.size(), nullptr);
+    for (const Norm* n : norms) p->lnpart[n->id] = a.take<float>((size_t)layernorm_bwd_blocks(T) * 2 * n->n);
     // split-K partials: up to 8 splits of a T x D activation GEMM or of the
     // D x 3D packed-QKV weight gradient (with its bias column sums)
     b.splitk_elems = std::max<long>(8 * T * D, 8 * (3 * D * D + 3 * D));
@@ -274,6 +280,7 @@ struct Ctx {
     hipStream_t st;
     int dt;
     float* ws = nullptr;        // split-K partials for launches on st
+    bool last = false;          // the mini-batch's last backward micro-batch
 };
 
 enum class Lane { Main, Side, Remat };
@@ -439,16 +446,21 @@ struct DwJob {
     long rows;
 };
 
+// LayerNorm backward: dx, and the gamma/beta gradient partials added into
+// the norm's partial buffer (overwritten on the first backward micro-batch);
+// after the last micro-batch they are reduced into the gradients.
 gp_status norm_bwd(const Ctx& c, const Norm& N, const float* dn, const float* x, const float* stats, long rows,
                    const float* dres, float* dx32, void* dxe, int accumulate) {
     int nblk = 0;
+    float* part = c.p->lnpart[N.id];
     const double rd = (double)rows * N.n;
     const double by = rd * (8.0 + (dres ? 4.0 : 0.0) + (dx32 ? 4.0 : 0.0) + (dxe ? (double)c.p->esz : 0.0)) +
-                      rows * 8.0 + N.n * 4.0 * (accumulate ? 4.0 : 2.0);
+                      rows * 8.0 + (double)layernorm_bwd_blocks(rows) * 2 * N.n * 4.0 * (accumulate ? 2.0 : 1.0);
     return timed(c, GP_K_LN_BWD, 0.0, by, [&] {
-        GP_TRY(layernorm_bwd(c.dt, dn, x, stats, c.p->master + N.g, rows, N.n, dres, dx32, dxe, c.p->bw.partial,
+        GP_TRY(layernorm_bwd(c.dt, dn, x, stats, c.p->master + N.g, rows, N.n, dres, dx32, dxe, part, accumulate,
                              &nblk, c.st));
-        return colsum_finalize(c.p->bw.partial, nblk, 2 * N.n, c.p->grads + N.g, accumulate, c.st);
+        if (!c.last) return GP_OK;
+        return colsum_finalize(part, nblk, 2 * N.n, c.p->grads + N.g, 0, c.st);
     });
 }
 
@@ -937,6 +949,7 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     const bool dec = p->g.kind == GP_DECODER_CROSS;
     if (!dec && dmem) return set_error(GP_ERR_INVALID_ARG, "encoder partitions have no memory gradient");
     Ctx c = make_ctx(p, (hipStream_t)stream);
+    c.last = mb == 0;
     Ctx cs = make_ctx(p, p->side, Lane::Side);
     const bool side = p->use_side && p->side;
     const bool first = p->sched.first_backward();

@@ -99,6 +99,7 @@ struct Linear {
 struct Norm {
     size_t g = 0, b = 0;
     int n = 0;
+    int id = 0;                 // index among the partition's LayerNorms
     bool present = false;
 };
 struct LayerPlan {
@@ -151,9 +152,11 @@ inline ParamPlan plan_params(const Dims& d, const Geometry& g) {
         e = align_up(x.nk + (size_t)in * out, 128);
         p.count += (size_t)in * out + out;
     };
+    int nnorm = 0;
     auto norm = [&](Norm& x, int n) {
         x.present = true;
         x.n = n;
+        x.id = nnorm++;
         x.g = f;
         x.b = f + n;
         f = align_up(x.b + n, 64);

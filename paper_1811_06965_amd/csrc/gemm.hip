@@ -33,6 +33,7 @@
 // own L2.
 #include <algorithm>
 
+#include <cstdlib>
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -616,6 +617,8 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
     constexpr int STAGE = (BM + BN) * 128;
     constexpr int PA = BM / (8 * NW), PB = BN / (8 * NW);  // 1 KB load blocks per wave for A and B
     static_assert(PA * 8 * NW == BM && PB * 8 * NW == BN, "load blocks");
+    // m-contiguous tiles swizzle 16-byte chunks by 4 (k % 4): rows need >= 16 chunks
+    static_assert(KM || (BM >= 128 && BN >= 128), "m-contiguous tiles must be at least 128 wide");
     constexpr int LPW = PA + PB;               // load instructions per wave per k-tile
     __shared__ __attribute__((aligned(1024))) char smem[NSTAGE * STAGE];
 
@@ -886,7 +889,8 @@ enum TileCfg {
     T_DL128x128_S2 = 4, T_DL128x128_S3 = 5, T_DL256x128_S2 = 6, T_DL256x256_S2 = 7,  // direct-to-LDS, k-contiguous
     T_DL256x256_W8 = 8, T_DL256x128_W8 = 9, T_DL128x256_W8 = 10,                          // ... with 8 waves
     T_DL128x128_W8A = 11, T_DL128x128_W8B = 12, T_DL256x128_W8S3 = 13, T_DL128x256_W8S3 = 14,
-    T_LAST = T_DL128x256_W8S3
+    T_DL128x64 = 15, T_DL64x128 = 16, T_DL128x64_S3 = 17,
+    T_LAST = T_DL128x64_S3
 };
 
 template <typename T, int BM, int BN, bool AK, bool BKM>
@@ -979,6 +983,15 @@ gp_status launch_bf16(const GemmArgs& a, int epi, int cfg, int splits, hipStream
         case T_DL128x128_W8B: return launch_dl<128, 128, 4, 2, 2, KM>(a, epi, splits, st);
         case T_DL256x128_W8S3: return launch_dl<256, 128, 4, 2, 3, KM>(a, epi, splits, st);
         case T_DL128x256_W8S3: return launch_dl<128, 256, 2, 4, 3, KM>(a, epi, splits, st);
+        case T_DL128x64:
+            if constexpr (KM) return launch_dl<128, 64, 2, 2, 2, KM>(a, epi, splits, st);
+            break;
+        case T_DL64x128:
+            if constexpr (KM) return launch_dl<64, 128, 2, 2, 2, KM>(a, epi, splits, st);
+            break;
+        case T_DL128x64_S3:
+            if constexpr (KM) return launch_dl<128, 64, 2, 2, 3, KM>(a, epi, splits, st);
+            break;
         default: break;
         }
     }
@@ -1009,32 +1022,48 @@ bool split_fits(const GemmArgs& a, int s, int nk) {
 // its CU or sharing it with a second one) + the fp32 read-modify-write of an
 // accumulating epilogue + the split-K partial traffic and reduce.  The
 // constants were fitted to measurements of the d_model 1024 partition's GEMMs
-// on MI355X at 512 and 2048 token rows, separately for k-contiguous operands
+// on MI355X at 512, 2048 and 4096 token rows, separately for k-contiguous operands
 // (forward and input-gradient GEMMs) and m/n-contiguous ones (weight
 // gradients, whose transposing LDS reads cost more per step).  Units: us.
+// Weight of the split-K cost terms (GP_SPLIT_WEIGHT, default 1): the fit was
+// made on GEMMs running alone; next to concurrent work the partial traffic
+// can cost more.
+double split_weight() {
+    static const double w = [] {
+        const char* e = std::getenv("GP_SPLIT_WEIGHT");
+        return e ? std::atof(e) : 1.0;
+    }();
+    return w;
+}
+
 void choose_dl(const GemmArgs& a, int epi, bool kmaj, int& cfg, int& splits) {
-    struct Cand { int cfg, bm, bn, resident; double step_alone[2], step_full[2]; };  // [k-contiguous, m-contiguous]
-    static const Cand cands[5] = {{T_DL128x128_W8A, 128, 128, 2, {0.516, 0.731}, {0.903, 0.966}},
-                                  {T_DL128x128_S2, 128, 128, 2, {0.587, 1.201}, {1.012, 1.280}},
-                                  {T_DL256x256_W8, 256, 256, 1, {1.360, 1.647}, {1.360, 1.647}},
-                                  {T_DL256x128_W8, 256, 128, 1, {0.815, 1.110}, {0.815, 1.110}},
-                                  {T_DL128x256_W8, 128, 256, 1, {0.766, 1.052}, {0.766, 1.052}}};
+    // per-step time with 1, 2 or 3 tiles sharing a CU; [k-contiguous][m-contiguous]; 0 = not available
+    struct Cand { int cfg, bm, bn, resident; double step[2][3]; };
+    static const Cand cands[7] = {
+        {T_DL128x128_W8A, 128, 128, 2, {{0.586, 1.154, 0}, {0.754, 0.952, 0}}},
+        {T_DL128x128_S2, 128, 128, 2, {{0.636, 1.192, 0}, {1.186, 1.259, 0}}},
+        {T_DL256x256_W8, 256, 256, 1, {{1.498, 0, 0}, {1.612, 0, 0}}},
+        {T_DL256x128_W8, 256, 128, 1, {{0.970, 0, 0}, {1.117, 0, 0}}},
+        {T_DL128x256_W8, 128, 256, 1, {{0.875, 0, 0}, {1.066, 0, 0}}},
+        {T_DL128x64, 128, 64, 3, {{0.443, 0.657, 1.030}, {0, 0, 0}}},
+        {T_DL64x128, 64, 128, 3, {{0.463, 0.640, 0.848}, {0, 0, 0}}}};
     const int v = kmaj ? 0 : 1;
-    const double c0 = kmaj ? 3.889 : 2.435, BW = kmaj ? 3.976e6 : 5.462e6, red0 = kmaj ? 7.233 : 10.12;
+    const double c0 = kmaj ? 3.052 : 1.519, BW = kmaj ? 3.704e6 : 4.646e6, red0 = kmaj ? 6.278 : 8.667;
     const int nk = a.K / 64;
     double best = 1e300;
     cfg = T_DL128x128_W8A;
     splits = 1;
     for (const Cand& c : cands) {
+        if (c.step[v][0] <= 0) continue;
         const long tiles = (long)((a.M + c.bm - 1) / c.bm) * ((a.N + c.bn - 1) / c.bn);
         for (int s = 1; s <= 8; s *= 2) {
             if (s > 1 && !split_fits(a, s, nk)) continue;
             const long per_cu = (tiles * s + NUM_CU - 1) / NUM_CU;
             const long rounds = (per_cu + c.resident - 1) / c.resident;
-            const double step = per_cu >= c.resident ? c.step_full[v] : c.step_alone[v];
-            double t = c0 + rounds * (double)((nk + s - 1) / s) * step;
-            if (epi == EPI_ACC_F32) t += (kmaj ? 1.074 : 0.0) + (double)a.M * a.N * 8.0 / BW;
-            if (s > 1) t += (double)a.M * a.N * 4.0 * (s + 1.0) / 2.0 / BW + red0;
+            const int occ = (int)std::min<long>(per_cu, c.resident);
+            double t = c0 + rounds * (double)((nk + s - 1) / s) * c.step[v][occ - 1];
+            if (epi == EPI_ACC_F32) t += (kmaj ? 3.0 : 0.0) + (double)a.M * a.N * 8.0 / BW;
+            if (s > 1) t += split_weight() * ((double)a.M * a.N * 4.0 * (s + 1.0) / 2.0 / BW + red0);
             if (t < best * 0.999) {
                 best = t;
                 cfg = c.cfg;
@@ -1106,6 +1135,7 @@ gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dty
             if (splits > 1 && !split_fits(a, splits, (a.K + 63) / 64)) splits = 1;
         }
         if (cfg > T128x128 && a.K % 64) cfg = T128x128;
+        if (!a_kmajor && cfg >= T_DL128x64) cfg = T_DL128x128_W8A;  // no 64-wide m-contiguous tiles
         return a_kmajor ? launch_bf16<true, true>(a, epi, cfg, splits, st)
                         : launch_bf16<false, false>(a, epi, cfg, splits, st);
     }

@@ -37,9 +37,11 @@ struct GemmArgs {
 gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dtype, hipStream_t st);
 
 // ------------------------------------------------------------- LayerNorm
-// out (elt) = gamma * (x - mu) * rstd + beta per row of D; stats[row] = {mu, rstd}
+// out (elt) = gamma * (x - mu) * rstd + beta per row of D; stats[row] = {mu, rstd}.
+// split (bf16 only): out rows are 2 D wide, [bf16(y) | bf16(y - bf16(y))], the
+// input of a GEMM that reads the row at about 16 more bits of precision.
 gp_status layernorm_fwd(int dtype, const float* x, long rows, int D, const float* gamma, const float* beta,
-                        float eps, void* out, float* stats, hipStream_t st);
+                        float eps, void* out, float* stats, int split, hipStream_t st);
 // dx = dres + rstd (g - mean g - xh mean(g xh)), g = dn * gamma; writes dx_f32 and/or dx_elt.
 // Per-block partial sums of dn * xh and dn go to partial[blk][2][D] (added to
 // what is there when accumulate != 0); *nblk receives the block count (for
@@ -64,6 +66,10 @@ struct AttnArgs {
     const void* k = nullptr; long ldk = 0; // row (b, j) at k + (b Sk + j) ldk + h dh
     const void* v = nullptr; long ldv = 0;
     void* o = nullptr; long ldo = 0;
+    // optional (bf16): the rounding residual o - bf16(o), rounded to bf16, in
+    // o's layout; the forward writes it and the dQ pass forms delta from
+    // o + olo, so that delta matches the probabilities the backward recomputes
+    void* olo = nullptr;
     float* lse = nullptr;                  // [n, H, Sq] log-sum-exp of the scaled scores
     int causal = 0;
     float scale = 1.f;
@@ -100,7 +106,9 @@ int xent_partials(long rows);
 gp_status sgd_update(float* w, const float* g, float lr, long count, hipStream_t st);
 // Working copies of one linear layer from its fp32 master W [in, out]:
 // kn (elt) = W, nk (elt) = W^T.
-gp_status refresh_linear(int dtype, const float* w, int in, int out, void* kn, void* nk, hipStream_t st);
+// kn = W [in, out]; nk = W^T [out, in], or with split [out, 2 in] holding
+// each row of W^T twice (the B operand of a GEMM whose input rows are split).
+gp_status refresh_linear(int dtype, const float* w, int in, int out, void* kn, void* nk, int split, hipStream_t st);
 // An empty launch labelled by its grid (role x (edge + 1) workgroups of one
 // wave): edge 0 before, 1 after a timed launch, so that per-dispatch profiler
 // records can be attributed to launch roles.

@@ -114,10 +114,11 @@ __global__ void __launch_bounds__(256) sgd_kernel(float* __restrict__ w, const f
     for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < count; i += (long)gridDim.x * 256) w[i] -= lr * g[i];
 }
 
-// kn = W, nk = W^T through a 64 x 64 LDS tile (both writes coalesced).
+// kn = W, nk = W^T through a 64 x 64 LDS tile (both writes coalesced); with
+// split the rows of nk are 2 in wide and hold the row of W^T twice.
 template <typename T>
 __global__ void __launch_bounds__(256) refresh_kernel(const float* __restrict__ w, int in, int out,
-                                                      T* __restrict__ kn, T* __restrict__ nk) {
+                                                      T* __restrict__ kn, T* __restrict__ nk, int split) {
     __shared__ float tile[64][65];
     const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
     const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
@@ -132,7 +133,15 @@ __global__ void __launch_bounds__(256) refresh_kernel(const float* __restrict__ 
     __syncthreads();
     for (int c = ty; c < 64; c += 4) {
         const int col = c0 + c, row = r0 + tx;
-        if (row < in && col < out) nk[(long)col * in + row] = to_elt<T>(tile[tx][c]);
+        if (row < in && col < out) {
+            const T v = to_elt<T>(tile[tx][c]);
+            if (split) {
+                nk[(long)col * 2 * in + row] = v;
+                nk[(long)col * 2 * in + in + row] = v;
+            } else {
+                nk[(long)col * in + row] = v;
+            }
+        }
     }
 }
 
@@ -206,12 +215,12 @@ gp_status sgd_update(float* w, const float* g, float lr, long count, hipStream_t
     return GP_OK;
 }
 
-gp_status refresh_linear(int dtype, const float* w, int in, int out, void* kn, void* nk, hipStream_t st) {
+gp_status refresh_linear(int dtype, const float* w, int in, int out, void* kn, void* nk, int split, hipStream_t st) {
     dim3 grid((out + 63) / 64, (in + 63) / 64);
     if (dtype == GP_BF16)
-        klaunch(refresh_kernel<bf16>, grid, 256, 0, st, w, in, out, reinterpret_cast<bf16*>(kn), reinterpret_cast<bf16*>(nk));
+        klaunch(refresh_kernel<bf16>, grid, 256, 0, st, w, in, out, reinterpret_cast<bf16*>(kn), reinterpret_cast<bf16*>(nk), split);
     else
-        klaunch(refresh_kernel<float>, grid, 256, 0, st, w, in, out, reinterpret_cast<float*>(kn), reinterpret_cast<float*>(nk));
+        klaunch(refresh_kernel<float>, grid, 256, 0, st, w, in, out, reinterpret_cast<float*>(kn), reinterpret_cast<float*>(nk), split);
     GP_LAUNCH_CHECK();
     return GP_OK;
 }

@@ -1,7 +1,8 @@
 // norm.hip -- LayerNorm forward/backward and deterministic column reductions.
 //
 // LayerNorm over the feature dimension D of each token row (biased variance,
-// eps inside the square root).  One wave owns one row; lane l holds features
+// eps inside the square root).  A split output row holds 2 D elements: the
+// bf16 values, then their rounding residuals (see layernorm_fwd).  One wave owns one row; lane l holds features
 // l, l + 64, ... so every global access is a coalesced 256-byte row segment.
 // Parameter gradients are reduced in two deterministic stages: per-block
 // partial sums, then a fixed-order column sum (no atomics), so re-running a
@@ -19,7 +20,7 @@ template <typename T, int C>
 __global__ void __launch_bounds__(256) ln_fwd_kernel(const float* __restrict__ x, long rows, int D,
                                                      const float* __restrict__ gamma,
                                                      const float* __restrict__ beta, float eps,
-                                                     T* __restrict__ out, float* __restrict__ stats) {
+                                                     T* __restrict__ out, float* __restrict__ stats, int split) {
     const int lane = threadIdx.x & 63;
     const long row = (long)blockIdx.x * LN_WAVES + (threadIdx.x >> 6);
     if (row >= rows) return;
@@ -41,11 +42,16 @@ __global__ void __launch_bounds__(256) ln_fwd_kernel(const float* __restrict__ x
         q += t * t;
     }
     const float rstd = 1.f / sqrtf(wave_sum(q) / D + eps);
-    T* orow = out + row * D;
+    T* orow = out + row * (split ? 2 * D : D);
 #pragma unroll
     for (int c = 0; c < C; ++c) {
         const int d = lane + c * 64;
-        if (d < D) orow[d] = to_elt<T>(gamma[d] * ((v[c] - mu) * rstd) + beta[d]);
+        if (d < D) {
+            const float y = gamma[d] * ((v[c] - mu) * rstd) + beta[d];
+            const T hi = to_elt<T>(y);
+            orow[d] = hi;
+            if (split) orow[D + d] = to_elt<T>(y - (float)hi);
+        }
     }
     if (stats && lane == 0) {
         stats[2 * row] = mu;
@@ -146,10 +152,18 @@ __global__ void __launch_bounds__(1024) colsum_kernel(const float* __restrict__ 
 template <typename T> struct Out4;
 template <> struct Out4<float> {
     static __device__ __forceinline__ void store(float* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
+    static __device__ __forceinline__ void store_lo(float*, f32x4) {}  // fp32 rows are never split
 };
 template <> struct Out4<bf16> {
     static __device__ __forceinline__ void store(bf16* p, f32x4 v) {
         bf16x4 b = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
+        *reinterpret_cast<bf16x4*>(p) = b;
+    }
+    // the rounding residual v - bf16(v), rounded to bf16
+    static __device__ __forceinline__ void store_lo(bf16* p, f32x4 v) {
+        bf16x4 b;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) b[i] = (bf16)(v[i] - (float)(bf16)v[i]);
         *reinterpret_cast<bf16x4*>(p) = b;
     }
 };
@@ -159,7 +173,8 @@ __device__ __forceinline__ float hsum(f32x4 v) { return (v[0] + v[1]) + (v[2] + 
 template <typename T, int C4>
 __global__ void __launch_bounds__(256) ln_fwd_v4(const float* __restrict__ x, long rows, int D,
                                                  const float* __restrict__ gamma, const float* __restrict__ beta,
-                                                 float eps, T* __restrict__ out, float* __restrict__ stats) {
+                                                 float eps, T* __restrict__ out, float* __restrict__ stats,
+                                                 int split) {
     const int lane = threadIdx.x & 63;
     const long row = (long)blockIdx.x * LN_WAVES + (threadIdx.x >> 6);
     if (row >= rows) return;
@@ -181,11 +196,13 @@ __global__ void __launch_bounds__(256) ln_fwd_v4(const float* __restrict__ x, lo
     const float rstd = 1.f / sqrtf(wave_sum(q) / D + eps);
     const f32x4* g4 = reinterpret_cast<const f32x4*>(gamma);
     const f32x4* b4 = reinterpret_cast<const f32x4*>(beta);
-    T* orow = out + row * D;
+    T* orow = out + row * (split ? 2 * D : D);
 #pragma unroll
     for (int c = 0; c < C4; ++c) {
         const int i = lane + 64 * c;
-        Out4<T>::store(orow + 4 * i, g4[i] * ((v[c] - mu) * rstd) + b4[i]);
+        const f32x4 y = g4[i] * ((v[c] - mu) * rstd) + b4[i];
+        Out4<T>::store(orow + 4 * i, y);
+        if (split) Out4<T>::store_lo(orow + D + 4 * i, y);
     }
     if (stats && lane == 0) {
         stats[2 * row] = mu;
@@ -271,30 +288,30 @@ __global__ void __launch_bounds__(256) bias_partial_kernel(const T* __restrict__
 
 template <typename T>
 gp_status ln_fwd_t(const float* x, long rows, int D, const float* g, const float* b, float eps, void* out,
-                   float* stats, hipStream_t st) {
+                   float* stats, int split, hipStream_t st) {
     const int grid = (int)((rows + LN_WAVES - 1) / LN_WAVES);
     T* o = reinterpret_cast<T*>(out);
     if (D % 256 == 0 && D <= 2048) {
         switch (D / 256) {
-        case 1: klaunch(ln_fwd_v4<T, 1>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats); break;
-        case 2: klaunch(ln_fwd_v4<T, 2>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats); break;
-        case 3: klaunch(ln_fwd_v4<T, 3>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats); break;
-        case 4: klaunch(ln_fwd_v4<T, 4>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats); break;
-        case 5: klaunch(ln_fwd_v4<T, 5>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats); break;
-        case 6: klaunch(ln_fwd_v4<T, 6>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats); break;
-        case 7: klaunch(ln_fwd_v4<T, 7>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats); break;
-        default: klaunch(ln_fwd_v4<T, 8>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats); break;
+        case 1: klaunch(ln_fwd_v4<T, 1>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split); break;
+        case 2: klaunch(ln_fwd_v4<T, 2>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split); break;
+        case 3: klaunch(ln_fwd_v4<T, 3>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split); break;
+        case 4: klaunch(ln_fwd_v4<T, 4>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split); break;
+        case 5: klaunch(ln_fwd_v4<T, 5>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split); break;
+        case 6: klaunch(ln_fwd_v4<T, 6>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split); break;
+        case 7: klaunch(ln_fwd_v4<T, 7>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split); break;
+        default: klaunch(ln_fwd_v4<T, 8>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split); break;
         }
         GP_LAUNCH_CHECK();
         return GP_OK;
     }
     const int C = (D + 63) / 64;
-    if (C <= 1) klaunch(ln_fwd_kernel<T, 1>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats);
-    else if (C <= 2) klaunch(ln_fwd_kernel<T, 2>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats);
-    else if (C <= 4) klaunch(ln_fwd_kernel<T, 4>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats);
-    else if (C <= 8) klaunch(ln_fwd_kernel<T, 8>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats);
-    else if (C <= 16) klaunch(ln_fwd_kernel<T, 16>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats);
-    else if (C <= 32) klaunch(ln_fwd_kernel<T, 32>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats);
+    if (C <= 1) klaunch(ln_fwd_kernel<T, 1>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split);
+    else if (C <= 2) klaunch(ln_fwd_kernel<T, 2>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split);
+    else if (C <= 4) klaunch(ln_fwd_kernel<T, 4>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split);
+    else if (C <= 8) klaunch(ln_fwd_kernel<T, 8>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split);
+    else if (C <= 16) klaunch(ln_fwd_kernel<T, 16>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split);
+    else if (C <= 32) klaunch(ln_fwd_kernel<T, 32>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split);
     else return set_error(GP_ERR_UNSUPPORTED, "layernorm: d_model > 2048");
     GP_LAUNCH_CHECK();
     return GP_OK;
@@ -347,9 +364,10 @@ int layernorm_bwd_blocks(long rows) {
 int bias_grad_blocks(long rows) { return rows < BIAS_BLOCKS ? (int)(rows > 0 ? rows : 1) : BIAS_BLOCKS; }
 
 gp_status layernorm_fwd(int dtype, const float* x, long rows, int D, const float* gamma, const float* beta,
-                        float eps, void* out, float* stats, hipStream_t st) {
-    if (dtype == GP_BF16) return ln_fwd_t<bf16>(x, rows, D, gamma, beta, eps, out, stats, st);
-    return ln_fwd_t<float>(x, rows, D, gamma, beta, eps, out, stats, st);
+                        float eps, void* out, float* stats, int split, hipStream_t st) {
+    if (dtype == GP_BF16) return ln_fwd_t<bf16>(x, rows, D, gamma, beta, eps, out, stats, split, st);
+    if (split) return set_error(GP_ERR_UNSUPPORTED, "layernorm: split output is for bf16 partitions");
+    return ln_fwd_t<float>(x, rows, D, gamma, beta, eps, out, stats, 0, st);
 }
 
 gp_status layernorm_bwd(int dtype, const float* dn, const float* x, const float* stats, const float* gamma,

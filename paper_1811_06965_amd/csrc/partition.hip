@@ -70,6 +70,7 @@ struct LayerWs {
     void *u = nullptr, *qkv = nullptr, *c = nullptr;
     float *stc = nullptr, *xlse = nullptr, *x2 = nullptr;
     void *uc = nullptr, *xq = nullptr, *xkv = nullptr, *xc = nullptr;
+    void *clo = nullptr, *xclo = nullptr;  // bf16 rounding residuals of c and xc (recompute only)
     float* stf = nullptr;
     void *v = nullptr, *a = nullptr;
 };
@@ -212,6 +213,7 @@ void plan_workspace(gp_partition* p, Arena& a) {
             l.u = a.take_elt(T * D, e);
             l.qkv = a.take_elt(T * 3 * D, e);
             l.c = a.take_elt(T * D, e);
+            if (p->g.dtype == GP_BF16) l.clo = a.take_elt(T * D, e);
             l.lse = a.take<float>(lse_n);
             l.x1 = a.take<float>(T * D);
             if (dec) {
@@ -220,11 +222,12 @@ void plan_workspace(gp_partition* p, Arena& a) {
                 l.xq = a.take_elt(T * D, e);
                 l.xkv = a.take_elt(Tm * 2 * D, e);
                 l.xc = a.take_elt(T * D, e);
+                if (p->g.dtype == GP_BF16) l.xclo = a.take_elt(T * D, e);
                 l.xlse = a.take<float>(lse_n);
                 l.x2 = a.take<float>(T * D);
             }
             l.stf = a.take<float>(2 * T);
-            l.v = a.take_elt(T * D, e);
+            l.v = a.take_elt(T * D * (p->g.dtype == GP_BF16 ? 2 : 1), e);  // split rows (see Linear::split)
             l.a = a.take_elt(T * F, e);
         }
     }
@@ -360,10 +363,10 @@ gp_status timed_attention(const Ctx& c, int role, const AttnArgs& a, bool bwd) {
 }
 
 gp_status timed_ln_fwd(const Ctx& c, const float* x, long rows, int D, const float* gamma, const float* beta,
-                       float eps, void* out, float* stats) {
-    const double by = (double)rows * D * (4.0 + c.p->esz) + rows * 8.0 + D * 8.0;
+                       float eps, void* out, float* stats, int split = 0) {
+    const double by = (double)rows * D * (4.0 + c.p->esz * (split ? 2 : 1)) + rows * 8.0 + D * 8.0;
     return timed(c, GP_K_LN_FWD, 0.0, by,
-                 [&] { return layernorm_fwd(c.dt, x, rows, D, gamma, beta, eps, out, stats, c.st); });
+                 [&] { return layernorm_fwd(c.dt, x, rows, D, gamma, beta, eps, out, stats, split, c.st); });
 }
 
 // Y = A W + b with an epilogue; A [M, K] k-contiguous, W^T working copy [N, K].
@@ -372,11 +375,11 @@ gp_status linear_fwd(const Ctx& c, const Linear& L, const void* A, long M, void*
     GemmArgs g;
     g.M = (int)M;
     g.N = L.out;
-    g.K = L.in;
+    g.K = L.split ? 2 * L.in : L.in;
     g.A = A;
-    g.lda = L.in;
+    g.lda = g.K;
     g.B = c.p->W(L.nk);
-    g.ldb = L.in;
+    g.ldb = g.K;
     g.C = C;
     g.ldc = ldc;
     g.C2 = C2;
@@ -422,7 +425,7 @@ gp_status linear_dw(const Ctx& c, const Linear& L, const void* X, const void* dY
     g.N = L.out;
     g.K = (int)rows;
     g.A = X;
-    g.lda = L.in;
+    g.lda = L.split ? 2 * L.in : L.in;  // split rows: the bf16 half
     g.B = dY;
     g.ldb = L.out;
     g.C = c.p->grads + L.w;
@@ -478,9 +481,10 @@ AttnArgs attn_args(const gp_partition* p, int Sk, int causal) {
 
 // One layer's forward.  `ws` holds its intermediates, x_in/x_out the residual
 // stream; mem is the decoder memory (elt [Tm, D]); y_out (optional) receives
-// the output rounded to the partition dtype.
+// the output rounded to the partition dtype.  keep: a recompute for the
+// backward, which also stores the attention outputs' rounding residuals.
 gp_status layer_forward(const Ctx& c, int l, LayerWs& w, const float* x_in, float* x_out, const void* mem,
-                        void* y_out) {
+                        void* y_out, bool keep) {
     gp_partition* p = c.p;
     const LayerPlan& P = p->plan.layers[l];
     const long T = p->g.T(), D = p->d.D;
@@ -497,6 +501,7 @@ gp_status layer_forward(const Ctx& c, int l, LayerWs& w, const float* x_in, floa
     a.o = w.c;
     a.ldo = D;
     a.lse = w.lse;
+    a.olo = keep ? w.clo : nullptr;
     GP_TRY(timed_attention(c, GP_K_ATTN_FWD, a, false));
     GP_TRY(linear_fwd(c, P.o, w.c, T, w.x1, D, EPI_RES_F32, 0, x_in, nullptr));
     const float* xf = w.x1;
@@ -514,13 +519,14 @@ gp_status layer_forward(const Ctx& c, int l, LayerWs& w, const float* x_in, floa
         x.o = w.xc;
         x.ldo = D;
         x.lse = w.xlse;
+        x.olo = keep ? w.xclo : nullptr;
         GP_TRY(timed_attention(c, GP_K_XATTN_FWD, x, false));
         GP_TRY(linear_fwd(c, P.xo, w.xc, T, w.x2, D, EPI_RES_F32, 0, w.x1, nullptr));
         xf = w.x2;
     }
     // feed-forward block
     const Norm& nf = dec ? P.ln3 : P.ln2;
-    GP_TRY(timed_ln_fwd(c, xf, T, (int)D, p->master + nf.g, p->master + nf.b, eps, w.v, w.stf));
+    GP_TRY(timed_ln_fwd(c, xf, T, (int)D, p->master + nf.g, p->master + nf.b, eps, w.v, w.stf, P.ffn1.split));
     GP_TRY(linear_fwd(c, P.ffn1, w.v, T, w.a, p->d.F, EPI_STORE, 1, nullptr, nullptr));
     GP_TRY(linear_fwd(c, P.ffn2, w.a, T, x_out, D, EPI_RES_F32, 0, xf, y_out));
     return GP_OK;
@@ -545,7 +551,7 @@ gp_status partition_forward(const Ctx& c, int m, bool keep, const void* x, const
         LayerWs& w = keep ? p->lw[set][l] : p->lw[set][0];
         const float* xi = keep ? xs[l] : xs[l & 1];
         float* xo = keep ? xs[l + 1] : xs[(l + 1) & 1];
-        GP_TRY(layer_forward(c, l, w, xi, xo, mem_m, (!keep && l == L - 1) ? y : nullptr));
+        GP_TRY(layer_forward(c, l, w, xi, xo, mem_m, (!keep && l == L - 1) ? y : nullptr, keep));
     }
     return GP_OK;
 }
@@ -613,6 +619,7 @@ gp_status layer_backward(const Ctx& c, int set, int l, bool first, float* in32, 
         x.dk = b.dxkv[par];
         x.dv = p->off_elt(b.dxkv[par], D);
         x.lddk = x.lddv = 2 * D;
+        x.olo = w.xclo;
         x.delta = b.delta;
         GP_TRY(timed_attention(c, GP_K_XATTN_BWD, x, true));
         jobs.push_back({&P.xq, w.uc, b.dxq[par], T});
@@ -644,6 +651,7 @@ gp_status layer_backward(const Ctx& c, int set, int l, bool first, float* in32, 
     a.dk = p->off_elt(b.dqkv[par], D);
     a.dv = p->off_elt(b.dqkv[par], 2 * D);
     a.lddq = a.lddk = a.lddv = 3 * D;
+    a.olo = w.clo;
     a.delta = b.delta;
     GP_TRY(timed_attention(c, GP_K_ATTN_BWD, a, true));
     jobs.push_back({&P.qkv, w.u, b.dqkv[par], T});
@@ -685,7 +693,7 @@ gp_status upload_param_block(gp_partition* p, const ParamRef& r, const float* ho
                        hipMemcpyHostToDevice));
     if (r.lin) {
         GP_TRY(refresh_linear(p->g.dtype, p->master + r.lin->w, r.lin->in, r.lin->out, p->W(r.lin->kn),
-                              p->W(r.lin->nk), nullptr));
+                              p->W(r.lin->nk), r.lin->split, nullptr));
         GP_HIP(hipDeviceSynchronize());
     }
     return GP_OK;
@@ -812,7 +820,7 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
         return hip_fail(e, __FILE__, __LINE__);
     }
     for (const Linear* l : p->plan.linears()) {
-        s = refresh_linear(g.dtype, p->master + l->w, l->in, l->out, p->W(l->kn), p->W(l->nk), nullptr);
+        s = refresh_linear(g.dtype, p->master + l->w, l->in, l->out, p->W(l->kn), p->W(l->nk), l->split, nullptr);
         if (s != GP_OK) {
             free_all(p);
             return s;
@@ -1074,7 +1082,7 @@ gp_status gp_accumulate_and_step(gp_partition* p, float lr, double* loss_out, gp
     }
     GP_TRY(sgd_update(p->master, p->grads, lr, (long)p->plan.n32, st));
     for (const Linear* l : p->plan.linears())
-        GP_TRY(refresh_linear(dt, p->master + l->w, l->in, l->out, p->W(l->kn), p->W(l->nk), st));
+        GP_TRY(refresh_linear(dt, p->master + l->w, l->in, l->out, p->W(l->kn), p->W(l->nk), l->split, st));
     if (loss_out) {
         double v = 0.0;
         if (p->g.loss != GP_LOSS_NONE)

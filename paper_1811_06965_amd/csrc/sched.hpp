@@ -94,6 +94,11 @@ struct Linear {
     size_t kn = 0, nk = 0;      // element offsets of the working copies
     int in = 0, out = 0;
     int role = 0;               // gp_kernel_role of its forward GEMM; +1 input gradient, +2 weight gradient
+    // bf16 feed-forward input projection: the forward reads its input rows as
+    // [bf16(y) | bf16(y - bf16(y))] against nk = [W^T | W^T] (reduction 2 in),
+    // so that the pre-activations, whose signs set the ReLU mask the backward
+    // uses, carry no rounding error from the LayerNorm output
+    bool split = false;
     bool present = false;
 };
 struct Norm {
@@ -139,17 +144,18 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 inline ParamPlan plan_params(const Dims& d, const Geometry& g) {
     ParamPlan p;
     size_t f = 0, e = 0;
-    auto lin = [&](Linear& x, int in, int out, int role) {
+    auto lin = [&](Linear& x, int in, int out, int role, bool split = false) {
         x.present = true;
         x.role = role;
         x.in = in;
         x.out = out;
+        x.split = split;
         x.w = f;
         x.b = f + (size_t)in * out;
         f = align_up(x.b + out, 64); // keep every block 256-byte aligned
         x.kn = e;
         x.nk = e + (size_t)in * out;
-        e = align_up(x.nk + (size_t)in * out, 128);
+        e = align_up(x.nk + (size_t)in * out * (split ? 2 : 1), 128);
         p.count += (size_t)in * out + out;
     };
     int nnorm = 0;
@@ -169,7 +175,7 @@ inline ParamPlan plan_params(const Dims& d, const Geometry& g) {
         lin(l.qkv, d.D, 3 * d.D, GP_K_QKV_FWD);
         lin(l.o, d.D, d.D, GP_K_O_FWD);
         norm(l.ln2, d.D);
-        lin(l.ffn1, d.D, d.F, GP_K_FFN1_FWD);
+        lin(l.ffn1, d.D, d.F, GP_K_FFN1_FWD, g.dtype == GP_BF16);
         lin(l.ffn2, d.F, d.D, GP_K_FFN2_FWD);
         if (dec) {
             lin(l.xq, d.D, d.D, GP_K_XQ_FWD);

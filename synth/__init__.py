@@ -118,10 +118,13 @@ def round_bf16(a: np.ndarray) -> np.ndarray:
     float32, whose top 16 bits are then kept with round-to-nearest-even.
     """
     f = np.ascontiguousarray(a, dtype=np.float32)
-    u = f.view(np.uint32).astype(np.uint64)
-    lsb = (u >> np.uint64(16)) & np.uint64(1)
-    r = ((u + np.uint64(0x7FFF) + lsb) >> np.uint64(16)) << np.uint64(16)
-    r = r.astype(np.uint32)
+    u = f.view(np.uint32)
+    # u + 0x7FFF + lsb stays below 2^32 for every non-NaN input (the largest
+    # finite pattern is 0xFF7FFFFF), so the sum needs no wider type
+    r = (u >> np.uint32(16)) & np.uint32(1)
+    r += np.uint32(0x7FFF)
+    r += u
+    r &= np.uint32(0xFFFF0000)
     nan = np.isnan(f)
     if nan.any():
         r[nan] = np.uint32(0x7FC00000)

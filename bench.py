@@ -95,18 +95,18 @@ def kernel_summary(d, command, top=25):
     print("| kernel | grid | calls | mean us | % of kernel time |\n|---|---|---|---|---|")
     for (n, gx, gy), (c, s) in sorted(agg.items(), key=lambda kv: -kv[1][1])[:top]:
         print(f"| `{n}` | ({gx},{gy}) | {c} | {s / c / 1e3:.1f} | {100 * s / total:.1f} |")
-    # launches between role markers
-    spans, cur = {}, None
-    for name, gx, gy, wx, t0, t1 in rows:
+    # launches between role markers, on the marker's stream, in enqueue order
+    spans, cur = {}, {}
+    for name, gx, gy, wx, t0, t1, sid in db.execute(
+            "select name, grid_x, grid_y, workgroup_x, start, end, stream_id from kernels order by dispatch_id"):
         if "role_marker" in name:
             role, edge = gx // max(wx, 1), gy - 1
             if edge == 0:
-                cur = (role, [])
-            elif cur is not None:
-                spans.setdefault(cur[0], []).append(cur[1])
-                cur = None
-        elif cur is not None:
-            cur[1].append((_short(name), t0, t1))
+                cur[sid] = (role, [])
+            elif sid in cur:
+                spans.setdefault(cur[sid][0], []).append(cur.pop(sid)[1])
+        elif sid in cur:
+            cur[sid][1].append((_short(name), t0, t1))
     if spans:
         print("\n## Launch roles (kernels between role markers)\n")
         print("| role | launches | mean kernel us per launch | mean first-start to last-end us | kernels |\n|---|---|---|---|---|")
@@ -147,31 +147,31 @@ def _pmc_rows(d):
 
 
 def _per_dispatch(rows, counter):
-    """[(dispatch id, kernel name, counter value)] for one counter (summed over
-    its instances)."""
+    """[(queue id, kernel name, counter value)] in dispatch order for one
+    counter (summed over its instances)."""
     acc = {}
     for r in rows:
         if r["Counter_Name"] != counter:
             continue
         k = int(r["Dispatch_Id"])
-        name, v = acc.get(k, (r["Kernel_Name"], 0.0))
-        acc[k] = (name, v + float(r["Counter_Value"]))
-    return [(k, n, v) for k, (n, v) in sorted(acc.items())]
+        q, name, v = acc.get(k, (r["Queue_Id"], r["Kernel_Name"], 0.0))
+        acc[k] = (q, name, v + float(r["Counter_Value"]))
+    return [(q, n, v) for k, (q, n, v) in sorted(acc.items())]
 
 
 def _between_markers(disp):
-    """Counter sums of the launches between role_marker pairs."""
-    out, cur = [], None
-    for _, name, v in disp:
+    """Counter sums of the launches between role_marker pairs, on the
+    marker's hardware queue (each library stream has its own)."""
+    out, cur = [], {}
+    for q, name, v in disp:
         if "role_marker" in name:
-            if cur is None:
-                cur = [0.0, []]
+            if q not in cur:
+                cur[q] = [0.0, []]
             else:
-                out.append(cur)
-                cur = None
-        elif cur is not None:
-            cur[0] += v
-            cur[1].append(name)
+                out.append(cur.pop(q))
+        elif q in cur:
+            cur[q][0] += v
+            cur[q][1].append(name)
     return out
 
 

@@ -7,11 +7,10 @@ projections, FFN, two attention products); the decoder adds the cross block
 keys/values, 4 S_mem D for its attention) and counts the causal self-attention
 at half (2 S D).  The vocabulary head adds 2 D V per token.
 Model FLOPs = 3 x forward (forward + backward); hardware FLOPs = 4 x forward,
-because re-materialisation runs every forward twice (GPipe, Section 2.3), plus,
-in bf16, the second half of the feed-forward input projection: its input rows
-carry the bf16 rounding residual of the LayerNorm output as a second operand
-(reduction 2 D), in the forward and in its recomputation, 2 x 2 D F per token
-and layer.
+because re-materialisation runs every forward twice (GPipe, Section 2.3).  Both
+count bf16 matrix work only: the fp4 correction term of the bf16 feed-forward
+input projection (2 D F per token and layer, in the forward and the recompute,
+at four times the bf16 rate) is not included.
 """
 
 
@@ -32,18 +31,10 @@ def forward_flops(cfg, batch=None) -> float:
     return float(f)
 
 
-def split_input_flops(cfg, batch=None) -> float:
-    """Extra MFMA work of the split feed-forward input (bf16 only) per step."""
-    if cfg.dtype != "bf16":
-        return 0.0
-    N = cfg.batch if batch is None else batch
-    return 2.0 * N * cfg.seq * cfg.layers * 2.0 * cfg.d_model * cfg.d_ff
-
-
 def step_flops(cfg, batch=None):
     """(model FLOPs, hardware FLOPs) of one mini-batch step."""
     f = forward_flops(cfg, batch)
-    return 3 * f, 4 * f + split_input_flops(cfg, batch)
+    return 3 * f, 4 * f
 
 
 # Linear layers of an encoder layer: name -> (in, out)

@@ -13,17 +13,17 @@
 // the row log-sum-exp for the backward pass.
 //
 // Backward (two kernels, no atomics, deterministic):
-//   dQ pass (per 32 queries, loop over key blocks):  S^T, dP^T = V dO^T,
-//     dS^T = P^T (dP^T - delta), dQ^T += K^T dS^T;  also writes
-//     delta_i = sum_d dO_id O_id.
-// delta must equal sum_j P_ij dP_ij to well below bf16 precision: the rows of
-// dS then sum to zero, and a component that all keys of a head share (it
-// grows with depth in a residual stack) drops out of dQ = dS K; likewise for
-// the common part of dK and the weight gradients built from it.  With O
-// rounded to bf16 the error of delta is amplified by that shared component
-// times the square root of the key count, several percent of dQ in a deep
-// stack.  So the forward also stores the rounding residual O - bf16(O) as a
-// second bf16 tensor, and delta is formed from their sum (about 16 more bits).
+//   dQ pass (per 32 queries, two loops over key blocks): first
+//     delta_i = sum_j P_ij dP_ij from the recomputed S^T and dP^T = V dO^T,
+//     then S^T, dP^T again, dS^T = P^T (dP^T - delta), dQ^T += K^T dS^T;
+//     writes delta for the second kernel.
+// delta is formed from the very probabilities and dP the backward uses, not
+// as dO . O: the forward's O comes from bf16-rounded probabilities (and is
+// stored in bf16), and any mismatch leaves the rows of dS summing to a
+// nonzero value.  A component that all keys (and queries) of a head share --
+// it grows with depth in a residual stack -- multiplies that sum coherently
+// over the keys in dQ = dS K and in the bias and weight gradients built from
+// dQ and dK (several percent of dQ in a 16-layer stack with delta = dO . O).
 //   dK/dV pass (per 32 keys, loop over query blocks):  S = Q K^T, dP = dO V^T,
 //     dS = P (dP - delta), dV^T += dO^T P, dK^T += Q^T dS.
 // In every product the register-held operand's accumulator layout (lane =
@@ -144,24 +144,6 @@ __device__ __forceinline__ void store_t(bf16* __restrict__ g, long ld, const f32
         }
 }
 
-// Store the bf16 rounding residual v - bf16(v) of the values store_t writes.
-__device__ __forceinline__ void store_lo_t(bf16* __restrict__ g, long ld, const f32x16* acc, float scale, int lane) {
-    bf16* row = g + (long)(lane & 31) * ld;
-#pragma unroll
-    for (int db = 0; db < 2; ++db)
-#pragma unroll
-        for (int rg = 0; rg < 4; ++rg) {
-            const int d = db * 32 + rg * 8 + (lane >> 5) * 4;
-            bf16x4 t;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float v = acc[db][rg * 4 + i] * scale;
-                t[i] = (bf16)(v - (float)(bf16)v);
-            }
-            *reinterpret_cast<bf16x4*>(row + d) = t;
-        }
-}
-
 // 2^x with the hardware transcendental (v_exp_f32); every argument here is
 // <= 0 or a finite difference of scaled scores, and a result that flushes
 // to zero below 2^-126 is irrelevant next to the row's largest term (1).
@@ -248,7 +230,6 @@ __global__ void __launch_bounds__(64 * QW) attn_fwd_mfma(AttnArgs a) {
     }
     bf16* O = reinterpret_cast<bf16*>(a.o) + ((long)b * a.Sq + q0) * a.ldo + hh * DH;
     store_t(O, a.ldo, o, 1.f / sum, lane);
-    if (a.olo) store_lo_t(reinterpret_cast<bf16*>(a.olo) + ((long)b * a.Sq + q0) * a.ldo + hh * DH, a.ldo, o, 1.f / sum, lane);
     if (a.lse && lane < 32) a.lse[(long)bh * a.Sq + q] = m * a.scale + logf(sum);
 }
 
@@ -272,30 +253,33 @@ __global__ void __launch_bounds__(64 * QW) attn_bwd_dq_mfma(AttnArgs a) {
     const long qrow = (long)b * a.Sq + q;
     const bf16* Qrow = reinterpret_cast<const bf16*>(a.q) + qrow * a.ldq + hh * DH;
     const bf16* dOrow = reinterpret_cast<const bf16*>(a.dout) + qrow * a.lddo + hh * DH;
-    const bf16* Orow = reinterpret_cast<const bf16*>(a.o) + qrow * a.ldo + hh * DH;
     bf16x8 qf[4], gf[4];
-    float dpart = 0.f;
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
         qf[s] = frag_global(Qrow, s, lane);
         gf[s] = frag_global(dOrow, s, lane);
-        const bf16x8 of = frag_global(Orow, s, lane);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) dpart += (float)gf[s][e] * (float)of[e];
     }
-    if (a.olo) {
-        const bf16* Olo = reinterpret_cast<const bf16*>(a.olo) + qrow * a.ldo + hh * DH;
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            const bf16x8 lf = frag_global(Olo, s, lane);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) dpart += (float)gf[s][e] * (float)lf[e];
-        }
-    }
-    const float delta = dpart + __shfl_xor(dpart, 32, 64);
     const float c = a.scale * LOG2E;
     const float lse2 = a.lse[(long)bh * a.Sq + q] * LOG2E;
     const int nkb = CAUSAL ? min(NKB, q0 / 32 + 1) : NKB;
+    // delta = sum_j P_ij dP_ij; lanes l and l + 32 hold the two key halves of a block
+    float dpart = 0.f;
+#pragma unroll 2
+    for (int kb = 0; kb < nkb; ++kb) {
+        f32x16 st = zero16(), dp = zero16();
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            st = mfma(frag_rows(Ks, kb * 32, s, lane), qf[s], st);
+            dp = mfma(frag_rows(Vs, kb * 32, s, lane), gf[s], dp);
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            float p = exp2_hw(fmaf(st[r], c, -lse2));
+            if (CAUSAL && kb * 32 + acc_row(r, lane) > q) p = 0.f;
+            dpart = fmaf(p, dp[r], dpart);
+        }
+    }
+    const float delta = dpart + __shfl_xor(dpart, 32, 64);
     f32x16 dq[2] = {zero16(), zero16()};
 #pragma unroll 2
     for (int kb = 0; kb < nkb; ++kb) {

@@ -36,6 +36,31 @@ __device__ __forceinline__ float wave_max(float v) {
     for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, WAVE));
     return v;
 }
+
+// ---- OCP e2m1 (fp4) with one E8M0 scale per row: the low-precision operand
+// of a GEMM correction term (see GemmArgs::a4).  The scale of a row is
+// 2^(e - 2), e = floor(log2 max|v|), so every |v| / scale < 8; values round to
+// the nearest of 0, 0.5, 1, 1.5, 2, 3, 4, 6 (ties to the even code) and
+// saturate at 6.
+__device__ __forceinline__ unsigned e8m0_for_amax(float amax) {
+    const int eb = (int)((__float_as_uint(amax) >> 23) & 255u);  // biased exponent of max|v|
+    return eb >= 2 ? (unsigned)(eb - 2) : 0u;                    // 0: the row is (nearly) zero
+}
+// 1 / scale for an E8M0 code (0 when the code is 0, which zeroes the row)
+__device__ __forceinline__ float e8m0_inv(unsigned code) {
+    return code ? __uint_as_float((254u - code) << 23) : 0.f;
+}
+__device__ __forceinline__ unsigned e2m1_code(float q) {
+    const float a = fabsf(q);
+    unsigned c = a > 0.25f ? 1u : 0u;
+    c = a >= 0.75f ? 2u : c;
+    c = a > 1.25f ? 3u : c;
+    c = a >= 1.75f ? 4u : c;
+    c = a > 2.5f ? 5u : c;
+    c = a >= 3.5f ? 6u : c;
+    c = a > 5.f ? 7u : c;
+    return c | ((q < 0.f && c) ? 8u : 0u);
+}
 __device__ __forceinline__ double wave_sum_d(double v) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, WAVE);

@@ -89,6 +89,29 @@ __device__ __forceinline__ V16<T> bload16(Rsrc r, uint32_t off) {
 // consecutive rows) and over rows 8 apart (conflict-free transposing stores,
 // where 8 lanes write rows 8 apart).
 __device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
+// fp4 rows of a stage are 32 bytes (two 16-byte chunks); swapping the chunks
+// of rows 8 .. 15 (mod 16) spreads 16 lanes reading 16 consecutive rows over
+// all banks
+__device__ __forceinline__ int sw4(int r) { return (r >> 3) & 1; }
+
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+// An empty use of registers loaded from memory: the compiler places its wait
+// for the loads here (the host pass of the build sees no body: the VGPR
+// constraint exists on the device only).
+template <int A, int B>
+__device__ __forceinline__ void pin_vgprs(int (&a)[A], int (&b)[B]) {
+#if defined(__HIP_DEVICE_COMPILE__)
+#pragma unroll
+    for (int i = 0; i < A; ++i) asm volatile("" : "+v"(a[i]));
+#pragma unroll
+    for (int j = 0; j < B; ++j) asm volatile("" : "+v"(b[j]));
+#endif
+}
+// OCP e2m1 x e2m1 (format code 4), both operands scaled per lane by E8M0 byte 0
+__device__ __forceinline__ void mma_fp4(f32x16& c, const i32x4& a, const i32x4& b, int sa, int sb) {
+    const i32x8 a8 = {a[0], a[1], a[2], a[3], 0, 0, 0, 0}, b8 = {b[0], b[1], b[2], b[3], 0, 0, 0, 0};
+    c = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, c, 4, 4, 0, sa, 0, sb);
+}
 __device__ __forceinline__ int lds_byte(int row, int kbyte) {
     return row * 128 + ((((kbyte >> 4) ^ swz(row)) << 4) | (kbyte & 15));
 }
@@ -487,7 +510,10 @@ __device__ __forceinline__ void wait_vmcnt_dyn(int n) {
     switch (n) {
     case 0: wait_vmcnt<0>(); break;
     case 4: wait_vmcnt<4>(); break;
+    case 5: wait_vmcnt<5>(); break;
     case 6: wait_vmcnt<6>(); break;
+    case 10: wait_vmcnt<10>(); break;
+    case 20: wait_vmcnt<20>(); break;
     case 8: wait_vmcnt<8>(); break;
     case 12: wait_vmcnt<12>(); break;
     case 16: wait_vmcnt<16>(); break;
@@ -506,6 +532,12 @@ template <int P>
 __device__ __forceinline__ void dl_load_blocks(Rsrc g, const uint32_t* vo, int so, char* dst) {
 #pragma unroll
     for (int i = 0; i < P; ++i) __builtin_amdgcn_raw_ptr_buffer_load_lds(g, (LdsPtr)(dst + i * 1024), 16, vo[i], so, 0, 0);
+}
+// 1 KB direct-to-LDS blocks, each from its own buffer resource
+template <int P>
+__device__ __forceinline__ void dl_load_rsrcs(const Rsrc* g, const uint32_t* vo, int so, char* dst) {
+#pragma unroll
+    for (int i = 0; i < P; ++i) __builtin_amdgcn_raw_ptr_buffer_load_lds(g[i], (LdsPtr)(dst + i * 1024), 16, vo[i], so, 0, 0);
 }
 
 // Wave index as a wave-uniform (scalar) value, so LDS base addresses derived
@@ -608,18 +640,29 @@ __device__ __forceinline__ bf16x8 tr_frag(const char* p, int second) {
 // destination) is wave-uniform; fragment offsets are precomputed and the stage
 // base folds into the ds_read immediate because the k-tile loop is unrolled
 // over the stages.
-template <int BM, int BN, int WM, int WN, int NSTAGE, int EPI, int SM, bool KM>
+//   MX: the fp4 correction term of GemmArgs (a4, b4, sa4, sb4).  Each stage
+//   also holds the k-tile's 32 bytes (64 e2m1 values) of every A and B row,
+//   loaded directly like the bf16 tiles (16-byte chunk h of row r at slot
+//   2 r + (h ^ sw4(r))); once per k-tile each output block takes one
+//   v_mfma_scale_f32_32x32x64_f8f6f4 into the same fp32 accumulator, the
+//   per-lane scale being the E8M0 byte of the lane's row (A) or column (B),
+//   which are loaded once, before the k loop.
+template <int BM, int BN, int WM, int WN, int NSTAGE, int EPI, int SM, bool KM, bool MX = false>
 __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
     // SM: 0 no split-K; 1 split-K, partial tiles only (summed by splitk_reduce)
     constexpr bool SPLIT = SM != 0;
     constexpr int BK = 64, KS = 4, NW = WM * WN;
     constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
-    constexpr int STAGE = (BM + BN) * 128;
+    constexpr int STAGE_BF = (BM + BN) * 128;
+    constexpr int STAGE = STAGE_BF + (MX ? (BM + BN) * 32 : 0);
     constexpr int PA = BM / (8 * NW), PB = BN / (8 * NW);  // 1 KB load blocks per wave for A and B
     static_assert(PA * 8 * NW == BM && PB * 8 * NW == BN, "load blocks");
     // m-contiguous tiles swizzle 16-byte chunks by 4 (k % 4): rows need >= 16 chunks
     static_assert(KM || (BM >= 128 && BN >= 128), "m-contiguous tiles must be at least 128 wide");
-    constexpr int LPW = PA + PB;               // load instructions per wave per k-tile
+    constexpr int NL4 = MX ? (BM + BN) * 2 / (64 * NW) : 0;  // 1 KB fp4 load blocks per wave
+    static_assert(!MX || (KM && NL4 * 64 * NW == (BM + BN) * 2 && (2 * BM) % 64 == 0), "fp4 load blocks");
+    static_assert(NSTAGE * STAGE <= 160 * 1024, "LDS");
+    constexpr int LPW = PA + PB + NL4;         // load instructions per wave per k-tile
     __shared__ __attribute__((aligned(1024))) char smem[NSTAGE * STAGE];
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -681,10 +724,41 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
         ka = (int)(BK * args.lda * 2);
         kb = (int)(BK * args.ldb * 2);
     }
+    // fp4 correction operands: per-lane chunk offsets, and the scales of the
+    // lane's rows (A) and columns (B), issued before the bf16 prologue so
+    // that the prologue's wait covers them
+    // (a conditional expression over buffer resources drops the kernel's host
+    // stub: the operand is chosen by pointer and size, one resource per block)
+    constexpr int NL4A = NL4 > 0 ? NL4 : 1;
+    Rsrc R4[NL4A];
+    uint32_t vo4[NL4A];
+    int sca[TM], scb[TN];
+    if constexpr (MX) {
+        const int kb4 = args.K / 2;  // bytes per fp4 row
+#pragma unroll
+        for (int p = 0; p < NL4; ++p) {
+            const int blk = wave * NL4 + p;     // 64 chunks per block, never straddling A and B
+            const int c = blk * 64 + lane;
+            const bool isa = blk * 64 < 2 * BM;
+            const int cc = isa ? c : c - 2 * BM, r = cc >> 1;
+            const int row = (isa ? m0 : n0) + r, lim = isa ? args.M : args.N;
+            R4[p] = make_rsrc(isa ? args.a4 : args.b4, (uint32_t)((long)lim * kb4));
+            vo4[p] = row < lim ? (uint32_t)((long)row * kb4 + (((cc & 1) ^ sw4(r)) << 4)) : OOB;
+        }
+        const Rsrc SA = make_rsrc(args.sa4, (uint32_t)args.M);
+        const Rsrc SB = make_rsrc(args.sb4, (uint32_t)args.N);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+            sca[i] = __builtin_amdgcn_raw_buffer_load_b8(SA, (uint32_t)(m0 + wm * (BM / WM) + i * 32 + (lane & 31)), 0, 0);
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+            scb[j] = __builtin_amdgcn_raw_buffer_load_b8(SB, (uint32_t)(n0 + wn * (BN / WN) + j * 32 + (lane & 31)), 0, 0);
+    }
 #define GP_DL_ISSUE(t, st)                                                                   \
     do {                                                                                     \
         dl_load_blocks<PA>(A, voa, (t) * ka, (st) + wave * PA * 1024);                       \
         dl_load_blocks<PB>(B, vob, (t) * kb, (st) + BM * 128 + wave * PB * 1024);            \
+        if constexpr (MX) dl_load_rsrcs<NL4>(R4, vo4, (t) * 32, (st) + STAGE_BF + wave * NL4 * 1024); \
     } while (0)
 
     f32x16 acc[TM][TN];
@@ -732,6 +806,19 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
             }
         }
     }
+    int f4a_off[TM], f4b_off[TN];
+    if constexpr (MX) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            const int r = wm * (BM / WM) + i * 32 + fr;
+            f4a_off[i] = STAGE_BF + (2 * r + (h ^ sw4(r))) * 16;
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int r = wn * (BN / WN) + j * 32 + fr;
+            f4b_off[j] = STAGE_BF + (2 * BM + 2 * r + (h ^ sw4(r))) * 16;
+        }
+    }
     Frag<bf16> fa[2][TM], fb[2][TN];
     auto load_frags = [&](int slot, const char* stg, int s) {
         if constexpr (KM) {
@@ -761,6 +848,7 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
         for (int p = 0; p < NSTAGE; ++p)
             if (p < nkt) GP_DL_ISSUE(kt0 + p, smem + p * STAGE);
         wait_vmcnt_dyn(min(NSTAGE - 1, nkt - 1) * LPW);
+        if constexpr (MX) pin_vgprs<TM, TN>(sca, scb);
         __syncthreads();
         load_frags(0, smem, 0);
         for (int i0 = 0; i0 < nkt; i0 += NSTAGE) {
@@ -793,10 +881,27 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
                         if (i + NSTAGE < nkt) GP_DL_ISSUE(kt0 + i + NSTAGE, smem + st * STAGE);
                         load_frags(cur ^ 1, nxt, 0);
                     }
+                    i32x4 a4[MX ? TM : 1], b4[MX ? TN : 1];
+                    if constexpr (MX) {
+                        if (s == 1) {
+#pragma unroll
+                            for (int ii = 0; ii < TM; ++ii) a4[ii] = *reinterpret_cast<const i32x4*>(stg + f4a_off[ii]);
+#pragma unroll
+                            for (int j = 0; j < TN; ++j) b4[j] = *reinterpret_cast<const i32x4*>(stg + f4b_off[j]);
+                        }
+                    }
 #pragma unroll
                     for (int ii = 0; ii < TM; ++ii)
 #pragma unroll
                         for (int j = 0; j < TN; ++j) mma(acc[ii][j], fa[cur][ii], fb[cur][j]);
+                    if constexpr (MX) {
+                        if (s == 1) {
+#pragma unroll
+                            for (int ii = 0; ii < TM; ++ii)
+#pragma unroll
+                                for (int j = 0; j < TN; ++j) mma_fp4(acc[ii][j], a4[ii], b4[j], sca[ii], scb[j]);
+                        }
+                    }
                 }
             }
         }
@@ -967,6 +1072,42 @@ gp_status launch_dl(const GemmArgs& a, int epi, int splits, hipStream_t st) {
     return GP_OK;
 }
 
+// The fp4-corrected forward GEMM (EPI_STORE, k-contiguous operands).
+template <int BM, int BN, int WM, int WN, int NSTAGE>
+gp_status launch_dl_mx(const GemmArgs& a, int splits, hipStream_t st) {
+    constexpr int NT = 64 * WM * WN;
+    const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+    if (splits > 1) {
+        klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_F32, 1, true, true>, dim3(tiles, splits), NT, 0, st, a);
+        GP_LAUNCH_CHECK();
+        const long nq = (long)a.M * (a.N / 4);
+        const int rg = (int)std::min<long>((nq + 255) / 256, 2048);
+        klaunch(splitk_reduce<bf16, EPI_STORE>, rg, 256, 0, st, a, splits);
+    } else {
+        klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_STORE, 0, true, true>, tiles, NT, 0, st, a);
+    }
+    GP_LAUNCH_CHECK();
+    return GP_OK;
+}
+
+// Tile shapes whose fp4 stage splits into whole 1 KB blocks per wave.
+bool mx_capable(int cfg) {
+    return cfg == T_DL128x128_S2 || cfg == T_DL128x128_S3 || cfg == T_DL256x128_S2 || cfg == T_DL256x256_S2 ||
+           cfg == T_DL256x256_W8 || cfg == T_DL128x128_W8A || cfg == T_DL128x128_W8B;
+}
+
+gp_status launch_mx(const GemmArgs& a, int cfg, int splits, hipStream_t st) {
+    switch (cfg) {
+    case T_DL128x128_S3: return launch_dl_mx<128, 128, 2, 2, 3>(a, splits, st);
+    case T_DL256x128_S2: return launch_dl_mx<256, 128, 2, 2, 2>(a, splits, st);
+    case T_DL256x256_S2: return launch_dl_mx<256, 256, 2, 2, 2>(a, splits, st);
+    case T_DL256x256_W8: return launch_dl_mx<256, 256, 2, 4, 2>(a, splits, st);
+    case T_DL128x128_W8A: return launch_dl_mx<128, 128, 2, 4, 2>(a, splits, st);
+    case T_DL128x128_W8B: return launch_dl_mx<128, 128, 4, 2, 2>(a, splits, st);
+    default: return launch_dl_mx<128, 128, 2, 2, 2>(a, splits, st);
+    }
+}
+
 template <bool AK, bool BKM>
 gp_status launch_bf16(const GemmArgs& a, int epi, int cfg, int splits, hipStream_t st) {
     if constexpr (AK == BKM) {
@@ -1037,6 +1178,10 @@ double split_weight() {
 }
 
 void choose_dl(const GemmArgs& a, int epi, bool kmaj, int& cfg, int& splits) {
+    // the fp4 correction adds one MFMA of a quarter of the bf16 time per k-tile
+    // and a quarter more tile traffic; only some shapes carry it
+    const bool mx = a.a4 != nullptr;
+    const double mx_step = mx ? 1.25 : 1.0;
     // per-step time with 1, 2 or 3 tiles sharing a CU; [k-contiguous][m-contiguous]; 0 = not available
     struct Cand { int cfg, bm, bn, resident; double step[2][3]; };
     static const Cand cands[7] = {
@@ -1054,14 +1199,14 @@ void choose_dl(const GemmArgs& a, int epi, bool kmaj, int& cfg, int& splits) {
     cfg = T_DL128x128_W8A;
     splits = 1;
     for (const Cand& c : cands) {
-        if (c.step[v][0] <= 0) continue;
+        if (c.step[v][0] <= 0 || (mx && !mx_capable(c.cfg))) continue;
         const long tiles = (long)((a.M + c.bm - 1) / c.bm) * ((a.N + c.bn - 1) / c.bn);
         for (int s = 1; s <= 8; s *= 2) {
             if (s > 1 && !split_fits(a, s, nk)) continue;
             const long per_cu = (tiles * s + NUM_CU - 1) / NUM_CU;
             const long rounds = (per_cu + c.resident - 1) / c.resident;
             const int occ = (int)std::min<long>(per_cu, c.resident);
-            double t = c0 + rounds * (double)((nk + s - 1) / s) * c.step[v][occ - 1];
+            double t = c0 + rounds * (double)((nk + s - 1) / s) * c.step[v][occ - 1] * mx_step;
             if (epi == EPI_ACC_F32) t += (kmaj ? 3.0 : 0.0) + (double)a.M * a.N * 8.0 / BW;
             if (s > 1) t += split_weight() * ((double)a.M * a.N * 4.0 * (s + 1.0) / 2.0 / BW + red0);
             if (t < best * 0.999) {
@@ -1121,6 +1266,22 @@ gp_status check_args(const GemmArgs& a, bool a_kmajor, bool b_kmajor) {
 } // namespace
 
 gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dtype, hipStream_t st) {
+    if (a.a4) {
+        if (dtype != GP_BF16 || !a_kmajor || !b_kmajor || epi != EPI_STORE || a.K % 64 || !a.b4 || !a.sa4 || !a.sb4)
+            return set_error(GP_ERR_UNSUPPORTED, "gemm: the fp4 correction needs bf16, k-contiguous operands, "
+                                                 "a stored epilogue and K % 64 == 0");
+        gp_status s = check_args<bf16>(a, true, true);
+        if (s != GP_OK) return s;
+        int cfg, splits;
+        choose_dl(a, epi, true, cfg, splits);
+        if (a.force_cfg >= 0 && a.force_cfg <= T_LAST) {
+            // a forced shape without an fp4 stage falls back to the 128 x 128 tile
+            cfg = mx_capable(a.force_cfg) ? a.force_cfg : T_DL128x128_S2;
+            splits = a.force_splits > 0 ? a.force_splits : 1;
+            if (splits > 1 && !split_fits(a, splits, a.K / 64)) splits = 1;
+        }
+        return launch_mx(a, cfg, splits, st);
+    }
     if (dtype == GP_BF16) {
         gp_status s = check_args<bf16>(a, a_kmajor, b_kmajor);
         if (s != GP_OK) return s;

@@ -32,16 +32,25 @@ struct GemmArgs {
     int force_cfg = -1;    // tile shape override (tests and tuning); -1 = heuristic
     int force_splits = 0;
     float* colsum = nullptr; // EPI_ACC_F32 with n-contiguous B: also colsum[n] (+)= sum_k B(n, k)
+    // Optional fp4 correction term (bf16, k-contiguous, EPI_STORE): the GEMM
+    // also adds sum_k a4(m, k) sa4[m] * b4(n, k) sb4[n].  a4 [M, K/2] and b4
+    // [N, K/2] hold OCP e2m1 values (element k of a row in byte k/2, low
+    // nibble first); sa4 [M] and sb4 [N] are E8M0 scales (2^(s - 127)).
+    const void* a4 = nullptr;
+    const void* b4 = nullptr;
+    const unsigned char* sa4 = nullptr;
+    const unsigned char* sb4 = nullptr;
 };
 
 gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dtype, hipStream_t st);
 
 // ------------------------------------------------------------- LayerNorm
 // out (elt) = gamma * (x - mu) * rstd + beta per row of D; stats[row] = {mu, rstd}.
-// split (bf16 only): out rows are 2 D wide, [bf16(y) | bf16(y - bf16(y))], the
-// input of a GEMM that reads the row at about 16 more bits of precision.
+// lo4 / lo_sc (optional; bf16, D % 64 == 0): the rounding residuals y - bf16(y)
+// of the row as fp4 [rows, D/2] bytes with one E8M0 scale per row, the
+// correction operand (GemmArgs::a4) of the GEMM that consumes out.
 gp_status layernorm_fwd(int dtype, const float* x, long rows, int D, const float* gamma, const float* beta,
-                        float eps, void* out, float* stats, int split, hipStream_t st);
+                        float eps, void* out, float* stats, void* lo4, unsigned char* lo_sc, hipStream_t st);
 // dx = dres + rstd (g - mean g - xh mean(g xh)), g = dn * gamma; writes dx_f32 and/or dx_elt.
 // Per-block partial sums of dn * xh and dn go to partial[blk][2][D] (added to
 // what is there when accumulate != 0); *nblk receives the block count (for
@@ -66,10 +75,6 @@ struct AttnArgs {
     const void* k = nullptr; long ldk = 0; // row (b, j) at k + (b Sk + j) ldk + h dh
     const void* v = nullptr; long ldv = 0;
     void* o = nullptr; long ldo = 0;
-    // optional (bf16): the rounding residual o - bf16(o), rounded to bf16, in
-    // o's layout; the forward writes it and the dQ pass forms delta from
-    // o + olo, so that delta matches the probabilities the backward recomputes
-    void* olo = nullptr;
     float* lse = nullptr;                  // [n, H, Sq] log-sum-exp of the scaled scores
     int causal = 0;
     float scale = 1.f;
@@ -77,7 +82,7 @@ struct AttnArgs {
     void* dq = nullptr; long lddq = 0;
     void* dk = nullptr; long lddk = 0;
     void* dv = nullptr; long lddv = 0;
-    float* delta = nullptr;                // [n, H, Sq] rowsum(dO * O) scratch
+    float* delta = nullptr;                // [n, H, Sq] rowsum(dO * O) = rowsum(P * dP) scratch
 };
 gp_status attention_fwd(int dtype, const AttnArgs& a, hipStream_t st);
 gp_status attention_bwd(int dtype, const AttnArgs& a, hipStream_t st);
@@ -106,9 +111,10 @@ int xent_partials(long rows);
 gp_status sgd_update(float* w, const float* g, float lr, long count, hipStream_t st);
 // Working copies of one linear layer from its fp32 master W [in, out]:
 // kn (elt) = W, nk (elt) = W^T.
-// kn = W [in, out]; nk = W^T [out, in], or with split [out, 2 in] holding
-// each row of W^T twice (the B operand of a GEMM whose input rows are split).
-gp_status refresh_linear(int dtype, const float* w, int in, int out, void* kn, void* nk, int split, hipStream_t st);
+// kn = W [in, out]; nk = W^T [out, in]; q4 / q4s (optional, bf16): the rows of
+// nk in fp4 [out, in/2] bytes with one E8M0 scale per row (GemmArgs::b4, sb4).
+gp_status refresh_linear(int dtype, const float* w, int in, int out, void* kn, void* nk, void* q4, void* q4s,
+                         hipStream_t st);
 // An empty launch labelled by its grid (role x (edge + 1) workgroups of one
 // wave): edge 0 before, 1 after a timed launch, so that per-dispatch profiler
 // records can be attributed to launch roles.

@@ -114,11 +114,10 @@ __global__ void __launch_bounds__(256) sgd_kernel(float* __restrict__ w, const f
     for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < count; i += (long)gridDim.x * 256) w[i] -= lr * g[i];
 }
 
-// kn = W, nk = W^T through a 64 x 64 LDS tile (both writes coalesced); with
-// split the rows of nk are 2 in wide and hold the row of W^T twice.
+// kn = W, nk = W^T through a 64 x 64 LDS tile (both writes coalesced).
 template <typename T>
 __global__ void __launch_bounds__(256) refresh_kernel(const float* __restrict__ w, int in, int out,
-                                                      T* __restrict__ kn, T* __restrict__ nk, int split) {
+                                                      T* __restrict__ kn, T* __restrict__ nk) {
     __shared__ float tile[64][65];
     const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
     const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
@@ -133,16 +132,36 @@ __global__ void __launch_bounds__(256) refresh_kernel(const float* __restrict__ 
     __syncthreads();
     for (int c = ty; c < 64; c += 4) {
         const int col = c0 + c, row = r0 + tx;
-        if (row < in && col < out) {
-            const T v = to_elt<T>(tile[tx][c]);
-            if (split) {
-                nk[(long)col * 2 * in + row] = v;
-                nk[(long)col * 2 * in + in + row] = v;
-            } else {
-                nk[(long)col * in + row] = v;
-            }
-        }
+        if (row < in && col < out) nk[(long)col * in + row] = to_elt<T>(tile[tx][c]);
     }
+}
+
+// fp4 copy of bf16 rows (the W^T working copy, rows of `in` values): one wave
+// per row; 8 values per lane step; one E8M0 scale per row (see e2m1_code).
+__global__ void __launch_bounds__(256) quant4_rows_kernel(const bf16* __restrict__ src, int rows, int in,
+                                                          unsigned char* __restrict__ q4, unsigned char* __restrict__ sc) {
+    const int lane = threadIdx.x & 63;
+    const long row = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= rows) return;
+    const bf16x8* r8 = reinterpret_cast<const bf16x8*>(src + row * in);
+    const int n8 = in / 8;
+    float amax = 0.f;
+    for (int i = lane; i < n8; i += 64) {
+        const bf16x8 v = r8[i];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf((float)v[e]));
+    }
+    const unsigned s = e8m0_for_amax(wave_max(amax));
+    const float inv = e8m0_inv(s);
+    unsigned* o4 = reinterpret_cast<unsigned*>(q4 + row * (in / 2));
+    for (int i = lane; i < n8; i += 64) {
+        const bf16x8 v = r8[i];
+        unsigned q = 0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) q |= e2m1_code((float)v[e] * inv) << (4 * e);
+        o4[i] = q;
+    }
+    if (lane == 0) sc[row] = (unsigned char)s;
 }
 
 __global__ void __launch_bounds__(256) finite_kernel(const float* __restrict__ x, long count, int* __restrict__ flag) {
@@ -215,13 +234,20 @@ gp_status sgd_update(float* w, const float* g, float lr, long count, hipStream_t
     return GP_OK;
 }
 
-gp_status refresh_linear(int dtype, const float* w, int in, int out, void* kn, void* nk, int split, hipStream_t st) {
+gp_status refresh_linear(int dtype, const float* w, int in, int out, void* kn, void* nk, void* q4, void* q4s,
+                         hipStream_t st) {
     dim3 grid((out + 63) / 64, (in + 63) / 64);
     if (dtype == GP_BF16)
-        klaunch(refresh_kernel<bf16>, grid, 256, 0, st, w, in, out, reinterpret_cast<bf16*>(kn), reinterpret_cast<bf16*>(nk), split);
+        klaunch(refresh_kernel<bf16>, grid, 256, 0, st, w, in, out, reinterpret_cast<bf16*>(kn), reinterpret_cast<bf16*>(nk));
     else
-        klaunch(refresh_kernel<float>, grid, 256, 0, st, w, in, out, reinterpret_cast<float*>(kn), reinterpret_cast<float*>(nk), split);
+        klaunch(refresh_kernel<float>, grid, 256, 0, st, w, in, out, reinterpret_cast<float*>(kn), reinterpret_cast<float*>(nk));
     GP_LAUNCH_CHECK();
+    if (q4) {
+        if (dtype != GP_BF16 || in % 8) return set_error(GP_ERR_UNSUPPORTED, "refresh: fp4 copies are made from bf16 rows");
+        klaunch(quant4_rows_kernel, (out + 3) / 4, 256, 0, st, reinterpret_cast<const bf16*>(nk), out, in,
+                static_cast<unsigned char*>(q4), static_cast<unsigned char*>(q4s));
+        GP_LAUNCH_CHECK();
+    }
     return GP_OK;
 }
 

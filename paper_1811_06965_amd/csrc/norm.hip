@@ -1,8 +1,9 @@
 // norm.hip -- LayerNorm forward/backward and deterministic column reductions.
 //
 // LayerNorm over the feature dimension D of each token row (biased variance,
-// eps inside the square root).  A split output row holds 2 D elements: the
-// bf16 values, then their rounding residuals (see layernorm_fwd).  One wave owns one row; lane l holds features
+// eps inside the square root).  Optionally the forward also writes the bf16
+// rounding residuals of its output in fp4 with one scale per row (see
+// layernorm_fwd).  One wave owns one row; lane l holds features
 // l, l + 64, ... so every global access is a coalesced 256-byte row segment.
 // Parameter gradients are reduced in two deterministic stages: per-block
 // partial sums, then a fixed-order column sum (no atomics), so re-running a
@@ -20,7 +21,8 @@ template <typename T, int C>
 __global__ void __launch_bounds__(256) ln_fwd_kernel(const float* __restrict__ x, long rows, int D,
                                                      const float* __restrict__ gamma,
                                                      const float* __restrict__ beta, float eps,
-                                                     T* __restrict__ out, float* __restrict__ stats, int split) {
+                                                     T* __restrict__ out, float* __restrict__ stats,
+                                                     unsigned char* __restrict__ lo4, unsigned char* __restrict__ lo_sc) {
     const int lane = threadIdx.x & 63;
     const long row = (long)blockIdx.x * LN_WAVES + (threadIdx.x >> 6);
     if (row >= rows) return;
@@ -42,16 +44,34 @@ __global__ void __launch_bounds__(256) ln_fwd_kernel(const float* __restrict__ x
         q += t * t;
     }
     const float rstd = 1.f / sqrtf(wave_sum(q) / D + eps);
-    T* orow = out + row * (split ? 2 * D : D);
+    T* orow = out + row * D;
+    float lo[C];
+    float amax = 0.f;
 #pragma unroll
     for (int c = 0; c < C; ++c) {
         const int d = lane + c * 64;
+        lo[c] = 0.f;
         if (d < D) {
             const float y = gamma[d] * ((v[c] - mu) * rstd) + beta[d];
             const T hi = to_elt<T>(y);
             orow[d] = hi;
-            if (split) orow[D + d] = to_elt<T>(y - (float)hi);
+            lo[c] = y - (float)hi;
+            amax = fmaxf(amax, fabsf(lo[c]));
         }
+    }
+    if (lo4) {
+        // fp4 rounding residuals (D % 64 == 0): features d, d + 1 of lanes 2k, 2k + 1 share a byte
+        const unsigned sc = e8m0_for_amax(wave_max(amax));
+        const float inv = e8m0_inv(sc);
+        unsigned char* lrow = lo4 + row * (D / 2);
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const unsigned q = e2m1_code(lo[c] * inv);
+            const unsigned nb = (unsigned)__shfl_xor((int)q, 1, 64);
+            const int d = lane + c * 64;
+            if (!(lane & 1) && d < D) lrow[d / 2] = (unsigned char)(q | (nb << 4));
+        }
+        if (lane == 0) lo_sc[row] = (unsigned char)sc;
     }
     if (stats && lane == 0) {
         stats[2 * row] = mu;
@@ -152,19 +172,19 @@ __global__ void __launch_bounds__(1024) colsum_kernel(const float* __restrict__ 
 template <typename T> struct Out4;
 template <> struct Out4<float> {
     static __device__ __forceinline__ void store(float* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
-    static __device__ __forceinline__ void store_lo(float*, f32x4) {}  // fp32 rows are never split
+    static __device__ __forceinline__ f32x4 residual(f32x4) { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 };
 template <> struct Out4<bf16> {
     static __device__ __forceinline__ void store(bf16* p, f32x4 v) {
         bf16x4 b = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
         *reinterpret_cast<bf16x4*>(p) = b;
     }
-    // the rounding residual v - bf16(v), rounded to bf16
-    static __device__ __forceinline__ void store_lo(bf16* p, f32x4 v) {
-        bf16x4 b;
+    // the rounding residual v - bf16(v)
+    static __device__ __forceinline__ f32x4 residual(f32x4 v) {
+        f32x4 r;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) b[i] = (bf16)(v[i] - (float)(bf16)v[i]);
-        *reinterpret_cast<bf16x4*>(p) = b;
+        for (int i = 0; i < 4; ++i) r[i] = v[i] - (float)(bf16)v[i];
+        return r;
     }
 };
 
@@ -174,7 +194,7 @@ template <typename T, int C4>
 __global__ void __launch_bounds__(256) ln_fwd_v4(const float* __restrict__ x, long rows, int D,
                                                  const float* __restrict__ gamma, const float* __restrict__ beta,
                                                  float eps, T* __restrict__ out, float* __restrict__ stats,
-                                                 int split) {
+                                                 unsigned char* __restrict__ lo4, unsigned char* __restrict__ lo_sc) {
     const int lane = threadIdx.x & 63;
     const long row = (long)blockIdx.x * LN_WAVES + (threadIdx.x >> 6);
     if (row >= rows) return;
@@ -196,13 +216,29 @@ __global__ void __launch_bounds__(256) ln_fwd_v4(const float* __restrict__ x, lo
     const float rstd = 1.f / sqrtf(wave_sum(q) / D + eps);
     const f32x4* g4 = reinterpret_cast<const f32x4*>(gamma);
     const f32x4* b4 = reinterpret_cast<const f32x4*>(beta);
-    T* orow = out + row * (split ? 2 * D : D);
+    T* orow = out + row * D;
+    f32x4 lo[C4];
+    float amax = 0.f;
 #pragma unroll
     for (int c = 0; c < C4; ++c) {
         const int i = lane + 64 * c;
         const f32x4 y = g4[i] * ((v[c] - mu) * rstd) + b4[i];
         Out4<T>::store(orow + 4 * i, y);
-        if (split) Out4<T>::store_lo(orow + D + 4 * i, y);
+        lo[c] = Out4<T>::residual(y);
+        amax = fmaxf(amax, fmaxf(fmaxf(fabsf(lo[c][0]), fabsf(lo[c][1])), fmaxf(fabsf(lo[c][2]), fabsf(lo[c][3]))));
+    }
+    if (lo4) {
+        // fp4 rounding residuals: the lane's 4 consecutive features fill 2 bytes
+        const unsigned sc = e8m0_for_amax(wave_max(amax));
+        const float inv = e8m0_inv(sc);
+        unsigned short* lrow = reinterpret_cast<unsigned short*>(lo4 + row * (D / 2));
+#pragma unroll
+        for (int c = 0; c < C4; ++c) {
+            const unsigned q = e2m1_code(lo[c][0] * inv) | (e2m1_code(lo[c][1] * inv) << 4) |
+                               (e2m1_code(lo[c][2] * inv) << 8) | (e2m1_code(lo[c][3] * inv) << 12);
+            lrow[lane + 64 * c] = (unsigned short)q;
+        }
+        if (lane == 0) lo_sc[row] = (unsigned char)sc;
     }
     if (stats && lane == 0) {
         stats[2 * row] = mu;
@@ -288,30 +324,30 @@ __global__ void __launch_bounds__(256) bias_partial_kernel(const T* __restrict__
 
 template <typename T>
 gp_status ln_fwd_t(const float* x, long rows, int D, const float* g, const float* b, float eps, void* out,
-                   float* stats, int split, hipStream_t st) {
+                   float* stats, unsigned char* lo4, unsigned char* lo_sc, hipStream_t st) {
     const int grid = (int)((rows + LN_WAVES - 1) / LN_WAVES);
     T* o = reinterpret_cast<T*>(out);
     if (D % 256 == 0 && D <= 2048) {
         switch (D / 256) {
-        case 1: klaunch(ln_fwd_v4<T, 1>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split); break;
-        case 2: klaunch(ln_fwd_v4<T, 2>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split); break;
-        case 3: klaunch(ln_fwd_v4<T, 3>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split); break;
-        case 4: klaunch(ln_fwd_v4<T, 4>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split); break;
-        case 5: klaunch(ln_fwd_v4<T, 5>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split); break;
-        case 6: klaunch(ln_fwd_v4<T, 6>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split); break;
-        case 7: klaunch(ln_fwd_v4<T, 7>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split); break;
-        default: klaunch(ln_fwd_v4<T, 8>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split); break;
+        case 1: klaunch(ln_fwd_v4<T, 1>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc); break;
+        case 2: klaunch(ln_fwd_v4<T, 2>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc); break;
+        case 3: klaunch(ln_fwd_v4<T, 3>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc); break;
+        case 4: klaunch(ln_fwd_v4<T, 4>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc); break;
+        case 5: klaunch(ln_fwd_v4<T, 5>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc); break;
+        case 6: klaunch(ln_fwd_v4<T, 6>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc); break;
+        case 7: klaunch(ln_fwd_v4<T, 7>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc); break;
+        default: klaunch(ln_fwd_v4<T, 8>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc); break;
         }
         GP_LAUNCH_CHECK();
         return GP_OK;
     }
     const int C = (D + 63) / 64;
-    if (C <= 1) klaunch(ln_fwd_kernel<T, 1>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split);
-    else if (C <= 2) klaunch(ln_fwd_kernel<T, 2>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split);
-    else if (C <= 4) klaunch(ln_fwd_kernel<T, 4>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split);
-    else if (C <= 8) klaunch(ln_fwd_kernel<T, 8>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split);
-    else if (C <= 16) klaunch(ln_fwd_kernel<T, 16>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split);
-    else if (C <= 32) klaunch(ln_fwd_kernel<T, 32>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, split);
+    if (C <= 1) klaunch(ln_fwd_kernel<T, 1>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc);
+    else if (C <= 2) klaunch(ln_fwd_kernel<T, 2>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc);
+    else if (C <= 4) klaunch(ln_fwd_kernel<T, 4>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc);
+    else if (C <= 8) klaunch(ln_fwd_kernel<T, 8>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc);
+    else if (C <= 16) klaunch(ln_fwd_kernel<T, 16>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc);
+    else if (C <= 32) klaunch(ln_fwd_kernel<T, 32>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc);
     else return set_error(GP_ERR_UNSUPPORTED, "layernorm: d_model > 2048");
     GP_LAUNCH_CHECK();
     return GP_OK;
@@ -364,10 +400,12 @@ int layernorm_bwd_blocks(long rows) {
 int bias_grad_blocks(long rows) { return rows < BIAS_BLOCKS ? (int)(rows > 0 ? rows : 1) : BIAS_BLOCKS; }
 
 gp_status layernorm_fwd(int dtype, const float* x, long rows, int D, const float* gamma, const float* beta,
-                        float eps, void* out, float* stats, int split, hipStream_t st) {
-    if (dtype == GP_BF16) return ln_fwd_t<bf16>(x, rows, D, gamma, beta, eps, out, stats, split, st);
-    if (split) return set_error(GP_ERR_UNSUPPORTED, "layernorm: split output is for bf16 partitions");
-    return ln_fwd_t<float>(x, rows, D, gamma, beta, eps, out, stats, 0, st);
+                        float eps, void* out, float* stats, void* lo4, unsigned char* lo_sc, hipStream_t st) {
+    unsigned char* l4 = static_cast<unsigned char*>(lo4);
+    if (l4 && (dtype != GP_BF16 || D % 64 || !lo_sc))
+        return set_error(GP_ERR_UNSUPPORTED, "layernorm: fp4 residuals need bf16 output and d_model % 64 == 0");
+    if (dtype == GP_BF16) return ln_fwd_t<bf16>(x, rows, D, gamma, beta, eps, out, stats, l4, lo_sc, st);
+    return ln_fwd_t<float>(x, rows, D, gamma, beta, eps, out, stats, nullptr, nullptr, st);
 }
 
 gp_status layernorm_bwd(int dtype, const float* dn, const float* x, const float* stats, const float* gamma,

@@ -70,9 +70,9 @@ struct LayerWs {
     void *u = nullptr, *qkv = nullptr, *c = nullptr;
     float *stc = nullptr, *xlse = nullptr, *x2 = nullptr;
     void *uc = nullptr, *xq = nullptr, *xkv = nullptr, *xc = nullptr;
-    void *clo = nullptr, *xclo = nullptr;  // bf16 rounding residuals of c and xc (recompute only)
     float* stf = nullptr;
     void *v = nullptr, *a = nullptr;
+    unsigned char *v4 = nullptr, *v4s = nullptr;  // fp4 rounding residuals of v and their row scales (bf16)
 };
 
 constexpr int ELT_RING = 10;      // bf16 residual-gradient buffers (see layer_backward)
@@ -213,7 +213,6 @@ void plan_workspace(gp_partition* p, Arena& a) {
             l.u = a.take_elt(T * D, e);
             l.qkv = a.take_elt(T * 3 * D, e);
             l.c = a.take_elt(T * D, e);
-            if (p->g.dtype == GP_BF16) l.clo = a.take_elt(T * D, e);
             l.lse = a.take<float>(lse_n);
             l.x1 = a.take<float>(T * D);
             if (dec) {
@@ -222,12 +221,15 @@ void plan_workspace(gp_partition* p, Arena& a) {
                 l.xq = a.take_elt(T * D, e);
                 l.xkv = a.take_elt(Tm * 2 * D, e);
                 l.xc = a.take_elt(T * D, e);
-                if (p->g.dtype == GP_BF16) l.xclo = a.take_elt(T * D, e);
                 l.xlse = a.take<float>(lse_n);
                 l.x2 = a.take<float>(T * D);
             }
             l.stf = a.take<float>(2 * T);
-            l.v = a.take_elt(T * D * (p->g.dtype == GP_BF16 ? 2 : 1), e);  // split rows (see Linear::split)
+            l.v = a.take_elt(T * D, e);
+            if (p->g.dtype == GP_BF16) {  // see Linear::split
+                l.v4 = a.take<unsigned char>(T * D / 2);
+                l.v4s = a.take<unsigned char>(T);
+            }
             l.a = a.take_elt(T * F, e);
         }
     }
@@ -363,23 +365,30 @@ gp_status timed_attention(const Ctx& c, int role, const AttnArgs& a, bool bwd) {
 }
 
 gp_status timed_ln_fwd(const Ctx& c, const float* x, long rows, int D, const float* gamma, const float* beta,
-                       float eps, void* out, float* stats, int split = 0) {
-    const double by = (double)rows * D * (4.0 + c.p->esz * (split ? 2 : 1)) + rows * 8.0 + D * 8.0;
+                       float eps, void* out, float* stats, unsigned char* lo4 = nullptr, unsigned char* lo_sc = nullptr) {
+    const double by = (double)rows * D * (4.0 + c.p->esz + (lo4 ? 0.5 : 0.0)) + rows * 8.0 + D * 8.0;
     return timed(c, GP_K_LN_FWD, 0.0, by,
-                 [&] { return layernorm_fwd(c.dt, x, rows, D, gamma, beta, eps, out, stats, split, c.st); });
+                 [&] { return layernorm_fwd(c.dt, x, rows, D, gamma, beta, eps, out, stats, lo4, lo_sc, c.st); });
 }
 
 // Y = A W + b with an epilogue; A [M, K] k-contiguous, W^T working copy [N, K].
+// A4 / A4s: fp4 rounding residuals of A and their row scales (split layers).
 gp_status linear_fwd(const Ctx& c, const Linear& L, const void* A, long M, void* C, long ldc, int epi, int relu,
-                     const float* res, void* C2) {
+                     const float* res, void* C2, const unsigned char* A4 = nullptr, const unsigned char* A4s = nullptr) {
     GemmArgs g;
     g.M = (int)M;
     g.N = L.out;
-    g.K = L.split ? 2 * L.in : L.in;
+    g.K = L.in;
     g.A = A;
-    g.lda = g.K;
+    g.lda = L.in;
     g.B = c.p->W(L.nk);
-    g.ldb = g.K;
+    g.ldb = L.in;
+    if (L.split) {
+        g.a4 = A4;
+        g.sa4 = A4s;
+        g.b4 = c.p->W(L.q4);
+        g.sb4 = static_cast<const unsigned char*>(c.p->W(L.q4s));
+    }
     g.C = C;
     g.ldc = ldc;
     g.C2 = C2;
@@ -425,7 +434,7 @@ gp_status linear_dw(const Ctx& c, const Linear& L, const void* X, const void* dY
     g.N = L.out;
     g.K = (int)rows;
     g.A = X;
-    g.lda = L.split ? 2 * L.in : L.in;  // split rows: the bf16 half
+    g.lda = L.in;
     g.B = dY;
     g.ldb = L.out;
     g.C = c.p->grads + L.w;
@@ -481,10 +490,9 @@ AttnArgs attn_args(const gp_partition* p, int Sk, int causal) {
 
 // One layer's forward.  `ws` holds its intermediates, x_in/x_out the residual
 // stream; mem is the decoder memory (elt [Tm, D]); y_out (optional) receives
-// the output rounded to the partition dtype.  keep: a recompute for the
-// backward, which also stores the attention outputs' rounding residuals.
+// the output rounded to the partition dtype.
 gp_status layer_forward(const Ctx& c, int l, LayerWs& w, const float* x_in, float* x_out, const void* mem,
-                        void* y_out, bool keep) {
+                        void* y_out) {
     gp_partition* p = c.p;
     const LayerPlan& P = p->plan.layers[l];
     const long T = p->g.T(), D = p->d.D;
@@ -501,8 +509,7 @@ gp_status layer_forward(const Ctx& c, int l, LayerWs& w, const float* x_in, floa
     a.o = w.c;
     a.ldo = D;
     a.lse = w.lse;
-    a.olo = keep ? w.clo : nullptr;
-    GP_TRY(timed_attention(c, GP_K_ATTN_FWD, a, false));
+GP_TRY(timed_attention(c, GP_K_ATTN_FWD, a, false));
     GP_TRY(linear_fwd(c, P.o, w.c, T, w.x1, D, EPI_RES_F32, 0, x_in, nullptr));
     const float* xf = w.x1;
     if (dec) {
@@ -519,15 +526,16 @@ gp_status layer_forward(const Ctx& c, int l, LayerWs& w, const float* x_in, floa
         x.o = w.xc;
         x.ldo = D;
         x.lse = w.xlse;
-        x.olo = keep ? w.xclo : nullptr;
         GP_TRY(timed_attention(c, GP_K_XATTN_FWD, x, false));
         GP_TRY(linear_fwd(c, P.xo, w.xc, T, w.x2, D, EPI_RES_F32, 0, w.x1, nullptr));
         xf = w.x2;
     }
     // feed-forward block
     const Norm& nf = dec ? P.ln3 : P.ln2;
-    GP_TRY(timed_ln_fwd(c, xf, T, (int)D, p->master + nf.g, p->master + nf.b, eps, w.v, w.stf, P.ffn1.split));
-    GP_TRY(linear_fwd(c, P.ffn1, w.v, T, w.a, p->d.F, EPI_STORE, 1, nullptr, nullptr));
+    const bool s4 = P.ffn1.split;
+    GP_TRY(timed_ln_fwd(c, xf, T, (int)D, p->master + nf.g, p->master + nf.b, eps, w.v, w.stf, s4 ? w.v4 : nullptr,
+                        s4 ? w.v4s : nullptr));
+    GP_TRY(linear_fwd(c, P.ffn1, w.v, T, w.a, p->d.F, EPI_STORE, 1, nullptr, nullptr, w.v4, w.v4s));
     GP_TRY(linear_fwd(c, P.ffn2, w.a, T, x_out, D, EPI_RES_F32, 0, xf, y_out));
     return GP_OK;
 }
@@ -551,7 +559,7 @@ gp_status partition_forward(const Ctx& c, int m, bool keep, const void* x, const
         LayerWs& w = keep ? p->lw[set][l] : p->lw[set][0];
         const float* xi = keep ? xs[l] : xs[l & 1];
         float* xo = keep ? xs[l + 1] : xs[(l + 1) & 1];
-        GP_TRY(layer_forward(c, l, w, xi, xo, mem_m, (!keep && l == L - 1) ? y : nullptr, keep));
+        GP_TRY(layer_forward(c, l, w, xi, xo, mem_m, (!keep && l == L - 1) ? y : nullptr));
     }
     return GP_OK;
 }
@@ -619,7 +627,6 @@ gp_status layer_backward(const Ctx& c, int set, int l, bool first, float* in32, 
         x.dk = b.dxkv[par];
         x.dv = p->off_elt(b.dxkv[par], D);
         x.lddk = x.lddv = 2 * D;
-        x.olo = w.xclo;
         x.delta = b.delta;
         GP_TRY(timed_attention(c, GP_K_XATTN_BWD, x, true));
         jobs.push_back({&P.xq, w.uc, b.dxq[par], T});
@@ -651,7 +658,6 @@ gp_status layer_backward(const Ctx& c, int set, int l, bool first, float* in32, 
     a.dk = p->off_elt(b.dqkv[par], D);
     a.dv = p->off_elt(b.dqkv[par], 2 * D);
     a.lddq = a.lddk = a.lddv = 3 * D;
-    a.olo = w.clo;
     a.delta = b.delta;
     GP_TRY(timed_attention(c, GP_K_ATTN_BWD, a, true));
     jobs.push_back({&P.qkv, w.u, b.dqkv[par], T});
@@ -693,7 +699,8 @@ gp_status upload_param_block(gp_partition* p, const ParamRef& r, const float* ho
                        hipMemcpyHostToDevice));
     if (r.lin) {
         GP_TRY(refresh_linear(p->g.dtype, p->master + r.lin->w, r.lin->in, r.lin->out, p->W(r.lin->kn),
-                              p->W(r.lin->nk), r.lin->split, nullptr));
+                              p->W(r.lin->nk), r.lin->split ? p->W(r.lin->q4) : nullptr,
+                              r.lin->split ? p->W(r.lin->q4s) : nullptr, nullptr));
         GP_HIP(hipDeviceSynchronize());
     }
     return GP_OK;
@@ -781,6 +788,7 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
     p->nsets = (p->remat_ahead && g.M >= 2) ? 2 : 1;
     if (const char* e = std::getenv("GP_GEMM_TILE")) p->gemm_tile = std::atoi(e);
     if (const char* e = std::getenv("GP_GEMM_SPLITS")) p->gemm_splits = std::atoi(e);
+    if (const char* e = std::getenv("GP_FFN_FP4")) g.ffn_fp4 = std::atoi(e) != 0;
     p->plan = plan_params(p->d, g);
     Arena measure;
     plan_workspace(p, measure);
@@ -820,7 +828,8 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
         return hip_fail(e, __FILE__, __LINE__);
     }
     for (const Linear* l : p->plan.linears()) {
-        s = refresh_linear(g.dtype, p->master + l->w, l->in, l->out, p->W(l->kn), p->W(l->nk), l->split, nullptr);
+        s = refresh_linear(g.dtype, p->master + l->w, l->in, l->out, p->W(l->kn), p->W(l->nk),
+                           l->split ? p->W(l->q4) : nullptr, l->split ? p->W(l->q4s) : nullptr, nullptr);
         if (s != GP_OK) {
             free_all(p);
             return s;
@@ -1082,7 +1091,8 @@ gp_status gp_accumulate_and_step(gp_partition* p, float lr, double* loss_out, gp
     }
     GP_TRY(sgd_update(p->master, p->grads, lr, (long)p->plan.n32, st));
     for (const Linear* l : p->plan.linears())
-        GP_TRY(refresh_linear(dt, p->master + l->w, l->in, l->out, p->W(l->kn), p->W(l->nk), l->split, st));
+        GP_TRY(refresh_linear(dt, p->master + l->w, l->in, l->out, p->W(l->kn), p->W(l->nk),
+                              l->split ? p->W(l->q4) : nullptr, l->split ? p->W(l->q4s) : nullptr, st));
     if (loss_out) {
         double v = 0.0;
         if (p->g.loss != GP_LOSS_NONE)

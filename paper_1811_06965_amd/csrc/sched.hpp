@@ -29,6 +29,7 @@ struct Geometry {
     int dtype = GP_BF16, kind = GP_ENCODER, Smem = 0, loss = GP_LOSS_NONE, V = 0;
     float ls = 0.f, eps = 1e-5f;
     int check_finite = 0;
+    int ffn_fp4 = 1;  // bf16: fp4 correction of the feed-forward input projection (see Linear::split)
     long long T() const { return (long long)n * S; }     // token rows of one micro-batch
     long long Tm() const { return (long long)n * Smem; } // memory rows of one micro-batch
 };
@@ -92,12 +93,13 @@ inline gp_status check_config(const Dims& d, const gp_config& c, std::string& ms
 struct Linear {
     size_t w = 0, b = 0;        // float offsets of W and bias in master/grad
     size_t kn = 0, nk = 0;      // element offsets of the working copies
+    size_t q4 = 0, q4s = 0;     // split: element offsets of the fp4 copy of W^T and its row scales
     int in = 0, out = 0;
     int role = 0;               // gp_kernel_role of its forward GEMM; +1 input gradient, +2 weight gradient
-    // bf16 feed-forward input projection: the forward reads its input rows as
-    // [bf16(y) | bf16(y - bf16(y))] against nk = [W^T | W^T] (reduction 2 in),
+    // bf16 feed-forward input projection: the forward adds the product of the
+    // LayerNorm output's bf16 rounding residuals (fp4) with an fp4 copy of W,
     // so that the pre-activations, whose signs set the ReLU mask the backward
-    // uses, carry no rounding error from the LayerNorm output
+    // uses, carry almost none of the rounding error of its bf16 input
     bool split = false;
     bool present = false;
 };
@@ -155,7 +157,13 @@ inline ParamPlan plan_params(const Dims& d, const Geometry& g) {
         f = align_up(x.b + out, 64); // keep every block 256-byte aligned
         x.kn = e;
         x.nk = e + (size_t)in * out;
-        e = align_up(x.nk + (size_t)in * out * (split ? 2 : 1), 128);
+        e = align_up(x.nk + (size_t)in * out, 128);
+        if (split) {  // bf16 elements: in / 2 bytes = in / 4 elements per row, one byte of scale per row
+            x.q4 = e;
+            e = align_up(x.q4 + (size_t)out * in / 4, 128);
+            x.q4s = e;
+            e = align_up(x.q4s + ((size_t)out + 1) / 2, 128);
+        }
         p.count += (size_t)in * out + out;
     };
     int nnorm = 0;
@@ -175,7 +183,7 @@ inline ParamPlan plan_params(const Dims& d, const Geometry& g) {
         lin(l.qkv, d.D, 3 * d.D, GP_K_QKV_FWD);
         lin(l.o, d.D, d.D, GP_K_O_FWD);
         norm(l.ln2, d.D);
-        lin(l.ffn1, d.D, d.F, GP_K_FFN1_FWD, g.dtype == GP_BF16);
+        lin(l.ffn1, d.D, d.F, GP_K_FFN1_FWD, g.dtype == GP_BF16 && g.ffn_fp4);
         lin(l.ffn2, d.F, d.D, GP_K_FFN2_FWD);
         if (dec) {
             lin(l.xq, d.D, d.D, GP_K_XQ_FWD);

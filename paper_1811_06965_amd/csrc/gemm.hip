@@ -524,6 +524,15 @@ __device__ __forceinline__ void wait_vmcnt_dyn(int n) {
     }
 }
 
+// All waves of the workgroup meet once every LDS read of this wave has
+// returned.  No memory fence: a fence would also wait for every outstanding
+// direct-to-LDS load of the wave (vmcnt(0)) and so drain the prefetch ring;
+// the loads a k-tile needs are waited for explicitly (wait_vmcnt) before.
+// The memory clobber keeps the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 typedef __attribute__((address_space(3))) void* LdsPtr;
 
 // P direct loads of 8 rows (1 KB) each into consecutive LDS blocks at dst;
@@ -847,9 +856,12 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
 #pragma unroll
         for (int p = 0; p < NSTAGE; ++p)
             if (p < nkt) GP_DL_ISSUE(kt0 + p, smem + p * STAGE);
-        wait_vmcnt_dyn(min(NSTAGE - 1, nkt - 1) * LPW);
+        if (nkt >= NSTAGE)
+            wait_vmcnt<(NSTAGE - 1) * LPW>();
+        else
+            wait_vmcnt<0>();
         if constexpr (MX) pin_vgprs<TM, TN>(sca, scb);
-        __syncthreads();
+        lds_barrier();
         load_frags(0, smem, 0);
         for (int i0 = 0; i0 < nkt; i0 += NSTAGE) {
 #pragma unroll
@@ -873,11 +885,15 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
                         load_frags(cur ^ 1, stg, s + 1);
                     } else {
                         // Tiles issued: 0 .. min(i + NSTAGE - 1, nkt - 1).  Tile i+1 must have
-                        // landed (tiles i+2 .. i+NSTAGE-1 may be in flight); then every wave is
-                        // past tile i, whose stage is refilled with tile i + NSTAGE.  Branch-free
-                        // around the LDS reads; on the last tile the fragment read is unused.
-                        wait_vmcnt_dyn(i + 1 < nkt ? min(NSTAGE - 2, nkt - 2 - i) * LPW : 0);
-                        __syncthreads();
+                        // landed (tiles i+2 .. i+NSTAGE-1 may be in flight; near the end of
+                        // the ring everything is waited for); then every wave is past tile i,
+                        // whose stage is refilled with tile i + NSTAGE.  Branch-free around
+                        // the LDS reads; on the last tile the fragment read is unused.
+                        if (i + NSTAGE - 1 < nkt)
+                            wait_vmcnt<(NSTAGE - 2) * LPW>();
+                        else
+                            wait_vmcnt<0>();
+                        lds_barrier();
                         if (i + NSTAGE < nkt) GP_DL_ISSUE(kt0 + i + NSTAGE, smem + st * STAGE);
                         load_frags(cur ^ 1, nxt, 0);
                     }
@@ -890,6 +906,11 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
                             for (int j = 0; j < TN; ++j) b4[j] = *reinterpret_cast<const i32x4*>(stg + f4b_off[j]);
                         }
                     }
+                    // The next k-step's fragment reads stay ahead of this
+                    // k-step's MFMAs (left to itself the scheduler sinks them
+                    // below the MFMAs into the same registers, which exposes
+                    // the LDS latency once per k-step).
+                    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                     for (int ii = 0; ii < TM; ++ii)
 #pragma unroll
@@ -989,14 +1010,112 @@ __global__ void __launch_bounds__(256) splitk_reduce(GemmArgs args, int splits) 
     }
 }
 
+// The same reduction with 16-byte accesses throughout (every leading
+// dimension a multiple of 4 and every base 16-byte aligned, which the host
+// checks): thread t of a block owns columns 4 t .. 4 t + 3 of a 1024-column
+// chunk (blockIdx.x) over `rows` consecutive rows (blockIdx.y), so no index
+// division is needed and each row of partials is read as whole 4 KB runs.
+template <int EPI>
+__global__ void __launch_bounds__(256) splitk_reduce_v4(GemmArgs args, int splits, int rows) {
+    const int col = blockIdx.x * 1024 + threadIdx.x * 4;
+    if (col >= args.N) return;
+    const long plane = (long)args.M * args.N;
+    if constexpr (EPI == EPI_ACC_F32) {
+        if (args.colsum && blockIdx.y == 0) {
+            const float* p = args.ws + (long)splits * plane + col;
+            f32x4 v = *reinterpret_cast<const f32x4*>(p);
+            for (int k = 1; k < splits; ++k) v += *reinterpret_cast<const f32x4*>(p + (long)k * args.N);
+            f32x4* o = reinterpret_cast<f32x4*>(args.colsum + col);
+            if (args.accumulate) v += *o;
+            *o = v;
+        }
+    }
+    f32x4 bv = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (EPI == EPI_STORE || EPI == EPI_RES_F32)
+        if (args.bias) bv = *reinterpret_cast<const f32x4*>(args.bias + col);
+    const int r0 = blockIdx.y * rows, r1 = min(args.M, r0 + rows);
+    for (int row = r0; row < r1; ++row) {
+        const float* p = args.ws + (long)row * args.N + col;
+        f32x4 s = *reinterpret_cast<const f32x4*>(p);
+        for (int k = 1; k < splits; ++k) s += *reinterpret_cast<const f32x4*>(p + (long)k * plane);
+        const long i = (long)row * args.ldc + col;
+        if constexpr (EPI == EPI_STORE) {
+            s += bv;
+            if (args.relu)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) s[j] = fmaxf(s[j], 0.f);
+            *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(args.C) + i) = {(bf16)s[0], (bf16)s[1], (bf16)s[2], (bf16)s[3]};
+        } else if constexpr (EPI == EPI_RES_F32) {
+            s += *reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(args.aux) + (long)row * args.ldaux + col) + bv;
+            *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(args.C) + i) = s;
+            if (args.C2)
+                *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(args.C2) + (long)row * args.ldc2 + col) =
+                    {(bf16)s[0], (bf16)s[1], (bf16)s[2], (bf16)s[3]};
+        } else if constexpr (EPI == EPI_F32) {
+            *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(args.C) + i) = s;
+        } else if constexpr (EPI == EPI_RELU_MASK) {
+            const bf16x4 z = *reinterpret_cast<const bf16x4*>(reinterpret_cast<const bf16*>(args.aux) + (long)row * args.ldaux + col);
+            *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(args.C) + i) = {
+                (bf16)((float)z[0] > 0.f ? s[0] : 0.f), (bf16)((float)z[1] > 0.f ? s[1] : 0.f),
+                (bf16)((float)z[2] > 0.f ? s[2] : 0.f), (bf16)((float)z[3] > 0.f ? s[3] : 0.f)};
+        } else if constexpr (EPI == EPI_ACC_F32) {
+            f32x4* c = reinterpret_cast<f32x4*>(reinterpret_cast<float*>(args.C) + i);
+            if (args.accumulate) s += *c;
+            *c = s;
+        }
+    }
+}
+
 enum TileCfg {
     T256x256 = 0, T256x128 = 1, T128x256 = 2, T128x128 = 3,  // register-staged (any operand form)
     T_DL128x128_S2 = 4, T_DL128x128_S3 = 5, T_DL256x128_S2 = 6, T_DL256x256_S2 = 7,  // direct-to-LDS, k-contiguous
     T_DL256x256_W8 = 8, T_DL256x128_W8 = 9, T_DL128x256_W8 = 10,                          // ... with 8 waves
     T_DL128x128_W8A = 11, T_DL128x128_W8B = 12, T_DL256x128_W8S3 = 13, T_DL128x256_W8S3 = 14,
     T_DL128x64 = 15, T_DL64x128 = 16, T_DL128x64_S3 = 17,
-    T_LAST = T_DL128x64_S3
+    T_DL128x128_W8S4 = 18, T_DL128x64_S4 = 19, T_DL128x128_W8S3 = 20,  // deeper prefetch rings
+    T_LAST = T_DL128x128_W8S3
 };
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+// The split-K reduce of a bf16 GEMM: 16-byte accesses when every operand of
+// the epilogue allows them, element accesses otherwise.
+gp_status launch_reduce(const GemmArgs& a, int epi, int splits, hipStream_t st) {
+    const bool res = epi == EPI_RES_F32, mask = epi == EPI_RELU_MASK;
+    const bool v4 = a.N % 4 == 0 && a.ldc % 4 == 0 && aligned16(a.C) && aligned16(a.ws) &&
+                    (!(epi == EPI_STORE || res) || !a.bias || aligned16(a.bias)) &&
+                    (!(res || mask) || (a.ldaux % 4 == 0 && aligned16(a.aux))) &&
+                    (!res || !a.C2 || (a.ldc2 % 4 == 0 && aligned16(a.C2))) &&
+                    (epi != EPI_ACC_F32 || !a.colsum || aligned16(a.colsum));
+    if (v4) {
+        const int cx = (a.N + 1023) / 1024;
+        // about 2048 workgroups, each over a run of whole rows
+        const int rows = std::max(1, (int)((long)a.M * cx / 2048));
+        const dim3 grid(cx, (a.M + rows - 1) / rows);
+        switch (epi) {
+        case EPI_STORE: klaunch(splitk_reduce_v4<EPI_STORE>, grid, 256, 0, st, a, splits, rows); break;
+        case EPI_RES_F32: klaunch(splitk_reduce_v4<EPI_RES_F32>, grid, 256, 0, st, a, splits, rows); break;
+        case EPI_F32: klaunch(splitk_reduce_v4<EPI_F32>, grid, 256, 0, st, a, splits, rows); break;
+        case EPI_RELU_MASK: klaunch(splitk_reduce_v4<EPI_RELU_MASK>, grid, 256, 0, st, a, splits, rows); break;
+        case EPI_ACC_F32: klaunch(splitk_reduce_v4<EPI_ACC_F32>, grid, 256, 0, st, a, splits, rows); break;
+        default: return set_error(GP_ERR_INVALID_ARG, "gemm: split-K epilogue");
+        }
+        GP_LAUNCH_CHECK();
+        return GP_OK;
+    }
+    const long nq = (long)a.M * (a.N / 4);
+    const int rg = (int)std::min<long>((nq + 255) / 256, 2048);
+    switch (epi) {
+    case EPI_STORE: klaunch(splitk_reduce<bf16, EPI_STORE>, rg, 256, 0, st, a, splits); break;
+    case EPI_RES_F32: klaunch(splitk_reduce<bf16, EPI_RES_F32>, rg, 256, 0, st, a, splits); break;
+    case EPI_F32: klaunch(splitk_reduce<bf16, EPI_F32>, rg, 256, 0, st, a, splits); break;
+    case EPI_RELU_MASK: klaunch(splitk_reduce<bf16, EPI_RELU_MASK>, rg, 256, 0, st, a, splits); break;
+    case EPI_ACC_F32: klaunch(splitk_reduce<bf16, EPI_ACC_F32>, rg, 256, 0, st, a, splits); break;
+    default: return set_error(GP_ERR_INVALID_ARG, "gemm: split-K epilogue");
+    }
+    GP_LAUNCH_CHECK();
+    return GP_OK;
+}
 
 template <typename T, int BM, int BN, bool AK, bool BKM>
 gp_status launch_tile(const GemmArgs& a, int epi, int splits, hipStream_t st) {
@@ -1039,19 +1158,7 @@ gp_status launch_dl(const GemmArgs& a, int epi, int splits, hipStream_t st) {
         dim3 grid(tiles, splits);
         klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_F32, 1, KM>, grid, NT, 0, st, a);
         GP_LAUNCH_CHECK();
-        const long nq = (long)a.M * (a.N / 4);
-        const int rg = (int)std::min<long>((nq + 255) / 256, 2048);
-        switch (epi) {
-        case EPI_STORE: klaunch(splitk_reduce<bf16, EPI_STORE>, rg, 256, 0, st, a, splits); break;
-        case EPI_RES_F32: klaunch(splitk_reduce<bf16, EPI_RES_F32>, rg, 256, 0, st, a, splits); break;
-        case EPI_F32: klaunch(splitk_reduce<bf16, EPI_F32>, rg, 256, 0, st, a, splits); break;
-        case EPI_RELU_MASK: klaunch(splitk_reduce<bf16, EPI_RELU_MASK>, rg, 256, 0, st, a, splits); break;
-        case EPI_ACC_F32: klaunch(splitk_reduce<bf16, EPI_ACC_F32>, rg, 256, 0, st, a, splits); break;
-        default: return set_error(GP_ERR_INVALID_ARG, "gemm: split-K epilogue");
-        }
-        GP_LAUNCH_CHECK();
-
-        return GP_OK;
+        return launch_reduce(a, epi, splits, st);
     }
     if constexpr (KM) {
         switch (epi) {
@@ -1080,9 +1187,7 @@ gp_status launch_dl_mx(const GemmArgs& a, int splits, hipStream_t st) {
     if (splits > 1) {
         klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_F32, 1, true, true>, dim3(tiles, splits), NT, 0, st, a);
         GP_LAUNCH_CHECK();
-        const long nq = (long)a.M * (a.N / 4);
-        const int rg = (int)std::min<long>((nq + 255) / 256, 2048);
-        klaunch(splitk_reduce<bf16, EPI_STORE>, rg, 256, 0, st, a, splits);
+        return launch_reduce(a, EPI_STORE, splits, st);
     } else {
         klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_STORE, 0, true, true>, tiles, NT, 0, st, a);
     }
@@ -1124,6 +1229,11 @@ gp_status launch_bf16(const GemmArgs& a, int epi, int cfg, int splits, hipStream
         case T_DL128x128_W8B: return launch_dl<128, 128, 4, 2, 2, KM>(a, epi, splits, st);
         case T_DL256x128_W8S3: return launch_dl<256, 128, 4, 2, 3, KM>(a, epi, splits, st);
         case T_DL128x256_W8S3: return launch_dl<128, 256, 2, 4, 3, KM>(a, epi, splits, st);
+        case T_DL128x128_W8S4: return launch_dl<128, 128, 2, 4, 4, KM>(a, epi, splits, st);
+        case T_DL128x128_W8S3: return launch_dl<128, 128, 2, 4, 3, KM>(a, epi, splits, st);
+        case T_DL128x64_S4:
+            if constexpr (KM) return launch_dl<128, 64, 2, 2, 4, KM>(a, epi, splits, st);
+            break;
         case T_DL128x64:
             if constexpr (KM) return launch_dl<128, 64, 2, 2, 2, KM>(a, epi, splits, st);
             break;
@@ -1296,7 +1406,8 @@ gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dty
             if (splits > 1 && !split_fits(a, splits, (a.K + 63) / 64)) splits = 1;
         }
         if (cfg > T128x128 && a.K % 64) cfg = T128x128;
-        if (!a_kmajor && cfg >= T_DL128x64) cfg = T_DL128x128_W8A;  // no 64-wide m-contiguous tiles
+        const bool narrow = cfg == T_DL128x64 || cfg == T_DL64x128 || cfg == T_DL128x64_S3 || cfg == T_DL128x64_S4;
+        if (!a_kmajor && narrow) cfg = T_DL128x128_W8A;  // no 64-wide m-contiguous tiles
         return a_kmajor ? launch_bf16<true, true>(a, epi, cfg, splits, st)
                         : launch_bf16<false, false>(a, epi, cfg, splits, st);
     }

@@ -656,11 +656,18 @@ __device__ __forceinline__ bf16x8 tr_frag(const char* p, int second) {
 //   v_mfma_scale_f32_32x32x64_f8f6f4 into the same fp32 accumulator, the
 //   per-lane scale being the E8M0 byte of the lane's row (A) or column (B),
 //   which are loaded once, before the k loop.
-template <int BM, int BN, int WM, int WN, int NSTAGE, int EPI, int SM, bool KM, bool MX = false>
-__global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
+//   KG: k-groups.  With KG = 2 the workgroup holds two groups of WM x WN
+//   waves (two per SIMD for 4-wave groups); group g takes k-tiles g, g + 2,
+//   ... of the same output tile through its own stage ring, both groups in
+//   lockstep (one workgroup barrier per k-tile each), and at the end group 1
+//   hands its accumulators to group 0 through LDS, which adds them and runs
+//   the epilogue.  The k-tile count must be a multiple of KG.
+template <int BM, int BN, int WM, int WN, int NSTAGE, int EPI, int SM, bool KM, bool MX = false, int KG = 1>
+__global__ void __launch_bounds__(64 * WM * WN * KG) gemm_dl(GemmArgs args) {
     // SM: 0 no split-K; 1 split-K, partial tiles only (summed by splitk_reduce)
     constexpr bool SPLIT = SM != 0;
-    constexpr int BK = 64, KS = 4, NW = WM * WN;
+    constexpr int BK = 64, KS = 4, NW = WM * WN;  // NW: waves per k-group
+    static_assert(KG == 1 || (KG == 2 && KM && !MX && !SPLIT), "k-groups: k-contiguous, unsplit, bf16 only");
     constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
     constexpr int STAGE_BF = (BM + BN) * 128;
     constexpr int STAGE = STAGE_BF + (MX ? (BM + BN) * 32 : 0);
@@ -670,19 +677,30 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
     static_assert(KM || (BM >= 128 && BN >= 128), "m-contiguous tiles must be at least 128 wide");
     constexpr int NL4 = MX ? (BM + BN) * 2 / (64 * NW) : 0;  // 1 KB fp4 load blocks per wave
     static_assert(!MX || (KM && NL4 * 64 * NW == (BM + BN) * 2 && (2 * BM) % 64 == 0), "fp4 load blocks");
-    static_assert(NSTAGE * STAGE <= 160 * 1024, "LDS");
+    static_assert(KG * NSTAGE * STAGE <= 160 * 1024, "LDS");
+    static_assert(KG == 1 || BM * BN * 4 <= NSTAGE * STAGE * KG, "LDS for the k-group hand-over");
     constexpr int LPW = PA + PB + NL4;         // load instructions per wave per k-tile
-    __shared__ __attribute__((aligned(1024))) char smem[NSTAGE * STAGE];
+    __shared__ __attribute__((aligned(1024))) char smem_all[KG * NSTAGE * STAGE];
 
     const int tid = threadIdx.x, lane = tid & 63;
-    const int wave = uniform_wave_id(tid);
+    const int wave_all = uniform_wave_id(tid);
+    const int kg = wave_all / NW, wave = wave_all % NW;  // k-group, wave within the group
+    char* const smem = smem_all + kg * NSTAGE * STAGE;   // the group's stage ring
     const int wm = wave / WN, wn = wave % WN;
     const int tiles_m = (args.M + BM - 1) / BM;
     const int G = gridDim.x;
     int bid = blockIdx.x;
     const int G8 = G & ~7;
     if (bid < G8) bid = (bid & 7) * (G8 >> 3) + (bid >> 3);
-    const int tm = bid % tiles_m, tn = bid / tiles_m;
+    // XCD x now holds a contiguous run of ids; number the tiles in bands of
+    // 4 tile rows, column by column within a band, so that the tiles one XCD
+    // runs at a time form a compact block (4 x 8 for 32 workgroups) and its
+    // L2 serves each A row panel and B column panel to several of them
+    // (a run down whole tile columns would stream all of A through every XCD)
+    const int tiles_n = (args.N + BN - 1) / BN;
+    const int band = bid / (4 * tiles_n), in_band = bid - band * 4 * tiles_n;
+    const int bh = min(4, tiles_m - band * 4);
+    const int tm = band * 4 + in_band % bh, tn = in_band / bh;
     const int m0 = tm * BM, n0 = tn * BN;
 
     const int nk_all = args.K / BK;
@@ -692,7 +710,9 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
         kt0 = blockIdx.y * per;
         kt1 = min(nk_all, kt0 + per);
     }
-    const int nkt = kt1 - kt0;
+    // group-local k-tile i is global k-tile kt0 + i KG + kg
+    const int nkt = (kt1 - kt0) / KG;
+    kt0 += kg;
 
     Rsrc A, B;
     uint32_t voa[PA], vob[PB];
@@ -765,8 +785,8 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
     }
 #define GP_DL_ISSUE(t, st)                                                                   \
     do {                                                                                     \
-        dl_load_blocks<PA>(A, voa, (t) * ka, (st) + wave * PA * 1024);                       \
-        dl_load_blocks<PB>(B, vob, (t) * kb, (st) + BM * 128 + wave * PB * 1024);            \
+        dl_load_blocks<PA>(A, voa, (kt0 + ((t) - kt0) * KG) * ka, (st) + wave * PA * 1024);  \
+        dl_load_blocks<PB>(B, vob, (kt0 + ((t) - kt0) * KG) * kb, (st) + BM * 128 + wave * PB * 1024); \
         if constexpr (MX) dl_load_rsrcs<NL4>(R4, vo4, (t) * 32, (st) + STAGE_BF + wave * NL4 * 1024); \
     } while (0)
 
@@ -929,6 +949,31 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_dl(GemmArgs args) {
     }
 
 #undef GP_DL_ISSUE
+    if constexpr (KG == 2) {
+        // group 1 hands its partial sums to group 0 through the (now idle) stage rings;
+        // lane-fastest layout, so both the writes and the reads are conflict-free
+        float* red = reinterpret_cast<float*>(smem_all) + (long)(wm * WN + wn) * TM * TN * 16 * 64 + lane;
+        lds_barrier();
+        if (kg == 1) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const float v = acc[i][j][r];
+                        red[((i * TN + j) * 16 + r) * 64] = v;
+                    }
+        }
+        lds_barrier();
+        if (kg == 1) return;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[i][j][r] += red[((i * TN + j) * 16 + r) * 64];
+    }
     const int row0 = m0 + wm * (BM / WM), col0 = n0 + wn * (BN / WN) + (lane & 31);
     if constexpr (COLSUM) {
         // lanes l and l + 32 hold the two k-halves of column l % 32
@@ -1073,7 +1118,8 @@ enum TileCfg {
     T_DL128x128_W8A = 11, T_DL128x128_W8B = 12, T_DL256x128_W8S3 = 13, T_DL128x256_W8S3 = 14,
     T_DL128x64 = 15, T_DL64x128 = 16, T_DL128x64_S3 = 17,
     T_DL128x128_W8S4 = 18, T_DL128x64_S4 = 19, T_DL128x128_W8S3 = 20,  // deeper prefetch rings
-    T_LAST = T_DL128x128_W8S3
+    T_DL128x64_KG2 = 21, T_DL128x128_KG2 = 22, T_DL64x128_KG2 = 23,     // two k-groups (8 waves)
+    T_LAST = T_DL64x128_KG2
 };
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
@@ -1179,6 +1225,24 @@ gp_status launch_dl(const GemmArgs& a, int epi, int splits, hipStream_t st) {
     return GP_OK;
 }
 
+// Two k-groups per workgroup (k-contiguous operands, no split-K; the host
+// guarantees an even k-tile count).
+template <int BM, int BN, int WM, int WN, int NSTAGE>
+gp_status launch_dl_kg2(const GemmArgs& a, int epi, hipStream_t st) {
+    constexpr int NT = 64 * WM * WN * 2;
+    const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+    switch (epi) {
+    case EPI_STORE: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_STORE, 0, true, false, 2>, tiles, NT, 0, st, a); break;
+    case EPI_RES_F32: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_RES_F32, 0, true, false, 2>, tiles, NT, 0, st, a); break;
+    case EPI_F32: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_F32, 0, true, false, 2>, tiles, NT, 0, st, a); break;
+    case EPI_RELU_MASK: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_RELU_MASK, 0, true, false, 2>, tiles, NT, 0, st, a); break;
+    case EPI_ACC_F32: klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_ACC_F32, 0, true, false, 2>, tiles, NT, 0, st, a); break;
+    default: return set_error(GP_ERR_INVALID_ARG, "gemm: epilogue not instantiated for k-groups");
+    }
+    GP_LAUNCH_CHECK();
+    return GP_OK;
+}
+
 // The fp4-corrected forward GEMM (EPI_STORE, k-contiguous operands).
 template <int BM, int BN, int WM, int WN, int NSTAGE>
 gp_status launch_dl_mx(const GemmArgs& a, int splits, hipStream_t st) {
@@ -1198,7 +1262,8 @@ gp_status launch_dl_mx(const GemmArgs& a, int splits, hipStream_t st) {
 // Tile shapes whose fp4 stage splits into whole 1 KB blocks per wave.
 bool mx_capable(int cfg) {
     return cfg == T_DL128x128_S2 || cfg == T_DL128x128_S3 || cfg == T_DL256x128_S2 || cfg == T_DL256x256_S2 ||
-           cfg == T_DL256x256_W8 || cfg == T_DL128x128_W8A || cfg == T_DL128x128_W8B;
+           cfg == T_DL256x256_W8 || cfg == T_DL128x128_W8A || cfg == T_DL128x128_W8B || cfg == T_DL128x128_W8S3 ||
+           cfg == T_DL128x128_W8S4;
 }
 
 gp_status launch_mx(const GemmArgs& a, int cfg, int splits, hipStream_t st) {
@@ -1209,6 +1274,8 @@ gp_status launch_mx(const GemmArgs& a, int cfg, int splits, hipStream_t st) {
     case T_DL256x256_W8: return launch_dl_mx<256, 256, 2, 4, 2>(a, splits, st);
     case T_DL128x128_W8A: return launch_dl_mx<128, 128, 2, 4, 2>(a, splits, st);
     case T_DL128x128_W8B: return launch_dl_mx<128, 128, 4, 2, 2>(a, splits, st);
+    case T_DL128x128_W8S3: return launch_dl_mx<128, 128, 2, 4, 3>(a, splits, st);
+    case T_DL128x128_W8S4: return launch_dl_mx<128, 128, 2, 4, 4>(a, splits, st);
     default: return launch_dl_mx<128, 128, 2, 2, 2>(a, splits, st);
     }
 }
@@ -1233,6 +1300,15 @@ gp_status launch_bf16(const GemmArgs& a, int epi, int cfg, int splits, hipStream
         case T_DL128x128_W8S3: return launch_dl<128, 128, 2, 4, 3, KM>(a, epi, splits, st);
         case T_DL128x64_S4:
             if constexpr (KM) return launch_dl<128, 64, 2, 2, 4, KM>(a, epi, splits, st);
+            break;
+        case T_DL128x64_KG2:
+            if constexpr (KM) return launch_dl_kg2<128, 64, 2, 2, 3>(a, epi, st);
+            break;
+        case T_DL128x128_KG2:
+            if constexpr (KM) return launch_dl_kg2<128, 128, 2, 2, 2>(a, epi, st);
+            break;
+        case T_DL64x128_KG2:
+            if constexpr (KM) return launch_dl_kg2<64, 128, 2, 2, 3>(a, epi, st);
             break;
         case T_DL128x64:
             if constexpr (KM) return launch_dl<128, 64, 2, 2, 2, KM>(a, epi, splits, st);
@@ -1273,9 +1349,10 @@ bool split_fits(const GemmArgs& a, int s, int nk) {
 // its CU or sharing it with a second one) + the fp32 read-modify-write of an
 // accumulating epilogue + the split-K partial traffic and reduce.  The
 // constants were fitted to measurements of the d_model 1024 partition's GEMMs
-// on MI355X at 512, 2048 and 4096 token rows, separately for k-contiguous operands
-// (forward and input-gradient GEMMs) and m/n-contiguous ones (weight
-// gradients, whose transposing LDS reads cost more per step).  Units: us.
+// on MI355X at 512, 1024, 2048 and 4096 token rows (random bf16 operands,
+// splits up to 4), separately for k-contiguous operands (forward and
+// input-gradient GEMMs) and m/n-contiguous ones (weight gradients, whose
+// transposing LDS reads cost more per step).  Units: us.
 // Weight of the split-K cost terms (GP_SPLIT_WEIGHT, default 1): the fit was
 // made on GEMMs running alone; next to concurrent work the partial traffic
 // can cost more.
@@ -1292,31 +1369,38 @@ void choose_dl(const GemmArgs& a, int epi, bool kmaj, int& cfg, int& splits) {
     // and a quarter more tile traffic; only some shapes carry it
     const bool mx = a.a4 != nullptr;
     const double mx_step = mx ? 1.25 : 1.0;
-    // per-step time with 1, 2 or 3 tiles sharing a CU; [k-contiguous][m-contiguous]; 0 = not available
-    struct Cand { int cfg, bm, bn, resident; double step[2][3]; };
-    static const Cand cands[7] = {
-        {T_DL128x128_W8A, 128, 128, 2, {{0.586, 1.154, 0}, {0.754, 0.952, 0}}},
-        {T_DL128x128_S2, 128, 128, 2, {{0.636, 1.192, 0}, {1.186, 1.259, 0}}},
-        {T_DL256x256_W8, 256, 256, 1, {{1.498, 0, 0}, {1.612, 0, 0}}},
-        {T_DL256x128_W8, 256, 128, 1, {{0.970, 0, 0}, {1.117, 0, 0}}},
-        {T_DL128x256_W8, 128, 256, 1, {{0.875, 0, 0}, {1.066, 0, 0}}},
-        {T_DL128x64, 128, 64, 3, {{0.443, 0.657, 1.030}, {0, 0, 0}}},
-        {T_DL64x128, 64, 128, 3, {{0.463, 0.640, 0.848}, {0, 0, 0}}}};
-    const int v = kmaj ? 0 : 1;
-    const double c0 = kmaj ? 3.052 : 1.519, BW = kmaj ? 3.704e6 : 4.646e6, red0 = kmaj ? 6.278 : 8.667;
+    // per-k-tile time with 1, 2 or 3 tiles sharing a CU (0 = cannot share)
+    struct Cand { int cfg, bm, bn, resident; double step[3]; };
+    static const Cand kc[] = {  // k-contiguous operands
+        {T_DL256x256_W8, 256, 256, 1, {1.289, 0, 0}},    {T_DL256x128_W8, 256, 128, 1, {0.872, 0, 0}},
+        {T_DL128x256_W8, 128, 256, 1, {0.814, 0, 0}},    {T_DL128x128_W8A, 128, 128, 2, {0.568, 1.005, 0}},
+        {T_DL128x256_W8S3, 128, 256, 1, {0.767, 0, 0}},  {T_DL128x64, 128, 64, 3, {0.445, 0.630, 0.885}},
+        {T_DL64x128, 64, 128, 3, {0.460, 0.611, 0.755}}, {T_DL128x64_S3, 128, 64, 2, {0.291, 0.785, 0}},
+        {T_DL128x128_W8S4, 128, 128, 1, {0.499, 0, 0}},  {T_DL128x64_S4, 128, 64, 1, {0.390, 0, 0}},
+        {T_DL128x128_W8S3, 128, 128, 1, {0.483, 0, 0}}};
+    static const Cand mc[] = {  // m/n-contiguous operands (weight gradients)
+        {T_DL256x256_W8, 256, 256, 1, {1.856, 0, 0}},    {T_DL256x128_W8, 256, 128, 1, {1.247, 0, 0}},
+        {T_DL128x256_W8, 128, 256, 1, {1.216, 0, 0}},    {T_DL128x128_W8A, 128, 128, 2, {0.831, 1.044, 0}},
+        {T_DL128x128_W8B, 128, 128, 2, {0.900, 1.082, 0}}, {T_DL256x128_W8S3, 256, 128, 1, {1.255, 0, 0}},
+        {T_DL128x256_W8S3, 128, 256, 1, {1.221, 0, 0}},  {T_DL128x128_W8S4, 128, 128, 1, {0.865, 0, 0}},
+        {T_DL128x128_W8S3, 128, 128, 1, {0.850, 0, 0}}};
+    const Cand* cands = kmaj ? kc : mc;
+    const int ncand = kmaj ? (int)(sizeof(kc) / sizeof(kc[0])) : (int)(sizeof(mc) / sizeof(mc[0]));
+    const double c0 = kmaj ? 3.759 : 0.985, BW = kmaj ? 1.758e6 : 4.958e6, red0 = kmaj ? 2.538 : 6.942;
     const int nk = a.K / 64;
     double best = 1e300;
     cfg = T_DL128x128_W8A;
     splits = 1;
-    for (const Cand& c : cands) {
-        if (c.step[v][0] <= 0 || (mx && !mx_capable(c.cfg))) continue;
+    for (int ci = 0; ci < ncand; ++ci) {
+        const Cand& c = cands[ci];
+        if (mx && !mx_capable(c.cfg)) continue;
         const long tiles = (long)((a.M + c.bm - 1) / c.bm) * ((a.N + c.bn - 1) / c.bn);
-        for (int s = 1; s <= 8; s *= 2) {
+        for (int s = 1; s <= 4; s *= 2) {
             if (s > 1 && !split_fits(a, s, nk)) continue;
             const long per_cu = (tiles * s + NUM_CU - 1) / NUM_CU;
             const long rounds = (per_cu + c.resident - 1) / c.resident;
             const int occ = (int)std::min<long>(per_cu, c.resident);
-            double t = c0 + rounds * (double)((nk + s - 1) / s) * c.step[v][occ - 1] * mx_step;
+            double t = c0 + rounds * (double)((nk + s - 1) / s) * c.step[occ - 1] * mx_step;
             if (epi == EPI_ACC_F32) t += (kmaj ? 3.0 : 0.0) + (double)a.M * a.N * 8.0 / BW;
             if (s > 1) t += split_weight() * ((double)a.M * a.N * 4.0 * (s + 1.0) / 2.0 / BW + red0);
             if (t < best * 0.999) {
@@ -1407,7 +1491,12 @@ gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dty
         }
         if (cfg > T128x128 && a.K % 64) cfg = T128x128;
         const bool narrow = cfg == T_DL128x64 || cfg == T_DL64x128 || cfg == T_DL128x64_S3 || cfg == T_DL128x64_S4;
-        if (!a_kmajor && narrow) cfg = T_DL128x128_W8A;  // no 64-wide m-contiguous tiles
+        const bool kg2 = cfg == T_DL128x64_KG2 || cfg == T_DL128x128_KG2 || cfg == T_DL64x128_KG2;
+        if (!a_kmajor && (narrow || kg2)) cfg = T_DL128x128_W8A;  // no 64-wide or k-group m-contiguous tiles
+        if (kg2 && (splits > 1 || (a.K / 64) % 2)) {               // k-groups: unsplit, even k-tile count
+            cfg = T_DL128x64_S4;
+            splits = 1;
+        }
         return a_kmajor ? launch_bf16<true, true>(a, epi, cfg, splits, st)
                         : launch_bf16<false, false>(a, epi, cfg, splits, st);
     }

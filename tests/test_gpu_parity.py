@@ -361,13 +361,14 @@ def test_call_order_is_enforced():
 TILE_CASES = [(0, 1), (1, 1), (2, 1), (3, 1), (0, 4), (3, 2),
               (4, 1), (5, 1), (6, 1), (7, 1), (8, 1), (9, 1), (10, 1), (4, 2), (8, 4), (10, 4),
               (11, 1), (12, 1), (13, 1), (14, 1), (11, 4), (15, 1), (16, 1), (17, 1), (15, 4),
-              (18, 1), (19, 1), (20, 1), (18, 2)]
+              (18, 1), (19, 1), (20, 1), (18, 2), (21, 1), (22, 1), (23, 1)]
 TILE_IDS = ["256x256", "256x128", "128x256", "128x128", "256x256_split4", "128x128_split2",
             "dl128x128", "dl128x128_3stage", "dl256x128", "dl256x256", "dl256x256_8w", "dl256x128_8w",
             "dl128x256_8w", "dl128x128_split2", "dl256x256_8w_split4", "dl128x256_8w_split4",
             "dl128x128_8w_a", "dl128x128_8w_b", "dl256x128_8w_3stage", "dl128x256_8w_3stage", "dl128x128_8w_split4",
             "dl128x64", "dl64x128", "dl128x64_3stage", "dl128x64_split4",
-            "dl128x128_8w_4stage", "dl128x64_4stage", "dl128x128_8w_3stage", "dl128x128_8w_4stage_split2"]
+            "dl128x128_8w_4stage", "dl128x64_4stage", "dl128x128_8w_3stage", "dl128x128_8w_4stage_split2",
+            "dl128x64_kgroups", "dl128x128_kgroups", "dl64x128_kgroups"]
 
 
 @pytest.mark.parametrize("tile,splits", TILE_CASES, ids=TILE_IDS)

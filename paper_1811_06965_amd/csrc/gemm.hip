@@ -693,14 +693,19 @@ __global__ void __launch_bounds__(64 * WM * WN * KG) gemm_dl(GemmArgs args) {
     const int G8 = G & ~7;
     if (bid < G8) bid = (bid & 7) * (G8 >> 3) + (bid >> 3);
     // XCD x now holds a contiguous run of ids; number the tiles in bands of
-    // 4 tile rows, column by column within a band, so that the tiles one XCD
+    // H tile rows, column by column within a band, so that the tiles one XCD
     // runs at a time form a compact block (4 x 8 for 32 workgroups) and its
     // L2 serves each A row panel and B column panel to several of them
     // (a run down whole tile columns would stream all of A through every XCD)
+    // The band height H suits the tiles an XCD runs at once (P: its 32 CUs
+    // times the workgroups that fit a CU): about sqrt(P BN / BM) rows.
+    constexpr int RES = (160 * 1024) / (KG * NSTAGE * STAGE) < 1 ? 1 : (160 * 1024) / (KG * NSTAGE * STAGE);
+    const int P = min(max(G >> 3, 1), 32 * min(RES, 3));
+    const int H = P * BN >= 64 * BM ? 8 : 4;
     const int tiles_n = (args.N + BN - 1) / BN;
-    const int band = bid / (4 * tiles_n), in_band = bid - band * 4 * tiles_n;
-    const int bh = min(4, tiles_m - band * 4);
-    const int tm = band * 4 + in_band % bh, tn = in_band / bh;
+    const int band = bid / (H * tiles_n), in_band = bid - band * H * tiles_n;
+    const int bh = min(H, tiles_m - band * H);
+    const int tm = band * H + in_band % bh, tn = in_band / bh;
     const int m0 = tm * BM, n0 = tn * BN;
 
     const int nk_all = args.K / BK;

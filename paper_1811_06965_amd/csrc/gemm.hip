@@ -1377,21 +1377,21 @@ void choose_dl(const GemmArgs& a, int epi, bool kmaj, int& cfg, int& splits) {
     // per-k-tile time with 1, 2 or 3 tiles sharing a CU (0 = cannot share)
     struct Cand { int cfg, bm, bn, resident; double step[3]; };
     static const Cand kc[] = {  // k-contiguous operands
-        {T_DL256x256_W8, 256, 256, 1, {1.289, 0, 0}},    {T_DL256x128_W8, 256, 128, 1, {0.872, 0, 0}},
-        {T_DL128x256_W8, 128, 256, 1, {0.814, 0, 0}},    {T_DL128x128_W8A, 128, 128, 2, {0.568, 1.005, 0}},
-        {T_DL128x256_W8S3, 128, 256, 1, {0.767, 0, 0}},  {T_DL128x64, 128, 64, 3, {0.445, 0.630, 0.885}},
-        {T_DL64x128, 64, 128, 3, {0.460, 0.611, 0.755}}, {T_DL128x64_S3, 128, 64, 2, {0.291, 0.785, 0}},
-        {T_DL128x128_W8S4, 128, 128, 1, {0.499, 0, 0}},  {T_DL128x64_S4, 128, 64, 1, {0.390, 0, 0}},
-        {T_DL128x128_W8S3, 128, 128, 1, {0.483, 0, 0}}};
+        {T_DL256x256_W8, 256, 256, 1, {1.259, 0, 0}},    {T_DL256x128_W8, 256, 128, 1, {0.793, 0, 0}},
+        {T_DL128x256_W8, 128, 256, 1, {0.782, 0, 0}},    {T_DL128x128_W8A, 128, 128, 2, {0.508, 0.863, 0}},
+        {T_DL128x256_W8S3, 128, 256, 1, {0.748, 0, 0}},  {T_DL128x64, 128, 64, 3, {0.400, 0.539, 0.681}},
+        {T_DL64x128, 64, 128, 3, {0.391, 0.533, 0.680}}, {T_DL128x64_S3, 128, 64, 2, {0.263, 0.533, 0}},
+        {T_DL128x128_W8S4, 128, 128, 1, {0.440, 0, 0}},  {T_DL128x64_S4, 128, 64, 1, {0.307, 0, 0}},
+        {T_DL128x128_W8S3, 128, 128, 1, {0.419, 0, 0}}};
     static const Cand mc[] = {  // m/n-contiguous operands (weight gradients)
-        {T_DL256x256_W8, 256, 256, 1, {1.856, 0, 0}},    {T_DL256x128_W8, 256, 128, 1, {1.247, 0, 0}},
-        {T_DL128x256_W8, 128, 256, 1, {1.216, 0, 0}},    {T_DL128x128_W8A, 128, 128, 2, {0.831, 1.044, 0}},
-        {T_DL128x128_W8B, 128, 128, 2, {0.900, 1.082, 0}}, {T_DL256x128_W8S3, 256, 128, 1, {1.255, 0, 0}},
-        {T_DL128x256_W8S3, 128, 256, 1, {1.221, 0, 0}},  {T_DL128x128_W8S4, 128, 128, 1, {0.865, 0, 0}},
-        {T_DL128x128_W8S3, 128, 128, 1, {0.850, 0, 0}}};
+        {T_DL256x256_W8, 256, 256, 1, {1.823, 0, 0}},    {T_DL256x128_W8, 256, 128, 1, {1.218, 0, 0}},
+        {T_DL128x256_W8, 128, 256, 1, {1.195, 0, 0}},    {T_DL128x128_W8A, 128, 128, 2, {0.778, 0.917, 0}},
+        {T_DL128x128_W8B, 128, 128, 2, {0.842, 0.964, 0}}, {T_DL256x128_W8S3, 256, 128, 1, {1.221, 0, 0}},
+        {T_DL128x256_W8S3, 128, 256, 1, {1.200, 0, 0}},  {T_DL128x128_W8S4, 128, 128, 1, {0.801, 0, 0}},
+        {T_DL128x128_W8S3, 128, 128, 1, {0.785, 0, 0}}};
     const Cand* cands = kmaj ? kc : mc;
     const int ncand = kmaj ? (int)(sizeof(kc) / sizeof(kc[0])) : (int)(sizeof(mc) / sizeof(mc[0]));
-    const double c0 = kmaj ? 3.759 : 0.985, BW = kmaj ? 1.758e6 : 4.958e6, red0 = kmaj ? 2.538 : 6.942;
+    const double c0 = kmaj ? 4.435 : 1.395, BW = kmaj ? 2.100e6 : 5.297e6, red0 = kmaj ? 3.367 : 7.255;
     const int nk = a.K / 64;
     double best = 1e300;
     cfg = T_DL128x128_W8A;

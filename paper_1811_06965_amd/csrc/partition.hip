@@ -383,7 +383,7 @@ gp_status linear_fwd(const Ctx& c, const Linear& L, const void* A, long M, void*
     g.lda = L.in;
     g.B = c.p->W(L.nk);
     g.ldb = L.in;
-    if (L.split) {
+    if (L.split && A4) {
         g.a4 = A4;
         g.sa4 = A4s;
         g.b4 = c.p->W(L.q4);
@@ -492,7 +492,7 @@ AttnArgs attn_args(const gp_partition* p, int Sk, int causal) {
 // stream; mem is the decoder memory (elt [Tm, D]); y_out (optional) receives
 // the output rounded to the partition dtype.
 gp_status layer_forward(const Ctx& c, int l, LayerWs& w, const float* x_in, float* x_out, const void* mem,
-                        void* y_out) {
+                        void* y_out, bool keep) {
     gp_partition* p = c.p;
     const LayerPlan& P = p->plan.layers[l];
     const long T = p->g.T(), D = p->d.D;
@@ -532,10 +532,13 @@ GP_TRY(timed_attention(c, GP_K_ATTN_FWD, a, false));
     }
     // feed-forward block
     const Norm& nf = dec ? P.ln3 : P.ln2;
-    const bool s4 = P.ffn1.split;
+    // The fp4 correction serves the ReLU mask that the backward takes from the
+    // recomputed forward; the first forward's output only leaves the partition.
+    const bool s4 = P.ffn1.split && keep;
     GP_TRY(timed_ln_fwd(c, xf, T, (int)D, p->master + nf.g, p->master + nf.b, eps, w.v, w.stf, s4 ? w.v4 : nullptr,
                         s4 ? w.v4s : nullptr));
-    GP_TRY(linear_fwd(c, P.ffn1, w.v, T, w.a, p->d.F, EPI_STORE, 1, nullptr, nullptr, w.v4, w.v4s));
+    GP_TRY(linear_fwd(c, P.ffn1, w.v, T, w.a, p->d.F, EPI_STORE, 1, nullptr, nullptr, s4 ? w.v4 : nullptr,
+                      s4 ? w.v4s : nullptr));
     GP_TRY(linear_fwd(c, P.ffn2, w.a, T, x_out, D, EPI_RES_F32, 0, xf, y_out));
     return GP_OK;
 }
@@ -559,7 +562,7 @@ gp_status partition_forward(const Ctx& c, int m, bool keep, const void* x, const
         LayerWs& w = keep ? p->lw[set][l] : p->lw[set][0];
         const float* xi = keep ? xs[l] : xs[l & 1];
         float* xo = keep ? xs[l + 1] : xs[(l + 1) & 1];
-        GP_TRY(layer_forward(c, l, w, xi, xo, mem_m, (!keep && l == L - 1) ? y : nullptr));
+        GP_TRY(layer_forward(c, l, w, xi, xo, mem_m, (!keep && l == L - 1) ? y : nullptr, keep));
     }
     return GP_OK;
 }

@@ -136,6 +136,30 @@ __global__ void __launch_bounds__(256) refresh_kernel(const float* __restrict__ 
     }
 }
 
+// The same for bf16 copies of whole 64 x 64 tiles (in, out multiples of 64):
+// 16-byte reads of W, 8-byte writes of both copies.
+__global__ void __launch_bounds__(256) refresh_bf16_tiles(const float* __restrict__ w, int in, int out,
+                                                          bf16* __restrict__ kn, bf16* __restrict__ nk) {
+    __shared__ float tile[64][65];
+    const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64, t = threadIdx.x;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int idx = t + 256 * k, r = idx >> 4, c = (idx & 15) * 4;
+        const long o = (long)(r0 + r) * out + c0 + c;
+        const f32x4 v = *reinterpret_cast<const f32x4*>(w + o);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) tile[r][c + j] = v[j];
+        *reinterpret_cast<bf16x4*>(kn + o) = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int idx = t + 256 * k, c = idx >> 4, r = (idx & 15) * 4;
+        *reinterpret_cast<bf16x4*>(nk + (long)(c0 + c) * in + r0 + r) =
+            {(bf16)tile[r][c], (bf16)tile[r + 1][c], (bf16)tile[r + 2][c], (bf16)tile[r + 3][c]};
+    }
+}
+
 // fp4 copy of bf16 rows (the W^T working copy, rows of `in` values): one wave
 // per row; 8 values per lane step; one E8M0 scale per row (see e2m1_code).
 __global__ void __launch_bounds__(256) quant4_rows_kernel(const bf16* __restrict__ src, int rows, int in,
@@ -237,7 +261,9 @@ gp_status sgd_update(float* w, const float* g, float lr, long count, hipStream_t
 gp_status refresh_linear(int dtype, const float* w, int in, int out, void* kn, void* nk, void* q4, void* q4s,
                          hipStream_t st) {
     dim3 grid((out + 63) / 64, (in + 63) / 64);
-    if (dtype == GP_BF16)
+    if (dtype == GP_BF16 && in % 64 == 0 && out % 64 == 0)
+        klaunch(refresh_bf16_tiles, grid, 256, 0, st, w, in, out, reinterpret_cast<bf16*>(kn), reinterpret_cast<bf16*>(nk));
+    else if (dtype == GP_BF16)
         klaunch(refresh_kernel<bf16>, grid, 256, 0, st, w, in, out, reinterpret_cast<bf16*>(kn), reinterpret_cast<bf16*>(nk));
     else
         klaunch(refresh_kernel<float>, grid, 256, 0, st, w, in, out, reinterpret_cast<float*>(kn), reinterpret_cast<float*>(nk));

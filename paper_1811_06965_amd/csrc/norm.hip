@@ -259,22 +259,38 @@ __global__ void __launch_bounds__(256) ln_bwd_v4(const float* __restrict__ dn, c
 #pragma unroll
     for (int c = 0; c < C4; ++c) pg[c] = pb[c] = f32x4{0.f, 0.f, 0.f, 0.f};
     const long row0 = ((long)blockIdx.x * LN_WAVES + wave) * rpw;
-    for (int rr = 0; rr < rpw; ++rr) {
-        const long row = row0 + rr;
-        if (row >= rows) break;
-        const float mu = stats[2 * row], rstd = stats[2 * row + 1];
+    const int nr = (int)max(0L, min((long)rpw, rows - row0));
+    // the next row's operands are loaded while the current row is computed
+    f32x4 dv[C4], xv[C4], rv[C4];
+    float mu = 0.f, rstd = 0.f;
+    auto load = [&](long row, f32x4* d, f32x4* xx, f32x4* r, float& m, float& s) {
+        m = stats[2 * row];
+        s = stats[2 * row + 1];
         const f32x4* dn4 = reinterpret_cast<const f32x4*>(dn + row * D);
         const f32x4* x4 = reinterpret_cast<const f32x4*>(x + row * D);
+        const f32x4* r4 = reinterpret_cast<const f32x4*>(dres + row * D);
+#pragma unroll
+        for (int c = 0; c < C4; ++c) {
+            d[c] = dn4[lane + 64 * c];
+            xx[c] = x4[lane + 64 * c];
+            r[c] = dres ? r4[lane + 64 * c] : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+    };
+    if (nr > 0) load(row0, dv, xv, rv, mu, rstd);
+    for (int rr = 0; rr < nr; ++rr) {
+        const long row = row0 + rr;
+        f32x4 dv2[C4], xv2[C4], rv2[C4];
+        float mu2 = 0.f, rstd2 = 0.f;
+        if (rr + 1 < nr) load(row + 1, dv2, xv2, rv2, mu2, rstd2);
         f32x4 g[C4], xh[C4];
         float sg = 0.f, sgx = 0.f;
 #pragma unroll
         for (int c = 0; c < C4; ++c) {
             const int i = lane + 64 * c;
-            const f32x4 dv = dn4[i];
-            xh[c] = (x4[i] - mu) * rstd;
-            g[c] = dv * g4[i];
-            pg[c] += dv * xh[c];
-            pb[c] += dv;
+            xh[c] = (xv[c] - mu) * rstd;
+            g[c] = dv[c] * g4[i];
+            pg[c] += dv[c] * xh[c];
+            pb[c] += dv[c];
             sg += hsum(g[c]);
             sgx += hsum(g[c] * xh[c]);
         }
@@ -283,10 +299,19 @@ __global__ void __launch_bounds__(256) ln_bwd_v4(const float* __restrict__ dn, c
 #pragma unroll
         for (int c = 0; c < C4; ++c) {
             const int i = lane + 64 * c;
-            f32x4 r = rstd * (g[c] - sg - xh[c] * sgx);
-            if (dres) r += reinterpret_cast<const f32x4*>(dres + row * D)[i];
+            const f32x4 r = rstd * (g[c] - sg - xh[c] * sgx) + rv[c];
             if (dx32) reinterpret_cast<f32x4*>(dx32 + row * D)[i] = r;
             if (dxe) Out4<T>::store(dxe + row * D + 4 * i, r);
+        }
+        if (rr + 1 < nr) {
+#pragma unroll
+            for (int c = 0; c < C4; ++c) {
+                dv[c] = dv2[c];
+                xv[c] = xv2[c];
+                rv[c] = rv2[c];
+            }
+            mu = mu2;
+            rstd = rstd2;
         }
     }
 #pragma unroll

@@ -230,6 +230,16 @@ def census(part, inp, dx):
     return dict(sorted(roles.items(), key=lambda kv: -kv[1]["ms"]))
 
 
+def dominant_role(roles):
+    """The role with the most launch time in the census step; roles within
+    10% of it count as tied (the split of a step between concurrent streams
+    moves by that much from run to run), and a tie goes to the role doing the
+    most algorithmic work per step."""
+    top = next(iter(roles.values()))["ms"]
+    tied = [(r["flops"], name) for name, r in roles.items() if r["ms"] >= 0.9 * top]
+    return max(tied)[1]
+
+
 def timed_eager(part, inp, steps, dx, role):
     """K eager steps between two events on the launch stream, with the role's
     launches bracketed by dispatch events."""
@@ -277,7 +287,7 @@ def time_steps(part, inp, steps, warmup, role=None, graph=False):
     torch.cuda.synchronize()
     roles = census(part, inp, dx) if role is None else None
     if role is None:
-        role = next(iter(roles))
+        role = dominant_role(roles)
     if not graph:
         ms, timed = timed_eager(part, inp, steps, dx, role)
         return ms, role, timed, roles, "dispatch events over the timed eager steps"

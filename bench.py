@@ -413,6 +413,11 @@ def main():
                       "memory_bytes": mem, "role": role, "timed": timed, "roles": roles, "how": how}
         print(f"[bench] M={M}: {ms:.2f} ms/step, {results[M]['tokens_per_s']:.0f} tokens/s, "
               f"HFU {100 * results[M]['hfu']:.1f}%, dominant role {role}", file=sys.stderr, flush=True)
+    # the sustained MFMA-loop rate of this device, measured after the timed runs
+    from paper_1811_06965_amd import gp
+    peak_meas = gp.gp_mfma_peak(torch.cuda.current_stream().cuda_stream) * 1e12
+    for res in results.values():
+        res["hfu_measured_peak"] = res["hfu"] * PEAK_BF16 / peak_meas
     r = results[a.micro]
     out = {
         "metric": METRIC, "value": r["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1, "steps": a.steps,
@@ -421,16 +426,20 @@ def main():
         "config": {"workload": workload, "global_batch": cfg.batch, "seq_len": cfg.seq, "micro_batches": cfg.micro,
                    "parallelism": "one pipeline partition on one GPU"},
         "hfu": r["hfu"], "mfu": r["mfu"],
+        "mfma_peak_measured_tflops": peak_meas * 1e-12, "hfu_measured_peak": r["hfu_measured_peak"],
         "roofline": roofline(r["role"], r["timed"], workload),
         "launch": "HIP graph: the whole step captured once, replayed" if a.graph else "eager (host-enqueued launches)",
     }
     out["roofline"]["timing"] = r["how"]
+    if out["roofline"]["bound"] == "mfma":
+        out["roofline"]["frac_of_measured_peak"] = out["roofline"]["achieved"] * 1e12 / peak_meas
     if r["roles"]:
         step_ms = r["ms_per_step"]
         out["roles_ms_per_step"] = {k: round(v["ms"], 3) for k, v in r["roles"].items()}
         out["roles_note"] = f"census step with every launch bracketed; step time {step_ms:.2f} ms unbracketed"
     if a.sweep:
-        out["sweep"] = [{k: v for k, v in results[M].items() if k in ("M", "ms_per_step", "tokens_per_s", "hfu", "mfu")}
+        out["sweep"] = [{k: v for k, v in results[M].items()
+                         if k in ("M", "ms_per_step", "tokens_per_s", "hfu", "mfu", "hfu_measured_peak")}
                         for M in sorted(results)]
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, a.cpu_layers)

@@ -249,6 +249,16 @@ gp_status gp_timer_read(gp_partition* p, int role, double* ms, long* launches, d
 /* Forget every recorded launch (the events are kept for reuse). */
 gp_status gp_timer_reset(gp_partition* p);
 
+/* Instrumentation: the sustained bf16 MFMA rate of the current device, the
+ * reference for "fraction of the measured MFMA peak".  Runs a register-only
+ * loop of v_mfma_f32_32x32x16_bf16 (pseudo-random operands, 8 independent
+ * accumulators per wave, two 4-wave workgroups per CU) on `stream` (a
+ * hipStream_t; NULL = the null stream), waits for it, and stores the best of
+ * three timed runs (after a warm-up run) in *tflops, in TFLOP/s.  Allocates a
+ * small output buffer stream-ordered and frees it.
+ * GP_ERR_INVALID_ARG: tflops is NULL; GP_ERR_HIP: a launch or event failed. */
+gp_status gp_mfma_peak(void* stream, double* tflops);
+
 /* Message of the calling thread's last failure (library-owned, valid until the
  * thread's next failing call); "" if none. */
 const char* gp_last_error(void);

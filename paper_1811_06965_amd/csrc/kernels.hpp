@@ -108,6 +108,9 @@ int xent_partials(long rows);
 
 // --------------------------------------------------------------- update
 // w[i] -= lr * g[i] for i < count (fp32 masters).
+// Sustained bf16 MFMA rate of a register-only 32x32x16 loop on every CU
+// (best of three timed runs after one warm-up), in TFLOP/s; synchronises st.
+gp_status mfma_peak(hipStream_t st, double* tflops);
 gp_status sgd_update(float* w, const float* g, float lr, long count, hipStream_t st);
 // Working copies of one linear layer from its fp32 master W [in, out]:
 // kn (elt) = W, nk (elt) = W^T.

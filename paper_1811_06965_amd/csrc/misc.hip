@@ -1,3 +1,4 @@
+#include <algorithm>
 // misc.hip -- boundary intake, casts, loss heads and the synchronous update.
 //
 // All reductions are two-stage with a fixed order (per-block partials, then
@@ -188,6 +189,42 @@ __global__ void __launch_bounds__(256) quant4_rows_kernel(const bf16* __restrict
     if (lane == 0) sc[row] = (unsigned char)s;
 }
 
+// MFMA-loop peak probe: 4 waves per workgroup, each with 8 independent
+// 32x32 accumulators and two operand sets of pseudo-random bf16 (so that the
+// multiplier inputs toggle as in a real GEMM); 16 MFMAs per trip.
+__global__ void __launch_bounds__(256) mfma_peak_kernel(float* __restrict__ out, int iters) {
+    typedef __bf16 b8 __attribute__((ext_vector_type(8)));
+    typedef float f16v __attribute__((ext_vector_type(16)));
+    unsigned h = (blockIdx.x * 256u + threadIdx.x) * 2654435761u + 12345u;
+    b8 a[2], b[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            h = h * 1664525u + 1013904223u;
+            a[k][e] = (__bf16)(((int)(h >> 16) - 32768) * (1.f / 32768.f));
+            h = h * 1664525u + 1013904223u;
+            b[k][e] = (__bf16)(((int)(h >> 16) - 32768) * (1.f / 32768.f));
+        }
+    f16v c[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) c[j][r] = 0.f;
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+        for (int k = 0; k < 2; ++k)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) c[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[k], b[k], c[j], 0, 0, 0);
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s += c[j][r];
+    out[blockIdx.x * 256 + threadIdx.x] = s;
+}
+
 __global__ void __launch_bounds__(256) finite_kernel(const float* __restrict__ x, long count, int* __restrict__ flag) {
     bool bad = false;
     for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < count; i += (long)gridDim.x * 256)
@@ -250,6 +287,38 @@ gp_status xent_ls(int dtype, void* z, long rows, int V, const int* labels, float
         klaunch(xent_kernel<float>, (unsigned)rows, 256, 0, st, reinterpret_cast<float*>(z), V, labels, ls, norm, partial);
     GP_LAUNCH_CHECK();
     return GP_OK;
+}
+
+gp_status mfma_peak(hipStream_t st, double* tflops) {
+    int dev = 0, cus = 0;
+    GP_HIP(hipGetDevice(&dev));
+    GP_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+    const int grid = 2 * cus, iters = 2000;
+    float* out = nullptr;
+    GP_HIP(hipMalloc(reinterpret_cast<void**>(&out), (size_t)grid * 256 * sizeof(float)));
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    gp_status s = GP_OK;
+    double best = 0.0;
+    if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) s = set_error(GP_ERR_HIP, "mfma_peak: event");
+    for (int rep = 0; rep < 4 && s == GP_OK; ++rep) {
+        hipEventRecord(e0, st);
+        klaunch(mfma_peak_kernel, grid, 256, 0, st, out, iters);
+        const hipError_t le = take_launch_status();
+        hipEventRecord(e1, st);
+        float ms = 0.f;
+        if (le != hipSuccess || hipEventSynchronize(e1) != hipSuccess || hipEventElapsedTime(&ms, e0, e1) != hipSuccess) {
+            s = set_error(GP_ERR_HIP, "mfma_peak: launch or timing failed");
+            break;
+        }
+        const double fl = (double)grid * 4 * iters * 16 * 32768.0;
+        if (rep > 0 && ms > 0.f) best = std::max(best, fl / (ms * 1e-3) * 1e-12);  // the first run warms up
+    }
+    if (e0) hipEventDestroy(e0);
+    if (e1) hipEventDestroy(e1);
+    hipStreamSynchronize(st);
+    hipFree(out);
+    if (s == GP_OK && tflops) *tflops = best;
+    return s;
 }
 
 gp_status sgd_update(float* w, const float* g, float lr, long count, hipStream_t st) {

@@ -920,6 +920,11 @@ gp_status gp_timer_read(gp_partition* p, int role, double* ms, long* launches, d
     return GP_OK;
 }
 
+gp_status gp_mfma_peak(void* stream, double* tflops) {
+    if (!tflops) return set_error(GP_ERR_INVALID_ARG, "tflops must not be NULL");
+    return mfma_peak(static_cast<hipStream_t>(stream), tflops);
+}
+
 gp_status gp_timer_reset(gp_partition* p) {
     if (!p) return set_error(GP_ERR_INVALID_ARG, "partition must not be NULL");
     p->timer.reset();

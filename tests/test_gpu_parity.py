@@ -384,3 +384,12 @@ def test_bf16_every_gemm_tile_shape(tile, splits, monkeypatch):
         # T = 2 x 128 rows: the weight-gradient GEMMs take the forced direct-to-LDS tile too
         case, ref, res = _run(ENC512_SMALL, 4, perturb=True)
         _check(ENC512_SMALL, ref, res, 2e-2, "cos", 0.999)
+
+
+def test_mfma_peak_probe_reports_a_plausible_rate():
+    """The measured-peak reference of the benchmark: a sustained bf16 MFMA
+    loop on every CU lands between a third of and just above MI355X's dense
+    bf16 spec (2.5 PFLOP/s)."""
+    from paper_1811_06965_amd import gp
+    t = gp.gp_mfma_peak(torch.cuda.current_stream().cuda_stream)
+    assert 800.0 < t < 2700.0, t

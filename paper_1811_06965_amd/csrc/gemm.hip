@@ -549,6 +549,30 @@ __device__ __forceinline__ void dl_load_rsrcs(const Rsrc* g, const uint32_t* vo,
     for (int i = 0; i < P; ++i) __builtin_amdgcn_raw_ptr_buffer_load_lds(g[i], (LdsPtr)(dst + i * 1024), 16, vo[i], so, 0, 0);
 }
 
+// The direct loads of one k-tile that go out in k-step `part` of KS: load
+// slot q (PA A blocks, then PB B blocks, then F fp4 blocks, 1 KB each at the
+// wave's place in the stage) belongs to k-step q KS / LPW.
+template <int PA, int PB, int F, int LPW, int KS, int BM, int STAGE_BF>
+__device__ __forceinline__ void dl_issue_part(int part, Rsrc A, Rsrc B, const uint32_t* voa, const uint32_t* vob,
+                                              const Rsrc* R4, const uint32_t* vo4, int soa, int sob, int so4,
+                                              char* st, int wave) {
+#pragma unroll
+    for (int q = 0; q < LPW; ++q) {
+        if (q * KS / LPW != part) continue;
+        if (q < PA) {
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(A, (LdsPtr)(st + (wave * PA + q) * 1024), 16, voa[q < PA ? q : 0], soa, 0, 0);
+        } else if (q < PA + PB) {
+            const int b = q - PA;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(B, (LdsPtr)(st + BM * 128 + (wave * PB + b) * 1024), 16,
+                                                     vob[b < PB ? b : 0], sob, 0, 0);
+        } else if constexpr (F > 0) {
+            const int f = q - PA - PB;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(R4[f < F ? f : 0], (LdsPtr)(st + STAGE_BF + (wave * F + f) * 1024), 16,
+                                                     vo4[f < F ? f : 0], so4, 0, 0);
+        }
+    }
+}
+
 // Wave index as a wave-uniform (scalar) value, so LDS base addresses derived
 // from it stay in SGPRs (M0 of the direct loads).
 __device__ __forceinline__ int uniform_wave_id(int tid) { return __builtin_amdgcn_readfirstlane(tid >> 6); }
@@ -795,6 +819,17 @@ __global__ void __launch_bounds__(64 * WM * WN * KG) gemm_dl(GemmArgs args) {
         if constexpr (MX) dl_load_rsrcs<NL4>(R4, vo4, (t) * 32, (st) + STAGE_BF + wave * NL4 * 1024); \
     } while (0)
 
+    // Rings of 3+ stages spread a tile's direct loads over the KS k-steps of
+    // the tile after the one whose stage they refill: load slot q (A blocks,
+    // then B blocks, then fp4 blocks) goes out in k-step q KS / LPW.  Issued
+    // in one burst right after the barrier, the loads of all waves queued at
+    // the CU's texture unit together and held up the MFMAs behind them.
+    constexpr bool SPREAD = NSTAGE >= 3;
+#define GP_DL_ISSUE_PART(t, st, part)                                                                        \
+    dl_issue_part<PA, PB, (MX ? NL4 : 0), LPW, KS, BM, STAGE_BF>((part), A, B, voa, vob, R4, vo4,               \
+                                                                 (kt0 + ((t) - kt0) * KG) * ka,                  \
+                                                                 (kt0 + ((t) - kt0) * KG) * kb, (t) * 32, (st), wave)
+
     f32x16 acc[TM][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -898,6 +933,11 @@ __global__ void __launch_bounds__(64 * WM * WN * KG) gemm_dl(GemmArgs args) {
 #pragma unroll
                 for (int s = 0; s < KS; ++s) {
                     const int cur = s & 1;
+                    if constexpr (SPREAD) {
+                        // part s of tile i - 1 + NSTAGE, into the stage tile i - 1 left
+                        if (i >= 1 && i - 1 + NSTAGE < nkt)
+                            GP_DL_ISSUE_PART(kt0 + i - 1 + NSTAGE, smem + ((st + NSTAGE - 1) % NSTAGE) * STAGE, s);
+                    }
                     if constexpr (COLSUM) {
                         if (do_colsum) {
 #pragma unroll
@@ -919,7 +959,9 @@ __global__ void __launch_bounds__(64 * WM * WN * KG) gemm_dl(GemmArgs args) {
                         else
                             wait_vmcnt<0>();
                         lds_barrier();
-                        if (i + NSTAGE < nkt) GP_DL_ISSUE(kt0 + i + NSTAGE, smem + st * STAGE);
+                        if constexpr (!SPREAD) {
+                            if (i + NSTAGE < nkt) GP_DL_ISSUE(kt0 + i + NSTAGE, smem + st * STAGE);
+                        }
                         load_frags(cur ^ 1, nxt, 0);
                     }
                     i32x4 a4[MX ? TM : 1], b4[MX ? TN : 1];
@@ -954,6 +996,7 @@ __global__ void __launch_bounds__(64 * WM * WN * KG) gemm_dl(GemmArgs args) {
     }
 
 #undef GP_DL_ISSUE
+#undef GP_DL_ISSUE_PART
     if constexpr (KG == 2) {
         // group 1 hands its partial sums to group 0 through the (now idle) stage rings;
         // lane-fastest layout, so both the writes and the reads are conflict-free

@@ -32,6 +32,7 @@
 // transposed from the row-major LDS tile with the matching k order (two runs
 // of four consecutive rows per lane).  A workgroup holds 1, 2 or 4 waves,
 // chosen so that small micro-batches still launch enough workgroups.
+#include <cstdlib>
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -410,6 +411,13 @@ __global__ void __launch_bounds__(64 * KW) attn_bwd_dkv_mfma(AttnArgs a) {
 // workgroups for a small batch, at most 4 (fewer waves per workgroup re-stage
 // the head's keys and values more often).
 int waves_for(long row_blocks) {
+    // GP_ATTN_WAVES (1, 2 or 4) forces the waves per workgroup (tuning)
+    static const int forced = [] {
+        const char* e = std::getenv("GP_ATTN_WAVES");
+        const int v = e ? std::atoi(e) : 0;
+        return v == 1 || v == 2 || v == 4 ? v : 0;
+    }();
+    if (forced) return forced;
     constexpr long CU2 = 2 * 256;
     return row_blocks >= 4 * CU2 ? 4 : row_blocks >= 2 * CU2 ? 2 : 1;
 }

@@ -425,7 +425,7 @@ def main():
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": workload, "global_batch": cfg.batch, "seq_len": cfg.seq, "micro_batches": cfg.micro,
                    "parallelism": "one pipeline partition on one GPU"},
-        "hfu": r["hfu"], "mfu": r["mfu"],
+        "hfu": r["hfu"], "mfu": r["mfu"], "memory_bytes": r["memory_bytes"],
         "mfma_peak_measured_tflops": peak_meas * 1e-12, "hfu_measured_peak": r["hfu_measured_peak"],
         "roofline": roofline(r["role"], r["timed"], workload),
         "launch": "HIP graph: the whole step captured once, replayed" if a.graph else "eager (host-enqueued launches)",
@@ -439,7 +439,8 @@ def main():
         out["roles_note"] = f"census step with every launch bracketed; step time {step_ms:.2f} ms unbracketed"
     if a.sweep:
         out["sweep"] = [{k: v for k, v in results[M].items()
-                         if k in ("M", "ms_per_step", "tokens_per_s", "hfu", "mfu", "hfu_measured_peak")}
+                         if k in ("M", "ms_per_step", "tokens_per_s", "hfu", "mfu", "hfu_measured_peak",
+                                  "memory_bytes")}
                         for M in sorted(results)]
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, a.cpu_layers)

@@ -1427,7 +1427,31 @@ double split_weight() {
     return w;
 }
 
+void choose_dl_model(const GemmArgs& a, int epi, bool kmaj, int& cfg, int& splits);
+
+// The choice depends only on the problem's shape and operand form; a small
+// per-thread memo (direct-mapped, full key checked) keeps the cost model off
+// the launch path for the handful of shapes a partition launches repeatedly.
 void choose_dl(const GemmArgs& a, int epi, bool kmaj, int& cfg, int& splits) {
+    struct Entry { long long key[4]; int cfg, splits; bool used; };
+    static thread_local Entry memo[64] = {};
+    const long long key[4] = {((long long)a.M << 32) | (unsigned)a.N,
+                              ((long long)a.K << 32) | (unsigned)(epi | (kmaj ? 256 : 0) | (a.a4 ? 512 : 0) |
+                                                                   (a.colsum ? 1024 : 0) | (a.ws ? 2048 : 0)),
+                              (long long)a.ws_elems, 0};
+    unsigned long long h = 1469598103934665603ull;
+    for (long long k : key) h = (h ^ (unsigned long long)k) * 1099511628211ull;
+    Entry& e = memo[(h >> 20) & 63];
+    if (e.used && e.key[0] == key[0] && e.key[1] == key[1] && e.key[2] == key[2]) {
+        cfg = e.cfg;
+        splits = e.splits;
+        return;
+    }
+    choose_dl_model(a, epi, kmaj, cfg, splits);
+    e = Entry{{key[0], key[1], key[2], 0}, cfg, splits, true};
+}
+
+void choose_dl_model(const GemmArgs& a, int epi, bool kmaj, int& cfg, int& splits) {
     // the fp4 correction adds one MFMA of a quarter of the bf16 time per k-tile
     // and a quarter more tile traffic; only some shapes carry it
     const bool mx = a.a4 != nullptr;

@@ -1167,9 +1167,7 @@ enum TileCfg {
     T_DL128x64 = 15, T_DL64x128 = 16, T_DL128x64_S3 = 17,
     T_DL128x128_W8S4 = 18, T_DL128x64_S4 = 19, T_DL128x128_W8S3 = 20,  // deeper prefetch rings
     T_DL128x64_KG2 = 21, T_DL128x128_KG2 = 22, T_DL64x128_KG2 = 23,     // two k-groups (8 waves)
-    T_DL128x64_S6 = 24, T_DL128x128_W8S5 = 25, T_DL64x128_S6 = 26,
-    T_DL128x64_KG2W2 = 27, T_DL64x128_KG2W2 = 28,  // two k-groups of two 64 x 64 waves
-    T_LAST = T_DL64x128_KG2W2
+    T_LAST = T_DL64x128_KG2
 };
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
@@ -1350,19 +1348,6 @@ gp_status launch_bf16(const GemmArgs& a, int epi, int cfg, int splits, hipStream
         case T_DL128x128_W8S3: return launch_dl<128, 128, 2, 4, 3, KM>(a, epi, splits, st);
         case T_DL128x64_S4:
             if constexpr (KM) return launch_dl<128, 64, 2, 2, 4, KM>(a, epi, splits, st);
-            break;
-        case T_DL128x128_W8S5: return launch_dl<128, 128, 2, 4, 5, KM>(a, epi, splits, st);
-        case T_DL128x64_S6:
-            if constexpr (KM) return launch_dl<128, 64, 2, 2, 6, KM>(a, epi, splits, st);
-            break;
-        case T_DL64x128_S6:
-            if constexpr (KM) return launch_dl<64, 128, 2, 2, 6, KM>(a, epi, splits, st);
-            break;
-        case T_DL128x64_KG2W2:
-            if constexpr (KM) return launch_dl_kg2<128, 64, 2, 1, 3>(a, epi, st);
-            break;
-        case T_DL64x128_KG2W2:
-            if constexpr (KM) return launch_dl_kg2<64, 128, 1, 2, 3>(a, epi, st);
             break;
         case T_DL128x64_KG2:
             if constexpr (KM) return launch_dl_kg2<128, 64, 2, 2, 3>(a, epi, st);
@@ -1577,10 +1562,8 @@ gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dty
             if (splits > 1 && !split_fits(a, splits, (a.K + 63) / 64)) splits = 1;
         }
         if (cfg > T128x128 && a.K % 64) cfg = T128x128;
-        const bool narrow = cfg == T_DL128x64 || cfg == T_DL64x128 || cfg == T_DL128x64_S3 || cfg == T_DL128x64_S4 ||
-                            cfg == T_DL128x64_S6 || cfg == T_DL64x128_S6;
-        const bool kg2 = cfg == T_DL128x64_KG2 || cfg == T_DL128x128_KG2 || cfg == T_DL64x128_KG2 ||
-                         cfg == T_DL128x64_KG2W2 || cfg == T_DL64x128_KG2W2;
+        const bool narrow = cfg == T_DL128x64 || cfg == T_DL64x128 || cfg == T_DL128x64_S3 || cfg == T_DL128x64_S4;
+        const bool kg2 = cfg == T_DL128x64_KG2 || cfg == T_DL128x128_KG2 || cfg == T_DL64x128_KG2;
         if (!a_kmajor && (narrow || kg2)) cfg = T_DL128x128_W8A;  // no 64-wide or k-group m-contiguous tiles
         if (kg2 && (splits > 1 || (a.K / 64) % 2)) {               // k-groups: unsplit, even k-tile count
             cfg = T_DL128x64_S4;

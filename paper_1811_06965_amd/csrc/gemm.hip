@@ -1444,21 +1444,21 @@ void choose_dl_model(const GemmArgs& a, int epi, bool kmaj, int& cfg, int& split
     // per-k-tile time with 1, 2 or 3 tiles sharing a CU (0 = cannot share)
     struct Cand { int cfg, bm, bn, resident; double step[3]; };
     static const Cand kc[] = {  // k-contiguous operands
-        {T_DL256x256_W8, 256, 256, 1, {1.259, 0, 0}},    {T_DL256x128_W8, 256, 128, 1, {0.793, 0, 0}},
-        {T_DL128x256_W8, 128, 256, 1, {0.782, 0, 0}},    {T_DL128x128_W8A, 128, 128, 2, {0.508, 0.863, 0}},
-        {T_DL128x256_W8S3, 128, 256, 1, {0.748, 0, 0}},  {T_DL128x64, 128, 64, 3, {0.400, 0.539, 0.681}},
-        {T_DL64x128, 64, 128, 3, {0.391, 0.533, 0.680}}, {T_DL128x64_S3, 128, 64, 2, {0.263, 0.533, 0}},
-        {T_DL128x128_W8S4, 128, 128, 1, {0.440, 0, 0}},  {T_DL128x64_S4, 128, 64, 1, {0.307, 0, 0}},
-        {T_DL128x128_W8S3, 128, 128, 1, {0.419, 0, 0}}};
+        {T_DL256x256_W8, 256, 256, 1, {1.263, 0, 0}},    {T_DL256x128_W8, 256, 128, 1, {0.801, 0, 0}},
+        {T_DL128x256_W8, 128, 256, 1, {0.790, 0, 0}},    {T_DL128x128_W8A, 128, 128, 2, {0.511, 0.879, 0}},
+        {T_DL256x128_W8S3, 256, 128, 1, {0.688, 0, 0}},  {T_DL128x256_W8S3, 128, 256, 1, {0.682, 0, 0}},
+        {T_DL128x64, 128, 64, 3, {0.402, 0.561, 0.714}}, {T_DL64x128, 64, 128, 3, {0.398, 0.552, 0.712}},
+        {T_DL128x128_W8S4, 128, 128, 1, {0.410, 0, 0}},  {T_DL128x64_S4, 128, 64, 1, {0.320, 0, 0}},
+        {T_DL128x128_W8S3, 128, 128, 1, {0.402, 0, 0}}};
     static const Cand mc[] = {  // m/n-contiguous operands (weight gradients)
-        {T_DL256x256_W8, 256, 256, 1, {1.823, 0, 0}},    {T_DL256x128_W8, 256, 128, 1, {1.218, 0, 0}},
-        {T_DL128x256_W8, 128, 256, 1, {1.195, 0, 0}},    {T_DL128x128_W8A, 128, 128, 2, {0.778, 0.917, 0}},
-        {T_DL128x128_W8B, 128, 128, 2, {0.842, 0.964, 0}}, {T_DL256x128_W8S3, 256, 128, 1, {1.221, 0, 0}},
-        {T_DL128x256_W8S3, 128, 256, 1, {1.200, 0, 0}},  {T_DL128x128_W8S4, 128, 128, 1, {0.801, 0, 0}},
-        {T_DL128x128_W8S3, 128, 128, 1, {0.785, 0, 0}}};
+        {T_DL256x256_W8, 256, 256, 1, {1.865, 0, 0}},    {T_DL256x128_W8, 256, 128, 1, {1.256, 0, 0}},
+        {T_DL128x256_W8, 128, 256, 1, {1.236, 0, 0}},    {T_DL128x128_W8A, 128, 128, 2, {0.831, 0.940, 0}},
+        {T_DL128x128_W8B, 128, 128, 2, {0.898, 1.012, 0}}, {T_DL256x128_W8S3, 256, 128, 1, {1.350, 0, 0}},
+        {T_DL128x256_W8S3, 128, 256, 1, {1.335, 0, 0}},  {T_DL128x128_W8S4, 128, 128, 1, {1.040, 0, 0}},
+        {T_DL128x128_W8S3, 128, 128, 1, {1.049, 0, 0}}};
     const Cand* cands = kmaj ? kc : mc;
     const int ncand = kmaj ? (int)(sizeof(kc) / sizeof(kc[0])) : (int)(sizeof(mc) / sizeof(mc[0]));
-    const double c0 = kmaj ? 4.435 : 1.395, BW = kmaj ? 2.100e6 : 5.297e6, red0 = kmaj ? 3.367 : 7.255;
+    const double c0 = kmaj ? 4.147 : 0.0, BW = kmaj ? 1.969e6 : 5.084e6, red0 = kmaj ? 3.285 : 7.821;
     const int nk = a.K / 64;
     double best = 1e300;
     cfg = T_DL128x128_W8A;

@@ -180,6 +180,11 @@ struct gp_partition {
     // back-propagated, micro-batch m - 1 is re-materialised on a third stream
     // into the other workspace set.
     bool remat_ahead = true;
+    // Early recompute of the last micro-batch (GP_REMAT_EARLY=0 turns it off):
+    // its backward comes first, so its re-materialising forward is started on
+    // the recompute stream by the last forward call itself, right after the
+    // boundary input is stashed, and runs beside that forward.
+    bool remat_early = true;
     hipStream_t remat = nullptr;
     hipEvent_t remat_done = nullptr;  // from evring
     int remat_pending = -1;  // micro-batch whose recompute-ahead is enqueued
@@ -546,14 +551,17 @@ GP_TRY(timed_attention(c, GP_K_ATTN_FWD, a, false));
 // Forward of micro-batch m through all layers.  keep = false: first pass,
 // intermediates discarded (slot 0, ping-pong residuals); keep = true:
 // re-materialisation from the stash, intermediates kept per layer.
-gp_status partition_forward(const Ctx& c, int m, bool keep, const void* x, const void* mem, void* y, int set = 0) {
+gp_status partition_forward(const Ctx& c, int m, bool keep, const void* x, const void* mem, void* y, int set = 0,
+                            bool skip_intake = false) {
     gp_partition* p = c.p;
     const long T = p->g.T(), D = p->d.D;
     const int L = p->d.L;
     std::vector<float*>& xs = p->xs[set];
     if (!keep) {
-        GP_TRY(intake(c.dt, x, p->stash_x_mb(m), xs[0], T * D, c.st));
-        if (mem) GP_TRY(intake(c.dt, mem, p->stash_m_mb(m), nullptr, p->g.Tm() * D, c.st));
+        if (!skip_intake) {
+            GP_TRY(intake(c.dt, x, p->stash_x_mb(m), xs[0], T * D, c.st));
+            if (mem) GP_TRY(intake(c.dt, mem, p->stash_m_mb(m), nullptr, p->g.Tm() * D, c.st));
+        }
     } else {
         GP_TRY(intake(c.dt, p->stash_x_mb(m), nullptr, xs[0], T * D, c.st));
     }
@@ -787,6 +795,7 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
     if (const char* e = std::getenv("GP_TIMER_MARKERS")) p->timer.markers = std::atoi(e) != 0;
     if (const char* e = std::getenv("GP_SIDE_STREAM")) p->use_side = std::atoi(e) != 0;
     if (const char* e = std::getenv("GP_REMAT_AHEAD")) p->remat_ahead = std::atoi(e) != 0;
+    if (const char* e = std::getenv("GP_REMAT_EARLY")) p->remat_early = std::atoi(e) != 0;
     if (const char* e = std::getenv("GP_DW_FLUSH")) p->dw_flush = std::atoi(e);
     p->nsets = (p->remat_ahead && g.M >= 2) ? 2 : 1;
     if (const char* e = std::getenv("GP_GEMM_TILE")) p->gemm_tile = std::atoi(e);
@@ -958,7 +967,27 @@ gp_status gp_forward_microbatch(gp_partition* p, int mb, const void* x, const vo
     if (dec && !mem) return set_error(GP_ERR_INVALID_ARG, "decoder partitions need the memory input");
     if (!dec && mem) return set_error(GP_ERR_INVALID_ARG, "encoder partitions take no memory input");
     Ctx c = make_ctx(p, (hipStream_t)stream);
-    s = partition_forward(c, mb, false, x, mem, y);
+    // The last micro-batch's recompute goes into workspace set 1 (its backward
+    // comes first and uses set mb & 1); the first forward pass itself only
+    // uses slot 0 of set 0, so the two can run side by side.
+    const bool early = p->remat_early && p->nsets > 1 && mb == p->g.M - 1 && (mb & 1) == 1;
+    if (early) {
+        const long T = p->g.T(), D = p->d.D;
+        GP_TRY(intake(c.dt, x, p->stash_x_mb(mb), p->xs[0][0], T * D, c.st));
+        if (mem) GP_TRY(intake(c.dt, mem, p->stash_m_mb(mb), nullptr, p->g.Tm() * D, c.st));
+        const hipEvent_t fork = p->next_event();
+        GP_HIP(hipEventRecord(fork, c.st));
+        Ctx cr = make_ctx(p, p->remat, Lane::Remat);
+        GP_HIP(hipStreamWaitEvent(cr.st, fork, 0));
+        s = partition_forward(cr, mb, true, nullptr, nullptr, nullptr, 1);
+        if (s != GP_OK) return s;
+        p->remat_done = p->next_event();
+        GP_HIP(hipEventRecord(p->remat_done, cr.st));
+        p->remat_pending = mb;
+        s = partition_forward(c, mb, false, x, mem, y, 0, true);
+    } else {
+        s = partition_forward(c, mb, false, x, mem, y);
+    }
     if (s != GP_OK) return s;
     p->sched.did_forward();
     return GP_OK;

@@ -173,17 +173,20 @@ __global__ void __launch_bounds__(64 * QW) attn_fwd_mfma(AttnArgs a) {
     const int bh = xcd_work(&blk), b = bh / a.H, hh = bh % a.H;
     const bf16* K = reinterpret_cast<const bf16*>(a.k) + (long)b * a.Sk * a.ldk + hh * DH;
     const bf16* V = reinterpret_cast<const bf16*>(a.v) + (long)b * a.Sk * a.ldv + hh * DH;
+    // this wave's queries are fetched while the keys and values stream into LDS
+    const int q0 = (blk * QW + wave) * 32;
+    const int q = q0 + (lane & 31);
+    bf16x8 qf[4];
+    if (q0 < a.Sq) {
+        const bf16* Qrow = reinterpret_cast<const bf16*>(a.q) + ((long)b * a.Sq + q) * a.ldq + hh * DH;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) qf[s] = frag_global(Qrow, s, lane);
+    }
     stage_dl<NKB * 32, QW>(Ks, K, a.ldk, wave, lane);
     stage_dl<NKB * 32, QW>(Vs, V, a.ldv, wave, lane);
     wait_loads();
     __syncthreads();
-    const int q0 = (blk * QW + wave) * 32;
     if (q0 >= a.Sq) return;
-    const int q = q0 + (lane & 31);
-    const bf16* Qrow = reinterpret_cast<const bf16*>(a.q) + ((long)b * a.Sq + q) * a.ldq + hh * DH;
-    bf16x8 qf[4];
-#pragma unroll
-    for (int s = 0; s < 4; ++s) qf[s] = frag_global(Qrow, s, lane);
     // key blocks at or below the diagonal (causal), else all
     const int nkb = CAUSAL ? min(NKB, q0 / 32 + 1) : NKB;
     f32x16 sc[NKB];
@@ -234,6 +237,102 @@ __global__ void __launch_bounds__(64 * QW) attn_fwd_mfma(AttnArgs a) {
     if (a.lse && lane < 32) a.lse[(long)bh * a.Sq + q] = m * a.scale + logf(sum);
 }
 
+// Forward with the keys split in two halves (non-causal, even key-block
+// count): 2 QW waves per workgroup, wave w takes query block w % QW and key
+// half w / QW.  Each wave runs the softmax over its half with its own running
+// maximum and sum and an unnormalised output; the second half's wave hands
+// (O, m, sum) to the first through LDS (the K/V tiles' space once every wave
+// is done with them), which rescales both to the common maximum, normalises
+// and stores.  Twice the waves of attn_fwd_mfma on the same LDS, each with
+// half the serial work.
+template <int NKB, int QW>
+__global__ void __launch_bounds__(128 * QW) attn_fwd_ks(AttnArgs a) {
+    static_assert(NKB % 2 == 0, "key halves");
+    constexpr int HB = NKB / 2;
+    constexpr int KVB = NKB * 32 * 128, XB = QW * 64 * 34 * 4;
+    __shared__ __attribute__((aligned(1024))) char KV[2 * KVB > XB ? 2 * KVB : XB];
+    char* const Ks = KV;
+    char* const Vs = KV + KVB;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int half = wave / QW, qw = wave % QW;
+    int blk;
+    const int bh = xcd_work(&blk), b = bh / a.H, hh = bh % a.H;
+    const bf16* K = reinterpret_cast<const bf16*>(a.k) + (long)b * a.Sk * a.ldk + hh * DH;
+    const bf16* V = reinterpret_cast<const bf16*>(a.v) + (long)b * a.Sk * a.ldv + hh * DH;
+    const int q0 = (blk * QW + qw) * 32;
+    const bool live = q0 < a.Sq;  // every wave takes part in all three barriers
+    const int q = q0 + (lane & 31);
+    bf16x8 qf[4];
+    if (live) {
+        const bf16* Qrow = reinterpret_cast<const bf16*>(a.q) + ((long)b * a.Sq + q) * a.ldq + hh * DH;
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2) qf[s2] = frag_global(Qrow, s2, lane);
+    }
+    stage_dl<NKB * 32, 2 * QW>(Ks, K, a.ldk, wave, lane);
+    stage_dl<NKB * 32, 2 * QW>(Vs, V, a.ldv, wave, lane);
+    wait_loads();
+    __syncthreads();
+    const float c = a.scale * LOG2E;
+    f32x16 o[2] = {zero16(), zero16()};
+    float m = -INFINITY, sum = 0.f;
+    if (live) {
+        f32x16 sc[HB];
+#pragma unroll
+        for (int j = 0; j < HB; ++j) {
+            const int kb = half * HB + j;
+            sc[j] = zero16();
+#pragma unroll
+            for (int s2 = 0; s2 < 4; ++s2) sc[j] = mfma(frag_rows(Ks, kb * 32, s2, lane), qf[s2], sc[j]);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) m = fmaxf(m, sc[j][r]);
+        }
+        m = fmaxf(m, __shfl_xor(m, 32, 64));
+        const float mc = m * c;
+#pragma unroll
+        for (int j = 0; j < HB; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const float pv = exp2_hw(fmaf(sc[j][r], c, -mc));
+                sc[j][r] = pv;
+                sum += pv;
+            }
+        sum += __shfl_xor(sum, 32, 64);
+#pragma unroll
+        for (int j = 0; j < HB; ++j) {
+            const int kb = half * HB + j;
+#pragma unroll
+            for (int cc = 0; cc < 2; ++cc) {
+                const bf16x8 pf = pack_chunk(sc[j], cc);
+#pragma unroll
+                for (int db = 0; db < 2; ++db) o[db] = mfma(frag_tr(Vs, db * 32, kb * 32 + cc * 16, lane), pf, o[db]);
+            }
+        }
+    }
+    __syncthreads();  // K and V are no longer read: their space carries the hand-over
+    float* xo = reinterpret_cast<float*>(KV) + (qw * 64 + lane) * 34;
+    if (half == 1 && live) {
+#pragma unroll
+        for (int db = 0; db < 2; ++db)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) xo[db * 16 + r] = o[db][r];
+        xo[32] = m;
+        xo[33] = sum;
+    }
+    __syncthreads();
+    if (half == 1 || !live) return;
+    const float m1 = xo[32], s1 = xo[33];
+    const float mn = fmaxf(m, m1);
+    const float a0 = exp2_hw((m - mn) * c), a1 = exp2_hw((m1 - mn) * c);
+#pragma unroll
+    for (int db = 0; db < 2; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[db][r] = o[db][r] * a0 + xo[db * 16 + r] * a1;
+    const float tot = sum * a0 + s1 * a1;
+    bf16* O = reinterpret_cast<bf16*>(a.o) + ((long)b * a.Sq + q0) * a.ldo + hh * DH;
+    store_t(O, a.ldo, o, 1.f / tot, lane);
+    if (a.lse && lane < 32) a.lse[(long)bh * a.Sq + q] = mn * a.scale + logf(tot);
+}
+
 // dQ pass: QW waves per workgroup, 32 queries each; also writes delta.
 template <int NKB, int QW, bool CAUSAL>
 __global__ void __launch_bounds__(64 * QW) attn_bwd_dq_mfma(AttnArgs a) {
@@ -244,24 +343,30 @@ __global__ void __launch_bounds__(64 * QW) attn_bwd_dq_mfma(AttnArgs a) {
     const int bh = xcd_work(&blk), b = bh / a.H, hh = bh % a.H;
     const bf16* K = reinterpret_cast<const bf16*>(a.k) + (long)b * a.Sk * a.ldk + hh * DH;
     const bf16* V = reinterpret_cast<const bf16*>(a.v) + (long)b * a.Sk * a.ldv + hh * DH;
+    // this wave's queries, output gradients and LSE are fetched while the
+    // keys and values stream into LDS
+    const int q0 = (blk * QW + wave) * 32;
+    const int q = q0 + (lane & 31);
+    bf16x8 qf[4], gf[4];
+    float lse = 0.f;
+    if (q0 < a.Sq) {
+        const long qrow = (long)b * a.Sq + q;
+        const bf16* Qrow = reinterpret_cast<const bf16*>(a.q) + qrow * a.ldq + hh * DH;
+        const bf16* dOrow = reinterpret_cast<const bf16*>(a.dout) + qrow * a.lddo + hh * DH;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            qf[s] = frag_global(Qrow, s, lane);
+            gf[s] = frag_global(dOrow, s, lane);
+        }
+        lse = a.lse[(long)bh * a.Sq + q];
+    }
     stage_dl<NKB * 32, QW>(Ks, K, a.ldk, wave, lane);
     stage_dl<NKB * 32, QW>(Vs, V, a.ldv, wave, lane);
     wait_loads();
     __syncthreads();
-    const int q0 = (blk * QW + wave) * 32;
     if (q0 >= a.Sq) return;
-    const int q = q0 + (lane & 31);
-    const long qrow = (long)b * a.Sq + q;
-    const bf16* Qrow = reinterpret_cast<const bf16*>(a.q) + qrow * a.ldq + hh * DH;
-    const bf16* dOrow = reinterpret_cast<const bf16*>(a.dout) + qrow * a.lddo + hh * DH;
-    bf16x8 qf[4], gf[4];
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-        qf[s] = frag_global(Qrow, s, lane);
-        gf[s] = frag_global(dOrow, s, lane);
-    }
     const float c = a.scale * LOG2E;
-    const float lse2 = a.lse[(long)bh * a.Sq + q] * LOG2E;
+    const float lse2 = lse * LOG2E;
     const int nkb = CAUSAL ? min(NKB, q0 / 32 + 1) : NKB;
     // delta = sum_j P_ij dP_ij; lanes l and l + 32 hold the two key halves of a block
     float dpart = 0.f;
@@ -320,6 +425,21 @@ __global__ void __launch_bounds__(64 * KW) attn_bwd_dkv_mfma(AttnArgs a) {
     const int Sq = NQB * 32;
     const bf16* Q = reinterpret_cast<const bf16*>(a.q) + (long)b * a.Sq * a.ldq + hh * DH;
     const bf16* G = reinterpret_cast<const bf16*>(a.dout) + (long)b * a.Sq * a.lddo + hh * DH;
+    // this wave's keys and values are fetched while the queries and output
+    // gradients stream into LDS
+    const int k0 = (blk * KW + wave) * 32;
+    const int key = k0 + (lane & 31);
+    bf16x8 kf[4], vf[4];
+    if (k0 < a.Sk) {
+        const long krow = (long)b * a.Sk + key;
+        const bf16* Krow = reinterpret_cast<const bf16*>(a.k) + krow * a.ldk + hh * DH;
+        const bf16* Vrow = reinterpret_cast<const bf16*>(a.v) + krow * a.ldv + hh * DH;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            kf[s] = frag_global(Krow, s, lane);
+            vf[s] = frag_global(Vrow, s, lane);
+        }
+    }
     stage_dl<NQB * 32, KW>(Qs, Q, a.ldq, wave, lane);
     stage_dl<NQB * 32, KW>(Gs, G, a.lddo, wave, lane);
     for (int i = tid; i < Sq; i += 64 * KW) {
@@ -328,18 +448,7 @@ __global__ void __launch_bounds__(64 * KW) attn_bwd_dkv_mfma(AttnArgs a) {
     }
     wait_loads();
     __syncthreads();
-    const int k0 = (blk * KW + wave) * 32;
     if (k0 >= a.Sk) return;
-    const int key = k0 + (lane & 31);
-    const long krow = (long)b * a.Sk + key;
-    const bf16* Krow = reinterpret_cast<const bf16*>(a.k) + krow * a.ldk + hh * DH;
-    const bf16* Vrow = reinterpret_cast<const bf16*>(a.v) + krow * a.ldv + hh * DH;
-    bf16x8 kf[4], vf[4];
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-        kf[s] = frag_global(Krow, s, lane);
-        vf[s] = frag_global(Vrow, s, lane);
-    }
     const float c = a.scale * LOG2E;
     f32x16 dk[2] = {zero16(), zero16()}, dv[2] = {zero16(), zero16()};
     const int qb0 = CAUSAL ? k0 / 32 : 0;
@@ -377,6 +486,220 @@ __global__ void __launch_bounds__(64 * KW) attn_bwd_dkv_mfma(AttnArgs a) {
             }
         }
     }
+    bf16* dK = reinterpret_cast<bf16*>(a.dk) + ((long)b * a.Sk + k0) * a.lddk + hh * DH;
+    bf16* dV = reinterpret_cast<bf16*>(a.dv) + ((long)b * a.Sk + k0) * a.lddv + hh * DH;
+    store_t(dK, a.lddk, dk, a.scale, lane);
+    store_t(dV, a.lddv, dv, 1.f, lane);
+}
+
+// dQ pass with the keys split in two halves (non-causal, even key-block
+// count): 2 QW waves per workgroup, wave w takes query block w % QW and key
+// half w / QW.  The two waves of a query block exchange their partial delta
+// through LDS (both add the halves in the same order, so both hold the same
+// delta), then each runs dS and dQ over its half; the second half's wave hands
+// its dQ partial to the first, which adds it and stores.  Halves the serial
+// chain of each wave.
+template <int NKB, int QW>
+__global__ void __launch_bounds__(128 * QW) attn_bwd_dq_ks(AttnArgs a) {
+    static_assert(NKB % 2 == 0, "key halves");
+    constexpr int HB = NKB / 2;
+    constexpr int KVB = NKB * 32 * 128, XB = QW * 64 * 32 * 4;
+    __shared__ __attribute__((aligned(1024))) char KV[2 * KVB > XB ? 2 * KVB : XB];
+    __shared__ float xd[2 * QW * 64];
+    char* const Ks = KV;
+    char* const Vs = KV + KVB;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int half = wave / QW, qw = wave % QW;
+    int blk;
+    const int bh = xcd_work(&blk), b = bh / a.H, hh = bh % a.H;
+    const bf16* K = reinterpret_cast<const bf16*>(a.k) + (long)b * a.Sk * a.ldk + hh * DH;
+    const bf16* V = reinterpret_cast<const bf16*>(a.v) + (long)b * a.Sk * a.ldv + hh * DH;
+    const int q0 = (blk * QW + qw) * 32;
+    const bool live = q0 < a.Sq;  // every wave takes part in all four barriers
+    const int q = q0 + (lane & 31);
+    bf16x8 qf[4], gf[4];
+    float lse = 0.f;
+    if (live) {
+        const long qrow = (long)b * a.Sq + q;
+        const bf16* Qrow = reinterpret_cast<const bf16*>(a.q) + qrow * a.ldq + hh * DH;
+        const bf16* dOrow = reinterpret_cast<const bf16*>(a.dout) + qrow * a.lddo + hh * DH;
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2) {
+            qf[s2] = frag_global(Qrow, s2, lane);
+            gf[s2] = frag_global(dOrow, s2, lane);
+        }
+        lse = a.lse[(long)bh * a.Sq + q];
+    }
+    stage_dl<NKB * 32, 2 * QW>(Ks, K, a.ldk, wave, lane);
+    stage_dl<NKB * 32, 2 * QW>(Vs, V, a.ldv, wave, lane);
+    wait_loads();
+    __syncthreads();
+    const float c = a.scale * LOG2E;
+    const float lse2 = lse * LOG2E;
+    const int kb0 = half * HB;
+    // partial delta = sum over this half's keys of P dP
+    float dpart = 0.f;
+    if (live) {
+#pragma unroll 2
+        for (int j = 0; j < HB; ++j) {
+            const int kb = kb0 + j;
+            f32x16 st = zero16(), dp = zero16();
+#pragma unroll
+            for (int s2 = 0; s2 < 4; ++s2) {
+                st = mfma(frag_rows(Ks, kb * 32, s2, lane), qf[s2], st);
+                dp = mfma(frag_rows(Vs, kb * 32, s2, lane), gf[s2], dp);
+            }
+#pragma unroll
+            for (int r = 0; r < 16; ++r) dpart = fmaf(exp2_hw(fmaf(st[r], c, -lse2)), dp[r], dpart);
+        }
+        dpart += __shfl_xor(dpart, 32, 64);
+    }
+    xd[wave * 64 + lane] = dpart;
+    __syncthreads();
+    const float delta = xd[qw * 64 + lane] + xd[(QW + qw) * 64 + lane];
+    f32x16 dq[2] = {zero16(), zero16()};
+    if (live) {
+#pragma unroll 2
+        for (int j = 0; j < HB; ++j) {
+            const int kb = kb0 + j;
+            f32x16 st = zero16(), dp = zero16();
+#pragma unroll
+            for (int s2 = 0; s2 < 4; ++s2) {
+                st = mfma(frag_rows(Ks, kb * 32, s2, lane), qf[s2], st);
+                dp = mfma(frag_rows(Vs, kb * 32, s2, lane), gf[s2], dp);
+            }
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const float p = exp2_hw(fmaf(st[r], c, -lse2));
+                st[r] = fmaf(p, dp[r], -p * delta);
+            }
+#pragma unroll
+            for (int cc = 0; cc < 2; ++cc) {
+                const bf16x8 df = pack_chunk(st, cc);
+#pragma unroll
+                for (int db = 0; db < 2; ++db) dq[db] = mfma(frag_tr(Ks, db * 32, kb * 32 + cc * 16, lane), df, dq[db]);
+            }
+        }
+    }
+    __syncthreads();  // K and V are no longer read: their space carries the hand-over
+    float* xo = reinterpret_cast<float*>(KV) + (qw * 32) * 64 + lane;  // register-major, lane fastest
+    if (half == 1 && live) {
+#pragma unroll
+        for (int db = 0; db < 2; ++db)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) xo[(db * 16 + r) * 64] = dq[db][r];
+    }
+    __syncthreads();
+    if (half == 1 || !live) return;
+#pragma unroll
+    for (int db = 0; db < 2; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) dq[db][r] += xo[(db * 16 + r) * 64];
+    bf16* dQ = reinterpret_cast<bf16*>(a.dq) + ((long)b * a.Sq + q0) * a.lddq + hh * DH;
+    store_t(dQ, a.lddq, dq, a.scale, lane);
+    if (lane < 32) a.delta[(long)bh * a.Sq + q] = delta;
+}
+
+// dK/dV pass with the queries split in two halves (non-causal, even
+// query-block count): 2 KW waves per workgroup, wave w takes key block w % KW
+// and query half w / KW; the second half's wave hands its dK and dV partials
+// to the first through LDS, which adds them and stores.
+template <int NQB, int KW>
+__global__ void __launch_bounds__(128 * KW) attn_bwd_dkv_ks(AttnArgs a) {
+    static_assert(NQB % 2 == 0, "query halves");
+    constexpr int HQ = NQB / 2;
+    constexpr int QGB = NQB * 32 * 128, XB = KW * 64 * 64 * 4;
+    __shared__ __attribute__((aligned(1024))) char QG[2 * QGB > XB ? 2 * QGB : XB];
+    __shared__ __attribute__((aligned(16))) float lse2s[NQB * 32], dls[NQB * 32];
+    char* const Qs = QG;
+    char* const Gs = QG + QGB;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int half = wave / KW, kw = wave % KW;
+    int blk;
+    const int bh = xcd_work(&blk), b = bh / a.H, hh = bh % a.H;
+    const int Sq = NQB * 32;
+    const bf16* Q = reinterpret_cast<const bf16*>(a.q) + (long)b * a.Sq * a.ldq + hh * DH;
+    const bf16* G = reinterpret_cast<const bf16*>(a.dout) + (long)b * a.Sq * a.lddo + hh * DH;
+    const int k0 = (blk * KW + kw) * 32;
+    const bool live = k0 < a.Sk;  // every wave takes part in all three barriers
+    const int key = k0 + (lane & 31);
+    bf16x8 kf[4], vf[4];
+    if (live) {
+        const long krow = (long)b * a.Sk + key;
+        const bf16* Krow = reinterpret_cast<const bf16*>(a.k) + krow * a.ldk + hh * DH;
+        const bf16* Vrow = reinterpret_cast<const bf16*>(a.v) + krow * a.ldv + hh * DH;
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2) {
+            kf[s2] = frag_global(Krow, s2, lane);
+            vf[s2] = frag_global(Vrow, s2, lane);
+        }
+    }
+    stage_dl<NQB * 32, 2 * KW>(Qs, Q, a.ldq, wave, lane);
+    stage_dl<NQB * 32, 2 * KW>(Gs, G, a.lddo, wave, lane);
+    for (int i = tid; i < Sq; i += 128 * KW) {
+        lse2s[i] = a.lse[(long)bh * a.Sq + i] * LOG2E;
+        dls[i] = a.delta[(long)bh * a.Sq + i];
+    }
+    wait_loads();
+    __syncthreads();
+    const float c = a.scale * LOG2E;
+    f32x16 dk[2] = {zero16(), zero16()}, dv[2] = {zero16(), zero16()};
+    if (live) {
+        for (int j = 0; j < HQ; ++j) {
+            const int qb = half * HQ + j;
+            f32x16 st = zero16(), dp = zero16();
+#pragma unroll
+            for (int s2 = 0; s2 < 4; ++s2) {
+                st = mfma(frag_rows(Qs, qb * 32, s2, lane), kf[s2], st);
+                dp = mfma(frag_rows(Gs, qb * 32, s2, lane), vf[s2], dp);
+            }
+            // this lane's rows of the block: 8 i + 4 (lane/32) + {0..3}, i = 0..3
+            f32x4 l4[4], d4[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int r0 = qb * 32 + 8 * i + 4 * (lane >> 5);
+                l4[i] = *reinterpret_cast<const f32x4*>(lse2s + r0);
+                d4[i] = *reinterpret_cast<const f32x4*>(dls + r0);
+            }
+            f32x16 pm;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const float p = exp2_hw(fmaf(st[r], c, -l4[r >> 2][r & 3]));
+                pm[r] = p;
+                st[r] = fmaf(p, dp[r], -p * d4[r >> 2][r & 3]);
+            }
+#pragma unroll
+            for (int cc = 0; cc < 2; ++cc) {
+                const bf16x8 pf = pack_chunk(pm, cc);
+                const bf16x8 df = pack_chunk(st, cc);
+#pragma unroll
+                for (int db = 0; db < 2; ++db) {
+                    dv[db] = mfma(frag_tr(Gs, db * 32, qb * 32 + cc * 16, lane), pf, dv[db]);
+                    dk[db] = mfma(frag_tr(Qs, db * 32, qb * 32 + cc * 16, lane), df, dk[db]);
+                }
+            }
+        }
+    }
+    __syncthreads();  // Q and dO are no longer read: their space carries the hand-over
+    float* xo = reinterpret_cast<float*>(QG) + (kw * 64) * 64 + lane;  // register-major, lane fastest
+    if (half == 1 && live) {
+#pragma unroll
+        for (int db = 0; db < 2; ++db)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                xo[(db * 16 + r) * 64] = dk[db][r];
+                xo[(32 + db * 16 + r) * 64] = dv[db][r];
+            }
+    }
+    __syncthreads();
+    if (half == 1 || !live) return;
+#pragma unroll
+    for (int db = 0; db < 2; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            dk[db][r] += xo[(db * 16 + r) * 64];
+            dv[db][r] += xo[(32 + db * 16 + r) * 64];
+        }
     bf16* dK = reinterpret_cast<bf16*>(a.dk) + ((long)b * a.Sk + k0) * a.lddk + hh * DH;
     bf16* dV = reinterpret_cast<bf16*>(a.dv) + ((long)b * a.Sk + k0) * a.lddv + hh * DH;
     store_t(dK, a.lddk, dk, a.scale, lane);
@@ -422,6 +745,39 @@ int waves_for(long row_blocks) {
     return row_blocks >= 4 * CU2 ? 4 : row_blocks >= 2 * CU2 ? 2 : 1;
 }
 
+// Split variants (two waves per 32-row block, each over half of the loop's
+// blocks): non-causal heads whose loop runs over an even block count, when
+// the row blocks alone would leave a SIMD with at most one wave (there the
+// one-wave kernels' serial chain sets the time; with more row blocks the two
+// forms tie or the split loses to the doubled wave count).
+// GP_ATTN_KSPLIT=0 keeps the one-wave kernels.
+bool split_ok(const AttnArgs& a, long row_blocks, int loop_blocks) {
+    static const bool on = [] {
+        const char* e = std::getenv("GP_ATTN_KSPLIT");
+        return !e || std::atoi(e) != 0;
+    }();
+    constexpr long SIMDS = 4 * 256;
+    return on && !a.causal && loop_blocks % 2 == 0 && row_blocks <= SIMDS;
+}
+
+// Launch KERNEL<NB, W> (split variants: 128 W threads) for an even block count NB <= 8.
+#define GP_KS_SWITCH(NB, W, KERNEL, GRID)                                                      \
+    switch ((NB) * 8 + (W)) {                                                                  \
+    case 2 * 8 + 1: klaunch(KERNEL<2, 1>, GRID, 128, 0, st, a); break;                         \
+    case 2 * 8 + 2: klaunch(KERNEL<2, 2>, GRID, 256, 0, st, a); break;                         \
+    case 2 * 8 + 4: klaunch(KERNEL<2, 4>, GRID, 512, 0, st, a); break;                         \
+    case 4 * 8 + 1: klaunch(KERNEL<4, 1>, GRID, 128, 0, st, a); break;                         \
+    case 4 * 8 + 2: klaunch(KERNEL<4, 2>, GRID, 256, 0, st, a); break;                         \
+    case 4 * 8 + 4: klaunch(KERNEL<4, 4>, GRID, 512, 0, st, a); break;                         \
+    case 6 * 8 + 1: klaunch(KERNEL<6, 1>, GRID, 128, 0, st, a); break;                         \
+    case 6 * 8 + 2: klaunch(KERNEL<6, 2>, GRID, 256, 0, st, a); break;                         \
+    case 6 * 8 + 4: klaunch(KERNEL<6, 4>, GRID, 512, 0, st, a); break;                         \
+    case 8 * 8 + 1: klaunch(KERNEL<8, 1>, GRID, 128, 0, st, a); break;                         \
+    case 8 * 8 + 2: klaunch(KERNEL<8, 2>, GRID, 256, 0, st, a); break;                         \
+    case 8 * 8 + 4: klaunch(KERNEL<8, 4>, GRID, 512, 0, st, a); break;                         \
+    default: return set_error(GP_ERR_UNSUPPORTED, "attention: sequence length > 256");         \
+    }
+
 bool mfma_ok(const AttnArgs& a) {
     return a.dh == DH && a.Sq % 32 == 0 && a.Sk % 32 == 0 && a.Sq <= MAXK && a.Sk <= MAXK &&
            a.ldq % 8 == 0 && a.ldk % 8 == 0 && a.ldv % 8 == 0 && a.ldo % 8 == 0;
@@ -434,7 +790,11 @@ gp_status attention_fwd(int dtype, const AttnArgs& a, hipStream_t st) {
     if (!mfma_ok(a)) return set_error(GP_ERR_UNSUPPORTED, "bf16 attention needs d_h = 64 and lengths multiple of 32, <= 256");
     const int w = waves_for((long)(a.Sq / 32) * a.n * a.H);
     dim3 grid((a.Sq + 32 * w - 1) / (32 * w), a.n * a.H);
-    GP_WC_SWITCH(a.Sk / 32, w, a.causal, attn_fwd_mfma, grid);
+    if (split_ok(a, (long)(a.Sq / 32) * a.n * a.H, a.Sk / 32)) {
+        GP_KS_SWITCH(a.Sk / 32, w, attn_fwd_ks, grid);
+    } else {
+        GP_WC_SWITCH(a.Sk / 32, w, a.causal, attn_fwd_mfma, grid);
+    }
     GP_LAUNCH_CHECK();
     return GP_OK;
 }
@@ -444,11 +804,19 @@ gp_status attention_bwd(int dtype, const AttnArgs& a, hipStream_t st) {
     if (!mfma_ok(a)) return set_error(GP_ERR_UNSUPPORTED, "bf16 attention needs d_h = 64 and lengths multiple of 32, <= 256");
     const int wq = waves_for((long)(a.Sq / 32) * a.n * a.H);
     dim3 gq((a.Sq + 32 * wq - 1) / (32 * wq), a.n * a.H);
-    GP_WC_SWITCH(a.Sk / 32, wq, a.causal, attn_bwd_dq_mfma, gq);
+    if (split_ok(a, (long)(a.Sq / 32) * a.n * a.H, a.Sk / 32)) {
+        GP_KS_SWITCH(a.Sk / 32, wq, attn_bwd_dq_ks, gq);
+    } else {
+        GP_WC_SWITCH(a.Sk / 32, wq, a.causal, attn_bwd_dq_mfma, gq);
+    }
     GP_LAUNCH_CHECK();
     const int wk = waves_for((long)(a.Sk / 32) * a.n * a.H);
     dim3 gk((a.Sk + 32 * wk - 1) / (32 * wk), a.n * a.H);
-    GP_WC_SWITCH(a.Sq / 32, wk, a.causal, attn_bwd_dkv_mfma, gk);
+    if (split_ok(a, (long)(a.Sk / 32) * a.n * a.H, a.Sq / 32)) {
+        GP_KS_SWITCH(a.Sq / 32, wk, attn_bwd_dkv_ks, gk);
+    } else {
+        GP_WC_SWITCH(a.Sq / 32, wk, a.causal, attn_bwd_dkv_mfma, gk);
+    }
     GP_LAUNCH_CHECK();
     return GP_OK;
 }

@@ -10,13 +10,12 @@ One step = M x gp_forward_microbatch + M x gp_backward_microbatch_remat +
 gp_accumulate_and_step (GPipe, Sections 2.2-2.3), enqueued on the caller's
 stream (the library runs the weight-gradient GEMMs on a second stream it
 joins before each call returns).  W untimed warm-up steps, one untimed census
-step that times every launch role to find the dominant one, then K steps
-timed between two events on the launch stream.  By default the step is
-captured once into a HIP graph and the K steps are graph replays (the launch
-overhead of thousands of small kernels per step is then off the host); the
-dominant role's launches are then timed with dispatch events over a few eager
-steps right after.  --eager times eager steps with the role bracketed inside
-the timed region.  Prints one JSON line.
+step that times every launch role to find the dominant one, then K eager
+steps timed between two events on the launch stream, with one launch in
+TIMER_EVERY of the dominant role bracketed by dispatch events inside the timed
+region.  --graph captures the step once into a HIP graph and times K replays
+instead (the role is then timed over a few eager steps right after).  Prints
+one JSON line.
 """
 import argparse
 import hashlib
@@ -240,12 +239,20 @@ def dominant_role(roles):
     return max(tied)[1]
 
 
+# One launch in this many of the timed role is bracketed by dispatch events
+# inside the timed region (each bracket holds the next launch back by a few
+# microseconds; bracketing all 256 ffn2.fwd launches of an M = 8 step cost
+# 0.6-0.7 ms of it).
+TIMER_EVERY = 8
+
+
 def timed_eager(part, inp, steps, dx, role):
-    """K eager steps between two events on the launch stream, with the role's
-    launches bracketed by dispatch events."""
+    """K eager steps between two events on the launch stream, with every
+    TIMER_EVERY-th launch of the role bracketed by dispatch events."""
     import torch
     st = torch.cuda.current_stream()
     part.timer_reset()
+    part.timer_sample(TIMER_EVERY)
     part.timer_select(role)
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
@@ -257,6 +264,7 @@ def timed_eager(part, inp, steps, dx, role):
     part.timer_select(None)
     timed = part.timer_read(role)
     part.timer_reset()
+    part.timer_sample(1)
     return t0.elapsed_time(t1) / steps, timed
 
 
@@ -290,10 +298,11 @@ def time_steps(part, inp, steps, warmup, role=None, graph=False):
         role = dominant_role(roles)
     if not graph:
         ms, timed = timed_eager(part, inp, steps, dx, role)
-        return ms, role, timed, roles, "dispatch events over the timed eager steps"
+        return ms, role, timed, roles, f"dispatch events on every {TIMER_EVERY}th launch over the timed eager steps"
     ms = timed_graph(part, inp, steps, dx)
     _, timed = timed_eager(part, inp, max(1, min(steps, 3)), dx, role)
-    return ms, role, timed, roles, "dispatch events over eager steps run after the graph-replay timed region"
+    return ms, role, timed, roles, (f"dispatch events on every {TIMER_EVERY}th launch over eager steps run after "
+                                    "the graph-replay timed region")
 
 
 def source_digest():

@@ -241,6 +241,13 @@ typedef enum {
  * GP_ERR_INVALID_ARG: role out of range. */
 gp_status gp_timer_select(gp_partition* p, int role);
 
+/* Time one launch in `every` of the selected role(s): launches 0, every,
+ * 2 every, ... since the last reset are bracketed, the others run without
+ * events (default 1: every launch).  Keeps the events' own cost out of most
+ * launches of a timed region; the recorded totals then cover the sampled
+ * launches only.  GP_ERR_INVALID_ARG: NULL partition or every < 1. */
+gp_status gp_timer_sample(gp_partition* p, int every);
+
 /* Totals of one role over the launches recorded since the last reset: summed
  * event-to-event milliseconds, launch count, algorithmic FLOPs and bytes.
  * Waits for the role's last recorded event.  Any output pointer may be NULL. */

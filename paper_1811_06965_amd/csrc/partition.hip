@@ -102,6 +102,8 @@ using namespace gp;
 struct LaunchTimer {
     int selected = GP_K_NONE;
     bool markers = false;  // GP_TIMER_MARKERS=1: also launch role_marker around each timed launch
+    int every = 1;         // time one launch in `every` of a selected role
+    long seen[GP_K_COUNT] = {};  // launches of each selected role since the last reset
     std::vector<std::pair<hipEvent_t, hipEvent_t>> recs[GP_K_COUNT];
     double flops[GP_K_COUNT] = {}, bytes[GP_K_COUNT] = {};
     std::vector<hipEvent_t> pool;  // created events not in use
@@ -128,6 +130,7 @@ struct LaunchTimer {
             }
             recs[r].clear();
             flops[r] = bytes[r] = 0.0;
+            seen[r] = 0;
         }
     }
 };
@@ -307,12 +310,14 @@ Ctx make_ctx(gp_partition* p, hipStream_t st, Lane lane = Lane::Main) {
         if (s_ != GP_OK) return s_;  \
     } while (0)
 
-// Run `launch` (which enqueues on c.st); when `role` is being timed, bracket
-// it with two events on c.st and add its algorithmic work.
+// Run `launch` (which enqueues on c.st); when `role` is being timed (and this
+// is a sampled launch of it), bracket it with two events on c.st and add its
+// algorithmic work.
 template <class F>
 gp_status timed(const Ctx& c, int role, double flops, double bytes, F&& launch) {
     LaunchTimer& t = c.p->timer;
     if (!t.on(role)) return launch();
+    if (t.seen[role]++ % t.every != 0) return launch();
     hipEvent_t e0, e1;
     GP_TRY(t.take(e0));
     GP_TRY(t.take(e1));
@@ -908,6 +913,13 @@ gp_status gp_timer_select(gp_partition* p, int role) {
     if (!p) return set_error(GP_ERR_INVALID_ARG, "partition must not be NULL");
     if (role < GP_K_NONE || role > GP_K_COUNT) return set_error(GP_ERR_INVALID_ARG, "timer role out of range");
     p->timer.selected = role;
+    return GP_OK;
+}
+
+gp_status gp_timer_sample(gp_partition* p, int every) {
+    if (!p) return set_error(GP_ERR_INVALID_ARG, "partition must not be NULL");
+    if (every < 1) return set_error(GP_ERR_INVALID_ARG, "timer sampling stride must be >= 1");
+    p->timer.every = every;
     return GP_OK;
 }
 

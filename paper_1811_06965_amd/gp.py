@@ -37,7 +37,7 @@ GP_K_NONE, GP_K_COUNT = 0, len(KERNEL_ROLES)
 EXPORTS = ["gp_partition_create", "gp_partition_configure", "gp_partition_destroy", "gp_set_param",
            "gp_get_param", "gp_get_grad", "gp_partition_memory", "gp_param_count", "gp_forward_microbatch",
            "gp_backward_microbatch_remat", "gp_accumulate_and_step", "gp_timer_select", "gp_timer_read",
-           "gp_timer_reset", "gp_mfma_peak", "gp_last_error"]
+           "gp_timer_reset", "gp_timer_sample", "gp_mfma_peak", "gp_last_error"]
 
 
 class gp_config(ctypes.Structure):
@@ -81,6 +81,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.gp_timer_select.argtypes = [P, I]
     lib.gp_timer_read.argtypes = [P, I, D, ctypes.POINTER(ctypes.c_long), D, D]
     lib.gp_timer_reset.argtypes = [P]
+    lib.gp_timer_sample.argtypes = [P, I]
     lib.gp_mfma_peak.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_double)]
     lib.gp_last_error.argtypes = []
     lib.gp_last_error.restype = ctypes.c_char_p
@@ -175,6 +176,10 @@ def gp_timer_read(h, role):
 
 def gp_timer_reset(h):
     _check(load().gp_timer_reset(h))
+
+
+def gp_timer_sample(h, every):
+    _check(load().gp_timer_sample(h, every))
 
 
 def gp_mfma_peak(stream=None):

@@ -162,3 +162,7 @@ class Partition:
 
     def timer_reset(self):
         gp.gp_timer_reset(self.h)
+
+    def timer_sample(self, every):
+        """Time one launch in `every` of the selected role (1: all)."""
+        gp.gp_timer_sample(self.h, every)

@@ -98,6 +98,7 @@ def test_calls_on_a_null_partition_are_rejected(lib):
     assert lib.gp_backward_microbatch_remat(None, 0, None, None, None, None) == 1
     assert lib.gp_accumulate_and_step(None, ctypes.c_float(0.1), None, None) == 1
     assert lib.gp_timer_select(None, 0) == 1
+    assert lib.gp_timer_sample(None, 1) == 1
     assert lib.gp_partition_destroy(None) == 0
 
 

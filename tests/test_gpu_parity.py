@@ -393,3 +393,33 @@ def test_mfma_peak_probe_reports_a_plausible_rate():
     from paper_1811_06965_amd import gp
     t = gp.gp_mfma_peak(torch.cuda.current_stream().cuda_stream)
     assert 800.0 < t < 2700.0, t
+
+
+def test_launch_timer_samples_one_launch_in_every():
+    """The role timer: with every launch bracketed, a step of the tiny
+    partition records at least one ffn1 forward launch per layer and
+    micro-batch (first pass; recomputes add more); with a stride of 3 the same
+    step records launches 0, 3, 6, ... of that sequence, and the algorithmic
+    FLOPs scale with the count."""
+    from paper_1811_06965_amd.runtime import Partition
+    case = synth.make_case(TINY, 0)
+    with Partition(TINY, micro=TINY.micro) as part:
+        part.load_params(case["layers"], case["head"])
+        inp = part.device_inputs(case)
+        got = {}
+        for every in (1, 3):
+            part.timer_reset()
+            part.timer_sample(every)
+            part.timer_select("ffn1.fwd")
+            part.step(inp["x"], inp["mem"], inp["dy"], lr=0.0)
+            torch.cuda.synchronize()
+            part.timer_select(None)
+            got[every] = part.timer_read("ffn1.fwd")
+        part.timer_sample(1)
+        part.timer_reset()
+    n = got[1]["launches"]
+    assert n >= TINY.layers * TINY.micro, got
+    assert got[3]["launches"] == (n + 2) // 3, got
+    assert got[3]["ms"] > 0.0
+    per = got[1]["flops"] / n
+    assert abs(got[3]["flops"] - per * got[3]["launches"]) <= 1e-6 * got[1]["flops"]

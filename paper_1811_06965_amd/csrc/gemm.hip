@@ -1252,6 +1252,10 @@ gp_status launch_dl(const GemmArgs& a, int epi, int splits, hipStream_t st) {
         dim3 grid(tiles, splits);
         klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_F32, 1, KM>, grid, NT, 0, st, a);
         GP_LAUNCH_CHECK();
+        if (a.deferred && (epi == EPI_RES_F32 || epi == EPI_F32)) {
+            *a.deferred = splits;  // the caller reduces
+            return GP_OK;
+        }
         return launch_reduce(a, epi, splits, st);
     }
     if constexpr (KM) {
@@ -1531,7 +1535,13 @@ gp_status check_args(const GemmArgs& a, bool a_kmajor, bool b_kmajor) {
 
 } // namespace
 
+gp_status gemm_reduce(const GemmArgs& a, int epi, int splits, hipStream_t st) {
+    if (!a.ws || splits < 2) return set_error(GP_ERR_INVALID_ARG, "gemm_reduce: no split-K partials");
+    return launch_reduce(a, epi, splits, st);
+}
+
 gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dtype, hipStream_t st) {
+    if (a.deferred) *a.deferred = 1;
     if (a.a4) {
         if (dtype != GP_BF16 || !a_kmajor || !b_kmajor || epi != EPI_STORE || a.K % 64 || !a.b4 || !a.sa4 || !a.sb4)
             return set_error(GP_ERR_UNSUPPORTED, "gemm: the fp4 correction needs bf16, k-contiguous operands, "

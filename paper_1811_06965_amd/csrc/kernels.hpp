@@ -40,9 +40,16 @@ struct GemmArgs {
     const void* b4 = nullptr;
     const unsigned char* sa4 = nullptr;
     const unsigned char* sb4 = nullptr;
+    // EPI_RES_F32 and EPI_F32 only: when set, a split-K launch leaves its
+    // partials in ws [splits][M][N] and stores the split count here instead of
+    // running the reduce (the caller then reduces, e.g. fused with the next
+    // LayerNorm); 1 when the GEMM completed its own epilogue.
+    int* deferred = nullptr;
 };
 
 gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dtype, hipStream_t st);
+// The split-K reduce and epilogue of a bf16 GEMM whose partials are in a.ws.
+gp_status gemm_reduce(const GemmArgs& a, int epi, int splits, hipStream_t st);
 
 // ------------------------------------------------------------- LayerNorm
 // out (elt) = gamma * (x - mu) * rstd + beta per row of D; stats[row] = {mu, rstd}.
@@ -51,13 +58,27 @@ gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dty
 // correction operand (GemmArgs::a4) of the GEMM that consumes out.
 gp_status layernorm_fwd(int dtype, const float* x, long rows, int D, const float* gamma, const float* beta,
                         float eps, void* out, float* stats, void* lo4, unsigned char* lo_sc, hipStream_t st);
+// The split-K reduce of a residual GEMM fused with the LayerNorm of its result:
+// x = sum over s < splits of ws[s plane + row D + col], plus (res + bias), in
+// the order of the GEMM's own reduce, is stored in xo (fp32) and xc (bf16, when
+// not null), then normalised as layernorm_fwd does.  Rows of D contiguous;
+// bf16 out, D % 256 == 0, D <= 2048, 16-byte aligned pointers
+// (layernorm_fwd_res_ok); GP_ERR_UNSUPPORTED otherwise.
+bool layernorm_fwd_res_ok(int dtype, int D, const void* ws, const float* bias, const float* res, const float* xo,
+                          const void* xc);
+gp_status layernorm_fwd_res(int dtype, const float* ws, int splits, long plane, const float* bias, const float* res,
+                            float* xo, void* xc, long rows, int D, const float* gamma, const float* beta, float eps,
+                            void* out, float* stats, void* lo4, unsigned char* lo_sc, hipStream_t st);
 // dx = dres + rstd (g - mean g - xh mean(g xh)), g = dn * gamma; writes dx_f32 and/or dx_elt.
 // Per-block partial sums of dn * xh and dn go to partial[blk][2][D] (added to
 // what is there when accumulate != 0); *nblk receives the block count (for
 // colsum_finalize over width 2 D).  The block count depends on rows only.
+// dn_splits > 1 (D % 256 == 0, D <= 2048): dn holds that many split-K
+// partial planes dn_plane floats apart, summed in plane order (the fused
+// reduce of the GEMM that produced dn).
 gp_status layernorm_bwd(int dtype, const float* dn, const float* x, const float* stats, const float* gamma,
                         long rows, int D, const float* dres, float* dx_f32, void* dx_elt, float* partial,
-                        int accumulate, int* nblk, hipStream_t st);
+                        int accumulate, int* nblk, hipStream_t st, int dn_splits = 1, long dn_plane = 0);
 // Rows the partial buffers of layernorm_bwd / bias_grad may need.
 int layernorm_bwd_blocks(long rows);
 int bias_grad_blocks(long rows);

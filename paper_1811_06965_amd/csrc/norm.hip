@@ -191,21 +191,13 @@ template <> struct Out4<bf16> {
 __device__ __forceinline__ float hsum(f32x4 v) { return (v[0] + v[1]) + (v[2] + v[3]); }
 
 template <typename T, int C4>
-__global__ void __launch_bounds__(256) ln_fwd_v4(const float* __restrict__ x, long rows, int D,
-                                                 const float* __restrict__ gamma, const float* __restrict__ beta,
-                                                 float eps, T* __restrict__ out, float* __restrict__ stats,
-                                                 unsigned char* __restrict__ lo4, unsigned char* __restrict__ lo_sc) {
-    const int lane = threadIdx.x & 63;
-    const long row = (long)blockIdx.x * LN_WAVES + (threadIdx.x >> 6);
-    if (row >= rows) return;
-    const f32x4* xr = reinterpret_cast<const f32x4*>(x + row * D);
-    f32x4 v[C4];
+__device__ __forceinline__ void ln_row_v4(const f32x4 (&v)[C4], int lane, long row, int D,
+                                          const float* __restrict__ gamma, const float* __restrict__ beta, float eps,
+                                          T* __restrict__ out, float* __restrict__ stats,
+                                          unsigned char* __restrict__ lo4, unsigned char* __restrict__ lo_sc) {
     float s = 0.f;
 #pragma unroll
-    for (int c = 0; c < C4; ++c) {
-        v[c] = xr[lane + 64 * c];
-        s += hsum(v[c]);
-    }
+    for (int c = 0; c < C4; ++c) s += hsum(v[c]);
     const float mu = wave_sum(s) / D;
     float q = 0.f;
 #pragma unroll
@@ -246,12 +238,64 @@ __global__ void __launch_bounds__(256) ln_fwd_v4(const float* __restrict__ x, lo
     }
 }
 
+// One wave per row: the row's float4 chunks lane + 64 c (c < C4), then ln_row_v4.
+template <typename T, int C4>
+__global__ void __launch_bounds__(256) ln_fwd_v4(const float* __restrict__ x, long rows, int D,
+                                                 const float* __restrict__ gamma, const float* __restrict__ beta,
+                                                 float eps, T* __restrict__ out, float* __restrict__ stats,
+                                                 unsigned char* __restrict__ lo4, unsigned char* __restrict__ lo_sc) {
+    const int lane = threadIdx.x & 63;
+    const long row = (long)blockIdx.x * LN_WAVES + (threadIdx.x >> 6);
+    if (row >= rows) return;
+    const f32x4* xr = reinterpret_cast<const f32x4*>(x + row * D);
+    f32x4 v[C4];
+#pragma unroll
+    for (int c = 0; c < C4; ++c) v[c] = xr[lane + 64 * c];
+    ln_row_v4<T, C4>(v, lane, row, D, gamma, beta, eps, out, stats, lo4, lo_sc);
+}
+
+// The split-K reduce of a residual GEMM fused with the LayerNorm of its
+// result (same wave-per-row layout as ln_fwd_v4): each chunk of x is the sum
+// of the split partials, in split order, plus (residual + bias) -- the
+// operations of the GEMM's own reduce -- stored in fp32 (and as a bf16 copy
+// when xc is given) and normalised from registers.
+template <typename T, int C4>
+__global__ void __launch_bounds__(256) ln_fwd_res_v4(const float* __restrict__ ws, int splits, long plane,
+                                                     const float* __restrict__ bias, const float* res, float* xo,
+                                                     bf16* __restrict__ xc, long rows, int D,
+                                                     const float* __restrict__ gamma, const float* __restrict__ beta,
+                                                     float eps, T* __restrict__ out, float* __restrict__ stats,
+                                                     unsigned char* __restrict__ lo4, unsigned char* __restrict__ lo_sc) {
+    const int lane = threadIdx.x & 63;
+    const long row = (long)blockIdx.x * LN_WAVES + (threadIdx.x >> 6);
+    if (row >= rows) return;
+    const f32x4* p4 = reinterpret_cast<const f32x4*>(ws + row * D);
+    const f32x4* r4 = reinterpret_cast<const f32x4*>(res + row * D);
+    const f32x4* b4 = reinterpret_cast<const f32x4*>(bias);
+    f32x4* x4 = reinterpret_cast<f32x4*>(xo + row * D);
+    const long plane4 = plane / 4;
+    f32x4 v[C4];
+#pragma unroll
+    for (int c = 0; c < C4; ++c) {
+        const int i = lane + 64 * c;
+        f32x4 s = p4[i];
+        for (int k = 1; k < splits; ++k) s += p4[i + k * plane4];
+        const f32x4 bv = bias ? b4[i] : f32x4{0.f, 0.f, 0.f, 0.f};
+        s += r4[i] + bv;
+        v[c] = s;
+        x4[i] = s;
+        if (xc) *reinterpret_cast<bf16x4*>(xc + row * D + 4 * i) = {(bf16)s[0], (bf16)s[1], (bf16)s[2], (bf16)s[3]};
+    }
+    ln_row_v4<T, C4>(v, lane, row, D, gamma, beta, eps, out, stats, lo4, lo_sc);
+}
+
 template <typename T, int C4>
 __global__ void __launch_bounds__(256) ln_bwd_v4(const float* __restrict__ dn, const float* __restrict__ x,
                                                  const float* __restrict__ stats, const float* __restrict__ gamma,
                                                  long rows, int D, int rpw, const float* __restrict__ dres,
                                                  float* __restrict__ dx32, T* __restrict__ dxe,
-                                                 float* __restrict__ partial, int accumulate) {
+                                                 float* __restrict__ partial, int accumulate, int dn_splits,
+                                                 long dn_plane) {
     __shared__ f32x4 red[LN_WAVES][2][C4 * 64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const f32x4* g4 = reinterpret_cast<const f32x4*>(gamma);
@@ -271,7 +315,10 @@ __global__ void __launch_bounds__(256) ln_bwd_v4(const float* __restrict__ dn, c
         const f32x4* r4 = reinterpret_cast<const f32x4*>(dres + row * D);
 #pragma unroll
         for (int c = 0; c < C4; ++c) {
+            // dn_splits > 1: dn is the split-K partials of the GEMM that produced
+            // it, summed here in split order (the order of that GEMM's reduce)
             d[c] = dn4[lane + 64 * c];
+            for (int k = 1; k < dn_splits; ++k) d[c] += dn4[lane + 64 * c + k * (dn_plane / 4)];
             xx[c] = x4[lane + 64 * c];
             r[c] = dres ? r4[lane + 64 * c] : f32x4{0.f, 0.f, 0.f, 0.f};
         }
@@ -381,13 +428,14 @@ gp_status ln_fwd_t(const float* x, long rows, int D, const float* g, const float
 template <typename T>
 gp_status ln_bwd_t(const float* dn, const float* x, const float* stats, const float* gamma, long rows, int D,
                    const float* dres, float* dx32, void* dxe, float* partial, int accumulate, int* nblk,
-                   hipStream_t st) {
+                   int dn_splits, long dn_plane, hipStream_t st) {
     const int rpw = ln_bwd_rows_per_wave(rows);
     const int grid = (int)((rows + (long)LN_WAVES * rpw - 1) / ((long)LN_WAVES * rpw));
     *nblk = grid;
     T* e = reinterpret_cast<T*>(dxe);
     if (D % 256 == 0 && D <= 2048) {
-#define GP_LNV(CC) klaunch(ln_bwd_v4<T, CC>, grid, 256, 0, st, dn, x, stats, gamma, rows, D, rpw, dres, dx32, e, partial, accumulate)
+#define GP_LNV(CC) klaunch(ln_bwd_v4<T, CC>, grid, 256, 0, st, dn, x, stats, gamma, rows, D, rpw, dres, dx32, e, partial, \
+                           accumulate, dn_splits, dn_plane)
         switch (D / 256) {
         case 1: GP_LNV(1); break;
         case 2: GP_LNV(2); break;
@@ -402,6 +450,7 @@ gp_status ln_bwd_t(const float* dn, const float* x, const float* stats, const fl
         GP_LAUNCH_CHECK();
         return GP_OK;
     }
+    if (dn_splits > 1) return set_error(GP_ERR_UNSUPPORTED, "layernorm backward over split-K partials: d_model % 256");
     const int C = (D + 63) / 64;
 #define GP_LNB(CC) klaunch(ln_bwd_kernel<T, CC>, grid, 256, 0, st, dn, x, stats, gamma, rows, D, rpw, dres, dx32, e, partial, accumulate)
     if (C <= 1) GP_LNB(1);
@@ -433,12 +482,51 @@ gp_status layernorm_fwd(int dtype, const float* x, long rows, int D, const float
     return ln_fwd_t<float>(x, rows, D, gamma, beta, eps, out, stats, nullptr, nullptr, st);
 }
 
+bool layernorm_fwd_res_ok(int dtype, int D, const void* ws, const float* bias, const float* res, const float* xo,
+                          const void* xc) {
+    auto a16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
+    return dtype == GP_BF16 && D % 256 == 0 && D >= 256 && D <= 2048 && ws && res && xo && a16(ws) && a16(bias) &&
+           a16(res) && a16(xo) && (!xc || (reinterpret_cast<uintptr_t>(xc) & 7) == 0);
+}
+
+gp_status layernorm_fwd_res(int dtype, const float* ws, int splits, long plane, const float* bias, const float* res,
+                            float* xo, void* xc, long rows, int D, const float* gamma, const float* beta, float eps,
+                            void* out, float* stats, void* lo4, unsigned char* lo_sc, hipStream_t st) {
+    if (!layernorm_fwd_res_ok(dtype, D, ws, bias, res, xo, xc) || splits < 1 || plane % 4 || plane < rows * D)
+        return set_error(GP_ERR_UNSUPPORTED, "layernorm with split-K reduce: bf16, d_model % 256 == 0 (<= 2048), "
+                                             "aligned rows");
+    unsigned char* l4 = static_cast<unsigned char*>(lo4);
+    if (l4 && (D % 64 || !lo_sc)) return set_error(GP_ERR_UNSUPPORTED, "layernorm: fp4 residuals need an E8M0 scale row");
+    const int grid = (int)((rows + LN_WAVES - 1) / LN_WAVES);
+    bf16* o = reinterpret_cast<bf16*>(out);
+    bf16* c = reinterpret_cast<bf16*>(xc);
+#define GP_LNR(C4) klaunch(ln_fwd_res_v4<bf16, C4>, grid, 256, 0, st, ws, splits, plane, bias, res, xo, c, rows, D, \
+                           gamma, beta, eps, o, stats, l4, lo_sc)
+    switch (D / 256) {
+    case 1: GP_LNR(1); break;
+    case 2: GP_LNR(2); break;
+    case 3: GP_LNR(3); break;
+    case 4: GP_LNR(4); break;
+    case 5: GP_LNR(5); break;
+    case 6: GP_LNR(6); break;
+    case 7: GP_LNR(7); break;
+    default: GP_LNR(8); break;
+    }
+#undef GP_LNR
+    GP_LAUNCH_CHECK();
+    return GP_OK;
+}
+
 gp_status layernorm_bwd(int dtype, const float* dn, const float* x, const float* stats, const float* gamma,
                         long rows, int D, const float* dres, float* dx_f32, void* dx_elt, float* partial,
-                        int accumulate, int* nblk, hipStream_t st) {
+                        int accumulate, int* nblk, hipStream_t st, int dn_splits, long dn_plane) {
+    if (dn_splits < 1 || (dn_splits > 1 && (dn_plane < rows * D || dn_plane % 4)))
+        return set_error(GP_ERR_INVALID_ARG, "layernorm backward: split-K partial layout");
     if (dtype == GP_BF16)
-        return ln_bwd_t<bf16>(dn, x, stats, gamma, rows, D, dres, dx_f32, dx_elt, partial, accumulate, nblk, st);
-    return ln_bwd_t<float>(dn, x, stats, gamma, rows, D, dres, dx_f32, dx_elt, partial, accumulate, nblk, st);
+        return ln_bwd_t<bf16>(dn, x, stats, gamma, rows, D, dres, dx_f32, dx_elt, partial, accumulate, nblk,
+                              dn_splits, dn_plane, st);
+    return ln_bwd_t<float>(dn, x, stats, gamma, rows, D, dres, dx_f32, dx_elt, partial, accumulate, nblk, dn_splits,
+                           dn_plane, st);
 }
 
 gp_status colsum_finalize(const float* partial, int nblk, int width, float* out, int accumulate, hipStream_t st) {

@@ -188,6 +188,8 @@ struct gp_partition {
     // the recompute stream by the last forward call itself, right after the
     // boundary input is stashed, and runs beside that forward.
     bool remat_early = true;
+    // split-K reduce of a residual GEMM fused into the next LayerNorm (GP_FUSE_RES_LN)
+    bool fuse_res_ln = true;
     hipStream_t remat = nullptr;
     hipEvent_t remat_done = nullptr;  // from evring
     int remat_pending = -1;  // micro-batch whose recompute-ahead is enqueued
@@ -288,12 +290,24 @@ void plan_workspace(gp_partition* p, Arena& a) {
     }
 }
 
+// A GEMM launched split-K whose reduce is left to the LayerNorm that takes its
+// output, the next launch on the same stream: a residual GEMM of a forward pass
+// (EPI_RES_F32; layernorm_fwd_res runs both in one kernel), or an fp32 input-
+// gradient GEMM of the backward (EPI_F32; the LayerNorm backward sums the
+// partials as it loads them).  splits == 0: nothing pending.
+struct PendingRes {
+    int splits = 0;
+    int epi = 0;
+    GemmArgs g;  // the GEMM's arguments: partials (ws), bias, residual (aux), outputs
+};
+
 struct Ctx {
     gp_partition* p;
     hipStream_t st;
     int dt;
     float* ws = nullptr;        // split-K partials for launches on st
     bool last = false;          // the mini-batch's last backward micro-batch
+    PendingRes* pend = nullptr; // forward passes: a deferred split-K reduce
 };
 
 enum class Lane { Main, Side, Remat };
@@ -374,8 +388,33 @@ gp_status timed_attention(const Ctx& c, int role, const AttnArgs& a, bool bwd) {
     return timed(c, role, f, by, [&] { return bwd ? attention_bwd(c.dt, a, c.st) : attention_fwd(c.dt, a, c.st); });
 }
 
+// The reduce of a deferred split-K GEMM on its own (when no LayerNorm takes it).
+gp_status flush_pending(const Ctx& c) {
+    if (!c.pend || c.pend->splits < 2) return GP_OK;
+    const int sp = c.pend->splits;
+    c.pend->splits = 0;
+    return gemm_reduce(c.pend->g, c.pend->epi, sp, c.st);
+}
+
 gp_status timed_ln_fwd(const Ctx& c, const float* x, long rows, int D, const float* gamma, const float* beta,
                        float eps, void* out, float* stats, unsigned char* lo4 = nullptr, unsigned char* lo_sc = nullptr) {
+    if (c.pend && c.pend->splits > 1) {
+        const GemmArgs& g = c.pend->g;
+        if (c.pend->epi == EPI_RES_F32 && g.C == x && g.M == rows && g.N == D) {
+            // x is the pending GEMM's output: its reduce and this LayerNorm in one kernel
+            const int sp = c.pend->splits;
+            c.pend->splits = 0;
+            const double plane = (double)rows * D;
+            const double by = plane * (4.0 * sp + 4.0 + 4.0 + (g.C2 ? 2.0 : 0.0) + c.p->esz + (lo4 ? 0.5 : 0.0)) +
+                              rows * 8.0 + D * 12.0;
+            return timed(c, GP_K_LN_FWD, 0.0, by, [&] {
+                return layernorm_fwd_res(c.dt, g.ws, sp, (long)rows * D, g.bias, static_cast<const float*>(g.aux),
+                                         static_cast<float*>(g.C), g.C2, rows, D, gamma, beta, eps, out, stats, lo4,
+                                         lo_sc, c.st);
+            });
+        }
+        GP_TRY(flush_pending(c));
+    }
     const double by = (double)rows * D * (4.0 + c.p->esz + (lo4 ? 0.5 : 0.0)) + rows * 8.0 + D * 8.0;
     return timed(c, GP_K_LN_FWD, 0.0, by,
                  [&] { return layernorm_fwd(c.dt, x, rows, D, gamma, beta, eps, out, stats, lo4, lo_sc, c.st); });
@@ -383,8 +422,12 @@ gp_status timed_ln_fwd(const Ctx& c, const float* x, long rows, int D, const flo
 
 // Y = A W + b with an epilogue; A [M, K] k-contiguous, W^T working copy [N, K].
 // A4 / A4s: fp4 rounding residuals of A and their row scales (split layers).
+// defer: the next launch on c.st is the LayerNorm of C, which may then take
+// over a split-K reduce (EPI_RES_F32, see PendingRes).
 gp_status linear_fwd(const Ctx& c, const Linear& L, const void* A, long M, void* C, long ldc, int epi, int relu,
-                     const float* res, void* C2, const unsigned char* A4 = nullptr, const unsigned char* A4s = nullptr) {
+                     const float* res, void* C2, const unsigned char* A4 = nullptr, const unsigned char* A4s = nullptr,
+                     bool defer = false) {
+    GP_TRY(flush_pending(c));
     GemmArgs g;
     g.M = (int)M;
     g.N = L.out;
@@ -411,12 +454,24 @@ gp_status linear_fwd(const Ctx& c, const Linear& L, const void* A, long M, void*
     g.ws_elems = c.p->bw.splitk_elems;
     g.force_cfg = c.p->gemm_tile;
     g.force_splits = c.p->gemm_splits;
-    return timed_gemm(c, L.role, g, epi, true);
+    int splits = 1;
+    if (defer && c.pend && c.p->fuse_res_ln && epi == EPI_RES_F32 && ldc == L.out &&
+        layernorm_fwd_res_ok(c.dt, L.out, c.ws, g.bias, res, static_cast<const float*>(C), C2))
+        g.deferred = &splits;
+    GP_TRY(timed_gemm(c, L.role, g, epi, true));
+    if (splits > 1) {
+        c.pend->splits = splits;
+        c.pend->epi = epi;
+        c.pend->g = g;
+        c.pend->g.deferred = nullptr;
+    }
+    return GP_OK;
 }
 
 // dX = dY W^T with an epilogue; dY [M, out] k-contiguous, W working copy [in, out].
 gp_status linear_dx(const Ctx& c, const Linear& L, const void* dY, long M, void* C, int epi, const void* aux,
-                    int accumulate) {
+                    int accumulate, bool defer = false) {
+    GP_TRY(flush_pending(c));
     GemmArgs g;
     g.M = (int)M;
     g.N = L.in;
@@ -434,11 +489,23 @@ gp_status linear_dx(const Ctx& c, const Linear& L, const void* dY, long M, void*
     g.ws_elems = c.p->bw.splitk_elems;
     g.force_cfg = c.p->gemm_tile;
     g.force_splits = c.p->gemm_splits;
-    return timed_gemm(c, L.role + 1, g, epi, true);
+    int splits = 1;
+    if (defer && c.pend && c.p->fuse_res_ln && epi == EPI_F32 && c.dt == GP_BF16 && L.in % 256 == 0 &&
+        L.in <= 2048)
+        g.deferred = &splits;
+    GP_TRY(timed_gemm(c, L.role + 1, g, epi, true));
+    if (splits > 1) {
+        c.pend->splits = splits;
+        c.pend->epi = epi;
+        c.pend->g = g;
+        c.pend->g.deferred = nullptr;
+    }
+    return GP_OK;
 }
 
 // G_W (+)= X^T dY and G_b (+)= sum_rows dY (one kernel).  X [rows, in], dY [rows, out].
 gp_status linear_dw(const Ctx& c, const Linear& L, const void* X, const void* dY, long rows, int accumulate) {
+    GP_TRY(flush_pending(c));
     GemmArgs g;
     g.M = L.in;
     g.N = L.out;
@@ -475,12 +542,24 @@ gp_status norm_bwd(const Ctx& c, const Norm& N, const float* dn, const float* x,
                    const float* dres, float* dx32, void* dxe, int accumulate) {
     int nblk = 0;
     float* part = c.p->lnpart[N.id];
+    // dn still as the split-K partials of the GEMM that produced it: summed while loading
+    int sp = 1;
+    if (c.pend && c.pend->splits > 1) {
+        const GemmArgs& g = c.pend->g;
+        if (c.pend->epi == EPI_F32 && g.C == dn && g.M == rows && g.N == N.n && g.ldc == N.n) {
+            sp = c.pend->splits;
+            dn = g.ws;
+            c.pend->splits = 0;
+        } else {
+            GP_TRY(flush_pending(c));
+        }
+    }
     const double rd = (double)rows * N.n;
-    const double by = rd * (8.0 + (dres ? 4.0 : 0.0) + (dx32 ? 4.0 : 0.0) + (dxe ? (double)c.p->esz : 0.0)) +
+    const double by = rd * (4.0 * sp + 4.0 + (dres ? 4.0 : 0.0) + (dx32 ? 4.0 : 0.0) + (dxe ? (double)c.p->esz : 0.0)) +
                       rows * 8.0 + (double)layernorm_bwd_blocks(rows) * 2 * N.n * 4.0 * (accumulate ? 2.0 : 1.0);
     return timed(c, GP_K_LN_BWD, 0.0, by, [&] {
         GP_TRY(layernorm_bwd(c.dt, dn, x, stats, c.p->master + N.g, rows, N.n, dres, dx32, dxe, part, accumulate,
-                             &nblk, c.st));
+                             &nblk, c.st, sp, rd > 0 ? (long)rd : 0));
         if (!c.last) return GP_OK;
         return colsum_finalize(part, nblk, 2 * N.n, c.p->grads + N.g, 0, c.st);
     });
@@ -520,7 +599,7 @@ gp_status layer_forward(const Ctx& c, int l, LayerWs& w, const float* x_in, floa
     a.ldo = D;
     a.lse = w.lse;
 GP_TRY(timed_attention(c, GP_K_ATTN_FWD, a, false));
-    GP_TRY(linear_fwd(c, P.o, w.c, T, w.x1, D, EPI_RES_F32, 0, x_in, nullptr));
+    GP_TRY(linear_fwd(c, P.o, w.c, T, w.x1, D, EPI_RES_F32, 0, x_in, nullptr, nullptr, nullptr, true));
     const float* xf = w.x1;
     if (dec) {
         // cross-attention block: queries from LN2(x1), keys/values from the memory
@@ -537,7 +616,7 @@ GP_TRY(timed_attention(c, GP_K_ATTN_FWD, a, false));
         x.ldo = D;
         x.lse = w.xlse;
         GP_TRY(timed_attention(c, GP_K_XATTN_FWD, x, false));
-        GP_TRY(linear_fwd(c, P.xo, w.xc, T, w.x2, D, EPI_RES_F32, 0, w.x1, nullptr));
+        GP_TRY(linear_fwd(c, P.xo, w.xc, T, w.x2, D, EPI_RES_F32, 0, w.x1, nullptr, nullptr, nullptr, true));
         xf = w.x2;
     }
     // feed-forward block
@@ -549,7 +628,8 @@ GP_TRY(timed_attention(c, GP_K_ATTN_FWD, a, false));
                         s4 ? w.v4s : nullptr));
     GP_TRY(linear_fwd(c, P.ffn1, w.v, T, w.a, p->d.F, EPI_STORE, 1, nullptr, nullptr, s4 ? w.v4 : nullptr,
                       s4 ? w.v4s : nullptr));
-    GP_TRY(linear_fwd(c, P.ffn2, w.a, T, x_out, D, EPI_RES_F32, 0, xf, y_out));
+    // the next layer begins with the LayerNorm of x_out
+    GP_TRY(linear_fwd(c, P.ffn2, w.a, T, x_out, D, EPI_RES_F32, 0, xf, y_out, nullptr, nullptr, l + 1 < p->d.L));
     return GP_OK;
 }
 
@@ -571,13 +651,16 @@ gp_status partition_forward(const Ctx& c, int m, bool keep, const void* x, const
         GP_TRY(intake(c.dt, p->stash_x_mb(m), nullptr, xs[0], T * D, c.st));
     }
     const void* mem_m = p->g.kind == GP_DECODER_CROSS ? p->stash_m_mb(m) : nullptr;
+    PendingRes pend;
+    Ctx cf = c;
+    cf.pend = &pend;
     for (int l = 0; l < L; ++l) {
         LayerWs& w = keep ? p->lw[set][l] : p->lw[set][0];
         const float* xi = keep ? xs[l] : xs[l & 1];
         float* xo = keep ? xs[l + 1] : xs[(l + 1) & 1];
-        GP_TRY(layer_forward(c, l, w, xi, xo, mem_m, (!keep && l == L - 1) ? y : nullptr, keep));
+        GP_TRY(layer_forward(cf, l, w, xi, xo, mem_m, (!keep && l == L - 1) ? y : nullptr, keep));
     }
-    return GP_OK;
+    return flush_pending(cf);
 }
 
 // Backward of one layer.  dY arrives in (in32, ine); dX leaves in the pair
@@ -614,7 +697,7 @@ gp_status layer_backward(const Ctx& c, int set, int l, bool first, float* in32, 
     GP_TRY(linear_dx(c, P.ffn2, ine, T, b.dz[par], EPI_RELU_MASK, w.a, 0));
     jobs.push_back({&P.ffn1, w.v, b.dz[par], T});
     GP_TRY(flush(0));
-    GP_TRY(linear_dx(c, P.ffn1, b.dz[par], T, b.dn, EPI_F32, nullptr, 0));
+    GP_TRY(linear_dx(c, P.ffn1, b.dz[par], T, b.dn, EPI_F32, nullptr, 0, true));
     GP_TRY(flush(1));
     void* sce = next_elt();
     GP_TRY(norm_bwd(c, nf, b.dn, xf, w.stf, T, in32, sc32, sce, acc));
@@ -678,7 +761,7 @@ gp_status layer_backward(const Ctx& c, int set, int l, bool first, float* in32, 
     GP_TRY(timed_attention(c, GP_K_ATTN_BWD, a, true));
     jobs.push_back({&P.qkv, w.u, b.dqkv[par], T});
     GP_TRY(flush(0));
-    GP_TRY(linear_dx(c, P.qkv, b.dqkv[par], T, b.dn, EPI_F32, nullptr, 0));
+    GP_TRY(linear_dx(c, P.qkv, b.dqkv[par], T, b.dn, EPI_F32, nullptr, 0, true));
     const float* x_in = p->xs[set][l];
     if (dxe_final || dx32_final || l == 0) {
         GP_TRY(norm_bwd(c, P.ln1, b.dn, x_in, w.st1, T, cur32, dx32_final, dxe_final, acc));
@@ -801,6 +884,7 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
     if (const char* e = std::getenv("GP_SIDE_STREAM")) p->use_side = std::atoi(e) != 0;
     if (const char* e = std::getenv("GP_REMAT_AHEAD")) p->remat_ahead = std::atoi(e) != 0;
     if (const char* e = std::getenv("GP_REMAT_EARLY")) p->remat_early = std::atoi(e) != 0;
+    if (const char* e = std::getenv("GP_FUSE_RES_LN")) p->fuse_res_ln = std::atoi(e) != 0;
     if (const char* e = std::getenv("GP_DW_FLUSH")) p->dw_flush = std::atoi(e);
     p->nsets = (p->remat_ahead && g.M >= 2) ? 2 : 1;
     if (const char* e = std::getenv("GP_GEMM_TILE")) p->gemm_tile = std::atoi(e);
@@ -1074,6 +1158,9 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     int ri = 1;
     std::vector<DwJob> jobs;
     hipEvent_t last_done = nullptr;  // latest side-stream event of this call
+    PendingRes pend;                 // a dX GEMM's split-K reduce left to the next LayerNorm backward
+    Ctx cb = c;
+    cb.pend = &pend;
     auto fail = [&](gp_status st) {
         if (last_done) (void)hipStreamWaitEvent(c.st, last_done, 0);
         return st;
@@ -1091,11 +1178,11 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
                 GP_HIP(hipEventRecord(fork, c.st));
                 GP_HIP(hipStreamWaitEvent(cs.st, fork, 0));
             }
-            for (const DwJob& j : jobs) GP_TRY(linear_dw(side ? cs : c, *j.L, j.X, j.dY, j.rows, acc));
+            for (const DwJob& j : jobs) GP_TRY(linear_dw(side ? cs : cb, *j.L, j.X, j.dY, j.rows, acc));
             jobs.clear();
             return GP_OK;
         };
-        s = layer_backward(c, set, l, first, in32, ine, sc32, ri, out32, oute, nullptr, l == 0 ? dx : nullptr, mem_m,
+        s = layer_backward(cb, set, l, first, in32, ine, sc32, ri, out32, oute, nullptr, l == 0 ? dx : nullptr, mem_m,
                            jobs, flush);
         if (s == GP_OK) s = flush(2);
         if (s != GP_OK) return fail(s);
@@ -1110,6 +1197,8 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
             ine = oute;
         }
     }
+    if (s == GP_OK) s = flush_pending(cb);
+    if (s != GP_OK) return fail(s);
     // the caller's stream resumes only after the last weight-gradient GEMM
     if (side) GP_HIP(hipStreamWaitEvent(c.st, p->side_done[0], 0));
     if (dec && dmem) {

@@ -423,3 +423,35 @@ def test_launch_timer_samples_one_launch_in_every():
     assert got[3]["ms"] > 0.0
     per = got[1]["flops"] / n
     assert abs(got[3]["flops"] - per * got[3]["launches"]) <= 1e-6 * got[1]["flops"]
+
+
+def _gpu_step(cfg, seed):
+    from paper_1811_06965_amd.runtime import Partition
+    case = synth.make_case(cfg, seed, perturb=True)
+    with Partition(cfg, micro=cfg.micro) as part:
+        part.load_params(case["layers"], case["head"])
+        inp = part.device_inputs(case)
+        out = part.step(inp["x"], inp["mem"], inp["dy"], lr=0.0)
+        torch.cuda.synchronize()
+        gl, _ = part.grads()
+        return to_np(out["y"]), to_np(out["dx"]), gl
+
+
+@pytest.mark.parametrize("tile,splits", [(18, 2), (11, 4)], ids=["dl128x128_8w_4stage_split2", "dl128x128_8w_a_split4"])
+def test_split_reduce_fused_into_layernorm_is_bitwise_identical(tile, splits, monkeypatch):
+    """A residual GEMM's split-K reduce taken over by the next LayerNorm
+    (GP_FUSE_RES_LN, on by default) sums the partials, residual and bias in the
+    reduce kernel's order and normalises exactly as the LayerNorm kernel does:
+    outputs, input gradient and every parameter gradient match the unfused
+    path bit for bit (split-K forced on every GEMM)."""
+    monkeypatch.setenv("GP_GEMM_TILE", str(tile))
+    monkeypatch.setenv("GP_GEMM_SPLITS", str(splits))
+    monkeypatch.setenv("GP_FUSE_RES_LN", "1")
+    y1, dx1, g1 = _gpu_step(RAGGED_BF16, 5)
+    monkeypatch.setenv("GP_FUSE_RES_LN", "0")
+    y0, dx0, g0 = _gpu_step(RAGGED_BF16, 5)
+    assert np.array_equal(y1, y0)
+    assert np.array_equal(dx1, dx0)
+    for l, (a, b) in enumerate(zip(g1, g0)):
+        for k in a:
+            assert np.array_equal(a[k], b[k]), (l, k)

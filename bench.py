@@ -233,10 +233,10 @@ def dominant_role(roles):
     """The role with the most launch time in the census step; roles within
     10% of it count as tied (the split of a step between concurrent streams
     moves by that much from run to run), and a tie goes to the role doing the
-    most algorithmic work per step."""
+    most algorithmic work per step, then to the one with more time."""
     top = next(iter(roles.values()))["ms"]
-    tied = [(r["flops"], name) for name, r in roles.items() if r["ms"] >= 0.9 * top]
-    return max(tied)[1]
+    tied = [(r["flops"], r["ms"], name) for name, r in roles.items() if r["ms"] >= 0.9 * top]
+    return max(tied)[2]
 
 
 # One launch in this many of the timed role is bracketed by dispatch events

@@ -838,41 +838,39 @@ __global__ void __launch_bounds__(64 * WM * WN * KG) gemm_dl(GemmArgs args) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    // fragment byte offsets within a stage, per k-step
+    // Fragment byte offsets within a stage.  KM: the lane's fragment of block
+    // i, k-step s is chunk (2 s + h) ^ swz(row) of row r = wm (BM / WM) + 32 i + fr.
+    // swz reads bits 0..5 of r: bits 0..4 are fr's, and bit 5 is the parity
+    // p of (wm (BM / WM)) / 32 + i.  So swz(r) = w ^ 4 p with w = swz(fr), and
+    // the offset is base + 4096 i + ((s ^ (w >> 1) ^ 2 p) << 5), the chunk's
+    // low bit h ^ (w & 1) folded into the base: per operand a base and a
+    // per-lane term with the wave's parity in it, the block's parity an XOR
+    // with 64 -- instead of one register per (k-step, block).
+    // !KM: k-step s moves the fragment down 16 k-rows, a constant stride, and
+    // leaves the k-row's swizzle (k % 4) unchanged: one offset per block.
     const int fr = lane & 31, h = lane >> 5;
-    int fa_off[KS][TM], fb_off[KS][TN];
+    int fa_base = 0, fb_base = 0, swa = 0, swb = 0;
+    int fa_off[KM ? 1 : TM], fb_off[KM ? 1 : TN];
     if constexpr (KM) {
-#pragma unroll
-        for (int s = 0; s < KS; ++s) {
-#pragma unroll
-            for (int i = 0; i < TM; ++i) {
-                const int row = wm * (BM / WM) + i * 32 + fr;
-                fa_off[s][i] = row * 128 + (((2 * s + h) ^ swz(row)) << 4);
-            }
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const int row = wn * (BN / WN) + j * 32 + fr;
-                fb_off[s][j] = BM * 128 + row * 128 + (((2 * s + h) ^ swz(row)) << 4);
-            }
-        }
+        const int w = swz(fr);
+        fa_base = (wm * (BM / WM) + fr) * 128 + ((h ^ (w & 1)) << 4);
+        fb_base = BM * 128 + (wn * (BN / WN) + fr) * 128 + ((h ^ (w & 1)) << 4);
+        swa = (w >> 1) ^ ((((wm * (BM / WM)) >> 5) & 1) << 1);
+        swb = (w >> 1) ^ ((((wn * (BN / WN)) >> 5) & 1) << 1);
     } else {
         // lane l of a 16-lane group g = l / 16 addresses k-row 8 (g / 2) + (l % 16) / 4
         // and m 16 (g % 2) + 4 (l % 4) of its fragment (plus 4 k-rows for the second read)
         const int g = lane >> 4, q = lane & 15;
         const int kr = 8 * (g >> 1) + (q >> 2), mo = 16 * (g & 1) + 4 * (q & 3);
 #pragma unroll
-        for (int s = 0; s < KS; ++s) {
-            const int k = 16 * s + kr;
+        for (int i = 0; i < TM; ++i) {
+            const int m = wm * (BM / WM) + i * 32 + mo;
+            fa_off[i] = kr * (2 * BM) + ((((m >> 3) ^ ((kr & 3) << 2))) << 4) + (m & 7) * 2;
+        }
 #pragma unroll
-            for (int i = 0; i < TM; ++i) {
-                const int m = wm * (BM / WM) + i * 32 + mo;
-                fa_off[s][i] = k * (2 * BM) + ((((m >> 3) ^ ((k & 3) << 2))) << 4) + (m & 7) * 2;
-            }
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const int n = wn * (BN / WN) + j * 32 + mo;
-                fb_off[s][j] = BM * 128 + k * (2 * BN) + ((((n >> 3) ^ ((k & 3) << 2))) << 4) + (n & 7) * 2;
-            }
+        for (int j = 0; j < TN; ++j) {
+            const int n = wn * (BN / WN) + j * 32 + mo;
+            fb_off[j] = BM * 128 + kr * (2 * BN) + ((((n >> 3) ^ ((kr & 3) << 2))) << 4) + (n & 7) * 2;
         }
     }
     int f4a_off[TM], f4b_off[TN];
@@ -891,15 +889,18 @@ __global__ void __launch_bounds__(64 * WM * WN * KG) gemm_dl(GemmArgs args) {
     Frag<bf16> fa[2][TM], fb[2][TN];
     auto load_frags = [&](int slot, const char* stg, int s) {
         if constexpr (KM) {
+            const int ta = (s ^ swa) << 5, tb = (s ^ swb) << 5;
+            const char* pa[2] = {stg + fa_base + ta, stg + fa_base + (ta ^ 64)};
+            const char* pb[2] = {stg + fb_base + tb, stg + fb_base + (tb ^ 64)};
 #pragma unroll
-            for (int i = 0; i < TM; ++i) fa[slot][i].v = *reinterpret_cast<const bf16x8*>(stg + fa_off[s][i]);
+            for (int i = 0; i < TM; ++i) fa[slot][i].v = *reinterpret_cast<const bf16x8*>(pa[i & 1] + i * 4096);
 #pragma unroll
-            for (int j = 0; j < TN; ++j) fb[slot][j].v = *reinterpret_cast<const bf16x8*>(stg + fb_off[s][j]);
+            for (int j = 0; j < TN; ++j) fb[slot][j].v = *reinterpret_cast<const bf16x8*>(pb[j & 1] + j * 4096);
         } else {
 #pragma unroll
-            for (int i = 0; i < TM; ++i) fa[slot][i].v = tr_frag(stg + fa_off[s][i], 4 * 2 * BM);
+            for (int i = 0; i < TM; ++i) fa[slot][i].v = tr_frag(stg + fa_off[i] + s * 32 * BM, 4 * 2 * BM);
 #pragma unroll
-            for (int j = 0; j < TN; ++j) fb[slot][j].v = tr_frag(stg + fb_off[s][j], 4 * 2 * BN);
+            for (int j = 0; j < TN; ++j) fb[slot][j].v = tr_frag(stg + fb_off[j] + s * 32 * BN, 4 * 2 * BN);
         }
     };
 

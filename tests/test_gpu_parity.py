@@ -443,15 +443,23 @@ def test_split_reduce_fused_into_layernorm_is_bitwise_identical(tile, splits, mo
     (GP_FUSE_RES_LN, on by default) sums the partials, residual and bias in the
     reduce kernel's order and normalises exactly as the LayerNorm kernel does:
     outputs, input gradient and every parameter gradient match the unfused
-    path bit for bit (split-K forced on every GEMM)."""
+    path bit for bit (split-K forced on every GEMM).  The single-stream
+    schedule, where the weight-gradient GEMMs share the workspace of a deferred
+    reduce and run it first, matches too."""
     monkeypatch.setenv("GP_GEMM_TILE", str(tile))
     monkeypatch.setenv("GP_GEMM_SPLITS", str(splits))
     monkeypatch.setenv("GP_FUSE_RES_LN", "1")
-    y1, dx1, g1 = _gpu_step(RAGGED_BF16, 5)
+    runs = [_gpu_step(RAGGED_BF16, 5)]
+    monkeypatch.setenv("GP_SIDE_STREAM", "0")
+    monkeypatch.setenv("GP_REMAT_AHEAD", "0")
+    runs.append(_gpu_step(RAGGED_BF16, 5))
+    monkeypatch.setenv("GP_SIDE_STREAM", "1")
+    monkeypatch.setenv("GP_REMAT_AHEAD", "1")
     monkeypatch.setenv("GP_FUSE_RES_LN", "0")
     y0, dx0, g0 = _gpu_step(RAGGED_BF16, 5)
-    assert np.array_equal(y1, y0)
-    assert np.array_equal(dx1, dx0)
-    for l, (a, b) in enumerate(zip(g1, g0)):
-        for k in a:
-            assert np.array_equal(a[k], b[k]), (l, k)
+    for y1, dx1, g1 in runs:
+        assert np.array_equal(y1, y0)
+        assert np.array_equal(dx1, dx0)
+        for l, (a, b) in enumerate(zip(g1, g0)):
+            for k in a:
+                assert np.array_equal(a[k], b[k]), (l, k)

@@ -750,14 +750,10 @@ int waves_for(long row_blocks) {
 // the row blocks alone would leave a SIMD with at most one wave (there the
 // one-wave kernels' serial chain sets the time; with more row blocks the two
 // forms tie or the split loses to the doubled wave count).
-// GP_ATTN_KSPLIT=0 keeps the one-wave kernels.
+// AttnArgs::split = 0 keeps the one-wave kernels.
 bool split_ok(const AttnArgs& a, long row_blocks, int loop_blocks) {
-    static const bool on = [] {
-        const char* e = std::getenv("GP_ATTN_KSPLIT");
-        return !e || std::atoi(e) != 0;
-    }();
     constexpr long SIMDS = 4 * 256;
-    return on && !a.causal && loop_blocks % 2 == 0 && row_blocks <= SIMDS;
+    return a.split && !a.causal && loop_blocks % 2 == 0 && row_blocks <= SIMDS;
 }
 
 // Launch KERNEL<NB, W> (split variants: 128 W threads) for an even block count NB <= 8.

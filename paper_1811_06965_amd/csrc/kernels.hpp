@@ -104,6 +104,7 @@ struct AttnArgs {
     void* dk = nullptr; long lddk = 0;
     void* dv = nullptr; long lddv = 0;
     float* delta = nullptr;                // [n, H, Sq] rowsum(dO * O) = rowsum(P * dP) scratch
+    int split = 1;                         // allow the two-wave (half-loop) kernels where they apply
 };
 gp_status attention_fwd(int dtype, const AttnArgs& a, hipStream_t st);
 gp_status attention_bwd(int dtype, const AttnArgs& a, hipStream_t st);

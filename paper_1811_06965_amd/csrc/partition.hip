@@ -190,6 +190,8 @@ struct gp_partition {
     bool remat_early = true;
     // split-K reduce of a residual GEMM fused into the next LayerNorm (GP_FUSE_RES_LN)
     bool fuse_res_ln = true;
+    // two-wave attention kernels where they apply (GP_ATTN_KSPLIT)
+    bool attn_split = true;
     hipStream_t remat = nullptr;
     hipEvent_t remat_done = nullptr;  // from evring
     int remat_pending = -1;  // micro-batch whose recompute-ahead is enqueued
@@ -574,6 +576,7 @@ AttnArgs attn_args(const gp_partition* p, int Sk, int causal) {
     a.dh = p->d.D / p->d.H;
     a.causal = causal;
     a.scale = 1.f / sqrtf((float)a.dh);
+    a.split = p->attn_split ? 1 : 0;
     return a;
 }
 
@@ -885,6 +888,7 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
     if (const char* e = std::getenv("GP_REMAT_AHEAD")) p->remat_ahead = std::atoi(e) != 0;
     if (const char* e = std::getenv("GP_REMAT_EARLY")) p->remat_early = std::atoi(e) != 0;
     if (const char* e = std::getenv("GP_FUSE_RES_LN")) p->fuse_res_ln = std::atoi(e) != 0;
+    if (const char* e = std::getenv("GP_ATTN_KSPLIT")) p->attn_split = std::atoi(e) != 0;
     if (const char* e = std::getenv("GP_DW_FLUSH")) p->dw_flush = std::atoi(e);
     p->nsets = (p->remat_ahead && g.M >= 2) ? 2 : 1;
     if (const char* e = std::getenv("GP_GEMM_TILE")) p->gemm_tile = std::atoi(e);

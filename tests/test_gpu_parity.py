@@ -95,6 +95,26 @@ def test_bf16_matches_oracle(cfg, perturb):
     _check(cfg, ref, res, 2e-2, "cos", 0.999)
 
 
+# attention loops over 6 key / query blocks (S = 192), and a cross-attention
+# whose 192-row memory gives 6 key blocks against 2 query blocks
+ENC192_BF16 = synth.PartitionConfig("enc192_bf16", layers=2, d_model=256, d_ff=512, heads=4, seq=192,
+                                    batch=4, micro=2, dtype="bf16", loss="none")
+DEC_MEM192_BF16 = synth.PartitionConfig("dec_mem192_bf16", layers=2, d_model=128, d_ff=256, heads=2, seq=64,
+                                        batch=4, micro=2, dtype="bf16", kind="decoder", loss="xent_ls",
+                                        vocab=512, label_smoothing=0.1, mem_seq=192)
+
+
+@pytest.mark.parametrize("ksplit", ["1", "0"], ids=["two_wave", "one_wave"])
+@pytest.mark.parametrize("cfg", [ENC192_BF16, DEC_MEM192_BF16], ids=lambda c: c.name)
+def test_bf16_attention_block_counts(cfg, ksplit, monkeypatch):
+    """Non-causal attention through the two-wave kernels (each wave over half
+    of the loop's blocks, here 3 of 6 or 1 of 2) and through the one-wave
+    kernels (GP_ATTN_KSPLIT=0), both against the oracle."""
+    monkeypatch.setenv("GP_ATTN_KSPLIT", ksplit)
+    case, ref, res = _run(cfg, 6, perturb=True)
+    _check(cfg, ref, res, 2e-2, "cos", 0.999)
+
+
 SHARED_ENC = synth.PartitionConfig("shared_enc", layers=2, d_model=512, d_ff=2048, heads=8, seq=256,
                                    batch=4, micro=2, dtype="bf16", loss="none")
 SHARED_DEC = synth.PartitionConfig("shared_dec", layers=2, d_model=128, d_ff=256, heads=2, seq=256, batch=4,

@@ -23,6 +23,19 @@ __global__ void __launch_bounds__(256) intake_kernel(const T* __restrict__ src, 
     }
 }
 
+// 8 bf16 elements per thread with 16-byte accesses (count % 8 == 0, aligned pointers).
+__global__ void __launch_bounds__(256) intake_bf16_v8(const bf16x8* __restrict__ src, bf16x8* __restrict__ stash,
+                                                      f32x4* __restrict__ x32, long n8) {
+    for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < n8; i += (long)gridDim.x * 256) {
+        const bf16x8 v = src[i];
+        if (stash) stash[i] = v;
+        if (x32) {
+            x32[2 * i] = f32x4{(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
+            x32[2 * i + 1] = f32x4{(float)v[4], (float)v[5], (float)v[6], (float)v[7]};
+        }
+    }
+}
+
 template <typename T>
 __global__ void __launch_bounds__(256) cast_kernel(const float* __restrict__ src, T* __restrict__ dst, long count) {
     for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < count; i += (long)gridDim.x * 256)
@@ -243,7 +256,11 @@ int loss_blocks() { return LOSS_BLOCKS; }
 int xent_partials(long rows) { return (int)rows; }
 
 gp_status intake(int dtype, const void* src, void* stash, float* x32, long count, hipStream_t st) {
-    if (dtype == GP_BF16)
+    auto a16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
+    if (dtype == GP_BF16 && count % 8 == 0 && a16(src) && a16(stash) && a16(x32)) {
+        klaunch(intake_bf16_v8, ew_grid(count / 8), 256, 0, st, reinterpret_cast<const bf16x8*>(src),
+                reinterpret_cast<bf16x8*>(stash), reinterpret_cast<f32x4*>(x32), count / 8);
+    } else if (dtype == GP_BF16)
         klaunch(intake_kernel<bf16>, ew_grid(count), 256, 0, st, reinterpret_cast<const bf16*>(src),
                                                              reinterpret_cast<bf16*>(stash), x32, count);
     else

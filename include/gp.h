@@ -75,6 +75,14 @@ typedef enum {
     GP_LOSS_XENT_LS = 2 /* final LayerNorm, [D, V] projection, label-smoothed cross-entropy / (N S) */
 } gp_loss;
 
+/* The one synchronous update of gp_accumulate_and_step.  The paper counts 12
+ * bytes per parameter because it trains with RMSProp (Table 1 caption):
+ * the parameter, its gradient and the running mean square. */
+typedef enum {
+    GP_OPT_SGD = 0,    /* W <- W - lr G */
+    GP_OPT_RMSPROP = 1 /* ms <- rho ms + (1 - rho) G^2;  W <- W - lr G / sqrt(ms + eps);  ms starts at 0 */
+} gp_optimizer;
+
 typedef struct {
     int seq_len;             /* S, tokens per sequence */
     int seqs_per_microbatch; /* n = N / M sequences in each micro-batch */
@@ -87,6 +95,17 @@ typedef struct {
     float label_smoothing;   /* GP_LOSS_XENT_LS: eps, target q = (1-eps) onehot + eps / V */
     float ln_eps;            /* LayerNorm epsilon inside the square root (e.g. 1e-5) */
     int check_finite;        /* nonzero: gp_accumulate_and_step checks G and syncs */
+    int keep_activations;    /* 0: re-materialise each micro-batch's forward inside its backward
+                                (Section 2.3); 1: keep every micro-batch's intermediates from its
+                                forward instead (no recompute; activation memory O(N L) rather than
+                                O(N + L N / M)), the stored-activation baseline */
+    int optimizer;           /* gp_optimizer */
+    float rms_decay;         /* GP_OPT_RMSPROP: rho in [0, 1) */
+    float rms_eps;           /* GP_OPT_RMSPROP: eps > 0, inside the square root */
+    float logit_clip;        /* GP_LOSS_XENT_LS: c > 0 clips every logit to [-c, c] before the softmax
+                                (Section 5: logit predictions are clipped when their magnitude
+                                exceeds a certain value); the gradient passes where |z| <= c.
+                                0 = off */
 } gp_config;
 
 /* Parameter tensors.  Matrices are logical [in, out] (y = x W + b); attention
@@ -203,6 +222,9 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
  *              and the call synchronises the stream.
  * With check_finite set the call synchronises, and if any gradient is
  * non-finite the update is skipped and GP_ERR_NONFINITE returned.
+ * GP_LOSS_XENT_LS: a label outside [0, V) is read as class 0 on the device
+ * and flagged; the next call that synchronises (loss_out non-NULL or
+ * check_finite) then skips the update and returns GP_ERR_INVALID_ARG.
  * GP_ERR_STATE: not all M backward micro-batches done.
  */
 gp_status gp_accumulate_and_step(gp_partition* p, float lr, double* loss_out, gp_stream stream);
@@ -256,13 +278,27 @@ gp_status gp_timer_read(gp_partition* p, int role, double* ms, long* launches, d
 /* Forget every recorded launch (the events are kept for reuse). */
 gp_status gp_timer_reset(gp_partition* p);
 
+/* Instrumentation (re-materialisation check, Section 2.3: the backward
+ * recomputes the same F_k): write the partition output F_k(x_mb) as
+ * re-materialised inside the most recent gp_backward_microbatch_remat call of
+ * this mini-batch (micro-batch mb), rounded to the partition dtype, into the
+ * caller's device buffer y [n, S, D].  Enqueued on `stream`, which must be the
+ * stream that backward call was given; valid until the next backward or step
+ * call, after which that recompute's workspace may be reused.  Recomputing
+ * with the kernels and launch shapes of the first pass, it equals the y that
+ * gp_forward_microbatch emitted for mb bit for bit.
+ * GP_ERR_INVALID_ARG: p or y NULL.  GP_ERR_STATE: not configured, or no
+ * backward micro-batch has run since the last step. */
+gp_status gp_recomputed_output(gp_partition* p, void* y, gp_stream stream);
+
 /* Instrumentation: the sustained bf16 MFMA rate of the current device, the
  * reference for "fraction of the measured MFMA peak".  Runs a register-only
  * loop of v_mfma_f32_32x32x16_bf16 (pseudo-random operands, 8 independent
  * accumulators per wave, two 4-wave workgroups per CU) on `stream` (a
  * hipStream_t; NULL = the null stream), waits for it, and stores the best of
  * three timed runs (after a warm-up run) in *tflops, in TFLOP/s.  Allocates a
- * small output buffer stream-ordered and frees it.
+ * small output buffer with hipMalloc and frees it with hipFree (so it must not
+ * be called under stream capture).
  * GP_ERR_INVALID_ARG: tflops is NULL; GP_ERR_HIP: a launch or event failed. */
 gp_status gp_mfma_peak(void* stream, double* tflops);
 

@@ -16,7 +16,9 @@ Readings where the paper is silent:
   * the backward pass visits the micro-batches in reverse order M-1 .. 0;
   * losses are normalised by the whole mini-batch, so the accumulated
     gradient is applied undivided;
-  * the update is plain SGD, W' = W - lr G.
+  * the update is plain SGD, W' = W - lr G, or RMSProp (the optimizer behind
+    the 12 bytes per parameter of Table 1) with its running mean square
+    starting at 0 and eps inside the square root.
 """
 from __future__ import annotations
 
@@ -62,7 +64,7 @@ def loss_and_grad(cfg, head, y, case_slice, norm):
         return loss, dy, {}
     if cfg.loss == "xent_ls":
         return tf.xent_ls_head(y, case_slice["labels"], head, cfg.label_smoothing,
-                               cfg.ln_eps, norm)
+                               cfg.ln_eps, norm, cfg.logit_clip)
     if cfg.loss == "none":
         loss, dy = tf.boundary_loss(y, case_slice["dy"])
         return loss, dy, {}
@@ -99,23 +101,57 @@ def sgd_update(layers, head, g_layers, g_head, lr):
     return new_layers, new_head
 
 
-def minibatch_step(cfg, case, lr=0.0):
+def rmsprop_tensor(w, g, ms, lr, rho, eps):
+    """RMSProp on one tensor (the optimizer of the paper's Table 1 runs, which
+    keeps a running mean square of each gradient): ms' = rho ms + (1 - rho) g^2,
+    w' = w - lr g / sqrt(ms' + eps).  Returns (w', ms')."""
+    ms_new = rho * ms + (1.0 - rho) * g * g
+    return w - lr * g / np.sqrt(ms_new + eps), ms_new
+
+
+def optimizer_state(layers, head):
+    """Initial RMSProp state: every running mean square starts at 0."""
+    return _zeros_like_grads(layers, head)
+
+
+def apply_update(cfg, layers, head, g_layers, g_head, lr, state=None):
+    """The one synchronous update of the configured optimizer.  Returns
+    (layers', head', state') -- state' is None for SGD."""
+    if cfg.optimizer == "sgd":
+        return (*sgd_update(layers, head, g_layers, g_head, lr), None)
+    if cfg.optimizer != "rmsprop":
+        raise ValueError(cfg.optimizer)
+    ms_layers, ms_head = optimizer_state(layers, head) if state is None else state
+    new_layers, new_ms_layers = [], []
+    for p, g, ms in zip(layers, g_layers, ms_layers):
+        upd = {k: rmsprop_tensor(p[k], g[k], ms[k], lr, cfg.rms_decay, cfg.rms_eps) for k in p}
+        new_layers.append({k: v[0] for k, v in upd.items()})
+        new_ms_layers.append({k: v[1] for k, v in upd.items()})
+    upd = {k: rmsprop_tensor(head[k], g_head[k], ms_head[k], lr, cfg.rms_decay, cfg.rms_eps) for k in head}
+    new_head = {k: v[0] for k, v in upd.items()}
+    new_ms_head = {k: v[1] for k, v in upd.items()}
+    return new_layers, new_head, (new_ms_layers, new_ms_head)
+
+
+def minibatch_step(cfg, case, lr=0.0, opt_state=None):
     """The plain definition: the whole mini-batch in one pass, activations stored.
 
-    Returns dict(y, dx, dmem, loss, grads, head_grads, layers, head) where
-    ``layers``/``head`` are the updated parameters."""
+    Returns dict(y, dx, dmem, loss, grads, head_grads, layers, head, opt_state)
+    where ``layers``/``head`` are the updated parameters and ``opt_state`` the
+    optimizer's state after the update (None for SGD; ``opt_state`` in: the
+    state before it, None for a fresh one)."""
     layers, head = case["layers"], case["head"]
     N = case["x"].shape[0]
     y, caches = partition_forward(cfg, layers, case["x"], case["mem"])
     loss, dy, g_head = loss_and_grad(cfg, head, y, _slice(case, 0, N), loss_norm(cfg, N))
     dx, dmem, g_layers = partition_backward(cfg, layers, caches, dy)
-    new_layers, new_head = sgd_update(layers, head, g_layers,
-                                      {k: g_head[k] for k in head}, lr)
+    new_layers, new_head, state = apply_update(cfg, layers, head, g_layers,
+                                               {k: g_head[k] for k in head}, lr, opt_state)
     return dict(y=y, dx=dx, dmem=dmem, loss=loss, grads=g_layers, head_grads=g_head,
-                layers=new_layers, head=new_head)
+                layers=new_layers, head=new_head, opt_state=state)
 
 
-def gpipe_step(cfg, case, M, lr=0.0, remat=True, trace=None):
+def gpipe_step(cfg, case, M, lr=0.0, remat=True, trace=None, opt_state=None):
     """One partition's share of a GPipe mini-batch step (Sections 2.2-2.3).
 
       1. split the N examples into M equal micro-batches (N % M must be 0);
@@ -125,7 +161,7 @@ def gpipe_step(cfg, case, M, lr=0.0, remat=True, trace=None):
       3. backward m = M-1 .. 0: re-run F_k from the stash to rebuild the
          intermediates (``remat``), take dL/dy_m from the loss head or the
          boundary, run B_k and add each parameter gradient into G;
-      4. apply G once: W' = W - lr G.
+      4. apply G once: W' = W - lr G (or the RMSProp step of ``apply_update``).
 
     ``trace``, when a list, receives ("fwd"|"remat"|"bwd", m) events in order.
     Returns the same dict as ``minibatch_step`` (y, dx, dmem concatenated over
@@ -168,10 +204,11 @@ def gpipe_step(cfg, case, M, lr=0.0, remat=True, trace=None):
             G_head[k] += gh[k]
         if trace is not None:
             trace.append(("bwd", m))
-    new_layers, new_head = sgd_update(layers, head, G, G_head, lr)
+    new_layers, new_head, state = apply_update(cfg, layers, head, G, G_head, lr, opt_state)
     return dict(y=np.concatenate(ys), dx=np.concatenate(dxs),
                 dmem=None if cfg.kind != "decoder" else np.concatenate(dmems),
-                loss=loss, grads=G, head_grads=G_head, layers=new_layers, head=new_head)
+                loss=loss, grads=G, head_grads=G_head, layers=new_layers, head=new_head,
+                opt_state=state)
 
 
 def partition_output(cfg, layers, x, mem):

@@ -198,22 +198,33 @@ def mse_loss(y, target, norm):
     return float((d * d).sum() / norm), 2.0 * d / norm
 
 
-def xent_ls_head(y, labels, hp, ls, eps, norm):
-    """Final LayerNorm, vocabulary projection and label-smoothed cross-entropy.
+def clip_logits(Z, c):
+    """Section 5: logit predictions (the softmax pre-activations) are clipped
+    when their magnitude exceeds c.  Returns min(max(Z, -c), c) and the clip's
+    derivative, 1 where -c <= Z <= c and 0 elsewhere; c = 0 means no clip."""
+    if c <= 0.0:
+        return Z, np.ones_like(Z)
+    return np.clip(Z, -c, c), (np.abs(Z) <= c).astype(Z.dtype)
+
+
+def xent_ls_head(y, labels, hp, ls, eps, norm, clip=0.0):
+    """Final LayerNorm, vocabulary projection, optional logit clipping and
+    label-smoothed cross-entropy.
 
     q = (1 - ls) onehot(label) + ls / V over all V classes;  loss = -sum q log p
     summed over tokens and divided by ``norm`` (tokens of the whole mini-batch).
     Returns (loss, dy, head grads).
     """
     h, lnf = layer_norm(y, hp["lnf_g"], hp["lnf_b"], eps)
-    Z = linear(h, hp["wout"], hp["bout"])
+    Zraw = linear(h, hp["wout"], hp["bout"])
+    Z, dclip = clip_logits(Zraw, clip)
     V = Z.shape[-1]
     Zs = Z - Z.max(axis=-1, keepdims=True)
     logp = Zs - np.log(np.exp(Zs).sum(axis=-1, keepdims=True))
     q = np.full(Z.shape, ls / V)
     np.put_along_axis(q, labels[..., None].astype(np.int64), 1.0 - ls + ls / V, axis=-1)
     loss = float(-(q * logp).sum() / norm)
-    dZ = (np.exp(logp) - q) / norm
+    dZ = (np.exp(logp) - q) / norm * dclip
     g = {}
     dh, g["wout"], g["bout"] = linear_backward(dZ, h, hp["wout"])
     dy, g["lnf_g"], g["lnf_b"] = layer_norm_backward(dh, lnf, hp["lnf_g"])

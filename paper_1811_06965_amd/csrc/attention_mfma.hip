@@ -32,7 +32,6 @@
 // transposed from the row-major LDS tile with the matching k order (two runs
 // of four consecutive rows per lane).  A workgroup holds 1, 2 or 4 waves,
 // chosen so that small micro-batches still launch enough workgroups.
-#include <cstdlib>
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -732,15 +731,10 @@ __global__ void __launch_bounds__(128 * KW) attn_bwd_dkv_ks(AttnArgs a) {
 
 // Waves per workgroup (32 rows each): as many as keep at least 2 x NUM_CU
 // workgroups for a small batch, at most 4 (fewer waves per workgroup re-stage
-// the head's keys and values more often).
-int waves_for(long row_blocks) {
-    // GP_ATTN_WAVES (1, 2 or 4) forces the waves per workgroup (tuning)
-    static const int forced = [] {
-        const char* e = std::getenv("GP_ATTN_WAVES");
-        const int v = e ? std::atoi(e) : 0;
-        return v == 1 || v == 2 || v == 4 ? v : 0;
-    }();
-    if (forced) return forced;
+// the head's keys and values more often).  AttnArgs::waves (1, 2 or 4)
+// overrides the choice.
+int waves_for(const AttnArgs& a, long row_blocks) {
+    if (a.waves == 1 || a.waves == 2 || a.waves == 4) return a.waves;
     constexpr long CU2 = 2 * 256;
     return row_blocks >= 4 * CU2 ? 4 : row_blocks >= 2 * CU2 ? 2 : 1;
 }
@@ -784,7 +778,7 @@ bool mfma_ok(const AttnArgs& a) {
 gp_status attention_fwd(int dtype, const AttnArgs& a, hipStream_t st) {
     if (dtype != GP_BF16) return attention_fwd_simt(dtype, a, st);
     if (!mfma_ok(a)) return set_error(GP_ERR_UNSUPPORTED, "bf16 attention needs d_h = 64 and lengths multiple of 32, <= 256");
-    const int w = waves_for((long)(a.Sq / 32) * a.n * a.H);
+    const int w = waves_for(a, (long)(a.Sq / 32) * a.n * a.H);
     dim3 grid((a.Sq + 32 * w - 1) / (32 * w), a.n * a.H);
     if (split_ok(a, (long)(a.Sq / 32) * a.n * a.H, a.Sk / 32)) {
         GP_KS_SWITCH(a.Sk / 32, w, attn_fwd_ks, grid);
@@ -798,7 +792,7 @@ gp_status attention_fwd(int dtype, const AttnArgs& a, hipStream_t st) {
 gp_status attention_bwd(int dtype, const AttnArgs& a, hipStream_t st) {
     if (dtype != GP_BF16) return attention_bwd_simt(dtype, a, st);
     if (!mfma_ok(a)) return set_error(GP_ERR_UNSUPPORTED, "bf16 attention needs d_h = 64 and lengths multiple of 32, <= 256");
-    const int wq = waves_for((long)(a.Sq / 32) * a.n * a.H);
+    const int wq = waves_for(a, (long)(a.Sq / 32) * a.n * a.H);
     dim3 gq((a.Sq + 32 * wq - 1) / (32 * wq), a.n * a.H);
     if (split_ok(a, (long)(a.Sq / 32) * a.n * a.H, a.Sk / 32)) {
         GP_KS_SWITCH(a.Sk / 32, wq, attn_bwd_dq_ks, gq);
@@ -806,7 +800,7 @@ gp_status attention_bwd(int dtype, const AttnArgs& a, hipStream_t st) {
         GP_WC_SWITCH(a.Sk / 32, wq, a.causal, attn_bwd_dq_mfma, gq);
     }
     GP_LAUNCH_CHECK();
-    const int wk = waves_for((long)(a.Sk / 32) * a.n * a.H);
+    const int wk = waves_for(a, (long)(a.Sk / 32) * a.n * a.H);
     dim3 gk((a.Sk + 32 * wk - 1) / (32 * wk), a.n * a.H);
     if (split_ok(a, (long)(a.Sk / 32) * a.n * a.H, a.Sq / 32)) {
         GP_KS_SWITCH(a.Sq / 32, wk, attn_bwd_dkv_ks, gk);

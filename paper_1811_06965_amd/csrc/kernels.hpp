@@ -105,6 +105,7 @@ struct AttnArgs {
     void* dv = nullptr; long lddv = 0;
     float* delta = nullptr;                // [n, H, Sq] rowsum(dO * O) = rowsum(P * dP) scratch
     int split = 1;                         // allow the two-wave (half-loop) kernels where they apply
+    int waves = 0;                         // waves (32-row blocks) per workgroup: 1, 2 or 4; 0 = by grid size
 };
 gp_status attention_fwd(int dtype, const AttnArgs& a, hipStream_t st);
 gp_status attention_bwd(int dtype, const AttnArgs& a, hipStream_t st);
@@ -123,9 +124,11 @@ gp_status loss_finalize(const double* partial, int nblk, double* acc, int accumu
 
 // Label-smoothed softmax cross-entropy over rows of V logits (f32 or elt in
 // z, overwritten by dZ in the elt type): dZ = (softmax(z) - q) / norm,
-// partial[row] += -sum q log p / norm in fp64.
-gp_status xent_ls(int dtype, void* z, long rows, int V, const int* labels, float ls, double norm,
-                  double* partial, hipStream_t st);
+// partial[row] = -sum q log p / norm in fp64.  A label outside [0, V) is read
+// as 0 and sets bad_label[0] = 1.  clip > 0: the logits are clipped to
+// [-clip, clip] first, and dZ is zero where |z| > clip.
+gp_status xent_ls(int dtype, void* z, long rows, int V, const int* labels, float ls, float clip, double norm,
+                  double* partial, int* bad_label, hipStream_t st);
 int xent_partials(long rows);
 
 // --------------------------------------------------------------- update
@@ -134,6 +137,9 @@ int xent_partials(long rows);
 // (best of three timed runs after one warm-up), in TFLOP/s; synchronises st.
 gp_status mfma_peak(hipStream_t st, double* tflops);
 gp_status sgd_update(float* w, const float* g, float lr, long count, hipStream_t st);
+// ms = rho ms + (1 - rho) g^2;  w -= lr g / sqrt(ms + eps)  (count % 4 == 0, 16-byte aligned).
+gp_status rmsprop_update(float* w, const float* g, float* ms, float lr, float rho, float eps, long count,
+                         hipStream_t st);
 // Working copies of one linear layer from its fp32 master W [in, out]:
 // kn (elt) = W, nk (elt) = W^T.
 // kn = W [in, out]; nk = W^T [out, in]; q4 / q4s (optional, bf16): the rows of

@@ -74,17 +74,24 @@ __global__ void loss_finalize_kernel(const double* __restrict__ partial, int nbl
 // q_v = ls / V + (1 - ls) [v == label];  loss_row = -sum_v q_v log p_v
 //   = lse - ls / V sum_v z_v - (1 - ls) z_label,   lse = log sum_v exp z_v;
 // dZ_v = (p_v - q_v) / norm.
+// With clip > 0 every logit first becomes min(max(z, -clip), clip) and the
+// gradient passes only where |z| <= clip (the clip's derivative).
+// A label outside [0, V) is read as class 0 (so every access stays inside
+// the row) and raises bad_label[0], which the host reports.
 template <typename T>
 __global__ void __launch_bounds__(256) xent_kernel(T* __restrict__ z, int V, const int* __restrict__ labels,
-                                                   float ls, double norm, double* __restrict__ partial) {
+                                                   float ls, float clip, double norm, double* __restrict__ partial,
+                                                   int* __restrict__ bad_label) {
     __shared__ float red[4];
     __shared__ float bc[2];
     const long row = blockIdx.x;
     T* zr = z + row * (long)V;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const float lim = clip > 0.f ? clip : INFINITY;
+    auto logit = [&](int v) { return fminf(fmaxf(to_f32(zr[v]), -lim), lim); };
     float m = -INFINITY, sz = 0.f;
     for (int v = tid; v < V; v += 256) {
-        const float x = to_f32(zr[v]);
+        const float x = logit(v);
         m = fmaxf(m, x);
         sz += x;
     }
@@ -102,7 +109,7 @@ __global__ void __launch_bounds__(256) xent_kernel(T* __restrict__ z, int V, con
     __syncthreads();
     sz = bc[1];
     float se = 0.f;
-    for (int v = tid; v < V; v += 256) se += expf(to_f32(zr[v]) - m);
+    for (int v = tid; v < V; v += 256) se += expf(logit(v) - m);
     se = wave_sum(se);
     __syncthreads();
     if (lane == 0) red[w] = se;
@@ -110,15 +117,19 @@ __global__ void __launch_bounds__(256) xent_kernel(T* __restrict__ z, int V, con
     if (tid == 0) bc[0] = red[0] + red[1] + red[2] + red[3];
     __syncthreads();
     se = bc[0];
-    const int lab = labels[row];
-    const float zl = to_f32(zr[lab]);
+    const int raw = labels[row];
+    const bool ok = raw >= 0 && raw < V;
+    const int lab = ok ? raw : 0;
+    if (!ok && tid == 0) bad_label[0] = 1;
+    const float zl = logit(lab);
     __syncthreads();
     const float lse = m + logf(se);
     const float inv = 1.f / se, u = ls / V, gn = (float)(1.0 / norm);
     for (int v = tid; v < V; v += 256) {
-        const float p = expf(to_f32(zr[v]) - m) * inv;
+        const float z = to_f32(zr[v]);
+        const float p = expf(fminf(fmaxf(z, -lim), lim) - m) * inv;
         const float q = u + (v == lab ? 1.f - ls : 0.f);
-        zr[v] = to_elt<T>((p - q) * gn);
+        zr[v] = to_elt<T>(fabsf(z) <= lim ? (p - q) * gn : 0.f);
     }
     if (tid == 0) partial[row] = ((double)lse - (double)u * sz - (1.0 - ls) * zl) / norm;
 }
@@ -126,6 +137,25 @@ __global__ void __launch_bounds__(256) xent_kernel(T* __restrict__ z, int V, con
 __global__ void __launch_bounds__(256) sgd_kernel(float* __restrict__ w, const float* __restrict__ g, float lr,
                                                   long count) {
     for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < count; i += (long)gridDim.x * 256) w[i] -= lr * g[i];
+}
+
+// RMSProp: ms <- rho ms + (1 - rho) g^2;  w <- w - lr g / sqrt(ms + eps).
+// Four parameters per thread with 16-byte accesses (count % 4 == 0: every
+// parameter block of the plan is 64-float aligned).
+__global__ void __launch_bounds__(256) rmsprop_kernel(f32x4* __restrict__ w, const f32x4* __restrict__ g,
+                                                      f32x4* __restrict__ ms, float lr, float rho, float eps,
+                                                      long n4) {
+    for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < n4; i += (long)gridDim.x * 256) {
+        const f32x4 gv = g[i];
+        f32x4 m = ms[i], wv = w[i];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            m[e] = rho * m[e] + (1.f - rho) * (gv[e] * gv[e]);
+            wv[e] -= lr * gv[e] / sqrtf(m[e] + eps);
+        }
+        ms[i] = m;
+        w[i] = wv;
+    }
 }
 
 // kn = W, nk = W^T through a 64 x 64 LDS tile (both writes coalesced).
@@ -296,12 +326,14 @@ gp_status loss_finalize(const double* partial, int nblk, double* acc, int accumu
     return GP_OK;
 }
 
-gp_status xent_ls(int dtype, void* z, long rows, int V, const int* labels, float ls, double norm, double* partial,
-                  hipStream_t st) {
+gp_status xent_ls(int dtype, void* z, long rows, int V, const int* labels, float ls, float clip, double norm,
+                  double* partial, int* bad_label, hipStream_t st) {
     if (dtype == GP_BF16)
-        klaunch(xent_kernel<bf16>, (unsigned)rows, 256, 0, st, reinterpret_cast<bf16*>(z), V, labels, ls, norm, partial);
+        klaunch(xent_kernel<bf16>, (unsigned)rows, 256, 0, st, reinterpret_cast<bf16*>(z), V, labels, ls, clip, norm,
+                partial, bad_label);
     else
-        klaunch(xent_kernel<float>, (unsigned)rows, 256, 0, st, reinterpret_cast<float*>(z), V, labels, ls, norm, partial);
+        klaunch(xent_kernel<float>, (unsigned)rows, 256, 0, st, reinterpret_cast<float*>(z), V, labels, ls, clip, norm,
+                partial, bad_label);
     GP_LAUNCH_CHECK();
     return GP_OK;
 }
@@ -340,6 +372,15 @@ gp_status mfma_peak(hipStream_t st, double* tflops) {
 
 gp_status sgd_update(float* w, const float* g, float lr, long count, hipStream_t st) {
     klaunch(sgd_kernel, ew_grid(count), 256, 0, st, w, g, lr, count);
+    GP_LAUNCH_CHECK();
+    return GP_OK;
+}
+
+gp_status rmsprop_update(float* w, const float* g, float* ms, float lr, float rho, float eps, long count,
+                         hipStream_t st) {
+    if (count % 4) return set_error(GP_ERR_INVALID_ARG, "rmsprop: parameter count must be a multiple of 4");
+    klaunch(rmsprop_kernel, ew_grid(count / 4), 256, 0, st, reinterpret_cast<f32x4*>(w),
+            reinterpret_cast<const f32x4*>(g), reinterpret_cast<f32x4*>(ms), lr, rho, eps, count / 4);
     GP_LAUNCH_CHECK();
     return GP_OK;
 }

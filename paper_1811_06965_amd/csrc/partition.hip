@@ -84,6 +84,7 @@ struct BwdWs {
     void *dz[2] = {}, *dqkv[2] = {}, *dxq[2] = {}, *dxkv[2] = {};  // by layer parity
     double *loss_partial = nullptr, *loss_acc = nullptr;
     int* flag = nullptr;
+    int* bad_label = nullptr;  // set by the cross-entropy head on a label outside [0, V)
     float* splitk = nullptr;   // split-K partial tiles (caller's stream)
     float* splitk_side = nullptr;  // split-K partial tiles of the weight-gradient stream
     float* splitk_remat = nullptr; // split-K partial tiles of the recompute-ahead stream
@@ -147,9 +148,11 @@ struct gp_partition {
     char* stash_x = nullptr;
     char* stash_m = nullptr;
     char* ws = nullptr;
-    std::vector<float*> xs[2];
-    std::vector<LayerWs> lw[2];
+    // workspace sets: set s holds a residual stream xs[s][0..L] and layer slots lw[s][0..L-1]
+    std::vector<std::vector<float*>> xs;
+    std::vector<std::vector<LayerWs>> lw;
     int nsets = 1;
+    float* opt_ms = nullptr;  // RMSProp: running mean square of every gradient [n32]
     // per LayerNorm: block partial sums of its gamma/beta gradients, added up
     // over the micro-batches of a mini-batch and reduced after the last one
     std::vector<float*> lnpart;
@@ -192,10 +195,16 @@ struct gp_partition {
     bool fuse_res_ln = true;
     // two-wave attention kernels where they apply (GP_ATTN_KSPLIT)
     bool attn_split = true;
+    // attention waves per workgroup (GP_ATTN_WAVES = 1, 2 or 4; 0: by grid size)
+    int attn_waves = 0;
     hipStream_t remat = nullptr;
     hipEvent_t remat_done = nullptr;  // from evring
     int remat_pending = -1;  // micro-batch whose recompute-ahead is enqueued
 
+    // Workspace set of micro-batch m: its own set when activations are kept,
+    // else set m % 2 with recompute-ahead (two sets) or set 0.
+    int set_of(int m) const { return g.keep_act ? m : (nsets > 1 ? (m & 1) : 0); }
+    bool ahead() const { return !g.keep_act && nsets > 1; }  // recompute-ahead / early-recompute stream in use
     void* W(size_t elt_off) const { return welt + elt_off * esz; }
     char* stash_x_mb(int m) const { return stash_x + (size_t)m * g.T() * d.D * esz; }
     char* stash_m_mb(int m) const { return stash_m + (size_t)m * g.Tm() * d.D * esz; }
@@ -213,10 +222,8 @@ void plan_workspace(gp_partition* p, Arena& a) {
     const long lse_n = (long)g.n * d.H * g.S;
     const size_t e = p->esz;
     const bool dec = g.kind == GP_DECODER_CROSS;
-    for (int set = 0; set < 2; ++set) {
-        p->xs[set].assign(set < p->nsets ? d.L + 1 : 0, nullptr);
-        p->lw[set].assign(set < p->nsets ? d.L : 0, LayerWs{});
-    }
+    p->xs.assign(p->nsets, std::vector<float*>(d.L + 1, nullptr));
+    p->lw.assign(p->nsets, std::vector<LayerWs>(d.L, LayerWs{}));
     for (int set = 0; set < p->nsets; ++set)
         for (auto& x : p->xs[set]) x = a.take<float>(T * D);
     for (int set = 0; set < p->nsets; ++set) {
@@ -279,12 +286,13 @@ void plan_workspace(gp_partition* p, Arena& a) {
     b.splitk_elems = std::max<long>(8 * T * D, 8 * (3 * D * D + 3 * D));
     b.splitk = a.take<float>((size_t)b.splitk_elems);
     b.splitk_side = a.take<float>((size_t)b.splitk_elems);
-    if (p->nsets > 1) b.splitk_remat = a.take<float>((size_t)b.splitk_elems);
+    if (p->ahead()) b.splitk_remat = a.take<float>((size_t)b.splitk_elems);
     size_t lp = (size_t)loss_blocks();
     if (g.loss == GP_LOSS_XENT_LS && (size_t)xent_partials(T) > lp) lp = xent_partials(T);
     b.loss_partial = a.take<double>(lp);
     b.loss_acc = a.take<double>(1);
     b.flag = a.take<int>(1);
+    b.bad_label = a.take<int>(1);
     if (g.loss == GP_LOSS_XENT_LS) {
         b.sth = a.take<float>(2 * T);
         b.h = a.take_elt(T * D, e);
@@ -577,6 +585,7 @@ AttnArgs attn_args(const gp_partition* p, int Sk, int causal) {
     a.causal = causal;
     a.scale = 1.f / sqrtf((float)a.dh);
     a.split = p->attn_split ? 1 : 0;
+    a.waves = p->attn_waves;
     return a;
 }
 
@@ -584,7 +593,7 @@ AttnArgs attn_args(const gp_partition* p, int Sk, int causal) {
 // stream; mem is the decoder memory (elt [Tm, D]); y_out (optional) receives
 // the output rounded to the partition dtype.
 gp_status layer_forward(const Ctx& c, int l, LayerWs& w, const float* x_in, float* x_out, const void* mem,
-                        void* y_out, bool keep) {
+                        void* y_out) {
     gp_partition* p = c.p;
     const LayerPlan& P = p->plan.layers[l];
     const long T = p->g.T(), D = p->d.D;
@@ -624,9 +633,11 @@ GP_TRY(timed_attention(c, GP_K_ATTN_FWD, a, false));
     }
     // feed-forward block
     const Norm& nf = dec ? P.ln3 : P.ln2;
-    // The fp4 correction serves the ReLU mask that the backward takes from the
-    // recomputed forward; the first forward's output only leaves the partition.
-    const bool s4 = P.ffn1.split && keep;
+    // The fp4 correction of the bf16-rounded LayerNorm output runs in the
+    // first pass and in the recompute alike, so that the recompute reproduces
+    // the first pass bit for bit (the backward differentiates the very F_k
+    // whose output left the partition).
+    const bool s4 = P.ffn1.split;
     GP_TRY(timed_ln_fwd(c, xf, T, (int)D, p->master + nf.g, p->master + nf.b, eps, w.v, w.stf, s4 ? w.v4 : nullptr,
                         s4 ? w.v4s : nullptr));
     GP_TRY(linear_fwd(c, P.ffn1, w.v, T, w.a, p->d.F, EPI_STORE, 1, nullptr, nullptr, s4 ? w.v4 : nullptr,
@@ -636,16 +647,18 @@ GP_TRY(timed_attention(c, GP_K_ATTN_FWD, a, false));
     return GP_OK;
 }
 
-// Forward of micro-batch m through all layers.  keep = false: first pass,
-// intermediates discarded (slot 0, ping-pong residuals); keep = true:
-// re-materialisation from the stash, intermediates kept per layer.
+// Forward of micro-batch m through all layers, in workspace set `set`.
+// x != nullptr: a first pass -- x (and mem) go into the stash unless
+// skip_intake, and y (optional) receives the output; x == nullptr: the
+// re-materialisation from the stash.  keep = false: intermediates discarded
+// (slot 0, ping-pong residuals); keep = true: intermediates kept per layer.
 gp_status partition_forward(const Ctx& c, int m, bool keep, const void* x, const void* mem, void* y, int set = 0,
                             bool skip_intake = false) {
     gp_partition* p = c.p;
     const long T = p->g.T(), D = p->d.D;
     const int L = p->d.L;
     std::vector<float*>& xs = p->xs[set];
-    if (!keep) {
+    if (x) {
         if (!skip_intake) {
             GP_TRY(intake(c.dt, x, p->stash_x_mb(m), xs[0], T * D, c.st));
             if (mem) GP_TRY(intake(c.dt, mem, p->stash_m_mb(m), nullptr, p->g.Tm() * D, c.st));
@@ -661,7 +674,7 @@ gp_status partition_forward(const Ctx& c, int m, bool keep, const void* x, const
         LayerWs& w = keep ? p->lw[set][l] : p->lw[set][0];
         const float* xi = keep ? xs[l] : xs[l & 1];
         float* xo = keep ? xs[l + 1] : xs[(l + 1) & 1];
-        GP_TRY(layer_forward(cf, l, w, xi, xo, mem_m, (!keep && l == L - 1) ? y : nullptr, keep));
+        GP_TRY(layer_forward(cf, l, w, xi, xo, mem_m, l == L - 1 ? y : nullptr));
     }
     return flush_pending(cf);
 }
@@ -789,7 +802,7 @@ gp_status head_backward(const Ctx& c, int set, bool first, const int* labels) {
     GP_TRY(timed_ln_fwd(c, y, T, (int)D, p->master + Hd.lnf.g, p->master + Hd.lnf.b, p->g.eps, b.h, b.sth));
     GP_TRY(linear_fwd(c, Hd.out, b.h, T, b.z, V, EPI_STORE, 0, nullptr, nullptr));
     const double norm = (double)p->g.n * p->g.M * p->g.S;
-    GP_TRY(xent_ls(c.dt, b.z, T, (int)V, labels, p->g.ls, norm, b.loss_partial, c.st));
+    GP_TRY(xent_ls(c.dt, b.z, T, (int)V, labels, p->g.ls, p->g.logit_clip, norm, b.loss_partial, b.bad_label, c.st));
     GP_TRY(loss_finalize(b.loss_partial, (int)T, b.loss_acc, acc, c.st));
     GP_TRY(linear_dw(c, Hd.out, b.h, b.z, T, acc));
     GP_TRY(linear_dx(c, Hd.out, b.z, T, b.dn, EPI_F32, nullptr, 0));
@@ -825,9 +838,9 @@ void free_all(gp_partition* p) {
     p->timer = LaunchTimer();
     p->timer.markers = markers;
     for (void* x : {(void*)p->master, (void*)p->grads, (void*)p->welt, (void*)p->stash_x, (void*)p->stash_m,
-                    (void*)p->ws})
+                    (void*)p->ws, (void*)p->opt_ms})
         if (x) (void)hipFree(x);
-    p->master = p->grads = nullptr;
+    p->master = p->grads = p->opt_ms = nullptr;
     p->welt = p->stash_x = p->stash_m = p->ws = nullptr;
 }
 
@@ -889,15 +902,24 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
     if (const char* e = std::getenv("GP_REMAT_EARLY")) p->remat_early = std::atoi(e) != 0;
     if (const char* e = std::getenv("GP_FUSE_RES_LN")) p->fuse_res_ln = std::atoi(e) != 0;
     if (const char* e = std::getenv("GP_ATTN_KSPLIT")) p->attn_split = std::atoi(e) != 0;
+    if (const char* e = std::getenv("GP_ATTN_WAVES")) p->attn_waves = std::atoi(e);
     if (const char* e = std::getenv("GP_DW_FLUSH")) p->dw_flush = std::atoi(e);
-    p->nsets = (p->remat_ahead && g.M >= 2) ? 2 : 1;
+    g.keep_act = cfg->keep_activations;
+    g.optimizer = cfg->optimizer;
+    g.rms_decay = cfg->rms_decay;
+    g.rms_eps = cfg->rms_eps;
+    g.logit_clip = cfg->logit_clip;
+    // one workspace set per micro-batch when activations are kept, else two
+    // (recompute-ahead) or one
+    p->nsets = g.keep_act ? g.M : (p->remat_ahead && g.M >= 2) ? 2 : 1;
     if (const char* e = std::getenv("GP_GEMM_TILE")) p->gemm_tile = std::atoi(e);
     if (const char* e = std::getenv("GP_GEMM_SPLITS")) p->gemm_splits = std::atoi(e);
     if (const char* e = std::getenv("GP_FFN_FP4")) g.ffn_fp4 = std::atoi(e) != 0;
     p->plan = plan_params(p->d, g);
     Arena measure;
     plan_workspace(p, measure);
-    p->bytes_params = p->plan.n32 * 4 + p->plan.nelt * p->esz;
+    const bool rms = g.optimizer == GP_OPT_RMSPROP;
+    p->bytes_params = p->plan.n32 * 4 * (rms ? 2 : 1) + p->plan.nelt * p->esz;
     p->bytes_grads = p->plan.n32 * 4;
     p->bytes_stash = (size_t)g.M * (g.T() + g.Tm()) * p->d.D * p->esz;
     p->bytes_ws = measure.off;
@@ -908,6 +930,9 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
     if (s == GP_OK) s = alloc(&sx, (size_t)g.M * g.T() * p->d.D * p->esz);
     if (s == GP_OK && g.Tm() > 0) s = alloc(&sm, (size_t)g.M * g.Tm() * p->d.D * p->esz);
     if (s == GP_OK) s = alloc(&ws, p->bytes_ws);
+    void* ms = nullptr;
+    if (s == GP_OK && rms) s = alloc(&ms, p->plan.n32 * 4);
+    p->opt_ms = (float*)ms;
     p->master = (float*)m;
     p->grads = (float*)gr;
     p->welt = (char*)we;
@@ -928,6 +953,7 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
     hipError_t e = hipMemcpy(p->master, init.data(), p->plan.n32 * 4, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemset(p->grads, 0, p->plan.n32 * 4);
     if (e == hipSuccess) e = hipMemset(p->ws, 0, p->bytes_ws);
+    if (e == hipSuccess && p->opt_ms) e = hipMemset(p->opt_ms, 0, p->plan.n32 * 4);
     if (e != hipSuccess) {
         free_all(p);
         return hip_fail(e, __FILE__, __LINE__);
@@ -944,7 +970,7 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
         // default priority, like every stream of the library
         e = hipStreamCreateWithFlags(&p->side, hipStreamNonBlocking);
     }
-    if (e == hipSuccess && p->nsets > 1) e = hipStreamCreateWithFlags(&p->remat, hipStreamNonBlocking);
+    if (e == hipSuccess && p->ahead()) e = hipStreamCreateWithFlags(&p->remat, hipStreamNonBlocking);
     if (e == hipSuccess && (p->side || p->remat)) {
         p->evring.assign(4096, nullptr);
         for (size_t i = 0; e == hipSuccess && i < p->evring.size(); ++i)
@@ -1070,7 +1096,7 @@ gp_status gp_forward_microbatch(gp_partition* p, int mb, const void* x, const vo
     // The last micro-batch's recompute goes into workspace set 1 (its backward
     // comes first and uses set mb & 1); the first forward pass itself only
     // uses slot 0 of set 0, so the two can run side by side.
-    const bool early = p->remat_early && p->nsets > 1 && mb == p->g.M - 1 && (mb & 1) == 1;
+    const bool early = p->remat_early && p->ahead() && mb == p->g.M - 1 && (mb & 1) == 1;
     if (early) {
         const long T = p->g.T(), D = p->d.D;
         GP_TRY(intake(c.dt, x, p->stash_x_mb(mb), p->xs[0][0], T * D, c.st));
@@ -1085,6 +1111,9 @@ gp_status gp_forward_microbatch(gp_partition* p, int mb, const void* x, const vo
         GP_HIP(hipEventRecord(p->remat_done, cr.st));
         p->remat_pending = mb;
         s = partition_forward(c, mb, false, x, mem, y, 0, true);
+    } else if (p->g.keep_act) {
+        // stored-activation mode: this micro-batch's intermediates stay in its own set
+        s = partition_forward(c, mb, true, x, mem, y, p->set_of(mb));
     } else {
         s = partition_forward(c, mb, false, x, mem, y);
     }
@@ -1108,25 +1137,27 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     const bool side = p->use_side && p->side;
     const bool first = p->sched.first_backward();
     const long T = p->g.T(), D = p->d.D;
-    const int set = p->nsets > 1 ? (mb & 1) : 0;
+    const int set = p->set_of(mb);
     // Everything enqueued on the caller's stream so far (all forwards, the
     // previous backward, which read the other workspace set) precedes a
     // recompute-ahead launched from this call.
     hipEvent_t remat_fork = nullptr;
-    if (p->nsets > 1 && mb > 0) {
+    if (p->ahead() && mb > 0) {
         remat_fork = p->next_event();
         GP_HIP(hipEventRecord(remat_fork, c.st));
     }
     // re-materialise this micro-batch's forward from the stash, unless the
     // previous backward call already did so on the recompute-ahead stream
-    if (p->remat_pending == mb) {
+    if (p->g.keep_act) {
+        // stored-activation mode: the forward kept every intermediate
+    } else if (p->remat_pending == mb) {
         GP_HIP(hipStreamWaitEvent(c.st, p->remat_done, 0));
         p->remat_pending = -1;
     } else {
         s = partition_forward(c, mb, true, nullptr, nullptr, nullptr, set);
         if (s != GP_OK) return s;
     }
-    if (p->nsets > 1 && mb > 0) {
+    if (p->ahead() && mb > 0) {
         // re-materialise micro-batch mb - 1 into the other set meanwhile
         // (GPipe, Section 2.3: the recompute can be scheduled earlier)
         Ctx cr = make_ctx(p, p->remat, Lane::Remat);
@@ -1213,6 +1244,15 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     return GP_OK;
 }
 
+gp_status gp_recomputed_output(gp_partition* p, void* y, gp_stream stream) {
+    if (!p || !y) return set_error(GP_ERR_INVALID_ARG, "partition and y must not be NULL");
+    if (!p->sched.configured()) return set_error(GP_ERR_STATE, "partition not configured");
+    const int mb = p->sched.last_backward();
+    if (mb < 0) return set_error(GP_ERR_STATE, "no backward micro-batch has run in this mini-batch");
+    const int set = p->set_of(mb);
+    return cast_out(p->g.dtype, p->xs[set][p->d.L], y, p->g.T() * p->d.D, (hipStream_t)stream);
+}
+
 gp_status gp_accumulate_and_step(gp_partition* p, float lr, double* loss_out, gp_stream stream) {
     if (!p) return set_error(GP_ERR_INVALID_ARG, "partition must not be NULL");
     std::string msg;
@@ -1220,6 +1260,18 @@ gp_status gp_accumulate_and_step(gp_partition* p, float lr, double* loss_out, gp
     if (s != GP_OK) return set_error(s, msg.c_str());
     hipStream_t st = (hipStream_t)stream;
     const int dt = p->g.dtype;
+    // Labels outside [0, V) were read as class 0 and flagged on the device; a
+    // step that synchronises anyway reports them and skips the update.
+    if (p->g.loss == GP_LOSS_XENT_LS && (loss_out || p->g.check_finite)) {
+        int bad = 0;
+        GP_HIP(hipMemcpyAsync(&bad, p->bw.bad_label, sizeof(int), hipMemcpyDeviceToHost, st));
+        GP_HIP(hipStreamSynchronize(st));
+        if (bad) {
+            GP_HIP(hipMemsetAsync(p->bw.bad_label, 0, sizeof(int), st));
+            p->sched.did_step();
+            return set_error(GP_ERR_INVALID_ARG, "a label was outside [0, vocab): update skipped");
+        }
+    }
     if (p->g.check_finite) {
         GP_HIP(hipMemsetAsync(p->bw.flag, 0, sizeof(int), st));
         GP_TRY(finite_check(p->grads, (long)p->plan.n32, p->bw.flag, st));
@@ -1231,7 +1283,10 @@ gp_status gp_accumulate_and_step(gp_partition* p, float lr, double* loss_out, gp
             return set_error(GP_ERR_NONFINITE, "non-finite gradient: update skipped");
         }
     }
-    GP_TRY(sgd_update(p->master, p->grads, lr, (long)p->plan.n32, st));
+    if (p->g.optimizer == GP_OPT_RMSPROP)
+        GP_TRY(rmsprop_update(p->master, p->grads, p->opt_ms, lr, p->g.rms_decay, p->g.rms_eps, (long)p->plan.n32, st));
+    else
+        GP_TRY(sgd_update(p->master, p->grads, lr, (long)p->plan.n32, st));
     for (const Linear* l : p->plan.linears())
         GP_TRY(refresh_linear(dt, p->master + l->w, l->in, l->out, p->W(l->kn), p->W(l->nk),
                               l->split ? p->W(l->q4) : nullptr, l->split ? p->W(l->q4s) : nullptr, st));

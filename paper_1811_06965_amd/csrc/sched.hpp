@@ -29,6 +29,10 @@ struct Geometry {
     int dtype = GP_BF16, kind = GP_ENCODER, Smem = 0, loss = GP_LOSS_NONE, V = 0;
     float ls = 0.f, eps = 1e-5f;
     int check_finite = 0;
+    int keep_act = 0;     // stored-activation mode: no recompute, every micro-batch's intermediates kept
+    int optimizer = GP_OPT_SGD;
+    float rms_decay = 0.f, rms_eps = 0.f;
+    float logit_clip = 0.f;
     int ffn_fp4 = 1;  // bf16: fp4 correction of the feed-forward input projection (see Linear::split)
     long long T() const { return (long long)n * S; }     // token rows of one micro-batch
     long long Tm() const { return (long long)n * Smem; } // memory rows of one micro-batch
@@ -65,6 +69,17 @@ inline gp_status check_config(const Dims& d, const gp_config& c, std::string& ms
     if (c.loss != GP_LOSS_XENT_LS && c.vocab != 0) { msg = "vocab is only used by the cross-entropy head"; return GP_ERR_INVALID_ARG; }
     if (!(c.label_smoothing >= 0.f && c.label_smoothing < 1.f)) { msg = "label_smoothing must be in [0, 1)"; return GP_ERR_INVALID_ARG; }
     if (!(c.ln_eps > 0.f)) { msg = "ln_eps must be positive"; return GP_ERR_INVALID_ARG; }
+    if (c.keep_activations != 0 && c.keep_activations != 1) { msg = "keep_activations must be 0 or 1"; return GP_ERR_INVALID_ARG; }
+    if (c.optimizer != GP_OPT_SGD && c.optimizer != GP_OPT_RMSPROP) { msg = "unknown optimizer"; return GP_ERR_INVALID_ARG; }
+    if (c.optimizer == GP_OPT_RMSPROP && !(c.rms_decay >= 0.f && c.rms_decay < 1.f && c.rms_eps > 0.f)) {
+        msg = "RMSProp needs rms_decay in [0, 1) and rms_eps > 0"; return GP_ERR_INVALID_ARG;
+    }
+    if (c.optimizer == GP_OPT_SGD && (c.rms_decay != 0.f || c.rms_eps != 0.f)) {
+        msg = "rms_decay and rms_eps are only used by RMSProp"; return GP_ERR_INVALID_ARG;
+    }
+    if (!(c.logit_clip >= 0.f) || (c.logit_clip > 0.f && c.loss != GP_LOSS_XENT_LS)) {
+        msg = "logit_clip must be >= 0, and nonzero only with the cross-entropy head"; return GP_ERR_INVALID_ARG;
+    }
     const int dh = d.D / d.H;
     if (d.D % 8 || d.F % 8 || (c.loss == GP_LOSS_XENT_LS && c.vocab % 8)) {
         msg = "d_model, d_ff and vocab must be multiples of 8"; return GP_ERR_UNSUPPORTED;
@@ -339,6 +354,12 @@ class Sched {
         return GP_OK;
     }
     bool first_backward() const { return next_bwd == M - 1; }
+    // micro-batch of the most recent backward of this mini-batch, or -1
+    int last_backward() const {
+        if (phase == Phase::Backward && next_bwd < M - 1) return next_bwd + 1;
+        if (phase == Phase::Ready) return 0;
+        return -1;
+    }
     void did_backward() {
         --next_bwd;
         if (next_bwd < 0) phase = Phase::Ready;

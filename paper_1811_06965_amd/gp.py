@@ -20,6 +20,7 @@ STATUS_NAMES = {0: "GP_OK", 1: "GP_ERR_INVALID_ARG", 2: "GP_ERR_STATE", 3: "GP_E
 GP_F32, GP_BF16 = 0, 1
 GP_ENCODER, GP_DECODER_CROSS = 0, 1
 GP_LOSS_NONE, GP_LOSS_MSE, GP_LOSS_XENT_LS = 0, 1, 2
+GP_OPT_SGD, GP_OPT_RMSPROP = 0, 1
 
 PARAM_IDS = ["ln1_g", "ln1_b", "wq", "bq", "wk", "bk", "wv", "bv", "wo", "bo", "ln2_g", "ln2_b",
              "w1", "b1", "w2", "b2", "xwq", "xbq", "xwk", "xbk", "xwv", "xbv", "xwo", "xbo",
@@ -37,7 +38,7 @@ GP_K_NONE, GP_K_COUNT = 0, len(KERNEL_ROLES)
 EXPORTS = ["gp_partition_create", "gp_partition_configure", "gp_partition_destroy", "gp_set_param",
            "gp_get_param", "gp_get_grad", "gp_partition_memory", "gp_param_count", "gp_forward_microbatch",
            "gp_backward_microbatch_remat", "gp_accumulate_and_step", "gp_timer_select", "gp_timer_read",
-           "gp_timer_reset", "gp_timer_sample", "gp_mfma_peak", "gp_last_error"]
+           "gp_timer_reset", "gp_timer_sample", "gp_mfma_peak", "gp_recomputed_output", "gp_last_error"]
 
 
 class gp_config(ctypes.Structure):
@@ -45,7 +46,8 @@ class gp_config(ctypes.Structure):
                 ("num_microbatches", ctypes.c_int), ("dtype", ctypes.c_int), ("kind", ctypes.c_int),
                 ("mem_seq_len", ctypes.c_int), ("loss", ctypes.c_int), ("vocab", ctypes.c_int),
                 ("label_smoothing", ctypes.c_float), ("ln_eps", ctypes.c_float),
-                ("check_finite", ctypes.c_int)]
+                ("check_finite", ctypes.c_int), ("keep_activations", ctypes.c_int), ("optimizer", ctypes.c_int),
+                ("rms_decay", ctypes.c_float), ("rms_eps", ctypes.c_float), ("logit_clip", ctypes.c_float)]
 
 
 class GpError(RuntimeError):
@@ -83,6 +85,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.gp_timer_reset.argtypes = [P]
     lib.gp_timer_sample.argtypes = [P, I]
     lib.gp_mfma_peak.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_double)]
+    lib.gp_recomputed_output.argtypes = [P, VP, VP]
     lib.gp_last_error.argtypes = []
     lib.gp_last_error.restype = ctypes.c_char_p
     for name in EXPORTS:
@@ -180,6 +183,11 @@ def gp_timer_reset(h):
 
 def gp_timer_sample(h, every):
     _check(load().gp_timer_sample(h, every))
+
+
+def gp_recomputed_output(h, y, stream):
+    """y: device address of an [n, S, D] buffer in the partition dtype."""
+    _check(load().gp_recomputed_output(h, y, stream))
 
 
 def gp_mfma_peak(stream=None):

@@ -17,9 +17,11 @@ from . import gp
 DTYPES = {"f32": (gp.GP_F32, torch.float32), "bf16": (gp.GP_BF16, torch.bfloat16)}
 KINDS = {"encoder": gp.GP_ENCODER, "decoder": gp.GP_DECODER_CROSS}
 LOSSES = {"none": gp.GP_LOSS_NONE, "mse": gp.GP_LOSS_MSE, "xent_ls": gp.GP_LOSS_XENT_LS}
+OPTIMIZERS = {"sgd": gp.GP_OPT_SGD, "rmsprop": gp.GP_OPT_RMSPROP}
 
 
-def make_config(cfg, micro: Optional[int] = None, check_finite: bool = False) -> gp.gp_config:
+def make_config(cfg, micro: Optional[int] = None, check_finite: bool = False,
+                keep_activations: bool = False) -> gp.gp_config:
     M = cfg.micro if micro is None else micro
     if cfg.batch % M:
         raise ValueError("mini-batch must split into M equal micro-batches")
@@ -35,19 +37,26 @@ def make_config(cfg, micro: Optional[int] = None, check_finite: bool = False) ->
     c.label_smoothing = cfg.label_smoothing
     c.ln_eps = cfg.ln_eps
     c.check_finite = 1 if check_finite else 0
+    c.keep_activations = 1 if keep_activations else 0
+    c.optimizer = OPTIMIZERS[cfg.optimizer]
+    if cfg.optimizer == "rmsprop":
+        c.rms_decay = cfg.rms_decay
+        c.rms_eps = cfg.rms_eps
+    c.logit_clip = cfg.logit_clip
     return c
 
 
 class Partition:
     """One configured partition on the current HIP device."""
 
-    def __init__(self, cfg, micro: Optional[int] = None, check_finite: bool = False):
+    def __init__(self, cfg, micro: Optional[int] = None, check_finite: bool = False,
+                 keep_activations: bool = False):
         self.cfg = cfg
         self.M = cfg.micro if micro is None else micro
         self.tdtype = DTYPES[cfg.dtype][1]
         self.h = gp.gp_partition_create(cfg.layers, cfg.d_model, cfg.d_ff, cfg.heads)
         try:
-            gp.gp_partition_configure(self.h, make_config(cfg, self.M, check_finite))
+            gp.gp_partition_configure(self.h, make_config(cfg, self.M, check_finite, keep_activations))
         except Exception:
             gp.gp_partition_destroy(self.h)
             raise
@@ -113,9 +122,12 @@ class Partition:
         return out
 
     def step(self, x, mem, dy, lr=0.0, want_y=True, want_dx=True, want_dmem=True, want_loss=True,
-             stream=None, y=None, dx=None, dmem=None):
+             stream=None, y=None, dx=None, dmem=None, want_recomputed=False):
         """One mini-batch through GPipe's schedule.  x/mem/dy: device tensors
-        of the whole mini-batch (dim 0 = sequences).  Returns dict(y, dx, dmem, loss)."""
+        of the whole mini-batch (dim 0 = sequences).  Returns dict(y, dx, dmem,
+        loss); with want_recomputed also "y_remat", the partition output as
+        each backward call re-materialised it (gp_recomputed_output), in
+        mini-batch order."""
         M = self.M
         st = stream if stream is not None else torch.cuda.current_stream().cuda_stream
         if want_y and y is None:
@@ -133,10 +145,17 @@ class Partition:
         ptr = lambda t: None if t is None else t.data_ptr()
         for m in range(M):
             gp.gp_forward_microbatch(self.h, m, ptr(xs[m]), ptr(ms[m]), ptr(ys[m]), st)
+        y_remat = torch.empty_like(x) if want_recomputed else None
+        yr = y_remat.chunk(M) if want_recomputed else None
         for m in range(M - 1, -1, -1):
             gp.gp_backward_microbatch_remat(self.h, m, ptr(dys[m]), ptr(dxs[m]), ptr(dms[m]), st)
+            if want_recomputed:
+                gp.gp_recomputed_output(self.h, ptr(yr[m]), st)
         loss = gp.gp_accumulate_and_step(self.h, lr, want_loss, st)
-        return {"y": y, "dx": dx, "dmem": dmem, "loss": loss}
+        out = {"y": y, "dx": dx, "dmem": dmem, "loss": loss}
+        if want_recomputed:
+            out["y_remat"] = y_remat
+        return out
 
     def capture_step(self, x, mem, dy, lr=0.0, dx=None, dmem=None, want_y=False, y=None):
         """Capture one whole mini-batch step (M forwards, M backwards, the

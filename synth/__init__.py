@@ -12,7 +12,9 @@ loss-specific tensor (MSE targets, boundary gradients, or token labels).
 
 Distributions (the workload recipe of the partition configurations):
   * weight matrices: Xavier-uniform, U(-a, a) with a = sqrt(6 / (fan_in + fan_out))
-    per logical [in, out] matrix;
+    per logical [in, out] matrix; with ``fixup_layers`` = L > 0 the feed-forward
+    matrices w1 and w2 are drawn the same way and divided by L (the scaled-down
+    feed-forward initialisation of the paper's Section 5);
   * biases 0, LayerNorm gain 1 and shift 0 -- unless ``perturb`` is set, in
     which case they are drawn as N(0, 0.1^2) (biases, shifts) and
     1 + N(0, 0.1^2) (gains) so that every parameter path carries signal;
@@ -61,6 +63,15 @@ class PartitionConfig:
     label_smoothing: float = 0.0
     mem_seq: int = 0
     ln_eps: float = 1e-5
+    # the one synchronous update: "sgd" or "rmsprop" (decay rho, eps inside the square root)
+    optimizer: str = "sgd"
+    rms_decay: float = 0.9
+    rms_eps: float = 1e-10
+    # cross-entropy head: clip the logits to [-logit_clip, logit_clip] (0 = off)
+    logit_clip: float = 0.0
+    # initialisation: > 0 divides the Xavier-uniform draws of the feed-forward
+    # matrices (w1, w2) by this number of layers of the whole model
+    fixup_layers: int = 0
 
     @property
     def d_head(self) -> int:
@@ -146,9 +157,15 @@ def _xavier(rng: np.random.Generator, shape) -> np.ndarray:
     return rng.uniform(-a, a, size=shape)
 
 
-def _draw_param(rng, name, shape, perturb):
+FFN_MATRICES = ("w1", "w2")
+
+
+def _draw_param(rng, name, shape, perturb, fixup_layers=0):
     if len(shape) == 2:
-        return _xavier(rng, shape)
+        w = _xavier(rng, shape)
+        # Section 5: the initialisation of every feed-forward layer is scaled
+        # down by the number of layers of the model
+        return w / fixup_layers if fixup_layers > 0 and name in FFN_MATRICES else w
     if name.endswith("_g"):
         return 1.0 + 0.1 * rng.standard_normal(shape) if perturb else np.ones(shape)
     return 0.1 * rng.standard_normal(shape) if perturb else np.zeros(shape)
@@ -168,7 +185,7 @@ def _make_params(rng, cfg, perturb):
     order = [p for p in PARAM_IDS if p in shapes]
     layers = []
     for _ in range(cfg.layers):
-        layers.append({p: round_storage(_draw_param(rng, p, shapes[p], perturb), cfg.dtype)
+        layers.append({p: round_storage(_draw_param(rng, p, shapes[p], perturb, cfg.fixup_layers), cfg.dtype)
                        for p in order})
     hshapes = cfg.head_shapes()
     head = {p: round_storage(_draw_param(rng, p, hshapes[p], perturb), cfg.dtype)

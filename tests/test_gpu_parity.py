@@ -222,8 +222,9 @@ def test_microbatch_count_invariance_fp32():
 
 @pytest.mark.parametrize("cfg", [TINY, RAGGED_BF16.with_(layers=1)], ids=lambda c: c.name)
 def test_steps_are_bitwise_deterministic(cfg):
-    """No atomics anywhere: the same mini-batch twice gives identical bits
-    (and the re-materialised forward therefore reproduces the first pass)."""
+    """No atomics anywhere: the same mini-batch twice gives identical bits.
+    (That the recompute reproduces the first pass is checked directly by
+    test_recompute_reproduces_first_pass_bitwise.)"""
     from paper_1811_06965_amd.runtime import Partition
     case = synth.make_case(cfg, 7, perturb=True)
     res = []
@@ -483,3 +484,92 @@ def test_split_reduce_fused_into_layernorm_is_bitwise_identical(tile, splits, mo
         for l, (a, b) in enumerate(zip(g1, g0)):
             for k in a:
                 assert np.array_equal(a[k], b[k]), (l, k)
+
+
+@pytest.mark.parametrize("cfg,fp4", [(TINY, "1"), (ENC512_SMALL, "0"), (ENC512_SMALL, "1"), (RAGGED_BF16, "1"),
+                                     (DEC_SMALL_BF16, "0"), (DEC_SMALL_BF16, "1")],
+                         ids=["tiny_fp32", "enc512_small_fp4off", "enc512_small", "ragged_bf16", "dec_small_fp4off",
+                              "dec_small"])
+def test_recompute_reproduces_first_pass_bitwise(cfg, fp4, monkeypatch):
+    """Section 2.3: the backward pass recomputes the same F_k.  The partition
+    output that each backward call re-materialises (gp_recomputed_output)
+    equals, bit for bit, the y its forward call emitted -- in fp32, and in bf16
+    with and without the fp4 correction of the feed-forward input (which runs
+    in both passes), with the recompute-ahead and early-recompute streams on."""
+    from paper_1811_06965_amd.runtime import Partition
+    monkeypatch.setenv("GP_FFN_FP4", fp4)
+    case = synth.make_case(cfg, 13, perturb=True)
+    with Partition(cfg) as part:
+        part.load_params(case["layers"], case["head"])
+        inp = part.device_inputs(case)
+        for _ in range(2):
+            o = part.step(inp["x"], inp["mem"], inp["dy"], lr=0.0, want_recomputed=True)
+            torch.cuda.synchronize()
+            y, yr = o["y"].cpu(), o["y_remat"].cpu()
+            assert torch.isfinite(y.float()).all()
+            assert torch.equal(y.view(torch.int16) if y.dtype == torch.bfloat16 else y.view(torch.int32),
+                               yr.view(torch.int16) if yr.dtype == torch.bfloat16 else yr.view(torch.int32))
+
+
+def test_recomputed_output_needs_a_backward():
+    from paper_1811_06965_amd import gp
+    from paper_1811_06965_amd.runtime import Partition
+    with Partition(TINY) as part:
+        buf = torch.empty(TINY.micro_batch, TINY.seq, TINY.d_model, device="cuda")
+        st = torch.cuda.current_stream().cuda_stream
+        with pytest.raises(gp.GpError) as e:
+            gp.gp_recomputed_output(part.h, buf.data_ptr(), st)
+        assert e.value.status == gp.GP_ERR_STATE
+
+
+# attention with 2 and 4 waves (32-row blocks) per workgroup: the forward, dQ
+# and dK/dV kernels of the larger micro-batches, forced on small cases with a
+# partial last workgroup (S = 64 and 96 rows of queries/keys per head).
+ATTN_ENC = synth.PartitionConfig("attn_enc", layers=2, d_model=256, d_ff=512, heads=4, seq=64,
+                                 batch=4, micro=2, dtype="bf16", loss="none")
+ATTN_ENC96 = ATTN_ENC.with_(name="attn_enc96", seq=96)
+ATTN_DEC = synth.PartitionConfig("attn_dec", layers=2, d_model=128, d_ff=256, heads=2, seq=96, batch=4, micro=2,
+                                 dtype="bf16", kind="decoder", loss="xent_ls", vocab=512, label_smoothing=0.1,
+                                 mem_seq=64)
+
+
+@pytest.mark.parametrize("waves", ["2", "4"])
+@pytest.mark.parametrize("cfg,ksplit", [(ATTN_ENC, "0"), (ATTN_ENC, "1"), (ATTN_ENC96, "0"), (ATTN_DEC, "0"),
+                                        (ATTN_DEC, "1")],
+                         ids=["enc_one_wave", "enc_two_wave", "enc96", "dec_causal", "dec_causal_ksplit"])
+def test_bf16_attention_waves_per_workgroup(cfg, ksplit, waves, monkeypatch):
+    """GP_ATTN_WAVES forces 2 or 4 query (key) blocks per workgroup: the
+    kernels the enc1024 workload runs at M = 4 (2048 and more row blocks),
+    non-causal (encoder, decoder cross-attention) and causal (decoder self-
+    attention), with the one-wave and the two-wave split loops, against the
+    oracle."""
+    monkeypatch.setenv("GP_ATTN_WAVES", waves)
+    monkeypatch.setenv("GP_ATTN_KSPLIT", ksplit)
+    case, ref, res = _run(cfg, 14, perturb=True)
+    _check(cfg, ref, res, 2e-2, "cos", 0.999)
+
+
+def test_out_of_range_label_is_reported():
+    """A label outside [0, V) is read as class 0 on the device and reported by
+    the next synchronising step, which skips the update; the partition then
+    takes the next mini-batch normally."""
+    from paper_1811_06965_amd import gp
+    from paper_1811_06965_amd.runtime import Partition
+    cfg = DEC_F32
+    case = synth.make_case(cfg, 15, perturb=True)
+    with Partition(cfg) as part:
+        part.load_params(case["layers"], case["head"])
+        inp = part.device_inputs(case)
+        before, _ = part.params()
+        for bad in (-1, cfg.vocab):
+            labels = inp["dy"].clone()
+            labels[1, 2] = bad
+            with pytest.raises(gp.GpError) as e:
+                part.step(inp["x"], inp["mem"], labels, lr=0.1)
+            assert e.value.status == gp.GP_ERR_INVALID_ARG
+            after, _ = part.params()
+            for a, b in zip(before, after):
+                for k in a:
+                    assert np.array_equal(a[k], b[k])
+        out = part.step(inp["x"], inp["mem"], inp["dy"], lr=0.0)
+        assert np.isfinite(out["loss"])

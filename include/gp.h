@@ -163,11 +163,23 @@ gp_status gp_set_param(gp_partition* p, int layer, int id, const float* host, si
 gp_status gp_get_param(gp_partition* p, int layer, int id, float* host, size_t count);
 gp_status gp_get_grad(gp_partition* p, int layer, int id, float* host, size_t count);
 
-/* Bytes held in device memory for parameters (masters and working copies),
- * gradient accumulators, the boundary stash, and all workspaces.  Any pointer
+/* Bytes held in device memory for parameters (masters, working copies and,
+ * with RMSProp, the running mean squares), gradient accumulators, the
+ * boundary stash, and all workspaces.  Any pointer
  * may be NULL.  Requires a configured partition. */
 gp_status gp_partition_memory(gp_partition* p, size_t* params, size_t* grads, size_t* stash,
                               size_t* workspace);
+
+/* The byte counts gp_partition_memory would report for a partition of these
+ * sizes configured with *cfg (Section 2.3: with re-materialisation the
+ * stash holds the N boundary inputs and the workspace one micro-batch's
+ * intermediates, O(N + L N / M); with keep_activations every micro-batch's,
+ * O(N L)), computed on the host without touching a device.  The schedule
+ * settings read from the environment at configure apply here too.
+ * GP_ERR_INVALID_ARG / GP_ERR_UNSUPPORTED: as gp_partition_create and
+ * gp_partition_configure. */
+gp_status gp_memory_plan(int layers, int d_model, int d_ff, int heads, const gp_config* cfg, size_t* params,
+                         size_t* grads, size_t* stash, size_t* workspace);
 
 /* Number of trainable parameters (layers plus head). */
 gp_status gp_param_count(gp_partition* p, size_t* count);

@@ -150,6 +150,8 @@ gp_status refresh_linear(int dtype, const float* w, int in, int out, void* kn, v
 // wave): edge 0 before, 1 after a timed launch, so that per-dispatch profiler
 // records can be attributed to launch roles.
 gp_status role_marker(int role, int edge, hipStream_t st);
+// Fill bytes [p, p + bytes) with 0xFF (NaN in every floating type); test mode only.
+gp_status poison_fill(void* p, size_t bytes, hipStream_t st);
 // flag[0] = 1 if any of x[0..count) is not finite (flag must be zeroed first).
 gp_status finite_check(const float* x, long count, int* flag, hipStream_t st);
 

@@ -404,6 +404,27 @@ gp_status refresh_linear(int dtype, const float* w, int in, int out, void* kn, v
     return GP_OK;
 }
 
+// All-ones bytes over [p, p + bytes): a NaN in every fp32, bf16 and fp64
+// element.  16-byte stores over the aligned middle, byte stores at the edges.
+__global__ void __launch_bounds__(256) poison_kernel(unsigned char* __restrict__ p, long head, long n16, long tail) {
+    const long t = (long)blockIdx.x * 256 + threadIdx.x, stride = (long)gridDim.x * 256;
+    if (t < head) p[t] = 0xFF;
+    uint4* q = reinterpret_cast<uint4*>(p + head);
+    for (long i = t; i < n16; i += stride) q[i] = make_uint4(~0u, ~0u, ~0u, ~0u);
+    if (t < tail) p[head + 16 * n16 + t] = 0xFF;
+}
+
+gp_status poison_fill(void* p, size_t bytes, hipStream_t st) {
+    if (!p || bytes == 0) return GP_OK;
+    unsigned char* c = static_cast<unsigned char*>(p);
+    const long head = (long)((16 - (reinterpret_cast<uintptr_t>(c) & 15)) & 15);
+    const long h = head < (long)bytes ? head : (long)bytes;
+    const long n16 = ((long)bytes - h) / 16, tail = (long)bytes - h - 16 * n16;
+    klaunch(poison_kernel, ew_grid(n16 > 256 ? n16 : 256), 256, 0, st, c, h, n16, tail);
+    GP_LAUNCH_CHECK();
+    return GP_OK;
+}
+
 // Empty kernel that delimits a timed launch in a profiler's dispatch list.
 // Its grid encodes the label (role workgroups in x, edge + 1 in y), which a
 // kernel trace records.

@@ -51,6 +51,10 @@ gp_status hip_fail(hipError_t e, const char* file, int line) {
 struct Arena {
     char* base = nullptr;
     size_t off = 0;
+    size_t mark() {  // aligned offset of the next buffer
+        off = align_up(off, 256);
+        return off;
+    }
     template <typename X> X* take(size_t count) {
         off = align_up(off, 256);
         X* p = reinterpret_cast<X*>(base + off);
@@ -76,6 +80,11 @@ struct LayerWs {
 };
 
 constexpr int ELT_RING = 10;      // bf16 residual-gradient buffers (see layer_backward)
+
+// A byte range of the workspace, as an offset from its base.
+struct Span {
+    size_t off = 0, bytes = 0;
+};
 
 struct BwdWs {
     float *p32 = nullptr, *q32 = nullptr, *dn = nullptr, *delta = nullptr, *partial = nullptr, *dmem32 = nullptr;
@@ -153,6 +162,16 @@ struct gp_partition {
     std::vector<std::vector<LayerWs>> lw;
     int nsets = 1;
     float* opt_ms = nullptr;  // RMSProp: running mean square of every gradient [n32]
+    // GP_POISON=1 (test mode): every workspace region is filled with NaN
+    // right before the phase that (re)writes it, so that a read of a stale or
+    // never-written value shows up in the results.  Regions, per set: the
+    // residual stream, each layer slot; and the backward scratch, the LayerNorm
+    // partial sums, the split-K partials of each stream, the loss partials.
+    bool poison = false;
+    std::vector<Span> xs_span;                // per set: xs[set][0..L]
+    std::vector<std::vector<Span>> slot_span; // per set and layer slot
+    Span bwd_span, lnpart_span, loss_span, loss_acc_span, head_span;
+    Span splitk_span[3];                      // caller's stream, weight-gradient stream, recompute stream
     // per LayerNorm: block partial sums of its gamma/beta gradients, added up
     // over the micro-batches of a mini-batch and reduced after the last one
     std::vector<float*> lnpart;
@@ -224,10 +243,18 @@ void plan_workspace(gp_partition* p, Arena& a) {
     const bool dec = g.kind == GP_DECODER_CROSS;
     p->xs.assign(p->nsets, std::vector<float*>(d.L + 1, nullptr));
     p->lw.assign(p->nsets, std::vector<LayerWs>(d.L, LayerWs{}));
-    for (int set = 0; set < p->nsets; ++set)
-        for (auto& x : p->xs[set]) x = a.take<float>(T * D);
+    p->xs_span.assign(p->nsets, Span{});
+    p->slot_span.assign(p->nsets, std::vector<Span>(d.L, Span{}));
+    auto span_from = [&](size_t start) { return Span{start, a.off - start}; };
     for (int set = 0; set < p->nsets; ++set) {
-        for (auto& l : p->lw[set]) {
+        const size_t s0 = a.mark();
+        for (auto& x : p->xs[set]) x = a.take<float>(T * D);
+        p->xs_span[set] = span_from(s0);
+    }
+    for (int set = 0; set < p->nsets; ++set) {
+        for (int li = 0; li < d.L; ++li) {
+            LayerWs& l = p->lw[set][li];
+            const size_t s0 = a.mark();
             l.st1 = a.take<float>(2 * T);
             l.u = a.take_elt(T * D, e);
             l.qkv = a.take_elt(T * 3 * D, e);
@@ -250,9 +277,11 @@ void plan_workspace(gp_partition* p, Arena& a) {
                 l.v4s = a.take<unsigned char>(T);
             }
             l.a = a.take_elt(T * F, e);
+            p->slot_span[set][li] = span_from(s0);
         }
     }
     BwdWs& b = p->bw;
+    const size_t b0 = a.mark();
     b.p32 = a.take<float>(T * D);
     b.q32 = a.take<float>(T * D);
     for (auto& r : b.ring) r = a.take_elt(T * D, e);
@@ -278,26 +307,57 @@ void plan_workspace(gp_partition* p, Arena& a) {
         if (pm > part) part = pm;
     }
     b.partial = a.take<float>(part);
+    p->bwd_span = span_from(b0);
     const std::vector<const Norm*> norms = p->plan.norms();
     p->lnpart.assign(norms.size(), nullptr);
+    const size_t n0 = a.mark();
     for (const Norm* n : norms) p->lnpart[n->id] = a.take<float>((size_t)layernorm_bwd_blocks(T) * 2 * n->n);
+    p->lnpart_span = span_from(n0);
     // split-K partials: up to 8 splits of a T x D activation GEMM or of the
     // D x 3D packed-QKV weight gradient (with its bias column sums)
     b.splitk_elems = std::max<long>(8 * T * D, 8 * (3 * D * D + 3 * D));
+    const size_t sk_bytes = (size_t)b.splitk_elems * sizeof(float);
+    p->splitk_span[0] = Span{a.mark(), sk_bytes};
     b.splitk = a.take<float>((size_t)b.splitk_elems);
+    p->splitk_span[1] = Span{a.mark(), sk_bytes};
     b.splitk_side = a.take<float>((size_t)b.splitk_elems);
-    if (p->ahead()) b.splitk_remat = a.take<float>((size_t)b.splitk_elems);
+    p->splitk_span[2] = Span{};
+    if (p->ahead()) {
+        p->splitk_span[2] = Span{a.mark(), sk_bytes};
+        b.splitk_remat = a.take<float>((size_t)b.splitk_elems);
+    }
     size_t lp = (size_t)loss_blocks();
     if (g.loss == GP_LOSS_XENT_LS && (size_t)xent_partials(T) > lp) lp = xent_partials(T);
+    p->loss_span = Span{a.mark(), lp * sizeof(double)};
     b.loss_partial = a.take<double>(lp);
+    p->loss_acc_span = Span{a.mark(), sizeof(double)};
     b.loss_acc = a.take<double>(1);
     b.flag = a.take<int>(1);
     b.bad_label = a.take<int>(1);
+    p->head_span = Span{};
     if (g.loss == GP_LOSS_XENT_LS) {
+        const size_t h0 = a.mark();
         b.sth = a.take<float>(2 * T);
         b.h = a.take_elt(T * D, e);
         b.z = a.take_elt(T * (long)g.V, e);
+        p->head_span = span_from(h0);
     }
+}
+
+// GP_POISON: fill one workspace region with NaN on stream st.
+gp_status poison_span(const gp_partition* p, const Span& sp, hipStream_t st) {
+    if (!p->poison || sp.bytes == 0) return GP_OK;
+    return poison_fill(p->ws + sp.off, sp.bytes, st);
+}
+
+// GP_POISON: a whole workspace set (residual stream and every layer slot),
+// before a pass that rewrites all of it.
+gp_status poison_set(const gp_partition* p, int set, hipStream_t st) {
+    if (!p->poison) return GP_OK;
+    gp_status s = poison_span(p, p->xs_span[set], st);
+    for (const Span& sp : p->slot_span[set])
+        if (s == GP_OK) s = poison_span(p, sp, st);
+    return s;
 }
 
 // A GEMM launched split-K whose reduce is left to the LayerNorm that takes its
@@ -857,6 +917,54 @@ gp_status alloc(void** ptr, size_t bytes) {
 
 } // namespace
 
+namespace {
+// Geometry, schedule knobs, parameter plan and byte counts of a partition for
+// cfg (already validated); host arithmetic only, no device is touched.
+void plan_partition(gp_partition* p, const gp_config* cfg) {
+    Geometry& g = p->g;
+    g.S = cfg->seq_len;
+    g.n = cfg->seqs_per_microbatch;
+    g.M = cfg->num_microbatches;
+    g.dtype = cfg->dtype;
+    g.kind = cfg->kind;
+    g.Smem = cfg->mem_seq_len;
+    g.loss = cfg->loss;
+    g.V = cfg->vocab;
+    g.ls = cfg->label_smoothing;
+    g.eps = cfg->ln_eps;
+    g.check_finite = cfg->check_finite;
+    g.keep_act = cfg->keep_activations;
+    g.optimizer = cfg->optimizer;
+    g.rms_decay = cfg->rms_decay;
+    g.rms_eps = cfg->rms_eps;
+    g.logit_clip = cfg->logit_clip;
+    p->esz = g.dtype == GP_BF16 ? 2 : 4;
+    if (const char* e = std::getenv("GP_TIMER_MARKERS")) p->timer.markers = std::atoi(e) != 0;
+    if (const char* e = std::getenv("GP_SIDE_STREAM")) p->use_side = std::atoi(e) != 0;
+    if (const char* e = std::getenv("GP_REMAT_AHEAD")) p->remat_ahead = std::atoi(e) != 0;
+    if (const char* e = std::getenv("GP_REMAT_EARLY")) p->remat_early = std::atoi(e) != 0;
+    if (const char* e = std::getenv("GP_FUSE_RES_LN")) p->fuse_res_ln = std::atoi(e) != 0;
+    if (const char* e = std::getenv("GP_ATTN_KSPLIT")) p->attn_split = std::atoi(e) != 0;
+    if (const char* e = std::getenv("GP_ATTN_WAVES")) p->attn_waves = std::atoi(e);
+    if (const char* e = std::getenv("GP_POISON")) p->poison = std::atoi(e) != 0;
+    if (const char* e = std::getenv("GP_DW_FLUSH")) p->dw_flush = std::atoi(e);
+    // one workspace set per micro-batch when activations are kept, else two
+    // (recompute-ahead) or one
+    p->nsets = g.keep_act ? g.M : (p->remat_ahead && g.M >= 2) ? 2 : 1;
+    if (const char* e = std::getenv("GP_GEMM_TILE")) p->gemm_tile = std::atoi(e);
+    if (const char* e = std::getenv("GP_GEMM_SPLITS")) p->gemm_splits = std::atoi(e);
+    if (const char* e = std::getenv("GP_FFN_FP4")) g.ffn_fp4 = std::atoi(e) != 0;
+    p->plan = plan_params(p->d, g);
+    Arena measure;
+    plan_workspace(p, measure);
+    const bool rms = g.optimizer == GP_OPT_RMSPROP;
+    p->bytes_params = p->plan.n32 * 4 * (rms ? 2 : 1) + p->plan.nelt * p->esz;
+    p->bytes_grads = p->plan.n32 * 4;
+    p->bytes_stash = (size_t)g.M * (g.T() + g.Tm()) * p->d.D * p->esz;
+    p->bytes_ws = measure.off;
+}
+} // namespace
+
 extern "C" {
 
 const char* gp_last_error(void) { return g_err.c_str(); }
@@ -877,52 +985,36 @@ gp_status gp_partition_create(int layers, int d_model, int d_ff, int heads, gp_p
     return GP_OK;
 }
 
+gp_status gp_memory_plan(int layers, int d_model, int d_ff, int heads, const gp_config* cfg, size_t* params,
+                         size_t* grads, size_t* stash, size_t* workspace) {
+    if (!cfg) return set_error(GP_ERR_INVALID_ARG, "config must not be NULL");
+    std::string msg;
+    gp_status s = check_dims(layers, d_model, d_ff, heads, msg);
+    if (s != GP_OK) return set_error(s, msg.c_str());
+    gp_partition p;
+    p.d.L = layers;
+    p.d.D = d_model;
+    p.d.F = d_ff;
+    p.d.H = heads;
+    s = check_config(p.d, *cfg, msg);
+    if (s != GP_OK) return set_error(s, msg.c_str());
+    plan_partition(&p, cfg);
+    if (params) *params = p.bytes_params;
+    if (grads) *grads = p.bytes_grads;
+    if (stash) *stash = p.bytes_stash;
+    if (workspace) *workspace = p.bytes_ws;
+    return GP_OK;
+}
+
 gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
     if (!p || !cfg) return set_error(GP_ERR_INVALID_ARG, "partition and config must not be NULL");
     std::string msg;
     if (p->sched.configured()) return set_error(GP_ERR_STATE, "partition already configured");
     gp_status s = check_config(p->d, *cfg, msg);
     if (s != GP_OK) return set_error(s, msg.c_str());
-    Geometry& g = p->g;
-    g.S = cfg->seq_len;
-    g.n = cfg->seqs_per_microbatch;
-    g.M = cfg->num_microbatches;
-    g.dtype = cfg->dtype;
-    g.kind = cfg->kind;
-    g.Smem = cfg->mem_seq_len;
-    g.loss = cfg->loss;
-    g.V = cfg->vocab;
-    g.ls = cfg->label_smoothing;
-    g.eps = cfg->ln_eps;
-    g.check_finite = cfg->check_finite;
-    p->esz = g.dtype == GP_BF16 ? 2 : 4;
-    if (const char* e = std::getenv("GP_TIMER_MARKERS")) p->timer.markers = std::atoi(e) != 0;
-    if (const char* e = std::getenv("GP_SIDE_STREAM")) p->use_side = std::atoi(e) != 0;
-    if (const char* e = std::getenv("GP_REMAT_AHEAD")) p->remat_ahead = std::atoi(e) != 0;
-    if (const char* e = std::getenv("GP_REMAT_EARLY")) p->remat_early = std::atoi(e) != 0;
-    if (const char* e = std::getenv("GP_FUSE_RES_LN")) p->fuse_res_ln = std::atoi(e) != 0;
-    if (const char* e = std::getenv("GP_ATTN_KSPLIT")) p->attn_split = std::atoi(e) != 0;
-    if (const char* e = std::getenv("GP_ATTN_WAVES")) p->attn_waves = std::atoi(e);
-    if (const char* e = std::getenv("GP_DW_FLUSH")) p->dw_flush = std::atoi(e);
-    g.keep_act = cfg->keep_activations;
-    g.optimizer = cfg->optimizer;
-    g.rms_decay = cfg->rms_decay;
-    g.rms_eps = cfg->rms_eps;
-    g.logit_clip = cfg->logit_clip;
-    // one workspace set per micro-batch when activations are kept, else two
-    // (recompute-ahead) or one
-    p->nsets = g.keep_act ? g.M : (p->remat_ahead && g.M >= 2) ? 2 : 1;
-    if (const char* e = std::getenv("GP_GEMM_TILE")) p->gemm_tile = std::atoi(e);
-    if (const char* e = std::getenv("GP_GEMM_SPLITS")) p->gemm_splits = std::atoi(e);
-    if (const char* e = std::getenv("GP_FFN_FP4")) g.ffn_fp4 = std::atoi(e) != 0;
-    p->plan = plan_params(p->d, g);
-    Arena measure;
-    plan_workspace(p, measure);
+    plan_partition(p, cfg);
+    const Geometry& g = p->g;
     const bool rms = g.optimizer == GP_OPT_RMSPROP;
-    p->bytes_params = p->plan.n32 * 4 * (rms ? 2 : 1) + p->plan.nelt * p->esz;
-    p->bytes_grads = p->plan.n32 * 4;
-    p->bytes_stash = (size_t)g.M * (g.T() + g.Tm()) * p->d.D * p->esz;
-    p->bytes_ws = measure.off;
     void *m = nullptr, *gr = nullptr, *we = nullptr, *sx = nullptr, *sm = nullptr, *ws = nullptr;
     s = alloc(&m, p->plan.n32 * 4);
     if (s == GP_OK) s = alloc(&gr, p->plan.n32 * 4);
@@ -1093,6 +1185,18 @@ gp_status gp_forward_microbatch(gp_partition* p, int mb, const void* x, const vo
     if (dec && !mem) return set_error(GP_ERR_INVALID_ARG, "decoder partitions need the memory input");
     if (!dec && mem) return set_error(GP_ERR_INVALID_ARG, "encoder partitions take no memory input");
     Ctx c = make_ctx(p, (hipStream_t)stream);
+    if (p->poison) {
+        const long T = p->g.T(), D = p->d.D;
+        GP_TRY(poison_span(p, p->splitk_span[0], c.st));
+        if (p->g.keep_act) {
+            GP_TRY(poison_set(p, p->set_of(mb), c.st));
+        } else {
+            // the first pass's layer slot and its two ping-pong residual buffers
+            GP_TRY(poison_span(p, p->slot_span[0][0], c.st));
+            for (int i = 0; i < 2 && i <= p->d.L; ++i)
+                GP_TRY(poison_span(p, Span{(size_t)((char*)p->xs[0][i] - p->ws), (size_t)(T * D) * 4}, c.st));
+        }
+    }
     // The last micro-batch's recompute goes into workspace set 1 (its backward
     // comes first and uses set mb & 1); the first forward pass itself only
     // uses slot 0 of set 0, so the two can run side by side.
@@ -1105,6 +1209,8 @@ gp_status gp_forward_microbatch(gp_partition* p, int mb, const void* x, const vo
         GP_HIP(hipEventRecord(fork, c.st));
         Ctx cr = make_ctx(p, p->remat, Lane::Remat);
         GP_HIP(hipStreamWaitEvent(cr.st, fork, 0));
+        GP_TRY(poison_set(p, 1, cr.st));
+        GP_TRY(poison_span(p, p->splitk_span[2], cr.st));
         s = partition_forward(cr, mb, true, nullptr, nullptr, nullptr, 1);
         if (s != GP_OK) return s;
         p->remat_done = p->next_event();
@@ -1138,6 +1244,16 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     const bool first = p->sched.first_backward();
     const long T = p->g.T(), D = p->d.D;
     const int set = p->set_of(mb);
+    if (p->poison) {
+        for (const Span* sp : {&p->bwd_span, &p->splitk_span[0], &p->splitk_span[1], &p->loss_span, &p->head_span})
+            GP_TRY(poison_span(p, *sp, c.st));
+        if (first) {
+            // overwritten (not accumulated into) by the first backward micro-batch
+            GP_TRY(poison_span(p, p->lnpart_span, c.st));
+            GP_TRY(poison_span(p, p->loss_acc_span, c.st));
+            GP_TRY(poison_fill(p->grads, p->plan.n32 * 4, c.st));
+        }
+    }
     // Everything enqueued on the caller's stream so far (all forwards, the
     // previous backward, which read the other workspace set) precedes a
     // recompute-ahead launched from this call.
@@ -1154,6 +1270,7 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
         GP_HIP(hipStreamWaitEvent(c.st, p->remat_done, 0));
         p->remat_pending = -1;
     } else {
+        GP_TRY(poison_set(p, set, c.st));
         s = partition_forward(c, mb, true, nullptr, nullptr, nullptr, set);
         if (s != GP_OK) return s;
     }
@@ -1162,6 +1279,8 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
         // (GPipe, Section 2.3: the recompute can be scheduled earlier)
         Ctx cr = make_ctx(p, p->remat, Lane::Remat);
         GP_HIP(hipStreamWaitEvent(cr.st, remat_fork, 0));
+        GP_TRY(poison_set(p, set ^ 1, cr.st));
+        GP_TRY(poison_span(p, p->splitk_span[2], cr.st));
         s = partition_forward(cr, mb - 1, true, nullptr, nullptr, nullptr, set ^ 1);
         if (s != GP_OK) return s;
         p->remat_done = p->next_event();

@@ -38,7 +38,7 @@ GP_K_NONE, GP_K_COUNT = 0, len(KERNEL_ROLES)
 EXPORTS = ["gp_partition_create", "gp_partition_configure", "gp_partition_destroy", "gp_set_param",
            "gp_get_param", "gp_get_grad", "gp_partition_memory", "gp_param_count", "gp_forward_microbatch",
            "gp_backward_microbatch_remat", "gp_accumulate_and_step", "gp_timer_select", "gp_timer_read",
-           "gp_timer_reset", "gp_timer_sample", "gp_mfma_peak", "gp_recomputed_output", "gp_last_error"]
+           "gp_timer_reset", "gp_timer_sample", "gp_mfma_peak", "gp_recomputed_output", "gp_memory_plan", "gp_last_error"]
 
 
 class gp_config(ctypes.Structure):
@@ -86,6 +86,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.gp_timer_sample.argtypes = [P, I]
     lib.gp_mfma_peak.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_double)]
     lib.gp_recomputed_output.argtypes = [P, VP, VP]
+    lib.gp_memory_plan.argtypes = [I, I, I, I, ctypes.POINTER(gp_config)] + [ctypes.POINTER(SZ)] * 4
     lib.gp_last_error.argtypes = []
     lib.gp_last_error.restype = ctypes.c_char_p
     for name in EXPORTS:
@@ -139,6 +140,13 @@ def gp_get_grad(h, layer, pid, host):
 def gp_partition_memory(h):
     v = [ctypes.c_size_t() for _ in range(4)]
     _check(load().gp_partition_memory(h, *[ctypes.byref(x) for x in v]))
+    return dict(params=v[0].value, grads=v[1].value, stash=v[2].value, workspace=v[3].value)
+
+
+def gp_memory_plan(layers, d_model, d_ff, heads, cfg: gp_config):
+    """Byte counts of a partition configured with cfg, computed on the host."""
+    v = [ctypes.c_size_t() for _ in range(4)]
+    _check(load().gp_memory_plan(layers, d_model, d_ff, heads, ctypes.byref(cfg), *[ctypes.byref(x) for x in v]))
     return dict(params=v[0].value, grads=v[1].value, stash=v[2].value, workspace=v[3].value)
 
 

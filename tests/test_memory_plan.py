@@ -1,0 +1,96 @@
+"""Device memory against M, with and without re-materialisation (Section 2.3,
+Table 1), from the library's own plan (gp_memory_plan: host arithmetic, no
+device).
+
+With re-materialisation a partition keeps the N boundary inputs of the
+mini-batch (the stash) and the intermediates of one micro-batch of N / M
+sequences: O(N + L N / M).  Keeping every micro-batch's intermediates instead
+takes O(N L).  At enc1024 (16 layers, N = 64 sequences of 256 tokens):
+
+* the stash does not depend on M;
+* one micro-batch's set of intermediates is proportional to its token rows
+  T = N S / M, and the workspace shrinks with M;
+* with kept activations the workspace is M sets of T-row intermediates, i.e.
+  nearly independent of M, and far larger than with re-materialisation;
+* parameters and gradient accumulators do not depend on M or on the mode.
+"""
+import pytest
+
+import synth
+
+
+@pytest.fixture(scope="module")
+def gp():
+    import os
+    from paper_1811_06965_amd import build, gp as g
+    if not os.path.exists(g.LIB_PATH):
+        build.build()
+    g.load()
+    return g
+
+
+def plan(gp, cfg, M, keep=False):
+    from paper_1811_06965_amd.runtime import make_config
+    c = make_config(cfg, M, keep_activations=keep)
+    return gp.gp_memory_plan(cfg.layers, cfg.d_model, cfg.d_ff, cfg.heads, c)
+
+
+CFG = synth.CONFIGS["enc1024"]
+MS = (4, 8, 16, 32)
+
+
+def test_stash_and_parameters_do_not_depend_on_m(gp):
+    plans = {M: plan(gp, CFG, M) for M in MS}
+    N, S, D = CFG.batch, CFG.seq, CFG.d_model
+    for M in MS:
+        assert plans[M]["stash"] == N * S * D * 2  # the mini-batch's boundary inputs, bf16
+        assert plans[M]["params"] == plans[4]["params"]
+        assert plans[M]["grads"] == plans[4]["grads"]
+        assert plans[M]["grads"] >= 4 * 335_822_848  # fp32 accumulator per parameter
+
+
+def test_one_micro_batch_of_intermediates_scales_as_one_over_m(gp, monkeypatch):
+    """The workspace set that holds one micro-batch's re-materialised
+    intermediates (all L layers) is (keep - remat) / (M - 1) bytes with one
+    recompute set: proportional to T = N S / M, so set x M is the same for
+    every M (up to the 256-byte alignment of each buffer)."""
+    monkeypatch.setenv("GP_REMAT_AHEAD", "0")
+    per_set = {M: (plan(gp, CFG, M, True)["workspace"] - plan(gp, CFG, M)["workspace"]) / (M - 1) for M in MS}
+    whole = [per_set[M] * M for M in MS]
+    assert max(whole) - min(whole) <= 1e-3 * max(whole), per_set
+    # and the re-materialising workspace shrinks with M
+    w = [plan(gp, CFG, M)["workspace"] for M in MS]
+    assert all(a > b for a, b in zip(w, w[1:])), w
+
+
+def test_kept_activations_scale_with_the_whole_mini_batch(gp, monkeypatch):
+    monkeypatch.setenv("GP_REMAT_AHEAD", "0")
+    remat = {M: plan(gp, CFG, M)["workspace"] for M in MS}
+    keep = {M: plan(gp, CFG, M, keep=True)["workspace"] for M in MS}
+    for M in MS:
+        # M sets of the T-row layer intermediates (the whole mini-batch's)
+        # against one set
+        assert keep[M] >= 3 * remat[M], (M, keep[M], remat[M])
+    # nearly independent of M: within the fixed-size backward scratch of each other
+    lo, hi = min(keep.values()), max(keep.values())
+    assert hi - lo <= 0.25 * hi, keep
+    # the per-micro-batch share falls as 1/M with re-materialisation
+    assert remat[32] < remat[4] / 4
+    # enc1024 intermediates: about 36 KB per token and layer in bf16 (u, q k v,
+    # c, x1, v and its fp4 residual, the ReLU activation a at d_ff = 8192,
+    # LayerNorm statistics), so 16 layers x 16384 tokens need about 9.6 GB
+    per_token_layer = (keep[8] - remat[8]) / (CFG.layers * CFG.batch * CFG.seq) / (1 - 1 / 8)
+    assert 30_000 < per_token_layer < 40_000, per_token_layer
+
+
+def test_table1_order_of_growth(gp, monkeypatch):
+    """Activation memory against layers: with re-materialisation the
+    workspace grows with L times the micro-batch (L N / M); kept activations
+    grow with L times the mini-batch (L N)."""
+    monkeypatch.setenv("GP_REMAT_AHEAD", "0")
+    w = lambda L, keep: plan(gp, CFG.with_(layers=L), 8, keep)["workspace"]
+    per_layer_remat = w(16, False) - w(8, False)
+    per_layer_keep = w(16, True) - w(8, True)
+    # M = 8 micro-batches' intermediates per layer against one micro-batch's
+    # (both also hold the layer's LayerNorm partial sums, which do not scale)
+    assert 0.9 * 8 <= per_layer_keep / per_layer_remat <= 8.0, (per_layer_keep, per_layer_remat)

@@ -201,6 +201,24 @@ gp_status gp_forward_microbatch(gp_partition* p, int mb, const void* x, const vo
                                 gp_stream stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * forward pass as gp_forward_microbatch, same arguments, same results bit
+ * for bit, with no allocation of any kind.  The split-K partial tiles of its
+ * GEMMs go to a static device array of the library (32 MiB, one per device,
+ * held until the process ends) instead of the partition's workspace; it does
+ * not start the early recompute of the last micro-batch (that backward then
+ * recomputes on its own stream).  Every call on a device shares the array:
+ * calls that overlap on one device (two streams, two host threads) race.
+ * GP_ERR_UNSUPPORTED: the partition's forward needs more split-K scratch
+ *   than the array holds (the message states both sizes).
+ * GP_ERR_HIP: the array has no address on this device.
+ * Otherwise as gp_forward_microbatch.
+ */
+gp_status gp_forward_microbatch_noalloc(gp_partition* p, int mb, const void* x, const void* mem, void* y,
+                                        gp_stream stream);
+
+/*
  * Backward pass of micro-batch `mb` with re-materialisation (Section 2.3):
  * the layers' forward is recomputed from the stashed boundary input, keeping
  * this micro-batch's intermediates only, then back-propagated in reverse

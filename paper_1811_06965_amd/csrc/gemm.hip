@@ -1541,6 +1541,46 @@ gp_status gemm_reduce(const GemmArgs& a, int epi, int splits, hipStream_t st) {
     return launch_reduce(a, epi, splits, st);
 }
 
+namespace {
+// The tile shape and split count gemm() launches a bf16 problem with.
+void decide_bf16(const GemmArgs& a, int epi, bool a_kmajor, int& cfg, int& splits) {
+    if (a.a4) {
+        choose_dl(a, epi, true, cfg, splits);
+        if (a.force_cfg >= 0 && a.force_cfg <= T_LAST) {
+            // a forced shape without an fp4 stage falls back to the 128 x 128 tile
+            cfg = mx_capable(a.force_cfg) ? a.force_cfg : T_DL128x128_S2;
+            splits = a.force_splits > 0 ? a.force_splits : 1;
+            if (splits > 1 && !split_fits(a, splits, a.K / 64)) splits = 1;
+        }
+        return;
+    }
+    if (a.K % 64 == 0)
+        choose_dl(a, epi, a_kmajor, cfg, splits);
+    else
+        choose(a, epi, cfg, splits);
+    if (a.force_cfg >= 0 && a.force_cfg <= T_LAST) {
+        cfg = a.force_cfg;
+        splits = a.force_splits > 0 ? a.force_splits : 1;
+        if (splits > 1 && !split_fits(a, splits, (a.K + 63) / 64)) splits = 1;
+    }
+    if (cfg > T128x128 && a.K % 64) cfg = T128x128;
+    const bool narrow = cfg == T_DL128x64 || cfg == T_DL64x128 || cfg == T_DL128x64_S3 || cfg == T_DL128x64_S4;
+    const bool kg2 = cfg == T_DL128x64_KG2 || cfg == T_DL128x128_KG2 || cfg == T_DL64x128_KG2;
+    if (!a_kmajor && (narrow || kg2)) cfg = T_DL128x128_W8A;  // no 64-wide or k-group m-contiguous tiles
+    if (kg2 && (splits > 1 || (a.K / 64) % 2)) {               // k-groups: unsplit, even k-tile count
+        cfg = T_DL128x64_S4;
+        splits = 1;
+    }
+}
+} // namespace
+
+long gemm_workspace_need(const GemmArgs& a, int epi, bool a_kmajor, int dtype) {
+    if (dtype != GP_BF16 || !a.ws) return 0;
+    int cfg = 0, splits = 1;
+    decide_bf16(a, epi, a_kmajor, cfg, splits);
+    return splits > 1 ? (long)splits * a.M * a.N + (a.colsum ? (long)splits * a.N : 0) : 0;
+}
+
 gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dtype, hipStream_t st) {
     if (a.deferred) *a.deferred = 1;
     if (a.a4) {
@@ -1550,36 +1590,14 @@ gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dty
         gp_status s = check_args<bf16>(a, true, true);
         if (s != GP_OK) return s;
         int cfg, splits;
-        choose_dl(a, epi, true, cfg, splits);
-        if (a.force_cfg >= 0 && a.force_cfg <= T_LAST) {
-            // a forced shape without an fp4 stage falls back to the 128 x 128 tile
-            cfg = mx_capable(a.force_cfg) ? a.force_cfg : T_DL128x128_S2;
-            splits = a.force_splits > 0 ? a.force_splits : 1;
-            if (splits > 1 && !split_fits(a, splits, a.K / 64)) splits = 1;
-        }
+        decide_bf16(a, epi, true, cfg, splits);
         return launch_mx(a, cfg, splits, st);
     }
     if (dtype == GP_BF16) {
         gp_status s = check_args<bf16>(a, a_kmajor, b_kmajor);
         if (s != GP_OK) return s;
         int cfg, splits;
-        if (a.K % 64 == 0)
-            choose_dl(a, epi, a_kmajor, cfg, splits);
-        else
-            choose(a, epi, cfg, splits);
-        if (a.force_cfg >= 0 && a.force_cfg <= T_LAST) {
-            cfg = a.force_cfg;
-            splits = a.force_splits > 0 ? a.force_splits : 1;
-            if (splits > 1 && !split_fits(a, splits, (a.K + 63) / 64)) splits = 1;
-        }
-        if (cfg > T128x128 && a.K % 64) cfg = T128x128;
-        const bool narrow = cfg == T_DL128x64 || cfg == T_DL64x128 || cfg == T_DL128x64_S3 || cfg == T_DL128x64_S4;
-        const bool kg2 = cfg == T_DL128x64_KG2 || cfg == T_DL128x128_KG2 || cfg == T_DL64x128_KG2;
-        if (!a_kmajor && (narrow || kg2)) cfg = T_DL128x128_W8A;  // no 64-wide or k-group m-contiguous tiles
-        if (kg2 && (splits > 1 || (a.K / 64) % 2)) {               // k-groups: unsplit, even k-tile count
-            cfg = T_DL128x64_S4;
-            splits = 1;
-        }
+        decide_bf16(a, epi, a_kmajor, cfg, splits);
         return a_kmajor ? launch_bf16<true, true>(a, epi, cfg, splits, st)
                         : launch_bf16<false, false>(a, epi, cfg, splits, st);
     }

@@ -48,6 +48,9 @@ struct GemmArgs {
 };
 
 gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dtype, hipStream_t st);
+// Floats of a.ws that gemm() with these arguments writes (its split-K partial
+// tiles and column-sum rows); 0 when it runs unsplit.  Host arithmetic only.
+long gemm_workspace_need(const GemmArgs& a, int epi, bool a_kmajor, int dtype);
 // The split-K reduce and epilogue of a bf16 GEMM whose partials are in a.ws.
 gp_status gemm_reduce(const GemmArgs& a, int epi, int splits, hipStream_t st);
 

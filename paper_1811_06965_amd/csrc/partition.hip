@@ -22,6 +22,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <utility>
 #include <vector>
@@ -172,6 +173,12 @@ struct gp_partition {
     std::vector<std::vector<Span>> slot_span; // per set and layer slot
     Span bwd_span, lnpart_span, loss_span, loss_acc_span, head_span;
     Span splitk_span[3];                      // caller's stream, weight-gradient stream, recompute stream
+    // gp_forward_microbatch_noalloc: this device's address of the static
+    // scratch array (nullptr if it could not be resolved) and the most
+    // split-K partial floats one first forward pass writes
+    float* noalloc_scratch = nullptr;
+    std::string noalloc_error;
+    long fwd_ws_need = 0;
     // per LayerNorm: block partial sums of its gamma/beta gradients, added up
     // over the micro-batches of a mini-batch and reduced after the last one
     std::vector<float*> lnpart;
@@ -536,6 +543,39 @@ gp_status linear_fwd(const Ctx& c, const Linear& L, const void* A, long M, void*
         c.pend->g.deferred = nullptr;
     }
     return GP_OK;
+}
+
+// The most split-K partial floats one first forward pass of a micro-batch
+// writes: the largest need among its GEMMs, with the tile and split choice
+// linear_fwd's arguments lead to (they depend on the shape, the epilogue, the
+// fp4 correction and the workspace size, not on the operands' addresses).
+long forward_workspace_need(const gp_partition* p) {
+    static const unsigned char with_fp4 = 0;
+    long need = 0;
+    auto one = [&](const Linear& L, long M, int epi) {
+        if (!L.present) return;
+        GemmArgs g;
+        g.M = (int)M;
+        g.N = L.out;
+        g.K = L.in;
+        g.ws = p->bw.splitk;
+        g.ws_elems = p->bw.splitk_elems;
+        g.force_cfg = p->gemm_tile;
+        g.force_splits = p->gemm_splits;
+        if (L.split) g.a4 = &with_fp4;
+        need = std::max(need, gemm_workspace_need(g, epi, true, p->g.dtype));
+    };
+    const long T = p->g.T(), Tm = p->g.Tm();
+    for (const LayerPlan& P : p->plan.layers) {
+        one(P.qkv, T, EPI_STORE);
+        one(P.o, T, EPI_RES_F32);
+        one(P.xq, T, EPI_STORE);
+        one(P.xkv, Tm, EPI_STORE);
+        one(P.xo, T, EPI_RES_F32);
+        one(P.ffn1, T, EPI_STORE);
+        one(P.ffn2, T, EPI_RES_F32);
+    }
+    return need;
 }
 
 // dX = dY W^T with an epilogue; dY [M, out] k-contiguous, W working copy [in, out].
@@ -917,6 +957,44 @@ gp_status alloc(void** ptr, size_t bytes) {
 
 } // namespace
 
+// Scratch of gp_forward_microbatch_noalloc: the split-K partial tiles of the
+// GEMMs of its forward pass live in this file-scope device array instead of
+// the partition's workspace, so that a caller can run that pass with no
+// allocation anywhere.  Each device the library runs on holds its own copy
+// until the process ends; every such call on a device shares it, so calls
+// that overlap on one device race.  Nothing in it needs clearing: a GEMM
+// writes every partial tile it later reads.
+constexpr size_t NOALLOC_SCRATCH_FLOATS = (size_t)8 << 20;  // 32 MiB
+static __device__ __align__(256) float scratch[NOALLOC_SCRATCH_FLOATS];
+
+namespace {
+// Host code cannot use `scratch` itself (its host-side name is a stand-in,
+// not a device address): the address is resolved once per device, with that
+// device current, and kept here.
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[MAX_DEVICES] = {};
+bool g_scratch_done[MAX_DEVICES] = {};
+hipError_t g_scratch_err[MAX_DEVICES] = {};
+
+// This device's address of `scratch` (nullptr and *err set on failure).
+float* scratch_for_device(int dev, hipError_t* err) {
+    if (dev < 0 || dev >= MAX_DEVICES) {
+        *err = hipErrorInvalidDevice;
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_done[dev]) {
+        void* ptr = nullptr;
+        g_scratch_err[dev] = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        g_scratch_ptr[dev] = g_scratch_err[dev] == hipSuccess ? static_cast<float*>(ptr) : nullptr;
+        g_scratch_done[dev] = true;
+    }
+    *err = g_scratch_err[dev];
+    return g_scratch_ptr[dev];
+}
+} // namespace
+
 namespace {
 // Geometry, schedule knobs, parameter plan and byte counts of a partition for
 // cfg (already validated); host arithmetic only, no device is touched.
@@ -1073,6 +1151,17 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
         free_all(p);
         return hip_fail(e, __FILE__, __LINE__);
     }
+    // the no-allocation forward's scratch on this device, and its need
+    int dev = 0;
+    hipError_t se = hipGetDevice(&dev);
+    if (se == hipSuccess) p->noalloc_scratch = scratch_for_device(dev, &se);
+    if (se != hipSuccess) {
+        (void)hipGetLastError();
+        p->noalloc_scratch = nullptr;
+        p->noalloc_error = std::string("the static scratch array has no address on this device: ") +
+                           hipGetErrorString(se);
+    }
+    p->fwd_ws_need = forward_workspace_need(p);
     p->sched.configure(g.M, msg);
     return GP_OK;
 }
@@ -1223,6 +1312,49 @@ gp_status gp_forward_microbatch(gp_partition* p, int mb, const void* x, const vo
     } else {
         s = partition_forward(c, mb, false, x, mem, y);
     }
+    if (s != GP_OK) return s;
+    p->sched.did_forward();
+    return GP_OK;
+}
+
+gp_status gp_forward_microbatch_noalloc(gp_partition* p, int mb, const void* x, const void* mem, void* y,
+                                       gp_stream stream) {
+    if (!p) return set_error(GP_ERR_INVALID_ARG, "partition must not be NULL");
+    std::string msg;
+    gp_status s = p->sched.can_forward(mb, msg);
+    if (s != GP_OK) return set_error(s, msg.c_str());
+    if (!x) return set_error(GP_ERR_INVALID_ARG, "x must not be NULL");
+    const bool dec = p->g.kind == GP_DECODER_CROSS;
+    if (dec && !mem) return set_error(GP_ERR_INVALID_ARG, "decoder partitions need the memory input");
+    if (!dec && mem) return set_error(GP_ERR_INVALID_ARG, "encoder partitions take no memory input");
+    if (!p->noalloc_scratch) return set_error(GP_ERR_HIP, p->noalloc_error.c_str());
+    if ((size_t)p->fwd_ws_need > NOALLOC_SCRATCH_FLOATS) {
+        const std::string m = "forward pass needs " + std::to_string(p->fwd_ws_need * 4 >> 20) +
+                              " MiB of split-K scratch; the static scratch holds " +
+                              std::to_string(NOALLOC_SCRATCH_FLOATS * 4 >> 20) + " MiB";
+        return set_error(GP_ERR_UNSUPPORTED, m.c_str());
+    }
+    // Same tile and split choices as gp_forward_microbatch (the workspace size
+    // the chooser sees is unchanged); the partials go to the static scratch.
+    Ctx c = make_ctx(p, (hipStream_t)stream);
+    c.ws = p->noalloc_scratch;
+    if (p->poison) {
+        const long T = p->g.T(), D = p->d.D;
+        GP_TRY(poison_fill(p->noalloc_scratch, (size_t)p->fwd_ws_need * 4, c.st));
+        if (p->g.keep_act) {
+            GP_TRY(poison_set(p, p->set_of(mb), c.st));
+        } else {
+            GP_TRY(poison_span(p, p->slot_span[0][0], c.st));
+            for (int i = 0; i < 2 && i <= p->d.L; ++i)
+                GP_TRY(poison_span(p, Span{(size_t)((char*)p->xs[0][i] - p->ws), (size_t)(T * D) * 4}, c.st));
+        }
+    }
+    // No early recompute on the library's recompute stream: the backward of
+    // the last micro-batch re-materialises it itself.
+    if (p->g.keep_act)
+        s = partition_forward(c, mb, true, x, mem, y, p->set_of(mb));
+    else
+        s = partition_forward(c, mb, false, x, mem, y);
     if (s != GP_OK) return s;
     p->sched.did_forward();
     return GP_OK;

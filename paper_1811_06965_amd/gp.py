@@ -38,7 +38,8 @@ GP_K_NONE, GP_K_COUNT = 0, len(KERNEL_ROLES)
 EXPORTS = ["gp_partition_create", "gp_partition_configure", "gp_partition_destroy", "gp_set_param",
            "gp_get_param", "gp_get_grad", "gp_partition_memory", "gp_param_count", "gp_forward_microbatch",
            "gp_backward_microbatch_remat", "gp_accumulate_and_step", "gp_timer_select", "gp_timer_read",
-           "gp_timer_reset", "gp_timer_sample", "gp_mfma_peak", "gp_recomputed_output", "gp_memory_plan", "gp_last_error"]
+           "gp_timer_reset", "gp_timer_sample", "gp_mfma_peak", "gp_recomputed_output", "gp_memory_plan", "gp_forward_microbatch_noalloc",
+           "gp_last_error"]
 
 
 class gp_config(ctypes.Structure):
@@ -77,6 +78,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.gp_partition_memory.argtypes = [P] + [ctypes.POINTER(SZ)] * 4
     lib.gp_param_count.argtypes = [P, ctypes.POINTER(SZ)]
     lib.gp_forward_microbatch.argtypes = [P, I, VP, VP, VP, VP]
+    lib.gp_forward_microbatch_noalloc.argtypes = [P, I, VP, VP, VP, VP]
     lib.gp_backward_microbatch_remat.argtypes = [P, I, VP, VP, VP, VP]
     lib.gp_accumulate_and_step.argtypes = [P, ctypes.c_float, ctypes.POINTER(ctypes.c_double), VP]
     D = ctypes.POINTER(ctypes.c_double)
@@ -158,6 +160,10 @@ def gp_param_count(h):
 
 def gp_forward_microbatch(h, mb, x, mem, y, stream):
     _check(load().gp_forward_microbatch(h, mb, x, mem, y, stream))
+
+
+def gp_forward_microbatch_noalloc(h, mb, x, mem, y, stream):
+    _check(load().gp_forward_microbatch_noalloc(h, mb, x, mem, y, stream))
 
 
 def gp_backward_microbatch_remat(h, mb, dy_or_target, dx, dmem, stream):

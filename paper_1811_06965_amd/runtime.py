@@ -122,12 +122,13 @@ class Partition:
         return out
 
     def step(self, x, mem, dy, lr=0.0, want_y=True, want_dx=True, want_dmem=True, want_loss=True,
-             stream=None, y=None, dx=None, dmem=None, want_recomputed=False):
+             stream=None, y=None, dx=None, dmem=None, want_recomputed=False, noalloc=False):
         """One mini-batch through GPipe's schedule.  x/mem/dy: device tensors
         of the whole mini-batch (dim 0 = sequences).  Returns dict(y, dx, dmem,
         loss); with want_recomputed also "y_remat", the partition output as
         each backward call re-materialised it (gp_recomputed_output), in
-        mini-batch order."""
+        mini-batch order.  noalloc: the forwards go through
+        gp_forward_microbatch_noalloc."""
         M = self.M
         st = stream if stream is not None else torch.cuda.current_stream().cuda_stream
         if want_y and y is None:
@@ -143,8 +144,9 @@ class Partition:
         dxs = dx.chunk(M) if dx is not None else [None] * M
         dms = dmem.chunk(M) if dmem is not None else [None] * M
         ptr = lambda t: None if t is None else t.data_ptr()
+        fwd = gp.gp_forward_microbatch_noalloc if noalloc else gp.gp_forward_microbatch
         for m in range(M):
-            gp.gp_forward_microbatch(self.h, m, ptr(xs[m]), ptr(ms[m]), ptr(ys[m]), st)
+            fwd(self.h, m, ptr(xs[m]), ptr(ms[m]), ptr(ys[m]), st)
         y_remat = torch.empty_like(x) if want_recomputed else None
         yr = y_remat.chunk(M) if want_recomputed else None
         for m in range(M - 1, -1, -1):

@@ -2,9 +2,12 @@
 
 Workload: one-eighth of a 128-layer Transformer -- a partition of 16 pre-LN
 encoder layers, d_model 1024, 16 heads, d_ff 8192, ReLU, sequence 256, a
-mini-batch of 64 sequences split into M micro-batches (default 8), bf16
-operands with fp32 accumulation, random N(0,1) boundary inputs and boundary
-gradients, Xavier-uniform weights (synthetic data).
+mini-batch of 64 sequences split into M micro-batches (8 for the headline
+value; every M in {4, 8, 16, 32} is timed too, each beside the
+stored-activation baseline that keeps every intermediate instead of
+recomputing it), bf16 operands with fp32 accumulation, random N(0,1)
+boundary inputs and boundary gradients, Xavier-uniform weights (synthetic
+data).
 
 One step = M x gp_forward_microbatch + M x gp_backward_microbatch_remat +
 gp_accumulate_and_step (GPipe, Sections 2.2-2.3), enqueued on the caller's
@@ -42,7 +45,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--micro", type=int, default=8, help="micro-batches M of the timed workload")
     ap.add_argument("--config", default="enc1024")
-    ap.add_argument("--sweep", action="store_true", help="also time M in {4, 8, 16, 32}")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="time only --micro (by default M in {4, 8, 16, 32} are all timed, and the stored-"
+                         "activation baseline beside each)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=16, help="layers in the oracle's timed sample")
     ap.add_argument("--role", default=None, help="time this launch role instead of the dominant one")
@@ -58,6 +63,9 @@ def parse():
                     help="print a markdown summary of a rocprofv3 --kernel-trace database under DIR "
                          "(per-kernel totals, and per-role launch durations when GP_TIMER_MARKERS=1 was set)")
     ap.add_argument("--command", default="", help="the profiled command, quoted in --kernel-summary output")
+    ap.add_argument("--roles-json", default=None,
+                    help="with --kernel-summary: also store the per-role launch durations of the trace here "
+                         "(read back by the benchmark's roofline figure)")
     return ap.parse_args()
 
 
@@ -73,7 +81,7 @@ def _short(name):
     return re.sub(r"\(gp::(GemmArgs|AttnArgs)\)|\(gp::GemmArgs, int\)", "", name)[:110]
 
 
-def kernel_summary(d, command, top=25):
+def kernel_summary(d, command, top=25, roles_json=None):
     """Markdown summary of a rocprofv3 kernel-trace database."""
     import glob
     import sqlite3
@@ -106,6 +114,18 @@ def kernel_summary(d, command, top=25):
                 spans.setdefault(cur[sid][0], []).append(cur.pop(sid)[1])
         elif sid in cur:
             cur[sid][1].append((_short(name), t0, t1))
+    if spans and roles_json:
+        rec = {"source_sha256": source_digest(), "command": command, "roles": {}}
+        for role, ls in spans.items():
+            ls = [l for l in ls if l]
+            if ls:
+                rec["roles"][gp.KERNEL_ROLES[role]] = {
+                    "launches": len(ls),
+                    "mean_kernel_us": sum(t1 - t0 for l in ls for _, t0, t1 in l) / len(ls) / 1e3,
+                    "mean_span_us": sum(l[-1][2] - l[0][1] for l in ls) / len(ls) / 1e3,
+                    "kernels": sorted({n for l in ls for n, _, _ in l})}
+        with open(roles_json, "w") as f:
+            json.dump(rec, f, indent=1)
     if spans:
         print("\n## Launch roles (kernels between role markers)\n")
         print("| role | launches | mean kernel us per launch | mean first-start to last-end us | kernels |\n|---|---|---|---|---|")
@@ -206,18 +226,20 @@ def traffic_summary(fetch_dir, write_dir, cal_fetch_dir, cal_write_dir, role, wo
     print(json.dumps({role: entry}, indent=1))
 
 
-def run_steps(part, inp, n, dx):
+def run_steps(part, inp, n, out):
+    """n whole steps with every boundary output the pipeline passes on: y to
+    the next partition (forward), dX to the previous one (backward)."""
     for _ in range(n):
-        part.step(inp["x"], inp["mem"], inp["dy"], lr=0.0, want_y=False, want_dx=True, want_loss=False, dx=dx)
+        part.step(inp["x"], inp["mem"], inp["dy"], lr=0.0, want_loss=False, y=out["y"], dx=out["dx"])
 
 
-def census(part, inp, dx):
+def census(part, inp, out):
     """One untimed step with every launch role timed; roles by total time."""
     import torch
     from paper_1811_06965_amd import gp
     part.timer_reset()
     part.timer_select("all")
-    run_steps(part, inp, 1, dx)
+    run_steps(part, inp, 1, out)
     torch.cuda.synchronize()
     part.timer_select(None)
     roles = {}
@@ -246,7 +268,7 @@ def dominant_role(roles):
 TIMER_EVERY = 8
 
 
-def timed_eager(part, inp, steps, dx, role):
+def timed_eager(part, inp, steps, out, role):
     """K eager steps between two events on the launch stream, with every
     TIMER_EVERY-th launch of the role bracketed by dispatch events."""
     import torch
@@ -258,7 +280,7 @@ def timed_eager(part, inp, steps, dx, role):
     t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0.record(st)
-    run_steps(part, inp, steps, dx)
+    run_steps(part, inp, steps, out)
     t1.record(st)
     torch.cuda.synchronize()
     part.timer_select(None)
@@ -268,11 +290,34 @@ def timed_eager(part, inp, steps, dx, role):
     return t0.elapsed_time(t1) / steps, timed
 
 
-def timed_graph(part, inp, steps, dx):
+def device_free():
+    import torch
+    torch.cuda.synchronize()
+    return torch.cuda.mem_get_info()[0]
+
+
+def time_plain(part, inp, steps, warmup):
+    """Milliseconds per step over `steps` eager steps after `warmup`, between
+    two events on the launch stream, no launch timed."""
+    import torch
+    out = {"y": torch.empty_like(inp["x"]), "dx": torch.empty_like(inp["x"])}
+    run_steps(part, inp, warmup, out)
+    st = torch.cuda.current_stream()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(st)
+    run_steps(part, inp, steps, out)
+    t1.record(st)
+    torch.cuda.synchronize()
+    return t0.elapsed_time(t1) / steps
+
+
+def timed_graph(part, inp, steps, out):
     """The step captured once into a HIP graph, then K replays between two
     events on the replay stream."""
     import torch
-    g = part.capture_step(inp["x"], inp["mem"], inp["dy"], lr=0.0, dx=dx)
+    g = part.capture_step(inp["x"], inp["mem"], inp["dy"], lr=0.0, dx=out["dx"], want_y=True, y=out["y"])
     g.replay()
     torch.cuda.synchronize()
     st = torch.cuda.current_stream()
@@ -290,17 +335,19 @@ def timed_graph(part, inp, steps, dx):
 def time_steps(part, inp, steps, warmup, role=None, graph=False):
     """Returns (ms per step, role, role timings, census, how the role was timed)."""
     import torch
-    dx = torch.empty_like(inp["x"])
-    run_steps(part, inp, warmup, dx)
+    out = {"y": torch.empty_like(inp["x"]), "dx": torch.empty_like(inp["x"])}
+    run_steps(part, inp, warmup, out)
     torch.cuda.synchronize()
-    roles = census(part, inp, dx) if role is None else None
+    roles = census(part, inp, out) if role is None else None
     if role is None:
         role = dominant_role(roles)
     if not graph:
-        ms, timed = timed_eager(part, inp, steps, dx, role)
-        return ms, role, timed, roles, f"dispatch events on every {TIMER_EVERY}th launch over the timed eager steps"
-    ms = timed_graph(part, inp, steps, dx)
-    _, timed = timed_eager(part, inp, max(1, min(steps, 3)), dx, role)
+        ms, timed = timed_eager(part, inp, steps, out, role)
+        return ms, role, timed, roles, (f"HIP events attached to the dispatches of every {TIMER_EVERY}th launch of "
+                                        "the role inside the timed eager steps (the kernels share the GPU with the "
+                                        "weight-gradient and recompute streams)")
+    ms = timed_graph(part, inp, steps, out)
+    _, timed = timed_eager(part, inp, max(1, min(steps, 3)), out, role)
     return ms, role, timed, roles, (f"dispatch events on every {TIMER_EVERY}th launch over eager steps run after "
                                     "the graph-replay timed region")
 
@@ -332,28 +379,76 @@ def stored_traffic(role, workload):
     return e["bytes_per_launch"]
 
 
+ROLES_FILE = os.path.join(ROOT, "profiles", "kernel_roles_enc1024_m8.json")
+
+
+def profiled_launch(role):
+    """The role's mean kernel time per launch in the committed rocprofv3
+    kernel trace of the benchmark (kernels between the role's markers), if
+    that trace was taken on the current kernels; else None."""
+    try:
+        with open(ROLES_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    e = rec.get("roles", {}).get(role)
+    if not e or rec.get("source_sha256") != source_digest():
+        return None
+    return dict(e, command=rec.get("command", ""))
+
+
 def roofline(role, timed, workload):
     """Roofline figure of the dominant launch role: algorithmic work per launch
-    over the mean event-to-event launch duration."""
+    over the mean event-to-event launch duration measured in this run; beside
+    it the same figure from the committed kernel trace's mean kernel time."""
     n = max(timed["launches"], 1)
     dur = timed["ms"] * 1e-3 / n
+    per = timed["flops"] / n if timed["flops"] > 0 else timed["bytes"] / n
     if timed["flops"] > 0:
-        achieved, peak, unit, bound = timed["flops"] / n / dur / 1e12, PEAK_BF16 / 1e12, "TFLOP/s", "mfma"
+        scale, peak, unit, bound = 1e12, PEAK_BF16 / 1e12, "TFLOP/s", "mfma"
     else:
-        achieved, peak, unit, bound = timed["bytes"] / n / dur / 1e9, PEAK_HBM / 1e9, "GB/s", "hbm"
-    return {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
-            "traffic": stored_traffic(role, workload), "role": role, "launches_timed": timed["launches"],
-            "mean_launch_us": dur * 1e6, "algorithmic_flops_per_launch": timed["flops"] / n,
-            "algorithmic_bytes_per_launch": timed["bytes"] / n}
+        scale, peak, unit, bound = 1e9, PEAK_HBM / 1e9, "GB/s", "hbm"
+    achieved = per / dur / scale
+    out = {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
+           "traffic": stored_traffic(role, workload), "role": role, "launches_timed": timed["launches"],
+           "mean_launch_us": dur * 1e6, "algorithmic_flops_per_launch": timed["flops"] / n,
+           "algorithmic_bytes_per_launch": timed["bytes"] / n}
+    prof = profiled_launch(role)
+    if prof:
+        out["rocprof"] = {"file": os.path.relpath(ROLES_FILE, ROOT), "command": prof["command"],
+                          "mean_kernel_us": prof["mean_kernel_us"], "launches": prof["launches"],
+                          "achieved": per / (prof["mean_kernel_us"] * 1e-6) / scale,
+                          "frac": per / (prof["mean_kernel_us"] * 1e-6) / scale / peak}
+    else:
+        out["rocprof"] = None
+    return out
 
 
-def blas_threads():
+def blas_info():
+    """(threads, description) of the BLAS numpy runs on."""
     try:
         from threadpoolctl import threadpool_info
-        n = [i["num_threads"] for i in threadpool_info() if i.get("user_api") == "blas"]
-        return max(n) if n else 1
+        libs = [i for i in threadpool_info() if i.get("user_api") == "blas"]
     except Exception:
-        return len(os.sched_getaffinity(0))
+        libs = []
+    if not libs:
+        return len(os.sched_getaffinity(0)), "unknown BLAS"
+    lib = max(libs, key=lambda i: i["num_threads"])
+    desc = f"{lib.get('internal_api', 'blas')} {lib.get('version', '')} ({lib.get('architecture', '')} kernels, " \
+           f"{lib['num_threads']} threads)"
+    return lib["num_threads"], desc
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
 
 
 def cpu_baseline(cfg, layers):
@@ -369,7 +464,9 @@ def cpu_baseline(cfg, layers):
     gpipe.gpipe_step(sample, case, 1)
     dt = time.perf_counter() - t
     tok_s = n * cfg.seq / (dt * cfg.layers / layers)
-    return {"value": tok_s, "unit": "tokens/s", "cores": blas_threads(), "kind": "oracle",
+    threads, blas = blas_info()
+    return {"value": tok_s, "unit": "tokens/s", "cores": threads, "kind": "oracle", "cpu": cpu_model(),
+            "blas": blas, "host_cpus_available": len(os.sched_getaffinity(0)),
             "sample": f"{layers} of {cfg.layers} layers, one micro-batch of {n} sequences x {cfg.seq} tokens, "
                       f"forward + re-materialised forward + backward in fp64 numpy ({dt:.1f} s), "
                       f"scaled by {cfg.layers}/{layers} layers"}
@@ -389,7 +486,7 @@ def main():
                 f"in M={cfg.micro} micro-batches, " +
                 ("boundary gradients" if cfg.loss == "none" else f"{cfg.loss} loss"))
     if a.kernel_summary:
-        kernel_summary(a.kernel_summary, a.command)
+        kernel_summary(a.kernel_summary, a.command, roles_json=a.roles_json)
         return
     if a.traffic_summary:
         if not a.role:
@@ -406,22 +503,42 @@ def main():
         return
     case = synth.make_case(cfg, 0)
     results = {}
-    Ms = [a.micro] + ([m for m in (4, 8, 16, 32) if m != a.micro] if a.sweep else [])
+    Ms = [a.micro] + ([] if a.no_sweep else [m for m in (4, 8, 16, 32) if m != a.micro])
     for M in Ms:
         c = base.with_(micro=M)
+        steps = a.steps if M == a.micro else max(3, a.steps // 2)
+        f0 = device_free()
         with Partition(c) as part:
+            allocated = f0 - device_free()
             part.load_params(case["layers"], case["head"])
             inp = part.device_inputs(case)
-            ms, role, timed, roles, how = time_steps(part, inp, a.steps if M == a.micro else max(3, a.steps // 2),
-                                                     a.warmup, a.role, graph=a.graph)
+            ms, role, timed, roles, how = time_steps(part, inp, steps, a.warmup, a.role, graph=a.graph)
             mem = part.memory()
             del inp
         model, hw = accounting.step_flops(c)
         results[M] = {"M": M, "ms_per_step": ms, "tokens_per_s": c.batch * c.seq / (ms * 1e-3),
                       "hfu": hw / (ms * 1e-3) / PEAK_BF16, "mfu": model / (ms * 1e-3) / PEAK_BF16,
-                      "memory_bytes": mem, "role": role, "timed": timed, "roles": roles, "how": how}
+                      "memory_bytes": mem, "device_bytes_measured": allocated,
+                      "role": role, "timed": timed, "roles": roles, "how": how}
         print(f"[bench] M={M}: {ms:.2f} ms/step, {results[M]['tokens_per_s']:.0f} tokens/s, "
-              f"HFU {100 * results[M]['hfu']:.1f}%, dominant role {role}", file=sys.stderr, flush=True)
+              f"HFU {100 * results[M]['hfu']:.1f}%, dominant role {role}, device memory "
+              f"{allocated / 2**30:.2f} GiB", file=sys.stderr, flush=True)
+        if not a.no_sweep:
+            # the stored-activation baseline: every micro-batch keeps its
+            # intermediates, no recompute (3 forward passes of work instead of 4)
+            f0 = device_free()
+            with Partition(c, keep_activations=True) as part:
+                allocated = f0 - device_free()
+                part.load_params(case["layers"], case["head"])
+                inp = part.device_inputs(case)
+                kms = time_plain(part, inp, max(3, a.steps // 2), a.warmup)
+                kmem = part.memory()
+                del inp
+            results[M]["stored_activations"] = {
+                "ms_per_step": kms, "tokens_per_s": c.batch * c.seq / (kms * 1e-3),
+                "hfu": model / (kms * 1e-3) / PEAK_BF16, "memory_bytes": kmem, "device_bytes_measured": allocated}
+            print(f"[bench] M={M} stored activations: {kms:.2f} ms/step, device memory "
+                  f"{allocated / 2**30:.2f} GiB", file=sys.stderr, flush=True)
     # the sustained MFMA-loop rate of this device, measured after the timed runs
     from paper_1811_06965_amd import gp
     peak_meas = gp.gp_mfma_peak(torch.cuda.current_stream().cuda_stream) * 1e12
@@ -446,11 +563,15 @@ def main():
         step_ms = r["ms_per_step"]
         out["roles_ms_per_step"] = {k: round(v["ms"], 3) for k, v in r["roles"].items()}
         out["roles_note"] = f"census step with every launch bracketed; step time {step_ms:.2f} ms unbracketed"
-    if a.sweep:
-        out["sweep"] = [{k: v for k, v in results[M].items()
-                         if k in ("M", "ms_per_step", "tokens_per_s", "hfu", "mfu", "hfu_measured_peak",
-                                  "memory_bytes")}
+    if not a.no_sweep:
+        keys = ("M", "ms_per_step", "tokens_per_s", "hfu", "mfu", "hfu_measured_peak", "memory_bytes",
+                "device_bytes_measured", "stored_activations")
+        out["sweep"] = [dict({k: v for k, v in results[M].items() if k in keys},
+                             roles_ms_per_step={k: round(v["ms"], 3) for k, v in (results[M]["roles"] or {}).items()})
                         for M in sorted(results)]
+        out["sweep_note"] = ("re-materialised steps (4 forward passes of work: hfu) beside the stored-activation "
+                             "baseline (no recompute, 3 forward passes: its hfu counts those); memory_bytes is the "
+                             "library's plan, device_bytes_measured the drop in free device memory at configure")
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, a.cpu_layers)
     print(json.dumps(out))

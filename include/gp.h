@@ -103,9 +103,8 @@ typedef struct {
     float rms_decay;         /* GP_OPT_RMSPROP: rho in [0, 1) */
     float rms_eps;           /* GP_OPT_RMSPROP: eps > 0, inside the square root */
     float logit_clip;        /* GP_LOSS_XENT_LS: c > 0 clips every logit to [-c, c] before the softmax
-                                (Section 5: logit predictions are clipped when their magnitude
-                                exceeds a certain value); the gradient passes where |z| <= c.
-                                0 = off */
+                                (Section 5 bounds the magnitude of the softmax pre-activations for
+                                trainability); the gradient passes where |z| <= c.  0 = off */
 } gp_config;
 
 /* Parameter tensors.  Matrices are logical [in, out] (y = x W + b); attention
@@ -180,6 +179,20 @@ gp_status gp_partition_memory(gp_partition* p, size_t* params, size_t* grads, si
  * gp_partition_configure. */
 gp_status gp_memory_plan(int layers, int d_model, int d_ff, int heads, const gp_config* cfg, size_t* params,
                          size_t* grads, size_t* stash, size_t* workspace);
+
+/*
+ * GPipe's partitioning algorithm (Sections 2.1-2.2): split `layers` layers,
+ * layer i with cost estimate costs[i] (host array, finite, >= 0), into
+ * `cells` cells of consecutive layers whose summed costs C_k have the least
+ * variance, (1/K) sum_k (C_k - mean)^2.  Exact (a dynamic program over the
+ * prefix sums, O(cells layers^2) host time); among equal optima the one with
+ * the smallest cuts.  first_layer (host, `cells` ints) receives the index of
+ * each cell's first layer (first_layer[0] = 0); variance (nullable) the
+ * least variance.  Host code only: no device is touched.
+ * GP_ERR_INVALID_ARG: NULL costs or first_layer, not 1 <= cells <= layers,
+ *   a negative or non-finite cost.
+ */
+gp_status gp_plan_cells(const double* costs, int layers, int cells, int* first_layer, double* variance);
 
 /* Number of trainable parameters (layers plus head). */
 gp_status gp_param_count(gp_partition* p, size_t* count);

@@ -199,8 +199,8 @@ def mse_loss(y, target, norm):
 
 
 def clip_logits(Z, c):
-    """Section 5: logit predictions (the softmax pre-activations) are clipped
-    when their magnitude exceeds c.  Returns min(max(Z, -c), c) and the clip's
+    """Section 5 bounds the magnitude of the softmax inputs for trainability;
+    here by a hard clip at c.  Returns min(max(Z, -c), c) and the clip's
     derivative, 1 where -c <= Z <= c and 0 elsewhere; c = 0 means no clip."""
     if c <= 0.0:
         return Z, np.ones_like(Z)

@@ -39,7 +39,7 @@ EXPORTS = ["gp_partition_create", "gp_partition_configure", "gp_partition_destro
            "gp_get_param", "gp_get_grad", "gp_partition_memory", "gp_param_count", "gp_forward_microbatch",
            "gp_backward_microbatch_remat", "gp_accumulate_and_step", "gp_timer_select", "gp_timer_read",
            "gp_timer_reset", "gp_timer_sample", "gp_mfma_peak", "gp_recomputed_output", "gp_memory_plan", "gp_forward_microbatch_noalloc",
-           "gp_last_error"]
+           "gp_plan_cells", "gp_last_error"]
 
 
 class gp_config(ctypes.Structure):
@@ -79,6 +79,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.gp_param_count.argtypes = [P, ctypes.POINTER(SZ)]
     lib.gp_forward_microbatch.argtypes = [P, I, VP, VP, VP, VP]
     lib.gp_forward_microbatch_noalloc.argtypes = [P, I, VP, VP, VP, VP]
+    lib.gp_plan_cells.argtypes = [ctypes.POINTER(ctypes.c_double), I, I, ctypes.POINTER(ctypes.c_int),
+                                  ctypes.POINTER(ctypes.c_double)]
     lib.gp_backward_microbatch_remat.argtypes = [P, I, VP, VP, VP, VP]
     lib.gp_accumulate_and_step.argtypes = [P, ctypes.c_float, ctypes.POINTER(ctypes.c_double), VP]
     D = ctypes.POINTER(ctypes.c_double)
@@ -150,6 +152,18 @@ def gp_memory_plan(layers, d_model, d_ff, heads, cfg: gp_config):
     v = [ctypes.c_size_t() for _ in range(4)]
     _check(load().gp_memory_plan(layers, d_model, d_ff, heads, ctypes.byref(cfg), *[ctypes.byref(x) for x in v]))
     return dict(params=v[0].value, grads=v[1].value, stash=v[2].value, workspace=v[3].value)
+
+
+def gp_plan_cells(costs, cells):
+    """Least-variance split of the layers (costs: 1-D float array) into
+    `cells` cells; returns (first layer of each cell, variance)."""
+    import numpy as np
+    c = np.ascontiguousarray(costs, dtype=np.float64)
+    first = (ctypes.c_int * max(cells, 1))()
+    var = ctypes.c_double()
+    _check(load().gp_plan_cells(c.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), c.size, cells, first,
+                                ctypes.byref(var)))
+    return [int(v) for v in first[:cells]], var.value
 
 
 def gp_param_count(h):

@@ -15,15 +15,19 @@
 //   workspace       per set: residual stream xs[0..L] fp32 [T, D] (T = n S) and
 //                   per-layer intermediates of one micro-batch; backward scratch
 // The forward pass writes its intermediates into layer slot 0 of set 0 and
-// ping-pongs xs[0]/xs[1]; the re-materialising pass of micro-batch m uses set
-// m % 2 (one set when M = 1 or recompute-ahead is off), slot l and xs[l] for
-// layer l.  All run the same kernels with the same launch shapes, so the
-// recomputed activations equal the first pass bit for bit.
+// ping-pongs xs[0]/xs[1]; the re-materialising pass of micro-batch m uses its
+// set (set_of: sets rotate so that the one being rebuilt ahead is never one
+// still read), slot l and xs[l] for layer l.  Sets come in groups of two
+// micro-batches whose buffers hold both back to back, so that the weight
+// gradients of a pair run as one GEMM.  All passes run the same kernels with
+// the same launch shapes, so the recomputed activations equal the first pass
+// bit for bit.
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <type_traits>
 #include <utility>
 #include <vector>
 
@@ -104,6 +108,24 @@ struct BwdWs {
     void *h = nullptr, *z = nullptr;
 };
 
+// Paired weight gradients: the weight-gradient GEMMs of micro-batches 2i and
+// 2i + 1 run as one GEMM with a reduction over both micro-batches' token rows
+// (one fp32 read-modify-write of the accumulator, one launch, per pair).
+// Their operands must then stay until the later backward call of the pair,
+// and sit back to back: per layer, the bf16 gradients a layer's weight-
+// gradient GEMMs take as dY live here, two micro-batches' rows each
+// (half 0 = the even micro-batch), instead of in the recycled ring and
+// parity buffers; the activations come from workspace sets allocated in pairs.
+struct DyStore {
+    void* gin = nullptr;    // dL/dx_out of the layer (dY of the ffn2 weight gradient)
+    void* gffn = nullptr;   // after the feed-forward block's LayerNorm backward (dY of o / xo)
+    void* gcross = nullptr; // decoder: after the cross-attention block's LayerNorm backward (dY of o)
+    void* dz = nullptr;     // dY of the ffn1 weight gradient
+    void* dqkv = nullptr;   // dY of the qkv weight gradient
+    void* dxq = nullptr;    // decoder: dY of the cross-attention query weight gradient
+    void* dxkv = nullptr;   // decoder: dY of the cross-attention key/value weight gradient (memory rows)
+};
+
 } // namespace gp
 
 using namespace gp;
@@ -162,6 +184,13 @@ struct gp_partition {
     std::vector<std::vector<float*>> xs;
     std::vector<std::vector<LayerWs>> lw;
     int nsets = 1;
+    // paired weight gradients (GP_PAIR_DW=0 turns them off): workspace sets are
+    // allocated in groups of `group` (2 when pairing) whose buffers hold the
+    // group's micro-batches back to back
+    bool pair_dw = true;
+    int group = 1;
+    std::vector<DyStore> dys;  // per layer (pairing only)
+    bool dw_started = false;   // a weight-gradient GEMM of this mini-batch was launched
     float* opt_ms = nullptr;  // RMSProp: running mean square of every gradient [n32]
     // GP_POISON=1 (test mode): every workspace region is filled with NaN
     // right before the phase that (re)writes it, so that a read of a stale or
@@ -170,7 +199,9 @@ struct gp_partition {
     // partial sums, the split-K partials of each stream, the loss partials.
     bool poison = false;
     std::vector<Span> xs_span;                // per set: xs[set][0..L]
-    std::vector<std::vector<Span>> slot_span; // per set and layer slot
+    std::vector<std::vector<Span>> slot_span; // per set: every buffer of its layer slots, layer by layer
+    int slot_bufs = 0;                        // buffers per layer slot
+    std::vector<std::vector<Span>> dys_span;  // per half: that half of every paired-gradient buffer
     Span bwd_span, lnpart_span, loss_span, loss_acc_span, head_span;
     Span splitk_span[3];                      // caller's stream, weight-gradient stream, recompute stream
     // gp_forward_microbatch_noalloc: this device's address of the static
@@ -227,10 +258,21 @@ struct gp_partition {
     hipEvent_t remat_done = nullptr;  // from evring
     int remat_pending = -1;  // micro-batch whose recompute-ahead is enqueued
 
-    // Workspace set of micro-batch m: its own set when activations are kept,
-    // else set m % 2 with recompute-ahead (two sets) or set 0.
-    int set_of(int m) const { return g.keep_act ? m : (nsets > 1 ? (m & 1) : 0); }
-    bool ahead() const { return !g.keep_act && nsets > 1; }  // recompute-ahead / early-recompute stream in use
+    // Workspace set of micro-batch m: its own set when activations are kept;
+    // else the sets rotate group by group -- micro-batch m takes member m % group
+    // of group (m / group) mod (nsets / group) -- so that with recompute-ahead
+    // the set being rebuilt is never one the backward or a pending paired
+    // weight gradient still reads.
+    int set_of(int m) const {
+        if (g.keep_act) return m;
+        return group * ((m / group) % (nsets / group)) + m % group;
+    }
+    // paired weight gradients: rows of micro-batch m's pair, and whether m's
+    // backward launches them (the even member; the odd one runs first and defers)
+    int pair_size(int m) const { return (m - m % 2) + 1 < g.M ? 2 : 1; }
+    bool launches_dw(int m) const { return group == 1 || m % 2 == 0; }
+    bool ahead_on = false;  // recompute-ahead / early-recompute stream in use
+    bool ahead() const { return ahead_on; }
     void* W(size_t elt_off) const { return welt + elt_off * esz; }
     char* stash_x_mb(int m) const { return stash_x + (size_t)m * g.T() * d.D * esz; }
     char* stash_m_mb(int m) const { return stash_m + (size_t)m * g.Tm() * d.D * esz; }
@@ -251,55 +293,88 @@ void plan_workspace(gp_partition* p, Arena& a) {
     p->xs.assign(p->nsets, std::vector<float*>(d.L + 1, nullptr));
     p->lw.assign(p->nsets, std::vector<LayerWs>(d.L, LayerWs{}));
     p->xs_span.assign(p->nsets, Span{});
-    p->slot_span.assign(p->nsets, std::vector<Span>(d.L, Span{}));
+    p->slot_span.assign(p->nsets, std::vector<Span>{});
+    p->slot_bufs = 0;
     auto span_from = [&](size_t start) { return Span{start, a.off - start}; };
     for (int set = 0; set < p->nsets; ++set) {
         const size_t s0 = a.mark();
         for (auto& x : p->xs[set]) x = a.take<float>(T * D);
         p->xs_span[set] = span_from(s0);
     }
-    for (int set = 0; set < p->nsets; ++set) {
+    // Layer slots, one group of sets at a time: each buffer holds the rows of
+    // the group's members back to back (member h at row h * rows).
+    const int G = p->group;
+    for (int g0 = 0; g0 < p->nsets; g0 += G) {
         for (int li = 0; li < d.L; ++li) {
-            LayerWs& l = p->lw[set][li];
-            const size_t s0 = a.mark();
-            l.st1 = a.take<float>(2 * T);
-            l.u = a.take_elt(T * D, e);
-            l.qkv = a.take_elt(T * 3 * D, e);
-            l.c = a.take_elt(T * D, e);
-            l.lse = a.take<float>(lse_n);
-            l.x1 = a.take<float>(T * D);
+            // one buffer of `count` elements of `esz` bytes per member
+            auto take = [&](auto LayerWs::*field, long count, size_t esz) {
+                const size_t off = a.mark();
+                char* base = static_cast<char*>(a.take_elt((size_t)count * G, esz));
+                for (int h = 0; h < G; ++h) {
+                    p->lw[g0 + h][li].*field = reinterpret_cast<typename std::remove_reference<
+                        decltype(p->lw[0][0].*field)>::type>(base + (size_t)h * count * esz);
+                    p->slot_span[g0 + h].push_back(Span{off + (size_t)h * count * esz, (size_t)count * esz});
+                }
+            };
+            take(&LayerWs::st1, 2 * T, 4);
+            take(&LayerWs::u, T * D, e);
+            take(&LayerWs::qkv, T * 3 * D, e);
+            take(&LayerWs::c, T * D, e);
+            take(&LayerWs::lse, lse_n, 4);
+            take(&LayerWs::x1, T * D, 4);
             if (dec) {
-                l.stc = a.take<float>(2 * T);
-                l.uc = a.take_elt(T * D, e);
-                l.xq = a.take_elt(T * D, e);
-                l.xkv = a.take_elt(Tm * 2 * D, e);
-                l.xc = a.take_elt(T * D, e);
-                l.xlse = a.take<float>(lse_n);
-                l.x2 = a.take<float>(T * D);
+                take(&LayerWs::stc, 2 * T, 4);
+                take(&LayerWs::uc, T * D, e);
+                take(&LayerWs::xq, T * D, e);
+                take(&LayerWs::xkv, Tm * 2 * D, e);
+                take(&LayerWs::xc, T * D, e);
+                take(&LayerWs::xlse, lse_n, 4);
+                take(&LayerWs::x2, T * D, 4);
             }
-            l.stf = a.take<float>(2 * T);
-            l.v = a.take_elt(T * D, e);
+            take(&LayerWs::stf, 2 * T, 4);
+            take(&LayerWs::v, T * D, e);
             if (p->g.dtype == GP_BF16) {  // see Linear::split
-                l.v4 = a.take<unsigned char>(T * D / 2);
-                l.v4s = a.take<unsigned char>(T);
+                take(&LayerWs::v4, T * D / 2, 1);
+                take(&LayerWs::v4s, T, 1);
             }
-            l.a = a.take_elt(T * F, e);
-            p->slot_span[set][li] = span_from(s0);
+            take(&LayerWs::a, T * F, e);
+            if (g0 == 0 && li == 0) p->slot_bufs = (int)p->slot_span[0].size();
+        }
+    }
+    // paired weight-gradient operands: per layer, two micro-batches' rows
+    p->dys.assign(G > 1 ? d.L : 0, DyStore{});
+    p->dys_span.assign(G > 1 ? 2 : 0, std::vector<Span>{});
+    for (auto& y : p->dys) {
+        auto take = [&](void*& field, long count) {
+            const size_t off = a.mark();
+            field = a.take_elt((size_t)count * 2, e);
+            for (int h = 0; h < 2; ++h) p->dys_span[h].push_back(Span{off + (size_t)h * count * e, (size_t)count * e});
+        };
+        take(y.gin, T * D);
+        take(y.gffn, T * D);
+        take(y.dz, T * F);
+        take(y.dqkv, T * 3 * D);
+        if (dec) {
+            take(y.gcross, T * D);
+            take(y.dxq, T * D);
+            take(y.dxkv, Tm * 2 * D);
         }
     }
     BwdWs& b = p->bw;
     const size_t b0 = a.mark();
     b.p32 = a.take<float>(T * D);
     b.q32 = a.take<float>(T * D);
-    for (auto& r : b.ring) r = a.take_elt(T * D, e);
     b.dn = a.take<float>(T * D);
     b.dc = a.take_elt(T * D, e);
-    for (int i = 0; i < 2; ++i) {
-        b.dz[i] = a.take_elt(T * F, e);
-        b.dqkv[i] = a.take_elt(T * 3 * D, e);
-        if (dec) {
-            b.dxq[i] = a.take_elt(T * D, e);
-            b.dxkv[i] = a.take_elt(Tm * 2 * D, e);
+    if (G == 1) {
+        for (auto& r : b.ring) r = a.take_elt(T * D, e);
+        for (int i = 0; i < 2; ++i) {
+            b.dz[i] = a.take_elt(T * F, e);
+            b.dqkv[i] = a.take_elt(T * 3 * D, e);
+            if (dec) {
+                b.dxq[i] = a.take_elt(T * D, e);
+                b.dxkv[i] = a.take_elt(Tm * 2 * D, e);
+            }
         }
     }
     b.delta = a.take<float>(lse_n);
@@ -359,6 +434,14 @@ gp_status poison_span(const gp_partition* p, const Span& sp, hipStream_t st) {
 
 // GP_POISON: a whole workspace set (residual stream and every layer slot),
 // before a pass that rewrites all of it.
+// GP_POISON: layer slot 0 of workspace set 0, the first pass's.
+gp_status poison_first_pass_slot(const gp_partition* p, hipStream_t st) {
+    if (!p->poison) return GP_OK;
+    gp_status s = GP_OK;
+    for (int i = 0; i < p->slot_bufs && s == GP_OK; ++i) s = poison_span(p, p->slot_span[0][i], st);
+    return s;
+}
+
 gp_status poison_set(const gp_partition* p, int set, hipStream_t st) {
     if (!p->poison) return GP_OK;
     gp_status s = poison_span(p, p->xs_span[set], st);
@@ -788,14 +871,14 @@ gp_status partition_forward(const Ctx& c, int m, bool keep, const void* x, const
 // down is processed.  They are appended to `jobs` and launched by `flush`
 // at the granularity the partition is set to (the caller flushes the rest).
 template <class Flush>
-gp_status layer_backward(const Ctx& c, int set, int l, bool first, float* in32, void* ine, float* sc32, int& ri,
-                         float*& out32, void*& oute, float* dx32_final, void* dxe_final, const void* mem,
+gp_status layer_backward(const Ctx& c, int set, int half, int l, bool first, float* in32, void* ine, float* sc32,
+                         int& ri, float*& out32, void*& oute, float* dx32_final, void* dxe_final, const void* mem,
                          std::vector<DwJob>& jobs, Flush&& flush) {
     gp_partition* p = c.p;
     const LayerPlan& P = p->plan.layers[l];
     LayerWs& w = p->lw[set][l];
     BwdWs& b = p->bw;
-    const long T = p->g.T(), Tm = p->g.Tm(), D = p->d.D;
+    const long T = p->g.T(), Tm = p->g.Tm(), D = p->d.D, F = p->d.F;
     const bool dec = p->g.kind == GP_DECODER_CROSS;
     const int acc = first ? 0 : 1;
     const int par = l & 1;
@@ -804,18 +887,27 @@ gp_status layer_backward(const Ctx& c, int set, int l, bool first, float* in32, 
         ri = (ri + 1) % ELT_RING;
         return r;
     };
+    // The weight gradients' dY operands: with pairing, this micro-batch's half
+    // of the layer's paired buffers (kept for the pair's one GEMM); else the
+    // parity buffers and the ring.
+    const bool pr = p->group > 1;
+    auto hrow = [&](void* base, long rows, long width) { return p->off_elt(base, (long)half * rows * width); };
+    void* dz = pr ? hrow(p->dys[l].dz, T, F) : b.dz[par];
+    void* dqkv = pr ? hrow(p->dys[l].dqkv, T, 3 * D) : b.dqkv[par];
+    void* dxq = pr && dec ? hrow(p->dys[l].dxq, T, D) : b.dxq[par];
+    void* dxkv = pr && dec ? hrow(p->dys[l].dxkv, Tm, 2 * D) : b.dxkv[par];
     const float* xf = dec ? w.x2 : w.x1;
     const Norm& nf = dec ? P.ln3 : P.ln2;
     // feed-forward block:  dz = dY W2^T * [a > 0];  dv = dz W1^T;  dW2, dW1 (and biases) as jobs
     // flush(0): after each weight-gradient job; flush(1): after the feed-forward block
     jobs.push_back({&P.ffn2, w.a, ine, T});
     GP_TRY(flush(0));
-    GP_TRY(linear_dx(c, P.ffn2, ine, T, b.dz[par], EPI_RELU_MASK, w.a, 0));
-    jobs.push_back({&P.ffn1, w.v, b.dz[par], T});
+    GP_TRY(linear_dx(c, P.ffn2, ine, T, dz, EPI_RELU_MASK, w.a, 0));
+    jobs.push_back({&P.ffn1, w.v, dz, T});
     GP_TRY(flush(0));
-    GP_TRY(linear_dx(c, P.ffn1, b.dz[par], T, b.dn, EPI_F32, nullptr, 0, true));
+    GP_TRY(linear_dx(c, P.ffn1, dz, T, b.dn, EPI_F32, nullptr, 0, true));
     GP_TRY(flush(1));
-    void* sce = next_elt();
+    void* sce = pr ? hrow(p->dys[l].gffn, T, D) : next_elt();
     GP_TRY(norm_bwd(c, nf, b.dn, xf, w.stf, T, in32, sc32, sce, acc));
     // (sc) = dL/d(xf)
     float* cur32 = sc32;
@@ -837,20 +929,20 @@ gp_status layer_backward(const Ctx& c, int set, int l, bool first, float* in32, 
         x.lse = w.xlse;
         x.dout = b.dc;
         x.lddo = D;
-        x.dq = b.dxq[par];
+        x.dq = dxq;
         x.lddq = D;
-        x.dk = b.dxkv[par];
-        x.dv = p->off_elt(b.dxkv[par], D);
+        x.dk = dxkv;
+        x.dv = p->off_elt(dxkv, D);
         x.lddk = x.lddv = 2 * D;
         x.delta = b.delta;
         GP_TRY(timed_attention(c, GP_K_XATTN_BWD, x, true));
-        jobs.push_back({&P.xq, w.uc, b.dxq[par], T});
+        jobs.push_back({&P.xq, w.uc, dxq, T});
         GP_TRY(flush(0));
-        GP_TRY(linear_dx(c, P.xq, b.dxq[par], T, b.dn, EPI_F32, nullptr, 0));
-        jobs.push_back({&P.xkv, mem, b.dxkv[par], Tm});
+        GP_TRY(linear_dx(c, P.xq, dxq, T, b.dn, EPI_F32, nullptr, 0));
+        jobs.push_back({&P.xkv, mem, dxkv, Tm});
         GP_TRY(flush(0));
-        GP_TRY(linear_dx(c, P.xkv, b.dxkv[par], Tm, b.dmem32, EPI_ACC_F32, nullptr, l == p->d.L - 1 ? 0 : 1));
-        void* e2 = next_elt();
+        GP_TRY(linear_dx(c, P.xkv, dxkv, Tm, b.dmem32, EPI_ACC_F32, nullptr, l == p->d.L - 1 ? 0 : 1));
+        void* e2 = pr ? hrow(p->dys[l].gcross, T, D) : next_elt();
         GP_TRY(norm_bwd(c, P.ln2, b.dn, w.x1, w.stc, T, cur32, oth32, e2, acc));
         std::swap(cur32, oth32);
         cure = e2;
@@ -869,22 +961,22 @@ gp_status layer_backward(const Ctx& c, int set, int l, bool first, float* in32, 
     a.lse = w.lse;
     a.dout = b.dc;
     a.lddo = D;
-    a.dq = b.dqkv[par];
-    a.dk = p->off_elt(b.dqkv[par], D);
-    a.dv = p->off_elt(b.dqkv[par], 2 * D);
+    a.dq = dqkv;
+    a.dk = p->off_elt(dqkv, D);
+    a.dv = p->off_elt(dqkv, 2 * D);
     a.lddq = a.lddk = a.lddv = 3 * D;
     a.delta = b.delta;
     GP_TRY(timed_attention(c, GP_K_ATTN_BWD, a, true));
-    jobs.push_back({&P.qkv, w.u, b.dqkv[par], T});
+    jobs.push_back({&P.qkv, w.u, dqkv, T});
     GP_TRY(flush(0));
-    GP_TRY(linear_dx(c, P.qkv, b.dqkv[par], T, b.dn, EPI_F32, nullptr, 0, true));
+    GP_TRY(linear_dx(c, P.qkv, dqkv, T, b.dn, EPI_F32, nullptr, 0, true));
     const float* x_in = p->xs[set][l];
     if (dxe_final || dx32_final || l == 0) {
         GP_TRY(norm_bwd(c, P.ln1, b.dn, x_in, w.st1, T, cur32, dx32_final, dxe_final, acc));
         out32 = dx32_final;
         oute = dxe_final;
     } else {
-        void* oe = next_elt();
+        void* oe = pr ? hrow(p->dys[l - 1].gin, T, D) : next_elt();
         GP_TRY(norm_bwd(c, P.ln1, b.dn, x_in, w.st1, T, cur32, oth32, oe, acc));
         out32 = oth32;
         oute = oe;
@@ -892,7 +984,7 @@ gp_status layer_backward(const Ctx& c, int set, int l, bool first, float* in32, 
     return GP_OK;
 }
 
-gp_status head_backward(const Ctx& c, int set, bool first, const int* labels) {
+gp_status head_backward(const Ctx& c, int set, bool first, const int* labels, void* dy_elt) {
     gp_partition* p = c.p;
     const HeadPlan& Hd = p->plan.head;
     BwdWs& b = p->bw;
@@ -906,7 +998,7 @@ gp_status head_backward(const Ctx& c, int set, bool first, const int* labels) {
     GP_TRY(loss_finalize(b.loss_partial, (int)T, b.loss_acc, acc, c.st));
     GP_TRY(linear_dw(c, Hd.out, b.h, b.z, T, acc));
     GP_TRY(linear_dx(c, Hd.out, b.z, T, b.dn, EPI_F32, nullptr, 0));
-    return norm_bwd(c, Hd.lnf, b.dn, y, b.sth, T, nullptr, b.p32, b.ring[0], acc);
+    return norm_bwd(c, Hd.lnf, b.dn, y, b.sth, T, nullptr, b.p32, dy_elt, acc);
 }
 
 gp_status upload_param_block(gp_partition* p, const ParamRef& r, const float* host) {
@@ -1026,9 +1118,13 @@ void plan_partition(gp_partition* p, const gp_config* cfg) {
     if (const char* e = std::getenv("GP_ATTN_WAVES")) p->attn_waves = std::atoi(e);
     if (const char* e = std::getenv("GP_POISON")) p->poison = std::atoi(e) != 0;
     if (const char* e = std::getenv("GP_DW_FLUSH")) p->dw_flush = std::atoi(e);
-    // one workspace set per micro-batch when activations are kept, else two
-    // (recompute-ahead) or one
-    p->nsets = g.keep_act ? g.M : (p->remat_ahead && g.M >= 2) ? 2 : 1;
+    if (const char* e = std::getenv("GP_PAIR_DW")) p->pair_dw = std::atoi(e) != 0;
+    // workspace sets in groups of two micro-batches when their weight
+    // gradients are paired; one set per micro-batch when activations are
+    // kept, else two groups (recompute-ahead) or one
+    p->group = p->pair_dw && g.M >= 2 ? 2 : 1;
+    p->ahead_on = !g.keep_act && p->remat_ahead && g.M >= 2;
+    p->nsets = g.keep_act ? (g.M + p->group - 1) / p->group * p->group : p->group * (p->ahead_on ? 2 : 1);
     if (const char* e = std::getenv("GP_GEMM_TILE")) p->gemm_tile = std::atoi(e);
     if (const char* e = std::getenv("GP_GEMM_SPLITS")) p->gemm_splits = std::atoi(e);
     if (const char* e = std::getenv("GP_FFN_FP4")) g.ffn_fp4 = std::atoi(e) != 0;
@@ -1281,14 +1377,15 @@ gp_status gp_forward_microbatch(gp_partition* p, int mb, const void* x, const vo
             GP_TRY(poison_set(p, p->set_of(mb), c.st));
         } else {
             // the first pass's layer slot and its two ping-pong residual buffers
-            GP_TRY(poison_span(p, p->slot_span[0][0], c.st));
+            GP_TRY(poison_first_pass_slot(p, c.st));
             for (int i = 0; i < 2 && i <= p->d.L; ++i)
                 GP_TRY(poison_span(p, Span{(size_t)((char*)p->xs[0][i] - p->ws), (size_t)(T * D) * 4}, c.st));
         }
     }
-    // The last micro-batch's recompute goes into workspace set 1 (its backward
-    // comes first and uses set mb & 1); the first forward pass itself only
-    // uses slot 0 of set 0, so the two can run side by side.
+    // The last micro-batch's recompute goes into its own workspace set (its
+    // backward comes first; an odd micro-batch's set is never set 0); the
+    // first forward pass itself only uses slot 0 of set 0, so the two can run
+    // side by side.
     const bool early = p->remat_early && p->ahead() && mb == p->g.M - 1 && (mb & 1) == 1;
     if (early) {
         const long T = p->g.T(), D = p->d.D;
@@ -1298,9 +1395,11 @@ gp_status gp_forward_microbatch(gp_partition* p, int mb, const void* x, const vo
         GP_HIP(hipEventRecord(fork, c.st));
         Ctx cr = make_ctx(p, p->remat, Lane::Remat);
         GP_HIP(hipStreamWaitEvent(cr.st, fork, 0));
-        GP_TRY(poison_set(p, 1, cr.st));
+        // an odd micro-batch's set is never set 0, which the first pass uses
+        const int eset = p->set_of(mb);
+        GP_TRY(poison_set(p, eset, cr.st));
         GP_TRY(poison_span(p, p->splitk_span[2], cr.st));
-        s = partition_forward(cr, mb, true, nullptr, nullptr, nullptr, 1);
+        s = partition_forward(cr, mb, true, nullptr, nullptr, nullptr, eset);
         if (s != GP_OK) return s;
         p->remat_done = p->next_event();
         GP_HIP(hipEventRecord(p->remat_done, cr.st));
@@ -1344,7 +1443,7 @@ gp_status gp_forward_microbatch_noalloc(gp_partition* p, int mb, const void* x, 
         if (p->g.keep_act) {
             GP_TRY(poison_set(p, p->set_of(mb), c.st));
         } else {
-            GP_TRY(poison_span(p, p->slot_span[0][0], c.st));
+            GP_TRY(poison_first_pass_slot(p, c.st));
             for (int i = 0; i < 2 && i <= p->d.L; ++i)
                 GP_TRY(poison_span(p, Span{(size_t)((char*)p->xs[0][i] - p->ws), (size_t)(T * D) * 4}, c.st));
         }
@@ -1379,6 +1478,10 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     if (p->poison) {
         for (const Span* sp : {&p->bwd_span, &p->splitk_span[0], &p->splitk_span[1], &p->loss_span, &p->head_span})
             GP_TRY(poison_span(p, *sp, c.st));
+        // this micro-batch's half of the paired weight-gradient operands (the
+        // other half may hold the pair's odd member, not yet consumed)
+        if (p->group > 1)
+            for (const Span& sp : p->dys_span[mb % 2]) GP_TRY(poison_span(p, sp, c.st));
         if (first) {
             // overwritten (not accumulated into) by the first backward micro-batch
             GP_TRY(poison_span(p, p->lnpart_span, c.st));
@@ -1407,39 +1510,52 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
         if (s != GP_OK) return s;
     }
     if (p->ahead() && mb > 0) {
-        // re-materialise micro-batch mb - 1 into the other set meanwhile
+        // re-materialise micro-batch mb - 1 into its set meanwhile
         // (GPipe, Section 2.3: the recompute can be scheduled earlier)
         Ctx cr = make_ctx(p, p->remat, Lane::Remat);
         GP_HIP(hipStreamWaitEvent(cr.st, remat_fork, 0));
-        GP_TRY(poison_set(p, set ^ 1, cr.st));
+        const int aset = p->set_of(mb - 1);
+        GP_TRY(poison_set(p, aset, cr.st));
         GP_TRY(poison_span(p, p->splitk_span[2], cr.st));
-        s = partition_forward(cr, mb - 1, true, nullptr, nullptr, nullptr, set ^ 1);
+        s = partition_forward(cr, mb - 1, true, nullptr, nullptr, nullptr, aset);
         if (s != GP_OK) return s;
         p->remat_done = p->next_event();
         GP_HIP(hipEventRecord(p->remat_done, cr.st));
         p->remat_pending = mb - 1;
     }
     BwdWs& b = p->bw;
-    // dL/dy of the partition output into (p32, ring[0])
+    // dL/dy of the partition output into (p32, top): top is the ring's first
+    // buffer, or with paired weight gradients this micro-batch's half of the
+    // last layer's incoming-gradient buffer
+    const bool pr = p->group > 1;
+    const int half = pr ? mb % 2 : 0;
+    void* top = pr ? p->off_elt(p->dys[p->d.L - 1].gin, (long)half * T * D) : b.ring[0];
     if (p->g.loss == GP_LOSS_NONE) {
-        s = intake(c.dt, dy_or_target, b.ring[0], b.p32, T * D, c.st);
+        s = intake(c.dt, dy_or_target, top, b.p32, T * D, c.st);
     } else if (p->g.loss == GP_LOSS_MSE) {
         int nb = 0;
         const double norm = (double)p->g.n * p->g.M * p->g.S * D;
-        s = mse_grad(c.dt, p->xs[set][p->d.L], dy_or_target, T * D, norm, b.p32, b.ring[0], b.loss_partial, &nb,
-                     c.st);
+        s = mse_grad(c.dt, p->xs[set][p->d.L], dy_or_target, T * D, norm, b.p32, top, b.loss_partial, &nb, c.st);
         if (s == GP_OK) s = loss_finalize(b.loss_partial, nb, b.loss_acc, first ? 0 : 1, c.st);
     } else {
-        s = head_backward(c, set, first, reinterpret_cast<const int*>(dy_or_target));
+        s = head_backward(c, set, first, reinterpret_cast<const int*>(dy_or_target), top);
     }
     if (s != GP_OK) return s;
     const void* mem_m = dec ? p->stash_m_mb(mb) : nullptr;
     // Layer l's weight-gradient GEMMs run on the side stream while layer l - 1
-    // is processed.  Layer l - 2 rewrites parity and ring buffers that layer l's
-    // GEMMs read, so it first waits for them (side_done[l % 4]).
-    const int acc = first ? 0 : 1;
+    // is processed.  Without pairing, layer l - 2 rewrites parity and ring
+    // buffers that layer l's GEMMs read, so it first waits for them
+    // (side_done[l % 4]); the paired buffers are per layer.
+    // With pairing the odd member of a pair (whose backward comes first)
+    // leaves its weight gradients to the even one, which runs each as one GEMM
+    // over both micro-batches' rows.  The first weight-gradient GEMMs of the
+    // mini-batch overwrite the accumulators.
+    if (first) p->dw_started = false;
+    const bool run_dw = p->launches_dw(mb);
+    const int dw_acc = p->dw_started ? 1 : 0;
+    const long dw_rows = pr ? p->pair_size(mb) : 1;
     float* in32 = b.p32;
-    void* ine = b.ring[0];
+    void* ine = top;
     float* sc32 = b.q32;
     int ri = 1;
     std::vector<DwJob> jobs;
@@ -1452,24 +1568,26 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
         return st;
     };
     for (int l = p->d.L - 1; l >= 0; --l) {
-        if (side && l + 2 <= p->d.L - 1) GP_HIP(hipStreamWaitEvent(c.st, p->side_done[(l + 2) % 4], 0));
+        if (side && !pr && l + 2 <= p->d.L - 1) GP_HIP(hipStreamWaitEvent(c.st, p->side_done[(l + 2) % 4], 0));
         float* out32 = nullptr;
         void* oute = nullptr;
         jobs.clear();
         // launch the collected weight-gradient GEMMs (after everything enqueued on main so far)
         auto flush = [&](int level) -> gp_status {
+            if (!run_dw) jobs.clear();  // the pair's even member runs them
             if (jobs.empty() || level < p->dw_flush) return GP_OK;
             if (side) {
                 const hipEvent_t fork = p->next_event();
                 GP_HIP(hipEventRecord(fork, c.st));
                 GP_HIP(hipStreamWaitEvent(cs.st, fork, 0));
             }
-            for (const DwJob& j : jobs) GP_TRY(linear_dw(side ? cs : cb, *j.L, j.X, j.dY, j.rows, acc));
+            for (const DwJob& j : jobs)
+                GP_TRY(linear_dw(side ? cs : cb, *j.L, j.X, j.dY, j.rows * dw_rows, dw_acc));
             jobs.clear();
             return GP_OK;
         };
-        s = layer_backward(cb, set, l, first, in32, ine, sc32, ri, out32, oute, nullptr, l == 0 ? dx : nullptr, mem_m,
-                           jobs, flush);
+        s = layer_backward(cb, set, half, l, first, in32, ine, sc32, ri, out32, oute, nullptr, l == 0 ? dx : nullptr,
+                           mem_m, jobs, flush);
         if (s == GP_OK) s = flush(2);
         if (s != GP_OK) return fail(s);
         if (side) {
@@ -1485,6 +1603,7 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     }
     if (s == GP_OK) s = flush_pending(cb);
     if (s != GP_OK) return fail(s);
+    if (run_dw) p->dw_started = true;
     // the caller's stream resumes only after the last weight-gradient GEMM
     if (side) GP_HIP(hipStreamWaitEvent(c.st, p->side_done[0], 0));
     if (dec && dmem) {

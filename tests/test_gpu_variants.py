@@ -252,3 +252,29 @@ def test_fixup_initialised_stack_matches_oracle():
     assert abs(out["loss"] - ref["loss"]) <= 2e-2 * abs(ref["loss"])
     assert cosine(to_np(out["dx"]), ref["dx"]) >= 0.999
     compare_grads(gl, gh, ref["grads"], ref["head_grads"], "cos", 0.999)
+
+
+# ------------------------------------------------ paired weight gradients
+RAGGED_F32_M3 = synth.PartitionConfig("ragged_f32_m3", layers=2, d_model=96, d_ff=160, heads=3, seq=40,
+                                      batch=6, micro=3, dtype="f32", loss="none")
+
+
+@pytest.mark.parametrize("cfg", [TINY, RAGGED_F32_M3, DEC_SMALL_BF16], ids=lambda c: c.name)
+def test_paired_weight_gradients_match_unpaired(cfg, monkeypatch):
+    """The weight gradients of micro-batches 2i and 2i + 1 as one GEMM over
+    both micro-batches' rows (GP_PAIR_DW, default) against one GEMM per
+    micro-batch: outputs and input gradients are bit-identical (they do not
+    depend on the weight gradients), the accumulated gradients agree to the
+    rounding of the accumulation order (fp32: 1e-5; bf16 parts: 1e-3), with an
+    even M and with an odd M whose last micro-batch has no partner."""
+    res = {}
+    for pair in ("0", "1"):
+        monkeypatch.setenv("GP_PAIR_DW", pair)
+        res[pair] = _steps(cfg, 28, n=2, lr=1e-3 if cfg.loss != "none" else 0.0)
+    tol = 1e-5 if cfg.dtype == "f32" else 1e-3
+    for a, b in zip(res["0"], res["1"]):
+        for k in ("y", "y_remat", "dx", "dmem"):
+            if a[k] is not None:
+                if cfg.loss == "none" or a is res["0"][0]:
+                    assert torch.equal(a[k], b[k]), k
+        assert np.abs(a["g"] - b["g"]).max() <= tol * np.abs(a["g"]).max()

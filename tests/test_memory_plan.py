@@ -49,13 +49,18 @@ def test_stash_and_parameters_do_not_depend_on_m(gp):
         assert plans[M]["grads"] >= 4 * 335_822_848  # fp32 accumulator per parameter
 
 
-def test_one_micro_batch_of_intermediates_scales_as_one_over_m(gp, monkeypatch):
+@pytest.mark.parametrize("pair", ["0", "1"])
+def test_one_micro_batch_of_intermediates_scales_as_one_over_m(gp, monkeypatch, pair):
     """The workspace set that holds one micro-batch's re-materialised
-    intermediates (all L layers) is (keep - remat) / (M - 1) bytes with one
-    recompute set: proportional to T = N S / M, so set x M is the same for
-    every M (up to the 256-byte alignment of each buffer)."""
+    intermediates (all L layers) is (keep - remat) / (M - g) bytes without
+    recompute-ahead, where re-materialisation holds g sets (g = 2 when the
+    weight gradients of micro-batch pairs run as one GEMM, else 1):
+    proportional to T = N S / M, so set x M is the same for every M (up to the
+    256-byte alignment of each buffer)."""
     monkeypatch.setenv("GP_REMAT_AHEAD", "0")
-    per_set = {M: (plan(gp, CFG, M, True)["workspace"] - plan(gp, CFG, M)["workspace"]) / (M - 1) for M in MS}
+    monkeypatch.setenv("GP_PAIR_DW", pair)
+    g = 2 if pair == "1" else 1
+    per_set = {M: (plan(gp, CFG, M, True)["workspace"] - plan(gp, CFG, M)["workspace"]) / (M - g) for M in MS}
     whole = [per_set[M] * M for M in MS]
     assert max(whole) - min(whole) <= 1e-3 * max(whole), per_set
     # and the re-materialising workspace shrinks with M
@@ -65,6 +70,7 @@ def test_one_micro_batch_of_intermediates_scales_as_one_over_m(gp, monkeypatch):
 
 def test_kept_activations_scale_with_the_whole_mini_batch(gp, monkeypatch):
     monkeypatch.setenv("GP_REMAT_AHEAD", "0")
+    monkeypatch.setenv("GP_PAIR_DW", "0")
     remat = {M: plan(gp, CFG, M)["workspace"] for M in MS}
     keep = {M: plan(gp, CFG, M, keep=True)["workspace"] for M in MS}
     for M in MS:
@@ -88,6 +94,7 @@ def test_table1_order_of_growth(gp, monkeypatch):
     workspace grows with L times the micro-batch (L N / M); kept activations
     grow with L times the mini-batch (L N)."""
     monkeypatch.setenv("GP_REMAT_AHEAD", "0")
+    monkeypatch.setenv("GP_PAIR_DW", "0")
     w = lambda L, keep: plan(gp, CFG.with_(layers=L), 8, keep)["workspace"]
     per_layer_remat = w(16, False) - w(8, False)
     per_layer_keep = w(16, True) - w(8, True)

@@ -272,9 +272,10 @@ def test_paired_weight_gradients_match_unpaired(cfg, monkeypatch):
         monkeypatch.setenv("GP_PAIR_DW", pair)
         res[pair] = _steps(cfg, 28, n=2, lr=1e-3 if cfg.loss != "none" else 0.0)
     tol = 1e-5 if cfg.dtype == "f32" else 1e-3
-    for a, b in zip(res["0"], res["1"]):
-        for k in ("y", "y_remat", "dx", "dmem"):
-            if a[k] is not None:
-                if cfg.loss == "none" or a is res["0"][0]:
-                    assert torch.equal(a[k], b[k]), k
-        assert np.abs(a["g"] - b["g"]).max() <= tol * np.abs(a["g"]).max()
+    for step, (a, b) in enumerate(zip(res["0"], res["1"])):
+        # with lr > 0 the second step starts from slightly different parameters
+        if step == 0 or cfg.loss == "none":
+            for k in ("y", "y_remat", "dx", "dmem"):
+                if a[k] is not None:
+                    assert torch.equal(a[k], b[k]), (step, k)
+        assert np.abs(a["g"] - b["g"]).max() <= tol * np.abs(a["g"]).max(), step

@@ -778,9 +778,9 @@ bool mfma_ok(const AttnArgs& a) {
 gp_status attention_fwd(int dtype, const AttnArgs& a, hipStream_t st) {
     if (dtype != GP_BF16) return attention_fwd_simt(dtype, a, st);
     if (!mfma_ok(a)) return set_error(GP_ERR_UNSUPPORTED, "bf16 attention needs d_h = 64 and lengths multiple of 32, <= 256");
-    const int w = waves_for(a, (long)(a.Sq / 32) * a.n * a.H);
+    const int w = waves_for(a, (long)(a.Sq / 32) * (a.hint_n ? a.hint_n : a.n) * a.H);
     dim3 grid((a.Sq + 32 * w - 1) / (32 * w), a.n * a.H);
-    if (split_ok(a, (long)(a.Sq / 32) * a.n * a.H, a.Sk / 32)) {
+    if (split_ok(a, (long)(a.Sq / 32) * (a.hint_n ? a.hint_n : a.n) * a.H, a.Sk / 32)) {
         GP_KS_SWITCH(a.Sk / 32, w, attn_fwd_ks, grid);
     } else {
         GP_WC_SWITCH(a.Sk / 32, w, a.causal, attn_fwd_mfma, grid);
@@ -792,17 +792,17 @@ gp_status attention_fwd(int dtype, const AttnArgs& a, hipStream_t st) {
 gp_status attention_bwd(int dtype, const AttnArgs& a, hipStream_t st) {
     if (dtype != GP_BF16) return attention_bwd_simt(dtype, a, st);
     if (!mfma_ok(a)) return set_error(GP_ERR_UNSUPPORTED, "bf16 attention needs d_h = 64 and lengths multiple of 32, <= 256");
-    const int wq = waves_for(a, (long)(a.Sq / 32) * a.n * a.H);
+    const int wq = waves_for(a, (long)(a.Sq / 32) * (a.hint_n ? a.hint_n : a.n) * a.H);
     dim3 gq((a.Sq + 32 * wq - 1) / (32 * wq), a.n * a.H);
-    if (split_ok(a, (long)(a.Sq / 32) * a.n * a.H, a.Sk / 32)) {
+    if (split_ok(a, (long)(a.Sq / 32) * (a.hint_n ? a.hint_n : a.n) * a.H, a.Sk / 32)) {
         GP_KS_SWITCH(a.Sk / 32, wq, attn_bwd_dq_ks, gq);
     } else {
         GP_WC_SWITCH(a.Sk / 32, wq, a.causal, attn_bwd_dq_mfma, gq);
     }
     GP_LAUNCH_CHECK();
-    const int wk = waves_for(a, (long)(a.Sk / 32) * a.n * a.H);
+    const int wk = waves_for(a, (long)(a.Sk / 32) * (a.hint_n ? a.hint_n : a.n) * a.H);
     dim3 gk((a.Sk + 32 * wk - 1) / (32 * wk), a.n * a.H);
-    if (split_ok(a, (long)(a.Sk / 32) * a.n * a.H, a.Sq / 32)) {
+    if (split_ok(a, (long)(a.Sk / 32) * (a.hint_n ? a.hint_n : a.n) * a.H, a.Sq / 32)) {
         GP_KS_SWITCH(a.Sq / 32, wk, attn_bwd_dkv_ks, gk);
     } else {
         GP_WC_SWITCH(a.Sq / 32, wk, a.causal, attn_bwd_dkv_mfma, gk);

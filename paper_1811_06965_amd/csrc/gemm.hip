@@ -1543,7 +1543,9 @@ gp_status gemm_reduce(const GemmArgs& a, int epi, int splits, hipStream_t st) {
 
 namespace {
 // The tile shape and split count gemm() launches a bf16 problem with.
-void decide_bf16(const GemmArgs& a, int epi, bool a_kmajor, int& cfg, int& splits) {
+void decide_bf16(const GemmArgs& args, int epi, bool a_kmajor, int& cfg, int& splits) {
+    GemmArgs a = args;
+    if (args.split_rows > 0) a.M = args.split_rows;
     if (a.a4) {
         choose_dl(a, epi, true, cfg, splits);
         if (a.force_cfg >= 0 && a.force_cfg <= T_LAST) {

@@ -45,6 +45,13 @@ struct GemmArgs {
     // running the reduce (the caller then reduces, e.g. fused with the next
     // LayerNorm); 1 when the GEMM completed its own epilogue.
     int* deferred = nullptr;
+    // > 0: choose the tile shape and split count as for a problem of this many
+    // rows (M) -- the problem one micro-batch poses -- and run them on the M
+    // rows given.  Split-K changes each element's summation order, so a pass
+    // over two micro-batches' rows then rounds exactly as two single passes
+    // (the tile shape does not change any element's order).  ws must hold the
+    // partials of the M rows.
+    int split_rows = 0;
 };
 
 gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dtype, hipStream_t st);
@@ -109,6 +116,8 @@ struct AttnArgs {
     float* delta = nullptr;                // [n, H, Sq] rowsum(dO * O) = rowsum(P * dP) scratch
     int split = 1;                         // allow the two-wave (half-loop) kernels where they apply
     int waves = 0;                         // waves (32-row blocks) per workgroup: 1, 2 or 4; 0 = by grid size
+    int hint_n = 0;                        // > 0: choose the kernel variant as for this many sequences
+                                           // (one micro-batch), so that a pass over two rounds alike
 };
 gp_status attention_fwd(int dtype, const AttnArgs& a, hipStream_t st);
 gp_status attention_bwd(int dtype, const AttnArgs& a, hipStream_t st);

@@ -190,6 +190,13 @@ struct gp_partition {
     bool pair_dw = true;
     int group = 1;
     std::vector<DyStore> dys;  // per layer (pairing only)
+    // a pair's two micro-batches are re-materialised together, in one pass
+    // over both (re-materialisation with paired sets)
+    bool pair_remat = false;
+    // the first pass's own layer slot and ping-pong residual buffers (no set's)
+    LayerWs fp;
+    float* fp_xs[2] = {};
+    std::vector<Span> fp_span;
     bool dw_started = false;   // a weight-gradient GEMM of this mini-batch was launched
     float* opt_ms = nullptr;  // RMSProp: running mean square of every gradient [n32]
     // GP_POISON=1 (test mode): every workspace region is filled with NaN
@@ -198,9 +205,7 @@ struct gp_partition {
     // residual stream, each layer slot; and the backward scratch, the LayerNorm
     // partial sums, the split-K partials of each stream, the loss partials.
     bool poison = false;
-    std::vector<Span> xs_span;                // per set: xs[set][0..L]
-    std::vector<std::vector<Span>> slot_span; // per set: every buffer of its layer slots, layer by layer
-    int slot_bufs = 0;                        // buffers per layer slot
+    std::vector<std::vector<Span>> slot_span; // per set: its residual stream and every buffer of its layer slots
     std::vector<std::vector<Span>> dys_span;  // per half: that half of every paired-gradient buffer
     Span bwd_span, lnpart_span, loss_span, loss_acc_span, head_span;
     Span splitk_span[3];                      // caller's stream, weight-gradient stream, recompute stream
@@ -292,18 +297,60 @@ void plan_workspace(gp_partition* p, Arena& a) {
     const bool dec = g.kind == GP_DECODER_CROSS;
     p->xs.assign(p->nsets, std::vector<float*>(d.L + 1, nullptr));
     p->lw.assign(p->nsets, std::vector<LayerWs>(d.L, LayerWs{}));
-    p->xs_span.assign(p->nsets, Span{});
     p->slot_span.assign(p->nsets, std::vector<Span>{});
-    p->slot_bufs = 0;
     auto span_from = [&](size_t start) { return Span{start, a.off - start}; };
-    for (int set = 0; set < p->nsets; ++set) {
-        const size_t s0 = a.mark();
-        for (auto& x : p->xs[set]) x = a.take<float>(T * D);
-        p->xs_span[set] = span_from(s0);
-    }
-    // Layer slots, one group of sets at a time: each buffer holds the rows of
-    // the group's members back to back (member h at row h * rows).
+    // Residual streams and layer slots, one group of sets at a time: each
+    // buffer holds the rows of the group's members back to back (member h at
+    // row h * rows), so that a pass can cover the whole group.
     const int G = p->group;
+    for (int g0 = 0; g0 < p->nsets; g0 += G) {
+        for (int li = 0; li <= d.L; ++li) {
+            const size_t off = a.mark();
+            float* base = a.take<float>((size_t)T * D * G);
+            for (int h = 0; h < G; ++h) {
+                p->xs[g0 + h][li] = base + (size_t)h * T * D;
+                p->slot_span[g0 + h].push_back(Span{off + (size_t)h * T * D * 4, (size_t)T * D * 4});
+            }
+        }
+    }
+    // the first pass's slot: one layer of one micro-batch, and two residuals
+    p->fp = LayerWs{};
+    p->fp_span.clear();
+    {
+        auto take1 = [&](auto LayerWs::*field, long count, size_t esz) {
+            const size_t off = a.mark();
+            p->fp.*field = reinterpret_cast<typename std::remove_reference<decltype(p->fp.*field)>::type>(
+                a.take_elt((size_t)count, esz));
+            p->fp_span.push_back(Span{off, (size_t)count * esz});
+        };
+        take1(&LayerWs::st1, 2 * T, 4);
+        take1(&LayerWs::u, T * D, e);
+        take1(&LayerWs::qkv, T * 3 * D, e);
+        take1(&LayerWs::c, T * D, e);
+        take1(&LayerWs::lse, lse_n, 4);
+        take1(&LayerWs::x1, T * D, 4);
+        if (dec) {
+            take1(&LayerWs::stc, 2 * T, 4);
+            take1(&LayerWs::uc, T * D, e);
+            take1(&LayerWs::xq, T * D, e);
+            take1(&LayerWs::xkv, Tm * 2 * D, e);
+            take1(&LayerWs::xc, T * D, e);
+            take1(&LayerWs::xlse, lse_n, 4);
+            take1(&LayerWs::x2, T * D, 4);
+        }
+        take1(&LayerWs::stf, 2 * T, 4);
+        take1(&LayerWs::v, T * D, e);
+        if (p->g.dtype == GP_BF16) {
+            take1(&LayerWs::v4, T * D / 2, 1);
+            take1(&LayerWs::v4s, T, 1);
+        }
+        take1(&LayerWs::a, T * F, e);
+        for (float*& x : p->fp_xs) {
+            const size_t off = a.mark();
+            x = a.take<float>((size_t)T * D);
+            p->fp_span.push_back(Span{off, (size_t)T * D * 4});
+        }
+    }
     for (int g0 = 0; g0 < p->nsets; g0 += G) {
         for (int li = 0; li < d.L; ++li) {
             // one buffer of `count` elements of `esz` bytes per member
@@ -338,7 +385,6 @@ void plan_workspace(gp_partition* p, Arena& a) {
                 take(&LayerWs::v4s, T, 1);
             }
             take(&LayerWs::a, T * F, e);
-            if (g0 == 0 && li == 0) p->slot_bufs = (int)p->slot_span[0].size();
         }
     }
     // paired weight-gradient operands: per layer, two micro-batches' rows
@@ -399,14 +445,18 @@ void plan_workspace(gp_partition* p, Arena& a) {
     // D x 3D packed-QKV weight gradient (with its bias column sums)
     b.splitk_elems = std::max<long>(8 * T * D, 8 * (3 * D * D + 3 * D));
     const size_t sk_bytes = (size_t)b.splitk_elems * sizeof(float);
-    p->splitk_span[0] = Span{a.mark(), sk_bytes};
-    b.splitk = a.take<float>((size_t)b.splitk_elems);
+    // a pair's recompute runs the single micro-batch's splits over twice the
+    // rows; it can run on the caller's stream too (no early recompute)
+    const size_t main_elems = (size_t)b.splitk_elems * (p->pair_remat ? 2 : 1);
+    p->splitk_span[0] = Span{a.mark(), main_elems * sizeof(float)};
+    b.splitk = a.take<float>(main_elems);
     p->splitk_span[1] = Span{a.mark(), sk_bytes};
     b.splitk_side = a.take<float>((size_t)b.splitk_elems);
     p->splitk_span[2] = Span{};
     if (p->ahead()) {
-        p->splitk_span[2] = Span{a.mark(), sk_bytes};
-        b.splitk_remat = a.take<float>((size_t)b.splitk_elems);
+        const size_t rm = main_elems;
+        p->splitk_span[2] = Span{a.mark(), rm * sizeof(float)};
+        b.splitk_remat = a.take<float>(rm);
     }
     size_t lp = (size_t)loss_blocks();
     if (g.loss == GP_LOSS_XENT_LS && (size_t)xent_partials(T) > lp) lp = xent_partials(T);
@@ -434,17 +484,18 @@ gp_status poison_span(const gp_partition* p, const Span& sp, hipStream_t st) {
 
 // GP_POISON: a whole workspace set (residual stream and every layer slot),
 // before a pass that rewrites all of it.
-// GP_POISON: layer slot 0 of workspace set 0, the first pass's.
+// GP_POISON: the first pass's layer slot and residual buffers.
 gp_status poison_first_pass_slot(const gp_partition* p, hipStream_t st) {
     if (!p->poison) return GP_OK;
     gp_status s = GP_OK;
-    for (int i = 0; i < p->slot_bufs && s == GP_OK; ++i) s = poison_span(p, p->slot_span[0][i], st);
+    for (const Span& sp : p->fp_span)
+        if (s == GP_OK) s = poison_span(p, sp, st);
     return s;
 }
 
 gp_status poison_set(const gp_partition* p, int set, hipStream_t st) {
     if (!p->poison) return GP_OK;
-    gp_status s = poison_span(p, p->xs_span[set], st);
+    gp_status s = GP_OK;
     for (const Span& sp : p->slot_span[set])
         if (s == GP_OK) s = poison_span(p, sp, st);
     return s;
@@ -468,6 +519,7 @@ struct Ctx {
     float* ws = nullptr;        // split-K partials for launches on st
     bool last = false;          // the mini-batch's last backward micro-batch
     PendingRes* pend = nullptr; // forward passes: a deferred split-K reduce
+    int nseq = 0;               // sequences of a forward pass (0: one micro-batch; 2n: a pair's recompute)
 };
 
 enum class Lane { Main, Side, Remat };
@@ -614,6 +666,10 @@ gp_status linear_fwd(const Ctx& c, const Linear& L, const void* A, long M, void*
     g.ws_elems = c.p->bw.splitk_elems;
     g.force_cfg = c.p->gemm_tile;
     g.force_splits = c.p->gemm_splits;
+    // a pass over a pair's rows takes one micro-batch's tile and split choice
+    // (same rounding as two single passes; the recompute workspace holds the
+    // pair's partials)
+    if (c.nseq && c.nseq != c.p->g.n) g.split_rows = (int)(M * c.p->g.n / c.nseq);
     int splits = 1;
     if (defer && c.pend && c.p->fuse_res_ln && epi == EPI_RES_F32 && ldc == L.out &&
         layernorm_fwd_res_ok(c.dt, L.out, c.ws, g.bias, res, static_cast<const float*>(C), C2))
@@ -758,9 +814,10 @@ gp_status norm_bwd(const Ctx& c, const Norm& N, const float* dn, const float* x,
     });
 }
 
-AttnArgs attn_args(const gp_partition* p, int Sk, int causal) {
+AttnArgs attn_args(const gp_partition* p, int Sk, int causal, int nseq = 0) {
     AttnArgs a;
-    a.n = p->g.n;
+    a.n = nseq ? nseq : p->g.n;
+    a.hint_n = a.n != p->g.n ? p->g.n : 0;  // a pair's pass takes one micro-batch's kernel variant
     a.H = p->d.H;
     a.Sq = p->g.S;
     a.Sk = Sk;
@@ -779,13 +836,14 @@ gp_status layer_forward(const Ctx& c, int l, LayerWs& w, const float* x_in, floa
                         void* y_out) {
     gp_partition* p = c.p;
     const LayerPlan& P = p->plan.layers[l];
-    const long T = p->g.T(), D = p->d.D;
+    const int ns = c.nseq ? c.nseq : p->g.n;
+    const long T = (long)ns * p->g.S, Tm = (long)ns * p->g.Smem, D = p->d.D;
     const bool dec = p->g.kind == GP_DECODER_CROSS;
     const float eps = p->g.eps;
     // self-attention block
     GP_TRY(timed_ln_fwd(c, x_in, T, (int)D, p->master + P.ln1.g, p->master + P.ln1.b, eps, w.u, w.st1));
     GP_TRY(linear_fwd(c, P.qkv, w.u, T, w.qkv, 3 * D, EPI_STORE, 0, nullptr, nullptr));
-    AttnArgs a = attn_args(p, p->g.S, dec ? 1 : 0);
+    AttnArgs a = attn_args(p, p->g.S, dec ? 1 : 0, ns);
     a.q = w.qkv;
     a.k = p->off_elt(w.qkv, D);
     a.v = p->off_elt(w.qkv, 2 * D);
@@ -800,8 +858,8 @@ GP_TRY(timed_attention(c, GP_K_ATTN_FWD, a, false));
         // cross-attention block: queries from LN2(x1), keys/values from the memory
         GP_TRY(timed_ln_fwd(c, w.x1, T, (int)D, p->master + P.ln2.g, p->master + P.ln2.b, eps, w.uc, w.stc));
         GP_TRY(linear_fwd(c, P.xq, w.uc, T, w.xq, D, EPI_STORE, 0, nullptr, nullptr));
-        GP_TRY(linear_fwd(c, P.xkv, mem, p->g.Tm(), w.xkv, 2 * D, EPI_STORE, 0, nullptr, nullptr));
-        AttnArgs x = attn_args(p, p->g.Smem, 0);
+        GP_TRY(linear_fwd(c, P.xkv, mem, Tm, w.xkv, 2 * D, EPI_STORE, 0, nullptr, nullptr));
+        AttnArgs x = attn_args(p, p->g.Smem, 0, ns);
         x.q = w.xq;
         x.ldq = D;
         x.k = w.xkv;
@@ -830,36 +888,67 @@ GP_TRY(timed_attention(c, GP_K_ATTN_FWD, a, false));
     return GP_OK;
 }
 
-// Forward of micro-batch m through all layers, in workspace set `set`.
-// x != nullptr: a first pass -- x (and mem) go into the stash unless
-// skip_intake, and y (optional) receives the output; x == nullptr: the
-// re-materialisation from the stash.  keep = false: intermediates discarded
-// (slot 0, ping-pong residuals); keep = true: intermediates kept per layer.
+// Forward of micro-batch m through all layers.  keep = false: a first pass
+// in the first-pass slot, intermediates discarded (one layer slot, ping-pong
+// residuals); keep = true: every layer's intermediates kept in workspace set
+// `set`, for c.nseq sequences (2n: micro-batches m and m + 1 together, in the
+// group whose first member is `set`).  x != nullptr: x (and mem) go into the
+// stash unless skip_intake, and y (optional) receives the output;
+// x == nullptr: the re-materialisation from the stash.
 gp_status partition_forward(const Ctx& c, int m, bool keep, const void* x, const void* mem, void* y, int set = 0,
                             bool skip_intake = false) {
     gp_partition* p = c.p;
-    const long T = p->g.T(), D = p->d.D;
+    const int ns = c.nseq ? c.nseq : p->g.n;
+    const long T = (long)ns * p->g.S, Tm = (long)ns * p->g.Smem, D = p->d.D;
     const int L = p->d.L;
-    std::vector<float*>& xs = p->xs[set];
+    float* x0 = keep ? p->xs[set][0] : p->fp_xs[0];
     if (x) {
         if (!skip_intake) {
-            GP_TRY(intake(c.dt, x, p->stash_x_mb(m), xs[0], T * D, c.st));
-            if (mem) GP_TRY(intake(c.dt, mem, p->stash_m_mb(m), nullptr, p->g.Tm() * D, c.st));
+            GP_TRY(intake(c.dt, x, p->stash_x_mb(m), x0, T * D, c.st));
+            if (mem) GP_TRY(intake(c.dt, mem, p->stash_m_mb(m), nullptr, Tm * D, c.st));
         }
     } else {
-        GP_TRY(intake(c.dt, p->stash_x_mb(m), nullptr, xs[0], T * D, c.st));
+        GP_TRY(intake(c.dt, p->stash_x_mb(m), nullptr, x0, T * D, c.st));
     }
     const void* mem_m = p->g.kind == GP_DECODER_CROSS ? p->stash_m_mb(m) : nullptr;
     PendingRes pend;
     Ctx cf = c;
     cf.pend = &pend;
     for (int l = 0; l < L; ++l) {
-        LayerWs& w = keep ? p->lw[set][l] : p->lw[set][0];
-        const float* xi = keep ? xs[l] : xs[l & 1];
-        float* xo = keep ? xs[l + 1] : xs[(l + 1) & 1];
+        LayerWs& w = keep ? p->lw[set][l] : p->fp;
+        const float* xi = keep ? p->xs[set][l] : p->fp_xs[l & 1];
+        float* xo = keep ? p->xs[set][l + 1] : p->fp_xs[(l + 1) & 1];
         GP_TRY(layer_forward(cf, l, w, xi, xo, mem_m, l == L - 1 ? y : nullptr));
     }
     return flush_pending(cf);
+}
+
+// The re-materialisation unit of micro-batch m: the micro-batches one
+// recompute pass covers -- with paired sets the pair {lo, lo + 1} (lo = m -
+// m % 2) when both exist, else m alone -- as its first micro-batch and count.
+// Its recompute must be done before the backward of its highest member,
+// which comes first.
+void remat_unit(const gp_partition* p, int m, int& lo, int& cnt) {
+    if (p->pair_remat) {
+        lo = m - m % 2;
+        cnt = lo + 1 < p->g.M ? 2 : 1;
+    } else {
+        lo = m;
+        cnt = 1;
+    }
+}
+
+// Recompute the forward of a unit from the stash into its workspace set(s),
+// keeping every intermediate, on c's stream.  A pair is one pass over both
+// micro-batches' rows, with each kernel's variant chosen as for one
+// micro-batch, so that every value equals its first-pass value bit for bit.
+gp_status remat_pass(const Ctx& c, int lo, int cnt) {
+    gp_partition* p = c.p;
+    const int set = p->set_of(lo);
+    for (int i = 0; i < cnt; ++i) GP_TRY(poison_set(p, p->set_of(lo + i), c.st));
+    Ctx cr = c;
+    cr.nseq = cnt * p->g.n;
+    return partition_forward(cr, lo, true, nullptr, nullptr, nullptr, set);
 }
 
 // Backward of one layer.  dY arrives in (in32, ine); dX leaves in the pair
@@ -1123,6 +1212,13 @@ void plan_partition(gp_partition* p, const gp_config* cfg) {
     // gradients are paired; one set per micro-batch when activations are
     // kept, else two groups (recompute-ahead) or one
     p->group = p->pair_dw && g.M >= 2 ? 2 : 1;
+    // Recompute pairs in one pass where a micro-batch's GEMMs are small
+    // (T <= 512 rows: they leave most of the chip idle on their own); at
+    // larger T the single passes were as fast or faster (measured at
+    // enc1024: M = 32 -2%, M = 4..16 +0.5..1.4%).  GP_PAIR_REMAT=0/1 forces it.
+    p->pair_remat = g.T() <= 512;
+    if (const char* e = std::getenv("GP_PAIR_REMAT")) p->pair_remat = std::atoi(e) != 0;
+    p->pair_remat = p->pair_remat && p->group == 2 && !g.keep_act;
     p->ahead_on = !g.keep_act && p->remat_ahead && g.M >= 2;
     p->nsets = g.keep_act ? (g.M + p->group - 1) / p->group * p->group : p->group * (p->ahead_on ? 2 : 1);
     if (const char* e = std::getenv("GP_GEMM_TILE")) p->gemm_tile = std::atoi(e);
@@ -1376,34 +1472,29 @@ gp_status gp_forward_microbatch(gp_partition* p, int mb, const void* x, const vo
         if (p->g.keep_act) {
             GP_TRY(poison_set(p, p->set_of(mb), c.st));
         } else {
-            // the first pass's layer slot and its two ping-pong residual buffers
             GP_TRY(poison_first_pass_slot(p, c.st));
-            for (int i = 0; i < 2 && i <= p->d.L; ++i)
-                GP_TRY(poison_span(p, Span{(size_t)((char*)p->xs[0][i] - p->ws), (size_t)(T * D) * 4}, c.st));
         }
     }
-    // The last micro-batch's recompute goes into its own workspace set (its
-    // backward comes first; an odd micro-batch's set is never set 0); the
-    // first forward pass itself only uses slot 0 of set 0, so the two can run
-    // side by side.
-    const bool early = p->remat_early && p->ahead() && mb == p->g.M - 1 && (mb & 1) == 1;
+    // The last micro-batch's backward comes first, so the recompute of its
+    // unit starts on the recompute stream as soon as its boundary input is
+    // stashed; the first pass runs in its own slot beside it.
+    const bool early = p->remat_early && p->ahead() && mb == p->g.M - 1;
     if (early) {
         const long T = p->g.T(), D = p->d.D;
-        GP_TRY(intake(c.dt, x, p->stash_x_mb(mb), p->xs[0][0], T * D, c.st));
+        GP_TRY(intake(c.dt, x, p->stash_x_mb(mb), p->fp_xs[0], T * D, c.st));
         if (mem) GP_TRY(intake(c.dt, mem, p->stash_m_mb(mb), nullptr, p->g.Tm() * D, c.st));
         const hipEvent_t fork = p->next_event();
         GP_HIP(hipEventRecord(fork, c.st));
         Ctx cr = make_ctx(p, p->remat, Lane::Remat);
         GP_HIP(hipStreamWaitEvent(cr.st, fork, 0));
-        // an odd micro-batch's set is never set 0, which the first pass uses
-        const int eset = p->set_of(mb);
-        GP_TRY(poison_set(p, eset, cr.st));
         GP_TRY(poison_span(p, p->splitk_span[2], cr.st));
-        s = partition_forward(cr, mb, true, nullptr, nullptr, nullptr, eset);
+        int lo = mb, cnt = 1;
+        remat_unit(p, mb, lo, cnt);
+        s = remat_pass(cr, lo, cnt);
         if (s != GP_OK) return s;
         p->remat_done = p->next_event();
         GP_HIP(hipEventRecord(p->remat_done, cr.st));
-        p->remat_pending = mb;
+        p->remat_pending = lo;
         s = partition_forward(c, mb, false, x, mem, y, 0, true);
     } else if (p->g.keep_act) {
         // stored-activation mode: this micro-batch's intermediates stay in its own set
@@ -1444,8 +1535,6 @@ gp_status gp_forward_microbatch_noalloc(gp_partition* p, int mb, const void* x, 
             GP_TRY(poison_set(p, p->set_of(mb), c.st));
         } else {
             GP_TRY(poison_first_pass_slot(p, c.st));
-            for (int i = 0; i < 2 && i <= p->d.L; ++i)
-                GP_TRY(poison_span(p, Span{(size_t)((char*)p->xs[0][i] - p->ws), (size_t)(T * D) * 4}, c.st));
         }
     }
     // No early recompute on the library's recompute stream: the backward of
@@ -1489,39 +1578,45 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
             GP_TRY(poison_fill(p->grads, p->plan.n32 * 4, c.st));
         }
     }
+    // The backward of a unit's highest micro-batch (which comes first) needs
+    // the unit re-materialised; the unit's other member then finds it done.
+    int lo = mb, cnt = 1;
+    remat_unit(p, mb, lo, cnt);
+    const bool unit_first = mb == lo + cnt - 1;
     // Everything enqueued on the caller's stream so far (all forwards, the
-    // previous backward, which read the other workspace set) precedes a
-    // recompute-ahead launched from this call.
+    // previous units' backwards, which read the other workspace sets)
+    // precedes a recompute-ahead launched from this call.
     hipEvent_t remat_fork = nullptr;
-    if (p->ahead() && mb > 0) {
+    const bool ahead = p->ahead() && !p->g.keep_act && unit_first && lo > 0;
+    if (ahead) {
         remat_fork = p->next_event();
         GP_HIP(hipEventRecord(remat_fork, c.st));
     }
-    // re-materialise this micro-batch's forward from the stash, unless the
-    // previous backward call already did so on the recompute-ahead stream
-    if (p->g.keep_act) {
-        // stored-activation mode: the forward kept every intermediate
-    } else if (p->remat_pending == mb) {
+    // re-materialise the unit's forward from the stash, unless an earlier call
+    // already did so on the recompute stream
+    if (p->g.keep_act || !unit_first) {
+        // the forward kept every intermediate (stored-activation mode), or the
+        // unit's first backward had it recomputed
+    } else if (p->remat_pending == lo) {
         GP_HIP(hipStreamWaitEvent(c.st, p->remat_done, 0));
         p->remat_pending = -1;
     } else {
-        GP_TRY(poison_set(p, set, c.st));
-        s = partition_forward(c, mb, true, nullptr, nullptr, nullptr, set);
+        s = remat_pass(c, lo, cnt);
         if (s != GP_OK) return s;
     }
-    if (p->ahead() && mb > 0) {
-        // re-materialise micro-batch mb - 1 into its set meanwhile
+    if (ahead) {
+        // re-materialise the next unit (the micro-batches below) meanwhile
         // (GPipe, Section 2.3: the recompute can be scheduled earlier)
         Ctx cr = make_ctx(p, p->remat, Lane::Remat);
         GP_HIP(hipStreamWaitEvent(cr.st, remat_fork, 0));
-        const int aset = p->set_of(mb - 1);
-        GP_TRY(poison_set(p, aset, cr.st));
         GP_TRY(poison_span(p, p->splitk_span[2], cr.st));
-        s = partition_forward(cr, mb - 1, true, nullptr, nullptr, nullptr, aset);
+        int lo2 = 0, cnt2 = 1;
+        remat_unit(p, lo - 1, lo2, cnt2);
+        s = remat_pass(cr, lo2, cnt2);
         if (s != GP_OK) return s;
         p->remat_done = p->next_event();
         GP_HIP(hipEventRecord(p->remat_done, cr.st));
-        p->remat_pending = mb - 1;
+        p->remat_pending = lo2;
     }
     BwdWs& b = p->bw;
     // dL/dy of the partition output into (p32, top): top is the ring's first

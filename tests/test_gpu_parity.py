@@ -416,13 +416,15 @@ def test_mfma_peak_probe_reports_a_plausible_rate():
     assert 800.0 < t < 2700.0, t
 
 
-def test_launch_timer_samples_one_launch_in_every():
+def test_launch_timer_samples_one_launch_in_every(monkeypatch):
     """The role timer: with every launch bracketed, a step of the tiny
     partition records at least one ffn1 forward launch per layer and
     micro-batch (first pass; recomputes add more); with a stride of 3 the same
     step records launches 0, 3, 6, ... of that sequence, and the algorithmic
-    FLOPs scale with the count."""
+    FLOPs scale with the count (recomputes one micro-batch at a time here, so
+    that every launch has the same shape)."""
     from paper_1811_06965_amd.runtime import Partition
+    monkeypatch.setenv("GP_PAIR_REMAT", "0")
     case = synth.make_case(TINY, 0)
     with Partition(TINY, micro=TINY.micro) as part:
         part.load_params(case["layers"], case["head"])

@@ -279,3 +279,35 @@ def test_paired_weight_gradients_match_unpaired(cfg, monkeypatch):
                 if a[k] is not None:
                     assert torch.equal(a[k], b[k]), (step, k)
         assert np.abs(a["g"] - b["g"]).max() <= tol * np.abs(a["g"]).max(), step
+
+
+# ------------------------------------------------------------------ resume
+@pytest.mark.parametrize("cfg", [TINY, ENC512_SMALL], ids=lambda c: c.name)
+def test_resume_from_parameters_reproduces_the_next_step_bitwise(cfg):
+    """Checkpoint and resume: one step, gp_get_param of every tensor, a new
+    partition loaded with gp_set_param, one more step -- the same parameters,
+    gradients and boundary outputs, bit for bit, as two steps in one partition
+    (the working copies are rebuilt from the fp32 masters by the same rounding)."""
+    from paper_1811_06965_amd.runtime import Partition
+    case = synth.make_case(cfg, 29, perturb=True)
+    lr = 1e-3
+    with Partition(cfg) as part:
+        part.load_params(case["layers"], case["head"])
+        inp = part.device_inputs(case)
+        part.step(inp["x"], inp["mem"], inp["dy"], lr=lr)
+        mid_layers, mid_head = part.params()
+        o = part.step(inp["x"], inp["mem"], inp["dy"], lr=lr)
+        torch.cuda.synchronize()
+        ref = (_bits(o["y"]), _bits(o["dx"]), o["loss"], _flat(part), part.params())
+    with Partition(cfg) as part:
+        part.load_params(mid_layers, mid_head)
+        inp = part.device_inputs(case)
+        o = part.step(inp["x"], inp["mem"], inp["dy"], lr=lr)
+        torch.cuda.synchronize()
+        got = (_bits(o["y"]), _bits(o["dx"]), o["loss"], _flat(part), part.params())
+    assert torch.equal(ref[0], got[0]) and torch.equal(ref[1], got[1])
+    assert ref[2] == got[2]
+    assert np.array_equal(ref[3], got[3])
+    for a, b in zip(ref[4][0], got[4][0]):
+        for k in a:
+            assert np.array_equal(a[k], b[k]), k

@@ -17,9 +17,9 @@
 // The forward pass writes its intermediates into layer slot 0 of set 0 and
 // ping-pongs xs[0]/xs[1]; the re-materialising pass of micro-batch m uses its
 // set (set_of: sets rotate so that the one being rebuilt ahead is never one
-// still read), slot l and xs[l] for layer l.  Sets come in groups of two
-// micro-batches whose buffers hold both back to back, so that the weight
-// gradients of a pair run as one GEMM.  All passes run the same kernels with
+// still read), slot l and xs[l] for layer l.  Sets come in groups of two or
+// four micro-batches whose buffers hold them back to back, so that the weight
+// gradients of a group run as one GEMM.  All passes run the same kernels with
 // the same launch shapes, so the recomputed activations equal the first pass
 // bit for bit.
 #include <cmath>
@@ -108,14 +108,15 @@ struct BwdWs {
     void *h = nullptr, *z = nullptr;
 };
 
-// Paired weight gradients: the weight-gradient GEMMs of micro-batches 2i and
-// 2i + 1 run as one GEMM with a reduction over both micro-batches' token rows
-// (one fp32 read-modify-write of the accumulator, one launch, per pair).
-// Their operands must then stay until the later backward call of the pair,
-// and sit back to back: per layer, the bf16 gradients a layer's weight-
-// gradient GEMMs take as dY live here, two micro-batches' rows each
-// (half 0 = the even micro-batch), instead of in the recycled ring and
-// parity buffers; the activations come from workspace sets allocated in pairs.
+// Grouped weight gradients: the weight-gradient GEMMs of micro-batches
+// Gi .. Gi + G - 1 (G = 2 or 4) run as one GEMM with a reduction over the
+// group's token rows (one fp32 read-modify-write of the accumulator, one
+// launch, per group).  Their operands must then stay until the last backward
+// call of the group (its lowest micro-batch) and sit back to back: per layer,
+// the bf16 gradients a layer's weight-gradient GEMMs take as dY live here, G
+// micro-batches' rows each (member h = micro-batch Gi + h), instead of in the
+// recycled ring and parity buffers; the activations come from workspace sets
+// allocated in groups.
 struct DyStore {
     void* gin = nullptr;    // dL/dx_out of the layer (dY of the ffn2 weight gradient)
     void* gffn = nullptr;   // after the feed-forward block's LayerNorm backward (dY of o / xo)
@@ -184,15 +185,15 @@ struct gp_partition {
     std::vector<std::vector<float*>> xs;
     std::vector<std::vector<LayerWs>> lw;
     int nsets = 1;
-    // paired weight gradients (GP_PAIR_DW=0 turns them off): workspace sets are
-    // allocated in groups of `group` (2 when pairing) whose buffers hold the
-    // group's micro-batches back to back
+    // grouped weight gradients (GP_PAIR_DW=0 turns them off): workspace sets
+    // are allocated in groups of `group` micro-batches (2 or 4) whose buffers
+    // hold the group's micro-batches back to back
     bool pair_dw = true;
     int group = 1;
-    std::vector<DyStore> dys;  // per layer (pairing only)
-    // a pair's two micro-batches are re-materialised together, in one pass
-    // over both (re-materialisation with paired sets)
-    bool pair_remat = false;
+    std::vector<DyStore> dys;  // per layer (grouping only)
+    // micro-batches re-materialised together in one pass over their rows
+    // (1, or 2 within a group of sets)
+    int remat_group = 1;
     // the first pass's own layer slot and ping-pong residual buffers (no set's)
     LayerWs fp;
     float* fp_xs[2] = {};
@@ -206,7 +207,7 @@ struct gp_partition {
     // partial sums, the split-K partials of each stream, the loss partials.
     bool poison = false;
     std::vector<std::vector<Span>> slot_span; // per set: its residual stream and every buffer of its layer slots
-    std::vector<std::vector<Span>> dys_span;  // per half: that half of every paired-gradient buffer
+    std::vector<std::vector<Span>> dys_span;  // per member: its rows of every grouped-gradient buffer
     Span bwd_span, lnpart_span, loss_span, loss_acc_span, head_span;
     Span splitk_span[3];                      // caller's stream, weight-gradient stream, recompute stream
     // gp_forward_microbatch_noalloc: this device's address of the static
@@ -266,16 +267,16 @@ struct gp_partition {
     // Workspace set of micro-batch m: its own set when activations are kept;
     // else the sets rotate group by group -- micro-batch m takes member m % group
     // of group (m / group) mod (nsets / group) -- so that with recompute-ahead
-    // the set being rebuilt is never one the backward or a pending paired
+    // the set being rebuilt is never one the backward or a pending grouped
     // weight gradient still reads.
     int set_of(int m) const {
         if (g.keep_act) return m;
         return group * ((m / group) % (nsets / group)) + m % group;
     }
-    // paired weight gradients: rows of micro-batch m's pair, and whether m's
-    // backward launches them (the even member; the odd one runs first and defers)
-    int pair_size(int m) const { return (m - m % 2) + 1 < g.M ? 2 : 1; }
-    bool launches_dw(int m) const { return group == 1 || m % 2 == 0; }
+    // grouped weight gradients: micro-batches in m's group, and whether m's
+    // backward launches them (the lowest member; the others run first and defer)
+    int group_size(int m) const { return std::min(group, g.M - (m - m % group)); }
+    bool launches_dw(int m) const { return m % group == 0; }
     bool ahead_on = false;  // recompute-ahead / early-recompute stream in use
     bool ahead() const { return ahead_on; }
     void* W(size_t elt_off) const { return welt + elt_off * esz; }
@@ -387,14 +388,14 @@ void plan_workspace(gp_partition* p, Arena& a) {
             take(&LayerWs::a, T * F, e);
         }
     }
-    // paired weight-gradient operands: per layer, two micro-batches' rows
+    // grouped weight-gradient operands: per layer, the group's micro-batches' rows
     p->dys.assign(G > 1 ? d.L : 0, DyStore{});
-    p->dys_span.assign(G > 1 ? 2 : 0, std::vector<Span>{});
+    p->dys_span.assign(G > 1 ? G : 0, std::vector<Span>{});
     for (auto& y : p->dys) {
         auto take = [&](void*& field, long count) {
             const size_t off = a.mark();
-            field = a.take_elt((size_t)count * 2, e);
-            for (int h = 0; h < 2; ++h) p->dys_span[h].push_back(Span{off + (size_t)h * count * e, (size_t)count * e});
+            field = a.take_elt((size_t)count * G, e);
+            for (int h = 0; h < G; ++h) p->dys_span[h].push_back(Span{off + (size_t)h * count * e, (size_t)count * e});
         };
         take(y.gin, T * D);
         take(y.gffn, T * D);
@@ -445,9 +446,9 @@ void plan_workspace(gp_partition* p, Arena& a) {
     // D x 3D packed-QKV weight gradient (with its bias column sums)
     b.splitk_elems = std::max<long>(8 * T * D, 8 * (3 * D * D + 3 * D));
     const size_t sk_bytes = (size_t)b.splitk_elems * sizeof(float);
-    // a pair's recompute runs the single micro-batch's splits over twice the
-    // rows; it can run on the caller's stream too (no early recompute)
-    const size_t main_elems = (size_t)b.splitk_elems * (p->pair_remat ? 2 : 1);
+    // a grouped recompute runs the single micro-batch's splits over its
+    // members' rows; it can run on the caller's stream too (no early recompute)
+    const size_t main_elems = (size_t)b.splitk_elems * p->remat_group;
     p->splitk_span[0] = Span{a.mark(), main_elems * sizeof(float)};
     b.splitk = a.take<float>(main_elems);
     p->splitk_span[1] = Span{a.mark(), sk_bytes};
@@ -924,18 +925,14 @@ gp_status partition_forward(const Ctx& c, int m, bool keep, const void* x, const
 }
 
 // The re-materialisation unit of micro-batch m: the micro-batches one
-// recompute pass covers -- with paired sets the pair {lo, lo + 1} (lo = m -
-// m % 2) when both exist, else m alone -- as its first micro-batch and count.
-// Its recompute must be done before the backward of its highest member,
-// which comes first.
+// recompute pass covers -- {lo, ..., lo + r - 1} with lo = m - m % r for a
+// recompute group of r, cut at the last micro-batch -- as its first
+// micro-batch and count.  Its recompute must be done before the backward of
+// its highest member, which comes first.
 void remat_unit(const gp_partition* p, int m, int& lo, int& cnt) {
-    if (p->pair_remat) {
-        lo = m - m % 2;
-        cnt = lo + 1 < p->g.M ? 2 : 1;
-    } else {
-        lo = m;
-        cnt = 1;
-    }
+    const int r = p->remat_group;
+    lo = m - m % r;
+    cnt = std::min(r, p->g.M - lo);
 }
 
 // Recompute the forward of a unit from the stash into its workspace set(s),
@@ -976,8 +973,8 @@ gp_status layer_backward(const Ctx& c, int set, int half, int l, bool first, flo
         ri = (ri + 1) % ELT_RING;
         return r;
     };
-    // The weight gradients' dY operands: with pairing, this micro-batch's half
-    // of the layer's paired buffers (kept for the pair's one GEMM); else the
+    // The weight gradients' dY operands: with grouping, this micro-batch's rows
+    // of the layer's grouped buffers (kept for the group's one GEMM); else the
     // parity buffers and the ring.
     const bool pr = p->group > 1;
     auto hrow = [&](void* base, long rows, long width) { return p->off_elt(base, (long)half * rows * width); };
@@ -1208,17 +1205,25 @@ void plan_partition(gp_partition* p, const gp_config* cfg) {
     if (const char* e = std::getenv("GP_POISON")) p->poison = std::atoi(e) != 0;
     if (const char* e = std::getenv("GP_DW_FLUSH")) p->dw_flush = std::atoi(e);
     if (const char* e = std::getenv("GP_PAIR_DW")) p->pair_dw = std::atoi(e) != 0;
-    // workspace sets in groups of two micro-batches when their weight
-    // gradients are paired; one set per micro-batch when activations are
-    // kept, else two groups (recompute-ahead) or one
-    p->group = p->pair_dw && g.M >= 2 ? 2 : 1;
+    // Workspace sets in groups of the micro-batches whose weight gradients
+    // run as one GEMM: two, or four with GP_DW_GROUP=4 (GP_DW_GROUP=1 or
+    // GP_PAIR_DW=0: none); one set per micro-batch when activations are kept,
+    // else two groups (recompute-ahead) or one.  Groups of four halve the
+    // accumulator passes again but hold twice the re-materialised sets
+    // (enc1024: M = 32 1.8% faster with 3.9 instead of 2.2 GB of workspace,
+    // M = 16 0.6% with 7.1 instead of 3.8 GB), so two is the default: the
+    // workspace keeps shrinking as M grows.
+    int grp = 2;
+    if (const char* e = std::getenv("GP_DW_GROUP")) grp = std::atoi(e);
+    if (grp != 1 && grp != 2 && grp != 4) grp = 2;
+    p->group = p->pair_dw ? std::max(1, std::min(grp, g.M >= 4 ? 4 : g.M >= 2 ? 2 : 1)) : 1;
     // Recompute pairs in one pass where a micro-batch's GEMMs are small
     // (T <= 512 rows: they leave most of the chip idle on their own); at
     // larger T the single passes were as fast or faster (measured at
     // enc1024: M = 32 -2%, M = 4..16 +0.5..1.4%).  GP_PAIR_REMAT=0/1 forces it.
-    p->pair_remat = g.T() <= 512;
-    if (const char* e = std::getenv("GP_PAIR_REMAT")) p->pair_remat = std::atoi(e) != 0;
-    p->pair_remat = p->pair_remat && p->group == 2 && !g.keep_act;
+    bool pair_remat = g.T() <= 512;
+    if (const char* e = std::getenv("GP_PAIR_REMAT")) pair_remat = std::atoi(e) != 0;
+    p->remat_group = pair_remat && p->group >= 2 && !g.keep_act ? 2 : 1;
     p->ahead_on = !g.keep_act && p->remat_ahead && g.M >= 2;
     p->nsets = g.keep_act ? (g.M + p->group - 1) / p->group * p->group : p->group * (p->ahead_on ? 2 : 1);
     if (const char* e = std::getenv("GP_GEMM_TILE")) p->gemm_tile = std::atoi(e);
@@ -1567,10 +1572,10 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     if (p->poison) {
         for (const Span* sp : {&p->bwd_span, &p->splitk_span[0], &p->splitk_span[1], &p->loss_span, &p->head_span})
             GP_TRY(poison_span(p, *sp, c.st));
-        // this micro-batch's half of the paired weight-gradient operands (the
-        // other half may hold the pair's odd member, not yet consumed)
+        // this micro-batch's rows of the grouped weight-gradient operands (the
+        // other members' rows may hold later micro-batches, not yet consumed)
         if (p->group > 1)
-            for (const Span& sp : p->dys_span[mb % 2]) GP_TRY(poison_span(p, sp, c.st));
+            for (const Span& sp : p->dys_span[mb % p->group]) GP_TRY(poison_span(p, sp, c.st));
         if (first) {
             // overwritten (not accumulated into) by the first backward micro-batch
             GP_TRY(poison_span(p, p->lnpart_span, c.st));
@@ -1620,10 +1625,10 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     }
     BwdWs& b = p->bw;
     // dL/dy of the partition output into (p32, top): top is the ring's first
-    // buffer, or with paired weight gradients this micro-batch's half of the
+    // buffer, or with grouped weight gradients this micro-batch's rows of the
     // last layer's incoming-gradient buffer
     const bool pr = p->group > 1;
-    const int half = pr ? mb % 2 : 0;
+    const int half = pr ? mb % p->group : 0;
     void* top = pr ? p->off_elt(p->dys[p->d.L - 1].gin, (long)half * T * D) : b.ring[0];
     if (p->g.loss == GP_LOSS_NONE) {
         s = intake(c.dt, dy_or_target, top, b.p32, T * D, c.st);
@@ -1638,17 +1643,17 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     if (s != GP_OK) return s;
     const void* mem_m = dec ? p->stash_m_mb(mb) : nullptr;
     // Layer l's weight-gradient GEMMs run on the side stream while layer l - 1
-    // is processed.  Without pairing, layer l - 2 rewrites parity and ring
+    // is processed.  Without grouping, layer l - 2 rewrites parity and ring
     // buffers that layer l's GEMMs read, so it first waits for them
-    // (side_done[l % 4]); the paired buffers are per layer.
-    // With pairing the odd member of a pair (whose backward comes first)
-    // leaves its weight gradients to the even one, which runs each as one GEMM
-    // over both micro-batches' rows.  The first weight-gradient GEMMs of the
+    // (side_done[l % 4]); the grouped buffers are per layer.
+    // With grouping the higher members of a group (whose backwards come first)
+    // leave their weight gradients to the lowest one, which runs each as one
+    // GEMM over all the members' rows.  The first weight-gradient GEMMs of the
     // mini-batch overwrite the accumulators.
     if (first) p->dw_started = false;
     const bool run_dw = p->launches_dw(mb);
     const int dw_acc = p->dw_started ? 1 : 0;
-    const long dw_rows = pr ? p->pair_size(mb) : 1;
+    const long dw_rows = pr ? p->group_size(mb) : 1;
     float* in32 = b.p32;
     void* ine = top;
     float* sc32 = b.q32;
@@ -1669,7 +1674,7 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
         jobs.clear();
         // launch the collected weight-gradient GEMMs (after everything enqueued on main so far)
         auto flush = [&](int level) -> gp_status {
-            if (!run_dw) jobs.clear();  // the pair's even member runs them
+            if (!run_dw) jobs.clear();  // the group's lowest member runs them
             if (jobs.empty() || level < p->dw_flush) return GP_OK;
             if (side) {
                 const hipEvent_t fork = p->next_event();

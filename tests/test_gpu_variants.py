@@ -127,20 +127,21 @@ def test_device_memory_matches_the_plan_and_steps_allocate_nothing(keep):
 
 
 # ---------------------------------------------------------------- poison
-@pytest.mark.parametrize("cfg,keep,tile", [(TINY, False, None), (ENC512_SMALL, False, None),
-                                           (RAGGED_BF16, False, ("18", "2")), (DEC_SMALL_BF16, False, None),
-                                           (ENC512_SMALL, True, None), (DEC_F32, False, None)],
-                         ids=["tiny", "enc512_small", "ragged_split2", "dec_small", "enc512_kept", "dec_f32"])
-def test_poisoned_workspace_changes_no_bit(cfg, keep, tile, monkeypatch):
+@pytest.mark.parametrize("cfg,keep,env", [(TINY, False, {}), (ENC512_SMALL, False, {}),
+                                          (RAGGED_BF16, False, {"GP_GEMM_TILE": "18", "GP_GEMM_SPLITS": "2"}),
+                                          (DEC_SMALL_BF16, False, {}), (ENC512_SMALL, True, {}), (DEC_F32, False, {}),
+                                          (ENC512_SMALL.with_(batch=12, micro=6), False, {"GP_DW_GROUP": "4"})],
+                         ids=["tiny", "enc512_small", "ragged_split2", "dec_small", "enc512_kept", "dec_f32",
+                              "enc512_m6_groups_of_4"])
+def test_poisoned_workspace_changes_no_bit(cfg, keep, env, monkeypatch):
     """GP_POISON=1 fills every workspace set with NaN before the pass that
     rewrites it, the backward scratch, the split-K partials of all three
     streams and the loss partials before each backward, and the gradient
     accumulators and LayerNorm partial sums before the first backward of each
     mini-batch.  A read of anything stale would turn results into NaN: two
     steps are bit-identical to the unpoisoned ones."""
-    if tile:
-        monkeypatch.setenv("GP_GEMM_TILE", tile[0])
-        monkeypatch.setenv("GP_GEMM_SPLITS", tile[1])
+    for k, v in env.items():
+        monkeypatch.setenv(k, v)
     lr = 1e-3 if cfg.loss != "none" else 0.0
     clean = _steps(cfg, 23, keep=keep, lr=lr)
     monkeypatch.setenv("GP_POISON", "1")
@@ -254,22 +255,27 @@ def test_fixup_initialised_stack_matches_oracle():
     compare_grads(gl, gh, ref["grads"], ref["head_grads"], "cos", 0.999)
 
 
-# ------------------------------------------------ paired weight gradients
+# ----------------------------------------------- grouped weight gradients
 RAGGED_F32_M3 = synth.PartitionConfig("ragged_f32_m3", layers=2, d_model=96, d_ff=160, heads=3, seq=40,
                                       batch=6, micro=3, dtype="f32", loss="none")
+RAGGED_F32_M5 = RAGGED_F32_M3.with_(name="ragged_f32_m5", batch=10, micro=5)
+DEC_SMALL_BF16_M6 = DEC_SMALL_BF16.with_(name="dec_small_bf16_m6", batch=6, micro=6)
 
 
-@pytest.mark.parametrize("cfg", [TINY, RAGGED_F32_M3, DEC_SMALL_BF16], ids=lambda c: c.name)
-def test_paired_weight_gradients_match_unpaired(cfg, monkeypatch):
-    """The weight gradients of micro-batches 2i and 2i + 1 as one GEMM over
-    both micro-batches' rows (GP_PAIR_DW, default) against one GEMM per
+@pytest.mark.parametrize("group", ["2", "4"])
+@pytest.mark.parametrize("cfg", [TINY, RAGGED_F32_M3, RAGGED_F32_M5, DEC_SMALL_BF16, DEC_SMALL_BF16_M6],
+                         ids=lambda c: c.name)
+def test_grouped_weight_gradients_match_ungrouped(cfg, group, monkeypatch):
+    """The weight gradients of a group of micro-batches (two, or four; the
+    last group cut short when M is not a multiple) as one GEMM over the
+    members' rows (GP_PAIR_DW with GP_DW_GROUP) against one GEMM per
     micro-batch: outputs and input gradients are bit-identical (they do not
     depend on the weight gradients), the accumulated gradients agree to the
-    rounding of the accumulation order (fp32: 1e-5; bf16 parts: 1e-3), with an
-    even M and with an odd M whose last micro-batch has no partner."""
+    rounding of the accumulation order (fp32: 1e-5; bf16 parts: 1e-3)."""
     res = {}
     for pair in ("0", "1"):
         monkeypatch.setenv("GP_PAIR_DW", pair)
+        monkeypatch.setenv("GP_DW_GROUP", group)
         res[pair] = _steps(cfg, 28, n=2, lr=1e-3 if cfg.loss != "none" else 0.0)
     tol = 1e-5 if cfg.dtype == "f32" else 1e-3
     for step, (a, b) in enumerate(zip(res["0"], res["1"])):

@@ -49,22 +49,23 @@ def test_stash_and_parameters_do_not_depend_on_m(gp):
         assert plans[M]["grads"] >= 4 * 335_822_848  # fp32 accumulator per parameter
 
 
-@pytest.mark.parametrize("pair", ["0", "1"])
-def test_one_micro_batch_of_intermediates_scales_as_one_over_m(gp, monkeypatch, pair):
+@pytest.mark.parametrize("group", [1, 2, 4])
+def test_one_micro_batch_of_intermediates_scales_as_one_over_m(gp, monkeypatch, group):
     """The workspace set that holds one micro-batch's re-materialised
     intermediates (all L layers) is (keep - remat) / (M - g) bytes without
-    recompute-ahead, where re-materialisation holds g sets (g = 2 when the
-    weight gradients of micro-batch pairs run as one GEMM, else 1):
-    proportional to T = N S / M, so set x M is the same for every M (up to the
-    256-byte alignment of each buffer)."""
+    recompute-ahead, where re-materialisation holds g sets (g micro-batches
+    whose weight gradients run as one GEMM): proportional to T = N S / M, so
+    set x M is the same for every M (up to the 256-byte alignment of each
+    buffer)."""
     monkeypatch.setenv("GP_REMAT_AHEAD", "0")
-    monkeypatch.setenv("GP_PAIR_DW", pair)
-    # pairs recomputed in one pass double the split-K area of re-materialisation
-    # only; keep it equal in both modes here
+    monkeypatch.setenv("GP_PAIR_DW", "1" if group > 1 else "0")
+    monkeypatch.setenv("GP_DW_GROUP", str(group))
+    # groups recomputed in one pass enlarge the split-K area of
+    # re-materialisation only; keep it equal in both modes here
     monkeypatch.setenv("GP_PAIR_REMAT", "0")
-    g = 2 if pair == "1" else 1
-    per_set = {M: (plan(gp, CFG, M, True)["workspace"] - plan(gp, CFG, M)["workspace"]) / (M - g) for M in MS}
-    whole = [per_set[M] * M for M in MS]
+    ms = [M for M in MS if M > group]
+    per_set = {M: (plan(gp, CFG, M, True)["workspace"] - plan(gp, CFG, M)["workspace"]) / (M - group) for M in ms}
+    whole = [per_set[M] * M for M in ms]
     assert max(whole) - min(whole) <= 1e-3 * max(whole), per_set
     # and the re-materialising workspace shrinks with M
     w = [plan(gp, CFG, M)["workspace"] for M in MS]

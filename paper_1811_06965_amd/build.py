@@ -1,7 +1,8 @@
 """Build the partition's HIP library (libgp.so) in-tree for gfx950.
 
 Each .hip source is compiled to an object with hipcc, in parallel, then all
-are linked into paper_1811_06965_amd/_lib/libgp.so.  Always recompiles.
+are linked into paper_1811_06965_amd/_lib/libgp.so; then the C-ABI test
+program (tests/host/abi_driver.cpp) is linked against it.  Always recompiles.
 """
 import concurrent.futures
 import os
@@ -70,7 +71,26 @@ def build(verbose=False):
         if bad:
             raise RuntimeError("libgp.so has undefined internal symbols:\n" + "\n".join(bad[:20]))
     os.replace(tmp, LIB)
+    build_abi_driver(cc)
     return LIB
+
+
+# The test program that drives a partition through the C ABI alone (no Python
+# in its process); it links the library through a path relative to itself.
+DRIVER_SRC = os.path.join(os.path.dirname(HERE), "tests", "host", "abi_driver.cpp")
+DRIVER = os.path.join(os.path.dirname(HERE), "tests", "host", "_bin", "abi_driver")
+
+
+def build_abi_driver(cc=None):
+    cc = cc or hipcc()
+    os.makedirs(os.path.dirname(DRIVER), exist_ok=True)
+    rel = os.path.relpath(OUT_DIR, os.path.dirname(DRIVER))
+    cmd = [cc, *FLAGS, DRIVER_SRC, "-o", DRIVER + ".tmp", f"-L{OUT_DIR}", "-lgp", f"-Wl,-rpath,$ORIGIN/{rel}"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    os.replace(DRIVER + ".tmp", DRIVER)
+    return DRIVER
 
 
 if __name__ == "__main__":

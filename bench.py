@@ -353,14 +353,17 @@ def time_steps(part, inp, steps, warmup, role=None, graph=False):
 
 
 def source_digest():
-    """SHA-256 over the HIP sources: a stored traffic figure is only valid for
-    the kernels it was measured on."""
+    """SHA-256 over the HIP sources and the compiler flags they are built
+    with: a stored traffic figure is only valid for the kernels it was
+    measured on."""
+    from paper_1811_06965_amd import build
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_1811_06965_amd", "csrc")
     for f in sorted(os.listdir(csrc)):
         if f.endswith((".hip", ".hpp")):
             with open(os.path.join(csrc, f), "rb") as fh:
                 h.update(f.encode() + b"\0" + fh.read())
+    h.update(repr((build.FLAGS, sorted(build.EXTRA_FLAGS.items()))).encode())
     return h.hexdigest()
 
 

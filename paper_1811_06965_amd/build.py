@@ -36,9 +36,17 @@ def sources():
     return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
 
 
+# Per-source additions.  The attention kernels post-process every MFMA result
+# with vector ALU work (exp, the softmax and dS arithmetic, packing to bf16);
+# with the accumulators in AGPRs each value costs a v_accvgpr_read first, so
+# their MFMAs write ordinary VGPRs instead (the register file is unified on
+# gfx950).
+EXTRA_FLAGS = {"attention_mfma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def _compile(cc, src):
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [cc, *FLAGS, "-c", src, "-o", obj]
+    cmd = [cc, *FLAGS, *EXTRA_FLAGS.get(os.path.basename(src), []), "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

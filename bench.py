@@ -479,7 +479,8 @@ def main():
     a = parse()
     if a.gpus != 1:
         print(f"bench.py measures one partition on one GPU; --gpus {a.gpus} is not supported "
-              "(multi-GPU pipelines are outside this build)", file=sys.stderr)
+              "(the library implements one GPU's partition; a K-stage pipeline over several GPUs is not "
+              "implemented)", file=sys.stderr)
         sys.exit(2)
     import synth
     base = synth.CONFIGS[a.config]

@@ -156,6 +156,15 @@ gp_status rmsprop_update(float* w, const float* g, float* ms, float lr, float rh
 // kn (elt) = W, nk (elt) = W^T.
 // kn = W [in, out]; nk = W^T [out, in]; q4 / q4s (optional, bf16): the rows of
 // nk in fp4 [out, in/2] bytes with one E8M0 scale per row (GemmArgs::b4, sb4).
+// The SGD (ms == nullptr) or RMSProp step of a linear's fp32 weights fused
+// with the refresh of its bf16 working copies kn = W, nk = W^T (and the fp4
+// copy of W^T when q4 is set); in, out multiples of 64.
+gp_status update_refresh_linear(float* w, const float* g, float* ms, float lr, float rho, float eps, int in,
+                                int out, void* kn, void* nk, void* q4, void* q4s, hipStream_t st);
+// The same update over nranges float ranges (offset, count pairs in device
+// memory), one workgroup each.
+gp_status update_ranges(float* w, const float* g, float* ms, float lr, float rho, float eps, const long* ranges,
+                        int nranges, hipStream_t st);
 gp_status refresh_linear(int dtype, const float* w, int in, int out, void* kn, void* nk, void* q4, void* q4s,
                          hipStream_t st);
 // An empty launch labelled by its grid (role x (edge + 1) workgroups of one

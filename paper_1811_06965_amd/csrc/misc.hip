@@ -204,6 +204,70 @@ __global__ void __launch_bounds__(256) refresh_bf16_tiles(const float* __restric
     }
 }
 
+// The update of a linear's weights fused with the refresh of its bf16 working
+// copies (in, out multiples of 64): W <- W - lr G (SGD) or the RMSProp step
+// (rms: ms <- rho ms + (1 - rho) G^2; W <- W - lr G / sqrt(ms + eps)) on the
+// fp32 master, then kn = W, nk = W^T from the updated values through a
+// 64 x 64 LDS tile -- one pass over W and G instead of an update pass and a
+// refresh pass.  Per element the same arithmetic as sgd_kernel and
+// rmsprop_kernel.
+__global__ void __launch_bounds__(256) update_refresh_tiles(float* __restrict__ w, const float* __restrict__ g,
+                                                            float* __restrict__ ms, float lr, float rho, float eps,
+                                                            int rms, int in, int out, bf16* __restrict__ kn,
+                                                            bf16* __restrict__ nk) {
+    __shared__ float tile[64][65];
+    const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64, t = threadIdx.x;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int idx = t + 256 * k, r = idx >> 4, c = (idx & 15) * 4;
+        const long o = (long)(r0 + r) * out + c0 + c;
+        f32x4 v = *reinterpret_cast<const f32x4*>(w + o);
+        const f32x4 gv = *reinterpret_cast<const f32x4*>(g + o);
+        if (rms) {
+            f32x4 m = *reinterpret_cast<const f32x4*>(ms + o);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                m[e] = rho * m[e] + (1.f - rho) * (gv[e] * gv[e]);
+                v[e] -= lr * gv[e] / sqrtf(m[e] + eps);
+            }
+            *reinterpret_cast<f32x4*>(ms + o) = m;
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] -= lr * gv[e];
+        }
+        *reinterpret_cast<f32x4*>(w + o) = v;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) tile[r][c + j] = v[j];
+        *reinterpret_cast<bf16x4*>(kn + o) = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int idx = t + 256 * k, c = idx >> 4, r = (idx & 15) * 4;
+        *reinterpret_cast<bf16x4*>(nk + (long)(c0 + c) * in + r0 + r) =
+            {(bf16)tile[r][c], (bf16)tile[r + 1][c], (bf16)tile[r + 2][c], (bf16)tile[r + 3][c]};
+    }
+}
+
+// The same update over the parameters outside the linears' weight blocks
+// (biases, LayerNorm gains and shifts): workgroup b takes the float range
+// [ranges[2 b], ranges[2 b] + ranges[2 b + 1]).
+__global__ void __launch_bounds__(256) update_ranges_kernel(float* __restrict__ w, const float* __restrict__ g,
+                                                            float* __restrict__ ms, float lr, float rho, float eps,
+                                                            int rms, const long* __restrict__ ranges) {
+    const long off = ranges[2 * blockIdx.x], n = ranges[2 * blockIdx.x + 1];
+    for (long i = off + threadIdx.x; i < off + n; i += 256) {
+        const float gv = g[i];
+        if (rms) {
+            const float m = rho * ms[i] + (1.f - rho) * (gv * gv);
+            ms[i] = m;
+            w[i] -= lr * gv / sqrtf(m + eps);
+        } else {
+            w[i] -= lr * gv;
+        }
+    }
+}
+
 // fp4 copy of bf16 rows (the W^T working copy, rows of `in` values): one wave
 // per row; 8 values per lane step; one E8M0 scale per row (see e2m1_code).
 __global__ void __launch_bounds__(256) quant4_rows_kernel(const bf16* __restrict__ src, int rows, int in,
@@ -381,6 +445,30 @@ gp_status rmsprop_update(float* w, const float* g, float* ms, float lr, float rh
     if (count % 4) return set_error(GP_ERR_INVALID_ARG, "rmsprop: parameter count must be a multiple of 4");
     klaunch(rmsprop_kernel, ew_grid(count / 4), 256, 0, st, reinterpret_cast<f32x4*>(w),
             reinterpret_cast<const f32x4*>(g), reinterpret_cast<f32x4*>(ms), lr, rho, eps, count / 4);
+    GP_LAUNCH_CHECK();
+    return GP_OK;
+}
+
+gp_status update_refresh_linear(float* w, const float* g, float* ms, float lr, float rho, float eps, int in,
+                                int out, void* kn, void* nk, void* q4, void* q4s, hipStream_t st) {
+    if (in % 64 || out % 64) return set_error(GP_ERR_INVALID_ARG, "update_refresh: in and out must be multiples of 64");
+    dim3 grid(out / 64, in / 64);
+    klaunch(update_refresh_tiles, grid, 256, 0, st, w, g, ms, lr, rho, eps, ms ? 1 : 0, in, out,
+            reinterpret_cast<bf16*>(kn), reinterpret_cast<bf16*>(nk));
+    GP_LAUNCH_CHECK();
+    if (q4) {
+        if (in % 8) return set_error(GP_ERR_UNSUPPORTED, "refresh: fp4 copies are made from bf16 rows");
+        klaunch(quant4_rows_kernel, (out + 3) / 4, 256, 0, st, reinterpret_cast<const bf16*>(nk), out, in,
+                reinterpret_cast<unsigned char*>(q4), reinterpret_cast<unsigned char*>(q4s));
+        GP_LAUNCH_CHECK();
+    }
+    return GP_OK;
+}
+
+gp_status update_ranges(float* w, const float* g, float* ms, float lr, float rho, float eps, const long* ranges,
+                        int nranges, hipStream_t st) {
+    if (nranges <= 0) return GP_OK;
+    klaunch(update_ranges_kernel, nranges, 256, 0, st, w, g, ms, lr, rho, eps, ms ? 1 : 0, ranges);
     GP_LAUNCH_CHECK();
     return GP_OK;
 }

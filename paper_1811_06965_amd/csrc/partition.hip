@@ -200,6 +200,12 @@ struct gp_partition {
     std::vector<Span> fp_span;
     bool dw_started = false;   // a weight-gradient GEMM of this mini-batch was launched
     float* opt_ms = nullptr;  // RMSProp: running mean square of every gradient [n32]
+    // bf16 partitions whose linears are whole 64 x 64 tiles update each
+    // linear's weights fused with the refresh of its working copies, and the
+    // rest (biases, LayerNorm parameters) from a table of float ranges
+    bool fused_update = false;
+    long* upd_ranges = nullptr;  // device: (offset, count) pairs
+    int n_upd_ranges = 0;
     // GP_POISON=1 (test mode): every workspace region is filled with NaN
     // right before the phase that (re)writes it, so that a read of a stale or
     // never-written value shows up in the results.  Regions, per set: the
@@ -1116,9 +1122,12 @@ void free_all(gp_partition* p) {
     p->timer = LaunchTimer();
     p->timer.markers = markers;
     for (void* x : {(void*)p->master, (void*)p->grads, (void*)p->welt, (void*)p->stash_x, (void*)p->stash_m,
-                    (void*)p->ws, (void*)p->opt_ms})
+                    (void*)p->ws, (void*)p->opt_ms, (void*)p->upd_ranges})
         if (x) (void)hipFree(x);
     p->master = p->grads = p->opt_ms = nullptr;
+    p->upd_ranges = nullptr;
+    p->n_upd_ranges = 0;
+    p->fused_update = false;
     p->welt = p->stash_x = p->stash_m = p->ws = nullptr;
 }
 
@@ -1321,6 +1330,30 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
     if (e == hipSuccess) e = hipMemset(p->grads, 0, p->plan.n32 * 4);
     if (e == hipSuccess) e = hipMemset(p->ws, 0, p->bytes_ws);
     if (e == hipSuccess && p->opt_ms) e = hipMemset(p->opt_ms, 0, p->plan.n32 * 4);
+    if (e == hipSuccess && g.dtype == GP_BF16) {
+        bool tiles = true;
+        std::vector<long> ranges;
+        size_t covered = 0;  // the weights and the ranges must cover every parameter once
+        for (const Linear* l : p->plan.linears()) {
+            tiles = tiles && l->in % 64 == 0 && l->out % 64 == 0;
+            ranges.push_back((long)l->b);
+            ranges.push_back(l->out);
+            covered += (size_t)l->in * l->out + l->out;
+        }
+        for (const Norm* n : p->plan.norms()) {
+            tiles = tiles && n->b == n->g + n->n;  // gains then shifts, contiguous
+            ranges.push_back((long)n->g);
+            ranges.push_back(2L * n->n);
+            covered += 2 * (size_t)n->n;
+        }
+        if (tiles && covered == p->plan.n32) {
+            e = hipMalloc((void**)&p->upd_ranges, ranges.size() * sizeof(long));
+            if (e == hipSuccess)
+                e = hipMemcpy(p->upd_ranges, ranges.data(), ranges.size() * sizeof(long), hipMemcpyHostToDevice);
+            p->n_upd_ranges = (int)(ranges.size() / 2);
+            p->fused_update = e == hipSuccess;
+        }
+    }
     if (e != hipSuccess) {
         free_all(p);
         return hip_fail(e, __FILE__, __LINE__);
@@ -1753,13 +1786,26 @@ gp_status gp_accumulate_and_step(gp_partition* p, float lr, double* loss_out, gp
             return set_error(GP_ERR_NONFINITE, "non-finite gradient: update skipped");
         }
     }
-    if (p->g.optimizer == GP_OPT_RMSPROP)
-        GP_TRY(rmsprop_update(p->master, p->grads, p->opt_ms, lr, p->g.rms_decay, p->g.rms_eps, (long)p->plan.n32, st));
-    else
-        GP_TRY(sgd_update(p->master, p->grads, lr, (long)p->plan.n32, st));
-    for (const Linear* l : p->plan.linears())
-        GP_TRY(refresh_linear(dt, p->master + l->w, l->in, l->out, p->W(l->kn), p->W(l->nk),
-                              l->split ? p->W(l->q4) : nullptr, l->split ? p->W(l->q4s) : nullptr, st));
+    const bool rms = p->g.optimizer == GP_OPT_RMSPROP;
+    if (p->fused_update) {
+        // one pass over each linear's W and G that also rewrites its working
+        // copies, then the biases and LayerNorm parameters
+        for (const Linear* l : p->plan.linears())
+            GP_TRY(update_refresh_linear(p->master + l->w, p->grads + l->w, rms ? p->opt_ms + l->w : nullptr, lr,
+                                         p->g.rms_decay, p->g.rms_eps, l->in, l->out, p->W(l->kn), p->W(l->nk),
+                                         l->split ? p->W(l->q4) : nullptr, l->split ? p->W(l->q4s) : nullptr, st));
+        GP_TRY(update_ranges(p->master, p->grads, rms ? p->opt_ms : nullptr, lr, p->g.rms_decay, p->g.rms_eps,
+                             p->upd_ranges, p->n_upd_ranges, st));
+    } else {
+        if (rms)
+            GP_TRY(rmsprop_update(p->master, p->grads, p->opt_ms, lr, p->g.rms_decay, p->g.rms_eps,
+                                  (long)p->plan.n32, st));
+        else
+            GP_TRY(sgd_update(p->master, p->grads, lr, (long)p->plan.n32, st));
+        for (const Linear* l : p->plan.linears())
+            GP_TRY(refresh_linear(dt, p->master + l->w, l->in, l->out, p->W(l->kn), p->W(l->nk),
+                                  l->split ? p->W(l->q4) : nullptr, l->split ? p->W(l->q4s) : nullptr, st));
+    }
     if (loss_out) {
         double v = 0.0;
         if (p->g.loss != GP_LOSS_NONE)

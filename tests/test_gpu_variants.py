@@ -196,6 +196,50 @@ def test_rmsprop_bf16_runs_and_holds_twelve_bytes_per_parameter():
         assert np.isfinite(after[0]["w1"]).all() and 0 < moved.max() < 1e-3
 
 
+@pytest.mark.parametrize("opt", ["sgd", "rmsprop"])
+@pytest.mark.parametrize("cfg", [ENC512_SMALL, DEC_BF16], ids=lambda c: c.name)
+def test_bf16_update_applies_the_accumulated_gradient(cfg, opt):
+    """The bf16 partitions' step (each linear's weights updated in the pass
+    that rewrites their working copies; biases and LayerNorm parameters from
+    a range table): every parameter tensor, head included, moves by exactly
+    the SGD or RMSProp step of its accumulated gradient (fp32 on the host,
+    within two roundings of the parameter and a few of the step), two steps
+    in a row."""
+    from paper_1811_06965_amd.runtime import Partition
+    cfg = cfg.with_(optimizer=opt, rms_decay=0.9, rms_eps=1e-8)
+    case = synth.make_case(cfg, 26, perturb=True)
+    lr, rho, eps = np.float32(1e-3), np.float32(0.9), np.float32(1e-8)
+    with Partition(cfg) as part:
+        part.load_params(case["layers"], case["head"])
+        inp = part.device_inputs(case)
+        ms = None
+        for _ in range(2):
+            w0 = part.params()
+            out = part.step(inp["x"], inp["mem"], inp["dy"], lr=float(lr), want_y=False)
+            torch.cuda.synchronize()
+            g = part.grads()
+            w1 = part.params()
+            if ms is None:
+                ms = ([{k: np.zeros_like(v) for k, v in d.items()} for d in g[0]], {k: np.zeros_like(v) for k, v in g[1].items()})
+            for side in (0, 1):
+                groups = zip(w0[0], g[0], w1[0], ms[0]) if side == 0 else [(w0[1], g[1], w1[1], ms[1])]
+                for a, gg, b, m in groups:
+                    for k in a:
+                        gk = gg[k].astype(np.float32)
+                        if opt == "sgd":
+                            step = lr * gk
+                        else:
+                            m[k] = rho * m[k] + (np.float32(1) - rho) * (gk * gk)
+                            step = lr * gk / np.sqrt(m[k] + eps)
+                        want = a[k] - step
+                        # one rounding of the parameter, plus a few of the step's
+                        # own (a fused multiply-add, the square root and the
+                        # division may round differently from the host's)
+                        tol = (np.spacing(np.maximum(np.abs(want), np.abs(a[k]))) * 2
+                               + np.spacing(np.abs(step)) * 8).astype(np.float32)
+                        assert (np.abs(b[k] - want) <= tol).all(), (k, np.abs(b[k] - want).max())
+
+
 # ------------------------------------------------------- logit clipping
 def _clip_at(cfg, case, q):
     """A clip bound at the q-quantile of the oracle's |logits|."""

@@ -199,12 +199,13 @@ def test_rmsprop_bf16_runs_and_holds_twelve_bytes_per_parameter():
 @pytest.mark.parametrize("opt", ["sgd", "rmsprop"])
 @pytest.mark.parametrize("cfg", [ENC512_SMALL, DEC_BF16], ids=lambda c: c.name)
 def test_bf16_update_applies_the_accumulated_gradient(cfg, opt):
-    """The bf16 partitions' step (each linear's weights updated in the pass
-    that rewrites their working copies; biases and LayerNorm parameters from
-    a range table): every parameter tensor, head included, moves by exactly
-    the SGD or RMSProp step of its accumulated gradient (fp32 on the host,
-    within two roundings of the parameter and a few of the step), two steps
-    in a row."""
+    """The bf16 partitions' step: every parameter tensor, head included,
+    moves by exactly the SGD or RMSProp step of its accumulated gradient (fp32
+    on the host, within two roundings of the parameter and a few of the
+    step), two steps in a row.  The encoder's linears are whole 64 x 64 tiles, so its weights
+    are updated in the pass that rewrites their working copies (biases and
+    LayerNorm parameters from a range table); the decoder's 1000-way head is
+    not, so it takes the separate update and refresh kernels."""
     from paper_1811_06965_amd.runtime import Partition
     cfg = cfg.with_(optimizer=opt, rms_decay=0.9, rms_eps=1e-8)
     case = synth.make_case(cfg, 26, perturb=True)

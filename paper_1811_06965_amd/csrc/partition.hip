@@ -1331,22 +1331,8 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
     if (e == hipSuccess) e = hipMemset(p->ws, 0, p->bytes_ws);
     if (e == hipSuccess && p->opt_ms) e = hipMemset(p->opt_ms, 0, p->plan.n32 * 4);
     if (e == hipSuccess && g.dtype == GP_BF16) {
-        bool tiles = true;
         std::vector<long> ranges;
-        size_t covered = 0;  // the weights and the ranges must cover every parameter once
-        for (const Linear* l : p->plan.linears()) {
-            tiles = tiles && l->in % 64 == 0 && l->out % 64 == 0;
-            ranges.push_back((long)l->b);
-            ranges.push_back(l->out);
-            covered += (size_t)l->in * l->out + l->out;
-        }
-        for (const Norm* n : p->plan.norms()) {
-            tiles = tiles && n->b == n->g + n->n;  // gains then shifts, contiguous
-            ranges.push_back((long)n->g);
-            ranges.push_back(2L * n->n);
-            covered += 2 * (size_t)n->n;
-        }
-        if (tiles && covered == p->plan.n32) {
+        if (plan_update_ranges(p->plan, ranges)) {
             e = hipMalloc((void**)&p->upd_ranges, ranges.size() * sizeof(long));
             if (e == hipSuccess)
                 e = hipMemcpy(p->upd_ranges, ranges.data(), ranges.size() * sizeof(long), hipMemcpyHostToDevice);

@@ -11,8 +11,10 @@
 #pragma once
 
 #include <cstddef>
+#include <algorithm>
 #include <cstdint>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "../../include/gp.h"
@@ -214,6 +216,47 @@ inline ParamPlan plan_params(const Dims& d, const Geometry& g) {
     p.n32 = f;
     p.nelt = e;
     return p;
+}
+
+// The bf16 update pass.  Each linear's W is updated in 64 x 64 tiles in the
+// same pass that rewrites its working copies; every other parameter (the
+// biases, LayerNorm gains and shifts) is updated from a list of (offset,
+// count) float ranges, written to `ranges` as flat pairs.  Returns false (and
+// leaves `ranges` empty) unless every linear is a whole number of tiles and
+// the weights and ranges together cover the n32 master floats exactly once.
+inline bool plan_update_ranges(const ParamPlan& p, std::vector<long>& ranges) {
+    ranges.clear();
+    std::vector<std::pair<size_t, size_t>> cover;  // (offset, count) of every block
+    for (const Linear* l : p.linears()) {
+        if (l->in % 64 || l->out % 64) {
+            ranges.clear();
+            return false;
+        }
+        cover.push_back({l->w, (size_t)l->in * l->out});
+        cover.push_back({l->b, (size_t)l->out});
+        ranges.push_back((long)l->b);
+        ranges.push_back(l->out);
+    }
+    for (const Norm* n : p.norms()) {
+        if (n->b != n->g + (size_t)n->n) {  // gains then shifts, contiguous
+            ranges.clear();
+            return false;
+        }
+        cover.push_back({n->g, 2 * (size_t)n->n});
+        ranges.push_back((long)n->g);
+        ranges.push_back(2L * n->n);
+    }
+    std::sort(cover.begin(), cover.end());
+    size_t end = 0;
+    for (const auto& c : cover) {
+        if (c.first != end) {  // a gap (padding) or an overlap
+            ranges.clear();
+            return false;
+        }
+        end = c.first + c.second;
+    }
+    if (end != p.n32) ranges.clear();
+    return end == p.n32;
 }
 
 // Where one logical parameter tensor lives in the fp32 master: `rows` rows of

@@ -6,6 +6,7 @@
 #include <set>
 #include <string>
 #include <utility>
+#include <vector>
 
 #include "../../paper_1811_06965_amd/csrc/sched.hpp"
 
@@ -80,6 +81,17 @@ int main() {
     ParamPlan pd = plan_params(d, gd);
     const size_t cross = 4 * 1024 * 1024 + 4 * 1024 + 2 * 1024;
     CHECK(pd.count == 16 * (per_layer + cross) + 2 * 1024 + 1024 * 32000 + 32000, "plan_count_decoder_head");
+
+    // ---- the bf16 update's range table: weights in tiles, every other parameter in a range
+    std::vector<long> ranges;
+    CHECK(plan_update_ranges(p, ranges) && ranges.size() == 2 * (4 * 16 + 2 * 16), "update_ranges_encoder");
+    bool biases = true;
+    for (size_t i = 0; i < ranges.size(); i += 2) biases = biases && ranges[i] % 64 == 0 && ranges[i + 1] > 0;
+    CHECK(biases && ranges[0] == (long)p.layers[0].qkv.b && ranges[1] == 3 * 1024, "update_ranges_first_bias");
+    CHECK(plan_update_ranges(pd, ranges) && ranges.size() == 2 * (7 * 16 + 3 * 16 + 2), "update_ranges_decoder_head");
+    Geometry gv = gd; gv.V = 1000;  // a head that is not a whole number of 64-wide tiles
+    CHECK(!plan_update_ranges(plan_params(d, gv), ranges) && ranges.empty(), "update_ranges_ragged_head");
+    CHECK(!plan_update_ranges(plan_params(d3, g), ranges) && ranges.empty(), "update_ranges_ragged_widths");
 
     // ---- parameter resolution: q/k/v are column slices of the packed projection
     ParamRef r;

@@ -59,6 +59,9 @@ def parse():
     ap.add_argument("--traffic-summary", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CAL_FETCH_DIR", "CAL_WRITE_DIR"),
                     help="summarise rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs of `--role R` (with "
                          "GP_TIMER_MARKERS=1) and of --copy-calibration into the stored traffic figures")
+    ap.add_argument("--counter-summary", metavar="DIR",
+                    help="print, as JSON, the median per launch of `--role R` of every counter in a rocprofv3 "
+                         "--pmc run of that role (GP_TIMER_MARKERS=1), summed over the counter's instances")
     ap.add_argument("--kernel-summary", metavar="DIR",
                     help="print a markdown summary of a rocprofv3 --kernel-trace database under DIR "
                          "(per-kernel totals, and per-role launch durations when GP_TIMER_MARKERS=1 was set)")
@@ -192,6 +195,21 @@ def _between_markers(disp):
             cur[q][0] += v
             cur[q][1].append(name)
     return out
+
+
+def counter_summary(d, role):
+    """Median per launch of the role (the kernels between its markers) of
+    every counter collected under d."""
+    rows = _pmc_rows(d)
+    out = {"role": role, "counters": {}}
+    for c in sorted({r["Counter_Name"] for r in rows}):
+        launches = _between_markers(_per_dispatch(rows, c))
+        vals = sorted(l[0] for l in launches)
+        if vals:
+            out["counters"][c] = vals[len(vals) // 2]
+            out["launches"] = len(vals)
+            out["kernels"] = sorted({k for l in launches for k in l[1]})
+    print(json.dumps(out, indent=1))
 
 
 def traffic_summary(fetch_dir, write_dir, cal_fetch_dir, cal_write_dir, role, workload):
@@ -491,6 +509,11 @@ def main():
                 ("boundary gradients" if cfg.loss == "none" else f"{cfg.loss} loss"))
     if a.kernel_summary:
         kernel_summary(a.kernel_summary, a.command, roles_json=a.roles_json)
+        return
+    if a.counter_summary:
+        if not a.role:
+            sys.exit("--counter-summary needs --role")
+        counter_summary(a.counter_summary, a.role)
         return
     if a.traffic_summary:
         if not a.role:

@@ -1464,6 +1464,11 @@ void choose_dl_model(const GemmArgs& a, int epi, bool kmaj, int& cfg, int& split
     const Cand* cands = kmaj ? kc : mc;
     const int ncand = kmaj ? (int)(sizeof(kc) / sizeof(kc[0])) : (int)(sizeof(mc) / sizeof(mc[0]));
     const double c0 = kmaj ? 4.147 : 0.0, BW = kmaj ? 1.969e6 : 5.084e6, red0 = kmaj ? 3.285 : 7.821;
+    // The m/n-contiguous shapes are the weight gradients, which run beside the
+    // backward's dX chain and the recompute: a split spends more CU time
+    // (partial planes and a reduce) to finish sooner alone, so it is costed
+    // three times over for them.
+    const double split_w = (kmaj ? 1.0 : 3.0) * split_weight();
     const int nk = a.K / 64;
     double best = 1e300;
     cfg = T_DL128x128_W8A;
@@ -1479,7 +1484,7 @@ void choose_dl_model(const GemmArgs& a, int epi, bool kmaj, int& cfg, int& split
             const int occ = (int)std::min<long>(per_cu, c.resident);
             double t = c0 + rounds * (double)((nk + s - 1) / s) * c.step[occ - 1] * mx_step;
             if (epi == EPI_ACC_F32) t += (kmaj ? 3.0 : 0.0) + (double)a.M * a.N * 8.0 / BW;
-            if (s > 1) t += split_weight() * ((double)a.M * a.N * 4.0 * (s + 1.0) / 2.0 / BW + red0);
+            if (s > 1) t += split_w * ((double)a.M * a.N * 4.0 * (s + 1.0) / 2.0 / BW + red0);
             if (t < best * 0.999) {
                 best = t;
                 cfg = c.cfg;

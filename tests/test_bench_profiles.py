@@ -2,7 +2,8 @@
 launches are the kernels between a pair of role markers on the marker's own
 hardware queue; counters are summed over their instances; FETCH_SIZE and
 WRITE_SIZE (KiB per dispatch) are scaled by what they read for a copy of
-known size.  Checked on small synthetic counter files."""
+known size; the kernel trace's role spans come from marker pairs on one
+stream.  Checked on small synthetic counter files and trace databases."""
 import csv
 import json
 import os
@@ -80,3 +81,39 @@ def test_traffic_is_scaled_by_the_copy_calibration(tmp_path, monkeypatch, capsys
     stored = json.load(open(tmp_path / "traffic.json"))
     assert stored["source_sha256"] == bench.source_digest() and stored["workload"] == "synthetic workload"
     assert stored["roles"]["qkv.dw"]["bytes_per_launch"] == pytest.approx(e["bytes_per_launch"])
+
+
+def test_kernel_trace_roles_from_marker_pairs(tmp_path, capsys):
+    """The kernel-trace summary attributes to a role the kernels that its
+    start and end markers (role = grid_x / workgroup_x, edge = grid_y - 1)
+    enclose on the same stream, in dispatch order."""
+    import sqlite3
+    from paper_1811_06965_amd import gp
+    role = gp.KERNEL_ROLE["ffn1.fwd"]
+    d = tmp_path / "trace"
+    d.mkdir()
+    db = sqlite3.connect(str(d / "run_results.db"))
+    db.execute("create table kernels (name text, grid_x int, grid_y int, workgroup_x int, start int, end int, "
+               "stream_id int, dispatch_id int)")
+    ns = 1000
+    rows = [("role_marker", role * 64, 1, 64, 0, 1, 1),
+            ("gemm_dl<256>(gp::GemmArgs)", 256, 1, 256, 10 * ns, 40 * ns, 1),
+            ("other_kernel", 64, 1, 64, 20 * ns, 60 * ns, 2),
+            ("role_marker", role * 64, 2, 64, 41 * ns, 41 * ns + 1, 1),
+            ("outside_kernel", 64, 1, 64, 60 * ns, 90 * ns, 1),
+            ("role_marker", role * 64, 1, 64, 95 * ns, 95 * ns + 1, 1),
+            ("gemm_dl<256>(gp::GemmArgs)", 256, 1, 256, 100 * ns, 140 * ns, 1),
+            ("splitk_reduce(gp::GemmArgs, int)", 64, 1, 64, 145 * ns, 150 * ns, 1),
+            ("role_marker", role * 64, 2, 64, 151 * ns, 151 * ns + 1, 1)]
+    db.executemany("insert into kernels values (?, ?, ?, ?, ?, ?, ?, ?)",
+                   [r + (i,) for i, r in enumerate(rows)])
+    db.commit()
+    db.close()
+    roles_json = tmp_path / "roles.json"
+    bench.kernel_summary(str(d), "cmd", roles_json=str(roles_json))
+    out = capsys.readouterr().out
+    assert "| ffn1.fwd | 2 | 37.5 | 40.0 |" in out  # kernel time 30 and 45 us; first start to last end 30 and 50
+    rec = json.load(open(roles_json))["roles"]["ffn1.fwd"]
+    assert rec["launches"] == 2 and rec["mean_kernel_us"] == pytest.approx(37.5)
+    assert rec["mean_span_us"] == pytest.approx(40.0)
+    assert "other_kernel" not in str(rec["kernels"]) and "outside_kernel" not in str(rec["kernels"])

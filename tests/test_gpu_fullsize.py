@@ -77,10 +77,11 @@ def enc1024():
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("M", [4, 8, 16, 32])
+@pytest.mark.parametrize("M", [4, 8, 16, 32, 64])
 def test_enc1024_full_size_every_micro_batch_count(enc1024, M):
     """enc1024 (16 layers, d_model 1024, d_ff 8192, 16 heads, S 256, N 64) at
-    each M of the benchmark sweep; M = 4 runs the 4-wave attention kernels
+    each M of the benchmark sweep, and at M = 64 (one sequence per
+    micro-batch, 256-row GEMMs); M = 4 runs the 4-wave attention kernels
     (4096 query blocks per launch), M = 32 the 512-row GEMM tiles."""
     cfg, case, sample, ref = enc1024
     y, dx, gl, gh = _sampled_step(cfg, case, sample, M)

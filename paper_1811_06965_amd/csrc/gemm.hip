@@ -61,6 +61,12 @@ template <> struct Frag<float> {
 __device__ __forceinline__ void mma(f32x16& c, const Frag<bf16>& a, const Frag<bf16>& b) {
     c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.v, b.v, c, 0, 0, 0);
 }
+// The same block with both operands' 16-bit elements read as fp16.
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ void mma16(f32x16& c, const Frag<bf16>& a, const Frag<bf16>& b) {
+    c = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a.v), __builtin_bit_cast(f16x8, b.v), c, 0,
+                                               0, 0);
+}
 __device__ __forceinline__ void mma(f32x16& c, const Frag<float>& a, const Frag<float>& b) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) c = __builtin_amdgcn_mfma_f32_32x32x2f32(a.lo[e], b.lo[e], c, 0, 0, 0);
@@ -686,8 +692,11 @@ __device__ __forceinline__ bf16x8 tr_frag(const char* p, int second) {
 //   lockstep (one workgroup barrier per k-tile each), and at the end group 1
 //   hands its accumulators to group 0 through LDS, which adds them and runs
 //   the epilogue.  The k-tile count must be a multiple of KG.
-template <int BM, int BN, int WM, int WN, int NSTAGE, int EPI, int SM, bool KM, bool MX = false, int KG = 1>
+// F16: A and B hold fp16 values (k-contiguous, no fp4 stage, one k-group).
+template <int BM, int BN, int WM, int WN, int NSTAGE, int EPI, int SM, bool KM, bool MX = false, int KG = 1,
+          bool F16 = false>
 __global__ void __launch_bounds__(64 * WM * WN * KG) gemm_dl(GemmArgs args) {
+    static_assert(!F16 || (KM && !MX && KG == 1), "fp16 operands: k-contiguous, no fp4 stage, one k-group");
     // SM: 0 no split-K; 1 split-K, partial tiles only (summed by splitk_reduce)
     constexpr bool SPLIT = SM != 0;
     constexpr int BK = 64, KS = 4, NW = WM * WN;  // NW: waves per k-group
@@ -982,7 +991,12 @@ __global__ void __launch_bounds__(64 * WM * WN * KG) gemm_dl(GemmArgs args) {
 #pragma unroll
                     for (int ii = 0; ii < TM; ++ii)
 #pragma unroll
-                        for (int j = 0; j < TN; ++j) mma(acc[ii][j], fa[cur][ii], fb[cur][j]);
+                        for (int j = 0; j < TN; ++j) {
+                            if constexpr (F16)
+                                mma16(acc[ii][j], fa[cur][ii], fb[cur][j]);
+                            else
+                                mma(acc[ii][j], fa[cur][ii], fb[cur][j]);
+                        }
                     if constexpr (MX) {
                         if (s == 1) {
 #pragma unroll
@@ -1312,6 +1326,38 @@ gp_status launch_dl_mx(const GemmArgs& a, int splits, hipStream_t st) {
     return GP_OK;
 }
 
+// The fp16 forward GEMM (EPI_STORE, k-contiguous fp16 operands).
+template <int BM, int BN, int WM, int WN, int NSTAGE>
+gp_status launch_dl16(const GemmArgs& a, int splits, hipStream_t st) {
+    constexpr int NT = 64 * WM * WN;
+    const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+    if (splits > 1) {
+        klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_F32, 1, true, false, 1, true>, dim3(tiles, splits), NT, 0, st, a);
+        GP_LAUNCH_CHECK();
+        return launch_reduce(a, EPI_STORE, splits, st);
+    }
+    klaunch(gemm_dl<BM, BN, WM, WN, NSTAGE, EPI_STORE, 0, true, false, 1, true>, tiles, NT, 0, st, a);
+    GP_LAUNCH_CHECK();
+    return GP_OK;
+}
+
+// The chooser's k-contiguous shapes, with fp16 operands.
+gp_status launch_f16(const GemmArgs& a, int cfg, int splits, hipStream_t st) {
+    switch (cfg) {
+    case T_DL256x256_W8: return launch_dl16<256, 256, 2, 4, 2>(a, splits, st);
+    case T_DL256x128_W8: return launch_dl16<256, 128, 4, 2, 2>(a, splits, st);
+    case T_DL128x256_W8: return launch_dl16<128, 256, 2, 4, 2>(a, splits, st);
+    case T_DL256x128_W8S3: return launch_dl16<256, 128, 4, 2, 3>(a, splits, st);
+    case T_DL128x256_W8S3: return launch_dl16<128, 256, 2, 4, 3>(a, splits, st);
+    case T_DL128x128_W8S4: return launch_dl16<128, 128, 2, 4, 4>(a, splits, st);
+    case T_DL128x128_W8S3: return launch_dl16<128, 128, 2, 4, 3>(a, splits, st);
+    case T_DL128x64_S4: return launch_dl16<128, 64, 2, 2, 4>(a, splits, st);
+    case T_DL128x64: return launch_dl16<128, 64, 2, 2, 2>(a, splits, st);
+    case T_DL64x128: return launch_dl16<64, 128, 2, 2, 2>(a, splits, st);
+    default: return launch_dl16<128, 128, 2, 4, 2>(a, splits, st);  // T_DL128x128_W8A and any other
+    }
+}
+
 // Tile shapes whose fp4 stage splits into whole 1 KB blocks per wave.
 bool mx_capable(int cfg) {
     return cfg == T_DL128x128_S2 || cfg == T_DL128x128_S3 || cfg == T_DL256x128_S2 || cfg == T_DL256x256_S2 ||
@@ -1590,6 +1636,16 @@ long gemm_workspace_need(const GemmArgs& a, int epi, bool a_kmajor, int dtype) {
 
 gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dtype, hipStream_t st) {
     if (a.deferred) *a.deferred = 1;
+    if (a.f16) {
+        if (dtype != GP_BF16 || !a_kmajor || !b_kmajor || epi != EPI_STORE || a.K % 64 || a.a4)
+            return set_error(GP_ERR_UNSUPPORTED, "gemm: fp16 operands need k-contiguous operands, a stored epilogue, "
+                                                 "K % 64 == 0 and no fp4 term");
+        gp_status s = check_args<bf16>(a, true, true);
+        if (s != GP_OK) return s;
+        int cfg, splits;
+        decide_bf16(a, epi, true, cfg, splits);
+        return launch_f16(a, cfg, splits, st);
+    }
     if (a.a4) {
         if (dtype != GP_BF16 || !a_kmajor || !b_kmajor || epi != EPI_STORE || a.K % 64 || !a.b4 || !a.sa4 || !a.sb4)
             return set_error(GP_ERR_UNSUPPORTED, "gemm: the fp4 correction needs bf16, k-contiguous operands, "

@@ -52,6 +52,9 @@ struct GemmArgs {
     // (the tile shape does not change any element's order).  ws must hold the
     // partials of the M rows.
     int split_rows = 0;
+    // A and B hold fp16 values instead of bf16 (EPI_STORE, k-contiguous, no
+    // fp4 term); the tile and split choice is the bf16 one
+    int f16 = 0;
 };
 
 gp_status gemm(const GemmArgs& a, int epi, bool a_kmajor, bool b_kmajor, int dtype, hipStream_t st);
@@ -66,8 +69,11 @@ gp_status gemm_reduce(const GemmArgs& a, int epi, int splits, hipStream_t st);
 // lo4 / lo_sc (optional; bf16, D % 64 == 0): the rounding residuals y - bf16(y)
 // of the row as fp4 [rows, D/2] bytes with one E8M0 scale per row, the
 // correction operand (GemmArgs::a4) of the GEMM that consumes out.
+// out16 (optional; bf16, D % 256 == 0, D <= 2048): out also in fp16, the A
+// operand of a GEMM with fp16 operands (GemmArgs::f16).
 gp_status layernorm_fwd(int dtype, const float* x, long rows, int D, const float* gamma, const float* beta,
-                        float eps, void* out, float* stats, void* lo4, unsigned char* lo_sc, hipStream_t st);
+                        float eps, void* out, float* stats, void* lo4, unsigned char* lo_sc, hipStream_t st,
+                        void* out16 = nullptr);
 // The split-K reduce of a residual GEMM fused with the LayerNorm of its result:
 // x = sum over s < splits of ws[s plane + row D + col], plus (res + bias), in
 // the order of the GEMM's own reduce, is stored in xo (fp32) and xc (bf16, when
@@ -78,7 +84,8 @@ bool layernorm_fwd_res_ok(int dtype, int D, const void* ws, const float* bias, c
                           const void* xc);
 gp_status layernorm_fwd_res(int dtype, const float* ws, int splits, long plane, const float* bias, const float* res,
                             float* xo, void* xc, long rows, int D, const float* gamma, const float* beta, float eps,
-                            void* out, float* stats, void* lo4, unsigned char* lo_sc, hipStream_t st);
+                            void* out, float* stats, void* lo4, unsigned char* lo_sc, hipStream_t st,
+                            void* out16 = nullptr);
 // dx = dres + rstd (g - mean g - xh mean(g xh)), g = dn * gamma; writes dx_f32 and/or dx_elt.
 // Per-block partial sums of dn * xh and dn go to partial[blk][2][D] (added to
 // what is there when accumulate != 0); *nblk receives the block count (for
@@ -152,21 +159,22 @@ gp_status sgd_update(float* w, const float* g, float lr, long count, hipStream_t
 // ms = rho ms + (1 - rho) g^2;  w -= lr g / sqrt(ms + eps)  (count % 4 == 0, 16-byte aligned).
 gp_status rmsprop_update(float* w, const float* g, float* ms, float lr, float rho, float eps, long count,
                          hipStream_t st);
-// Working copies of one linear layer from its fp32 master W [in, out]:
-// kn (elt) = W, nk (elt) = W^T.
-// kn = W [in, out]; nk = W^T [out, in]; q4 / q4s (optional, bf16): the rows of
-// nk in fp4 [out, in/2] bytes with one E8M0 scale per row (GemmArgs::b4, sb4).
+// Working copies of one linear layer from its fp32 master W [in, out], in the
+// partition dtype: kn = W [in, out], nk = W^T [out, in].  q4 / q4s (optional,
+// bf16): the rows of nk in fp4 [out, in/2] bytes with one E8M0 scale per row
+// (GemmArgs::b4, sb4).  nk16 (bf16, in and out multiples of 64): nk in fp16
+// instead (the B operand of a GEMM with fp16 operands, GemmArgs::f16).
+gp_status refresh_linear(int dtype, const float* w, int in, int out, void* kn, void* nk, void* q4, void* q4s,
+                         hipStream_t st, bool nk16 = false);
 // The SGD (ms == nullptr) or RMSProp step of a linear's fp32 weights fused
-// with the refresh of its bf16 working copies kn = W, nk = W^T (and the fp4
-// copy of W^T when q4 is set); in, out multiples of 64.
+// with the refresh of its bf16 working copies as refresh_linear makes them;
+// in, out multiples of 64.
 gp_status update_refresh_linear(float* w, const float* g, float* ms, float lr, float rho, float eps, int in,
-                                int out, void* kn, void* nk, void* q4, void* q4s, hipStream_t st);
+                                int out, void* kn, void* nk, void* q4, void* q4s, hipStream_t st, bool nk16 = false);
 // The same update over nranges float ranges (offset, count pairs in device
 // memory), one workgroup each.
 gp_status update_ranges(float* w, const float* g, float* ms, float lr, float rho, float eps, const long* ranges,
                         int nranges, hipStream_t st);
-gp_status refresh_linear(int dtype, const float* w, int in, int out, void* kn, void* nk, void* q4, void* q4s,
-                         hipStream_t st);
 // An empty launch labelled by its grid (role x (edge + 1) workgroups of one
 // wave): edge 0 before, 1 after a timed launch, so that per-dispatch profiler
 // records can be attributed to launch roles.

@@ -180,10 +180,26 @@ __global__ void __launch_bounds__(256) refresh_kernel(const float* __restrict__ 
     }
 }
 
+// Four consecutive elements of a 16-bit working copy, rounded from fp32.
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+template <typename E> struct Copy4;
+template <> struct Copy4<bf16> {
+    static __device__ __forceinline__ void store(bf16* p, float a, float b, float c, float d) {
+        *reinterpret_cast<bf16x4*>(p) = {(bf16)a, (bf16)b, (bf16)c, (bf16)d};
+    }
+};
+template <> struct Copy4<_Float16> {
+    static __device__ __forceinline__ void store(_Float16* p, float a, float b, float c, float d) {
+        *reinterpret_cast<f16x4*>(p) = {(_Float16)a, (_Float16)b, (_Float16)c, (_Float16)d};
+    }
+};
+
 // The same for bf16 copies of whole 64 x 64 tiles (in, out multiples of 64):
-// 16-byte reads of W, 8-byte writes of both copies.
+// 16-byte reads of W, 8-byte writes of both copies.  NK: the element type of
+// the transposed copy (bf16, or fp16 for a GEMM with fp16 operands).
+template <typename NK>
 __global__ void __launch_bounds__(256) refresh_bf16_tiles(const float* __restrict__ w, int in, int out,
-                                                          bf16* __restrict__ kn, bf16* __restrict__ nk) {
+                                                          bf16* __restrict__ kn, NK* __restrict__ nk) {
     __shared__ float tile[64][65];
     const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64, t = threadIdx.x;
 #pragma unroll
@@ -199,8 +215,7 @@ __global__ void __launch_bounds__(256) refresh_bf16_tiles(const float* __restric
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int idx = t + 256 * k, c = idx >> 4, r = (idx & 15) * 4;
-        *reinterpret_cast<bf16x4*>(nk + (long)(c0 + c) * in + r0 + r) =
-            {(bf16)tile[r][c], (bf16)tile[r + 1][c], (bf16)tile[r + 2][c], (bf16)tile[r + 3][c]};
+        Copy4<NK>::store(nk + (long)(c0 + c) * in + r0 + r, tile[r][c], tile[r + 1][c], tile[r + 2][c], tile[r + 3][c]);
     }
 }
 
@@ -211,10 +226,11 @@ __global__ void __launch_bounds__(256) refresh_bf16_tiles(const float* __restric
 // 64 x 64 LDS tile -- one pass over W and G instead of an update pass and a
 // refresh pass.  Per element the same arithmetic as sgd_kernel and
 // rmsprop_kernel.
+template <typename NK>
 __global__ void __launch_bounds__(256) update_refresh_tiles(float* __restrict__ w, const float* __restrict__ g,
                                                             float* __restrict__ ms, float lr, float rho, float eps,
                                                             int rms, int in, int out, bf16* __restrict__ kn,
-                                                            bf16* __restrict__ nk) {
+                                                            NK* __restrict__ nk) {
     __shared__ float tile[64][65];
     const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64, t = threadIdx.x;
 #pragma unroll
@@ -244,8 +260,7 @@ __global__ void __launch_bounds__(256) update_refresh_tiles(float* __restrict__ 
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int idx = t + 256 * k, c = idx >> 4, r = (idx & 15) * 4;
-        *reinterpret_cast<bf16x4*>(nk + (long)(c0 + c) * in + r0 + r) =
-            {(bf16)tile[r][c], (bf16)tile[r + 1][c], (bf16)tile[r + 2][c], (bf16)tile[r + 3][c]};
+        Copy4<NK>::store(nk + (long)(c0 + c) * in + r0 + r, tile[r][c], tile[r + 1][c], tile[r + 2][c], tile[r + 3][c]);
     }
 }
 
@@ -450,11 +465,16 @@ gp_status rmsprop_update(float* w, const float* g, float* ms, float lr, float rh
 }
 
 gp_status update_refresh_linear(float* w, const float* g, float* ms, float lr, float rho, float eps, int in,
-                                int out, void* kn, void* nk, void* q4, void* q4s, hipStream_t st) {
+                                int out, void* kn, void* nk, void* q4, void* q4s, hipStream_t st, bool nk16) {
     if (in % 64 || out % 64) return set_error(GP_ERR_INVALID_ARG, "update_refresh: in and out must be multiples of 64");
+    if (nk16 && q4) return set_error(GP_ERR_INVALID_ARG, "update_refresh: an fp16 W^T has no fp4 copy");
     dim3 grid(out / 64, in / 64);
-    klaunch(update_refresh_tiles, grid, 256, 0, st, w, g, ms, lr, rho, eps, ms ? 1 : 0, in, out,
-            reinterpret_cast<bf16*>(kn), reinterpret_cast<bf16*>(nk));
+    if (nk16)
+        klaunch(update_refresh_tiles<_Float16>, grid, 256, 0, st, w, g, ms, lr, rho, eps, ms ? 1 : 0, in, out,
+                reinterpret_cast<bf16*>(kn), reinterpret_cast<_Float16*>(nk));
+    else
+        klaunch(update_refresh_tiles<bf16>, grid, 256, 0, st, w, g, ms, lr, rho, eps, ms ? 1 : 0, in, out,
+                reinterpret_cast<bf16*>(kn), reinterpret_cast<bf16*>(nk));
     GP_LAUNCH_CHECK();
     if (q4) {
         if (in % 8) return set_error(GP_ERR_UNSUPPORTED, "refresh: fp4 copies are made from bf16 rows");
@@ -474,10 +494,16 @@ gp_status update_ranges(float* w, const float* g, float* ms, float lr, float rho
 }
 
 gp_status refresh_linear(int dtype, const float* w, int in, int out, void* kn, void* nk, void* q4, void* q4s,
-                         hipStream_t st) {
+                         hipStream_t st, bool nk16) {
     dim3 grid((out + 63) / 64, (in + 63) / 64);
-    if (dtype == GP_BF16 && in % 64 == 0 && out % 64 == 0)
-        klaunch(refresh_bf16_tiles, grid, 256, 0, st, w, in, out, reinterpret_cast<bf16*>(kn), reinterpret_cast<bf16*>(nk));
+    if (nk16 && (dtype != GP_BF16 || in % 64 || out % 64 || q4))
+        return set_error(GP_ERR_INVALID_ARG, "refresh: an fp16 W^T needs bf16 whole 64 x 64 tiles and no fp4 copy");
+    if (nk16)
+        klaunch(refresh_bf16_tiles<_Float16>, grid, 256, 0, st, w, in, out, reinterpret_cast<bf16*>(kn),
+                reinterpret_cast<_Float16*>(nk));
+    else if (dtype == GP_BF16 && in % 64 == 0 && out % 64 == 0)
+        klaunch(refresh_bf16_tiles<bf16>, grid, 256, 0, st, w, in, out, reinterpret_cast<bf16*>(kn),
+                reinterpret_cast<bf16*>(nk));
     else if (dtype == GP_BF16)
         klaunch(refresh_kernel<bf16>, grid, 256, 0, st, w, in, out, reinterpret_cast<bf16*>(kn), reinterpret_cast<bf16*>(nk));
     else

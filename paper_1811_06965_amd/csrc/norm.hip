@@ -190,11 +190,16 @@ template <> struct Out4<bf16> {
 
 __device__ __forceinline__ float hsum(f32x4 v) { return (v[0] + v[1]) + (v[2] + v[3]); }
 
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+
+// o16 (optional): the output also in fp16 (the operand of a GEMM that takes
+// fp16 inputs).
 template <typename T, int C4>
 __device__ __forceinline__ void ln_row_v4(const f32x4 (&v)[C4], int lane, long row, int D,
                                           const float* __restrict__ gamma, const float* __restrict__ beta, float eps,
                                           T* __restrict__ out, float* __restrict__ stats,
-                                          unsigned char* __restrict__ lo4, unsigned char* __restrict__ lo_sc) {
+                                          unsigned char* __restrict__ lo4, unsigned char* __restrict__ lo_sc,
+                                          _Float16* __restrict__ o16) {
     float s = 0.f;
 #pragma unroll
     for (int c = 0; c < C4; ++c) s += hsum(v[c]);
@@ -216,6 +221,9 @@ __device__ __forceinline__ void ln_row_v4(const f32x4 (&v)[C4], int lane, long r
         const int i = lane + 64 * c;
         const f32x4 y = g4[i] * ((v[c] - mu) * rstd) + b4[i];
         Out4<T>::store(orow + 4 * i, y);
+        if (o16)
+            *reinterpret_cast<f16x4*>(o16 + row * D + 4 * i) = {(_Float16)y[0], (_Float16)y[1], (_Float16)y[2],
+                                                                (_Float16)y[3]};
         lo[c] = Out4<T>::residual(y);
         amax = fmaxf(amax, fmaxf(fmaxf(fabsf(lo[c][0]), fabsf(lo[c][1])), fmaxf(fabsf(lo[c][2]), fabsf(lo[c][3]))));
     }
@@ -243,7 +251,8 @@ template <typename T, int C4>
 __global__ void __launch_bounds__(256) ln_fwd_v4(const float* __restrict__ x, long rows, int D,
                                                  const float* __restrict__ gamma, const float* __restrict__ beta,
                                                  float eps, T* __restrict__ out, float* __restrict__ stats,
-                                                 unsigned char* __restrict__ lo4, unsigned char* __restrict__ lo_sc) {
+                                                 unsigned char* __restrict__ lo4, unsigned char* __restrict__ lo_sc,
+                                                 _Float16* __restrict__ o16) {
     const int lane = threadIdx.x & 63;
     const long row = (long)blockIdx.x * LN_WAVES + (threadIdx.x >> 6);
     if (row >= rows) return;
@@ -251,7 +260,7 @@ __global__ void __launch_bounds__(256) ln_fwd_v4(const float* __restrict__ x, lo
     f32x4 v[C4];
 #pragma unroll
     for (int c = 0; c < C4; ++c) v[c] = xr[lane + 64 * c];
-    ln_row_v4<T, C4>(v, lane, row, D, gamma, beta, eps, out, stats, lo4, lo_sc);
+    ln_row_v4<T, C4>(v, lane, row, D, gamma, beta, eps, out, stats, lo4, lo_sc, o16);
 }
 
 // The split-K reduce of a residual GEMM fused with the LayerNorm of its
@@ -265,7 +274,8 @@ __global__ void __launch_bounds__(256) ln_fwd_res_v4(const float* __restrict__ w
                                                      bf16* __restrict__ xc, long rows, int D,
                                                      const float* __restrict__ gamma, const float* __restrict__ beta,
                                                      float eps, T* __restrict__ out, float* __restrict__ stats,
-                                                     unsigned char* __restrict__ lo4, unsigned char* __restrict__ lo_sc) {
+                                                     unsigned char* __restrict__ lo4, unsigned char* __restrict__ lo_sc,
+                                                     _Float16* __restrict__ o16) {
     const int lane = threadIdx.x & 63;
     const long row = (long)blockIdx.x * LN_WAVES + (threadIdx.x >> 6);
     if (row >= rows) return;
@@ -286,7 +296,7 @@ __global__ void __launch_bounds__(256) ln_fwd_res_v4(const float* __restrict__ w
         x4[i] = s;
         if (xc) *reinterpret_cast<bf16x4*>(xc + row * D + 4 * i) = {(bf16)s[0], (bf16)s[1], (bf16)s[2], (bf16)s[3]};
     }
-    ln_row_v4<T, C4>(v, lane, row, D, gamma, beta, eps, out, stats, lo4, lo_sc);
+    ln_row_v4<T, C4>(v, lane, row, D, gamma, beta, eps, out, stats, lo4, lo_sc, o16);
 }
 
 template <typename T, int C4>
@@ -396,19 +406,19 @@ __global__ void __launch_bounds__(256) bias_partial_kernel(const T* __restrict__
 
 template <typename T>
 gp_status ln_fwd_t(const float* x, long rows, int D, const float* g, const float* b, float eps, void* out,
-                   float* stats, unsigned char* lo4, unsigned char* lo_sc, hipStream_t st) {
+                   float* stats, unsigned char* lo4, unsigned char* lo_sc, _Float16* o16, hipStream_t st) {
     const int grid = (int)((rows + LN_WAVES - 1) / LN_WAVES);
     T* o = reinterpret_cast<T*>(out);
     if (D % 256 == 0 && D <= 2048) {
         switch (D / 256) {
-        case 1: klaunch(ln_fwd_v4<T, 1>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc); break;
-        case 2: klaunch(ln_fwd_v4<T, 2>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc); break;
-        case 3: klaunch(ln_fwd_v4<T, 3>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc); break;
-        case 4: klaunch(ln_fwd_v4<T, 4>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc); break;
-        case 5: klaunch(ln_fwd_v4<T, 5>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc); break;
-        case 6: klaunch(ln_fwd_v4<T, 6>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc); break;
-        case 7: klaunch(ln_fwd_v4<T, 7>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc); break;
-        default: klaunch(ln_fwd_v4<T, 8>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc); break;
+        case 1: klaunch(ln_fwd_v4<T, 1>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc, o16); break;
+        case 2: klaunch(ln_fwd_v4<T, 2>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc, o16); break;
+        case 3: klaunch(ln_fwd_v4<T, 3>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc, o16); break;
+        case 4: klaunch(ln_fwd_v4<T, 4>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc, o16); break;
+        case 5: klaunch(ln_fwd_v4<T, 5>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc, o16); break;
+        case 6: klaunch(ln_fwd_v4<T, 6>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc, o16); break;
+        case 7: klaunch(ln_fwd_v4<T, 7>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc, o16); break;
+        default: klaunch(ln_fwd_v4<T, 8>, grid, 256, 0, st, x, rows, D, g, b, eps, o, stats, lo4, lo_sc, o16); break;
         }
         GP_LAUNCH_CHECK();
         return GP_OK;
@@ -474,12 +484,16 @@ int layernorm_bwd_blocks(long rows) {
 int bias_grad_blocks(long rows) { return rows < BIAS_BLOCKS ? (int)(rows > 0 ? rows : 1) : BIAS_BLOCKS; }
 
 gp_status layernorm_fwd(int dtype, const float* x, long rows, int D, const float* gamma, const float* beta,
-                        float eps, void* out, float* stats, void* lo4, unsigned char* lo_sc, hipStream_t st) {
+                        float eps, void* out, float* stats, void* lo4, unsigned char* lo_sc, hipStream_t st,
+                        void* out16) {
     unsigned char* l4 = static_cast<unsigned char*>(lo4);
     if (l4 && (dtype != GP_BF16 || D % 64 || !lo_sc))
         return set_error(GP_ERR_UNSUPPORTED, "layernorm: fp4 residuals need bf16 output and d_model % 64 == 0");
-    if (dtype == GP_BF16) return ln_fwd_t<bf16>(x, rows, D, gamma, beta, eps, out, stats, l4, lo_sc, st);
-    return ln_fwd_t<float>(x, rows, D, gamma, beta, eps, out, stats, nullptr, nullptr, st);
+    if (out16 && (dtype != GP_BF16 || D % 256 || D > 2048))
+        return set_error(GP_ERR_UNSUPPORTED, "layernorm: an fp16 copy needs bf16 output and d_model % 256 == 0");
+    _Float16* o16 = static_cast<_Float16*>(out16);
+    if (dtype == GP_BF16) return ln_fwd_t<bf16>(x, rows, D, gamma, beta, eps, out, stats, l4, lo_sc, o16, st);
+    return ln_fwd_t<float>(x, rows, D, gamma, beta, eps, out, stats, nullptr, nullptr, nullptr, st);
 }
 
 bool layernorm_fwd_res_ok(int dtype, int D, const void* ws, const float* bias, const float* res, const float* xo,
@@ -491,7 +505,7 @@ bool layernorm_fwd_res_ok(int dtype, int D, const void* ws, const float* bias, c
 
 gp_status layernorm_fwd_res(int dtype, const float* ws, int splits, long plane, const float* bias, const float* res,
                             float* xo, void* xc, long rows, int D, const float* gamma, const float* beta, float eps,
-                            void* out, float* stats, void* lo4, unsigned char* lo_sc, hipStream_t st) {
+                            void* out, float* stats, void* lo4, unsigned char* lo_sc, hipStream_t st, void* out16) {
     if (!layernorm_fwd_res_ok(dtype, D, ws, bias, res, xo, xc) || splits < 1 || plane % 4 || plane < rows * D)
         return set_error(GP_ERR_UNSUPPORTED, "layernorm with split-K reduce: bf16, d_model % 256 == 0 (<= 2048), "
                                              "aligned rows");
@@ -500,8 +514,9 @@ gp_status layernorm_fwd_res(int dtype, const float* ws, int splits, long plane, 
     const int grid = (int)((rows + LN_WAVES - 1) / LN_WAVES);
     bf16* o = reinterpret_cast<bf16*>(out);
     bf16* c = reinterpret_cast<bf16*>(xc);
+    _Float16* o16 = static_cast<_Float16*>(out16);
 #define GP_LNR(C4) klaunch(ln_fwd_res_v4<bf16, C4>, grid, 256, 0, st, ws, splits, plane, bias, res, xo, c, rows, D, \
-                           gamma, beta, eps, o, stats, l4, lo_sc)
+                           gamma, beta, eps, o, stats, l4, lo_sc, o16)
     switch (D / 256) {
     case 1: GP_LNR(1); break;
     case 2: GP_LNR(2); break;

@@ -82,6 +82,7 @@ struct LayerWs {
     float* stf = nullptr;
     void *v = nullptr, *a = nullptr;
     unsigned char *v4 = nullptr, *v4s = nullptr;  // fp4 rounding residuals of v and their row scales (bf16)
+    void* v16 = nullptr;  // v in fp16 (Linear::f16)
 };
 
 constexpr int ELT_RING = 10;      // bf16 residual-gradient buffers (see layer_backward)
@@ -302,6 +303,7 @@ void plan_workspace(gp_partition* p, Arena& a) {
     const long lse_n = (long)g.n * d.H * g.S;
     const size_t e = p->esz;
     const bool dec = g.kind == GP_DECODER_CROSS;
+    const bool f16 = !p->plan.layers.empty() && p->plan.layers[0].ffn1.f16;
     p->xs.assign(p->nsets, std::vector<float*>(d.L + 1, nullptr));
     p->lw.assign(p->nsets, std::vector<LayerWs>(d.L, LayerWs{}));
     p->slot_span.assign(p->nsets, std::vector<Span>{});
@@ -347,7 +349,9 @@ void plan_workspace(gp_partition* p, Arena& a) {
         }
         take1(&LayerWs::stf, 2 * T, 4);
         take1(&LayerWs::v, T * D, e);
-        if (p->g.dtype == GP_BF16) {
+        if (f16) {
+            take1(&LayerWs::v16, T * D, 2);
+        } else if (p->g.dtype == GP_BF16) {
             take1(&LayerWs::v4, T * D / 2, 1);
             take1(&LayerWs::v4s, T, 1);
         }
@@ -387,7 +391,9 @@ void plan_workspace(gp_partition* p, Arena& a) {
             }
             take(&LayerWs::stf, 2 * T, 4);
             take(&LayerWs::v, T * D, e);
-            if (p->g.dtype == GP_BF16) {  // see Linear::split
+            if (f16) {  // see Linear::f16
+                take(&LayerWs::v16, T * D, 2);
+            } else if (p->g.dtype == GP_BF16) {  // see Linear::split
                 take(&LayerWs::v4, T * D / 2, 1);
                 take(&LayerWs::v4s, T, 1);
             }
@@ -616,7 +622,8 @@ gp_status flush_pending(const Ctx& c) {
 }
 
 gp_status timed_ln_fwd(const Ctx& c, const float* x, long rows, int D, const float* gamma, const float* beta,
-                       float eps, void* out, float* stats, unsigned char* lo4 = nullptr, unsigned char* lo_sc = nullptr) {
+                       float eps, void* out, float* stats, unsigned char* lo4 = nullptr, unsigned char* lo_sc = nullptr,
+                       void* out16 = nullptr) {
     if (c.pend && c.pend->splits > 1) {
         const GemmArgs& g = c.pend->g;
         if (c.pend->epi == EPI_RES_F32 && g.C == x && g.M == rows && g.N == D) {
@@ -624,19 +631,22 @@ gp_status timed_ln_fwd(const Ctx& c, const float* x, long rows, int D, const flo
             const int sp = c.pend->splits;
             c.pend->splits = 0;
             const double plane = (double)rows * D;
-            const double by = plane * (4.0 * sp + 4.0 + 4.0 + (g.C2 ? 2.0 : 0.0) + c.p->esz + (lo4 ? 0.5 : 0.0)) +
-                              rows * 8.0 + D * 12.0;
+            const double by =
+                plane * (4.0 * sp + 4.0 + 4.0 + (g.C2 ? 2.0 : 0.0) + c.p->esz + (lo4 ? 0.5 : 0.0) + (out16 ? 2.0 : 0.0)) +
+                rows * 8.0 + D * 12.0;
             return timed(c, GP_K_LN_FWD, 0.0, by, [&] {
                 return layernorm_fwd_res(c.dt, g.ws, sp, (long)rows * D, g.bias, static_cast<const float*>(g.aux),
                                          static_cast<float*>(g.C), g.C2, rows, D, gamma, beta, eps, out, stats, lo4,
-                                         lo_sc, c.st);
+                                         lo_sc, c.st, out16);
             });
         }
         GP_TRY(flush_pending(c));
     }
-    const double by = (double)rows * D * (4.0 + c.p->esz + (lo4 ? 0.5 : 0.0)) + rows * 8.0 + D * 8.0;
-    return timed(c, GP_K_LN_FWD, 0.0, by,
-                 [&] { return layernorm_fwd(c.dt, x, rows, D, gamma, beta, eps, out, stats, lo4, lo_sc, c.st); });
+    const double by = (double)rows * D * (4.0 + c.p->esz + (lo4 ? 0.5 : 0.0) + (out16 ? 2.0 : 0.0)) + rows * 8.0 +
+                      D * 8.0;
+    return timed(c, GP_K_LN_FWD, 0.0, by, [&] {
+        return layernorm_fwd(c.dt, x, rows, D, gamma, beta, eps, out, stats, lo4, lo_sc, c.st, out16);
+    });
 }
 
 // Y = A W + b with an epilogue; A [M, K] k-contiguous, W^T working copy [N, K].
@@ -673,6 +683,7 @@ gp_status linear_fwd(const Ctx& c, const Linear& L, const void* A, long M, void*
     g.ws_elems = c.p->bw.splitk_elems;
     g.force_cfg = c.p->gemm_tile;
     g.force_splits = c.p->gemm_splits;
+    g.f16 = L.f16 ? 1 : 0;  // A is then the fp16 copy of the input, nk holds fp16
     // a pass over a pair's rows takes one micro-batch's tile and split choice
     // (same rounding as two single passes; the recompute workspace holds the
     // pair's partials)
@@ -885,11 +896,11 @@ GP_TRY(timed_attention(c, GP_K_ATTN_FWD, a, false));
     // first pass and in the recompute alike, so that the recompute reproduces
     // the first pass bit for bit (the backward differentiates the very F_k
     // whose output left the partition).
-    const bool s4 = P.ffn1.split;
+    const bool s4 = P.ffn1.split, h16 = P.ffn1.f16;
     GP_TRY(timed_ln_fwd(c, xf, T, (int)D, p->master + nf.g, p->master + nf.b, eps, w.v, w.stf, s4 ? w.v4 : nullptr,
-                        s4 ? w.v4s : nullptr));
-    GP_TRY(linear_fwd(c, P.ffn1, w.v, T, w.a, p->d.F, EPI_STORE, 1, nullptr, nullptr, s4 ? w.v4 : nullptr,
-                      s4 ? w.v4s : nullptr));
+                        s4 ? w.v4s : nullptr, h16 ? w.v16 : nullptr));
+    GP_TRY(linear_fwd(c, P.ffn1, h16 ? w.v16 : w.v, T, w.a, p->d.F, EPI_STORE, 1, nullptr, nullptr,
+                      s4 ? w.v4 : nullptr, s4 ? w.v4s : nullptr));
     // the next layer begins with the LayerNorm of x_out
     GP_TRY(linear_fwd(c, P.ffn2, w.a, T, x_out, D, EPI_RES_F32, 0, xf, y_out, nullptr, nullptr, l + 1 < p->d.L));
     return GP_OK;
@@ -1099,7 +1110,7 @@ gp_status upload_param_block(gp_partition* p, const ParamRef& r, const float* ho
     if (r.lin) {
         GP_TRY(refresh_linear(p->g.dtype, p->master + r.lin->w, r.lin->in, r.lin->out, p->W(r.lin->kn),
                               p->W(r.lin->nk), r.lin->split ? p->W(r.lin->q4) : nullptr,
-                              r.lin->split ? p->W(r.lin->q4s) : nullptr, nullptr));
+                              r.lin->split ? p->W(r.lin->q4s) : nullptr, nullptr, r.lin->f16));
         GP_HIP(hipDeviceSynchronize());
     }
     return GP_OK;
@@ -1238,6 +1249,7 @@ void plan_partition(gp_partition* p, const gp_config* cfg) {
     if (const char* e = std::getenv("GP_GEMM_TILE")) p->gemm_tile = std::atoi(e);
     if (const char* e = std::getenv("GP_GEMM_SPLITS")) p->gemm_splits = std::atoi(e);
     if (const char* e = std::getenv("GP_FFN_FP4")) g.ffn_fp4 = std::atoi(e) != 0;
+    if (const char* e = std::getenv("GP_FFN_F16")) g.ffn_f16 = std::atoi(e) != 0;
     p->plan = plan_params(p->d, g);
     Arena measure;
     plan_workspace(p, measure);
@@ -1346,7 +1358,7 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
     }
     for (const Linear* l : p->plan.linears()) {
         s = refresh_linear(g.dtype, p->master + l->w, l->in, l->out, p->W(l->kn), p->W(l->nk),
-                           l->split ? p->W(l->q4) : nullptr, l->split ? p->W(l->q4s) : nullptr, nullptr);
+                           l->split ? p->W(l->q4) : nullptr, l->split ? p->W(l->q4s) : nullptr, nullptr, l->f16);
         if (s != GP_OK) {
             free_all(p);
             return s;
@@ -1779,7 +1791,8 @@ gp_status gp_accumulate_and_step(gp_partition* p, float lr, double* loss_out, gp
         for (const Linear* l : p->plan.linears())
             GP_TRY(update_refresh_linear(p->master + l->w, p->grads + l->w, rms ? p->opt_ms + l->w : nullptr, lr,
                                          p->g.rms_decay, p->g.rms_eps, l->in, l->out, p->W(l->kn), p->W(l->nk),
-                                         l->split ? p->W(l->q4) : nullptr, l->split ? p->W(l->q4s) : nullptr, st));
+                                         l->split ? p->W(l->q4) : nullptr, l->split ? p->W(l->q4s) : nullptr, st,
+                                         l->f16));
         GP_TRY(update_ranges(p->master, p->grads, rms ? p->opt_ms : nullptr, lr, p->g.rms_decay, p->g.rms_eps,
                              p->upd_ranges, p->n_upd_ranges, st));
     } else {
@@ -1790,7 +1803,7 @@ gp_status gp_accumulate_and_step(gp_partition* p, float lr, double* loss_out, gp
             GP_TRY(sgd_update(p->master, p->grads, lr, (long)p->plan.n32, st));
         for (const Linear* l : p->plan.linears())
             GP_TRY(refresh_linear(dt, p->master + l->w, l->in, l->out, p->W(l->kn), p->W(l->nk),
-                                  l->split ? p->W(l->q4) : nullptr, l->split ? p->W(l->q4s) : nullptr, st));
+                                  l->split ? p->W(l->q4) : nullptr, l->split ? p->W(l->q4s) : nullptr, st, l->f16));
     }
     if (loss_out) {
         double v = 0.0;

@@ -36,6 +36,7 @@ struct Geometry {
     float rms_decay = 0.f, rms_eps = 0.f;
     float logit_clip = 0.f;
     int ffn_fp4 = 1;  // bf16: fp4 correction of the feed-forward input projection (see Linear::split)
+    int ffn_f16 = 1;  // bf16: that projection with fp16 operands instead, where the widths allow (Linear::f16)
     long long T() const { return (long long)n * S; }     // token rows of one micro-batch
     long long Tm() const { return (long long)n * Smem; } // memory rows of one micro-batch
 };
@@ -118,6 +119,11 @@ struct Linear {
     // so that the pre-activations, whose signs set the ReLU mask the backward
     // uses, carry almost none of the rounding error of its bf16 input
     bool split = false;
+    // bf16 feed-forward input projection with fp16 operands instead: the
+    // LayerNorm output and W^T carry three more mantissa bits into the
+    // pre-activations at the bf16 MFMA rate (nk holds fp16; kn stays bf16 for
+    // the input gradient, and the bf16 LayerNorm output for the weight gradient)
+    bool f16 = false;
     bool present = false;
 };
 struct Norm {
@@ -200,7 +206,9 @@ inline ParamPlan plan_params(const Dims& d, const Geometry& g) {
         lin(l.qkv, d.D, 3 * d.D, GP_K_QKV_FWD);
         lin(l.o, d.D, d.D, GP_K_O_FWD);
         norm(l.ln2, d.D);
-        lin(l.ffn1, d.D, d.F, GP_K_FFN1_FWD, g.dtype == GP_BF16 && g.ffn_fp4);
+        const bool f16 = g.dtype == GP_BF16 && g.ffn_f16 && d.D % 256 == 0 && d.D <= 2048 && d.F % 64 == 0;
+        lin(l.ffn1, d.D, d.F, GP_K_FFN1_FWD, g.dtype == GP_BF16 && g.ffn_fp4 && !f16);
+        l.ffn1.f16 = f16;
         lin(l.ffn2, d.F, d.D, GP_K_FFN2_FWD);
         if (dec) {
             lin(l.xq, d.D, d.D, GP_K_XQ_FWD);

@@ -182,8 +182,29 @@ def test_bf16_fp4_correction_reduces_gradient_error(monkeypatch):
     are closer to the oracle with it than without it (same seeded case)."""
     cfg = SHARED_DEC
     errs = {}
+    monkeypatch.setenv("GP_FFN_F16", "0")  # d_model 128 takes no fp16 operands anyway
     for on in ("1", "0"):
         monkeypatch.setenv("GP_FFN_FP4", on)
+        case, ref, res = _run(cfg, 5)
+        gl = res["grads"][0]
+        errs[on] = np.mean([1.0 - cosine(gl[l][k], ref["grads"][l][k])
+                            for l in range(cfg.layers) for k in ("w1", "b1", "ln3_g", "ln3_b")])
+        if on == "1":
+            _check(cfg, ref, res, 2e-2, "cos", 0.999)
+    assert errs["1"] < 0.85 * errs["0"], errs
+
+
+def test_bf16_fp16_operands_reduce_gradient_error(monkeypatch):
+    """The feed-forward input projection with fp16 operands (the LayerNorm
+    output and W1 with three more mantissa bits than bf16, at the bf16 MFMA
+    rate) moves the pre-activations, and so the ReLU mask, towards the fp64
+    network's: that block's gradients are closer to the oracle than with bf16
+    operands (same seeded case), and the whole step meets the bf16 bars."""
+    cfg = SHARED_DEC.with_(name="shared_dec256", d_model=256, heads=4)
+    errs = {}
+    monkeypatch.setenv("GP_FFN_FP4", "0")
+    for on in ("1", "0"):
+        monkeypatch.setenv("GP_FFN_F16", on)
         case, ref, res = _run(cfg, 5)
         gl = res["grads"][0]
         errs[on] = np.mean([1.0 - cosine(gl[l][k], ref["grads"][l][k])
@@ -513,18 +534,26 @@ def test_split_reduce_fused_into_layernorm_is_bitwise_identical(tile, splits, mo
                 assert np.array_equal(a[k], b[k]), (l, k)
 
 
-@pytest.mark.parametrize("cfg,fp4", [(TINY, "1"), (ENC512_SMALL, "0"), (ENC512_SMALL, "1"), (RAGGED_BF16, "1"),
-                                     (DEC_SMALL_BF16, "0"), (DEC_SMALL_BF16, "1")],
-                         ids=["tiny_fp32", "enc512_small_fp4off", "enc512_small", "ragged_bf16", "dec_small_fp4off",
-                              "dec_small"])
-def test_recompute_reproduces_first_pass_bitwise(cfg, fp4, monkeypatch):
+# feed-forward input projection: fp16 operands (default), bf16 with the fp4
+# correction, plain bf16
+FFN_MODES = {"f16": ("1", "0"), "fp4": ("0", "1"), "bf16": ("0", "0")}
+
+
+@pytest.mark.parametrize("cfg,mode", [(TINY, "f16"), (ENC512_SMALL, "bf16"), (ENC512_SMALL, "fp4"),
+                                      (ENC512_SMALL, "f16"), (RAGGED_BF16, "f16"), (DEC_SMALL_BF16, "bf16"),
+                                      (DEC_SMALL_BF16, "fp4"), (DEC_SMALL_BF16, "f16")],
+                         ids=["tiny_fp32", "enc512_small_bf16", "enc512_small_fp4", "enc512_small_f16",
+                              "ragged_bf16_f16", "dec_small_bf16", "dec_small_fp4", "dec_small_f16"])
+def test_recompute_reproduces_first_pass_bitwise(cfg, mode, monkeypatch):
     """Section 2.3: the backward pass recomputes the same F_k.  The partition
     output that each backward call re-materialises (gp_recomputed_output)
     equals, bit for bit, the y its forward call emitted -- in fp32, and in bf16
-    with and without the fp4 correction of the feed-forward input (which runs
-    in both passes), with the recompute-ahead and early-recompute streams on."""
+    with each form of the feed-forward input projection (fp16 operands, bf16
+    with the fp4 correction, plain bf16; each runs in both passes), with the
+    recompute-ahead and early-recompute streams on."""
     from paper_1811_06965_amd.runtime import Partition
-    monkeypatch.setenv("GP_FFN_FP4", fp4)
+    monkeypatch.setenv("GP_FFN_F16", FFN_MODES[mode][0])
+    monkeypatch.setenv("GP_FFN_FP4", FFN_MODES[mode][1])
     case = synth.make_case(cfg, 13, perturb=True)
     with Partition(cfg) as part:
         part.load_params(case["layers"], case["head"])

@@ -82,7 +82,6 @@ struct LayerWs {
     float* stf = nullptr;
     void *v = nullptr, *a = nullptr;
     unsigned char *v4 = nullptr, *v4s = nullptr;  // fp4 rounding residuals of v and their row scales (bf16)
-    void* v16 = nullptr;  // v in fp16 (Linear::f16)
 };
 
 constexpr int ELT_RING = 10;      // bf16 residual-gradient buffers (see layer_backward)
@@ -103,6 +102,10 @@ struct BwdWs {
     float* splitk = nullptr;   // split-K partial tiles (caller's stream)
     float* splitk_side = nullptr;  // split-K partial tiles of the weight-gradient stream
     float* splitk_remat = nullptr; // split-K partial tiles of the recompute-ahead stream
+    // the feed-forward input in fp16 (Linear::f16): read only by the GEMM right
+    // after the LayerNorm that writes it, so one buffer per stream that runs
+    // forward passes (rows of a recompute unit), not one per layer and set
+    void *v16_main = nullptr, *v16_remat = nullptr;
     long splitk_elems = 0;
     // loss head
     float* sth = nullptr;
@@ -349,9 +352,7 @@ void plan_workspace(gp_partition* p, Arena& a) {
         }
         take1(&LayerWs::stf, 2 * T, 4);
         take1(&LayerWs::v, T * D, e);
-        if (f16) {
-            take1(&LayerWs::v16, T * D, 2);
-        } else if (p->g.dtype == GP_BF16) {
+        if (!f16 && p->g.dtype == GP_BF16) {
             take1(&LayerWs::v4, T * D / 2, 1);
             take1(&LayerWs::v4s, T, 1);
         }
@@ -391,9 +392,7 @@ void plan_workspace(gp_partition* p, Arena& a) {
             }
             take(&LayerWs::stf, 2 * T, 4);
             take(&LayerWs::v, T * D, e);
-            if (f16) {  // see Linear::f16
-                take(&LayerWs::v16, T * D, 2);
-            } else if (p->g.dtype == GP_BF16) {  // see Linear::split
+            if (!f16 && p->g.dtype == GP_BF16) {  // see Linear::split
                 take(&LayerWs::v4, T * D / 2, 1);
                 take(&LayerWs::v4s, T, 1);
             }
@@ -471,6 +470,11 @@ void plan_workspace(gp_partition* p, Arena& a) {
         p->splitk_span[2] = Span{a.mark(), rm * sizeof(float)};
         b.splitk_remat = a.take<float>(rm);
     }
+    if (f16) {
+        const size_t n16 = (size_t)p->remat_group * T * D;
+        b.v16_main = a.take_elt(n16, 2);
+        if (p->ahead()) b.v16_remat = a.take_elt(n16, 2);
+    }
     size_t lp = (size_t)loss_blocks();
     if (g.loss == GP_LOSS_XENT_LS && (size_t)xent_partials(T) > lp) lp = xent_partials(T);
     p->loss_span = Span{a.mark(), lp * sizeof(double)};
@@ -533,6 +537,7 @@ struct Ctx {
     bool last = false;          // the mini-batch's last backward micro-batch
     PendingRes* pend = nullptr; // forward passes: a deferred split-K reduce
     int nseq = 0;               // sequences of a forward pass (0: one micro-batch; 2n: a pair's recompute)
+    void* v16 = nullptr;        // the feed-forward input in fp16 for passes on st (Linear::f16)
 };
 
 enum class Lane { Main, Side, Remat };
@@ -540,6 +545,7 @@ enum class Lane { Main, Side, Remat };
 Ctx make_ctx(gp_partition* p, hipStream_t st, Lane lane = Lane::Main) {
     Ctx c{p, st, p->g.dtype};
     c.ws = lane == Lane::Side ? p->bw.splitk_side : lane == Lane::Remat ? p->bw.splitk_remat : p->bw.splitk;
+    c.v16 = lane == Lane::Side ? nullptr : lane == Lane::Remat ? p->bw.v16_remat : p->bw.v16_main;
     return c;
 }
 
@@ -897,9 +903,10 @@ GP_TRY(timed_attention(c, GP_K_ATTN_FWD, a, false));
     // the first pass bit for bit (the backward differentiates the very F_k
     // whose output left the partition).
     const bool s4 = P.ffn1.split, h16 = P.ffn1.f16;
+    if (h16 && !c.v16) return set_error(GP_ERR_INVALID_ARG, "fp16 feed-forward input buffer missing on this stream");
     GP_TRY(timed_ln_fwd(c, xf, T, (int)D, p->master + nf.g, p->master + nf.b, eps, w.v, w.stf, s4 ? w.v4 : nullptr,
-                        s4 ? w.v4s : nullptr, h16 ? w.v16 : nullptr));
-    GP_TRY(linear_fwd(c, P.ffn1, h16 ? w.v16 : w.v, T, w.a, p->d.F, EPI_STORE, 1, nullptr, nullptr,
+                        s4 ? w.v4s : nullptr, h16 ? c.v16 : nullptr));
+    GP_TRY(linear_fwd(c, P.ffn1, h16 ? c.v16 : w.v, T, w.a, p->d.F, EPI_STORE, 1, nullptr, nullptr,
                       s4 ? w.v4 : nullptr, s4 ? w.v4s : nullptr));
     // the next layer begins with the LayerNorm of x_out
     GP_TRY(linear_fwd(c, P.ffn2, w.a, T, x_out, D, EPI_RES_F32, 0, xf, y_out, nullptr, nullptr, l + 1 < p->d.L));

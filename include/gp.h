@@ -34,6 +34,10 @@
  *  - Calls on one partition are not thread-safe; use one partition per host
  *    thread.  Work is ordered by the stream passed in; device faults surface
  *    as GP_ERR_HIP at the next call that synchronises.
+ *  - Forward calls may be given different streams (see
+ *    gp_forward_microbatch); the library orders what they share.  The other
+ *    calls of a mini-batch take streams the caller has ordered one after the
+ *    other (normally one stream).
  */
 #ifndef GP_H
 #define GP_H
@@ -207,6 +211,14 @@ gp_status gp_param_count(gp_partition* p, size_t* count);
  *   y   : device [n, S, D] partition dtype, the partition output F_k(x);
  *         may be NULL (loss partitions need not emit it).
  * Every intermediate of the layers is discarded; only the stash is kept.
+ * Streams: consecutive micro-batches' forwards may be issued on two streams
+ * and then run side by side.  The library keeps two first-pass workspaces,
+ * for even and odd mb, and orders each forward after the previous one in its
+ * workspace and after the last gp_accumulate_and_step (the weights it reads),
+ * and the mini-batch's first backward after all M forwards, whatever streams
+ * they ran on.  y is written on the call's stream; a consumer on another
+ * stream waits for that stream.  Under stream capture only waits within the
+ * same capture are made.
  * GP_ERR_STATE: not configured, mb out of order, or backward already begun.
  * GP_ERR_INVALID_ARG: x (or mem for the decoder) NULL, mb out of range.
  */
@@ -222,7 +234,9 @@ gp_status gp_forward_microbatch(gp_partition* p, int mb, const void* x, const vo
  * held until the process ends) instead of the partition's workspace; it does
  * not start the early recompute of the last micro-batch (that backward then
  * recomputes on its own stream).  Every call on a device shares the array:
- * calls that overlap on one device (two streams, two host threads) race.
+ * calls that overlap on one device (two streams, two host threads) race; on
+ * one partition each of these calls waits for the previous forward in both
+ * first-pass workspaces, so they never overlap each other.
  * GP_ERR_UNSUPPORTED: the partition's forward needs more split-K scratch
  *   than the array holds (the message states both sizes).
  * GP_ERR_HIP: the array has no address on this device.

@@ -131,6 +131,27 @@ struct DyStore {
     void* dxkv = nullptr;   // decoder: dY of the cross-attention key/value weight gradient (memory rows)
 };
 
+// The working memory of a first forward pass (re-materialisation off: one
+// layer slot and two ping-pong residual buffers, nothing kept).  There are two,
+// taken by micro-batch parity, so that consecutive forwards issued on two
+// streams run side by side.  The even one uses the split-K partials and the
+// fp16 buffer of the caller's stream (those of the backward, which starts after
+// every forward); the odd one has its own.
+struct FirstPass {
+    LayerWs w;
+    float* xs[2] = {};
+    std::vector<Span> span;  // the layer slot and the residual buffers
+    float* splitk = nullptr; // odd slot: split-K partials (the most one forward writes)
+    void* v16 = nullptr;     // odd slot: the feed-forward input in fp16 (Linear::f16)
+    Span splitk_span;
+    // The last forward in this slot: its stream, events recorded on it after
+    // the boundary input was stashed and at its end (from the event ring), and
+    // the capture its recordings belong to (0: none).
+    hipStream_t stream = nullptr;
+    hipEvent_t stashed = nullptr, done = nullptr;
+    unsigned long long capture = 0;
+};
+
 } // namespace gp
 
 using namespace gp;
@@ -198,10 +219,16 @@ struct gp_partition {
     // micro-batches re-materialised together in one pass over their rows
     // (1, or 2 within a group of sets)
     int remat_group = 1;
-    // the first pass's own layer slot and ping-pong residual buffers (no set's)
-    LayerWs fp;
-    float* fp_xs[2] = {};
-    std::vector<Span> fp_span;
+    // the first passes' own working memory (no set's), by micro-batch parity
+    // (one when M = 1 or GP_FWD_LANES=1)
+    FirstPass fpass[2];
+    int fp_lanes = 1;
+    int lane_of(int m) const { return fp_lanes > 1 ? m & 1 : 0; }
+    // the last update's stream and an event recorded at its end, with its
+    // capture: a forward issued on another stream waits for it
+    hipStream_t tail_stream = nullptr;
+    hipEvent_t tail_done = nullptr;
+    unsigned long long tail_capture = 0;
     bool dw_started = false;   // a weight-gradient GEMM of this mini-batch was launched
     float* opt_ms = nullptr;  // RMSProp: running mean square of every gradient [n32]
     // bf16 partitions whose linears are whole 64 x 64 tiles update each
@@ -243,6 +270,7 @@ struct gp_partition {
     // run many calls ahead of the device).
     std::vector<hipEvent_t> evring;
     size_t ev_next = 0;
+    bool events() const { return !evring.empty(); }
     hipEvent_t next_event() {
         hipEvent_t e = evring[ev_next];
         ev_next = (ev_next + 1) % evring.size();
@@ -299,6 +327,8 @@ struct gp_partition {
 namespace {
 
 // Carve the workspace; with a.base == nullptr only measures it.
+long forward_workspace_need(const gp_partition* p);
+
 void plan_workspace(gp_partition* p, Arena& a) {
     const Dims& d = p->d;
     const Geometry& g = p->g;
@@ -325,15 +355,18 @@ void plan_workspace(gp_partition* p, Arena& a) {
             }
         }
     }
-    // the first pass's slot: one layer of one micro-batch, and two residuals
-    p->fp = LayerWs{};
-    p->fp_span.clear();
-    {
+    // the first passes' slots: one layer of one micro-batch, and two residuals
+    for (int ln = 0; ln < 2; ++ln) {
+        FirstPass& f = p->fpass[ln];
+        f.w = LayerWs{};
+        f.xs[0] = f.xs[1] = nullptr;
+        f.span.clear();
+        if (ln >= p->fp_lanes) continue;
         auto take1 = [&](auto LayerWs::*field, long count, size_t esz) {
             const size_t off = a.mark();
-            p->fp.*field = reinterpret_cast<typename std::remove_reference<decltype(p->fp.*field)>::type>(
+            f.w.*field = reinterpret_cast<typename std::remove_reference<decltype(f.w.*field)>::type>(
                 a.take_elt((size_t)count, esz));
-            p->fp_span.push_back(Span{off, (size_t)count * esz});
+            f.span.push_back(Span{off, (size_t)count * esz});
         };
         take1(&LayerWs::st1, 2 * T, 4);
         take1(&LayerWs::u, T * D, e);
@@ -357,10 +390,10 @@ void plan_workspace(gp_partition* p, Arena& a) {
             take1(&LayerWs::v4s, T, 1);
         }
         take1(&LayerWs::a, T * F, e);
-        for (float*& x : p->fp_xs) {
+        for (float*& x : f.xs) {
             const size_t off = a.mark();
             x = a.take<float>((size_t)T * D);
-            p->fp_span.push_back(Span{off, (size_t)T * D * 4});
+            f.span.push_back(Span{off, (size_t)T * D * 4});
         }
     }
     for (int g0 = 0; g0 < p->nsets; g0 += G) {
@@ -475,6 +508,18 @@ void plan_workspace(gp_partition* p, Arena& a) {
         b.v16_main = a.take_elt(n16, 2);
         if (p->ahead()) b.v16_remat = a.take_elt(n16, 2);
     }
+    // the odd first-pass slot's own partials and fp16 buffer (one micro-batch)
+    for (int ln = 1; ln < 2; ++ln) {
+        FirstPass& f = p->fpass[ln];
+        f.splitk = nullptr;
+        f.v16 = nullptr;
+        f.splitk_span = Span{};
+        if (ln >= p->fp_lanes) continue;
+        const size_t need = (size_t)std::max<long>(1, forward_workspace_need(p));
+        f.splitk_span = Span{a.mark(), need * sizeof(float)};
+        f.splitk = a.take<float>(need);
+        if (f16) f.v16 = a.take_elt((size_t)T * D, 2);
+    }
     size_t lp = (size_t)loss_blocks();
     if (g.loss == GP_LOSS_XENT_LS && (size_t)xent_partials(T) > lp) lp = xent_partials(T);
     p->loss_span = Span{a.mark(), lp * sizeof(double)};
@@ -499,17 +544,17 @@ gp_status poison_span(const gp_partition* p, const Span& sp, hipStream_t st) {
     return poison_fill(p->ws + sp.off, sp.bytes, st);
 }
 
-// GP_POISON: a whole workspace set (residual stream and every layer slot),
-// before a pass that rewrites all of it.
-// GP_POISON: the first pass's layer slot and residual buffers.
-gp_status poison_first_pass_slot(const gp_partition* p, hipStream_t st) {
+// GP_POISON: a first-pass slot's layer slot and residual buffers.
+gp_status poison_first_pass_slot(const gp_partition* p, int lane, hipStream_t st) {
     if (!p->poison) return GP_OK;
     gp_status s = GP_OK;
-    for (const Span& sp : p->fp_span)
+    for (const Span& sp : p->fpass[lane].span)
         if (s == GP_OK) s = poison_span(p, sp, st);
     return s;
 }
 
+// GP_POISON: a whole workspace set (residual stream and every layer slot),
+// before a pass that rewrites all of it.
 gp_status poison_set(const gp_partition* p, int set, hipStream_t st) {
     if (!p->poison) return GP_OK;
     gp_status s = GP_OK;
@@ -538,6 +583,7 @@ struct Ctx {
     PendingRes* pend = nullptr; // forward passes: a deferred split-K reduce
     int nseq = 0;               // sequences of a forward pass (0: one micro-batch; 2n: a pair's recompute)
     void* v16 = nullptr;        // the feed-forward input in fp16 for passes on st (Linear::f16)
+    int lane = 0;               // first forward passes: the slot (FirstPass) they run in
 };
 
 enum class Lane { Main, Side, Remat };
@@ -926,7 +972,8 @@ gp_status partition_forward(const Ctx& c, int m, bool keep, const void* x, const
     const int ns = c.nseq ? c.nseq : p->g.n;
     const long T = (long)ns * p->g.S, Tm = (long)ns * p->g.Smem, D = p->d.D;
     const int L = p->d.L;
-    float* x0 = keep ? p->xs[set][0] : p->fp_xs[0];
+    FirstPass& f = p->fpass[c.lane];
+    float* x0 = keep ? p->xs[set][0] : f.xs[0];
     if (x) {
         if (!skip_intake) {
             GP_TRY(intake(c.dt, x, p->stash_x_mb(m), x0, T * D, c.st));
@@ -940,9 +987,9 @@ gp_status partition_forward(const Ctx& c, int m, bool keep, const void* x, const
     Ctx cf = c;
     cf.pend = &pend;
     for (int l = 0; l < L; ++l) {
-        LayerWs& w = keep ? p->lw[set][l] : p->fp;
-        const float* xi = keep ? p->xs[set][l] : p->fp_xs[l & 1];
-        float* xo = keep ? p->xs[set][l + 1] : p->fp_xs[(l + 1) & 1];
+        LayerWs& w = keep ? p->lw[set][l] : f.w;
+        const float* xi = keep ? p->xs[set][l] : f.xs[l & 1];
+        float* xo = keep ? p->xs[set][l + 1] : f.xs[(l + 1) & 1];
         GP_TRY(layer_forward(cf, l, w, xi, xo, mem_m, l == L - 1 ? y : nullptr));
     }
     return flush_pending(cf);
@@ -970,6 +1017,63 @@ gp_status remat_pass(const Ctx& c, int lo, int cnt) {
     Ctx cr = c;
     cr.nseq = cnt * p->g.n;
     return partition_forward(cr, lo, true, nullptr, nullptr, nullptr, set);
+}
+
+// The capture a stream is recording into (0: none).
+unsigned long long capture_of(hipStream_t st) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    unsigned long long id = 0;
+    if (hipStreamGetCaptureInfo(st, &cs, &id) != hipSuccess) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    return cs == hipStreamCaptureStatusActive ? id : 0;
+}
+
+// Make st wait for an event an earlier call recorded on stream `from`, unless
+// there is none, it was st itself (stream order covers it), or the two belong
+// to different captures (a graph is ordered by its own edges, and a capture
+// cannot wait on work outside it).
+gp_status wait_recorded(hipStream_t st, hipStream_t from, hipEvent_t ev, unsigned long long cap) {
+    if (!ev || from == st || cap != capture_of(st)) return GP_OK;
+    GP_HIP(hipStreamWaitEvent(st, ev, 0));
+    return GP_OK;
+}
+
+// Context of a first forward pass in slot `lane`: the odd slot has its own
+// split-K partials and fp16 buffer.
+Ctx first_pass_ctx(gp_partition* p, hipStream_t st, int lane) {
+    Ctx c = make_ctx(p, st);
+    c.lane = lane;
+    if (lane) {
+        c.ws = p->fpass[lane].splitk;
+        c.v16 = p->fpass[lane].v16;
+    }
+    return c;
+}
+
+// Order a first forward pass on c.st after the previous forward in its slot
+// (and, with `both`, in the other slot) and after the last update, whose
+// weights it reads and whose mini-batch's backward used the even slot's
+// partials.  Calls on one stream are ordered by the stream already.
+gp_status order_first_pass(gp_partition* p, const Ctx& c, bool both) {
+    for (int ln = 0; ln < p->fp_lanes; ++ln) {
+        if (ln != c.lane && !both) continue;
+        const FirstPass& f = p->fpass[ln];
+        GP_TRY(wait_recorded(c.st, f.stream, f.done, f.capture));
+    }
+    return wait_recorded(c.st, p->tail_stream, p->tail_done, p->tail_capture);
+}
+
+// Record the end of a first forward pass in its slot.
+gp_status record_first_pass(gp_partition* p, const Ctx& c) {
+    if (!p->events()) return GP_OK;
+    FirstPass& f = p->fpass[c.lane];
+    f.done = p->next_event();
+    GP_HIP(hipEventRecord(f.done, c.st));
+    f.stream = c.st;
+    f.capture = capture_of(c.st);
+    return GP_OK;
 }
 
 // Backward of one layer.  dY arrives in (in32, ine); dX leaves in the pair
@@ -1252,6 +1356,11 @@ void plan_partition(gp_partition* p, const gp_config* cfg) {
     if (const char* e = std::getenv("GP_PAIR_REMAT")) pair_remat = std::atoi(e) != 0;
     p->remat_group = pair_remat && p->group >= 2 && !g.keep_act ? 2 : 1;
     p->ahead_on = !g.keep_act && p->remat_ahead && g.M >= 2;
+    // two first-pass slots (GP_FWD_LANES=1: one), so that forwards issued on
+    // two streams overlap
+    int lanes = 2;
+    if (const char* e = std::getenv("GP_FWD_LANES")) lanes = std::atoi(e) == 1 ? 1 : 2;
+    p->fp_lanes = g.M >= 2 ? lanes : 1;
     p->nsets = g.keep_act ? (g.M + p->group - 1) / p->group * p->group : p->group * (p->ahead_on ? 2 : 1);
     if (const char* e = std::getenv("GP_GEMM_TILE")) p->gemm_tile = std::atoi(e);
     if (const char* e = std::getenv("GP_GEMM_SPLITS")) p->gemm_splits = std::atoi(e);
@@ -1376,7 +1485,7 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
         e = hipStreamCreateWithFlags(&p->side, hipStreamNonBlocking);
     }
     if (e == hipSuccess && p->ahead()) e = hipStreamCreateWithFlags(&p->remat, hipStreamNonBlocking);
-    if (e == hipSuccess && (p->side || p->remat)) {
+    if (e == hipSuccess && (p->side || p->remat || p->fp_lanes > 1)) {
         p->evring.assign(4096, nullptr);
         for (size_t i = 0; e == hipSuccess && i < p->evring.size(); ++i)
             e = hipEventCreateWithFlags(&p->evring[i], hipEventDisableTiming);
@@ -1508,44 +1617,53 @@ gp_status gp_forward_microbatch(gp_partition* p, int mb, const void* x, const vo
     const bool dec = p->g.kind == GP_DECODER_CROSS;
     if (dec && !mem) return set_error(GP_ERR_INVALID_ARG, "decoder partitions need the memory input");
     if (!dec && mem) return set_error(GP_ERR_INVALID_ARG, "encoder partitions take no memory input");
-    Ctx c = make_ctx(p, (hipStream_t)stream);
+    const int lane = p->lane_of(mb);
+    Ctx c = first_pass_ctx(p, (hipStream_t)stream, lane);
+    GP_TRY(order_first_pass(p, c, false));
+    const int set = p->g.keep_act ? p->set_of(mb) : 0;
     if (p->poison) {
-        const long T = p->g.T(), D = p->d.D;
-        GP_TRY(poison_span(p, p->splitk_span[0], c.st));
+        GP_TRY(poison_span(p, lane ? p->fpass[lane].splitk_span : p->splitk_span[0], c.st));
         if (p->g.keep_act) {
-            GP_TRY(poison_set(p, p->set_of(mb), c.st));
+            GP_TRY(poison_set(p, set, c.st));
         } else {
-            GP_TRY(poison_first_pass_slot(p, c.st));
+            GP_TRY(poison_first_pass_slot(p, lane, c.st));
         }
     }
+    const long T = p->g.T(), D = p->d.D;
+    FirstPass& f = p->fpass[lane];
+    GP_TRY(intake(c.dt, x, p->stash_x_mb(mb), p->g.keep_act ? p->xs[set][0] : f.xs[0], T * D, c.st));
+    if (mem) GP_TRY(intake(c.dt, mem, p->stash_m_mb(mb), nullptr, p->g.Tm() * D, c.st));
     // The last micro-batch's backward comes first, so the recompute of its
-    // unit starts on the recompute stream as soon as its boundary input is
+    // unit starts on the recompute stream as soon as its boundary inputs are
     // stashed; the first pass runs in its own slot beside it.
-    const bool early = p->remat_early && p->ahead() && mb == p->g.M - 1;
-    if (early) {
-        const long T = p->g.T(), D = p->d.D;
-        GP_TRY(intake(c.dt, x, p->stash_x_mb(mb), p->fp_xs[0], T * D, c.st));
-        if (mem) GP_TRY(intake(c.dt, mem, p->stash_m_mb(mb), nullptr, p->g.Tm() * D, c.st));
+    const bool early_on = p->remat_early && p->ahead();
+    int lo = mb, cnt = 1;
+    remat_unit(p, p->g.M - 1, lo, cnt);
+    if (early_on && mb >= lo && mb < p->g.M - 1 && p->events()) {
+        // a lower member of that unit: the early recompute reads its stash
+        f.stashed = p->next_event();
+        GP_HIP(hipEventRecord(f.stashed, c.st));
+    }
+    if (early_on && mb == p->g.M - 1) {
         const hipEvent_t fork = p->next_event();
         GP_HIP(hipEventRecord(fork, c.st));
         Ctx cr = make_ctx(p, p->remat, Lane::Remat);
         GP_HIP(hipStreamWaitEvent(cr.st, fork, 0));
+        for (int m2 = lo; m2 < mb; ++m2) {
+            const FirstPass& o = p->fpass[p->lane_of(m2)];
+            GP_TRY(wait_recorded(cr.st, o.stream, o.stashed, o.capture));
+        }
         GP_TRY(poison_span(p, p->splitk_span[2], cr.st));
-        int lo = mb, cnt = 1;
-        remat_unit(p, mb, lo, cnt);
         s = remat_pass(cr, lo, cnt);
         if (s != GP_OK) return s;
         p->remat_done = p->next_event();
         GP_HIP(hipEventRecord(p->remat_done, cr.st));
         p->remat_pending = lo;
-        s = partition_forward(c, mb, false, x, mem, y, 0, true);
-    } else if (p->g.keep_act) {
-        // stored-activation mode: this micro-batch's intermediates stay in its own set
-        s = partition_forward(c, mb, true, x, mem, y, p->set_of(mb));
-    } else {
-        s = partition_forward(c, mb, false, x, mem, y);
     }
+    // stored-activation mode: this micro-batch's intermediates stay in its own set
+    s = partition_forward(c, mb, p->g.keep_act != 0, x, mem, y, set, true);
     if (s != GP_OK) return s;
+    GP_TRY(record_first_pass(p, c));
     p->sched.did_forward();
     return GP_OK;
 }
@@ -1568,16 +1686,19 @@ gp_status gp_forward_microbatch_noalloc(gp_partition* p, int mb, const void* x, 
         return set_error(GP_ERR_UNSUPPORTED, m.c_str());
     }
     // Same tile and split choices as gp_forward_microbatch (the workspace size
-    // the chooser sees is unchanged); the partials go to the static scratch.
-    Ctx c = make_ctx(p, (hipStream_t)stream);
+    // the chooser sees is unchanged); the partials go to the static scratch,
+    // so this pass also waits for the other slot's last forward (two of these
+    // in flight would share the array).
+    const int lane = p->lane_of(mb);
+    Ctx c = first_pass_ctx(p, (hipStream_t)stream, lane);
     c.ws = p->noalloc_scratch;
+    GP_TRY(order_first_pass(p, c, true));
     if (p->poison) {
-        const long T = p->g.T(), D = p->d.D;
         GP_TRY(poison_fill(p->noalloc_scratch, (size_t)p->fwd_ws_need * 4, c.st));
         if (p->g.keep_act) {
             GP_TRY(poison_set(p, p->set_of(mb), c.st));
         } else {
-            GP_TRY(poison_first_pass_slot(p, c.st));
+            GP_TRY(poison_first_pass_slot(p, lane, c.st));
         }
     }
     // No early recompute on the library's recompute stream: the backward of
@@ -1587,6 +1708,7 @@ gp_status gp_forward_microbatch_noalloc(gp_partition* p, int mb, const void* x, 
     else
         s = partition_forward(c, mb, false, x, mem, y);
     if (s != GP_OK) return s;
+    GP_TRY(record_first_pass(p, c));
     p->sched.did_forward();
     return GP_OK;
 }
@@ -1607,6 +1729,13 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     const bool first = p->sched.first_backward();
     const long T = p->g.T(), D = p->d.D;
     const int set = p->set_of(mb);
+    if (first) {
+        // every forward of the mini-batch, on whatever stream, precedes its backward
+        for (FirstPass& f : p->fpass) {
+            GP_TRY(wait_recorded(c.st, f.stream, f.done, f.capture));
+            f.done = f.stashed = nullptr;
+        }
+    }
     if (p->poison) {
         for (const Span* sp : {&p->bwd_span, &p->splitk_span[0], &p->splitk_span[1], &p->loss_span, &p->head_span})
             GP_TRY(poison_span(p, *sp, c.st));
@@ -1818,6 +1947,12 @@ gp_status gp_accumulate_and_step(gp_partition* p, float lr, double* loss_out, gp
             GP_HIP(hipMemcpyAsync(&v, p->bw.loss_acc, sizeof(double), hipMemcpyDeviceToHost, st));
         GP_HIP(hipStreamSynchronize(st));
         *loss_out = v;
+    }
+    if (p->events()) {
+        p->tail_done = p->next_event();
+        GP_HIP(hipEventRecord(p->tail_done, st));
+        p->tail_stream = st;
+        p->tail_capture = capture_of(st);
     }
     p->sched.did_step();
     return GP_OK;

@@ -54,6 +54,7 @@ class Partition:
         self.cfg = cfg
         self.M = cfg.micro if micro is None else micro
         self.tdtype = DTYPES[cfg.dtype][1]
+        self._lane = None  # second stream for the odd micro-batches' forwards
         self.h = gp.gp_partition_create(cfg.layers, cfg.d_model, cfg.d_ff, cfg.heads)
         try:
             gp.gp_partition_configure(self.h, make_config(cfg, self.M, check_finite, keep_activations))
@@ -122,15 +123,25 @@ class Partition:
         return out
 
     def step(self, x, mem, dy, lr=0.0, want_y=True, want_dx=True, want_dmem=True, want_loss=True,
-             stream=None, y=None, dx=None, dmem=None, want_recomputed=False, noalloc=False):
+             stream=None, y=None, dx=None, dmem=None, want_recomputed=False, noalloc=False, fwd_streams=2):
         """One mini-batch through GPipe's schedule.  x/mem/dy: device tensors
         of the whole mini-batch (dim 0 = sequences).  Returns dict(y, dx, dmem,
         loss); with want_recomputed also "y_remat", the partition output as
         each backward call re-materialised it (gp_recomputed_output), in
         mini-batch order.  noalloc: the forwards go through
-        gp_forward_microbatch_noalloc."""
+        gp_forward_microbatch_noalloc.  fwd_streams=2: the odd micro-batches'
+        forwards are issued on a second stream, so that consecutive forwards
+        run side by side (the library keeps one first-pass slot per parity);
+        the launch stream waits for it before the backwards."""
         M = self.M
-        st = stream if stream is not None else torch.cuda.current_stream().cuda_stream
+        main = torch.cuda.current_stream() if stream is None else torch.cuda.ExternalStream(stream)
+        st = main.cuda_stream
+        lanes = [st]
+        if fwd_streams > 1 and M > 1:
+            if self._lane is None:
+                self._lane = torch.cuda.Stream()
+            self._lane.wait_stream(main)
+            lanes.append(self._lane.cuda_stream)
         if want_y and y is None:
             y = torch.empty_like(x)
         if want_dx and dx is None:
@@ -146,7 +157,9 @@ class Partition:
         ptr = lambda t: None if t is None else t.data_ptr()
         fwd = gp.gp_forward_microbatch_noalloc if noalloc else gp.gp_forward_microbatch
         for m in range(M):
-            fwd(self.h, m, ptr(xs[m]), ptr(ms[m]), ptr(ys[m]), st)
+            fwd(self.h, m, ptr(xs[m]), ptr(ms[m]), ptr(ys[m]), lanes[m % len(lanes)])
+        if len(lanes) > 1:
+            main.wait_stream(self._lane)
         y_remat = torch.empty_like(x) if want_recomputed else None
         yr = y_remat.chunk(M) if want_recomputed else None
         for m in range(M - 1, -1, -1):

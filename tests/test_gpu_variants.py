@@ -6,6 +6,8 @@
   library's plan, with and without re-materialisation (Section 2.3, Table 1);
 * GP_POISON=1 (every workspace region filled with NaN before the phase that
   rewrites it) leaves every result bit-identical, with all three streams on;
+* forwards issued on two streams (two first-pass slots) against one, bit for
+  bit;
 * RMSProp (Table 1's optimizer), logit clipping and the scaled-down
   feed-forward initialisation (Section 5) against the fp64 oracle.
 
@@ -47,7 +49,7 @@ def _flat(part):
     return np.concatenate([v.ravel() for p in gl for v in p.values()] + [v.ravel() for v in gh.values()])
 
 
-def _steps(cfg, seed, n=2, keep=False, lr=0.0):
+def _steps(cfg, seed, n=2, keep=False, lr=0.0, fwd_streams=2):
     """n steps of one partition; per step the outputs, the loss and every
     gradient (fp32 arrays / tensors)."""
     from paper_1811_06965_amd.runtime import Partition
@@ -57,7 +59,7 @@ def _steps(cfg, seed, n=2, keep=False, lr=0.0):
         part.load_params(case["layers"], case["head"])
         inp = part.device_inputs(case)
         for _ in range(n):
-            o = part.step(inp["x"], inp["mem"], inp["dy"], lr=lr, want_recomputed=True)
+            o = part.step(inp["x"], inp["mem"], inp["dy"], lr=lr, want_recomputed=True, fwd_streams=fwd_streams)
             torch.cuda.synchronize()
             out.append(dict(y=_bits(o["y"]), y_remat=_bits(o["y_remat"]), dx=_bits(o["dx"]),
                             dmem=None if o["dmem"] is None else _bits(o["dmem"]), loss=o["loss"], g=_flat(part)))
@@ -149,6 +151,29 @@ def test_poisoned_workspace_changes_no_bit(cfg, keep, env, monkeypatch):
     for r in poisoned:
         assert np.isfinite(r["g"]).all()
     _same(clean, poisoned)
+
+
+# ---------------------------------------------- forwards on two streams
+@pytest.mark.parametrize("cfg,keep", [(TINY, False), (ENC512_SMALL, False), (RAGGED_BF16, False),
+                                      (DEC_SMALL_BF16, False), (ENC512_SMALL, True),
+                                      (ENC512_SMALL.with_(batch=12, micro=6), False)],
+                         ids=["tiny", "enc512_small", "ragged_pairs", "dec_small", "enc512_kept", "enc512_m6"])
+def test_forwards_on_two_streams_change_no_bit(cfg, keep, monkeypatch):
+    """The odd micro-batches' forwards issued on a second stream (the library's
+    second first-pass slot; with recompute pairs, the early recompute of the
+    last pair reads the stash the other stream wrote) against every forward on
+    the launch stream in one slot (GP_FWD_LANES=1), with the workspace
+    poisoned: three steps with an update between them (which the second
+    stream's forwards must wait for) are bit-identical."""
+    lr = 1e-3 if cfg.loss != "none" else 0.0
+    monkeypatch.setenv("GP_POISON", "1")
+    monkeypatch.setenv("GP_FWD_LANES", "1")
+    one = _steps(cfg, 31, n=3, keep=keep, lr=lr, fwd_streams=1)
+    monkeypatch.delenv("GP_FWD_LANES")
+    two = _steps(cfg, 31, n=3, keep=keep, lr=lr, fwd_streams=2)
+    for r in two:
+        assert np.isfinite(r["g"]).all()
+    _same(one, two)
 
 
 # --------------------------------------------------------------- RMSProp

@@ -96,15 +96,11 @@ gp_status layernorm_fwd_res(int dtype, const float* ws, int splits, long plane, 
 gp_status layernorm_bwd(int dtype, const float* dn, const float* x, const float* stats, const float* gamma,
                         long rows, int D, const float* dres, float* dx_f32, void* dx_elt, float* partial,
                         int accumulate, int* nblk, hipStream_t st, int dn_splits = 1, long dn_plane = 0);
-// Rows the partial buffers of layernorm_bwd / bias_grad may need.
+// Blocks (rows of the partial buffer) layernorm_bwd uses for `rows` rows.
 int layernorm_bwd_blocks(long rows);
-int bias_grad_blocks(long rows);
 
 // out[c] = (accumulate ? out[c] : 0) + sum_b partial[b * width + c]
 gp_status colsum_finalize(const float* partial, int nblk, int width, float* out, int accumulate, hipStream_t st);
-// Column sums of dy (elt, [rows, N], leading dim ld) into out[N] (f32), via partial.
-gp_status bias_grad(int dtype, const void* dy, long rows, int N, long ld, float* partial, float* out,
-                    int accumulate, hipStream_t st);
 
 // ------------------------------------------------------------- attention
 struct AttnArgs {

@@ -389,21 +389,6 @@ __global__ void __launch_bounds__(256) ln_bwd_v4(const float* __restrict__ dn, c
     }
 }
 
-constexpr int BIAS_BLOCKS = 64;
-
-template <typename T>
-__global__ void __launch_bounds__(256) bias_partial_kernel(const T* __restrict__ dy, long rows, int N, long ld,
-                                                           long rows_per_block, float* __restrict__ partial) {
-    const int c = blockIdx.x * 256 + threadIdx.x;
-    if (c >= N) return;
-    const long r0 = (long)blockIdx.y * rows_per_block;
-    long r1 = r0 + rows_per_block;
-    if (r1 > rows) r1 = rows;
-    float s = 0.f;
-    for (long r = r0; r < r1; ++r) s += to_f32(dy[r * ld + c]);
-    partial[(long)blockIdx.y * N + c] = s;
-}
-
 template <typename T>
 gp_status ln_fwd_t(const float* x, long rows, int D, const float* g, const float* b, float eps, void* out,
                    float* stats, unsigned char* lo4, unsigned char* lo_sc, _Float16* o16, hipStream_t st) {
@@ -481,7 +466,6 @@ int layernorm_bwd_blocks(long rows) {
     const int rpw = ln_bwd_rows_per_wave(rows);
     return (int)((rows + (long)LN_WAVES * rpw - 1) / ((long)LN_WAVES * rpw));
 }
-int bias_grad_blocks(long rows) { return rows < BIAS_BLOCKS ? (int)(rows > 0 ? rows : 1) : BIAS_BLOCKS; }
 
 gp_status layernorm_fwd(int dtype, const float* x, long rows, int D, const float* gamma, const float* beta,
                         float eps, void* out, float* stats, void* lo4, unsigned char* lo_sc, hipStream_t st,
@@ -548,19 +532,6 @@ gp_status colsum_finalize(const float* partial, int nblk, int width, float* out,
     klaunch(colsum_kernel, (width + 63) / 64, 1024, 0, st, partial, nblk, width, out, accumulate);
     GP_LAUNCH_CHECK();
     return GP_OK;
-}
-
-gp_status bias_grad(int dtype, const void* dy, long rows, int N, long ld, float* partial, float* out,
-                    int accumulate, hipStream_t st) {
-    const int nb = bias_grad_blocks(rows);
-    const long rpb = (rows + nb - 1) / nb;
-    dim3 grid((N + 255) / 256, nb);
-    if (dtype == GP_BF16)
-        klaunch(bias_partial_kernel<bf16>, grid, 256, 0, st, reinterpret_cast<const bf16*>(dy), rows, N, ld, rpb, partial);
-    else
-        klaunch(bias_partial_kernel<float>, grid, 256, 0, st, reinterpret_cast<const float*>(dy), rows, N, ld, rpb, partial);
-    GP_LAUNCH_CHECK();
-    return colsum_finalize(partial, nb, N, out, accumulate, st);
 }
 
 } // namespace gp

@@ -92,7 +92,7 @@ struct Span {
 };
 
 struct BwdWs {
-    float *p32 = nullptr, *q32 = nullptr, *dn = nullptr, *delta = nullptr, *partial = nullptr, *dmem32 = nullptr;
+    float *p32 = nullptr, *q32 = nullptr, *dn = nullptr, *delta = nullptr, *dmem32 = nullptr;
     void* ring[ELT_RING] = {};  // dL/dx in the partition dtype, rotating across layers
     void *dc = nullptr;
     void *dz[2] = {}, *dqkv[2] = {}, *dxq[2] = {}, *dxkv[2] = {};  // by layer parity
@@ -470,16 +470,6 @@ void plan_workspace(gp_partition* p, Arena& a) {
     }
     b.delta = a.take<float>(lse_n);
     if (dec) b.dmem32 = a.take<float>(Tm * D);
-    long maxN = 3 * D > F ? 3 * D : F;
-    if (g.loss == GP_LOSS_XENT_LS && g.V > maxN) maxN = g.V;
-    size_t part = (size_t)layernorm_bwd_blocks(T) * 2 * D;
-    size_t pb = (size_t)bias_grad_blocks(T) * maxN;
-    if (pb > part) part = pb;
-    if (dec) {
-        size_t pm = (size_t)bias_grad_blocks(Tm) * 2 * D;
-        if (pm > part) part = pm;
-    }
-    b.partial = a.take<float>(part);
     p->bwd_span = span_from(b0);
     const std::vector<const Norm*> norms = p->plan.norms();
     p->lnpart.assign(norms.size(), nullptr);

@@ -34,10 +34,10 @@
  *  - Calls on one partition are not thread-safe; use one partition per host
  *    thread.  Work is ordered by the stream passed in; device faults surface
  *    as GP_ERR_HIP at the next call that synchronises.
- *  - Forward calls may be given different streams (see
- *    gp_forward_microbatch); the library orders what they share.  The other
- *    calls of a mini-batch take streams the caller has ordered one after the
- *    other (normally one stream).
+ *  - Forward and backward calls may be given different streams (see
+ *    gp_forward_microbatch and gp_backward_microbatch_remat); the library
+ *    orders what they share.  The caller orders its own data: the inputs a
+ *    call reads, and the outputs it wrote on another stream.
  */
 #ifndef GP_H
 #define GP_H
@@ -263,11 +263,35 @@ gp_status gp_forward_microbatch_noalloc(gp_partition* p, int mb, const void* x, 
  *          partition; may be NULL.
  *   dmem : decoder: device [n, S_mem, D] partition dtype, dL/dmem summed over
  *          the layers; may be NULL.  Else must be NULL.
+ * Streams: each backward call is ordered after the previous one, and the
+ * update after the last, whatever streams they were given, except that with
+ * no loss head, where a recompute unit is a pair of micro-batches (at most
+ * 512 rows each, recompute-ahead and the weight-gradient stream on), the
+ * pair's two calls issued on two streams run side by side: the odd member's
+ * in a second set of scratch buffers, the even member's following it layer
+ * by layer (its LayerNorm gradient sums after the odd member's, so every
+ * result equals the one-stream result bit for bit).
  * GP_ERR_STATE: forwards incomplete, or mb out of order.
  * GP_ERR_INVALID_ARG: dy_or_target NULL, mb out of range.
  */
 gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_or_target, void* dx,
                                        void* dmem, gp_stream stream);
+
+/*
+ * A non-blocking HIP stream of default priority on the current device, for a
+ * caller that issues micro-batches on a second stream (a helper, not a step
+ * of the method).  HIP maps streams onto a small pool of hardware queues
+ * (GPU_MAX_HW_QUEUES); two busy streams on one queue run one after the other,
+ * and a wait issued on one holds the other back.  A framework's stream pool
+ * spreads many streams over the queues, so a second stream taken from it may
+ * share a queue with one of the library's; a stream created here, once per
+ * process, does not as long as the process keeps no more busy streams than
+ * there are queues.  Destroy it with gp_stream_destroy once no work on it is
+ * pending.
+ * GP_ERR_INVALID_ARG: out (or stream) NULL.  GP_ERR_HIP: the runtime failed.
+ */
+gp_status gp_stream_create(gp_stream* out);
+gp_status gp_stream_destroy(gp_stream stream);
 
 /*
  * The one synchronous update at the end of the mini-batch (Section 2.2):

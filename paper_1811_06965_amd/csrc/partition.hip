@@ -224,6 +224,26 @@ struct gp_partition {
     FirstPass fpass[2];
     int fp_lanes = 1;
     int lane_of(int m) const { return fp_lanes > 1 ? m & 1 : 0; }
+    // Backward lanes: the two members of a recompute pair (T <= 512 rows) are
+    // back-propagated side by side when the caller issues them on two streams.
+    // The odd member (whose call comes first) uses `bw1` and its own split-K
+    // partials; it records hi_ev[l] after each layer l, and the even member
+    // waits for it before its first LayerNorm backward of layer l (so the
+    // LayerNorm partial sums accumulate in micro-batch order, as with one
+    // lane) and before launching the pair's weight gradients of layer l.
+    // A pair starts after the previous pair's even member (its weight
+    // gradients and recompute-ahead fork included); each call waits for the
+    // previous call in its lane.  GP_BWD_LANES=1 turns this off.
+    int bwd_lanes = 1;
+    int blane(int m) const { return bwd_lanes > 1 ? m & 1 : 0; }
+    std::vector<hipEvent_t> hi_ev;
+    hipEvent_t lane_end[2] = {};
+    hipStream_t lane_stream[2] = {};
+    unsigned long long lane_capture[2] = {};
+    hipEvent_t unit_ready = nullptr;  // the pair's recompute available (on its first call's stream)
+    hipStream_t unit_ready_stream = nullptr;
+    unsigned long long unit_ready_capture = 0;
+    Span bwd1_span, splitk1_span;
     // the last update's stream and an event recorded at its end, with its
     // capture: a forward issued on another stream waits for it
     hipStream_t tail_stream = nullptr;
@@ -257,6 +277,7 @@ struct gp_partition {
     // over the micro-batches of a mini-batch and reduced after the last one
     std::vector<float*> lnpart;
     BwdWs bw;
+    BwdWs bw1;  // the odd backward lane's scratch (p32, q32, dn, dc, delta, dmem32, splitk, v16)
     size_t bytes_params = 0, bytes_grads = 0, bytes_stash = 0, bytes_ws = 0;
     // GEMM tile-shape override (GP_GEMM_TILE = 0..10, GP_GEMM_SPLITS), read at
     // configure; -1 lets the library choose per problem.
@@ -498,6 +519,24 @@ void plan_workspace(gp_partition* p, Arena& a) {
         b.v16_main = a.take_elt(n16, 2);
         if (p->ahead()) b.v16_remat = a.take_elt(n16, 2);
     }
+    // the odd backward lane's scratch
+    p->bw1 = BwdWs{};
+    p->bwd1_span = p->splitk1_span = Span{};
+    if (p->bwd_lanes > 1) {
+        BwdWs& q = p->bw1;
+        const size_t q0 = a.mark();
+        q.p32 = a.take<float>(T * D);
+        q.q32 = a.take<float>(T * D);
+        q.dn = a.take<float>(T * D);
+        q.dc = a.take_elt(T * D, e);
+        q.delta = a.take<float>(lse_n);
+        if (dec) q.dmem32 = a.take<float>(Tm * D);
+        p->bwd1_span = span_from(q0);
+        q.splitk_elems = b.splitk_elems;
+        p->splitk1_span = Span{a.mark(), main_elems * sizeof(float)};
+        q.splitk = a.take<float>(main_elems);
+        if (f16) q.v16_main = a.take_elt((size_t)p->remat_group * T * D, 2);
+    }
     // the odd first-pass slot's own partials and fp16 buffer (one micro-batch)
     for (int ln = 1; ln < 2; ++ln) {
         FirstPass& f = p->fpass[ln];
@@ -574,6 +613,8 @@ struct Ctx {
     int nseq = 0;               // sequences of a forward pass (0: one micro-batch; 2n: a pair's recompute)
     void* v16 = nullptr;        // the feed-forward input in fp16 for passes on st (Linear::f16)
     int lane = 0;               // first forward passes: the slot (FirstPass) they run in
+    BwdWs* bw = nullptr;        // backward scratch of the call's lane (nullptr: p->bw)
+    const hipEvent_t* ln_gate = nullptr;  // even backward lane: the odd member's per-layer events
 };
 
 enum class Lane { Main, Side, Remat };
@@ -1081,7 +1122,7 @@ gp_status layer_backward(const Ctx& c, int set, int half, int l, bool first, flo
     gp_partition* p = c.p;
     const LayerPlan& P = p->plan.layers[l];
     LayerWs& w = p->lw[set][l];
-    BwdWs& b = p->bw;
+    BwdWs& b = c.bw ? *c.bw : p->bw;
     const long T = p->g.T(), Tm = p->g.Tm(), D = p->d.D, F = p->d.F;
     const bool dec = p->g.kind == GP_DECODER_CROSS;
     const int acc = first ? 0 : 1;
@@ -1112,6 +1153,8 @@ gp_status layer_backward(const Ctx& c, int set, int half, int l, bool first, flo
     GP_TRY(linear_dx(c, P.ffn1, dz, T, b.dn, EPI_F32, nullptr, 0, true));
     GP_TRY(flush(1));
     void* sce = pr ? hrow(p->dys[l].gffn, T, D) : next_elt();
+    // the other lane's layer l first: the LayerNorm partial sums accumulate in micro-batch order
+    if (c.ln_gate) GP_HIP(hipStreamWaitEvent(c.st, c.ln_gate[l], 0));
     GP_TRY(norm_bwd(c, nf, b.dn, xf, w.stf, T, in32, sc32, sce, acc));
     // (sc) = dL/d(xf)
     float* cur32 = sc32;
@@ -1352,6 +1395,14 @@ void plan_partition(gp_partition* p, const gp_config* cfg) {
     if (const char* e = std::getenv("GP_FWD_LANES")) lanes = std::atoi(e) == 1 ? 1 : 2;
     p->fp_lanes = g.M >= 2 ? lanes : 1;
     p->nsets = g.keep_act ? (g.M + p->group - 1) / p->group * p->group : p->group * (p->ahead_on ? 2 : 1);
+    // two backward lanes for recompute pairs (partitions without a loss head:
+    // the head's gradient and loss sums would need ordering of their own)
+    int blanes = 2;
+    if (const char* e = std::getenv("GP_BWD_LANES")) blanes = std::atoi(e) == 1 ? 1 : 2;
+    p->bwd_lanes = blanes > 1 && p->group == 2 && p->remat_group == 2 && p->ahead_on && p->use_side &&
+                           g.loss == GP_LOSS_NONE
+                       ? 2
+                       : 1;
     if (const char* e = std::getenv("GP_GEMM_TILE")) p->gemm_tile = std::atoi(e);
     if (const char* e = std::getenv("GP_GEMM_SPLITS")) p->gemm_splits = std::atoi(e);
     if (const char* e = std::getenv("GP_FFN_FP4")) g.ffn_fp4 = std::atoi(e) != 0;
@@ -1470,12 +1521,13 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
             return s;
         }
     }
-    if (p->use_side) {
-        // default priority, like every stream of the library
-        e = hipStreamCreateWithFlags(&p->side, hipStreamNonBlocking);
-    }
+    // default priority, like every stream of the library
+    if (p->use_side) e = hipStreamCreateWithFlags(&p->side, hipStreamNonBlocking);
     if (e == hipSuccess && p->ahead()) e = hipStreamCreateWithFlags(&p->remat, hipStreamNonBlocking);
-    if (e == hipSuccess && (p->side || p->remat || p->fp_lanes > 1)) {
+    p->hi_ev.assign(p->d.L, nullptr);
+    // events that order the library's streams and the calls a caller issues
+    // on different streams
+    if (e == hipSuccess) {
         p->evring.assign(4096, nullptr);
         for (size_t i = 0; e == hipSuccess && i < p->evring.size(); ++i)
             e = hipEventCreateWithFlags(&p->evring[i], hipEventDisableTiming);
@@ -1712,8 +1764,15 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     if (!dy_or_target) return set_error(GP_ERR_INVALID_ARG, "dy_or_target must not be NULL");
     const bool dec = p->g.kind == GP_DECODER_CROSS;
     if (!dec && dmem) return set_error(GP_ERR_INVALID_ARG, "encoder partitions have no memory gradient");
+    const bool lanes = p->bwd_lanes > 1;
+    const int bl = p->blane(mb);
     Ctx c = make_ctx(p, (hipStream_t)stream);
     c.last = mb == 0;
+    if (bl) {
+        c.bw = &p->bw1;
+        c.ws = p->bw1.splitk;
+        c.v16 = p->bw1.v16_main;
+    }
     Ctx cs = make_ctx(p, p->side, Lane::Side);
     const bool side = p->use_side && p->side;
     const bool first = p->sched.first_backward();
@@ -1726,9 +1785,25 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
             f.done = f.stashed = nullptr;
         }
     }
+    // The backward of a unit's highest micro-batch (which comes first) needs
+    // the unit re-materialised; the unit's other member then finds it done.
+    int lo = mb, cnt = 1;
+    remat_unit(p, mb, lo, cnt);
+    const bool unit_first = mb == lo + cnt - 1;
+    // The previous call in this lane (with one lane: the previous backward
+    // call, whatever stream it was given); with two lanes a unit's first call
+    // also waits for the previous unit's last call, which waited for that
+    // unit's weight gradients (they read the grouped rows this unit rewrites,
+    // and the recompute-ahead forked below rebuilds their sets).
+    GP_TRY(wait_recorded(c.st, p->lane_stream[bl], p->lane_end[bl], p->lane_capture[bl]));
+    if (lanes && unit_first)
+        GP_TRY(wait_recorded(c.st, p->lane_stream[bl ^ 1], p->lane_end[bl ^ 1], p->lane_capture[bl ^ 1]));
     if (p->poison) {
-        for (const Span* sp : {&p->bwd_span, &p->splitk_span[0], &p->splitk_span[1], &p->loss_span, &p->head_span})
-            GP_TRY(poison_span(p, *sp, c.st));
+        const Span* sk_side = lanes ? nullptr : &p->splitk_span[1];  // lanes: poisoned on the side stream
+        const Span* own_bwd = bl ? &p->bwd1_span : &p->bwd_span;
+        const Span* own_sk = bl ? &p->splitk1_span : &p->splitk_span[0];
+        for (const Span* sp : {own_bwd, own_sk, sk_side, (const Span*)&p->loss_span, (const Span*)&p->head_span})
+            if (sp) GP_TRY(poison_span(p, *sp, c.st));
         // this micro-batch's rows of the grouped weight-gradient operands (the
         // other members' rows may hold later micro-batches, not yet consumed)
         if (p->group > 1)
@@ -1740,11 +1815,6 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
             GP_TRY(poison_fill(p->grads, p->plan.n32 * 4, c.st));
         }
     }
-    // The backward of a unit's highest micro-batch (which comes first) needs
-    // the unit re-materialised; the unit's other member then finds it done.
-    int lo = mb, cnt = 1;
-    remat_unit(p, mb, lo, cnt);
-    const bool unit_first = mb == lo + cnt - 1;
     // Everything enqueued on the caller's stream so far (all forwards, the
     // previous units' backwards, which read the other workspace sets)
     // precedes a recompute-ahead launched from this call.
@@ -1759,6 +1829,8 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     if (p->g.keep_act || !unit_first) {
         // the forward kept every intermediate (stored-activation mode), or the
         // unit's first backward had it recomputed
+        if (lanes && !unit_first)
+            GP_TRY(wait_recorded(c.st, p->unit_ready_stream, p->unit_ready, p->unit_ready_capture));
     } else if (p->remat_pending == lo) {
         GP_HIP(hipStreamWaitEvent(c.st, p->remat_done, 0));
         p->remat_pending = -1;
@@ -1766,6 +1838,16 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
         s = remat_pass(c, lo, cnt);
         if (s != GP_OK) return s;
     }
+    if (lanes && unit_first && cnt > 1) {
+        p->unit_ready = p->next_event();
+        GP_HIP(hipEventRecord(p->unit_ready, c.st));
+        p->unit_ready_stream = c.st;
+        p->unit_ready_capture = capture_of(c.st);
+    }
+    // lanes: the unit's first call records the end of each layer; its other
+    // member follows it layer by layer
+    const bool record_hi = lanes && unit_first && cnt > 1;
+    if (lanes && !unit_first) c.ln_gate = p->hi_ev.data();
     if (ahead) {
         // re-materialise the next unit (the micro-batches below) meanwhile
         // (GPipe, Section 2.3: the recompute can be scheduled earlier)
@@ -1780,7 +1862,7 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
         GP_HIP(hipEventRecord(p->remat_done, cr.st));
         p->remat_pending = lo2;
     }
-    BwdWs& b = p->bw;
+    BwdWs& b = bl ? p->bw1 : p->bw;
     // dL/dy of the partition output into (p32, top): top is the ring's first
     // buffer, or with grouped weight gradients this micro-batch's rows of the
     // last layer's incoming-gradient buffer
@@ -1837,6 +1919,9 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
                 const hipEvent_t fork = p->next_event();
                 GP_HIP(hipEventRecord(fork, c.st));
                 GP_HIP(hipStreamWaitEvent(cs.st, fork, 0));
+                // lanes: the group's other member's rows of layer l
+                if (c.ln_gate) GP_HIP(hipStreamWaitEvent(cs.st, c.ln_gate[l], 0));
+                if (lanes) GP_TRY(poison_span(p, p->splitk_span[1], cs.st));
             }
             for (const DwJob& j : jobs)
                 GP_TRY(linear_dw(side ? cs : cb, *j.L, j.X, j.dY, j.rows * dw_rows, dw_acc));
@@ -1847,10 +1932,14 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
                            mem_m, jobs, flush);
         if (s == GP_OK) s = flush(2);
         if (s != GP_OK) return fail(s);
-        if (side) {
+        if (side && (run_dw || !lanes)) {
             p->side_done[l % 4] = p->next_event();
             GP_HIP(hipEventRecord(p->side_done[l % 4], cs.st));
             last_done = p->side_done[l % 4];
+        }
+        if (record_hi) {
+            p->hi_ev[l] = p->next_event();
+            GP_HIP(hipEventRecord(p->hi_ev[l], c.st));
         }
         if (l > 0) {
             sc32 = (out32 == b.p32) ? b.q32 : b.p32;
@@ -1862,12 +1951,34 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     if (s != GP_OK) return fail(s);
     if (run_dw) p->dw_started = true;
     // the caller's stream resumes only after the last weight-gradient GEMM
-    if (side) GP_HIP(hipStreamWaitEvent(c.st, p->side_done[0], 0));
+    // (lanes: the one of the call that launched them; the other member's
+    // next call waits for that call)
+    if (side && (run_dw || !lanes)) GP_HIP(hipStreamWaitEvent(c.st, p->side_done[0], 0));
     if (dec && dmem) {
         s = cast_out(c.dt, b.dmem32, dmem, p->g.Tm() * D, c.st);
         if (s != GP_OK) return s;
     }
+    if (p->events()) {
+        p->lane_end[bl] = p->next_event();
+        GP_HIP(hipEventRecord(p->lane_end[bl], c.st));
+        p->lane_stream[bl] = c.st;
+        p->lane_capture[bl] = capture_of(c.st);
+    }
     p->sched.did_backward();
+    return GP_OK;
+}
+
+gp_status gp_stream_create(gp_stream* out) {
+    if (!out) return set_error(GP_ERR_INVALID_ARG, "out must not be NULL");
+    hipStream_t st = nullptr;
+    GP_HIP(hipStreamCreateWithFlags(&st, hipStreamNonBlocking));  // default priority
+    *out = st;
+    return GP_OK;
+}
+
+gp_status gp_stream_destroy(gp_stream stream) {
+    if (!stream) return set_error(GP_ERR_INVALID_ARG, "stream must not be NULL");
+    GP_HIP(hipStreamDestroy((hipStream_t)stream));
     return GP_OK;
 }
 
@@ -1887,6 +1998,11 @@ gp_status gp_accumulate_and_step(gp_partition* p, float lr, double* loss_out, gp
     if (s != GP_OK) return set_error(s, msg.c_str());
     hipStream_t st = (hipStream_t)stream;
     const int dt = p->g.dtype;
+    // both backward lanes' last calls (their weight gradients included)
+    for (int ln = 0; ln < 2; ++ln) {
+        GP_TRY(wait_recorded(st, p->lane_stream[ln], p->lane_end[ln], p->lane_capture[ln]));
+        p->lane_end[ln] = nullptr;
+    }
     // Labels outside [0, V) were read as class 0 and flagged on the device; a
     // step that synchronises anyway reports them and skips the update.
     if (p->g.loss == GP_LOSS_XENT_LS && (loss_out || p->g.check_finite)) {

@@ -38,8 +38,8 @@ GP_K_NONE, GP_K_COUNT = 0, len(KERNEL_ROLES)
 EXPORTS = ["gp_partition_create", "gp_partition_configure", "gp_partition_destroy", "gp_set_param",
            "gp_get_param", "gp_get_grad", "gp_partition_memory", "gp_param_count", "gp_forward_microbatch",
            "gp_backward_microbatch_remat", "gp_accumulate_and_step", "gp_timer_select", "gp_timer_read",
-           "gp_timer_reset", "gp_timer_sample", "gp_mfma_peak", "gp_recomputed_output", "gp_memory_plan", "gp_forward_microbatch_noalloc",
-           "gp_plan_cells", "gp_last_error"]
+           "gp_timer_reset", "gp_timer_sample", "gp_mfma_peak", "gp_recomputed_output", "gp_memory_plan",
+           "gp_forward_microbatch_noalloc", "gp_plan_cells", "gp_stream_create", "gp_stream_destroy", "gp_last_error"]
 
 
 class gp_config(ctypes.Structure):
@@ -90,6 +90,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.gp_timer_sample.argtypes = [P, I]
     lib.gp_mfma_peak.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_double)]
     lib.gp_recomputed_output.argtypes = [P, VP, VP]
+    lib.gp_stream_create.argtypes = [ctypes.POINTER(VP)]
+    lib.gp_stream_destroy.argtypes = [VP]
     lib.gp_memory_plan.argtypes = [I, I, I, I, ctypes.POINTER(gp_config)] + [ctypes.POINTER(SZ)] * 4
     lib.gp_last_error.argtypes = []
     lib.gp_last_error.restype = ctypes.c_char_p
@@ -211,6 +213,17 @@ def gp_timer_reset(h):
 
 def gp_timer_sample(h, every):
     _check(load().gp_timer_sample(h, every))
+
+
+def gp_stream_create():
+    """A non-blocking stream of default priority (its raw handle)."""
+    s = ctypes.c_void_p()
+    _check(load().gp_stream_create(ctypes.byref(s)))
+    return s.value
+
+
+def gp_stream_destroy(stream):
+    _check(load().gp_stream_destroy(stream))
 
 
 def gp_recomputed_output(h, y, stream):

@@ -14,6 +14,19 @@ import torch
 
 from . import gp
 
+# One second stream per device for the odd micro-batches, created by the
+# library once per process (a stream from torch's pool may share a hardware
+# queue with one of the library's streams).
+_SECOND_STREAM: Dict[int, "torch.cuda.ExternalStream"] = {}
+
+
+def second_stream():
+    dev = torch.cuda.current_device()
+    if dev not in _SECOND_STREAM:
+        _SECOND_STREAM[dev] = torch.cuda.ExternalStream(gp.gp_stream_create(), device=dev)
+    return _SECOND_STREAM[dev]
+
+
 DTYPES = {"f32": (gp.GP_F32, torch.float32), "bf16": (gp.GP_BF16, torch.bfloat16)}
 KINDS = {"encoder": gp.GP_ENCODER, "decoder": gp.GP_DECODER_CROSS}
 LOSSES = {"none": gp.GP_LOSS_NONE, "mse": gp.GP_LOSS_MSE, "xent_ls": gp.GP_LOSS_XENT_LS}
@@ -54,7 +67,7 @@ class Partition:
         self.cfg = cfg
         self.M = cfg.micro if micro is None else micro
         self.tdtype = DTYPES[cfg.dtype][1]
-        self._lane = None  # second stream for the odd micro-batches' forwards
+        self._lane = None  # second stream for the odd micro-batches
         self.h = gp.gp_partition_create(cfg.layers, cfg.d_model, cfg.d_ff, cfg.heads)
         try:
             gp.gp_partition_configure(self.h, make_config(cfg, self.M, check_finite, keep_activations))
@@ -123,7 +136,8 @@ class Partition:
         return out
 
     def step(self, x, mem, dy, lr=0.0, want_y=True, want_dx=True, want_dmem=True, want_loss=True,
-             stream=None, y=None, dx=None, dmem=None, want_recomputed=False, noalloc=False, fwd_streams=2):
+             stream=None, y=None, dx=None, dmem=None, want_recomputed=False, noalloc=False, fwd_streams=2,
+             bwd_streams=2):
         """One mini-batch through GPipe's schedule.  x/mem/dy: device tensors
         of the whole mini-batch (dim 0 = sequences).  Returns dict(y, dx, dmem,
         loss); with want_recomputed also "y_remat", the partition output as
@@ -132,14 +146,18 @@ class Partition:
         gp_forward_microbatch_noalloc.  fwd_streams=2: the odd micro-batches'
         forwards are issued on a second stream, so that consecutive forwards
         run side by side (the library keeps one first-pass slot per parity);
-        the launch stream waits for it before the backwards."""
+        the launch stream waits for it before the backwards.  bwd_streams=2:
+        likewise the odd micro-batches' backwards (the library runs the two
+        members of a recompute pair side by side where it has two backward
+        lanes, and orders them itself otherwise); the launch stream waits for
+        the second stream before the update."""
         M = self.M
         main = torch.cuda.current_stream() if stream is None else torch.cuda.ExternalStream(stream)
         st = main.cuda_stream
         lanes = [st]
+        if (fwd_streams > 1 or bwd_streams > 1) and M > 1 and self._lane is None:
+            self._lane = second_stream()
         if fwd_streams > 1 and M > 1:
-            if self._lane is None:
-                self._lane = torch.cuda.Stream()
             self._lane.wait_stream(main)
             lanes.append(self._lane.cuda_stream)
         if want_y and y is None:
@@ -162,10 +180,17 @@ class Partition:
             main.wait_stream(self._lane)
         y_remat = torch.empty_like(x) if want_recomputed else None
         yr = y_remat.chunk(M) if want_recomputed else None
+        blanes = [st]
+        if bwd_streams > 1 and M > 1:
+            self._lane.wait_stream(main)
+            blanes.append(self._lane.cuda_stream)
         for m in range(M - 1, -1, -1):
-            gp.gp_backward_microbatch_remat(self.h, m, ptr(dys[m]), ptr(dxs[m]), ptr(dms[m]), st)
+            bs = blanes[m % len(blanes)]
+            gp.gp_backward_microbatch_remat(self.h, m, ptr(dys[m]), ptr(dxs[m]), ptr(dms[m]), bs)
             if want_recomputed:
-                gp.gp_recomputed_output(self.h, ptr(yr[m]), st)
+                gp.gp_recomputed_output(self.h, ptr(yr[m]), bs)
+        if len(blanes) > 1:
+            main.wait_stream(self._lane)
         loss = gp.gp_accumulate_and_step(self.h, lr, want_loss, st)
         out = {"y": y, "dx": dx, "dmem": dmem, "loss": loss}
         if want_recomputed:
@@ -177,11 +202,15 @@ class Partition:
         update) into a HIP graph on a capture stream and return it; replay()
         runs the step again on the same buffers.  The capture itself runs no
         work.  The loss is not read (that would synchronise), and the
-        partition must not check gradients for finiteness (same reason)."""
+        partition must not check gradients for finiteness (same reason).
+        The step is captured on the capture stream alone (one stream for the
+        forwards and the backwards): a capture of the step issued over two
+        streams ended in a segmentation fault inside the HIP runtime's end of
+        capture, cause not found."""
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             self.step(x, mem, dy, lr=lr, want_y=want_y, want_dx=dx is not None, want_dmem=dmem is not None,
-                      want_loss=False, y=y, dx=dx, dmem=dmem)
+                      want_loss=False, y=y, dx=dx, dmem=dmem, fwd_streams=1, bwd_streams=1)
         return g
 
     # ------------------------------------------------------------ timers

@@ -100,6 +100,8 @@ def test_calls_on_a_null_partition_are_rejected(lib):
     assert lib.gp_timer_select(None, 0) == 1
     assert lib.gp_timer_sample(None, 1) == 1
     assert lib.gp_partition_destroy(None) == 0
+    assert lib.gp_stream_create(None) == 1
+    assert lib.gp_stream_destroy(None) == 1
 
 
 def test_host_logic_program():

@@ -6,8 +6,9 @@
   library's plan, with and without re-materialisation (Section 2.3, Table 1);
 * GP_POISON=1 (every workspace region filled with NaN before the phase that
   rewrites it) leaves every result bit-identical, with all three streams on;
-* forwards issued on two streams (two first-pass slots) against one, bit for
-  bit;
+* forwards issued on two streams (two first-pass slots) against one, and the
+  two members of a recompute pair back-propagated side by side (two backward
+  lanes) against one lane, bit for bit;
 * RMSProp (Table 1's optimizer), logit clipping and the scaled-down
   feed-forward initialisation (Section 5) against the fp64 oracle.
 
@@ -49,7 +50,7 @@ def _flat(part):
     return np.concatenate([v.ravel() for p in gl for v in p.values()] + [v.ravel() for v in gh.values()])
 
 
-def _steps(cfg, seed, n=2, keep=False, lr=0.0, fwd_streams=2):
+def _steps(cfg, seed, n=2, keep=False, lr=0.0, fwd_streams=2, bwd_streams=2):
     """n steps of one partition; per step the outputs, the loss and every
     gradient (fp32 arrays / tensors)."""
     from paper_1811_06965_amd.runtime import Partition
@@ -59,7 +60,8 @@ def _steps(cfg, seed, n=2, keep=False, lr=0.0, fwd_streams=2):
         part.load_params(case["layers"], case["head"])
         inp = part.device_inputs(case)
         for _ in range(n):
-            o = part.step(inp["x"], inp["mem"], inp["dy"], lr=lr, want_recomputed=True, fwd_streams=fwd_streams)
+            o = part.step(inp["x"], inp["mem"], inp["dy"], lr=lr, want_recomputed=True, fwd_streams=fwd_streams,
+                          bwd_streams=bwd_streams)
             torch.cuda.synchronize()
             out.append(dict(y=_bits(o["y"]), y_remat=_bits(o["y_remat"]), dx=_bits(o["dx"]),
                             dmem=None if o["dmem"] is None else _bits(o["dmem"]), loss=o["loss"], g=_flat(part)))
@@ -171,6 +173,37 @@ def test_forwards_on_two_streams_change_no_bit(cfg, keep, monkeypatch):
     one = _steps(cfg, 31, n=3, keep=keep, lr=lr, fwd_streams=1)
     monkeypatch.delenv("GP_FWD_LANES")
     two = _steps(cfg, 31, n=3, keep=keep, lr=lr, fwd_streams=2)
+    for r in two:
+        assert np.isfinite(r["g"]).all()
+    _same(one, two)
+
+
+LANES_F32 = synth.PartitionConfig("lanes_f32", layers=2, d_model=64, d_ff=128, heads=2, seq=16, batch=8, micro=4,
+                                  dtype="f32", loss="none")
+LANES_DEC = synth.PartitionConfig("lanes_dec", layers=2, d_model=256, d_ff=512, heads=4, seq=64, batch=4, micro=2,
+                                  kind="decoder", mem_seq=64, loss="none")
+
+
+@pytest.mark.parametrize("cfg", [RAGGED_BF16, RAGGED_BF16.with_(name="ragged_m3", batch=9, micro=3),
+                                 RAGGED_BF16.with_(name="ragged_m6", batch=18, micro=6), LANES_F32, LANES_DEC],
+                         ids=lambda c: c.name)
+def test_backward_lanes_change_no_bit(cfg, monkeypatch):
+    """The two members of a recompute pair back-propagated side by side (the
+    odd micro-batch on a second stream, in the library's second backward
+    lane; M odd leaves the top micro-batch alone) against one lane on one
+    stream, with the workspace poisoned: three steps with updates between
+    them are bit-identical (the LayerNorm partial sums keep their micro-batch
+    order)."""
+    from paper_1811_06965_amd.runtime import Partition
+    monkeypatch.setenv("GP_POISON", "1")
+    monkeypatch.setenv("GP_BWD_LANES", "1")
+    with Partition(cfg) as part:
+        ws_one = part.memory()["workspace"]
+    one = _steps(cfg, 37, n=3, lr=1e-3, fwd_streams=1, bwd_streams=1)
+    monkeypatch.delenv("GP_BWD_LANES")
+    with Partition(cfg) as part:
+        assert part.memory()["workspace"] > ws_one  # the second lane's scratch: the lanes are on
+    two = _steps(cfg, 37, n=3, lr=1e-3)
     for r in two:
         assert np.isfinite(r["g"]).all()
     _same(one, two)

@@ -266,7 +266,7 @@ gp_status gp_forward_microbatch_noalloc(gp_partition* p, int mb, const void* x, 
  * Streams: each backward call is ordered after the previous one, and the
  * update after the last, whatever streams they were given, except that with
  * no loss head, where a recompute unit is a pair of micro-batches (at most
- * 512 rows each, recompute-ahead and the weight-gradient stream on), the
+ * 2048 rows each, recompute-ahead and the weight-gradient stream on), the
  * pair's two calls issued on two streams run side by side: the odd member's
  * in a second set of scratch buffers, the even member's following it layer
  * by layer (its LayerNorm gradient sums after the odd member's, so every

@@ -224,7 +224,7 @@ struct gp_partition {
     FirstPass fpass[2];
     int fp_lanes = 1;
     int lane_of(int m) const { return fp_lanes > 1 ? m & 1 : 0; }
-    // Backward lanes: the two members of a recompute pair (T <= 512 rows) are
+    // Backward lanes: the two members of a recompute pair are
     // back-propagated side by side when the caller issues them on two streams.
     // The odd member (whose call comes first) uses `bw1` and its own split-K
     // partials; it records hi_ev[l] after each layer l, and the even member
@@ -1381,11 +1381,12 @@ void plan_partition(gp_partition* p, const gp_config* cfg) {
     if (const char* e = std::getenv("GP_DW_GROUP")) grp = std::atoi(e);
     if (grp != 1 && grp != 2 && grp != 4) grp = 2;
     p->group = p->pair_dw ? std::max(1, std::min(grp, g.M >= 4 ? 4 : g.M >= 2 ? 2 : 1)) : 1;
-    // Recompute pairs in one pass where a micro-batch's GEMMs are small
-    // (T <= 512 rows: they leave most of the chip idle on their own); at
-    // larger T the single passes were as fast or faster (measured at
-    // enc1024: M = 32 -2%, M = 4..16 +0.5..1.4%).  GP_PAIR_REMAT=0/1 forces it.
-    bool pair_remat = g.T() <= 512;
+    // Recompute pairs in one pass where a micro-batch has at most 2048 rows:
+    // the pass's GEMMs fill more of the chip, and (without a loss head) the
+    // pair's backwards can then run side by side in two lanes.  Measured at
+    // enc1024 with both: M = 32 -14%, M = 16 -8%, M = 8 -1.4%; at M = 4
+    // (4096 rows) +1%.  GP_PAIR_REMAT=0/1 forces it.
+    bool pair_remat = g.T() <= 2048;
     if (const char* e = std::getenv("GP_PAIR_REMAT")) pair_remat = std::atoi(e) != 0;
     p->remat_group = pair_remat && p->group >= 2 && !g.keep_act ? 2 : 1;
     p->ahead_on = !g.keep_act && p->remat_ahead && g.M >= 2;

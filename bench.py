@@ -10,9 +10,12 @@ boundary inputs and boundary gradients, Xavier-uniform weights (synthetic
 data).
 
 One step = M x gp_forward_microbatch + M x gp_backward_microbatch_remat +
-gp_accumulate_and_step (GPipe, Sections 2.2-2.3), enqueued on the caller's
-stream (the library runs the weight-gradient GEMMs on a second stream it
-joins before each call returns).  W untimed warm-up steps, one untimed census
+gp_accumulate_and_step (GPipe, Sections 2.2-2.3), enqueued by
+runtime.Partition.step: even micro-batches on the launch stream, odd ones on
+a second stream from gp_stream_create (consecutive forwards, and the two
+backwards of a recompute pair, run side by side), joined before the update;
+the library runs the weight gradients and the recompute-ahead on streams of
+its own.  W untimed warm-up steps, one untimed census
 step that times every launch role to find the dominant one, then K eager
 steps timed between two events on the launch stream, with one launch in
 TIMER_EVERY of the dominant role bracketed by dispatch events inside the timed

@@ -244,6 +244,15 @@ struct gp_partition {
     hipStream_t unit_ready_stream = nullptr;
     unsigned long long unit_ready_capture = 0;
     Span bwd1_span, splitk1_span;
+    // Per-layer update: the mini-batch's last backward call records, per layer
+    // l, an event on its stream after layer l (every read of layer l's weights
+    // by the backward is behind it) and the weight-gradient stream's event
+    // after layer l's last weight-gradient GEMM; the update then refreshes
+    // layer l on the recompute stream (idle by then) as soon as both have
+    // passed, beside the backward of the layers below.
+    std::vector<hipEvent_t> lay_main, lay_side;
+    bool lay_ready = false;
+    bool layer_update = true;  // GP_LAYER_UPDATE=0: the whole update after the last backward
     // the last update's stream and an event recorded at its end, with its
     // capture: a forward issued on another stream waits for it
     hipStream_t tail_stream = nullptr;
@@ -1361,6 +1370,7 @@ void plan_partition(gp_partition* p, const gp_config* cfg) {
     p->esz = g.dtype == GP_BF16 ? 2 : 4;
     if (const char* e = std::getenv("GP_TIMER_MARKERS")) p->timer.markers = std::atoi(e) != 0;
     if (const char* e = std::getenv("GP_SIDE_STREAM")) p->use_side = std::atoi(e) != 0;
+    if (const char* e = std::getenv("GP_LAYER_UPDATE")) p->layer_update = std::atoi(e) != 0;
     if (const char* e = std::getenv("GP_REMAT_AHEAD")) p->remat_ahead = std::atoi(e) != 0;
     if (const char* e = std::getenv("GP_REMAT_EARLY")) p->remat_early = std::atoi(e) != 0;
     if (const char* e = std::getenv("GP_FUSE_RES_LN")) p->fuse_res_ln = std::atoi(e) != 0;
@@ -1526,6 +1536,8 @@ gp_status gp_partition_configure(gp_partition* p, const gp_config* cfg) {
     if (p->use_side) e = hipStreamCreateWithFlags(&p->side, hipStreamNonBlocking);
     if (e == hipSuccess && p->ahead()) e = hipStreamCreateWithFlags(&p->remat, hipStreamNonBlocking);
     p->hi_ev.assign(p->d.L, nullptr);
+    p->lay_main.assign(p->d.L, nullptr);
+    p->lay_side.assign(p->d.L, nullptr);
     // events that order the library's streams and the calls a caller issues
     // on different streams
     if (e == hipSuccess) {
@@ -1942,6 +1954,11 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
             p->hi_ev[l] = p->next_event();
             GP_HIP(hipEventRecord(p->hi_ev[l], c.st));
         }
+        if (c.last && p->remat && p->layer_update) {
+            p->lay_main[l] = p->next_event();
+            GP_HIP(hipEventRecord(p->lay_main[l], c.st));
+            p->lay_side[l] = side ? p->side_done[l % 4] : nullptr;
+        }
         if (l > 0) {
             sc32 = (out32 == b.p32) ? b.q32 : b.p32;
             in32 = out32;
@@ -1951,6 +1968,7 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     if (s == GP_OK) s = flush_pending(cb);
     if (s != GP_OK) return fail(s);
     if (run_dw) p->dw_started = true;
+    p->lay_ready = p->layer_update && c.last && p->remat && side && run_dw;
     // the caller's stream resumes only after the last weight-gradient GEMM
     // (lanes: the one of the call that launched them; the other member's
     // next call waits for that call)
@@ -2028,14 +2046,35 @@ gp_status gp_accumulate_and_step(gp_partition* p, float lr, double* loss_out, gp
         }
     }
     const bool rms = p->g.optimizer == GP_OPT_RMSPROP;
-    if (p->fused_update) {
+    auto update_linear = [&](const Linear* l, hipStream_t us) {
+        return update_refresh_linear(p->master + l->w, p->grads + l->w, rms ? p->opt_ms + l->w : nullptr, lr,
+                                     p->g.rms_decay, p->g.rms_eps, l->in, l->out, p->W(l->kn), p->W(l->nk),
+                                     l->split ? p->W(l->q4) : nullptr, l->split ? p->W(l->q4s) : nullptr, us,
+                                     l->f16);
+    };
+    if (p->fused_update && p->lay_ready) {
+        // each layer's linears as soon as the last backward is past that layer
+        // (top layer first, as the backward goes), then the head's linear, the
+        // biases and LayerNorm parameters on the caller's stream
+        const hipStream_t us = p->remat;
+        const int L = p->d.L;
+        for (int l = L - 1; l >= 0; --l) {
+            GP_HIP(hipStreamWaitEvent(us, p->lay_main[l], 0));
+            if (p->lay_side[l]) GP_HIP(hipStreamWaitEvent(us, p->lay_side[l], 0));
+            const LayerPlan& P = p->plan.layers[l];
+            for (const Linear* x : {&P.qkv, &P.o, &P.ffn1, &P.ffn2, &P.xq, &P.xkv, &P.xo})
+                if (x->present) GP_TRY(update_linear(x, us));
+        }
+        const hipEvent_t upd = p->next_event();
+        GP_HIP(hipEventRecord(upd, us));
+        GP_HIP(hipStreamWaitEvent(st, upd, 0));
+        if (p->plan.head.out.present) GP_TRY(update_linear(&p->plan.head.out, st));
+        GP_TRY(update_ranges(p->master, p->grads, rms ? p->opt_ms : nullptr, lr, p->g.rms_decay, p->g.rms_eps,
+                             p->upd_ranges, p->n_upd_ranges, st));
+    } else if (p->fused_update) {
         // one pass over each linear's W and G that also rewrites its working
         // copies, then the biases and LayerNorm parameters
-        for (const Linear* l : p->plan.linears())
-            GP_TRY(update_refresh_linear(p->master + l->w, p->grads + l->w, rms ? p->opt_ms + l->w : nullptr, lr,
-                                         p->g.rms_decay, p->g.rms_eps, l->in, l->out, p->W(l->kn), p->W(l->nk),
-                                         l->split ? p->W(l->q4) : nullptr, l->split ? p->W(l->q4s) : nullptr, st,
-                                         l->f16));
+        for (const Linear* l : p->plan.linears()) GP_TRY(update_linear(l, st));
         GP_TRY(update_ranges(p->master, p->grads, rms ? p->opt_ms : nullptr, lr, p->g.rms_decay, p->g.rms_eps,
                              p->upd_ranges, p->n_upd_ranges, st));
     } else {
@@ -2055,6 +2094,7 @@ gp_status gp_accumulate_and_step(gp_partition* p, float lr, double* loss_out, gp
         GP_HIP(hipStreamSynchronize(st));
         *loss_out = v;
     }
+    p->lay_ready = false;
     if (p->events()) {
         p->tail_done = p->next_event();
         GP_HIP(hipEventRecord(p->tail_done, st));

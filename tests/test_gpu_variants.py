@@ -6,9 +6,10 @@
   library's plan, with and without re-materialisation (Section 2.3, Table 1);
 * GP_POISON=1 (every workspace region filled with NaN before the phase that
   rewrites it) leaves every result bit-identical, with all three streams on;
-* forwards issued on two streams (two first-pass slots) against one, and the
-  two members of a recompute pair back-propagated side by side (two backward
-  lanes) against one lane, bit for bit;
+* forwards issued on two streams (two first-pass slots) against one, the two
+  members of a recompute pair back-propagated side by side (two backward
+  lanes) against one lane, and the per-layer update against the whole update
+  after the last backward, bit for bit;
 * RMSProp (Table 1's optimizer), logit clipping and the scaled-down
   feed-forward initialisation (Section 5) against the fp64 oracle.
 
@@ -207,6 +208,21 @@ def test_backward_lanes_change_no_bit(cfg, monkeypatch):
     for r in two:
         assert np.isfinite(r["g"]).all()
     _same(one, two)
+
+
+@pytest.mark.parametrize("cfg", [RAGGED_BF16, ENC512_SMALL, DEC_SMALL_BF16, LANES_DEC], ids=lambda c: c.name)
+def test_per_layer_update_changes_no_bit(cfg, monkeypatch):
+    """Each layer's weights updated as soon as the last backward is past that
+    layer (on the recompute stream, beside the backward of the layers below)
+    against the whole update after the last backward (GP_LAYER_UPDATE=0):
+    three steps with lr > 0 and the workspace poisoned are bit-identical, so
+    no backward read of a layer's weights sees them updated."""
+    monkeypatch.setenv("GP_POISON", "1")
+    monkeypatch.setenv("GP_LAYER_UPDATE", "0")
+    whole = _steps(cfg, 41, n=3, lr=1e-3)
+    monkeypatch.delenv("GP_LAYER_UPDATE")
+    per_layer = _steps(cfg, 41, n=3, lr=1e-3)
+    _same(whole, per_layer)
 
 
 # --------------------------------------------------------------- RMSProp

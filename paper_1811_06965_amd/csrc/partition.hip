@@ -14,14 +14,16 @@
 //   stash           M boundary inputs [n, S, D] (and decoder memories [n, S_mem, D])
 //   workspace       per set: residual stream xs[0..L] fp32 [T, D] (T = n S) and
 //                   per-layer intermediates of one micro-batch; backward scratch
-// The forward pass writes its intermediates into layer slot 0 of set 0 and
-// ping-pongs xs[0]/xs[1]; the re-materialising pass of micro-batch m uses its
-// set (set_of: sets rotate so that the one being rebuilt ahead is never one
-// still read), slot l and xs[l] for layer l.  Sets come in groups of two or
-// four micro-batches whose buffers hold them back to back, so that the weight
-// gradients of a group run as one GEMM.  All passes run the same kernels with
-// the same launch shapes, so the recomputed activations equal the first pass
-// bit for bit.
+// The first forward pass writes its intermediates into a layer slot of its
+// own (one of two, by micro-batch parity, so that forwards issued on two
+// streams run side by side) and ping-pongs that slot's two residual buffers;
+// the re-materialising pass of micro-batch m uses its set (set_of: sets rotate
+// so that the one being rebuilt ahead is never one still read), slot l and
+// xs[l] for layer l.  Sets come in groups of two or four micro-batches whose
+// buffers hold them back to back, so that the weight gradients of a group run
+// as one GEMM and a pair can be recomputed in one pass.  All passes run the
+// same kernels with the same tile splits, so the recomputed activations equal
+// the first pass bit for bit.
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
@@ -99,7 +101,7 @@ struct BwdWs {
     double *loss_partial = nullptr, *loss_acc = nullptr;
     int* flag = nullptr;
     int* bad_label = nullptr;  // set by the cross-entropy head on a label outside [0, V)
-    float* splitk = nullptr;   // split-K partial tiles (caller's stream)
+    float* splitk = nullptr;   // split-K partial tiles (the call's stream)
     float* splitk_side = nullptr;  // split-K partial tiles of the weight-gradient stream
     float* splitk_remat = nullptr; // split-K partial tiles of the recompute-ahead stream
     // the feed-forward input in fp16 (Linear::f16): read only by the GEMM right
@@ -1828,9 +1830,10 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
             GP_TRY(poison_fill(p->grads, p->plan.n32 * 4, c.st));
         }
     }
-    // Everything enqueued on the caller's stream so far (all forwards, the
-    // previous units' backwards, which read the other workspace sets)
-    // precedes a recompute-ahead launched from this call.
+    // Everything this call's stream is ordered after so far (all forwards,
+    // the previous units' backwards, which read the other workspace sets, and
+    // their weight gradients) precedes a recompute-ahead launched from this
+    // call.
     hipEvent_t remat_fork = nullptr;
     const bool ahead = p->ahead() && !p->g.keep_act && unit_first && lo > 0;
     if (ahead) {

@@ -264,13 +264,14 @@ gp_status gp_forward_microbatch_noalloc(gp_partition* p, int mb, const void* x, 
  *   dmem : decoder: device [n, S_mem, D] partition dtype, dL/dmem summed over
  *          the layers; may be NULL.  Else must be NULL.
  * Streams: each backward call is ordered after the previous one, and the
- * update after the last, whatever streams they were given, except that with
- * no loss head, where a recompute unit is a pair of micro-batches (at most
- * 2048 rows each, recompute-ahead and the weight-gradient stream on), the
- * pair's two calls issued on two streams run side by side: the odd member's
- * in a second set of scratch buffers, the even member's following it layer
- * by layer (its LayerNorm gradient sums after the odd member's, so every
- * result equals the one-stream result bit for bit).
+ * update after the last, whatever streams they were given, except that where
+ * a recompute unit is a pair of micro-batches (at most 2048 rows each,
+ * recompute-ahead and the weight-gradient stream on), the pair's two calls
+ * issued on two streams run side by side: the odd member's in a second set of
+ * scratch buffers, the even member's following it (its loss head after the
+ * odd member's, each layer's LayerNorm gradient sums after the odd member's
+ * layer, so every result, the loss included, equals the one-stream result bit
+ * for bit).
  * GP_ERR_STATE: forwards incomplete, or mb out of order.
  * GP_ERR_INVALID_ARG: dy_or_target NULL, mb out of range.
  */

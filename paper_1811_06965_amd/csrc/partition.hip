@@ -245,7 +245,10 @@ struct gp_partition {
     hipEvent_t unit_ready = nullptr;  // the pair's recompute available (on its first call's stream)
     hipStream_t unit_ready_stream = nullptr;
     unsigned long long unit_ready_capture = 0;
-    Span bwd1_span, splitk1_span;
+    Span bwd1_span, splitk1_span, loss1_span, head1_span;
+    // the odd member's loss head done (its loss sum and head gradient come
+    // first; the even member's head waits for it)
+    hipEvent_t head_ev = nullptr;
     // Per-layer update: the mini-batch's last backward call records, per layer
     // l, an event on its stream after layer l (every read of layer l's weights
     // by the backward is behind it) and the weight-gradient stream's event
@@ -575,6 +578,24 @@ void plan_workspace(gp_partition* p, Arena& a) {
         b.h = a.take_elt(T * D, e);
         b.z = a.take_elt(T * (long)g.V, e);
         p->head_span = span_from(h0);
+    }
+    // the odd backward lane's loss partials and head scratch; the loss sum and
+    // the flags stay shared (the odd member's head runs first)
+    p->loss1_span = p->head1_span = Span{};
+    if (p->bwd_lanes > 1) {
+        BwdWs& q = p->bw1;
+        p->loss1_span = Span{a.mark(), lp * sizeof(double)};
+        q.loss_partial = a.take<double>(lp);
+        q.loss_acc = b.loss_acc;
+        q.flag = b.flag;
+        q.bad_label = b.bad_label;
+        if (g.loss == GP_LOSS_XENT_LS) {
+            const size_t h0 = a.mark();
+            q.sth = a.take<float>(2 * T);
+            q.h = a.take_elt(T * D, e);
+            q.z = a.take_elt(T * (long)g.V, e);
+            p->head1_span = span_from(h0);
+        }
     }
 }
 
@@ -1245,7 +1266,7 @@ gp_status layer_backward(const Ctx& c, int set, int half, int l, bool first, flo
 gp_status head_backward(const Ctx& c, int set, bool first, const int* labels, void* dy_elt) {
     gp_partition* p = c.p;
     const HeadPlan& Hd = p->plan.head;
-    BwdWs& b = p->bw;
+    BwdWs& b = c.bw ? *c.bw : p->bw;
     const long T = p->g.T(), D = p->d.D, V = p->g.V;
     const int acc = first ? 0 : 1;
     const float* y = p->xs[set][p->d.L];
@@ -1408,14 +1429,10 @@ void plan_partition(gp_partition* p, const gp_config* cfg) {
     if (const char* e = std::getenv("GP_FWD_LANES")) lanes = std::atoi(e) == 1 ? 1 : 2;
     p->fp_lanes = g.M >= 2 ? lanes : 1;
     p->nsets = g.keep_act ? (g.M + p->group - 1) / p->group * p->group : p->group * (p->ahead_on ? 2 : 1);
-    // two backward lanes for recompute pairs (partitions without a loss head:
-    // the head's gradient and loss sums would need ordering of their own)
+    // two backward lanes for recompute pairs
     int blanes = 2;
     if (const char* e = std::getenv("GP_BWD_LANES")) blanes = std::atoi(e) == 1 ? 1 : 2;
-    p->bwd_lanes = blanes > 1 && p->group == 2 && p->remat_group == 2 && p->ahead_on && p->use_side &&
-                           g.loss == GP_LOSS_NONE
-                       ? 2
-                       : 1;
+    p->bwd_lanes = blanes > 1 && p->group == 2 && p->remat_group == 2 && p->ahead_on && p->use_side ? 2 : 1;
     if (const char* e = std::getenv("GP_GEMM_TILE")) p->gemm_tile = std::atoi(e);
     if (const char* e = std::getenv("GP_GEMM_SPLITS")) p->gemm_splits = std::atoi(e);
     if (const char* e = std::getenv("GP_FFN_FP4")) g.ffn_fp4 = std::atoi(e) != 0;
@@ -1817,7 +1834,9 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
         const Span* sk_side = lanes ? nullptr : &p->splitk_span[1];  // lanes: poisoned on the side stream
         const Span* own_bwd = bl ? &p->bwd1_span : &p->bwd_span;
         const Span* own_sk = bl ? &p->splitk1_span : &p->splitk_span[0];
-        for (const Span* sp : {own_bwd, own_sk, sk_side, (const Span*)&p->loss_span, (const Span*)&p->head_span})
+        const Span* own_loss = bl ? &p->loss1_span : &p->loss_span;
+        const Span* own_head = bl ? &p->head1_span : &p->head_span;
+        for (const Span* sp : {own_bwd, own_sk, sk_side, own_loss, own_head})
             if (sp) GP_TRY(poison_span(p, *sp, c.st));
         // this micro-batch's rows of the grouped weight-gradient operands (the
         // other members' rows may hold later micro-batches, not yet consumed)
@@ -1885,6 +1904,9 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
     const bool pr = p->group > 1;
     const int half = pr ? mb % p->group : 0;
     void* top = pr ? p->off_elt(p->dys[p->d.L - 1].gin, (long)half * T * D) : b.ring[0];
+    // lanes: the loss sum and the head's gradient accumulate in micro-batch order
+    const bool head_order = lanes && p->g.loss != GP_LOSS_NONE;
+    if (head_order && !unit_first) GP_HIP(hipStreamWaitEvent(c.st, p->head_ev, 0));
     if (p->g.loss == GP_LOSS_NONE) {
         s = intake(c.dt, dy_or_target, top, b.p32, T * D, c.st);
     } else if (p->g.loss == GP_LOSS_MSE) {
@@ -1896,6 +1918,10 @@ gp_status gp_backward_microbatch_remat(gp_partition* p, int mb, const void* dy_o
         s = head_backward(c, set, first, reinterpret_cast<const int*>(dy_or_target), top);
     }
     if (s != GP_OK) return s;
+    if (head_order && record_hi) {
+        p->head_ev = p->next_event();
+        GP_HIP(hipEventRecord(p->head_ev, c.st));
+    }
     const void* mem_m = dec ? p->stash_m_mb(mb) : nullptr;
     // Layer l's weight-gradient GEMMs run on the side stream while layer l - 1
     // is processed.  Without grouping, layer l - 2 rewrites parity and ring

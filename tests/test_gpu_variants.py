@@ -186,15 +186,17 @@ LANES_DEC = synth.PartitionConfig("lanes_dec", layers=2, d_model=256, d_ff=512, 
 
 
 @pytest.mark.parametrize("cfg", [RAGGED_BF16, RAGGED_BF16.with_(name="ragged_m3", batch=9, micro=3),
-                                 RAGGED_BF16.with_(name="ragged_m6", batch=18, micro=6), LANES_F32, LANES_DEC],
+                                 RAGGED_BF16.with_(name="ragged_m6", batch=18, micro=6), LANES_F32, LANES_DEC,
+                                 ENC512_SMALL, DEC_SMALL_BF16, DEC_SMALL_BF16.with_(name="dec_xent_m3", batch=6,
+                                                                                   micro=3)],
                          ids=lambda c: c.name)
 def test_backward_lanes_change_no_bit(cfg, monkeypatch):
     """The two members of a recompute pair back-propagated side by side (the
     odd micro-batch on a second stream, in the library's second backward
     lane; M odd leaves the top micro-batch alone) against one lane on one
     stream, with the workspace poisoned: three steps with updates between
-    them are bit-identical (the LayerNorm partial sums keep their micro-batch
-    order)."""
+    them are bit-identical, the loss included (the LayerNorm partial sums,
+    the loss sum and the head's gradient keep their micro-batch order)."""
     from paper_1811_06965_amd.runtime import Partition
     monkeypatch.setenv("GP_POISON", "1")
     monkeypatch.setenv("GP_BWD_LANES", "1")

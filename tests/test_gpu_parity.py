@@ -321,7 +321,9 @@ def test_library_streams_are_bitwise_neutral(cfg, monkeypatch):
 def test_graph_replay_matches_eager_steps(cfg):
     """A step captured into a HIP graph and replayed three times (with eager
     reads and synchronisations between the replays) gives bit for bit the
-    parameters, gradients and boundary gradients of three eager steps."""
+    parameters, gradients and boundary gradients of three eager steps.  The
+    capture issues the step on one stream (the library's own streams fork
+    and join inside it); the eager steps use two."""
     from paper_1811_06965_amd.runtime import Partition
     case = synth.make_case(cfg, 12, perturb=True)
     lr = 1e-4  # the boundary gradient is unnormalised: keep three updates finite

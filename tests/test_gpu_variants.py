@@ -212,6 +212,16 @@ def test_backward_lanes_change_no_bit(cfg, monkeypatch):
     _same(one, two)
 
 
+@pytest.mark.parametrize("cfg", [RAGGED_BF16.with_(name="ragged_m6", batch=18, micro=6), DEC_SMALL_BF16],
+                         ids=lambda c: c.name)
+def test_backward_lanes_without_early_recompute_change_no_bit(cfg, monkeypatch):
+    """As above with the early recompute off (GP_REMAT_EARLY=0, the default
+    at 2048 rows per micro-batch): the top pair is then re-materialised by
+    the odd member's call on its own stream, in the second lane's scratch."""
+    monkeypatch.setenv("GP_REMAT_EARLY", "0")
+    test_backward_lanes_change_no_bit(cfg, monkeypatch)
+
+
 @pytest.mark.parametrize("cfg", [RAGGED_BF16, ENC512_SMALL, DEC_SMALL_BF16, LANES_DEC], ids=lambda c: c.name)
 def test_per_layer_update_changes_no_bit(cfg, monkeypatch):
     """Each layer's weights updated as soon as the last backward is past that
